@@ -1,0 +1,268 @@
+"""Oracle for GeoCache's per-step cross-view transport -- TEST INFRASTRUCTURE.
+
+Only the tests, the smoke check and the benchmark's CPU-baseline leg may
+import this package.  The product library (paper_2608_13255_amd) never
+imports it and shares no code with it.
+
+Thin numpy/ctypes marshalling over oracle.c (plain single-threaded C, double
+precision for continuous outputs, float where a float decides an integer).
+Every arithmetic step lives in oracle.c and cites the paper there; this file
+adds only the trajectory loop, which strings the C steps together in the
+order of Sec. 3.2 ("Loop order") and Sec. 3.2 ("Drift-bounding schedule").
+
+Latent arrays are float32 for dtype "f32" and uint16 bfloat16 bit patterns
+for dtype "bf16".
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Dict, List, Sequence, Tuple
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB = None
+
+DTYPES = {"f32": 0, "bf16": 1}
+PRED = {"none": 0, "eps": 1, "v": 2, "vel": 3}
+KIND = {"ddim": 0, "flow": 1}
+FULL_RULE = {"periodic": 0, "head_mid_tail": 1}
+
+_i32p = ctypes.POINTER(ctypes.c_int32)
+_f32p = ctypes.POINTER(ctypes.c_float)
+_f64p = ctypes.POINTER(ctypes.c_double)
+_u8p = ctypes.POINTER(ctypes.c_uint8)
+_vp = ctypes.c_void_p
+
+
+def lib():
+    global _LIB
+    if _LIB is None:
+        path = os.path.join(_HERE, "liboracle.so")
+        if not os.path.exists(path):
+            raise RuntimeError(f"{path} is missing: build it with `make -C oracle`")
+        L = ctypes.CDLL(path)
+        L.orc_downsample.argtypes = [_f32p, ctypes.c_int64, ctypes.c_int, ctypes.c_int, ctypes.c_int, _f32p]
+        L.orc_bbox.argtypes = [_f32p, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                               ctypes.c_float, _f32p]
+        L.orc_build.argtypes = [_f32p, _i32p, _f32p, _f32p, _f32p, ctypes.c_int, ctypes.c_int,
+                                ctypes.c_int, ctypes.c_int, _i32p, ctypes.c_int, ctypes.c_int, _f32p,
+                                _i32p, _f64p, _i32p]
+        L.orc_transport.argtypes = [_vp, _vp, _i32p, _f64p, _i32p, ctypes.c_int, ctypes.c_int,
+                                    ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                    ctypes.c_int, ctypes.c_int, _f64p, _vp]
+        L.orc_reconstruct.argtypes = [_vp, _vp, ctypes.c_int64, ctypes.c_int, ctypes.c_int,
+                                      ctypes.c_int, ctypes.c_int, ctypes.c_double, ctypes.c_double,
+                                      ctypes.c_double, ctypes.c_double, _f64p, _f64p]
+        L.orc_alpha_bar.argtypes = [ctypes.c_int, ctypes.c_double, ctypes.c_double, ctypes.c_int]
+        L.orc_alpha_bar.restype = ctypes.c_double
+        L.orc_anchors.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int64, _i32p]
+        L.orc_full_steps.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, _u8p]
+        L.orc_ddim_timesteps.argtypes = [ctypes.c_int, ctypes.c_int, _i32p]
+        L.orc_store.argtypes = [_f64p, ctypes.c_int64, ctypes.c_int, _vp]
+        for f in ("orc_downsample", "orc_bbox", "orc_build", "orc_transport", "orc_reconstruct",
+                  "orc_anchors", "orc_full_steps", "orc_ddim_timesteps", "orc_store"):
+            getattr(L, f).restype = ctypes.c_int
+        _LIB = L
+    return _LIB
+
+
+def _p(a, t):
+    return a.ctypes.data_as(t)
+
+
+def _check(rc, what):
+    if rc != 0:
+        raise ValueError(f"oracle {what} rejected its arguments (code {rc})")
+
+
+def _storage_dtype(dtype):
+    return np.float32 if dtype == "f32" else np.uint16
+
+
+# --------------------------------------------------------------------------
+# steps
+# --------------------------------------------------------------------------
+
+def downsample(hi: np.ndarray, f: int) -> np.ndarray:
+    """Area-downsample position maps [..., Hr, Wr, 3] by f (see oracle.c O1)."""
+    hi = np.ascontiguousarray(hi, np.float32)
+    lead = hi.shape[:-3]
+    Hr, Wr = hi.shape[-3], hi.shape[-2]
+    M = int(np.prod(lead)) if lead else 1
+    out = np.empty(lead + (Hr // f, Wr // f, 3), np.float32)
+    _check(lib().orc_downsample(_p(hi, _f32p), M, Hr, Wr, f, _p(out, _f32p)), "downsample")
+    return out
+
+
+def bbox(pos: np.ndarray, tol_frac: float = 0.01) -> np.ndarray:
+    """Per-asset bbox + squared tolerance, [B][8] (see oracle.c O2)."""
+    pos = np.ascontiguousarray(pos, np.float32)
+    B, N, H, W, _ = pos.shape
+    out = np.empty((B, 8), np.float32)
+    _check(lib().orc_bbox(_p(pos, _f32p), B, N, H, W, tol_frac, _p(out, _f32p)), "bbox")
+    return out
+
+
+def _cam_arrays(cams: Dict[str, np.ndarray], B: int, N: int):
+    model = np.ascontiguousarray(np.broadcast_to(cams["model"], (B, N)), np.int32)
+    R = np.ascontiguousarray(np.broadcast_to(cams["R"], (B, N, 3, 3)), np.float32)
+    t = np.ascontiguousarray(np.broadcast_to(cams["t"], (B, N, 3)), np.float32)
+    k = np.ascontiguousarray(np.stack([np.broadcast_to(cams[n], (B, N)) for n in ("fx", "fy", "cx", "cy")],
+                                      -1), np.float32)
+    return model, R, t, k
+
+
+def build(pos: np.ndarray, cams: Dict[str, np.ndarray], anchors: Sequence[int], K: int,
+          bbox_arr: np.ndarray):
+    """Correspondence G_{A->v} for every non-anchor view (see oracle.c O3).
+
+    Returns (corr int32 [B][N-a][H][W][a], weights float64 [B][N-a][H][W][a][K],
+    nvis int32 [B][N-a][H][W])."""
+    pos = np.ascontiguousarray(pos, np.float32)
+    B, N, H, W, _ = pos.shape
+    A = np.ascontiguousarray(anchors, np.int32)
+    a = A.shape[0]
+    model, R, t, k = _cam_arrays(cams, B, N)
+    bb = np.ascontiguousarray(bbox_arr, np.float32)
+    NT = N - a
+    corr = np.zeros((B, NT, H, W, a), np.int32)
+    wts = np.zeros((B, NT, H, W, a, K), np.float64)
+    nvis = np.zeros((B, NT, H, W), np.int32)
+    _check(lib().orc_build(_p(pos, _f32p), _p(model, _i32p), _p(R, _f32p), _p(t, _f32p), _p(k, _f32p),
+                           B, N, H, W, _p(A, _i32p), a, K, _p(bb, _f32p), _p(corr, _i32p),
+                           _p(wts, _f64p), _p(nvis, _i32p)), "build")
+    return corr, wts, nvis
+
+
+def transport(x0_prev: np.ndarray, x0_anchor_new: np.ndarray, corr: np.ndarray, weights: np.ndarray,
+              anchors: Sequence[int], dtype: str) -> Tuple[np.ndarray, np.ndarray]:
+    """Delta transport, Eq. 1 (see oracle.c O4).
+
+    Returns (x0 float64 unrounded [B][N][H][W][C], x0 state in storage dtype)."""
+    sd = _storage_dtype(dtype)
+    x0_prev = np.ascontiguousarray(x0_prev, sd)
+    x0_anchor_new = np.ascontiguousarray(x0_anchor_new, sd)
+    B, N, H, W, C = x0_prev.shape
+    A = np.ascontiguousarray(anchors, np.int32)
+    a = A.shape[0]
+    K = weights.shape[-1]
+    corr = np.ascontiguousarray(corr, np.int32)
+    weights = np.ascontiguousarray(weights, np.float64)
+    assert x0_anchor_new.shape == (B, a, H, W, C)
+    assert corr.shape == (B, N - a, H, W, a) and weights.shape == (B, N - a, H, W, a, K)
+    exact = np.empty(x0_prev.shape, np.float64)
+    state = np.empty(x0_prev.shape, sd)
+    _check(lib().orc_transport(x0_prev.ctypes.data, x0_anchor_new.ctypes.data, _p(corr, _i32p),
+                               _p(weights, _f64p), _p(A, _i32p), a, B, N, H, W, C, K, DTYPES[dtype],
+                               _p(exact, _f64p), state.ctypes.data), "transport")
+    return exact, state
+
+
+def reconstruct(x_t: np.ndarray, x0: np.ndarray, dtype: str, kind: str, t: float, t_next: float,
+                pred: str = "none", T: int = 1000, beta_start: float = 1e-4,
+                beta_end: float = 0.02) -> Tuple[np.ndarray, np.ndarray]:
+    """Sampler-consistent reconstruction (see oracle.c O5).
+
+    Returns (x_next float64, model_out float64 or None)."""
+    sd = _storage_dtype(dtype)
+    x_t = np.ascontiguousarray(x_t, sd)
+    x0 = np.ascontiguousarray(x0, sd)
+    assert x_t.shape == x0.shape
+    xn = np.empty(x_t.shape, np.float64)
+    mo = np.empty(x_t.shape, np.float64) if pred != "none" else None
+    _check(lib().orc_reconstruct(x_t.ctypes.data, x0.ctypes.data, x_t.size, DTYPES[dtype], KIND[kind],
+                                 PRED[pred], T, beta_start, beta_end, float(t), float(t_next),
+                                 _p(xn, _f64p), _p(mo, _f64p) if mo is not None else None),
+           "reconstruct")
+    return xn, mo
+
+
+def store(x: np.ndarray, dtype: str) -> np.ndarray:
+    """Round float64 values into the storage dtype."""
+    x = np.ascontiguousarray(x, np.float64)
+    out = np.empty(x.shape, _storage_dtype(dtype))
+    _check(lib().orc_store(_p(x, _f64p), x.size, DTYPES[dtype], out.ctypes.data), "store")
+    return out
+
+
+def alpha_bar(t: int, T: int = 1000, beta_start: float = 1e-4, beta_end: float = 0.02) -> float:
+    return lib().orc_alpha_bar(T, beta_start, beta_end, int(t))
+
+
+# --------------------------------------------------------------------------
+# schedule
+# --------------------------------------------------------------------------
+
+def anchors(N: int, a: int, c: int) -> List[int]:
+    out = np.empty(a, np.int32)
+    _check(lib().orc_anchors(N, a, c, _p(out, _i32p)), "anchors")
+    return out.tolist()
+
+
+def full_steps(rule: str, S: int, E: int = 0) -> List[int]:
+    out = np.zeros(S, np.uint8)
+    _check(lib().orc_full_steps(FULL_RULE[rule], S, E, _p(out, _u8p)), "full_steps")
+    return out.tolist()
+
+
+def ddim_timesteps(S: int, T: int = 1000) -> List[int]:
+    out = np.empty(S + 1, np.int32)
+    _check(lib().orc_ddim_timesteps(T, S, _p(out, _i32p)), "ddim_timesteps")
+    return out.tolist()
+
+
+def step_times(kind: str, S: int, k: int, T: int = 1000) -> Tuple[float, float]:
+    """(t, t_next) of sampler step k: DDIM integer timesteps, flow sigmas 1 - k/S."""
+    if kind == "ddim":
+        ts = ddim_timesteps(S, T)
+        return float(ts[k]), float(ts[k + 1])
+    return 1.0 - k / S, 1.0 - (k + 1) / S
+
+
+# --------------------------------------------------------------------------
+# trajectory (Sec. 3.2: loop order and drift-bounding schedule)
+# --------------------------------------------------------------------------
+
+def trajectory(x_t0: np.ndarray, stub, pos: np.ndarray, cams, K: int, tol_frac: float, dtype: str,
+               kind: str, S: int, full: Sequence[int], a: int, steps: int = None,
+               times=None):
+    """Run `steps` sampler steps (default S) of the cached loop.
+
+    stub(k, views) -> x0 storage array [B][len(views)][H][W][C]: the denoiser's
+    prediction at step k for the given views (a synthetic stand-in).
+    At a full step every view is predicted and only the reconstruction runs;
+    at a cached step c the anchors A_c are predicted, their increment against
+    the stored x0 is transported to the other views, and every view is then
+    reconstructed.  x0(t) of all N views becomes the next reference.
+
+    Returns the list of per-step records (x_t, x0 state, anchors)."""
+    steps = S if steps is None else steps
+    B, N = pos.shape[0], pos.shape[1]
+    bb = bbox(pos, tol_frac)
+    cache = {}
+    x_t = x_t0
+    x0_store = None
+    c = 0
+    out = []
+    for k in range(steps):
+        t, tn = times(k) if times is not None else step_times(kind, S, k)
+        if full[k] or x0_store is None:
+            x0_new = stub(k, list(range(N)))
+            x0_state = x0_new
+            A = list(range(N))
+        else:
+            A = anchors(N, a, c)
+            c += 1
+            key = tuple(A)
+            if key not in cache:
+                corr, w, _ = build(pos, cams, A, K, bb)
+                cache[key] = (corr, w)
+            corr, w = cache[key]
+            _, x0_state = transport(x0_store, stub(k, A), corr, w, A, dtype)
+        xn, _ = reconstruct(x_t, x0_state, dtype, kind, t, tn)
+        x_t = store(xn, dtype)
+        x0_store = x0_state
+        out.append({"k": k, "anchors": A, "x_t": x_t, "x0": x0_state})
+    return out

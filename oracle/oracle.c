@@ -1,0 +1,551 @@
+/*
+ * Oracle for GeoCache's per-step cross-view transport.
+ *
+ * TEST INFRASTRUCTURE ONLY.  This file is the plain, slow, single-threaded
+ * CPU statement of what the transport path computes.  Only the test suite,
+ * the smoke check and the CPU-baseline leg of the benchmark use it; the
+ * product library never links, loads or calls it, and it shares no code with
+ * the HIP path.
+ *
+ * Paper: "GeoCache: Training-Free Acceleration of Multi-View Texture Diffusion
+ * via Geometric Delta Transport", Sec. 3.2 (Methodology): the correspondence
+ * operator, delta transport (Eq. 1), multi-anchor aggregation, invalid
+ * matches, loop order, sampler-consistent reconstruction, and the
+ * drift-bounding schedule.
+ *
+ * Precision:
+ *   - every continuous output (area-downsampled positions, tap weights,
+ *     transported x0, sampler outputs) is computed in double;
+ *   - every quantity that decides an integer (which taps are visible, which
+ *     are nearest, which footprint a projection lands in, the tolerance
+ *     test) is computed in IEEE float with a fixed left-to-right operation
+ *     order, because the GPU takes those decisions in float as well;
+ *   - build with -ffp-contract=off -fno-fast-math (no fused multiply-add).
+ *
+ * Layouts (row-major, C order):
+ *   position maps  float [B][N][H][W][3], NaN (any component) = background
+ *   latents        [B][N][H][W][C] (float32, or bfloat16 bit patterns)
+ *   correspondence int32 [B][N-a][H][W][a]   (target views ascending)
+ *   weights        double [B][N-a][H][W][a][K]
+ *   cameras        model int32 [B][N], R float [B][N][9] (world->camera,
+ *                  row-major), t float [B][N][3], k float [B][N][4]
+ *                  = fx, fy, cx, cy in latent-pixel units; pixel i spans
+ *                  [i, i+1).
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#define ORC_F32 0
+#define ORC_BF16 1
+
+int orc_version(void) { return 1; }
+
+/* ------------------------------------------------------------------ */
+/* bf16 storage                                                         */
+/* ------------------------------------------------------------------ */
+
+static float bf16_to_float(uint16_t h) {
+  uint32_t u = (uint32_t)h << 16;
+  float f;
+  memcpy(&f, &u, 4);
+  return f;
+}
+
+/* Round a double to the nearest bfloat16 (ties to even), directly. */
+static uint16_t double_to_bf16(double x) {
+  if (isnan(x)) return 0x7FC0;
+  if (isinf(x)) return x > 0 ? 0x7F80 : 0xFF80;
+  double ax = fabs(x);
+  uint16_t sign = (x < 0 || (x == 0 && signbit(x))) ? 0x8000 : 0;
+  if (ax == 0) return sign;
+  /* candidate: truncate the float nearest below |x| to bf16, then pick the
+   * closer of the two neighbouring bf16 values in exact double arithmetic. */
+  float fl = (float)ax;           /* may round up; fix below */
+  if ((double)fl > ax) fl = nextafterf(fl, 0.0f);
+  uint32_t u;
+  memcpy(&u, &fl, 4);
+  uint32_t lo_bits = u & 0xFFFF0000u;
+  uint32_t hi_bits = lo_bits + 0x00010000u;
+  float lo, hi;
+  memcpy(&lo, &lo_bits, 4);
+  memcpy(&hi, &hi_bits, 4);
+  double dlo = ax - (double)lo, dhi = (double)hi - ax;
+  uint32_t pick;
+  if (dlo < dhi) pick = lo_bits;
+  else if (dhi < dlo) pick = hi_bits;
+  else pick = ((lo_bits >> 16) & 1) ? hi_bits : lo_bits;
+  return (uint16_t)(sign | (pick >> 16));
+}
+
+static double load_val(const void* base, int64_t i, int dtype) {
+  if (dtype == ORC_F32) return (double)((const float*)base)[i];
+  return (double)bf16_to_float(((const uint16_t*)base)[i]);
+}
+
+static void store_val(void* base, int64_t i, int dtype, double v) {
+  if (dtype == ORC_F32) ((float*)base)[i] = (float)v;
+  else ((uint16_t*)base)[i] = double_to_bf16(v);
+}
+
+static void copy_val(void* dst, int64_t di, const void* src, int64_t si, int dtype) {
+  if (dtype == ORC_F32) ((float*)dst)[di] = ((const float*)src)[si];
+  else ((uint16_t*)dst)[di] = ((const uint16_t*)src)[si];
+}
+
+/* Round n doubles into the storage dtype. */
+int orc_store(const double* x, int64_t n, int dtype, void* out) {
+  if (dtype != ORC_F32 && dtype != ORC_BF16) return -3;
+  for (int64_t i = 0; i < n; ++i) store_val(out, i, dtype, x[i]);
+  return 0;
+}
+
+/* ------------------------------------------------------------------ */
+/* O1: area downsample of a position map to the latent grid            */
+/* ------------------------------------------------------------------ */
+/*
+ * Position maps give each latent token its 3D surface point (Sec. 3.1, "the
+ * rendered position maps provide the 3D coordinates").  A render-resolution
+ * map is reduced to the latent grid by averaging each f x f block over its
+ * foreground samples (a sample is foreground when all three components are
+ * finite).  A block whose foreground covers less than half of it is
+ * background.  The mean is taken in double and stored as float.
+ */
+int orc_downsample(const float* hi, int64_t M, int Hr, int Wr, int f, float* lo) {
+  if (f <= 0 || Hr % f || Wr % f) return -2;
+  const int H = Hr / f, W = Wr / f;
+  for (int64_t m = 0; m < M; ++m) {
+    for (int j = 0; j < H; ++j) {
+      for (int i = 0; i < W; ++i) {
+        int n_fg = 0;
+        double s[3] = {0.0, 0.0, 0.0};
+        for (int dy = 0; dy < f; ++dy) {
+          for (int dx = 0; dx < f; ++dx) {
+            const float* p = hi + (((m * Hr) + (int64_t)j * f + dy) * Wr + (int64_t)i * f + dx) * 3;
+            if (isfinite(p[0]) && isfinite(p[1]) && isfinite(p[2])) {
+              n_fg += 1;
+              s[0] += p[0];
+              s[1] += p[1];
+              s[2] += p[2];
+            }
+          }
+        }
+        float* o = lo + ((m * H + j) * (int64_t)W + i) * 3;
+        if (2 * n_fg < f * f) {
+          o[0] = o[1] = o[2] = NAN;
+        } else {
+          for (int c = 0; c < 3; ++c) o[c] = (float)(s[c] / (double)n_fg);
+        }
+      }
+    }
+  }
+  return 0;
+}
+
+/* ------------------------------------------------------------------ */
+/* O2: per-asset bounding box and squared tolerance                    */
+/* ------------------------------------------------------------------ */
+/*
+ * The tolerance is 1% of the bounding-box diagonal (Sec. 3.2, correspondence
+ * operator).  The box is taken per asset over every foreground latent sample
+ * of every view.  The tolerance is only ever compared against squared float
+ * distances, so it is kept squared, in float:
+ *   e = max - min per axis;  d2 = (ex*ex + ey*ey) + ez*ez;
+ *   tol2 = (tol_frac*tol_frac) * d2.
+ * out[b] = {min x,y,z, max x,y,z, tol2, 0}; an asset with no foreground
+ * sample gets all zeros.
+ */
+int orc_bbox(const float* pos, int B, int N, int H, int W, float tol_frac, float* out) {
+  const int64_t per = (int64_t)N * H * W;
+  for (int b = 0; b < B; ++b) {
+    float mn[3] = {INFINITY, INFINITY, INFINITY}, mx[3] = {-INFINITY, -INFINITY, -INFINITY};
+    int64_t cnt = 0;
+    for (int64_t q = 0; q < per; ++q) {
+      const float* p = pos + ((int64_t)b * per + q) * 3;
+      if (!(isfinite(p[0]) && isfinite(p[1]) && isfinite(p[2]))) continue;
+      ++cnt;
+      for (int c = 0; c < 3; ++c) {
+        if (p[c] < mn[c]) mn[c] = p[c];
+        if (p[c] > mx[c]) mx[c] = p[c];
+      }
+    }
+    float* o = out + (int64_t)b * 8;
+    if (cnt == 0) {
+      for (int c = 0; c < 8; ++c) o[c] = 0.0f;
+      continue;
+    }
+    const float ex = mx[0] - mn[0], ey = mx[1] - mn[1], ez = mx[2] - mn[2];
+    const float d2 = (ex * ex + ey * ey) + ez * ez;
+    const float tf2 = tol_frac * tol_frac;
+    for (int c = 0; c < 3; ++c) {
+      o[c] = mn[c];
+      o[3 + c] = mx[c];
+    }
+    o[6] = tf2 * d2;
+    o[7] = 0.0f;
+  }
+  return 0;
+}
+
+/* ------------------------------------------------------------------ */
+/* O3: correspondence operator G_{A->v}                                 */
+/* ------------------------------------------------------------------ */
+/*
+ * For every target token p of a non-anchor view v and every anchor u
+ * (Sec. 3.2, correspondence operator and multi-anchor aggregation):
+ *   1. P = pos_v(p); background -> no source anywhere.
+ *   2. Project P into anchor u's camera (float, fixed order).  A pinhole
+ *      point with z <= 0, a non-finite projection, or one far off-screen
+ *      ([-2, W+2] x [-2, H+2]) sees nothing.
+ *   3. Candidate source taps are the 2x2 pixels whose centres surround the
+ *      projection: g = proj - 0.5, (x0, y0) = floor(g), a = g - floor(g);
+ *      taps k = 0..3 at (x0 + (k&1), y0 + (k>>1)).
+ *   4. A tap is in tolerance if it is on the grid, its source point Q is
+ *      foreground and |Q - P|^2 <= tol2 (float).  This per-tap test is the
+ *      visibility/occlusion test.
+ *   5. Keep the K in-tolerance taps nearest in 3D (ties: lower k).
+ *   6. Area weights: the overlap of a unit pixel centred on the projection
+ *      with each source pixel, i.e. the bilinear weights
+ *      (1-ax)(1-ay), ax(1-ay), (1-ax)ay, ax*ay, renormalised over the kept
+ *      taps so the anchor's row sums to 1.  If every kept tap has zero area
+ *      the nearest kept tap takes weight 1.  Zero-weight taps are dropped.
+ *   7. Several anchors: the normalised sum of their transports, i.e. each
+ *      visible anchor's row divided by the number n_vis of anchors that see
+ *      p.  Rows with no in-tolerance tap stay zero (disocclusion).
+ * Output word per (pixel, anchor): bits 0-11 = x0+1, bits 12-23 = y0+1,
+ * bits 24-27 = tap mask (bit k = tap k), 0 iff the anchor contributes
+ * nothing.  weights[..][s][j] = final weight of the j-th tap set in the mask
+ * (ascending k), 0 beyond.
+ */
+static int anchor_slot_of(const int32_t* anchors, int a, int v) {
+  for (int s = 0; s < a; ++s)
+    if (anchors[s] == v) return s;
+  return -1;
+}
+
+int orc_build(const float* pos, const int32_t* cam_model, const float* cam_R, const float* cam_t,
+              const float* cam_k, int B, int N, int H, int W, const int32_t* anchors, int a,
+              int K, const float* bbox, int32_t* corr, double* weights, int32_t* nvis_out) {
+  if (a < 1 || a > N || a > 8 || K < 1 || K > 4 || H < 1 || W < 1 || H > 4094 || W > 4094)
+    return -1;
+  for (int s = 0; s < a; ++s) {
+    if (anchors[s] < 0 || anchors[s] >= N) return -1;
+    for (int r = 0; r < s; ++r)
+      if (anchors[r] == anchors[s]) return -1;
+  }
+  const int NT = N - a;
+  const int64_t HW = (int64_t)H * W;
+  int ti = 0;
+  for (int v = 0; v < N; ++v) {
+    if (anchor_slot_of(anchors, a, v) >= 0) continue;
+    for (int b = 0; b < B; ++b) {
+      const float tol2 = bbox[(int64_t)b * 8 + 6];
+      for (int64_t p = 0; p < HW; ++p) {
+        const int64_t row = ((int64_t)b * NT + ti) * HW + p;
+        int32_t* words = corr + row * a;
+        double* wrow = weights + row * a * K;
+        for (int s = 0; s < a; ++s) words[s] = 0;
+        for (int s = 0; s < a * K; ++s) wrow[s] = 0.0;
+        const float* P = pos + (((int64_t)b * N + v) * HW + p) * 3;
+        double wtap[8][4];
+        int masks[8];
+        int n_vis = 0;
+        for (int s = 0; s < a; ++s) {
+          masks[s] = 0;
+          for (int k = 0; k < 4; ++k) wtap[s][k] = 0.0;
+        }
+        if (isfinite(P[0]) && isfinite(P[1]) && isfinite(P[2])) {
+          for (int s = 0; s < a; ++s) {
+            const int u = anchors[s];
+            const int64_t ci = (int64_t)b * N + u;
+            const float* R = cam_R + ci * 9;
+            const float* t = cam_t + ci * 3;
+            const float* kk = cam_k + ci * 4;
+            const float xc = ((R[0] * P[0] + R[1] * P[1]) + R[2] * P[2]) + t[0];
+            const float yc = ((R[3] * P[0] + R[4] * P[1]) + R[5] * P[2]) + t[1];
+            const float zc = ((R[6] * P[0] + R[7] * P[1]) + R[8] * P[2]) + t[2];
+            float px, py;
+            if (cam_model[ci] == 0) {
+              if (!(zc > 0.0f)) continue;
+              px = kk[0] * (xc / zc) + kk[2];
+              py = kk[1] * (yc / zc) + kk[3];
+            } else {
+              px = kk[0] * xc + kk[2];
+              py = kk[1] * yc + kk[3];
+            }
+            if (!(isfinite(px) && isfinite(py))) continue;
+            if (px < -2.0f || px > (float)W + 2.0f || py < -2.0f || py > (float)H + 2.0f) continue;
+            const float gx = px - 0.5f, gy = py - 0.5f;
+            const float fx0 = floorf(gx), fy0 = floorf(gy);
+            const float ax = gx - fx0, ay = gy - fy0;
+            const int x0 = (int)fx0, y0 = (int)fy0;
+            int valid[4];
+            float d2[4];
+            int nvalid = 0;
+            for (int k = 0; k < 4; ++k) {
+              const int x = x0 + (k & 1), y = y0 + (k >> 1);
+              valid[k] = 0;
+              d2[k] = 0.0f;
+              if (x < 0 || x >= W || y < 0 || y >= H) continue;
+              const float* Q = pos + (ci * HW + (int64_t)y * W + x) * 3;
+              if (!(isfinite(Q[0]) && isfinite(Q[1]) && isfinite(Q[2]))) continue;
+              const float dx = Q[0] - P[0], dy = Q[1] - P[1], dz = Q[2] - P[2];
+              const float dd = (dx * dx + dy * dy) + dz * dz;
+              if (!(dd <= tol2)) continue;
+              valid[k] = 1;
+              d2[k] = dd;
+              ++nvalid;
+            }
+            if (nvalid == 0) continue;
+            int sel[4] = {0, 0, 0, 0};
+            if (nvalid <= K) {
+              for (int k = 0; k < 4; ++k) sel[k] = valid[k];
+            } else {
+              for (int r = 0; r < K; ++r) {
+                int best = -1;
+                for (int k = 0; k < 4; ++k) {
+                  if (!valid[k] || sel[k]) continue;
+                  if (best < 0 || d2[k] < d2[best]) best = k;
+                }
+                sel[best] = 1;
+              }
+            }
+            /* one-dimensional overlap factors (float, as the decision of a
+             * zero-area tap is taken in float) */
+            const float wx[2] = {1.0f - ax, ax};
+            const float wy[2] = {1.0f - ay, ay};
+            double area[4];
+            double S = 0.0;
+            for (int k = 0; k < 4; ++k) {
+              area[k] = sel[k] ? (double)wx[k & 1] * (double)wy[k >> 1] : 0.0;
+              S += area[k];
+            }
+            int mask = 0;
+            if (S > 0.0) {
+              for (int k = 0; k < 4; ++k) {
+                if (sel[k] && area[k] > 0.0) {
+                  wtap[s][k] = area[k] / S;
+                  mask |= 1 << k;
+                }
+              }
+            } else {
+              int best = -1;
+              for (int k = 0; k < 4; ++k)
+                if (sel[k] && (best < 0 || d2[k] < d2[best])) best = k;
+              wtap[s][best] = 1.0;
+              mask = 1 << best;
+            }
+            masks[s] = mask;
+            ++n_vis;
+            words[s] = (int32_t)((uint32_t)(x0 + 1) | ((uint32_t)(y0 + 1) << 12) |
+                                 ((uint32_t)mask << 24));
+          }
+        }
+        if (nvis_out) nvis_out[row] = n_vis;
+        if (n_vis == 0) continue;
+        for (int s = 0; s < a; ++s) {
+          int j = 0;
+          for (int k = 0; k < 4; ++k) {
+            if (masks[s] & (1 << k)) {
+              wrow[s * K + j] = wtap[s][k] / (double)n_vis;
+              ++j;
+            }
+          }
+        }
+      }
+    }
+    ++ti;
+  }
+  return 0;
+}
+
+/* ------------------------------------------------------------------ */
+/* O4: delta transport (Eq. 1)                                          */
+/* ------------------------------------------------------------------ */
+/*
+ * One cached step (Sec. 3.2, delta transport and loop order):
+ *   anchor view u = A[s]:   x0_out(u) = x0_anchor_new(s)         (the store
+ *                           keeps x0(t) for all N views)
+ *   target view v not in A: x0_out(v) = x0_prev(v) + G_{A->v}[x0_anchor_new - x0_prev(A)]
+ *   tokens with no valid source keep x0_prev unchanged.
+ * The sum is formed in double; x0_exact receives the unrounded value and
+ * x0_state the value rounded into the storage dtype.
+ */
+int orc_transport(const void* x0_prev, const void* x0_anew, const int32_t* corr,
+                  const double* weights, const int32_t* anchors, int a, int B, int N, int H,
+                  int W, int C, int K, int dtype, double* x0_exact, void* x0_state) {
+  if (a < 1 || a > N || K < 1 || K > 4 || C < 1) return -1;
+  if (dtype != ORC_F32 && dtype != ORC_BF16) return -3;
+  const int NT = N - a;
+  const int64_t HW = (int64_t)H * W;
+  int ti = 0;
+  for (int v = 0; v < N; ++v) {
+    const int sv = anchor_slot_of(anchors, a, v);
+    for (int b = 0; b < B; ++b) {
+      for (int64_t p = 0; p < HW; ++p) {
+        const int64_t orow = (((int64_t)b * N + v) * HW + p) * C;
+        if (sv >= 0) {
+          const int64_t irow = (((int64_t)b * a + sv) * HW + p) * C;
+          for (int c = 0; c < C; ++c) {
+            x0_exact[orow + c] = load_val(x0_anew, irow + c, dtype);
+            copy_val(x0_state, orow + c, x0_anew, irow + c, dtype);
+          }
+          continue;
+        }
+        const int64_t crow = ((int64_t)b * NT + ti) * HW + p;
+        const int32_t* words = corr + crow * a;
+        const double* wrow = weights + crow * a * K;
+        int n_vis = 0;
+        for (int s = 0; s < a; ++s) n_vis += words[s] != 0;
+        for (int c = 0; c < C; ++c) {
+          const double prev = load_val(x0_prev, orow + c, dtype);
+          if (n_vis == 0) {
+            x0_exact[orow + c] = prev;
+            copy_val(x0_state, orow + c, x0_prev, orow + c, dtype);
+            continue;
+          }
+          double acc = 0.0;
+          for (int s = 0; s < a; ++s) {
+            const uint32_t word = (uint32_t)words[s];
+            if (!word) continue;
+            const int x0 = (int)(word & 0xFFFu) - 1;
+            const int y0 = (int)((word >> 12) & 0xFFFu) - 1;
+            const int mask = (int)((word >> 24) & 0xFu);
+            const int u = anchors[s];
+            int j = 0;
+            for (int k = 0; k < 4; ++k) {
+              if (!(mask & (1 << k))) continue;
+              const int64_t q = (int64_t)(y0 + (k >> 1)) * W + (x0 + (k & 1));
+              const double dnew = load_val(x0_anew, (((int64_t)b * a + s) * HW + q) * C + c, dtype);
+              const double dold = load_val(x0_prev, (((int64_t)b * N + u) * HW + q) * C + c, dtype);
+              acc += wrow[s * K + j] * (dnew - dold);
+              ++j;
+            }
+          }
+          const double out = prev + acc;
+          x0_exact[orow + c] = out;
+          store_val(x0_state, orow + c, dtype, out);
+        }
+      }
+    }
+    if (sv < 0) ++ti;
+  }
+  return 0;
+}
+
+/* ------------------------------------------------------------------ */
+/* O5: sampler-consistent reconstruction                                */
+/* ------------------------------------------------------------------ */
+/*
+ * From the transported x0 the sampler's own quantities are recovered with
+ * the closed forms at the step's noise level (Sec. 3.2, after Eq. 1):
+ *   DDIM (eta = 0):  eps = (x_t - sqrt(abar_t) x0) / sqrt(1 - abar_t)
+ *                    v   = sqrt(abar_t) eps - sqrt(1 - abar_t) x0
+ *                    x_next = sqrt(abar_n) x0 + sqrt(1 - abar_n) eps
+ *   flow matching:   x_sigma = (1 - sigma) x0 + sigma eps, velocity
+ *                    vel = (x_t - x0) / sigma_t,
+ *                    x_next = x_t + (sigma_n - sigma_t) vel   (Euler)
+ * abar_t = prod_{i<=t} (1 - beta_i), beta linear from beta_start to
+ * beta_end over T steps (0-based), abar_{-1} = 1.
+ * pred: 0 none, 1 eps, 2 v (DDIM), 3 velocity (flow).
+ */
+double orc_alpha_bar(int T, double beta_start, double beta_end, int t) {
+  if (t < 0) return 1.0;
+  double ab = 1.0;
+  for (int i = 0; i <= t; ++i) {
+    const double beta = beta_start + (beta_end - beta_start) * (double)i / (double)(T - 1);
+    ab *= 1.0 - beta;
+  }
+  return ab;
+}
+
+int orc_reconstruct(const void* x_t, const void* x0, int64_t n, int dtype, int kind, int pred,
+                    int T, double beta_start, double beta_end, double t, double t_next,
+                    double* x_next, double* model_out) {
+  if (dtype != ORC_F32 && dtype != ORC_BF16) return -3;
+  if (kind == 0) {
+    if (T < 2 || t < 0 || t >= T || t_next >= t || t_next < -1) return -1;
+    if (pred != 0 && pred != 1 && pred != 2) return -1;
+    const double ab_t = orc_alpha_bar(T, beta_start, beta_end, (int)t);
+    const double ab_n = orc_alpha_bar(T, beta_start, beta_end, (int)t_next);
+    const double a_t = sqrt(ab_t), s_t = sqrt(1.0 - ab_t);
+    const double a_n = sqrt(ab_n), s_n = sqrt(1.0 - ab_n);
+    for (int64_t i = 0; i < n; ++i) {
+      const double xt = load_val(x_t, i, dtype), z = load_val(x0, i, dtype);
+      const double eps = (xt - a_t * z) / s_t;
+      x_next[i] = a_n * z + s_n * eps;
+      if (pred == 1 && model_out) model_out[i] = eps;
+      if (pred == 2 && model_out) model_out[i] = a_t * eps - s_t * z;
+    }
+    return 0;
+  }
+  if (kind == 1) {
+    if (!(t > 0.0) || t > 1.0 || t_next < 0.0 || t_next > t) return -1;
+    if (pred != 0 && pred != 3) return -1;
+    for (int64_t i = 0; i < n; ++i) {
+      const double xt = load_val(x_t, i, dtype), z = load_val(x0, i, dtype);
+      const double vel = (xt - z) / t;
+      x_next[i] = xt + (t_next - t) * vel;
+      if (pred == 3 && model_out) model_out[i] = vel;
+    }
+    return 0;
+  }
+  return -1;
+}
+
+/* ------------------------------------------------------------------ */
+/* O6: host schedule                                                    */
+/* ------------------------------------------------------------------ */
+/*
+ * Anchors rotate every cached step and every view returns to the anchor set
+ * within ceil(N/a) cached steps (Sec. 3.2, batch-sliced anchor forward).
+ * Rule: A_c = {(c + floor(j*N/a)) mod N : j < a}, slots in ascending view
+ * order.
+ */
+int orc_anchors(int N, int a, int64_t c, int32_t* out) {
+  if (a < 1 || a > N || c < 0) return -1;
+  for (int j = 0; j < a; ++j) out[j] = (int32_t)((c + ((int64_t)j * N) / a) % N);
+  for (int i = 1; i < a; ++i) {
+    int32_t x = out[i];
+    int k = i - 1;
+    while (k >= 0 && out[k] > x) {
+      out[k + 1] = out[k];
+      --k;
+    }
+    out[k + 1] = x;
+  }
+  return 0;
+}
+
+/*
+ * Full-view steps (Sec. 3.2, drift-bounding schedule; Sec. 4.1,
+ * configurations).  rule 0: every E-th step (0, E, 2E, ...); rule 1:
+ * two-step head, one mid refresh at floor(S/2), one tail step S-1.
+ * Step 0 is always full.  out[k] = 1 for a full step.
+ */
+int orc_full_steps(int rule, int S, int E, uint8_t* out) {
+  if (S < 1) return -1;
+  for (int k = 0; k < S; ++k) out[k] = 0;
+  if (rule == 0) {
+    if (E < 1) return -1;
+    for (int k = 0; k < S; k += E) out[k] = 1;
+  } else if (rule == 1) {
+    out[0] = 1;
+    if (S > 1) out[1] = 1;
+    out[S / 2] = 1;
+    out[S - 1] = 1;
+  } else {
+    return -1;
+  }
+  out[0] = 1;
+  return 0;
+}
+
+/* DDIM "trailing" timesteps: t_k = round((S - k) * T / S) - 1, t_S = -1. */
+int orc_ddim_timesteps(int T, int S, int32_t* out) {
+  if (S < 1 || T < S) return -1;
+  for (int k = 0; k < S; ++k) out[k] = (int32_t)floor((double)(S - k) * T / S + 0.5) - 1;
+  out[S] = -1;
+  return 0;
+}
