@@ -1,0 +1,313 @@
+"""Benchmark of the per-step cross-view transport on one MI355X.
+
+One timed step is one cached denoising step of the workload: the host
+schedule picks the step's anchor set (gc_schedule_anchors) and its
+precomputed correspondence, then gc_transport_reconstruct runs Eq. 1 and the
+sampler-consistent Euler/DDIM update over every view of every asset.  Inputs
+are resident in HBM; each step uses the next of several buffer sets so that
+the 256 MB last-level cache cannot serve a step from the previous one.
+
+Reported (one JSON line):
+  value      transported view-pixels per second, B * (N - a) * H * W per step
+  roofline   the fused kernel's algorithmic bytes per launch over its average
+             launch duration (HIP events on the launch stream), against 8 TB/s
+  cpu_baseline  the oracle's transport + reconstruction on one asset, timed
+             single-threaded on the host
+The once-per-asset rows (area downsample, bbox, correspondence builds) and
+the unfused pair are timed too and reported under "rows".
+"""
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBS = 8000.0
+FUSED_KERNEL = "k_transport<1, 8, true>"     # bf16, 16-byte vectors, fused
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--config", default="stress_torusknot_12v_128x16_b8")
+    ap.add_argument("--ring", type=int, default=3, help="buffer sets cycled through (defeats the LLC)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="also run a plain 1 GiB device copy (reference kernel for counter scaling)")
+    ap.add_argument("--quiet", action="store_true")
+    return ap.parse_args()
+
+
+def log(args, *a):
+    if not args.quiet:
+        print(*a, file=sys.stderr, flush=True)
+
+
+def kernel_source_hash():
+    h = hashlib.sha256()
+    for f in ("gc_transport.hip", "gc_common.h"):
+        h.update(open(os.path.join(ROOT, "paper_2608_13255_amd", "csrc", f), "rb").read())
+    return h.hexdigest()[:16]
+
+
+def read_traffic(workload):
+    """HBM bytes per launch of the fused kernel from the committed rocprofv3
+    counter summary, if it was taken on the current kernel source."""
+    path = os.path.join(ROOT, "profiles", f"fused_transport_reconstruct_{workload}_counters.txt")
+    if not os.path.exists(path):
+        return None
+    vals = {}
+    for line in open(path):
+        if ":" in line and line.split(":")[0].strip() in ("source_hash", "hbm_bytes_per_launch"):
+            k, v = line.split(":", 1)
+            vals[k.strip()] = v.strip()
+    if vals.get("source_hash") != kernel_source_hash() or "hbm_bytes_per_launch" not in vals:
+        return None
+    return float(vals["hbm_bytes_per_launch"])
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU: --gpus {args.gpus} is not supported (assets shard across GPUs with "
+              f"no communication; run one process per GPU)", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2608_13255_amd as gc
+    import synth
+
+    w = synth.CONFIGS[args.config]
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    tdtype = torch.float32 if w.dtype == "f32" else torch.bfloat16
+    B, N, H, W, C, a, K = w.B, w.N, w.H, w.W, w.C, w.a, w.K
+    HW = H * W
+    es = 4 if w.dtype == "f32" else 2
+
+    # ---- inputs (seeded, synthetic) --------------------------------------
+    t0 = time.time()
+    hi = synth.render_position_maps(w)
+    cams_np = synth.batch_cameras(w)
+    log(args, f"[bench] rendered {hi.shape} in {time.time() - t0:.1f}s")
+    hi_d = torch.from_numpy(hi).to(dev)
+    del hi
+    cams = gc.camera_tensor(cams_np, dev)
+
+    smp = gc.Sampler(kind=gc.GC_DDIM if w.sampler == "ddim" else gc.GC_FLOW_EULER)
+    full = gc.gc_schedule_full_steps(gc.GC_FULL_PERIODIC if w.full_rule == "periodic" else gc.GC_FULL_HEAD_MID_TAIL,
+                                     w.S, w.full_E)
+    cached_steps = [k for k in range(w.S) if not full[k]]
+    anchor_sets = []
+    for c in range(N):
+        A = tuple(gc.gc_schedule_anchors(N, a, c))
+        if A not in anchor_sets:
+            anchor_sets.append(A)
+
+    def ev():
+        return torch.cuda.Event(enable_timing=True)
+
+    # ---- once per asset: downsample, bbox, builds (rows a0-a2) -------------
+    rows = {}
+    for rep in range(3):
+        e0, e1, e2, e3 = ev(), ev(), ev(), ev()
+        e0.record()
+        if w.factor > 1:
+            pos = gc.gc_posmap_downsample(hi_d, w.factor)
+        else:
+            pos = hi_d.clone()
+        e1.record()
+        bbox = gc.gc_posmap_bbox(pos, w.tol_frac)
+        e2.record()
+        ops = {}
+        stats = {}
+        for A in anchor_sets:
+            st = torch.empty((B, 4), dtype=torch.int32, device=dev)
+            ops[A] = gc.gc_build_correspondence(pos, cams, list(A), K, bbox, stats=st)
+            stats[A] = st
+        e3.record()
+        torch.cuda.synchronize()
+    rows["downsample_ms"] = e0.elapsed_time(e1)
+    rows["downsample_GBps"] = hi_d.numel() * 4 / (e0.elapsed_time(e1) * 1e-3) / 1e9 if w.factor > 1 else None
+    rows["bbox_ms"] = e1.elapsed_time(e2)
+    rows["build_ms_per_anchor_set"] = e2.elapsed_time(e3) / len(anchor_sets)
+    rows["anchor_sets"] = len(anchor_sets)
+    vis_pairs = {A: int(stats[A][:, 0].sum().item()) for A in anchor_sets}
+    cover = {A: float(stats[A][:, 1].sum().item()) / max(1, float(stats[A][:, 2].sum().item())) for A in anchor_sets}
+    del hi_d
+    torch.cuda.empty_cache()
+
+    # ---- latent buffers: a ring of sets ------------------------------------
+    t0 = time.time()
+    x0_prev_np = synth.x0_state(w, pos.cpu().numpy(), cached_steps[0] - 1)
+    eps_np = synth.eps_noise(w, 0)
+    log(args, f"[bench] synthetic latents in {time.time() - t0:.1f}s")
+
+    def dev_lat(x):
+        return torch.from_numpy(x).to(dev).to(tdtype)
+
+    base_prev = dev_lat(x0_prev_np)
+    base_eps = dev_lat(eps_np)
+    ring = []
+    for r in range(args.ring):
+        x0_prev = base_prev.clone()
+        x_t = (base_prev.float() * 0.5 + base_eps.float() * 0.5).to(tdtype)
+        x0_new = (base_prev[:, :a].float() + 0.01 * (r + 1)).to(tdtype).contiguous()
+        ring.append(dict(x0_prev=x0_prev, x0_new=x0_new, x_t=x_t, x0_out=torch.empty_like(x0_prev),
+                         x_next=torch.empty_like(x0_prev)))
+    del base_prev, base_eps
+    torch.cuda.synchronize()
+
+    latent_view = HW * C * es
+    V = B * (N - a) * HW
+
+    def algo_bytes(A):
+        return B * (4 * N + a) * latent_view + 4 * B * (N - a) * HW * a + 4 * K * vis_pairs[A]
+
+    def step(i, events=None):
+        c = i
+        A = gc.gc_schedule_anchors(N, a, c)
+        corr, wts = ops[tuple(A)]
+        k = cached_steps[i % len(cached_steps)]
+        t, tn = gc.gc_sampler_step_times(smp, w.S, k)
+        buf = ring[i % len(ring)]
+        if events is not None:
+            events[0].record()
+        gc.gc_transport_reconstruct(buf["x0_prev"], buf["x0_new"], corr, wts, buf["x_t"], A, smp, t, tn,
+                                    x0_out=buf["x0_out"], x_next=buf["x_next"])
+        if events is not None:
+            events[1].record()
+        return tuple(A)
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+
+    # ---- timed region -------------------------------------------------------
+    per_launch = [(ev(), ev()) for _ in range(args.steps)]
+    used = []
+    start, end = ev(), ev()
+    torch.cuda.synchronize()
+    start.record()
+    for i in range(args.steps):
+        used.append(step(args.warmup + i, per_launch[i]))
+    end.record()
+    torch.cuda.synchronize()
+    total_ms = start.elapsed_time(end)
+    ms_per_step = total_ms / args.steps
+    durs = np.array([s.elapsed_time(e) for s, e in per_launch])
+    avg_kernel_ms = float(durs.mean())
+    bytes_per_launch = float(np.mean([algo_bytes(A) for A in used]))
+    achieved = bytes_per_launch / (avg_kernel_ms * 1e-3) / 1e9
+
+    # ---- unfused pair and full step, for the record -------------------------
+    def timed(fn, n=20):
+        fn()
+        torch.cuda.synchronize()
+        s, e = ev(), ev()
+        s.record()
+        for _ in range(n):
+            fn()
+        e.record()
+        torch.cuda.synchronize()
+        return s.elapsed_time(e) / n
+
+    A0 = list(anchor_sets[0])
+    corr0, wts0 = ops[anchor_sets[0]]
+    buf = ring[0]
+    kc = cached_steps[0]
+    tt, ttn = gc.gc_sampler_step_times(smp, w.S, kc)
+    rows["transport_only_ms"] = timed(lambda: gc.gc_transport_step(buf["x0_prev"], buf["x0_new"], corr0, wts0, A0,
+                                                                   x0_out=buf["x0_out"]))
+    rows["reconstruct_only_ms"] = timed(lambda: gc.gc_sampler_reconstruct(buf["x_t"], buf["x0_out"], smp, tt, ttn,
+                                                                          x_next=buf["x_next"]))
+    rows["unfused_pair_ms"] = rows["transport_only_ms"] + rows["reconstruct_only_ms"]
+    rows["coverage_per_anchor_set"] = [round(cover[A], 4) for A in anchor_sets]
+    rows["visible_pairs_per_anchor_set"] = [vis_pairs[A] for A in anchor_sets]
+    rows["p10_p50_p90_kernel_us"] = [round(float(np.percentile(durs, q)) * 1e3, 2) for q in (10, 50, 90)]
+
+    copy_gbps = None
+    if args.copy_probe:
+        src = torch.empty(1 << 28, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        src.fill_(1.0)
+        ms = timed(lambda: dst.copy_(src), n=10)
+        copy_gbps = 2 * src.numel() * 4 / (ms * 1e-3) / 1e9
+        rows["copy_1GiB_GBps"] = copy_gbps
+        del src, dst
+
+    # ---- CPU baseline: the oracle on one asset ------------------------------
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(w, pos[:1].cpu().numpy(), cams_np, x0_prev_np[:1], args.cpu_seconds)
+
+    traffic = read_traffic(w.name)
+    out = {
+        "metric": "transported view-pixels/s per denoising step; achieved HBM GB/s vs peak",
+        "value": V / (ms_per_step * 1e-3),
+        "unit": "view-pixels/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if w.dtype == "bf16" else "f32",
+        "data": "synthetic (seeded torus-knot renders, synthetic x0 fields)",
+        "config": {"workload": w.name, "assets": B, "views": N, "latent": [H, W, C], "anchors": a, "K": K,
+                   "sampler": w.sampler, "steps_S": w.S, "render": w.render, "ring_buffers": args.ring,
+                   "parallelism": "single GPU"},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                     "frac": achieved / PEAK_HBM_GBS,
+                     "traffic": traffic, "kernel": FUSED_KERNEL, "algorithmic_bytes_per_launch": bytes_per_launch,
+                     "avg_launch_us": avg_kernel_ms * 1e3},
+        "cpu_baseline": cpu,
+        "rows": rows,
+    }
+    print(json.dumps(out), flush=True)
+
+
+def cpu_baseline(w, pos1, cams_np, x0_prev1, seconds):
+    """The oracle's cached step (transport + reconstruction) on one asset,
+    single-threaded, repeated for about `seconds` seconds."""
+    import numpy as np
+
+    import oracle
+    import synth
+
+    cams1 = {k: v[:1] for k, v in cams_np.items()}
+    A = oracle.anchors(w.N, w.a, 0)
+    bb = oracle.bbox(pos1, w.tol_frac)
+    corr, wts, _ = oracle.build(pos1, cams1, A, w.K, bb)
+    prev = synth.storage(x0_prev1, w.dtype)
+    new = synth.storage(x0_prev1[:, A] + np.float32(0.01), w.dtype)
+    xt = synth.storage(0.5 * x0_prev1, w.dtype)
+    t, tn = oracle.step_times(w.sampler, w.S, 2)
+    reps = 0
+    t0 = time.perf_counter()
+    while True:
+        _, st = oracle.transport(prev, new, corr, wts, A, w.dtype)
+        oracle.reconstruct(xt, st, w.dtype, w.sampler, t, tn)
+        reps += 1
+        el = time.perf_counter() - t0
+        if el >= seconds:
+            break
+    vp = reps * (w.N - w.a) * w.H * w.W
+    return {"value": vp / el, "unit": "view-pixels/s", "cores": 1, "kind": "oracle",
+            "sample": f"{reps} cached steps of 1 of {w.B} assets ({w.N} views, {w.H}x{w.W}x{w.C} {w.dtype}, "
+                      f"a={w.a}, K={w.K}), transport + reconstruction, {el:.1f}s on one host thread"}
+
+
+if __name__ == "__main__":
+    main()

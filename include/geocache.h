@@ -1,0 +1,282 @@
+/*
+ * geocache.h -- C ABI of the MI355X (gfx950) cross-view delta-transport library.
+ *
+ * GeoCache ("Training-Free Acceleration of Multi-View Texture Diffusion via
+ * Geometric Delta Transport") runs the denoiser on a rotating subset of anchor
+ * views at a cached step and carries the anchors' per-step change in the
+ * predicted clean signal x0 to every other view through a geometric
+ * correspondence built from the views' position maps (Sec. 3.2).  This
+ * library implements that per-step path on the GPU:
+ *
+ *   once per asset       gc_posmap_downsample   render-res position maps -> latent grid
+ *                        gc_posmap_bbox         per-asset bbox and squared tolerance
+ *                        gc_build_correspondence   G_{A->v} for one anchor set
+ *   every cached step    gc_transport_step      Eq. 1: x0(v) = x0_prev(v) + G[dx0(A)]
+ *                        gc_sampler_reconstruct sampler-consistent eps / v / velocity + x_t update
+ *                        gc_transport_reconstruct  the two above fused in one pass
+ *   host schedule        gc_schedule_anchors, gc_schedule_full_steps, gc_sampler_step_times
+ *
+ * Conventions shared by every call
+ *   - Every call returns GC_OK (0) or a negative GC_ERR_* code and never
+ *     throws.  gc_last_error() returns a thread-local description of the last
+ *     failure on the calling thread.
+ *   - All arguments are validated on the host before anything is launched, so
+ *     a call that fails has no side effects on device memory.
+ *   - The library never allocates, frees or copies device memory on its own:
+ *     every device buffer is owned by the caller, contiguous, and passed as a
+ *     plain device pointer.  Host arrays (anchor lists, sampler parameters) are
+ *     read during the call only.
+ *   - Device work is enqueued on the given HIP stream (0 = the null stream)
+ *     and is asynchronous: nothing synchronises.  A launch failure maps to
+ *     GC_ERR_HIP; faults during execution surface at the caller's next
+ *     synchronisation.  With the environment variable GC_SYNC_CHECK=1 every
+ *     call synchronises its stream and checks for errors before returning.
+ *   - Calls keep no state between invocations and are safe to issue
+ *     concurrently on different streams with disjoint outputs.
+ *   - Latent tensors are NHWC per view: [B][views][H][W][C], B assets, C a
+ *     multiple of 4 (at most GC_MAX_CHANNELS), stored as float32 (GC_F32) or
+ *     bfloat16 (GC_BF16, round-to-nearest-even on output); arithmetic is
+ *     float32.  NaN/Inf in latents is data and propagates.
+ *   - Position maps are float32 [..][H][W][3] world coordinates of the surface
+ *     point seen through each pixel; a pixel with any non-finite component is
+ *     background.
+ *   - Pointer alignment: latents, position maps, correspondence words and
+ *     weights must be 16-byte aligned (GC_ERR_ALIGN otherwise).
+ */
+#ifndef GEOCACHE_H
+#define GEOCACHE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define GC_ABI_VERSION 1
+
+/* limits */
+#define GC_MAX_VIEWS 64     /* views per asset */
+#define GC_MAX_ANCHORS 8    /* anchors per cached step */
+#define GC_MAX_GRID 4094    /* latent H and W (12-bit packed tap coordinates) */
+#define GC_MAX_CHANNELS 256 /* latent channels */
+
+/* status codes */
+#define GC_OK 0
+#define GC_ERR_ARG (-1)      /* null pointer, out-of-range scalar, bad anchor list */
+#define GC_ERR_SHAPE (-2)    /* inconsistent or unsupported sizes */
+#define GC_ERR_DTYPE (-3)    /* unknown latent dtype */
+#define GC_ERR_ALIGN (-4)    /* a device pointer is not 16-byte aligned */
+#define GC_ERR_ALIAS (-5)    /* an output overlaps an input it must not overlap */
+#define GC_ERR_CAPACITY (-6) /* a size exceeds a library limit */
+#define GC_ERR_HIP (-7)      /* the HIP runtime reported an error */
+
+/* latent storage types */
+#define GC_F32 0
+#define GC_BF16 1
+
+/* sampler kinds and optional model-parameterisation outputs */
+#define GC_DDIM 0         /* DDIM, eta = 0, linear beta schedule over T steps */
+#define GC_FLOW_EULER 1   /* flow matching x = (1 - sigma) x0 + sigma eps, Euler */
+#define GC_PRED_NONE 0
+#define GC_PRED_EPS 1     /* DDIM: eps */
+#define GC_PRED_V 2       /* DDIM: v = sqrt(abar) eps - sqrt(1 - abar) x0 */
+#define GC_PRED_VEL 3     /* flow: velocity (x_t - x0) / sigma */
+
+/* full-step rules for gc_schedule_full_steps */
+#define GC_FULL_PERIODIC 0      /* steps 0, E, 2E, ... */
+#define GC_FULL_HEAD_MID_TAIL 1 /* steps 0, 1, floor(S/2), S-1 */
+
+/*
+ * A pinhole or orthographic camera (68 bytes, 4-byte aligned).
+ * World -> camera: x_c = R * X + t, R row-major; camera axes x right, y down,
+ * z forward.  Intrinsics are in latent-pixel units; pixel i spans [i, i+1).
+ *   model 0 (pinhole):      u = fx * (x_c / z_c) + cx,  v = fy * (y_c / z_c) + cy,
+ *                           a point with z_c <= 0 is not seen
+ *   model 1 (orthographic): u = fx * x_c + cx,          v = fy * y_c + cy
+ * Any other model value makes the camera see nothing.
+ */
+typedef struct gc_camera {
+  int32_t model;
+  float R[9];
+  float t[3];
+  float fx, fy, cx, cy;
+} gc_camera;
+
+/*
+ * Sampler description (32 bytes).  kind = GC_DDIM uses T, beta_start and
+ * beta_end (beta_i linear in i over 0..T-1, abar_t = prod_{i<=t}(1 - beta_i),
+ * abar_{-1} = 1); kind = GC_FLOW_EULER ignores them.  pred_out selects the
+ * optional model_out tensor of the reconstruction (GC_PRED_*).
+ */
+typedef struct gc_sampler {
+  int32_t kind;
+  int32_t pred_out;
+  int32_t T;
+  int32_t reserved;
+  double beta_start;
+  double beta_end;
+} gc_sampler;
+
+/* GC_ABI_VERSION of the loaded library. */
+int gc_abi_version(void);
+
+/* Description of the last error on this thread ("" if none).  The pointer is
+ * valid until the next gc_* call on the same thread. */
+const char* gc_last_error(void);
+
+/*
+ * Area-downsample render-resolution position maps to the latent grid.
+ * Position maps supply each latent token's 3D point (Sec. 3.1, motivating
+ * study; Sec. 3.2, correspondence operator); a render at f times the latent
+ * resolution is reduced by averaging each f x f block over its foreground
+ * samples.  A block with fewer than half foreground samples is background
+ * (NaN).  The block mean is accumulated in double and rounded once to float.
+ *   pos_hi   device float [n_maps][Hr][Wr][3]
+ *   pos_lat  device float [n_maps][Hr/f][Wr/f][3] (output; must not overlap pos_hi)
+ *   f        1..64, dividing Hr and Wr; Hr/f and Wr/f at most GC_MAX_GRID.
+ */
+int gc_posmap_downsample(const float* pos_hi, int64_t n_maps, int Hr, int Wr, int f, float* pos_lat,
+                         hipStream_t stream);
+
+/*
+ * Per-asset bounding box and squared match tolerance.  The tolerance is
+ * tol_frac (the paper uses 1%) of the bounding-box diagonal of the asset
+ * (Sec. 3.2, correspondence operator); it is kept squared in float:
+ *   e = max - min per axis, d2 = (ex*ex + ey*ey) + ez*ez,
+ *   tol2 = (tol_frac*tol_frac) * d2.
+ *   pos   device float [B][N][H][W][3] latent-grid position maps
+ *   bbox  device float [B][8] output = {min x,y,z, max x,y,z, tol2, 0};
+ *         an asset without a foreground sample gets all zeros.
+ * 0 < tol_frac <= 1.
+ */
+int gc_posmap_bbox(const float* pos, int B, int N, int H, int W, float tol_frac, float* bbox,
+                   hipStream_t stream);
+
+/*
+ * Build the correspondence operator G_{A->v} for every non-anchor view v of
+ * every asset, for one anchor set A (Sec. 3.2: correspondence operator,
+ * multi-anchor aggregation, invalid matches).  For target token p with 3D
+ * point P and anchor slot s (view u = anchors[s]):
+ *   - project P into camera u; the 2x2 source pixels whose centres surround
+ *     the projection are the candidate taps (g = proj - 0.5, (x0, y0) =
+ *     floor(g), taps k = 0..3 at (x0 + (k&1), y0 + (k>>1)));
+ *   - a tap is valid if on the grid, foreground and |Q - P|^2 <= tol2
+ *     (the per-tap visibility/occlusion test);
+ *   - keep the K valid taps nearest in 3D (ties: lower k);
+ *   - weights are the taps' overlap areas with a unit pixel centred on the
+ *     projection (bilinear weights), renormalised over the kept taps; if all
+ *     kept areas are zero the nearest kept tap gets 1; zero-weight taps are
+ *     dropped; finally every anchor that sees p is divided by n_vis, the
+ *     number of such anchors, so each visible row sums to 1 and rows no
+ *     anchor sees are zero.
+ * All projection and distance arithmetic is IEEE float in a fixed order.
+ *   pos      device float [B][N][H][W][3]
+ *   cams     device gc_camera [B][N]
+ *   anchors  host int32 [a]: distinct views in [0, N); slot s = position in the list
+ *   a        1..min(N, GC_MAX_ANCHORS); a == N is legal and produces empty outputs
+ *   K        taps kept per anchor, 1..4
+ *   bbox     device float [B][8] from gc_posmap_bbox (only tol2 is read)
+ *   corr     device int32 [B][N-a][H][W][a] output, target views in ascending
+ *            view order: word = (x0+1) | (y0+1) << 12 | mask << 24, mask bit k
+ *            set for each kept tap; 0 iff anchor s contributes nothing
+ *   weights  device float [B][N-a][H][W][a][K] output: final weight of the j-th
+ *            tap set in the word (ascending k), 0 beyond
+ *   stats    nullable device uint32 [B][4] output (zeroed by the call):
+ *            {visible (pixel, anchor) pairs, target pixels seen by >= 1 anchor,
+ *             foreground target pixels, kept taps}
+ * H, W at most GC_MAX_GRID; N at most GC_MAX_VIEWS.
+ */
+int gc_build_correspondence(const float* pos, const gc_camera* cams, int B, int N, int H, int W,
+                            const int32_t* anchors, int a, int K, const float* bbox, int32_t* corr,
+                            float* weights, uint32_t* stats, hipStream_t stream);
+
+/*
+ * Delta transport, Eq. 1 (Sec. 3.2, delta transport and loop order), for one
+ * cached step:
+ *   anchor view u = anchors[s]:  x0_out(u) = x0_anchor_new(s)          (copy)
+ *   other view v:  x0_out(v) = x0_prev(v) + sum_s sum_k w * (x0_anchor_new(s)[q] - x0_prev(u)[q])
+ * accumulated in float (anchors in slot order, taps in ascending k), added to
+ * x0_prev(v) and rounded to the storage dtype.  Tokens no anchor sees are a
+ * bit copy of x0_prev(v).
+ *   x0_prev        device [B][N][H][W][C]  stored x0 of the previous step, all views
+ *   x0_anchor_new  device [B][a][H][W][C]  this step's anchor predictions, slot order
+ *   corr, weights  as written by gc_build_correspondence for the same anchor list, B, N, H, W, K
+ *   x0_out         device [B][N][H][W][C]  output; must not overlap x0_prev or x0_anchor_new
+ */
+int gc_transport_step(const void* x0_prev, const void* x0_anchor_new, const int32_t* corr,
+                      const float* weights, int B, int N, int H, int W, int C, const int32_t* anchors,
+                      int a, int K, int dtype, void* x0_out, hipStream_t stream);
+
+/*
+ * Sampler-consistent reconstruction (Sec. 3.2, after Eq. 1): from x0 and the
+ * current state x_t at the step's noise level, recover the sampler's own
+ * quantities by the closed forms and take the sampler step.  Elementwise over
+ * n_elems values, float32 arithmetic with coefficients computed on the host in
+ * double and rounded once to float.
+ *   GC_DDIM (eta = 0; t, t_next integer timesteps, t_next = -1 for the end):
+ *     eps = (x_t - sqrt(abar_t) x0) / sqrt(1 - abar_t)
+ *     x_next = sqrt(abar_n) x0 + sqrt(1 - abar_n) eps
+ *     model_out = eps (GC_PRED_EPS) or sqrt(abar_t) eps - sqrt(1 - abar_t) x0 (GC_PRED_V)
+ *   GC_FLOW_EULER (t = sigma_t in (0, 1], t_next = sigma_n in [0, t]):
+ *     vel = (x_t - x0) / sigma_t,  x_next = x_t + (sigma_n - sigma_t) vel
+ *     model_out = vel (GC_PRED_VEL)
+ *   x_t, x0    device [n_elems]
+ *   x_next     device [n_elems] output; may be x_t itself (in place), must not
+ *              otherwise overlap x_t or x0
+ *   model_out  nullable device [n_elems] output (required iff pred_out != GC_PRED_NONE)
+ *   n_elems    a multiple of 4
+ */
+int gc_sampler_reconstruct(const void* x_t, const void* x0, void* x_next, void* model_out,
+                           int64_t n_elems, int dtype, const gc_sampler* smp, double t, double t_next,
+                           hipStream_t stream);
+
+/*
+ * gc_transport_step followed by gc_sampler_reconstruct over all B*N views, in
+ * one pass (one read of every input, one write of every output).  The
+ * reconstruction consumes x0_out as stored (rounded to the dtype), so the
+ * result is bit-identical to the two separate calls.
+ *   x_t        device [B][N][H][W][C]
+ *   x0_out     device [B][N][H][W][C] output (the next step's x0_prev)
+ *   x_next     device [B][N][H][W][C] output; may be x_t itself
+ *   model_out  nullable device [B][N][H][W][C] output
+ * x0_out, x_next and model_out must not overlap x0_prev, x0_anchor_new or each
+ * other (x_next == x_t excepted).
+ */
+int gc_transport_reconstruct(const void* x0_prev, const void* x0_anchor_new, const int32_t* corr,
+                             const float* weights, const void* x_t, int B, int N, int H, int W,
+                             int C, const int32_t* anchors, int a, int K, int dtype,
+                             const gc_sampler* smp, double t, double t_next, void* x0_out,
+                             void* x_next, void* model_out, hipStream_t stream);
+
+/*
+ * Host schedule (no device work).
+ *
+ * gc_schedule_anchors: anchors of cached step c (Sec. 3.2, batch-sliced anchor
+ * forward: anchors rotate every step and each view returns to the anchor set
+ * within ceil(N/a) steps): A_c = {(c + floor(j*N/a)) mod N : j < a}, written
+ * in ascending view order to anchors_out[a].
+ *
+ * gc_schedule_full_steps: is_full_out[k] = 1 for the full-view steps of an
+ * S-step trajectory (Sec. 3.2, drift-bounding schedule; Sec. 4.1,
+ * configurations): GC_FULL_PERIODIC every E-th step, GC_FULL_HEAD_MID_TAIL
+ * steps {0, 1, floor(S/2), S-1}.  Step 0 is always full.
+ *
+ * gc_sampler_step_times: (t, t_next) of step k of an S-step trajectory.
+ * DDIM: trailing timesteps t_k = round((S-k) T / S) - 1 and t_S = -1.
+ * Flow: sigma_k = 1 - k/S.
+ *
+ * gc_sampler_alpha_bar: abar_t of the DDIM schedule (1 for t = -1).
+ */
+int gc_schedule_anchors(int N, int a, int64_t c, int32_t* anchors_out);
+int gc_schedule_full_steps(int rule, int S, int E, uint8_t* is_full_out);
+int gc_sampler_step_times(const gc_sampler* smp, int S, int k, double* t, double* t_next);
+int gc_sampler_alpha_bar(const gc_sampler* smp, int t, double* abar);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GEOCACHE_H */

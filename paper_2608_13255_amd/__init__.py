@@ -1,0 +1,321 @@
+"""MI355X-native GeoCache cross-view delta transport.
+
+Python binding of libgeocache.so (hand-written HIP kernels for gfx950 behind
+the C ABI declared in include/geocache.h).  Every function here has the name
+of the C entry point it wraps and only marshals arguments: it checks torch
+tensors (device, dtype, contiguity, shape), allocates outputs the caller did
+not supply, passes raw device pointers and the current HIP stream, and turns
+a negative status into GeoCacheError.  All computation runs in the library's
+kernels; there is no CPU fallback, and importing the package fails if the
+library has not been built.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+from typing import Dict, List, Optional, Sequence, Tuple
+
+import numpy as np
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libgeocache.so")
+
+# constants mirrored from include/geocache.h
+GC_OK = 0
+GC_F32, GC_BF16 = 0, 1
+GC_DDIM, GC_FLOW_EULER = 0, 1
+GC_PRED_NONE, GC_PRED_EPS, GC_PRED_V, GC_PRED_VEL = 0, 1, 2, 3
+GC_FULL_PERIODIC, GC_FULL_HEAD_MID_TAIL = 0, 1
+GC_MAX_VIEWS, GC_MAX_ANCHORS, GC_MAX_GRID = 64, 8, 4094
+ERRORS = {-1: "GC_ERR_ARG", -2: "GC_ERR_SHAPE", -3: "GC_ERR_DTYPE", -4: "GC_ERR_ALIGN",
+          -5: "GC_ERR_ALIAS", -6: "GC_ERR_CAPACITY", -7: "GC_ERR_HIP"}
+
+# gc_camera: int32 model, float R[9], float t[3], fx, fy, cx, cy (68 bytes)
+CAMERA_DTYPE = np.dtype([("model", "<i4"), ("R", "<f4", (9,)), ("t", "<f4", (3,)), ("fx", "<f4"),
+                         ("fy", "<f4"), ("cx", "<f4"), ("cy", "<f4")])
+assert CAMERA_DTYPE.itemsize == 68
+
+
+class GeoCacheError(RuntimeError):
+    def __init__(self, func: str, code: int, msg: str):
+        super().__init__(f"{func} failed with {ERRORS.get(code, code)}: {msg}")
+        self.code = code
+
+
+class _Sampler(ctypes.Structure):
+    _fields_ = [("kind", ctypes.c_int32), ("pred_out", ctypes.c_int32), ("T", ctypes.c_int32),
+                ("reserved", ctypes.c_int32), ("beta_start", ctypes.c_double), ("beta_end", ctypes.c_double)]
+
+
+@dataclass(frozen=True)
+class Sampler:
+    """gc_sampler: kind GC_DDIM (linear betas over T steps) or GC_FLOW_EULER."""
+    kind: int = GC_DDIM
+    pred_out: int = GC_PRED_NONE
+    T: int = 1000
+    beta_start: float = 1e-4
+    beta_end: float = 0.02
+
+    def c(self) -> _Sampler:
+        return _Sampler(self.kind, self.pred_out, self.T, 0, self.beta_start, self.beta_end)
+
+
+_LIB = None
+_vp = ctypes.c_void_p
+_i32p = ctypes.POINTER(ctypes.c_int32)
+_i = ctypes.c_int
+_i64 = ctypes.c_int64
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded libgeocache.so (raises if it has not been built)."""
+    global _LIB
+    if _LIB is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} is missing: build it (python -c 'import __graft_entry__ as g; g.build()' "
+                              "or make -C paper_2608_13255_amd)")
+        L = ctypes.CDLL(LIB_PATH)
+        sig = {
+            "gc_abi_version": ([], _i),
+            "gc_last_error": ([], ctypes.c_char_p),
+            "gc_posmap_downsample": ([_vp, _i64, _i, _i, _i, _vp, _vp], _i),
+            "gc_posmap_bbox": ([_vp, _i, _i, _i, _i, ctypes.c_float, _vp, _vp], _i),
+            "gc_build_correspondence": ([_vp, _vp, _i, _i, _i, _i, _i32p, _i, _i, _vp, _vp, _vp, _vp, _vp], _i),
+            "gc_transport_step": ([_vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i32p, _i, _i, _i, _vp, _vp], _i),
+            "gc_sampler_reconstruct": ([_vp, _vp, _vp, _vp, _i64, _i, ctypes.POINTER(_Sampler), ctypes.c_double,
+                                        ctypes.c_double, _vp], _i),
+            "gc_transport_reconstruct": ([_vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i32p, _i, _i, _i,
+                                          ctypes.POINTER(_Sampler), ctypes.c_double, ctypes.c_double, _vp, _vp,
+                                          _vp, _vp], _i),
+            "gc_schedule_anchors": ([_i, _i, _i64, _i32p], _i),
+            "gc_schedule_full_steps": ([_i, _i, _i, ctypes.POINTER(ctypes.c_uint8)], _i),
+            "gc_sampler_step_times": ([ctypes.POINTER(_Sampler), _i, _i, ctypes.POINTER(ctypes.c_double),
+                                       ctypes.POINTER(ctypes.c_double)], _i),
+            "gc_sampler_alpha_bar": ([ctypes.POINTER(_Sampler), _i, ctypes.POINTER(ctypes.c_double)], _i),
+        }
+        for name, (args, res) in sig.items():
+            f = getattr(L, name)
+            f.argtypes = args
+            f.restype = res
+        if L.gc_abi_version() != 1:
+            raise ImportError(f"libgeocache ABI {L.gc_abi_version()} != 1")
+        _LIB = L
+    return _LIB
+
+
+def _check(rc: int, func: str) -> None:
+    if rc != GC_OK:
+        raise GeoCacheError(func, rc, lib().gc_last_error().decode(errors="replace"))
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, torch.cuda.Stream):
+        return stream.cuda_stream
+    return int(stream)
+
+
+def _dev(t: torch.Tensor, name: str) -> int:
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name} must be a device tensor (got {t.device})")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return t.data_ptr()
+
+
+def _opt(t: Optional[torch.Tensor], name: str) -> Optional[int]:
+    return None if t is None else _dev(t, name)
+
+
+def dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.float32:
+        return GC_F32
+    if t.dtype == torch.bfloat16:
+        return GC_BF16
+    raise ValueError(f"latents must be float32 or bfloat16 (got {t.dtype})")
+
+
+def _anchors(anchors: Sequence[int]):
+    arr = (ctypes.c_int32 * len(anchors))(*[int(x) for x in anchors])
+    return arr, len(anchors)
+
+
+def camera_tensor(cams: Dict[str, np.ndarray], device="cuda") -> torch.Tensor:
+    """Pack camera arrays (keys model, R, t, fx, fy, cx, cy with a common
+    leading shape, e.g. [B][N]) into a device uint8 tensor of gc_camera."""
+    lead = np.shape(cams["model"])
+    rec = np.zeros(lead, CAMERA_DTYPE)
+    rec["model"] = cams["model"]
+    rec["R"] = np.reshape(cams["R"], lead + (9,))
+    rec["t"] = cams["t"]
+    for k in ("fx", "fy", "cx", "cy"):
+        rec[k] = cams[k]
+    raw = np.ascontiguousarray(rec).view(np.uint8).reshape(lead + (68,))
+    return torch.from_numpy(raw.copy()).to(device)
+
+
+# ---------------------------------------------------------------------------
+# entry points
+# ---------------------------------------------------------------------------
+
+def gc_posmap_downsample(pos_hi: torch.Tensor, f: int, pos_lat: torch.Tensor = None, stream=None) -> torch.Tensor:
+    """pos_hi float32 [..., Hr, Wr, 3] -> pos_lat float32 [..., Hr/f, Wr/f, 3]."""
+    if pos_hi.dtype != torch.float32 or pos_hi.dim() < 3 or pos_hi.shape[-1] != 3:
+        raise ValueError("pos_hi must be float32 [..., Hr, Wr, 3]")
+    Hr, Wr = pos_hi.shape[-3], pos_hi.shape[-2]
+    lead = tuple(pos_hi.shape[:-3])
+    n = int(np.prod(lead)) if lead else 1
+    if pos_lat is None:
+        pos_lat = torch.empty(lead + (Hr // f, Wr // f, 3), dtype=torch.float32, device=pos_hi.device)
+    _check(lib().gc_posmap_downsample(_dev(pos_hi, "pos_hi"), n, Hr, Wr, f, _dev(pos_lat, "pos_lat"),
+                                      _stream(stream)), "gc_posmap_downsample")
+    return pos_lat
+
+
+def gc_posmap_bbox(pos: torch.Tensor, tol_frac: float = 0.01, bbox: torch.Tensor = None, stream=None) -> torch.Tensor:
+    """pos float32 [B, N, H, W, 3] -> bbox float32 [B, 8]."""
+    if pos.dtype != torch.float32 or pos.dim() != 5 or pos.shape[-1] != 3:
+        raise ValueError("pos must be float32 [B, N, H, W, 3]")
+    B, N, H, W, _ = pos.shape
+    if bbox is None:
+        bbox = torch.empty((B, 8), dtype=torch.float32, device=pos.device)
+    _check(lib().gc_posmap_bbox(_dev(pos, "pos"), B, N, H, W, float(tol_frac), _dev(bbox, "bbox"),
+                                _stream(stream)), "gc_posmap_bbox")
+    return bbox
+
+
+def gc_build_correspondence(pos: torch.Tensor, cams: torch.Tensor, anchors: Sequence[int], K: int,
+                            bbox: torch.Tensor, corr: torch.Tensor = None, weights: torch.Tensor = None,
+                            stats: torch.Tensor = None, stream=None) -> Tuple[torch.Tensor, torch.Tensor]:
+    """pos float32 [B, N, H, W, 3], cams uint8 [B, N, 68] (camera_tensor),
+    bbox float32 [B, 8] -> (corr int32 [B, N-a, H, W, a], weights float32
+    [B, N-a, H, W, a, K]); stats (optional) int32/uint32 [B, 4]."""
+    if pos.dtype != torch.float32 or pos.dim() != 5 or pos.shape[-1] != 3:
+        raise ValueError("pos must be float32 [B, N, H, W, 3]")
+    B, N, H, W, _ = pos.shape
+    if cams.dtype != torch.uint8 or tuple(cams.shape) != (B, N, 68):
+        raise ValueError(f"cams must be uint8 [B={B}, N={N}, 68]")
+    arr, a = _anchors(anchors)
+    NT = N - a
+    dev = pos.device
+    if corr is None:
+        corr = torch.empty((B, NT, H, W, a), dtype=torch.int32, device=dev)
+    if weights is None:
+        weights = torch.empty((B, NT, H, W, a, K), dtype=torch.float32, device=dev)
+    if tuple(corr.shape) != (B, NT, H, W, a) or corr.dtype != torch.int32:
+        raise ValueError("corr must be int32 [B, N-a, H, W, a]")
+    if tuple(weights.shape) != (B, NT, H, W, a, K) or weights.dtype != torch.float32:
+        raise ValueError("weights must be float32 [B, N-a, H, W, a, K]")
+    if stats is not None and (tuple(stats.shape) != (B, 4) or stats.element_size() != 4):
+        raise ValueError("stats must be a 32-bit [B, 4] tensor")
+    _check(lib().gc_build_correspondence(_dev(pos, "pos"), _dev(cams, "cams"), B, N, H, W, arr, a, K,
+                                         _dev(bbox, "bbox"), _dev(corr, "corr") if corr.numel() else None,
+                                         _dev(weights, "weights") if weights.numel() else None,
+                                         _opt(stats, "stats"), _stream(stream)), "gc_build_correspondence")
+    return corr, weights
+
+
+def _latent_shape(x0_prev: torch.Tensor):
+    if x0_prev.dim() != 5:
+        raise ValueError("latents must be [B, N, H, W, C]")
+    return tuple(x0_prev.shape)
+
+
+def gc_transport_step(x0_prev: torch.Tensor, x0_anchor_new: torch.Tensor, corr: torch.Tensor,
+                      weights: torch.Tensor, anchors: Sequence[int], x0_out: torch.Tensor = None,
+                      stream=None) -> torch.Tensor:
+    """Eq. 1 over one cached step; returns x0_out [B, N, H, W, C]."""
+    B, N, H, W, C = _latent_shape(x0_prev)
+    arr, a = _anchors(anchors)
+    if tuple(x0_anchor_new.shape) != (B, a, H, W, C) or x0_anchor_new.dtype != x0_prev.dtype:
+        raise ValueError(f"x0_anchor_new must be [B, a={a}, H, W, C] of the same dtype as x0_prev")
+    K = weights.shape[-1]
+    if x0_out is None:
+        x0_out = torch.empty_like(x0_prev)
+    _check(lib().gc_transport_step(_dev(x0_prev, "x0_prev"), _dev(x0_anchor_new, "x0_anchor_new"),
+                                   _dev(corr, "corr") if corr.numel() else None,
+                                   _dev(weights, "weights") if weights.numel() else None,
+                                   B, N, H, W, C, arr, a, K, dtype_code(x0_prev), _dev(x0_out, "x0_out"),
+                                   _stream(stream)), "gc_transport_step")
+    return x0_out
+
+
+def gc_sampler_reconstruct(x_t: torch.Tensor, x0: torch.Tensor, sampler: Sampler, t: float, t_next: float,
+                           x_next: torch.Tensor = None, model_out: torch.Tensor = None, stream=None):
+    """Elementwise sampler step from x0; returns (x_next, model_out or None)."""
+    if x0.shape != x_t.shape or x0.dtype != x_t.dtype:
+        raise ValueError("x_t and x0 must have the same shape and dtype")
+    if x_next is None:
+        x_next = torch.empty_like(x_t)
+    if sampler.pred_out != GC_PRED_NONE and model_out is None:
+        model_out = torch.empty_like(x_t)
+    smp = sampler.c()
+    _check(lib().gc_sampler_reconstruct(_dev(x_t, "x_t"), _dev(x0, "x0"), _dev(x_next, "x_next"),
+                                        _opt(model_out, "model_out"), x_t.numel(), dtype_code(x_t),
+                                        ctypes.byref(smp), float(t), float(t_next), _stream(stream)),
+           "gc_sampler_reconstruct")
+    return x_next, model_out
+
+
+def gc_transport_reconstruct(x0_prev: torch.Tensor, x0_anchor_new: torch.Tensor, corr: torch.Tensor,
+                             weights: torch.Tensor, x_t: torch.Tensor, anchors: Sequence[int], sampler: Sampler,
+                             t: float, t_next: float, x0_out: torch.Tensor = None, x_next: torch.Tensor = None,
+                             model_out: torch.Tensor = None, stream=None):
+    """Fused Eq. 1 + reconstruction; returns (x0_out, x_next, model_out or None)."""
+    B, N, H, W, C = _latent_shape(x0_prev)
+    arr, a = _anchors(anchors)
+    if tuple(x0_anchor_new.shape) != (B, a, H, W, C) or x0_anchor_new.dtype != x0_prev.dtype:
+        raise ValueError(f"x0_anchor_new must be [B, a={a}, H, W, C] of the same dtype as x0_prev")
+    if x_t.shape != x0_prev.shape or x_t.dtype != x0_prev.dtype:
+        raise ValueError("x_t must match x0_prev in shape and dtype")
+    K = weights.shape[-1]
+    if x0_out is None:
+        x0_out = torch.empty_like(x0_prev)
+    if x_next is None:
+        x_next = torch.empty_like(x_t)
+    if sampler.pred_out != GC_PRED_NONE and model_out is None:
+        model_out = torch.empty_like(x_t)
+    smp = sampler.c()
+    _check(lib().gc_transport_reconstruct(_dev(x0_prev, "x0_prev"), _dev(x0_anchor_new, "x0_anchor_new"),
+                                          _dev(corr, "corr") if corr.numel() else None,
+                                          _dev(weights, "weights") if weights.numel() else None,
+                                          _dev(x_t, "x_t"), B, N, H, W, C, arr, a, K, dtype_code(x0_prev),
+                                          ctypes.byref(smp), float(t), float(t_next), _dev(x0_out, "x0_out"),
+                                          _dev(x_next, "x_next"), _opt(model_out, "model_out"), _stream(stream)),
+           "gc_transport_reconstruct")
+    return x0_out, x_next, model_out
+
+
+def gc_schedule_anchors(N: int, a: int, c: int) -> List[int]:
+    out = (ctypes.c_int32 * a)()
+    _check(lib().gc_schedule_anchors(N, a, c, out), "gc_schedule_anchors")
+    return list(out)
+
+
+def gc_schedule_full_steps(rule: int, S: int, E: int = 0) -> List[int]:
+    out = (ctypes.c_uint8 * S)()
+    _check(lib().gc_schedule_full_steps(rule, S, E, out), "gc_schedule_full_steps")
+    return list(out)
+
+
+def gc_sampler_step_times(sampler: Sampler, S: int, k: int) -> Tuple[float, float]:
+    t, tn = ctypes.c_double(), ctypes.c_double()
+    smp = sampler.c()
+    _check(lib().gc_sampler_step_times(ctypes.byref(smp), S, k, ctypes.byref(t), ctypes.byref(tn)),
+           "gc_sampler_step_times")
+    return t.value, tn.value
+
+
+def gc_sampler_alpha_bar(sampler: Sampler, t: int) -> float:
+    out = ctypes.c_double()
+    smp = sampler.c()
+    _check(lib().gc_sampler_alpha_bar(ctypes.byref(smp), int(t), ctypes.byref(out)), "gc_sampler_alpha_bar")
+    return out.value
+
+
+lib()

@@ -1,0 +1,58 @@
+// Internal helpers shared by the library's translation units.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <cstring>
+
+#include "geocache.h"
+
+namespace gc {
+
+// ---------------------------------------------------------------------------
+// error reporting (host)
+// ---------------------------------------------------------------------------
+int fail(int code, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+void clear_error();
+// Map the launch status (hipGetLastError) and, with GC_SYNC_CHECK=1, the
+// stream's completion status to GC_OK / GC_ERR_HIP.
+int after_launch(hipStream_t stream, const char* what);
+
+inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+inline bool overlaps(const void* a, size_t na, const void* b, size_t nb) {
+  const uintptr_t a0 = reinterpret_cast<uintptr_t>(a), b0 = reinterpret_cast<uintptr_t>(b);
+  return na && nb && a0 < b0 + nb && b0 < a0 + na;
+}
+
+inline int dtype_bytes(int dtype) { return dtype == GC_F32 ? 4 : (dtype == GC_BF16 ? 2 : 0); }
+
+// Sampler coefficients, computed on the host in double and rounded once.
+struct Recon {
+  int32_t kind;     // GC_DDIM / GC_FLOW_EULER
+  int32_t pred;     // GC_PRED_*
+  float a_t, s_t, inv_s_t, a_n, s_n;   // DDIM: sqrt(abar), sqrt(1-abar), 1/sqrt(1-abar)
+  float inv_sigma, dsigma;             // flow: 1/sigma_t, sigma_n - sigma_t
+};
+
+// Validate a sampler description and step and fill the coefficients.
+int make_recon(const gc_sampler* smp, double t, double t_next, Recon* out);
+
+// ---------------------------------------------------------------------------
+// device helpers
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ bool finite_f(float x) {
+  return (__float_as_uint(x) & 0x7f800000u) != 0x7f800000u;
+}
+
+__device__ __forceinline__ float bf16_bits_to_f(uint32_t h) { return __uint_as_float(h << 16); }
+
+// float -> bfloat16 bits, round to nearest even; NaN -> canonical quiet NaN.
+__device__ __forceinline__ uint32_t f_to_bf16_bits(float f) {
+  const uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return 0x7fc0u;
+  return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
+}
+
+}  // namespace gc

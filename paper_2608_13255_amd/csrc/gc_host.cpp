@@ -1,0 +1,175 @@
+// Host-side parts of the library: error state, launch checking, the host
+// schedule (anchor rotation, full-view steps, sampler step times) and the
+// sampler coefficients.  No device memory is touched here.
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstdlib>
+
+#include "gc_common.h"
+
+namespace gc {
+
+namespace {
+thread_local char g_err[512] = "";
+
+bool sync_check_enabled() {
+  static const bool on = [] {
+    const char* e = std::getenv("GC_SYNC_CHECK");
+    return e && e[0] && e[0] != '0';
+  }();
+  return on;
+}
+}  // namespace
+
+int fail(int code, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  std::vsnprintf(g_err, sizeof(g_err), fmt, ap);
+  va_end(ap);
+  return code;
+}
+
+void clear_error() { g_err[0] = '\0'; }
+
+int after_launch(hipStream_t stream, const char* what) {
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return fail(GC_ERR_HIP, "%s: launch failed: %s", what, hipGetErrorString(e));
+  if (sync_check_enabled()) {
+    e = hipStreamSynchronize(stream);
+    if (e != hipSuccess) return fail(GC_ERR_HIP, "%s: execution failed: %s", what, hipGetErrorString(e));
+  }
+  return GC_OK;
+}
+
+// abar_t = prod_{i<=t} (1 - beta_i), beta_i = beta_start + (beta_end - beta_start) i / (T - 1)
+static double alpha_bar(const gc_sampler* smp, int t) {
+  if (t < 0) return 1.0;
+  double ab = 1.0;
+  for (int i = 0; i <= t; ++i) {
+    const double beta = smp->beta_start + (smp->beta_end - smp->beta_start) * (double)i / (double)(smp->T - 1);
+    ab *= 1.0 - beta;
+  }
+  return ab;
+}
+
+static int check_sampler(const gc_sampler* smp) {
+  if (!smp) return fail(GC_ERR_ARG, "sampler is null");
+  if (smp->kind == GC_DDIM) {
+    if (smp->T < 2 || smp->T > 100000) return fail(GC_ERR_ARG, "DDIM T=%d out of range [2, 100000]", smp->T);
+    if (!(smp->beta_start > 0.0 && smp->beta_end < 1.0 && smp->beta_start <= smp->beta_end))
+      return fail(GC_ERR_ARG, "DDIM betas must satisfy 0 < beta_start <= beta_end < 1");
+    if (smp->pred_out != GC_PRED_NONE && smp->pred_out != GC_PRED_EPS && smp->pred_out != GC_PRED_V)
+      return fail(GC_ERR_ARG, "DDIM pred_out %d is not NONE, EPS or V", smp->pred_out);
+  } else if (smp->kind == GC_FLOW_EULER) {
+    if (smp->pred_out != GC_PRED_NONE && smp->pred_out != GC_PRED_VEL)
+      return fail(GC_ERR_ARG, "flow pred_out %d is not NONE or VEL", smp->pred_out);
+  } else {
+    return fail(GC_ERR_ARG, "unknown sampler kind %d", smp->kind);
+  }
+  return GC_OK;
+}
+
+int make_recon(const gc_sampler* smp, double t, double t_next, Recon* r) {
+  int rc = check_sampler(smp);
+  if (rc) return rc;
+  std::memset(r, 0, sizeof(*r));
+  r->kind = smp->kind;
+  r->pred = smp->pred_out;
+  if (smp->kind == GC_DDIM) {
+    if (t != std::floor(t) || t_next != std::floor(t_next))
+      return fail(GC_ERR_ARG, "DDIM timesteps must be integers (t=%g, t_next=%g)", t, t_next);
+    if (t < 0 || t >= smp->T || t_next >= t || t_next < -1)
+      return fail(GC_ERR_ARG, "DDIM step %g -> %g outside 0 <= t < T, -1 <= t_next < t", t, t_next);
+    const double ab_t = alpha_bar(smp, (int)t), ab_n = alpha_bar(smp, (int)t_next);
+    const double s_t = std::sqrt(1.0 - ab_t);
+    r->a_t = (float)std::sqrt(ab_t);
+    r->s_t = (float)s_t;
+    r->inv_s_t = (float)(1.0 / s_t);
+    r->a_n = (float)std::sqrt(ab_n);
+    r->s_n = (float)std::sqrt(1.0 - ab_n);
+  } else {
+    if (!(t > 0.0 && t <= 1.0) || !(t_next >= 0.0 && t_next <= t))
+      return fail(GC_ERR_ARG, "flow step sigma %g -> %g outside 0 < sigma_t <= 1, 0 <= sigma_n <= sigma_t", t,
+                  t_next);
+    r->inv_sigma = (float)(1.0 / t);
+    r->dsigma = (float)(t_next - t);
+  }
+  return GC_OK;
+}
+
+}  // namespace gc
+
+using namespace gc;
+
+extern "C" {
+
+int gc_abi_version(void) { return GC_ABI_VERSION; }
+
+const char* gc_last_error(void) { return g_err; }
+
+int gc_schedule_anchors(int N, int a, int64_t c, int32_t* anchors_out) {
+  clear_error();
+  if (!anchors_out) return fail(GC_ERR_ARG, "anchors_out is null");
+  if (N < 1 || N > GC_MAX_VIEWS) return fail(GC_ERR_CAPACITY, "N=%d outside [1, %d]", N, GC_MAX_VIEWS);
+  if (a < 1 || a > N) return fail(GC_ERR_ARG, "a=%d outside [1, N=%d]", a, N);
+  if (c < 0) return fail(GC_ERR_ARG, "cached-step counter %lld is negative", (long long)c);
+  // rotate the evenly spread set {floor(j*N/a)} by c, then order by view
+  bool member[GC_MAX_VIEWS] = {};
+  for (int j = 0; j < a; ++j) member[(int)((c + (int64_t)j * N / a) % N)] = true;
+  int n = 0;
+  for (int v = 0; v < N; ++v)
+    if (member[v]) anchors_out[n++] = v;
+  return GC_OK;
+}
+
+int gc_schedule_full_steps(int rule, int S, int E, uint8_t* is_full_out) {
+  clear_error();
+  if (!is_full_out) return fail(GC_ERR_ARG, "is_full_out is null");
+  if (S < 1) return fail(GC_ERR_ARG, "S=%d must be positive", S);
+  std::memset(is_full_out, 0, (size_t)S);
+  if (rule == GC_FULL_PERIODIC) {
+    if (E < 1) return fail(GC_ERR_ARG, "periodic full steps need E >= 1 (got %d)", E);
+    for (int k = 0; k < S; k += E) is_full_out[k] = 1;
+  } else if (rule == GC_FULL_HEAD_MID_TAIL) {
+    is_full_out[0] = 1;
+    if (S > 1) is_full_out[1] = 1;
+    is_full_out[S / 2] = 1;
+    is_full_out[S - 1] = 1;
+  } else {
+    return fail(GC_ERR_ARG, "unknown full-step rule %d", rule);
+  }
+  is_full_out[0] = 1;
+  return GC_OK;
+}
+
+int gc_sampler_step_times(const gc_sampler* smp, int S, int k, double* t, double* t_next) {
+  clear_error();
+  int rc = check_sampler(smp);
+  if (rc) return rc;
+  if (!t || !t_next) return fail(GC_ERR_ARG, "output pointer is null");
+  if (S < 1 || k < 0 || k >= S) return fail(GC_ERR_ARG, "step %d outside [0, S=%d)", k, S);
+  if (smp->kind == GC_DDIM) {
+    if (S > smp->T) return fail(GC_ERR_ARG, "S=%d exceeds T=%d", S, smp->T);
+    auto ts = [&](int j) { return j >= S ? -1.0 : std::floor((double)(S - j) * smp->T / S + 0.5) - 1.0; };
+    *t = ts(k);
+    *t_next = ts(k + 1);
+  } else {
+    *t = 1.0 - (double)k / S;
+    *t_next = 1.0 - (double)(k + 1) / S;
+  }
+  return GC_OK;
+}
+
+int gc_sampler_alpha_bar(const gc_sampler* smp, int t, double* abar) {
+  clear_error();
+  if (!smp || !abar) return fail(GC_ERR_ARG, "null argument");
+  if (smp->kind != GC_DDIM) return fail(GC_ERR_ARG, "alpha_bar needs a DDIM sampler");
+  int rc = check_sampler(smp);
+  if (rc) return rc;
+  if (t < -1 || t >= smp->T) return fail(GC_ERR_ARG, "t=%d outside [-1, T)", t);
+  *abar = alpha_bar(smp, t);
+  return GC_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,379 @@
+// Per-step kernels: delta transport (Eq. 1), sampler-consistent
+// reconstruction, and the two fused into one pass.
+//
+// All three are HBM-streaming: each latent element is read and written once;
+// the only reuse is the gather of anchor taps, which neighbouring target
+// tokens share and which stays in L2.  No MFMA: nothing here is a dense
+// contraction.
+//
+// Work mapping: one thread per (asset, view, pixel, channel vector); a
+// channel vector is 16 bytes (4 floats or 8 bfloat16; 4 bfloat16 when C is
+// not a multiple of 8), so every latent access is one 16-byte (or 8-byte)
+// load/store, consecutive lanes touch consecutive addresses, and the threads
+// of one pixel share its correspondence words and weights through L1.
+// Blocks are remapped so that each of the 8 XCDs processes one contiguous
+// slice of the (asset, view, pixel) space: an XCD then gathers from only its
+// own assets' anchor views, which fit its L2.
+#include "gc_common.h"
+
+namespace gc {
+namespace {
+
+constexpr int kBlock = 256;
+constexpr int kXcds = 8;
+
+template <int BYTES> struct RawT;
+template <> struct RawT<16> { using type = uint4; };
+template <> struct RawT<8> { using type = uint2; };
+
+// Storage codec for VEC elements of dtype DT packed in one raw vector.
+template <int DT, int VEC> struct Codec {
+  static constexpr int kBytes = VEC * (DT == GC_F32 ? 4 : 2);
+  using Raw = typename RawT<kBytes>::type;
+
+  __device__ __forceinline__ static Raw load(const void* base, int64_t elem) {
+    return *reinterpret_cast<const Raw*>(static_cast<const char*>(base) + elem * (DT == GC_F32 ? 4 : 2));
+  }
+  __device__ __forceinline__ static void store(void* base, int64_t elem, const Raw& r) {
+    *reinterpret_cast<Raw*>(static_cast<char*>(base) + elem * (DT == GC_F32 ? 4 : 2)) = r;
+  }
+  __device__ __forceinline__ static void unpack(const Raw& r, float (&f)[VEC]) {
+    const uint32_t* w = reinterpret_cast<const uint32_t*>(&r);
+    if constexpr (DT == GC_F32) {
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) f[e] = __uint_as_float(w[e]);
+    } else {
+#pragma unroll
+      for (int e = 0; e < VEC / 2; ++e) {
+        f[2 * e] = bf16_bits_to_f(w[e] & 0xffffu);
+        f[2 * e + 1] = bf16_bits_to_f(w[e] >> 16);
+      }
+    }
+  }
+  __device__ __forceinline__ static Raw pack(const float (&f)[VEC]) {
+    Raw r;
+    uint32_t* w = reinterpret_cast<uint32_t*>(&r);
+    if constexpr (DT == GC_F32) {
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) w[e] = __float_as_uint(f[e]);
+    } else {
+#pragma unroll
+      for (int e = 0; e < VEC / 2; ++e) w[e] = f_to_bf16_bits(f[2 * e]) | (f_to_bf16_bits(f[2 * e + 1]) << 16);
+    }
+    return r;
+  }
+};
+
+struct TArgs {
+  const void* x0_prev;
+  const void* x0_new;
+  const int32_t* corr;
+  const float* weights;
+  const void* x_t;
+  void* x0_out;
+  void* x_next;
+  void* model_out;
+  int64_t n_threads;   // B * N * H * W * (C / VEC)
+  int N, H, W, HW, C, a, K, NT, CV;
+  int n_blocks;        // logical blocks (before XCD padding)
+  int remap;           // 1: XCD-contiguous block order
+  int8_t slot_of_view[GC_MAX_VIEWS];    // anchor slot of view v, or -1
+  int8_t tslot_of_view[GC_MAX_VIEWS];   // target slot of view v, or -1
+  int32_t anchor_view[GC_MAX_ANCHORS];
+  Recon r;
+};
+
+__device__ __forceinline__ int logical_block(int n_blocks, int remap) {
+  const int i = blockIdx.x;
+  if (!remap) return i;
+  const int per = (n_blocks + kXcds - 1) / kXcds;   // grid is padded to kXcds * per
+  return (i % kXcds) * per + i / kXcds;
+}
+
+template <int VEC>
+__device__ __forceinline__ void reconstruct_vec(const Recon& r, const float (&xt)[VEC], const float (&x0)[VEC],
+                                                float (&xn)[VEC], float (&mo)[VEC]) {
+  if (r.kind == GC_DDIM) {
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) {
+      const float eps = (xt[e] - r.a_t * x0[e]) * r.inv_s_t;
+      xn[e] = r.a_n * x0[e] + r.s_n * eps;
+      mo[e] = r.pred == GC_PRED_V ? r.a_t * eps - r.s_t * x0[e] : eps;
+    }
+  } else {
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) {
+      const float vel = (xt[e] - x0[e]) * r.inv_sigma;
+      xn[e] = xt[e] + r.dsigma * vel;
+      mo[e] = vel;
+    }
+  }
+}
+
+template <int DT, int VEC, bool FUSED>
+__global__ __launch_bounds__(kBlock) void k_transport(TArgs g) {
+  using CD = Codec<DT, VEC>;
+  using Raw = typename CD::Raw;
+  const int lb = logical_block(g.n_blocks, g.remap);
+  if (lb >= g.n_blocks) return;
+  const int64_t gid = (int64_t)lb * kBlock + threadIdx.x;
+  if (gid >= g.n_threads) return;
+  const int cv = (int)(gid % g.CV);
+  const int64_t pix = gid / g.CV;              // (b * N + v) * HW + p
+  const int p = (int)(pix % g.HW);
+  const int64_t bv = pix / g.HW;
+  const int v = (int)(bv % g.N);
+  const int b = (int)(bv / g.N);
+  const int64_t base = pix * g.C + (int64_t)cv * VEC;
+  const int s_self = g.slot_of_view[v];
+
+  Raw x0r;
+  float x0f[VEC];
+  if (s_self >= 0) {
+    // anchor row: the store keeps this step's prediction
+    x0r = CD::load(g.x0_new, (((int64_t)b * g.a + s_self) * g.HW + p) * g.C + (int64_t)cv * VEC);
+    CD::unpack(x0r, x0f);
+  } else {
+    const int ti = g.tslot_of_view[v];
+    const int64_t crow = ((int64_t)b * g.NT + ti) * g.HW + p;
+    const int32_t* cw = g.corr + crow * g.a;
+    int32_t words[GC_MAX_ANCHORS];
+    bool any = false;
+#pragma unroll
+    for (int s = 0; s < GC_MAX_ANCHORS; ++s) {
+      words[s] = s < g.a ? cw[s] : 0;
+      any |= words[s] != 0;
+    }
+    const Raw prevr = CD::load(g.x0_prev, base);
+    if (!any) {
+      x0r = prevr;   // no anchor sees this token: it keeps its own state
+      CD::unpack(x0r, x0f);
+    } else {
+      float prevf[VEC], acc[VEC];
+      CD::unpack(prevr, prevf);
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) acc[e] = 0.0f;
+      const float* wr = g.weights + crow * g.a * g.K;
+#pragma unroll
+      for (int s = 0; s < GC_MAX_ANCHORS; ++s) {
+        const uint32_t w = (uint32_t)words[s];
+        if (!w) continue;
+        const int x0 = (int)(w & 0xfffu) - 1;
+        const int y0 = (int)((w >> 12) & 0xfffu) - 1;
+        const uint32_t mask = (w >> 24) & 0xfu;
+        const int64_t new_view = ((int64_t)b * g.a + s) * g.HW;
+        const int64_t old_view = ((int64_t)b * g.N + g.anchor_view[s]) * g.HW;
+        const float* ws = wr + s * g.K;
+        int j = 0;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          if (!(mask & (1u << k))) continue;
+          // words come from the caller: taps off the grid or beyond K are ignored
+          const int x = x0 + (k & 1), y = y0 + (k >> 1);
+          if (j >= g.K || x < 0 || x >= g.W || y < 0 || y >= g.H) continue;
+          const int q = y * g.W + x;
+          const float wt = ws[j++];
+          float nf[VEC], of[VEC];
+          CD::unpack(CD::load(g.x0_new, (new_view + q) * g.C + (int64_t)cv * VEC), nf);
+          CD::unpack(CD::load(g.x0_prev, (old_view + q) * g.C + (int64_t)cv * VEC), of);
+#pragma unroll
+          for (int e = 0; e < VEC; ++e) acc[e] = acc[e] + wt * (nf[e] - of[e]);
+        }
+      }
+      float y[VEC];
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) y[e] = prevf[e] + acc[e];
+      x0r = CD::pack(y);
+      CD::unpack(x0r, x0f);   // the reconstruction reads x0 as stored
+    }
+  }
+  CD::store(g.x0_out, base, x0r);
+  if constexpr (FUSED) {
+    float xtf[VEC], xn[VEC], mo[VEC];
+    CD::unpack(CD::load(g.x_t, base), xtf);
+    reconstruct_vec<VEC>(g.r, xtf, x0f, xn, mo);
+    CD::store(g.x_next, base, CD::pack(xn));
+    if (g.model_out) CD::store(g.model_out, base, CD::pack(mo));
+  }
+}
+
+template <int DT, int VEC>
+__global__ __launch_bounds__(kBlock) void k_reconstruct(const void* __restrict__ x_t, const void* __restrict__ x0,
+                                                        void* x_next, void* __restrict__ model_out, int64_t n_vec,
+                                                        Recon r) {
+  using CD = Codec<DT, VEC>;
+  const int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+  if (i >= n_vec) return;
+  float xtf[VEC], x0f[VEC], xn[VEC], mo[VEC];
+  CD::unpack(CD::load(x_t, i * VEC), xtf);
+  CD::unpack(CD::load(x0, i * VEC), x0f);
+  reconstruct_vec<VEC>(r, xtf, x0f, xn, mo);
+  CD::store(x_next, i * VEC, CD::pack(xn));
+  if (model_out) CD::store(model_out, i * VEC, CD::pack(mo));
+}
+
+int pick_vec(int dtype, int64_t c) { return dtype == GC_F32 ? 4 : (c % 8 == 0 ? 8 : 4); }
+
+// Validation shared by the transport entry points; fills g (except the
+// reconstruction coefficients and the fused-only pointers).
+int prepare_transport(const void* x0_prev, const void* x0_new, const int32_t* corr, const float* weights, int B,
+                      int N, int H, int W, int C, const int32_t* anchors, int a, int K, int dtype, void* x0_out,
+                      const char* who, TArgs* g) {
+  if (!x0_prev || !x0_new || !anchors || !x0_out) return fail(GC_ERR_ARG, "%s: null pointer", who);
+  if (dtype != GC_F32 && dtype != GC_BF16) return fail(GC_ERR_DTYPE, "%s: unknown dtype %d", who, dtype);
+  if (B < 1 || N < 1 || H < 1 || W < 1 || C < 1)
+    return fail(GC_ERR_SHAPE, "%s: bad shape B=%d N=%d H=%d W=%d C=%d", who, B, N, H, W, C);
+  if (C % 4) return fail(GC_ERR_SHAPE, "%s: C=%d is not a multiple of 4", who, C);
+  if (C > GC_MAX_CHANNELS) return fail(GC_ERR_CAPACITY, "%s: C=%d exceeds %d", who, C, GC_MAX_CHANNELS);
+  if (N > GC_MAX_VIEWS) return fail(GC_ERR_CAPACITY, "%s: N=%d exceeds %d", who, N, GC_MAX_VIEWS);
+  if (H > GC_MAX_GRID || W > GC_MAX_GRID) return fail(GC_ERR_CAPACITY, "%s: grid %dx%d exceeds %d", who, H, W, GC_MAX_GRID);
+  if (a < 1 || a > N) return fail(GC_ERR_ARG, "%s: a=%d outside [1, N=%d]", who, a, N);
+  if (a > GC_MAX_ANCHORS) return fail(GC_ERR_CAPACITY, "%s: a=%d exceeds %d", who, a, GC_MAX_ANCHORS);
+  if (K < 1 || K > 4) return fail(GC_ERR_ARG, "%s: K=%d outside [1, 4]", who, K);
+  const int NT = N - a;
+  if (NT > 0 && (!corr || !weights)) return fail(GC_ERR_ARG, "%s: null correspondence", who);
+  if (!aligned16(x0_prev) || !aligned16(x0_new) || !aligned16(x0_out) || (corr && !aligned16(corr)) ||
+      (weights && !aligned16(weights)))
+    return fail(GC_ERR_ALIGN, "%s: device pointers must be 16-byte aligned", who);
+  std::memset(g, 0, sizeof(*g));
+  for (int v = 0; v < GC_MAX_VIEWS; ++v) g->slot_of_view[v] = g->tslot_of_view[v] = -1;
+  for (int s = 0; s < a; ++s) {
+    const int u = anchors[s];
+    if (u < 0 || u >= N) return fail(GC_ERR_ARG, "%s: anchor %d outside [0, %d)", who, u, N);
+    if (g->slot_of_view[u] >= 0) return fail(GC_ERR_ARG, "%s: anchor %d listed twice", who, u);
+    g->slot_of_view[u] = (int8_t)s;
+    g->anchor_view[s] = u;
+  }
+  int t = 0;
+  for (int v = 0; v < N; ++v)
+    if (g->slot_of_view[v] < 0) g->tslot_of_view[v] = (int8_t)t++;
+  const size_t es = (size_t)dtype_bytes(dtype);
+  const size_t HW = (size_t)H * W;
+  const size_t n_all = (size_t)B * N * HW * C * es, n_new = (size_t)B * a * HW * C * es;
+  if (overlaps(x0_out, n_all, x0_prev, n_all) || overlaps(x0_out, n_all, x0_new, n_new))
+    return fail(GC_ERR_ALIAS, "%s: x0_out overlaps x0_prev or x0_anchor_new", who);
+  const int vec = pick_vec(dtype, C);
+  g->x0_prev = x0_prev;
+  g->x0_new = x0_new;
+  g->corr = corr;
+  g->weights = weights;
+  g->x0_out = x0_out;
+  g->N = N;
+  g->H = H;
+  g->HW = (int)HW;
+  g->W = W;
+  g->C = C;
+  g->a = a;
+  g->K = K;
+  g->NT = NT;
+  g->CV = C / vec;
+  g->n_threads = (int64_t)B * N * (int64_t)HW * g->CV;
+  const int64_t nb = (g->n_threads + kBlock - 1) / kBlock;
+  if (nb > (int64_t)0x7fffffff - kXcds) return fail(GC_ERR_CAPACITY, "%s: problem too large for one launch", who);
+  g->n_blocks = (int)nb;
+  g->remap = 1;
+  return GC_OK;
+}
+
+template <bool FUSED>
+void launch_transport(const TArgs& g, int dtype, hipStream_t stream) {
+  const int per = (g.n_blocks + kXcds - 1) / kXcds;
+  const dim3 grid(g.remap ? (unsigned)(per * kXcds) : (unsigned)g.n_blocks);
+  const int vec = g.C / g.CV;
+  if (dtype == GC_F32)
+    hipLaunchKernelGGL((k_transport<GC_F32, 4, FUSED>), grid, dim3(kBlock), 0, stream, g);
+  else if (vec == 8)
+    hipLaunchKernelGGL((k_transport<GC_BF16, 8, FUSED>), grid, dim3(kBlock), 0, stream, g);
+  else
+    hipLaunchKernelGGL((k_transport<GC_BF16, 4, FUSED>), grid, dim3(kBlock), 0, stream, g);
+}
+
+}  // namespace
+}  // namespace gc
+
+using namespace gc;
+
+extern "C" int gc_transport_step(const void* x0_prev, const void* x0_anchor_new, const int32_t* corr,
+                                 const float* weights, int B, int N, int H, int W, int C, const int32_t* anchors,
+                                 int a, int K, int dtype, void* x0_out, hipStream_t stream) {
+  clear_error();
+  TArgs g;
+  int rc = prepare_transport(x0_prev, x0_anchor_new, corr, weights, B, N, H, W, C, anchors, a, K, dtype, x0_out,
+                             "gc_transport_step", &g);
+  if (rc) return rc;
+  if (g.n_threads == 0) return GC_OK;
+  launch_transport<false>(g, dtype, stream);
+  return after_launch(stream, "gc_transport_step");
+}
+
+extern "C" int gc_sampler_reconstruct(const void* x_t, const void* x0, void* x_next, void* model_out,
+                                      int64_t n_elems, int dtype, const gc_sampler* smp, double t, double t_next,
+                                      hipStream_t stream) {
+  clear_error();
+  if (!x_t || !x0 || !x_next) return fail(GC_ERR_ARG, "gc_sampler_reconstruct: null pointer");
+  if (dtype != GC_F32 && dtype != GC_BF16) return fail(GC_ERR_DTYPE, "gc_sampler_reconstruct: unknown dtype %d", dtype);
+  if (n_elems < 0 || n_elems % 4) return fail(GC_ERR_SHAPE, "gc_sampler_reconstruct: n_elems=%lld must be a non-negative multiple of 4",
+                                              (long long)n_elems);
+  Recon r;
+  int rc = make_recon(smp, t, t_next, &r);
+  if (rc) return rc;
+  if ((r.pred != GC_PRED_NONE) != (model_out != nullptr))
+    return fail(GC_ERR_ARG, "gc_sampler_reconstruct: model_out must be given iff pred_out != GC_PRED_NONE");
+  if (!aligned16(x_t) || !aligned16(x0) || !aligned16(x_next) || (model_out && !aligned16(model_out)))
+    return fail(GC_ERR_ALIGN, "gc_sampler_reconstruct: device pointers must be 16-byte aligned");
+  const size_t nb = (size_t)n_elems * dtype_bytes(dtype);
+  if ((x_next != x_t && overlaps(x_next, nb, x_t, nb)) || overlaps(x_next, nb, x0, nb) ||
+      overlaps(model_out, nb, x_t, nb) || overlaps(model_out, nb, x0, nb) || overlaps(model_out, nb, x_next, nb))
+    return fail(GC_ERR_ALIAS, "gc_sampler_reconstruct: outputs overlap inputs (only x_next == x_t is allowed)");
+  if (n_elems == 0) return GC_OK;
+  const int vec = pick_vec(dtype, n_elems);
+  const int64_t n_vec = n_elems / vec;
+  const int64_t blocks = (n_vec + kBlock - 1) / kBlock;
+  if (blocks > 0x7fffffff) return fail(GC_ERR_CAPACITY, "gc_sampler_reconstruct: too many elements");
+  if (dtype == GC_F32)
+    hipLaunchKernelGGL((k_reconstruct<GC_F32, 4>), dim3((unsigned)blocks), dim3(kBlock), 0, stream, x_t, x0, x_next,
+                       model_out, n_vec, r);
+  else if (vec == 8)
+    hipLaunchKernelGGL((k_reconstruct<GC_BF16, 8>), dim3((unsigned)blocks), dim3(kBlock), 0, stream, x_t, x0, x_next,
+                       model_out, n_vec, r);
+  else
+    hipLaunchKernelGGL((k_reconstruct<GC_BF16, 4>), dim3((unsigned)blocks), dim3(kBlock), 0, stream, x_t, x0, x_next,
+                       model_out, n_vec, r);
+  return after_launch(stream, "gc_sampler_reconstruct");
+}
+
+extern "C" int gc_transport_reconstruct(const void* x0_prev, const void* x0_anchor_new, const int32_t* corr,
+                                        const float* weights, const void* x_t, int B, int N, int H, int W, int C,
+                                        const int32_t* anchors, int a, int K, int dtype, const gc_sampler* smp,
+                                        double t, double t_next, void* x0_out, void* x_next, void* model_out,
+                                        hipStream_t stream) {
+  clear_error();
+  TArgs g;
+  int rc = prepare_transport(x0_prev, x0_anchor_new, corr, weights, B, N, H, W, C, anchors, a, K, dtype, x0_out,
+                             "gc_transport_reconstruct", &g);
+  if (rc) return rc;
+  if (!x_t || !x_next) return fail(GC_ERR_ARG, "gc_transport_reconstruct: null x_t or x_next");
+  rc = make_recon(smp, t, t_next, &g.r);
+  if (rc) return rc;
+  if ((g.r.pred != GC_PRED_NONE) != (model_out != nullptr))
+    return fail(GC_ERR_ARG, "gc_transport_reconstruct: model_out must be given iff pred_out != GC_PRED_NONE");
+  if (!aligned16(x_t) || !aligned16(x_next) || (model_out && !aligned16(model_out)))
+    return fail(GC_ERR_ALIGN, "gc_transport_reconstruct: device pointers must be 16-byte aligned");
+  const size_t es = (size_t)dtype_bytes(dtype);
+  const size_t n_all = (size_t)B * N * H * W * C * es, n_new = (size_t)B * a * H * W * C * es;
+  const void* ins[3] = {x0_prev, x0_anchor_new, x0_out};
+  const size_t lens[3] = {n_all, n_new, n_all};
+  for (int i = 0; i < 3; ++i) {
+    if (overlaps(x_next, n_all, ins[i], lens[i]) || overlaps(model_out, n_all, ins[i], lens[i]))
+      return fail(GC_ERR_ALIAS, "gc_transport_reconstruct: x_next/model_out overlap x0_prev, x0_anchor_new or x0_out");
+  }
+  if (overlaps(x_t, n_all, x0_out, n_all) || (x_next != x_t && overlaps(x_next, n_all, x_t, n_all)) ||
+      overlaps(model_out, n_all, x_t, n_all) || overlaps(model_out, n_all, x_next, n_all))
+    return fail(GC_ERR_ALIAS, "gc_transport_reconstruct: outputs overlap x_t (only x_next == x_t is allowed)");
+  g.x_t = x_t;
+  g.x_next = x_next;
+  g.model_out = model_out;
+  if (g.n_threads == 0) return GC_OK;
+  launch_transport<true>(g, dtype, stream);
+  return after_launch(stream, "gc_transport_reconstruct");
+}

@@ -1,0 +1,170 @@
+"""C-ABI checks that need no GPU: the library loads, exports exactly what
+include/geocache.h declares, rejects bad arguments on the host before any
+launch, and its host schedule agrees with the oracle's."""
+import ctypes
+import math
+import os
+import re
+import shutil
+import subprocess
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "geocache.h")
+LIBSO = os.path.join(ROOT, "paper_2608_13255_amd", "libgeocache.so")
+
+# fake, never-dereferenced device addresses: every call below fails validation
+# before anything is launched
+A0, A1, A2, A3, A4, A5 = (0x10000000 * (i + 1) for i in range(6))
+
+
+def header_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:int|const char\*)\s+(gc_\w+)\s*\(", src, flags=re.M)))
+
+
+@pytest.fixture(scope="module")
+def gc():
+    import paper_2608_13255_amd as gc
+    return gc
+
+
+@pytest.fixture(scope="module")
+def L(gc):
+    return gc.lib()
+
+
+def test_exports_match_header(L):
+    declared = header_functions()
+    assert len(declared) >= 12
+    out = subprocess.run(["nm", "-D", "--defined-only", LIBSO], capture_output=True, text=True, check=True).stdout
+    exported = sorted(set(re.findall(r"\sT\s+(gc_\w+)$", out, flags=re.M)))
+    assert exported == declared
+    for name in declared:
+        assert getattr(L, name) is not None
+    assert L.gc_abi_version() == 1
+
+
+def test_struct_layouts(gc):
+    assert gc.CAMERA_DTYPE.itemsize == 68
+    assert ctypes.sizeof(gc._Sampler) == 32
+
+
+def _err(L):
+    return L.gc_last_error().decode()
+
+
+def test_transport_validation(gc, L):
+    anchors = (ctypes.c_int32 * 2)(0, 3)
+
+    def call(x0_prev=A0, new=A1, corr=A2, w=A3, B=1, N=6, H=8, W=8, C=16, anc=anchors, a=2, K=4, dt=1, out=A4):
+        return L.gc_transport_step(x0_prev, new, corr, w, B, N, H, W, C, anc, a, K, dt, out, None)
+
+    assert call(x0_prev=None) == -1 and "null" in _err(L)
+    assert call(a=0) == -1
+    assert call(a=7) == -1
+    assert call(K=5) == -1 and "K=5" in _err(L)
+    assert call(K=0) == -1
+    assert call(C=6) == -2
+    assert call(C=260) == -6
+    assert call(N=65, a=2) == -6
+    assert call(H=4095) == -6
+    assert call(dt=7) == -3
+    assert call(x0_prev=A0 + 8) == -4
+    assert call(out=A0 + 16) == -5            # x0_out overlaps x0_prev
+    dup = (ctypes.c_int32 * 2)(3, 3)
+    assert call(anc=dup) == -1 and "twice" in _err(L)
+    bad = (ctypes.c_int32 * 2)(0, 6)
+    assert call(anc=bad) == -1
+    assert call(corr=None) == -1               # targets exist, so the operator is required
+    nine = (ctypes.c_int32 * 9)(*range(9))
+    assert call(anc=nine, a=9, N=12) == -6
+
+
+def test_fused_validation(gc, L):
+    anchors = (ctypes.c_int32 * 2)(0, 3)
+    smp = gc.Sampler(kind=gc.GC_FLOW_EULER).c()
+    n = 1 * 6 * 8 * 8 * 16 * 2
+
+    def call(xt=A5, smpp=ctypes.byref(smp), t=0.5, tn=0.4, out=A4, xn=A5 + n, mo=None):
+        return L.gc_transport_reconstruct(A0, A1, A2, A3, xt, 1, 6, 8, 8, 16, anchors, 2, 4, 1, smpp, t, tn,
+                                          out, xn, mo, None)
+
+    assert call(t=0.0) == -1                   # sigma_t must be > 0
+    assert call(tn=0.6) == -1                  # sigma_next must not exceed sigma_t
+    assert call(smpp=None) == -1
+    assert call(mo=A5 + 4 * n) == -1           # pred NONE but model_out given
+    assert call(xn=A4) == -5                   # x_next == x0_out
+    bad = gc.Sampler(kind=gc.GC_DDIM, pred_out=gc.GC_PRED_VEL).c()
+    assert call(smpp=ctypes.byref(bad), t=500, tn=400) == -1
+    ddim = gc.Sampler(kind=gc.GC_DDIM).c()
+    assert call(smpp=ctypes.byref(ddim), t=500.5, tn=400) == -1
+    assert call(smpp=ctypes.byref(ddim), t=1000, tn=400) == -1
+
+
+def test_reconstruct_and_build_validation(gc, L):
+    smp = gc.Sampler(kind=gc.GC_DDIM, pred_out=gc.GC_PRED_EPS).c()
+    assert L.gc_sampler_reconstruct(A0, A1, A2, None, 64, 0, ctypes.byref(smp), 500, 400, None) == -1
+    assert L.gc_sampler_reconstruct(A0, A1, A2, A3, 66, 0, ctypes.byref(smp), 500, 400, None) == -2
+    assert L.gc_sampler_reconstruct(A0, A1, A0 + 16, A3, 64, 0, ctypes.byref(smp), 500, 400, None) == -5
+    anchors = (ctypes.c_int32 * 1)(0)
+    assert L.gc_build_correspondence(A0, A1, 1, 4, 8, 8, anchors, 1, 0, A2, A3, A4, None, None) == -1
+    assert L.gc_build_correspondence(A0, A1, 1, 4, 8, 8, anchors, 1, 4, A2, A0, A4, None, None) == -5
+    assert L.gc_build_correspondence(A0, A1, 1, 4, 5000, 8, anchors, 1, 4, A2, A3, A4, None, None) == -6
+    assert L.gc_posmap_downsample(A0, 2, 30, 32, 8, A1, None) == -2
+    assert L.gc_posmap_downsample(A0, 2, 32, 32, 8, A0 + 64, None) == -5
+    assert L.gc_posmap_bbox(A0, 1, 4, 8, 8, 0.0, A1, None) == -1
+    assert L.gc_posmap_bbox(A0, 1, 4, 8, 8, 0.01, A1 + 4, None) == -4
+
+
+def test_host_schedule_matches_oracle(gc):
+    for N, a in [(4, 1), (6, 2), (10, 3), (12, 4), (7, 3), (6, 6)]:
+        for c in range(2 * N + 3):
+            assert gc.gc_schedule_anchors(N, a, c) == oracle.anchors(N, a, c)
+        win = math.ceil(N / a)
+        for c0 in range(N):
+            seen = set()
+            for c in range(c0, c0 + win):
+                seen |= set(gc.gc_schedule_anchors(N, a, c))
+            assert seen == set(range(N))
+    for rule, name, S, E in [(0, "periodic", 30, 5), (0, "periodic", 30, 4), (1, "head_mid_tail", 30, 0),
+                             (1, "head_mid_tail", 50, 0), (1, "head_mid_tail", 10, 0), (0, "periodic", 1, 3)]:
+        assert gc.gc_schedule_full_steps(rule, S, E) == oracle.full_steps(name, S, E)
+    ddim = gc.Sampler(kind=gc.GC_DDIM)
+    flow = gc.Sampler(kind=gc.GC_FLOW_EULER)
+    for S in (1, 10, 30, 50):
+        for k in range(S):
+            assert gc.gc_sampler_step_times(ddim, S, k) == oracle.step_times("ddim", S, k)
+            t, tn = gc.gc_sampler_step_times(flow, S, k)
+            ot, otn = oracle.step_times("flow", S, k)
+            assert abs(t - ot) < 1e-15 and abs(tn - otn) < 1e-15
+    for t in (-1, 0, 32, 500, 999):
+        assert abs(gc.gc_sampler_alpha_bar(ddim, t) - oracle.alpha_bar(t)) <= 1e-15
+    with pytest.raises(gc.GeoCacheError):
+        gc.gc_schedule_anchors(6, 7, 0)
+    with pytest.raises(gc.GeoCacheError):
+        gc.gc_schedule_full_steps(5, 10, 1)
+
+
+def test_product_fails_loudly_without_library(tmp_path):
+    pkg = tmp_path / "paper_2608_13255_amd"
+    pkg.mkdir()
+    shutil.copy(os.path.join(ROOT, "paper_2608_13255_amd", "__init__.py"), pkg / "__init__.py")
+    r = subprocess.run([sys.executable, "-c", "import paper_2608_13255_amd"], cwd=tmp_path,
+                       capture_output=True, text=True)
+    assert r.returncode != 0 and "libgeocache.so is missing" in r.stderr
+
+
+def test_product_never_touches_the_oracle():
+    pkg = os.path.join(ROOT, "paper_2608_13255_amd")
+    for dirpath, _, files in os.walk(pkg):
+        for f in files:
+            if f.endswith((".py", ".hip", ".cpp", ".h", "Makefile")) or f == "Makefile":
+                text = open(os.path.join(dirpath, f)).read()
+                assert not re.search(r"\boracle\b|\borc_\w+|liboracle|\bsynth\b", text), f

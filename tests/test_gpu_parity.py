@@ -1,0 +1,375 @@
+"""HIP path vs oracle, element by element, through the C ABI.
+
+Bars (float outputs are compared against the oracle's unrounded double
+values):
+  * correspondence words, visibility, downsampled maps, bbox: bit-exact;
+  * tap weights: |dw| <= 1e-6 (float vs double of values in [0, 1]);
+  * latents (x0_out, x_next): float32 <= 1e-5, bfloat16 <= 2e-2 max-abs;
+    rows no anchor sees and anchor rows: bit-exact copies;
+  * model outputs (eps, v, velocity): the latent bound times the
+    conditioning factor 1/sqrt(1 - abar_t) (DDIM) or 1/sigma_t (flow).
+Every workload runs at its full size.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+from synth.configs import C1, C2, C3, C4, C5
+
+from conftest import latent_maps
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda:0"
+ALL = [C1, C2, C3, C4, C5]
+TOL = {"f32": 1e-5, "bf16": 2e-2}
+
+
+@pytest.fixture(scope="module")
+def gc():
+    import paper_2608_13255_amd as gc
+    if not torch.cuda.is_available():
+        pytest.fail("no GPU visible")
+    return gc
+
+
+def tdt(dtype):
+    return torch.float32 if dtype == "f32" else torch.bfloat16
+
+
+def to_dev(arr, dtype):
+    """storage array (float32, or uint16 bf16 bits) -> device tensor."""
+    if dtype == "f32":
+        return torch.from_numpy(np.ascontiguousarray(arr)).to(DEV)
+    return torch.from_numpy(np.ascontiguousarray(arr).view(np.int16)).to(DEV).view(torch.bfloat16)
+
+
+def to_host(t, dtype):
+    """device tensor -> storage array (float32, or uint16 bf16 bits)."""
+    if dtype == "f32":
+        return t.cpu().numpy()
+    return t.view(torch.int16).cpu().numpy().view(np.uint16)
+
+
+def sampler_of(gc, w, pred=None):
+    if w.sampler == "ddim":
+        return gc.Sampler(kind=gc.GC_DDIM, pred_out=gc.GC_PRED_EPS if pred is None else pred)
+    return gc.Sampler(kind=gc.GC_FLOW_EULER, pred_out=gc.GC_PRED_VEL if pred is None else pred)
+
+
+def step_of(w, k):
+    if w.ddim_single:
+        return w.ddim_single
+    return oracle.step_times(w.sampler, w.S, k)
+
+
+def cond(w, t):
+    """conditioning factor of the model outputs at step time t."""
+    if w.sampler == "ddim":
+        return max(1.0, 1.0 / math.sqrt(1.0 - oracle.alpha_bar(int(t))))
+    return max(1.0, 1.0 / t)
+
+
+def anchors_of(w, c=0):
+    return list(w.fixed_anchors) if w.fixed_anchors else oracle.anchors(w.N, w.a, c)
+
+
+def latents(w, P, A, k):
+    """Synthetic (x0_prev all views, x0_new anchors, x_t) storage arrays for step k."""
+    x0_prev = synth.x0_state(w, P, k - 1 if k > 0 else 0)
+    x0_new = synth.x0_state(w, P, k, views=A)
+    t, _ = step_of(w, k)
+    if w.sampler == "ddim":
+        ab = oracle.alpha_bar(int(t))
+        cs, cn = math.sqrt(ab), math.sqrt(1 - ab)
+    else:
+        cs, cn = 1 - t, t
+    x_t = synth.mix(x0_prev, synth.eps_noise(w, k), cs, cn)
+    return (synth.storage(x0_prev, w.dtype), synth.storage(x0_new, w.dtype), synth.storage(x_t, w.dtype))
+
+
+# ---------------------------------------------------------------------------
+# once per asset
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("w", [C2, C3, C4, C5], ids=lambda w: w.name)
+def test_downsample_bit_exact(gc, w):
+    hi = synth.render_position_maps(w)
+    want = oracle.downsample(hi, w.factor)
+    got = gc.gc_posmap_downsample(torch.from_numpy(hi).to(DEV), w.factor).cpu().numpy()
+    np.testing.assert_array_equal(got.view(np.uint32) == want.view(np.uint32), True)
+
+
+def test_downsample_ragged_and_small_factors(gc):
+    rs = np.random.default_rng(11)
+    for f, Hr, Wr, M in [(1, 7, 5, 3), (2, 10, 6, 2), (4, 12, 20, 1), (8, 24, 40, 2), (16, 32, 16, 1)]:
+        hi = rs.standard_normal((M, Hr, Wr, 3)).astype(np.float32)
+        hi[rs.random((M, Hr, Wr)) < 0.3] = np.nan
+        hi[..., 1][rs.random((M, Hr, Wr)) < 0.05] = np.inf
+        want = oracle.downsample(hi, f)
+        got = gc.gc_posmap_downsample(torch.from_numpy(hi).to(DEV), f).cpu().numpy()
+        assert np.array_equal(got.view(np.uint32), want.view(np.uint32)), (f, Hr, Wr)
+
+
+@pytest.mark.parametrize("w", ALL, ids=lambda w: w.name)
+def test_bbox_bit_exact(gc, w):
+    P = latent_maps(w.name)
+    want = oracle.bbox(P, w.tol_frac)
+    got = gc.gc_posmap_bbox(torch.from_numpy(P).to(DEV), w.tol_frac).cpu().numpy()
+    np.testing.assert_array_equal(got[:, :6], want[:, :6])
+    np.testing.assert_array_equal(got[:, 6].view(np.uint32), want[:, 6].view(np.uint32))
+
+
+def test_bbox_empty_asset_and_nonfinite(gc):
+    P = np.full((3, 2, 5, 7, 3), np.nan, np.float32)
+    P[0, 1, 2, 3] = (1, 2, 3)
+    P[0, 0, 4, 6] = (-1, 0.5, np.inf)            # not foreground
+    P[2, 0, 0, 0] = (0, 0, 0)
+    P[2, 1, 3, 1] = (3, 4, 12)
+    want = oracle.bbox(P, 0.01)
+    got = gc.gc_posmap_bbox(torch.from_numpy(P).to(DEV), 0.01).cpu().numpy()
+    np.testing.assert_array_equal(got, want)
+    assert np.all(got[1] == 0)
+
+
+def _build_both(gc, w, P, A, K):
+    bb = oracle.bbox(P, w.tol_frac)
+    corr_o, wts_o, nvis_o = oracle.build(P, synth.batch_cameras(w), A, K, bb)
+    cams = gc.camera_tensor(synth.batch_cameras(w), DEV)
+    stats = torch.empty((P.shape[0], 4), dtype=torch.int32, device=DEV)
+    Pd = torch.from_numpy(P).to(DEV)
+    bbd = gc.gc_posmap_bbox(Pd, w.tol_frac)
+    corr, wts = gc.gc_build_correspondence(Pd, cams, A, K, bbd, stats=stats)
+    return (corr_o, wts_o, nvis_o), (corr.cpu().numpy(), wts.cpu().numpy(), stats.cpu().numpy())
+
+
+@pytest.mark.parametrize("w", ALL, ids=lambda w: w.name)
+@pytest.mark.parametrize("K", [1, 4])
+def test_correspondence_parity(gc, w, K):
+    P = latent_maps(w.name)
+    for c in (0, 1):
+        A = anchors_of(w, c)
+        (corr_o, wts_o, nvis_o), (corr, wts, stats) = _build_both(gc, w, P, A, K)
+        np.testing.assert_array_equal(corr, corr_o)
+        assert np.abs(wts.astype(np.float64) - wts_o).max() <= 1e-6
+        # the words decide which weights are zero: they must agree exactly
+        np.testing.assert_array_equal(wts == 0, wts_o == 0)
+        targets = [v for v in range(w.N) if v not in A]
+        fg = np.isfinite(P[:, targets]).all(-1)
+        mask = (corr.view(np.uint32) >> 24) & 15
+        taps = np.zeros(mask.shape, np.int64)
+        for k in range(4):
+            taps += (mask >> k) & 1
+        for b in range(P.shape[0]):
+            assert stats[b, 0] == (corr[b] != 0).sum()
+            assert stats[b, 1] == (nvis_o[b] > 0).sum()
+            assert stats[b, 2] == fg[b].sum()
+            assert stats[b, 3] == taps[b].sum()
+        if w.fixed_anchors:
+            break
+
+
+def test_correspondence_ragged_grid_and_all_anchor_set(gc):
+    # a grid that is not a multiple of the block size, elevated cameras, a = N
+    w = synth.shrink(C1, elevations_deg=(10.0, -25.0, 30.0, 5.0))
+    cams = synth.cameras(w)                      # square rig; re-derive the intrinsics for 37 x 23
+    cams["fx"][:] = np.float32(23 / (2 * C1.ortho_half_extent))
+    cams["fy"][:] = np.float32(37 / (2 * C1.ortho_half_extent))
+    cams["cx"][:] = 23 / 2
+    cams["cy"][:] = 37 / 2
+    P = synth.raycast_radial(w.displacement, synth.sphere_params(w, 0), cams, 37, 23)[None]
+    bcams = {k: v[None] for k, v in cams.items()}
+    bb = oracle.bbox(P)
+    for A in ([2], [0, 3], [1, 2, 3]):
+        for K in (1, 2, 3, 4):
+            corr_o, wts_o, _ = oracle.build(P, bcams, A, K, bb)
+            Pd = torch.from_numpy(P).to(DEV)
+            corr, wts = gc.gc_build_correspondence(Pd, gc.camera_tensor(bcams, DEV), A, K,
+                                                   gc.gc_posmap_bbox(Pd, 0.01))
+            np.testing.assert_array_equal(corr.cpu().numpy(), corr_o)
+            assert np.abs(wts.cpu().numpy() - wts_o).max() <= 1e-6
+    Pd = torch.from_numpy(P).to(DEV)
+    corr, wts = gc.gc_build_correspondence(Pd, gc.camera_tensor(bcams, DEV), [0, 1, 2, 3], 4,
+                                           gc.gc_posmap_bbox(Pd, 0.01))
+    assert corr.numel() == 0 and wts.numel() == 0
+
+
+# ---------------------------------------------------------------------------
+# per cached step
+# ---------------------------------------------------------------------------
+
+def _oracle_step(w, P, A, k, K=None, pred=None):
+    K = w.K if K is None else K
+    pred = pred or ("eps" if w.sampler == "ddim" else "vel")
+    x0_prev, x0_new, x_t = latents(w, P, A, k)
+    corr_o, wts_o, nvis_o = oracle.build(P, synth.batch_cameras(w), A, K, oracle.bbox(P, w.tol_frac))
+    x0_exact, x0_state = oracle.transport(x0_prev, x0_new, corr_o, wts_o, A, w.dtype)
+    t, tn = step_of(w, k)
+    xn_o, mo_o = oracle.reconstruct(x_t, x0_state, w.dtype, w.sampler, t, tn, pred=pred)
+    return dict(x0_prev=x0_prev, x0_new=x0_new, x_t=x_t, nvis=nvis_o, x0_exact=x0_exact, x0_state=x0_state,
+                xn=xn_o, mo=mo_o, t=t, tn=tn, K=K)
+
+
+def _gpu_build(gc, w, P, A, K):
+    Pd = torch.from_numpy(P).to(DEV)
+    return gc.gc_build_correspondence(Pd, gc.camera_tensor(synth.batch_cameras(w), DEV), A, K,
+                                      gc.gc_posmap_bbox(Pd, w.tol_frac))
+
+
+def _check_x0(w, A, o, x0_out):
+    got = synth.values(x0_out, w.dtype).astype(np.float64)
+    assert np.abs(got - o["x0_exact"]).max() <= TOL[w.dtype]
+    for u in A:                                               # anchor rows: exact copies
+        np.testing.assert_array_equal(x0_out[:, u], o["x0_state"][:, u])
+    targets = [v for v in range(w.N) if v not in A]
+    inv = o["nvis"] == 0                                       # unseen tokens keep their state
+    for ti, v in enumerate(targets):
+        np.testing.assert_array_equal(x0_out[:, v][inv[:, ti]], o["x0_prev"][:, v][inv[:, ti]])
+
+
+@pytest.mark.parametrize("w", ALL, ids=lambda w: w.name)
+def test_transport_step_parity(gc, w):
+    P = latent_maps(w.name)
+    A = anchors_of(w, 1)
+    o = _oracle_step(w, P, A, 3 if w.S > 3 else 0)
+    corr, wts = _gpu_build(gc, w, P, A, o["K"])
+    x0_out = gc.gc_transport_step(to_dev(o["x0_prev"], w.dtype), to_dev(o["x0_new"], w.dtype), corr, wts, A)
+    _check_x0(w, A, o, to_host(x0_out, w.dtype))
+
+
+@pytest.mark.parametrize("w", ALL, ids=lambda w: w.name)
+def test_fused_parity_and_equals_two_calls(gc, w):
+    P = latent_maps(w.name)
+    A = anchors_of(w, 2)
+    k = 4 if w.S > 4 else 0
+    o = _oracle_step(w, P, A, k)
+    corr, wts = _gpu_build(gc, w, P, A, o["K"])
+    smp = sampler_of(gc, w)
+    prev, new, xt = (to_dev(o[n], w.dtype) for n in ("x0_prev", "x0_new", "x_t"))
+    x0_out, x_next, mo = gc.gc_transport_reconstruct(prev, new, corr, wts, xt, A, smp, o["t"], o["tn"])
+    x0_h = to_host(x0_out, w.dtype)
+    _check_x0(w, A, o, x0_h)
+    xn = synth.values(to_host(x_next, w.dtype), w.dtype).astype(np.float64)
+    assert np.abs(xn - o["xn"]).max() <= TOL[w.dtype]
+    # the model output depends on the stored x0.  float32: the stored values differ by at most
+    # an ulp, which the conditioned bound covers.  bfloat16: the two sides may round a stored
+    # x0 to neighbouring values in rare ties; compare where both stored the same x0.
+    mog = synth.values(to_host(mo, w.dtype), w.dtype).astype(np.float64)
+    if w.dtype == "f32":
+        same = np.ones(x0_h.shape, bool)
+    else:
+        same = x0_h == o["x0_state"]
+        assert same.mean() > 0.999
+    assert np.abs(mog - o["mo"])[same].max() <= TOL[w.dtype] * cond(w, o["t"])
+    # fused == transport then reconstruct, bit for bit
+    x0_2 = gc.gc_transport_step(prev, new, corr, wts, A)
+    xn_2, mo_2 = gc.gc_sampler_reconstruct(xt, x0_2, smp, o["t"], o["tn"])
+    assert torch.equal(x0_2.view(torch.int16 if w.dtype == "bf16" else torch.int32),
+                       x0_out.view(torch.int16 if w.dtype == "bf16" else torch.int32))
+    iv = torch.int16 if w.dtype == "bf16" else torch.int32
+    assert torch.equal(xn_2.view(iv), x_next.view(iv)) and torch.equal(mo_2.view(iv), mo.view(iv))
+
+
+def test_fused_in_place_and_deterministic(gc):
+    w = C5
+    P = latent_maps(w.name)
+    A = anchors_of(w, 0)
+    x0_prev, x0_new, x_t = latents(w, P, A, 5)
+    corr, wts = _gpu_build(gc, w, P, A, w.K)
+    smp = sampler_of(gc, w)
+    t, tn = step_of(w, 5)
+    prev, new = to_dev(x0_prev, w.dtype), to_dev(x0_new, w.dtype)
+    outs = []
+    for _ in range(2):
+        xt = to_dev(x_t, w.dtype)
+        x0_out, x_next, mo = gc.gc_transport_reconstruct(prev, new, corr, wts, xt, A, smp, t, tn, x_next=xt)
+        assert x_next.data_ptr() == xt.data_ptr()
+        outs.append((to_host(x0_out, w.dtype), to_host(x_next, w.dtype), to_host(mo, w.dtype)))
+    for a_, b_ in zip(*outs):
+        np.testing.assert_array_equal(a_, b_)
+    xt = to_dev(x_t, w.dtype)
+    _, xn_sep, _ = gc.gc_transport_reconstruct(prev, new, corr, wts, xt, A, smp, t, tn)
+    np.testing.assert_array_equal(to_host(xn_sep, w.dtype), outs[0][1])
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("kind,pred,t,tn", [("ddim", "eps", 800, 760), ("ddim", "v", 32, -1),
+                                            ("ddim", "eps", 999, 966), ("flow", "vel", 1.0, 0.98),
+                                            ("flow", "vel", 0.04, 0.02), ("flow", "vel", 0.5, 0.0)])
+def test_reconstruct_parity(gc, dtype, kind, pred, t, tn):
+    rs = np.random.default_rng(int(t * 10) + 1)
+    n = 3 * 4096 + 8
+    x0 = rs.standard_normal(n).astype(np.float32)
+    xt = rs.standard_normal(n).astype(np.float32) * 1.5
+    x0s, xts = synth.storage(x0, dtype), synth.storage(xt, dtype)
+    xn_o, mo_o = oracle.reconstruct(xts, x0s, dtype, kind, t, tn, pred=pred)
+    P = {"eps": gc.GC_PRED_EPS, "v": gc.GC_PRED_V, "vel": gc.GC_PRED_VEL}[pred]
+    smp = gc.Sampler(kind=gc.GC_DDIM if kind == "ddim" else gc.GC_FLOW_EULER, pred_out=P)
+    xn, mo = gc.gc_sampler_reconstruct(to_dev(xts, dtype), to_dev(x0s, dtype), smp, t, tn)
+    xn = synth.values(to_host(xn, dtype), dtype).astype(np.float64)
+    mo = synth.values(to_host(mo, dtype), dtype).astype(np.float64)
+    c = max(1.0, 1 / math.sqrt(1 - oracle.alpha_bar(int(t)))) if kind == "ddim" else max(1.0, 1 / t)
+    assert np.abs(xn - xn_o).max() <= TOL[dtype]
+    assert np.abs(mo - mo_o).max() <= TOL[dtype] * c
+    # no model output requested; in place
+    smp0 = gc.Sampler(kind=smp.kind, pred_out=gc.GC_PRED_NONE)
+    xtd = to_dev(xts, dtype)
+    xn2, none = gc.gc_sampler_reconstruct(xtd, to_dev(x0s, dtype), smp0, t, tn, x_next=xtd)
+    assert none is None
+    np.testing.assert_allclose(synth.values(to_host(xn2, dtype), dtype), xn, rtol=0, atol=0)
+
+
+def test_nan_latents_propagate(gc):
+    w = C2
+    P = latent_maps(w.name)
+    A = anchors_of(w, 0)
+    o = _oracle_step(w, P, A, 2)
+    prev = o["x0_prev"].copy()
+    prev[0, 1, 10:12] = np.nan
+    new = o["x0_new"].copy()
+    new[0, 0, 20:22] = np.inf
+    corr_o, wts_o, _ = oracle.build(P, synth.batch_cameras(w), A, 4, oracle.bbox(P))
+    ex, st = oracle.transport(prev, new, corr_o, wts_o, A, "f32")
+    corr, wts = _gpu_build(gc, w, P, A, 4)
+    got = gc.gc_transport_step(to_dev(prev, "f32"), to_dev(new, "f32"), corr, wts, A).cpu().numpy()
+    np.testing.assert_array_equal(np.isnan(got), np.isnan(ex))
+    np.testing.assert_array_equal(np.isinf(got), np.isinf(ex))
+    fin = np.isfinite(ex)
+    assert np.abs(got[fin] - ex[fin]).max() <= 1e-5
+
+
+def test_all_views_anchor_is_plain_sampler_step(gc):
+    """a = N: the cached step reduces exactly to the plain sampler step."""
+    w = synth.shrink(C2, dtype="bf16")
+    P = latent_maps(C2.name)
+    A = list(range(w.N))
+    x0_prev, x0_new, x_t = latents(w, P, A, 2)
+    smp = sampler_of(gc, w)
+    t, tn = step_of(w, 2)
+    empty_c = torch.empty((1, 0, w.H, w.W, w.N), dtype=torch.int32, device=DEV)
+    empty_w = torch.empty((1, 0, w.H, w.W, w.N, 4), dtype=torch.float32, device=DEV)
+    x0_out, xn, mo = gc.gc_transport_reconstruct(to_dev(x0_prev, "bf16"), to_dev(x0_new, "bf16"), empty_c, empty_w,
+                                                 to_dev(x_t, "bf16"), A, smp, t, tn)
+    np.testing.assert_array_equal(to_host(x0_out, "bf16"), x0_new)
+    xn_p, mo_p = gc.gc_sampler_reconstruct(to_dev(x_t, "bf16"), to_dev(x0_new, "bf16"), smp, t, tn)
+    assert torch.equal(xn.view(torch.int16), xn_p.view(torch.int16))
+    assert torch.equal(mo.view(torch.int16), mo_p.view(torch.int16))
+
+
+def test_k1_transport_and_channel_widths(gc):
+    """K = 1 operators, and C = 4 / 8 / 12 channels in both dtypes (covers the
+    8-byte and 16-byte bfloat16 vectors)."""
+    base = C2
+    P = latent_maps(base.name)
+    A = anchors_of(base, 1)
+    for K in (1, 2):
+        for dtype, C in (("f32", 8), ("bf16", 4), ("bf16", 8), ("bf16", 12), ("f32", 12)):
+            w = synth.shrink(base, C=C, dtype=dtype)
+            o = _oracle_step(w, P, A, 3, K=K)
+            corr, wts = _gpu_build(gc, w, P, A, K)
+            x0_out = gc.gc_transport_step(to_dev(o["x0_prev"], dtype), to_dev(o["x0_new"], dtype), corr, wts, A)
+            _check_x0(w, A, o, to_host(x0_out, dtype))
