@@ -291,6 +291,47 @@ def gc_transport_reconstruct(x0_prev: torch.Tensor, x0_anchor_new: torch.Tensor,
     return x0_out, x_next, model_out
 
 
+class BoundCall:
+    """A gc_transport_reconstruct call with every argument but (t, t_next)
+    already marshalled: calling it issues exactly one ctypes call.  For
+    step loops where per-call Python checks would cost more host time than
+    the kernel takes on the GPU."""
+    __slots__ = ("_fn", "_pre", "_post", "_smp", "keep")
+
+    def __init__(self, fn, pre, smp, post, keep):
+        self._fn, self._pre, self._smp, self._post, self.keep = fn, pre, smp, post, keep
+
+    def __call__(self, t: float, t_next: float) -> None:
+        rc = self._fn(*self._pre, ctypes.byref(self._smp), t, t_next, *self._post)
+        if rc != GC_OK:
+            _check(rc, "gc_transport_reconstruct")
+
+
+def bind_transport_reconstruct(x0_prev: torch.Tensor, x0_anchor_new: torch.Tensor, corr: torch.Tensor,
+                               weights: torch.Tensor, x_t: torch.Tensor, anchors: Sequence[int], sampler: Sampler,
+                               x0_out: torch.Tensor, x_next: torch.Tensor, model_out: torch.Tensor = None,
+                               stream=None) -> BoundCall:
+    """Marshal gc_transport_reconstruct's buffer arguments once (same checks
+    as gc_transport_reconstruct); the returned object takes (t, t_next).
+    The tensors must stay alive and unmoved while the object is used."""
+    B, N, H, W, C = _latent_shape(x0_prev)
+    arr, a = _anchors(anchors)
+    if tuple(x0_anchor_new.shape) != (B, a, H, W, C) or x0_anchor_new.dtype != x0_prev.dtype:
+        raise ValueError(f"x0_anchor_new must be [B, a={a}, H, W, C] of the same dtype as x0_prev")
+    for name, t in (("x_t", x_t), ("x0_out", x0_out), ("x_next", x_next)):
+        if t.shape != x0_prev.shape or t.dtype != x0_prev.dtype:
+            raise ValueError(f"{name} must match x0_prev in shape and dtype")
+    if (sampler.pred_out != GC_PRED_NONE) != (model_out is not None):
+        raise ValueError("model_out must be given iff the sampler has a prediction output")
+    K = weights.shape[-1]
+    pre = (_dev(x0_prev, "x0_prev"), _dev(x0_anchor_new, "x0_anchor_new"),
+           _dev(corr, "corr") if corr.numel() else None, _dev(weights, "weights") if weights.numel() else None,
+           _dev(x_t, "x_t"), B, N, H, W, C, arr, a, K, dtype_code(x0_prev))
+    post = (_dev(x0_out, "x0_out"), _dev(x_next, "x_next"), _opt(model_out, "model_out"), _stream(stream))
+    return BoundCall(lib().gc_transport_reconstruct, pre, sampler.c(), post,
+                     (x0_prev, x0_anchor_new, corr, weights, x_t, x0_out, x_next, model_out, arr))
+
+
 def gc_schedule_anchors(N: int, a: int, c: int) -> List[int]:
     out = (ctypes.c_int32 * a)()
     _check(lib().gc_schedule_anchors(N, a, c, out), "gc_schedule_anchors")

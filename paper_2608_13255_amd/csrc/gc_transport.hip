@@ -13,7 +13,9 @@
 // of one pixel share its correspondence words and weights through L1.
 // Blocks are remapped so that each of the 8 XCDs processes one contiguous
 // slice of the (asset, view, pixel) space: an XCD then gathers from only its
-// own assets' anchor views, which fit its L2.
+// own assets' anchor views, which fit its L2.  Data each thread touches once
+// (its own x0_prev and x_t, every output) is read and written with
+// nontemporal hints; only the gathered anchor tiles go through L2 normally.
 #include "gc_common.h"
 
 namespace gc {
@@ -22,20 +24,35 @@ namespace {
 constexpr int kBlock = 256;
 constexpr int kXcds = 8;
 
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 template <int BYTES> struct RawT;
-template <> struct RawT<16> { using type = uint4; };
-template <> struct RawT<8> { using type = uint2; };
+template <> struct RawT<16> { using type = uint4; using nt = u32x4; };
+template <> struct RawT<8> { using type = uint2; using nt = u32x2; };
 
 // Storage codec for VEC elements of dtype DT packed in one raw vector.
 template <int DT, int VEC> struct Codec {
   static constexpr int kBytes = VEC * (DT == GC_F32 ? 4 : 2);
   using Raw = typename RawT<kBytes>::type;
+  using NT = typename RawT<kBytes>::nt;
 
+  // cached load: anchor tiles gathered by several target tokens
   __device__ __forceinline__ static Raw load(const void* base, int64_t elem) {
     return *reinterpret_cast<const Raw*>(static_cast<const char*>(base) + elem * (DT == GC_F32 ? 4 : 2));
   }
-  __device__ __forceinline__ static void store(void* base, int64_t elem, const Raw& r) {
-    *reinterpret_cast<Raw*>(static_cast<char*>(base) + elem * (DT == GC_F32 ? 4 : 2)) = r;
+  // streamed load / store: data touched exactly once per step.  The
+  // nontemporal hint keeps it from displacing the gathered anchor tiles in L2.
+  __device__ __forceinline__ static Raw load_stream(const void* base, int64_t elem) {
+    const NT* p = reinterpret_cast<const NT*>(static_cast<const char*>(base) + elem * (DT == GC_F32 ? 4 : 2));
+    const NT v = __builtin_nontemporal_load(p);
+    Raw r;
+    __builtin_memcpy(&r, &v, sizeof(Raw));
+    return r;
+  }
+  __device__ __forceinline__ static void store_stream(void* base, int64_t elem, const Raw& r) {
+    NT v;
+    __builtin_memcpy(&v, &r, sizeof(Raw));
+    __builtin_nontemporal_store(v, reinterpret_cast<NT*>(static_cast<char*>(base) + elem * (DT == GC_F32 ? 4 : 2)));
   }
   __device__ __forceinline__ static void unpack(const Raw& r, float (&f)[VEC]) {
     const uint32_t* w = reinterpret_cast<const uint32_t*>(&r);
@@ -73,9 +90,11 @@ struct TArgs {
   void* x0_out;
   void* x_next;
   void* model_out;
-  int64_t n_threads;   // B * N * H * W * (C / VEC)
+  int64_t n_threads;   // B * N * H * W * (C / VEC) chunks
   int N, H, W, HW, C, a, K, NT, CV;
-  int n_blocks;        // logical blocks (before XCD padding)
+  int cv_shift;        // log2(CV) when CV is a power of two, else -1
+  int bpv;             // blocks per view: ceil(HW * CV / kBlock)
+  int n_blocks;        // logical blocks = B * N * bpv (before XCD padding)
   int remap;           // 1: XCD-contiguous block order
   int8_t slot_of_view[GC_MAX_VIEWS];    // anchor slot of view v, or -1
   int8_t tslot_of_view[GC_MAX_VIEWS];   // target slot of view v, or -1
@@ -114,19 +133,29 @@ template <int DT, int VEC, bool FUSED>
 __global__ __launch_bounds__(kBlock) void k_transport(TArgs g) {
   using CD = Codec<DT, VEC>;
   using Raw = typename CD::Raw;
+  // Blocks never straddle a view, so the (asset, view) split is block-uniform
+  // scalar work and only the chunk -> (token, channel vector) split is per lane.
   const int lb = logical_block(g.n_blocks, g.remap);
   if (lb >= g.n_blocks) return;
-  const int64_t gid = (int64_t)lb * kBlock + threadIdx.x;
-  if (gid >= g.n_threads) return;
-  const int cv = (int)(gid % g.CV);
-  const int64_t pix = gid / g.CV;              // (b * N + v) * HW + p
-  const int p = (int)(pix % g.HW);
-  const int64_t bv = pix / g.HW;
-  const int v = (int)(bv % g.N);
-  const int b = (int)(bv / g.N);
+  const int bv = lb / g.bpv;                   // b * N + v
+  const int t = (lb - bv * g.bpv) * kBlock + (int)threadIdx.x;
+  if (t >= g.HW * g.CV) return;
+  const int b = bv / g.N;
+  const int v = bv - b * g.N;
+  int p, cv;
+  if (g.cv_shift >= 0) {
+    p = t >> g.cv_shift;
+    cv = t & (g.CV - 1);
+  } else {
+    p = t / g.CV;
+    cv = t - p * g.CV;
+  }
+  const int64_t pix = (int64_t)bv * g.HW + p;
   const int64_t base = pix * g.C + (int64_t)cv * VEC;
   const int s_self = g.slot_of_view[v];
 
+  Raw xtr;
+  if constexpr (FUSED) xtr = CD::load_stream(g.x_t, base);   // independent of the transport: issue first
   Raw x0r;
   float x0f[VEC];
   if (s_self >= 0) {
@@ -138,13 +167,22 @@ __global__ __launch_bounds__(kBlock) void k_transport(TArgs g) {
     const int64_t crow = ((int64_t)b * g.NT + ti) * g.HW + p;
     const int32_t* cw = g.corr + crow * g.a;
     int32_t words[GC_MAX_ANCHORS];
+    if (g.a == 4) {   // the common layout: one 16-byte load (rows are 16-byte aligned)
+      const int4 q = *reinterpret_cast<const int4*>(cw);
+      words[0] = q.x;
+      words[1] = q.y;
+      words[2] = q.z;
+      words[3] = q.w;
+#pragma unroll
+      for (int s = 4; s < GC_MAX_ANCHORS; ++s) words[s] = 0;
+    } else {
+#pragma unroll
+      for (int s = 0; s < GC_MAX_ANCHORS; ++s) words[s] = s < g.a ? cw[s] : 0;
+    }
     bool any = false;
 #pragma unroll
-    for (int s = 0; s < GC_MAX_ANCHORS; ++s) {
-      words[s] = s < g.a ? cw[s] : 0;
-      any |= words[s] != 0;
-    }
-    const Raw prevr = CD::load(g.x0_prev, base);
+    for (int s = 0; s < GC_MAX_ANCHORS; ++s) any |= words[s] != 0;
+    const Raw prevr = CD::load_stream(g.x0_prev, base);
     if (!any) {
       x0r = prevr;   // no anchor sees this token: it keeps its own state
       CD::unpack(x0r, x0f);
@@ -187,13 +225,13 @@ __global__ __launch_bounds__(kBlock) void k_transport(TArgs g) {
       CD::unpack(x0r, x0f);   // the reconstruction reads x0 as stored
     }
   }
-  CD::store(g.x0_out, base, x0r);
+  CD::store_stream(g.x0_out, base, x0r);
   if constexpr (FUSED) {
     float xtf[VEC], xn[VEC], mo[VEC];
-    CD::unpack(CD::load(g.x_t, base), xtf);
+    CD::unpack(xtr, xtf);
     reconstruct_vec<VEC>(g.r, xtf, x0f, xn, mo);
-    CD::store(g.x_next, base, CD::pack(xn));
-    if (g.model_out) CD::store(g.model_out, base, CD::pack(mo));
+    CD::store_stream(g.x_next, base, CD::pack(xn));
+    if (g.model_out) CD::store_stream(g.model_out, base, CD::pack(mo));
   }
 }
 
@@ -205,11 +243,11 @@ __global__ __launch_bounds__(kBlock) void k_reconstruct(const void* __restrict__
   const int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x;
   if (i >= n_vec) return;
   float xtf[VEC], x0f[VEC], xn[VEC], mo[VEC];
-  CD::unpack(CD::load(x_t, i * VEC), xtf);
-  CD::unpack(CD::load(x0, i * VEC), x0f);
+  CD::unpack(CD::load_stream(x_t, i * VEC), xtf);
+  CD::unpack(CD::load_stream(x0, i * VEC), x0f);
   reconstruct_vec<VEC>(r, xtf, x0f, xn, mo);
-  CD::store(x_next, i * VEC, CD::pack(xn));
-  if (model_out) CD::store(model_out, i * VEC, CD::pack(mo));
+  CD::store_stream(x_next, i * VEC, CD::pack(xn));
+  if (model_out) CD::store_stream(model_out, i * VEC, CD::pack(mo));
 }
 
 int pick_vec(int dtype, int64_t c) { return dtype == GC_F32 ? 4 : (c % 8 == 0 ? 8 : 4); }
@@ -267,8 +305,12 @@ int prepare_transport(const void* x0_prev, const void* x0_new, const int32_t* co
   g->K = K;
   g->NT = NT;
   g->CV = C / vec;
+  g->cv_shift = -1;
+  for (int sh = 0; sh < 8; ++sh)
+    if ((1 << sh) == g->CV) g->cv_shift = sh;
   g->n_threads = (int64_t)B * N * (int64_t)HW * g->CV;
-  const int64_t nb = (g->n_threads + kBlock - 1) / kBlock;
+  g->bpv = (int)(((int64_t)HW * g->CV + kBlock - 1) / kBlock);
+  const int64_t nb = (int64_t)B * N * g->bpv;
   if (nb > (int64_t)0x7fffffff - kXcds) return fail(GC_ERR_CAPACITY, "%s: problem too large for one launch", who);
   g->n_blocks = (int)nb;
   g->remap = 1;
