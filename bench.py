@@ -29,7 +29,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 PEAK_HBM_GBS = 8000.0
-FUSED_KERNEL = "k_transport<1, 8, true>"     # bf16, 16-byte vectors, fused
+FUSED_KERNEL = "k_transport<1, 8, true, true>"   # bf16, 16-byte vectors, fused, split launch
 
 
 def parse():
@@ -143,6 +143,14 @@ def main():
     rows["bbox_ms"] = e1.elapsed_time(e2)
     rows["build_ms_per_anchor_set"] = e2.elapsed_time(e3) / len(anchor_sets)
     rows["anchor_sets"] = len(anchor_sets)
+    index = {}
+    e4, e5 = ev(), ev()
+    e4.record()
+    for A in anchor_sets:
+        index[A] = gc.gc_index_correspondence(ops[A][0])
+    e5.record()
+    torch.cuda.synchronize()
+    rows["index_ms_per_anchor_set"] = e4.elapsed_time(e5) / len(anchor_sets)
     vis_pairs = {A: int(stats[A][:, 0].sum().item()) for A in anchor_sets}
     cover = {A: float(stats[A][:, 1].sum().item()) / max(1, float(stats[A][:, 2].sum().item())) for A in anchor_sets}
     del hi_d
@@ -172,8 +180,14 @@ def main():
     latent_view = HW * C * es
     V = B * (N - a) * HW
 
+    n_tok = B * (N - a) * HW
+
     def algo_bytes(A):
-        return B * (4 * N + a) * latent_view + 4 * B * (N - a) * HW * a + 4 * K * vis_pairs[A]
+        # latents: read x0_prev, x0_anchor_new, x_t, write x0_out, x_next; index: one bit per
+        # target token + the list of visible tokens; their words; the weights of visible pairs
+        nv = index[A].n_vis
+        return (B * (4 * N + a) * latent_view + 4 * ((n_tok + 31) // 32) + 4 * nv + 4 * a * nv
+                + 4 * K * vis_pairs[A])
 
     # every (buffer set, anchor set) pair gets its call marshalled once, so the
     # host issues one ctypes call per step and stays ahead of the GPU
@@ -182,7 +196,8 @@ def main():
         for A in anchor_sets:
             corr, wts = ops[A]
             plans[(r, A)] = gc.bind_transport_reconstruct(buf["x0_prev"], buf["x0_new"], corr, wts, buf["x_t"],
-                                                          list(A), smp, buf["x0_out"], buf["x_next"])
+                                                          list(A), smp, buf["x0_out"], buf["x_next"],
+                                                          index=index[A])
 
     def step(i):
         A = tuple(gc.gc_schedule_anchors(N, a, i))        # host schedule: cached step i
@@ -230,12 +245,13 @@ def main():
     kc = cached_steps[0]
     tt, ttn = gc.gc_sampler_step_times(smp, w.S, kc)
     rows["transport_only_ms"] = timed(lambda: gc.gc_transport_step(buf["x0_prev"], buf["x0_new"], corr0, wts0, A0,
-                                                                   x0_out=buf["x0_out"]))
+                                                                   x0_out=buf["x0_out"], index=index[anchor_sets[0]]))
     rows["reconstruct_only_ms"] = timed(lambda: gc.gc_sampler_reconstruct(buf["x_t"], buf["x0_out"], smp, tt, ttn,
                                                                           x_next=buf["x_next"]))
     rows["unfused_pair_ms"] = rows["transport_only_ms"] + rows["reconstruct_only_ms"]
     rows["coverage_per_anchor_set"] = [round(cover[A], 4) for A in anchor_sets]
     rows["visible_pairs_per_anchor_set"] = [vis_pairs[A] for A in anchor_sets]
+    rows["visible_tokens_per_anchor_set"] = [index[A].n_vis for A in anchor_sets]
 
     copy_gbps = None
     if args.copy_probe:

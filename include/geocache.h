@@ -11,6 +11,7 @@
  *   once per asset       gc_posmap_downsample   render-res position maps -> latent grid
  *                        gc_posmap_bbox         per-asset bbox and squared tolerance
  *                        gc_build_correspondence   G_{A->v} for one anchor set
+ *                        gc_index_correspondence   visible-token index of G_{A->v}
  *   every cached step    gc_transport_step      Eq. 1: x0(v) = x0_prev(v) + G[dx0(A)]
  *                        gc_sampler_reconstruct sampler-consistent eps / v / velocity + x_t update
  *                        gc_transport_reconstruct  the two above fused in one pass
@@ -194,6 +195,29 @@ int gc_build_correspondence(const float* pos, const gc_camera* cams, int B, int 
                             float* weights, uint32_t* stats, hipStream_t stream);
 
 /*
+ * Visible-token index of a correspondence operator (once per asset and
+ * anchor set).  A token's row of G_{A->v} is non-zero iff at least one anchor
+ * sees it (Sec. 3.2: rows with no in-tolerance tap are zero).  The index lets
+ * the per-step calls split their work: the visible tokens, listed compactly,
+ * get the gathering; every other token is streamed and recognised by one bit
+ * instead of its a correspondence words.
+ *   corr       device int32 [n_tokens][a] words from gc_build_correspondence,
+ *              n_tokens = B * (N - a) * H * W (at most 2^31 - 1)
+ *   vis_bits   device uint32 [ceil(n_tokens / 32)] output: bit (i & 31) of word
+ *              i >> 5 is set iff token i has a non-zero word
+ *   vis_list   device int32 [n_tokens] output (capacity): the first *n_vis
+ *              entries are the visible token indices in ascending order
+ *   n_vis      device int32 [1] output
+ *   workspace  device scratch of at least gc_index_workspace_bytes(n_tokens)
+ *              bytes, owned by the caller; its contents are not meaningful
+ *              after the call and calls sharing one workspace must not overlap
+ * The result is deterministic.  n_tokens = 0 is legal (n_vis = 0).
+ */
+size_t gc_index_workspace_bytes(int64_t n_tokens);
+int gc_index_correspondence(const int32_t* corr, int64_t n_tokens, int a, uint32_t* vis_bits, int32_t* vis_list,
+                            int32_t* n_vis, void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
  * Delta transport, Eq. 1 (Sec. 3.2, delta transport and loop order), for one
  * cached step:
  *   anchor view u = anchors[s]:  x0_out(u) = x0_anchor_new(s)          (copy)
@@ -204,11 +228,17 @@ int gc_build_correspondence(const float* pos, const gc_camera* cams, int B, int 
  *   x0_prev        device [B][N][H][W][C]  stored x0 of the previous step, all views
  *   x0_anchor_new  device [B][a][H][W][C]  this step's anchor predictions, slot order
  *   corr, weights  as written by gc_build_correspondence for the same anchor list, B, N, H, W, K
+ *   vis_bits, vis_list, n_vis
+ *                  optional index of corr from gc_index_correspondence (n_vis
+ *                  read back to the host); both null for the plain launch.
+ *                  With the index the visible tokens are processed by their own
+ *                  blocks; the result is bit-identical either way.
  *   x0_out         device [B][N][H][W][C]  output; must not overlap x0_prev or x0_anchor_new
  */
 int gc_transport_step(const void* x0_prev, const void* x0_anchor_new, const int32_t* corr,
-                      const float* weights, int B, int N, int H, int W, int C, const int32_t* anchors,
-                      int a, int K, int dtype, void* x0_out, hipStream_t stream);
+                      const float* weights, const uint32_t* vis_bits, const int32_t* vis_list, int64_t n_vis,
+                      int B, int N, int H, int W, int C, const int32_t* anchors, int a, int K, int dtype,
+                      void* x0_out, hipStream_t stream);
 
 /*
  * Sampler-consistent reconstruction (Sec. 3.2, after Eq. 1): from x0 and the
@@ -236,6 +266,7 @@ int gc_sampler_reconstruct(const void* x_t, const void* x0, void* x_next, void* 
 /*
  * gc_transport_step followed by gc_sampler_reconstruct over all B*N views, in
  * one pass (one read of every input, one write of every output).  The
+ * optional index (vis_bits, vis_list, n_vis) is as for gc_transport_step.  The
  * reconstruction consumes x0_out as stored (rounded to the dtype), so the
  * result is bit-identical to the two separate calls.
  *   x_t        device [B][N][H][W][C]
@@ -246,10 +277,11 @@ int gc_sampler_reconstruct(const void* x_t, const void* x0, void* x_next, void* 
  * other (x_next == x_t excepted).
  */
 int gc_transport_reconstruct(const void* x0_prev, const void* x0_anchor_new, const int32_t* corr,
-                             const float* weights, const void* x_t, int B, int N, int H, int W,
-                             int C, const int32_t* anchors, int a, int K, int dtype,
-                             const gc_sampler* smp, double t, double t_next, void* x0_out,
-                             void* x_next, void* model_out, hipStream_t stream);
+                             const float* weights, const uint32_t* vis_bits, const int32_t* vis_list,
+                             int64_t n_vis, const void* x_t, int B, int N, int H, int W, int C,
+                             const int32_t* anchors, int a, int K, int dtype, const gc_sampler* smp,
+                             double t, double t_next, void* x0_out, void* x_next, void* model_out,
+                             hipStream_t stream);
 
 /*
  * Host schedule (no device work).

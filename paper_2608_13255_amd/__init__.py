@@ -83,12 +83,15 @@ def lib() -> ctypes.CDLL:
             "gc_posmap_downsample": ([_vp, _i64, _i, _i, _i, _vp, _vp], _i),
             "gc_posmap_bbox": ([_vp, _i, _i, _i, _i, ctypes.c_float, _vp, _vp], _i),
             "gc_build_correspondence": ([_vp, _vp, _i, _i, _i, _i, _i32p, _i, _i, _vp, _vp, _vp, _vp, _vp], _i),
-            "gc_transport_step": ([_vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i32p, _i, _i, _i, _vp, _vp], _i),
+            "gc_index_workspace_bytes": ([_i64], ctypes.c_size_t),
+            "gc_index_correspondence": ([_vp, _i64, _i, _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp], _i),
+            "gc_transport_step": ([_vp, _vp, _vp, _vp, _vp, _vp, _i64, _i, _i, _i, _i, _i, _i32p, _i, _i, _i, _vp,
+                                   _vp], _i),
             "gc_sampler_reconstruct": ([_vp, _vp, _vp, _vp, _i64, _i, ctypes.POINTER(_Sampler), ctypes.c_double,
                                         ctypes.c_double, _vp], _i),
-            "gc_transport_reconstruct": ([_vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i32p, _i, _i, _i,
-                                          ctypes.POINTER(_Sampler), ctypes.c_double, ctypes.c_double, _vp, _vp,
-                                          _vp, _vp], _i),
+            "gc_transport_reconstruct": ([_vp, _vp, _vp, _vp, _vp, _vp, _i64, _vp, _i, _i, _i, _i, _i, _i32p, _i,
+                                          _i, _i, ctypes.POINTER(_Sampler), ctypes.c_double, ctypes.c_double, _vp,
+                                          _vp, _vp, _vp], _i),
             "gc_schedule_anchors": ([_i, _i, _i64, _i32p], _i),
             "gc_schedule_full_steps": ([_i, _i, _i, ctypes.POINTER(ctypes.c_uint8)], _i),
             "gc_sampler_step_times": ([ctypes.POINTER(_Sampler), _i, _i, ctypes.POINTER(ctypes.c_double),
@@ -220,6 +223,44 @@ def gc_build_correspondence(pos: torch.Tensor, cams: torch.Tensor, anchors: Sequ
     return corr, weights
 
 
+@dataclass
+class VisibleIndex:
+    """Output of gc_index_correspondence: vis_bits (int32 view of the uint32
+    words), vis_list (int32) and the host count n_vis."""
+    vis_bits: torch.Tensor
+    vis_list: torch.Tensor
+    n_vis: int
+
+
+def gc_index_correspondence(corr: torch.Tensor, workspace: torch.Tensor = None, stream=None) -> VisibleIndex:
+    """Visible-token index of a correspondence (corr int32 [B, N-a, H, W, a]).
+    Reads the visible count back to the host (one synchronisation)."""
+    if corr.dtype != torch.int32 or corr.dim() != 5:
+        raise ValueError("corr must be int32 [B, N-a, H, W, a]")
+    a = corr.shape[-1]
+    n_tok = int(corr.numel() // a) if a else 0
+    dev = corr.device
+    need = int(lib().gc_index_workspace_bytes(n_tok))
+    if workspace is None:
+        workspace = torch.empty(need, dtype=torch.uint8, device=dev)
+    if workspace.numel() * workspace.element_size() < need:
+        raise ValueError(f"workspace must hold at least {need} bytes")
+    bits = torch.empty(max(1, (n_tok + 31) // 32), dtype=torch.int32, device=dev)
+    lst = torch.empty(max(1, n_tok), dtype=torch.int32, device=dev)
+    nv = torch.empty(1, dtype=torch.int32, device=dev)
+    _check(lib().gc_index_correspondence(_dev(corr, "corr") if n_tok else None, n_tok, a, _dev(bits, "vis_bits"),
+                                         _dev(lst, "vis_list"), _dev(nv, "n_vis"), _dev(workspace, "workspace"),
+                                         workspace.numel() * workspace.element_size(), _stream(stream)),
+           "gc_index_correspondence")
+    return VisibleIndex(bits, lst, int(nv.item()))
+
+
+def _index_args(index: Optional[VisibleIndex]):
+    if index is None:
+        return None, None, 0
+    return _dev(index.vis_bits, "vis_bits"), _dev(index.vis_list, "vis_list"), int(index.n_vis)
+
+
 def _latent_shape(x0_prev: torch.Tensor):
     if x0_prev.dim() != 5:
         raise ValueError("latents must be [B, N, H, W, C]")
@@ -228,8 +269,9 @@ def _latent_shape(x0_prev: torch.Tensor):
 
 def gc_transport_step(x0_prev: torch.Tensor, x0_anchor_new: torch.Tensor, corr: torch.Tensor,
                       weights: torch.Tensor, anchors: Sequence[int], x0_out: torch.Tensor = None,
-                      stream=None) -> torch.Tensor:
-    """Eq. 1 over one cached step; returns x0_out [B, N, H, W, C]."""
+                      index: VisibleIndex = None, stream=None) -> torch.Tensor:
+    """Eq. 1 over one cached step; returns x0_out [B, N, H, W, C].  `index`
+    (gc_index_correspondence of corr) selects the split launch."""
     B, N, H, W, C = _latent_shape(x0_prev)
     arr, a = _anchors(anchors)
     if tuple(x0_anchor_new.shape) != (B, a, H, W, C) or x0_anchor_new.dtype != x0_prev.dtype:
@@ -239,7 +281,7 @@ def gc_transport_step(x0_prev: torch.Tensor, x0_anchor_new: torch.Tensor, corr: 
         x0_out = torch.empty_like(x0_prev)
     _check(lib().gc_transport_step(_dev(x0_prev, "x0_prev"), _dev(x0_anchor_new, "x0_anchor_new"),
                                    _dev(corr, "corr") if corr.numel() else None,
-                                   _dev(weights, "weights") if weights.numel() else None,
+                                   _dev(weights, "weights") if weights.numel() else None, *_index_args(index),
                                    B, N, H, W, C, arr, a, K, dtype_code(x0_prev), _dev(x0_out, "x0_out"),
                                    _stream(stream)), "gc_transport_step")
     return x0_out
@@ -265,8 +307,9 @@ def gc_sampler_reconstruct(x_t: torch.Tensor, x0: torch.Tensor, sampler: Sampler
 def gc_transport_reconstruct(x0_prev: torch.Tensor, x0_anchor_new: torch.Tensor, corr: torch.Tensor,
                              weights: torch.Tensor, x_t: torch.Tensor, anchors: Sequence[int], sampler: Sampler,
                              t: float, t_next: float, x0_out: torch.Tensor = None, x_next: torch.Tensor = None,
-                             model_out: torch.Tensor = None, stream=None):
-    """Fused Eq. 1 + reconstruction; returns (x0_out, x_next, model_out or None)."""
+                             model_out: torch.Tensor = None, index: VisibleIndex = None, stream=None):
+    """Fused Eq. 1 + reconstruction; returns (x0_out, x_next, model_out or None).
+    `index` (gc_index_correspondence of corr) selects the split launch."""
     B, N, H, W, C = _latent_shape(x0_prev)
     arr, a = _anchors(anchors)
     if tuple(x0_anchor_new.shape) != (B, a, H, W, C) or x0_anchor_new.dtype != x0_prev.dtype:
@@ -284,7 +327,8 @@ def gc_transport_reconstruct(x0_prev: torch.Tensor, x0_anchor_new: torch.Tensor,
     _check(lib().gc_transport_reconstruct(_dev(x0_prev, "x0_prev"), _dev(x0_anchor_new, "x0_anchor_new"),
                                           _dev(corr, "corr") if corr.numel() else None,
                                           _dev(weights, "weights") if weights.numel() else None,
-                                          _dev(x_t, "x_t"), B, N, H, W, C, arr, a, K, dtype_code(x0_prev),
+                                          *_index_args(index), _dev(x_t, "x_t"), B, N, H, W, C, arr, a, K,
+                                          dtype_code(x0_prev),
                                           ctypes.byref(smp), float(t), float(t_next), _dev(x0_out, "x0_out"),
                                           _dev(x_next, "x_next"), _opt(model_out, "model_out"), _stream(stream)),
            "gc_transport_reconstruct")
@@ -310,7 +354,7 @@ class BoundCall:
 def bind_transport_reconstruct(x0_prev: torch.Tensor, x0_anchor_new: torch.Tensor, corr: torch.Tensor,
                                weights: torch.Tensor, x_t: torch.Tensor, anchors: Sequence[int], sampler: Sampler,
                                x0_out: torch.Tensor, x_next: torch.Tensor, model_out: torch.Tensor = None,
-                               stream=None) -> BoundCall:
+                               index: VisibleIndex = None, stream=None) -> BoundCall:
     """Marshal gc_transport_reconstruct's buffer arguments once (same checks
     as gc_transport_reconstruct); the returned object takes (t, t_next).
     The tensors must stay alive and unmoved while the object is used."""
@@ -326,10 +370,10 @@ def bind_transport_reconstruct(x0_prev: torch.Tensor, x0_anchor_new: torch.Tenso
     K = weights.shape[-1]
     pre = (_dev(x0_prev, "x0_prev"), _dev(x0_anchor_new, "x0_anchor_new"),
            _dev(corr, "corr") if corr.numel() else None, _dev(weights, "weights") if weights.numel() else None,
-           _dev(x_t, "x_t"), B, N, H, W, C, arr, a, K, dtype_code(x0_prev))
+           *_index_args(index), _dev(x_t, "x_t"), B, N, H, W, C, arr, a, K, dtype_code(x0_prev))
     post = (_dev(x0_out, "x0_out"), _dev(x_next, "x_next"), _opt(model_out, "model_out"), _stream(stream))
     return BoundCall(lib().gc_transport_reconstruct, pre, sampler.c(), post,
-                     (x0_prev, x0_anchor_new, corr, weights, x_t, x0_out, x_next, model_out, arr))
+                     (x0_prev, x0_anchor_new, corr, weights, x_t, x0_out, x_next, model_out, arr, index))
 
 
 def gc_schedule_anchors(N: int, a: int, c: int) -> List[int]:

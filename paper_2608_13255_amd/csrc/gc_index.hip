@@ -1,0 +1,154 @@
+// Visible-token index of a correspondence operator (once per asset and
+// anchor set).
+//
+// G_{A->v} has a non-zero row only for tokens some anchor sees (Sec. 3.2:
+// rows with no in-tolerance tap are zero).  The per-step kernel splits its
+// work on that: blocks over a compact list of the visible tokens do the
+// gathers, and blocks over all tokens stream everything else, skipping
+// visible tokens by a one-bit-per-token mask instead of reading their words.
+//
+// Three passes, deterministic (the list is in ascending token order):
+//   count    per 1024-token chunk, visible tokens (ballot + popcount);
+//            also writes the bitmask (one 64-bit ballot per wave)
+//   scan     exclusive prefix over the chunk counts, total -> n_vis
+//   scatter  each chunk writes its visible tokens at its offset, ranked
+//            inside the chunk by (round, wave, mbcnt of the ballot)
+#include "gc_common.h"
+
+namespace gc {
+namespace {
+
+constexpr int kBlock = 256;
+constexpr int kRounds = 4;                 // tokens per block = kRounds * kBlock
+constexpr int kChunk = kRounds * kBlock;
+constexpr int kWaves = kBlock / 64;
+
+__device__ __forceinline__ bool token_visible(const int32_t* __restrict__ corr, int64_t tok, int64_t n_tokens,
+                                              int a) {
+  if (tok >= n_tokens) return false;
+  const int32_t* w = corr + tok * a;
+  if (a == 4) {
+    const int4 q = *reinterpret_cast<const int4*>(w);
+    return (q.x | q.y | q.z | q.w) != 0;
+  }
+  int32_t any = 0;
+  for (int s = 0; s < a; ++s) any |= w[s];
+  return any != 0;
+}
+
+__global__ __launch_bounds__(kBlock) void k_index_count(const int32_t* __restrict__ corr, int64_t n_tokens, int a,
+                                                        uint32_t* __restrict__ bits, int64_t n_words,
+                                                        int32_t* __restrict__ counts) {
+  __shared__ int32_t wave_cnt[kWaves];
+  const int wv = threadIdx.x / 64;
+  int32_t total = 0;
+  for (int r = 0; r < kRounds; ++r) {
+    const int64_t tok = (int64_t)blockIdx.x * kChunk + r * kBlock + threadIdx.x;
+    const unsigned long long m = __ballot(token_visible(corr, tok, n_tokens, a));
+    if (__lane_id() == 0) {
+      const int64_t w0 = ((int64_t)blockIdx.x * kChunk + r * kBlock + wv * 64) >> 5;
+      if (w0 < n_words) bits[w0] = (uint32_t)m;
+      if (w0 + 1 < n_words) bits[w0 + 1] = (uint32_t)(m >> 32);
+      wave_cnt[wv] = __popcll(m);
+    }
+    __syncthreads();
+    if (threadIdx.x == 0)
+      for (int w = 0; w < kWaves; ++w) total += wave_cnt[w];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) counts[blockIdx.x] = total;
+}
+
+// one block: exclusive scan of counts[n] into offsets[n], total into n_vis
+__global__ __launch_bounds__(kBlock) void k_index_scan(const int32_t* __restrict__ counts, int64_t n,
+                                                       int32_t* __restrict__ offsets, int32_t* __restrict__ n_vis) {
+  __shared__ int32_t buf[kBlock];
+  int32_t carry = 0;
+  for (int64_t base = 0; base < n; base += kBlock) {
+    const int64_t i = base + threadIdx.x;
+    const int32_t c = i < n ? counts[i] : 0;
+    buf[threadIdx.x] = c;
+    __syncthreads();
+    // inclusive Hillis-Steele scan over the block
+    for (int o = 1; o < kBlock; o <<= 1) {
+      const int32_t add = threadIdx.x >= o ? buf[threadIdx.x - o] : 0;
+      __syncthreads();
+      buf[threadIdx.x] += add;
+      __syncthreads();
+    }
+    if (i < n) offsets[i] = carry + buf[threadIdx.x] - c;
+    const int32_t block_total = buf[kBlock - 1];
+    __syncthreads();
+    carry += block_total;
+  }
+  if (threadIdx.x == 0) *n_vis = carry;
+}
+
+__global__ __launch_bounds__(kBlock) void k_index_scatter(const int32_t* __restrict__ corr, int64_t n_tokens, int a,
+                                                          const int32_t* __restrict__ offsets,
+                                                          int32_t* __restrict__ list) {
+  __shared__ int32_t wave_cnt[kWaves];
+  const int wv = threadIdx.x / 64;
+  int32_t pos = offsets[blockIdx.x];
+  for (int r = 0; r < kRounds; ++r) {
+    const int64_t tok = (int64_t)blockIdx.x * kChunk + r * kBlock + threadIdx.x;
+    const bool vis = token_visible(corr, tok, n_tokens, a);
+    const unsigned long long m = __ballot(vis);
+    if (__lane_id() == 0) wave_cnt[wv] = __popcll(m);
+    __syncthreads();
+    int32_t before = 0;
+    for (int w = 0; w < wv; ++w) before += wave_cnt[w];
+    const int32_t rank = (int32_t)__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
+                                                            __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+    if (vis) list[pos + before + rank] = (int32_t)tok;
+    int32_t round_total = 0;
+    for (int w = 0; w < kWaves; ++w) round_total += wave_cnt[w];
+    __syncthreads();
+    pos += round_total;
+  }
+}
+
+}  // namespace
+}  // namespace gc
+
+using namespace gc;
+
+extern "C" size_t gc_index_workspace_bytes(int64_t n_tokens) {
+  if (n_tokens <= 0) return 256;
+  const int64_t nb = (n_tokens + kChunk - 1) / kChunk;
+  return (size_t)(((2 * nb * 4) + 255) / 256 * 256);
+}
+
+extern "C" int gc_index_correspondence(const int32_t* corr, int64_t n_tokens, int a, uint32_t* vis_bits,
+                                       int32_t* vis_list, int32_t* n_vis, void* workspace, size_t workspace_bytes,
+                                       hipStream_t stream) {
+  clear_error();
+  if (!n_vis || !workspace) return fail(GC_ERR_ARG, "index: null n_vis or workspace");
+  if (n_tokens < 0) return fail(GC_ERR_SHAPE, "index: n_tokens=%lld is negative", (long long)n_tokens);
+  if (n_tokens > 0x7fffffffLL) return fail(GC_ERR_CAPACITY, "index: n_tokens=%lld exceeds 2^31-1", (long long)n_tokens);
+  if (a < 1 || a > GC_MAX_ANCHORS) return fail(GC_ERR_ARG, "index: a=%d outside [1, %d]", a, GC_MAX_ANCHORS);
+  if (n_tokens > 0 && (!corr || !vis_bits || !vis_list)) return fail(GC_ERR_ARG, "index: null pointer");
+  if ((corr && !aligned16(corr)) || (vis_bits && !aligned16(vis_bits)) || (vis_list && !aligned16(vis_list)) ||
+      !aligned16(workspace))
+    return fail(GC_ERR_ALIGN, "index: pointers must be 16-byte aligned");
+  if (workspace_bytes < gc_index_workspace_bytes(n_tokens))
+    return fail(GC_ERR_CAPACITY, "index: workspace of %zu bytes is below the %zu required", workspace_bytes,
+                gc_index_workspace_bytes(n_tokens));
+  const int64_t n_words = (n_tokens + 31) / 32;
+  const size_t nc = (size_t)n_tokens * a * 4, nl = (size_t)n_tokens * 4, nbits = (size_t)n_words * 4;
+  if (overlaps(vis_bits, nbits, corr, nc) || overlaps(vis_list, nl, corr, nc) || overlaps(vis_list, nl, vis_bits, nbits) ||
+      overlaps(n_vis, 4, vis_list, nl) || overlaps(n_vis, 4, vis_bits, nbits) || overlaps(workspace, workspace_bytes, corr, nc) ||
+      overlaps(workspace, workspace_bytes, vis_list, nl) || overlaps(workspace, workspace_bytes, vis_bits, nbits))
+    return fail(GC_ERR_ALIAS, "index: buffers overlap");
+  const int64_t nb = n_tokens > 0 ? (n_tokens + kChunk - 1) / kChunk : 0;
+  int32_t* counts = static_cast<int32_t*>(workspace);
+  int32_t* offsets = counts + nb;
+  if (nb > 0)
+    hipLaunchKernelGGL(k_index_count, dim3((unsigned)nb), dim3(kBlock), 0, stream, corr, n_tokens, a, vis_bits,
+                       n_words, counts);
+  hipLaunchKernelGGL(k_index_scan, dim3(1), dim3(kBlock), 0, stream, counts, nb, offsets, n_vis);
+  if (nb > 0)
+    hipLaunchKernelGGL(k_index_scatter, dim3((unsigned)nb), dim3(kBlock), 0, stream, corr, n_tokens, a, offsets,
+                       vis_list);
+  return after_launch(stream, "gc_index_correspondence");
+}

@@ -2,9 +2,9 @@
 // the per-asset bounding box / squared match tolerance.
 //
 // Both are HBM-streaming reductions (no contraction): each render sample is
-// read once.  The downsample keeps the mean exact-in-practice by summing in
-// double in the same order as a plain row-major loop (rows of the block, then
-// samples in a row), so its float result does not depend on the launch shape.
+// read once.  The downsample sums each block in double in the order of a
+// plain row-major loop (rows of the block, then samples in a row), whichever
+// kernel runs, so its float result does not depend on the launch shape.
 #include "gc_common.h"
 
 namespace gc {
@@ -13,8 +13,7 @@ namespace {
 constexpr int kBlock = 256;
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
-// One thread per latent pixel.  Rows of the f x f block are read as float4
-// groups of four samples (12 floats) when f is a multiple of 4.
+// One thread per latent pixel, reading its f x f block directly (any f).
 __global__ __launch_bounds__(kBlock) void k_downsample(const float* __restrict__ hi, int64_t n_pix,
                                                        int Hr, int Wr, int f, int H, int W,
                                                        float* __restrict__ lo) {
@@ -28,38 +27,92 @@ __global__ __launch_bounds__(kBlock) void k_downsample(const float* __restrict__
   double sx = 0.0, sy = 0.0, sz = 0.0;
   for (int dy = 0; dy < f; ++dy) {
     const float* row = hi + ((m * Hr + (int64_t)j * f + dy) * Wr + (int64_t)i * f) * 3;
-    if ((f & 3) == 0) {
-      const f32x4* r4 = reinterpret_cast<const f32x4*>(row);
-      for (int g = 0; g < f / 4; ++g) {
-        const f32x4 a = __builtin_nontemporal_load(r4 + 3 * g);
-        const f32x4 b = __builtin_nontemporal_load(r4 + 3 * g + 1);
-        const f32x4 c = __builtin_nontemporal_load(r4 + 3 * g + 2);
-        const float s[12] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w, c.x, c.y, c.z, c.w};
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const float x = s[3 * q], y = s[3 * q + 1], z = s[3 * q + 2];
-          if (finite_f(x) && finite_f(y) && finite_f(z)) {
-            n_fg += 1;
-            sx += (double)x;
-            sy += (double)y;
-            sz += (double)z;
-          }
-        }
-      }
-    } else {
-      for (int dx = 0; dx < f; ++dx) {
-        const float x = row[3 * dx], y = row[3 * dx + 1], z = row[3 * dx + 2];
-        if (finite_f(x) && finite_f(y) && finite_f(z)) {
-          n_fg += 1;
-          sx += (double)x;
-          sy += (double)y;
-          sz += (double)z;
-        }
+    for (int dx = 0; dx < f; ++dx) {
+      const float x = row[3 * dx], y = row[3 * dx + 1], z = row[3 * dx + 2];
+      if (finite_f(x) && finite_f(y) && finite_f(z)) {
+        n_fg += 1;
+        sx += (double)x;
+        sy += (double)y;
+        sz += (double)z;
       }
     }
   }
   float* o = lo + gid * 3;
   if (2 * n_fg < f * f) {
+    const float qnan = __uint_as_float(0x7fc00000u);
+    o[0] = qnan;
+    o[1] = qnan;
+    o[2] = qnan;
+  } else {
+    const double n = (double)n_fg;
+    o[0] = (float)(sx / n);
+    o[1] = (float)(sy / n);
+    o[2] = (float)(sz / n);
+  }
+}
+
+// Tiled variant for f = 8: a block handles kTilePix consecutive latent
+// pixels of one latent row.  All threads first copy the block's 8 render-row
+// segments into LDS with coalesced 16-byte loads (each segment is contiguous
+// in the render map); then one thread per latent pixel folds its 8 x 8
+// samples from LDS in the same row-major order as the direct kernel.
+constexpr int kTilePix = 64;
+constexpr int kTileF = 8;
+constexpr int kTileFloats = kTileF * kTilePix * kTileF * 3;   // 12288 floats = 48 KiB
+static_assert(kTileFloats % (4 * 256) == 0, "tile must split evenly over the block");
+
+__global__ __launch_bounds__(kBlock) void k_downsample_f8(const float* __restrict__ hi, int64_t n_maps, int Hr,
+                                                          int Wr, int H, int W, float* __restrict__ lo) {
+  __shared__ f32x4 tile[kTileFloats / 4];
+  const int tiles_per_row = (W + kTilePix - 1) / kTilePix;
+  const int64_t row_id = blockIdx.x / tiles_per_row;          // m * H + j
+  const int i0 = (int)(blockIdx.x - row_id * tiles_per_row) * kTilePix;
+  const int np = min(kTilePix, W - i0);                       // latent pixels in this tile
+  const int64_t m = row_id / H;
+  const int j = (int)(row_id - m * H);
+  const int seg4 = np * kTileF * 3 / 4;                       // float4s per render-row segment
+  constexpr int kPer = kTileFloats / 4 / kBlock;              // 12 float4 per thread for a full tile
+  f32x4 v[kPer];
+  // issue every load of the tile before the first LDS write
+#pragma unroll
+  for (int r = 0; r < kPer; ++r) {
+    const int q = threadIdx.x + r * kBlock;
+    if (q < kTileF * seg4) {
+      const int dy = q / seg4, c = q - dy * seg4;
+      const f32x4* src = reinterpret_cast<const f32x4*>(hi + ((m * Hr + (int64_t)j * kTileF + dy) * Wr +
+                                                              (int64_t)i0 * kTileF) * 3);
+      v[r] = __builtin_nontemporal_load(src + c);
+    }
+  }
+#pragma unroll
+  for (int r = 0; r < kPer; ++r) {
+    const int q = threadIdx.x + r * kBlock;
+    if (q < kTileF * seg4) {
+      const int dy = q / seg4, c = q - dy * seg4;
+      tile[dy * (kTilePix * kTileF * 3 / 4) + c] = v[r];
+    }
+  }
+  __syncthreads();
+  const int t = threadIdx.x;
+  if (t >= np) return;
+  const float* ts = reinterpret_cast<const float*>(tile);
+  int n_fg = 0;
+  double sx = 0.0, sy = 0.0, sz = 0.0;
+  for (int dy = 0; dy < kTileF; ++dy) {
+    const float* row = ts + dy * (kTilePix * kTileF * 3) + t * kTileF * 3;
+#pragma unroll
+    for (int dx = 0; dx < kTileF; ++dx) {
+      const float x = row[3 * dx], y = row[3 * dx + 1], z = row[3 * dx + 2];
+      if (finite_f(x) && finite_f(y) && finite_f(z)) {
+        n_fg += 1;
+        sx += (double)x;
+        sy += (double)y;
+        sz += (double)z;
+      }
+    }
+  }
+  float* o = lo + ((m * H + j) * (int64_t)W + i0 + t) * 3;
+  if (2 * n_fg < kTileF * kTileF) {
     const float qnan = __uint_as_float(0x7fc00000u);
     o[0] = qnan;
     o[1] = qnan;
@@ -102,10 +155,12 @@ __device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
   return v;
 }
 
-// grid (chunks, B): every thread folds a strided slice of asset b's samples,
-// the wave reduces with cross-lane shuffles and one lane issues the atomics.
+// grid (chunks, B): every thread folds a strided slice of asset b's samples;
+// waves reduce with cross-lane shuffles, the block through LDS, and one
+// thread per block issues the atomics.
 __global__ __launch_bounds__(kBlock) void k_bbox_accum(const float* __restrict__ pos, int64_t per_asset,
                                                        uint32_t* __restrict__ acc) {
+  __shared__ uint32_t part[kBlock / 64][7];
   const int b = blockIdx.y;
   const float* p = pos + (int64_t)b * per_asset * 3;
   uint32_t mn[3] = {0xFFFFFFFFu, 0xFFFFFFFFu, 0xFFFFFFFFu};
@@ -123,20 +178,38 @@ __global__ __launch_bounds__(kBlock) void k_bbox_accum(const float* __restrict__
       mx[c] = max(mx[c], e[c]);
     }
   }
-  const unsigned long long seen = __ballot(any);
+  const uint32_t seen = __ballot(any) ? 1u : 0u;
 #pragma unroll
   for (int c = 0; c < 3; ++c) {
     mn[c] = wave_min_u32(mn[c]);
     mx[c] = wave_max_u32(mx[c]);
   }
-  if (seen && __lane_id() == 0) {
-    uint32_t* a = acc + (int64_t)b * 8;
-#pragma unroll
+  const int wv = threadIdx.x / 64;
+  if (__lane_id() == 0) {
     for (int c = 0; c < 3; ++c) {
-      atomicMin(a + c, mn[c]);
-      atomicMax(a + 3 + c, mx[c]);
+      part[wv][c] = mn[c];
+      part[wv][3 + c] = mx[c];
     }
-    atomicOr(a + 7, 1u);
+    part[wv][6] = seen;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint32_t bmn[3] = {0xFFFFFFFFu, 0xFFFFFFFFu, 0xFFFFFFFFu}, bmx[3] = {0u, 0u, 0u}, bseen = 0u;
+    for (int w = 0; w < kBlock / 64; ++w) {
+      for (int c = 0; c < 3; ++c) {
+        bmn[c] = min(bmn[c], part[w][c]);
+        bmx[c] = max(bmx[c], part[w][3 + c]);
+      }
+      bseen |= part[w][6];
+    }
+    if (bseen) {
+      uint32_t* a = acc + (int64_t)b * 8;
+      for (int c = 0; c < 3; ++c) {
+        atomicMin(a + c, bmn[c]);
+        atomicMax(a + 3 + c, bmx[c]);
+      }
+      atomicOr(a + 7, 1u);
+    }
   }
 }
 
@@ -188,8 +261,15 @@ extern "C" int gc_posmap_downsample(const float* pos_hi, int64_t n_maps, int Hr,
   if (n_pix == 0) return GC_OK;
   const int64_t blocks = (n_pix + kBlock - 1) / kBlock;
   if (blocks > 0x7fffffff) return fail(GC_ERR_CAPACITY, "downsample: too many latent pixels");
-  hipLaunchKernelGGL(k_downsample, dim3((unsigned)blocks), dim3(kBlock), 0, stream, pos_hi, n_pix, Hr, Wr, f, H,
-                     W, pos_lat);
+  if (f == kTileF) {
+    const int64_t tblocks = n_maps * H * (int64_t)((W + kTilePix - 1) / kTilePix);
+    if (tblocks > 0x7fffffff) return fail(GC_ERR_CAPACITY, "downsample: too many latent rows");
+    hipLaunchKernelGGL(k_downsample_f8, dim3((unsigned)tblocks), dim3(kBlock), 0, stream, pos_hi, n_maps, Hr, Wr, H,
+                       W, pos_lat);
+  } else {
+    hipLaunchKernelGGL(k_downsample, dim3((unsigned)blocks), dim3(kBlock), 0, stream, pos_hi, n_pix, Hr, Wr, f, H,
+                       W, pos_lat);
+  }
   return after_launch(stream, "gc_posmap_downsample");
 }
 
@@ -205,8 +285,10 @@ extern "C" int gc_posmap_bbox(const float* pos, int B, int N, int H, int W, floa
   if (overlaps(pos, (size_t)B * per * 12, bbox, (size_t)B * 32)) return fail(GC_ERR_ALIAS, "bbox: output overlaps input");
   uint32_t* acc = reinterpret_cast<uint32_t*>(bbox);
   hipLaunchKernelGGL(k_bbox_init, dim3((B + 63) / 64), dim3(64), 0, stream, acc, B);
-  int64_t chunks = (per + 4 * kBlock - 1) / (4 * kBlock);
-  if (chunks > 1024) chunks = 1024;
+  // enough blocks to stream the maps, few enough that the per-block atomics
+  // on the asset's eight words stay cheap
+  int64_t chunks = (per + 16 * kBlock - 1) / (16 * kBlock);
+  if (chunks > 256) chunks = 256;
   if (chunks < 1) chunks = 1;
   hipLaunchKernelGGL(k_bbox_accum, dim3((unsigned)chunks, B), dim3(kBlock), 0, stream, pos, per, acc);
   hipLaunchKernelGGL(k_bbox_final, dim3((B + 63) / 64), dim3(64), 0, stream, acc, B, tol_frac);

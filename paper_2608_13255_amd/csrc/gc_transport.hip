@@ -96,14 +96,18 @@ struct TArgs {
   int bpv;             // blocks per view: ceil(HW * CV / kBlock)
   int n_blocks;        // logical blocks = B * N * bpv (before XCD padding)
   int remap;           // 1: XCD-contiguous block order
-  int8_t slot_of_view[GC_MAX_VIEWS];    // anchor slot of view v, or -1
-  int8_t tslot_of_view[GC_MAX_VIEWS];   // target slot of view v, or -1
-  int32_t anchor_view[GC_MAX_ANCHORS];
+  int32_t anchor_view[GC_MAX_ANCHORS];   // view of anchor slot s
+  // optional visible-token index (gc_index_correspondence): split launch
+  const uint32_t* vis_bits;
+  const int32_t* vis_list;
+  int64_t n_tokens;    // B * NT * HW
+  int n_vis;
+  int gblocks;         // gather blocks in front of the streaming blocks (multiple of kXcds)
+  int32_t sorted_anchor[GC_MAX_ANCHORS];  // anchor views ascending, padded with INT_MAX
   Recon r;
 };
 
-__device__ __forceinline__ int logical_block(int n_blocks, int remap) {
-  const int i = blockIdx.x;
+__device__ __forceinline__ int logical_block(int i, int n_blocks, int remap) {
   if (!remap) return i;
   const int per = (n_blocks + kXcds - 1) / kXcds;   // grid is padded to kXcds * per
   return (i % kXcds) * per + i / kXcds;
@@ -129,42 +133,30 @@ __device__ __forceinline__ void reconstruct_vec(const Recon& r, const float (&xt
   }
 }
 
+// What the caller of token_step knows about a target token.
+enum TokenMode { kAnchorRow = 0, kTargetCheck = 1, kTargetSeen = 2, kTargetUnseen = 3 };
+
+// One cached step for one (token, channel vector): Eq. 1 for a target token
+// (or the copy for an anchor row), then, when fused, the reconstruction.
 template <int DT, int VEC, bool FUSED>
-__global__ __launch_bounds__(kBlock) void k_transport(TArgs g) {
+__device__ __forceinline__ void token_step(const TArgs& g, int b, int p, int cv, int s_self, int64_t crow,
+                                           int64_t base, TokenMode mode) {
   using CD = Codec<DT, VEC>;
   using Raw = typename CD::Raw;
-  // Blocks never straddle a view, so the (asset, view) split is block-uniform
-  // scalar work and only the chunk -> (token, channel vector) split is per lane.
-  const int lb = logical_block(g.n_blocks, g.remap);
-  if (lb >= g.n_blocks) return;
-  const int bv = lb / g.bpv;                   // b * N + v
-  const int t = (lb - bv * g.bpv) * kBlock + (int)threadIdx.x;
-  if (t >= g.HW * g.CV) return;
-  const int b = bv / g.N;
-  const int v = bv - b * g.N;
-  int p, cv;
-  if (g.cv_shift >= 0) {
-    p = t >> g.cv_shift;
-    cv = t & (g.CV - 1);
-  } else {
-    p = t / g.CV;
-    cv = t - p * g.CV;
-  }
-  const int64_t pix = (int64_t)bv * g.HW + p;
-  const int64_t base = pix * g.C + (int64_t)cv * VEC;
-  const int s_self = g.slot_of_view[v];
-
+  // issue every load of data this thread owns before using any of it
   Raw xtr;
-  if constexpr (FUSED) xtr = CD::load_stream(g.x_t, base);   // independent of the transport: issue first
+  if constexpr (FUSED) xtr = CD::load_stream(g.x_t, base);
   Raw x0r;
   float x0f[VEC];
-  if (s_self >= 0) {
+  if (mode == kAnchorRow) {
     // anchor row: the store keeps this step's prediction
     x0r = CD::load(g.x0_new, (((int64_t)b * g.a + s_self) * g.HW + p) * g.C + (int64_t)cv * VEC);
     CD::unpack(x0r, x0f);
+  } else if (mode == kTargetUnseen) {
+    x0r = CD::load_stream(g.x0_prev, base);   // no anchor sees this token: it keeps its own state
+    CD::unpack(x0r, x0f);
   } else {
-    const int ti = g.tslot_of_view[v];
-    const int64_t crow = ((int64_t)b * g.NT + ti) * g.HW + p;
+    const Raw prevr = CD::load_stream(g.x0_prev, base);
     const int32_t* cw = g.corr + crow * g.a;
     int32_t words[GC_MAX_ANCHORS];
     if (g.a == 4) {   // the common layout: one 16-byte load (rows are 16-byte aligned)
@@ -182,9 +174,8 @@ __global__ __launch_bounds__(kBlock) void k_transport(TArgs g) {
     bool any = false;
 #pragma unroll
     for (int s = 0; s < GC_MAX_ANCHORS; ++s) any |= words[s] != 0;
-    const Raw prevr = CD::load_stream(g.x0_prev, base);
     if (!any) {
-      x0r = prevr;   // no anchor sees this token: it keeps its own state
+      x0r = prevr;
       CD::unpack(x0r, x0f);
     } else {
       float prevf[VEC], acc[VEC];
@@ -205,10 +196,10 @@ __global__ __launch_bounds__(kBlock) void k_transport(TArgs g) {
         int j = 0;
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
-          if (!(mask & (1u << k))) continue;
           // words come from the caller: taps off the grid or beyond K are ignored
           const int x = x0 + (k & 1), y = y0 + (k >> 1);
-          if (j >= g.K || x < 0 || x >= g.W || y < 0 || y >= g.H) continue;
+          const bool on = (mask & (1u << k)) && j < g.K && x >= 0 && x < g.W && y >= 0 && y < g.H;
+          if (!on) continue;
           const int q = y * g.W + x;
           const float wt = ws[j++];
           float nf[VEC], of[VEC];
@@ -235,6 +226,83 @@ __global__ __launch_bounds__(kBlock) void k_transport(TArgs g) {
   }
 }
 
+// Dense launch: blocks tile every (asset, view) in order.  Split launch (with
+// a visible-token index): the first g.gblocks blocks each take a slice of the
+// visible-token list and do all the gathering; the remaining blocks stream
+// every other token, skipping the visible ones by their bit.  Gather blocks go
+// first so that their dependent-load latency overlaps the streaming.
+template <int DT, int VEC, bool FUSED, bool SPLIT>
+__global__ __launch_bounds__(kBlock) void k_transport(TArgs g) {
+  int i = blockIdx.x;
+  if constexpr (SPLIT) {
+    if (i < g.gblocks) {
+      const int per = g.gblocks / kXcds;           // XCD-contiguous slices of the list
+      const int lb = (i % kXcds) * per + i / kXcds;
+      const int e = lb * kBlock + (int)threadIdx.x;
+      if (e >= g.n_vis * g.CV) return;
+      int le, cv;
+      if (g.cv_shift >= 0) {
+        le = e >> g.cv_shift;
+        cv = e & (g.CV - 1);
+      } else {
+        le = e / g.CV;
+        cv = e - le * g.CV;
+      }
+      const int tok = g.vis_list[le];
+      if (tok < 0 || (int64_t)tok >= g.n_tokens) return;   // list entries come from the caller
+      const int bt = tok / g.HW;
+      const int p = tok - bt * g.HW;
+      const int b = bt / g.NT;
+      int v = bt - b * g.NT;                        // target slot -> view
+#pragma unroll
+      for (int s = 0; s < GC_MAX_ANCHORS; ++s) v += g.sorted_anchor[s] <= v ? 1 : 0;
+      const int64_t base = (((int64_t)b * g.N + v) * g.HW + p) * g.C + (int64_t)cv * VEC;
+      token_step<DT, VEC, FUSED>(g, b, p, cv, -1, tok, base, kTargetSeen);
+      return;
+    }
+    i -= g.gblocks;
+  }
+  // Blocks never straddle a view, so the (asset, view) split and the view's
+  // role (anchor slot or target slot) are wave-uniform scalar values; only
+  // the chunk -> (token, channel vector) split is per lane.
+  const int lb = logical_block(i, g.n_blocks, g.remap);
+  if (lb >= g.n_blocks) return;
+  const int bv = __builtin_amdgcn_readfirstlane(lb / g.bpv);   // b * N + v
+  const int t = (lb - bv * g.bpv) * kBlock + (int)threadIdx.x;
+  if (t >= g.HW * g.CV) return;
+  const int b = __builtin_amdgcn_readfirstlane(bv / g.N);
+  const int v = bv - b * g.N;
+  int s_self = -1, n_before = 0;
+#pragma unroll
+  for (int s = 0; s < GC_MAX_ANCHORS; ++s) {
+    if (s < g.a) {
+      const int u = g.anchor_view[s];
+      s_self = u == v ? s : s_self;
+      n_before += u < v;
+    }
+  }
+  int p, cv;
+  if (g.cv_shift >= 0) {
+    p = t >> g.cv_shift;
+    cv = t & (g.CV - 1);
+  } else {
+    p = t / g.CV;
+    cv = t - p * g.CV;
+  }
+  const int64_t base = ((int64_t)bv * g.HW + p) * g.C + (int64_t)cv * VEC;
+  if (s_self >= 0) {
+    token_step<DT, VEC, FUSED>(g, b, p, cv, s_self, 0, base, kAnchorRow);
+    return;
+  }
+  const int64_t crow = ((int64_t)b * g.NT + (v - n_before)) * g.HW + p;
+  if constexpr (SPLIT) {
+    if ((g.vis_bits[crow >> 5] >> (crow & 31)) & 1u) return;   // a gather block owns this token
+    token_step<DT, VEC, FUSED>(g, b, p, cv, -1, crow, base, kTargetUnseen);
+  } else {
+    token_step<DT, VEC, FUSED>(g, b, p, cv, -1, crow, base, kTargetCheck);
+  }
+}
+
 template <int DT, int VEC>
 __global__ __launch_bounds__(kBlock) void k_reconstruct(const void* __restrict__ x_t, const void* __restrict__ x0,
                                                         void* x_next, void* __restrict__ model_out, int64_t n_vec,
@@ -254,9 +322,10 @@ int pick_vec(int dtype, int64_t c) { return dtype == GC_F32 ? 4 : (c % 8 == 0 ? 
 
 // Validation shared by the transport entry points; fills g (except the
 // reconstruction coefficients and the fused-only pointers).
-int prepare_transport(const void* x0_prev, const void* x0_new, const int32_t* corr, const float* weights, int B,
-                      int N, int H, int W, int C, const int32_t* anchors, int a, int K, int dtype, void* x0_out,
-                      const char* who, TArgs* g) {
+int prepare_transport(const void* x0_prev, const void* x0_new, const int32_t* corr, const float* weights,
+                      const uint32_t* vis_bits, const int32_t* vis_list, int64_t n_vis, int B, int N, int H, int W,
+                      int C, const int32_t* anchors, int a, int K, int dtype, void* x0_out, const char* who,
+                      TArgs* g) {
   if (!x0_prev || !x0_new || !anchors || !x0_out) return fail(GC_ERR_ARG, "%s: null pointer", who);
   if (dtype != GC_F32 && dtype != GC_BF16) return fail(GC_ERR_DTYPE, "%s: unknown dtype %d", who, dtype);
   if (B < 1 || N < 1 || H < 1 || W < 1 || C < 1)
@@ -274,17 +343,14 @@ int prepare_transport(const void* x0_prev, const void* x0_new, const int32_t* co
       (weights && !aligned16(weights)))
     return fail(GC_ERR_ALIGN, "%s: device pointers must be 16-byte aligned", who);
   std::memset(g, 0, sizeof(*g));
-  for (int v = 0; v < GC_MAX_VIEWS; ++v) g->slot_of_view[v] = g->tslot_of_view[v] = -1;
+  bool is_anchor[GC_MAX_VIEWS] = {};
   for (int s = 0; s < a; ++s) {
     const int u = anchors[s];
     if (u < 0 || u >= N) return fail(GC_ERR_ARG, "%s: anchor %d outside [0, %d)", who, u, N);
-    if (g->slot_of_view[u] >= 0) return fail(GC_ERR_ARG, "%s: anchor %d listed twice", who, u);
-    g->slot_of_view[u] = (int8_t)s;
+    if (is_anchor[u]) return fail(GC_ERR_ARG, "%s: anchor %d listed twice", who, u);
+    is_anchor[u] = true;
     g->anchor_view[s] = u;
   }
-  int t = 0;
-  for (int v = 0; v < N; ++v)
-    if (g->slot_of_view[v] < 0) g->tslot_of_view[v] = (int8_t)t++;
   const size_t es = (size_t)dtype_bytes(dtype);
   const size_t HW = (size_t)H * W;
   const size_t n_all = (size_t)B * N * HW * C * es, n_new = (size_t)B * a * HW * C * es;
@@ -314,20 +380,59 @@ int prepare_transport(const void* x0_prev, const void* x0_new, const int32_t* co
   if (nb > (int64_t)0x7fffffff - kXcds) return fail(GC_ERR_CAPACITY, "%s: problem too large for one launch", who);
   g->n_blocks = (int)nb;
   g->remap = 1;
+  // optional visible-token index
+  if ((vis_bits == nullptr) != (vis_list == nullptr))
+    return fail(GC_ERR_ARG, "%s: vis_bits and vis_list must both be given or both be null", who);
+  g->n_tokens = (int64_t)B * NT * (int64_t)HW;
+  if (vis_bits) {
+    if (g->n_tokens > 0x7fffffffLL) return fail(GC_ERR_CAPACITY, "%s: too many target tokens for an index", who);
+    if (n_vis < 0 || n_vis > g->n_tokens)
+      return fail(GC_ERR_ARG, "%s: n_vis=%lld outside [0, %lld]", who, (long long)n_vis, (long long)g->n_tokens);
+    if (!aligned16(vis_bits) || !aligned16(vis_list)) return fail(GC_ERR_ALIGN, "%s: index pointers must be 16-byte aligned", who);
+    if (overlaps(x0_out, n_all, vis_bits, (size_t)(g->n_tokens + 31) / 32 * 4) ||
+        overlaps(x0_out, n_all, vis_list, (size_t)n_vis * 4))
+      return fail(GC_ERR_ALIAS, "%s: x0_out overlaps the index", who);
+    g->vis_bits = vis_bits;
+    g->vis_list = vis_list;
+    g->n_vis = (int)n_vis;
+    const int64_t gb = ((int64_t)n_vis * g->CV + kBlock - 1) / kBlock;
+    g->gblocks = (int)((gb + kXcds - 1) / kXcds * kXcds);
+    if ((int64_t)g->gblocks + nb > (int64_t)0x7fffffff - kXcds)
+      return fail(GC_ERR_CAPACITY, "%s: problem too large for one launch", who);
+  }
+  int sorted[GC_MAX_ANCHORS];
+  for (int s = 0; s < a; ++s) sorted[s] = anchors[s];
+  for (int s = 1; s < a; ++s)
+    for (int r = s; r > 0 && sorted[r - 1] > sorted[r]; --r) {
+      const int tmp = sorted[r];
+      sorted[r] = sorted[r - 1];
+      sorted[r - 1] = tmp;
+    }
+  for (int s = 0; s < GC_MAX_ANCHORS; ++s) g->sorted_anchor[s] = s < a ? sorted[s] : 0x7fffffff;
   return GC_OK;
 }
 
 template <bool FUSED>
 void launch_transport(const TArgs& g, int dtype, hipStream_t stream) {
   const int per = (g.n_blocks + kXcds - 1) / kXcds;
-  const dim3 grid(g.remap ? (unsigned)(per * kXcds) : (unsigned)g.n_blocks);
+  const unsigned stream_blocks = g.remap ? (unsigned)(per * kXcds) : (unsigned)g.n_blocks;
+  const bool split = g.vis_bits != nullptr;
+  const dim3 grid(stream_blocks + (split ? (unsigned)g.gblocks : 0u));
   const int vec = g.C / g.CV;
+#define GC_LAUNCH(DT_, VEC_)                                                                        \
+  do {                                                                                              \
+    if (split)                                                                                      \
+      hipLaunchKernelGGL((k_transport<DT_, VEC_, FUSED, true>), grid, dim3(kBlock), 0, stream, g);  \
+    else                                                                                            \
+      hipLaunchKernelGGL((k_transport<DT_, VEC_, FUSED, false>), grid, dim3(kBlock), 0, stream, g); \
+  } while (0)
   if (dtype == GC_F32)
-    hipLaunchKernelGGL((k_transport<GC_F32, 4, FUSED>), grid, dim3(kBlock), 0, stream, g);
+    GC_LAUNCH(GC_F32, 4);
   else if (vec == 8)
-    hipLaunchKernelGGL((k_transport<GC_BF16, 8, FUSED>), grid, dim3(kBlock), 0, stream, g);
+    GC_LAUNCH(GC_BF16, 8);
   else
-    hipLaunchKernelGGL((k_transport<GC_BF16, 4, FUSED>), grid, dim3(kBlock), 0, stream, g);
+    GC_LAUNCH(GC_BF16, 4);
+#undef GC_LAUNCH
 }
 
 }  // namespace
@@ -336,12 +441,13 @@ void launch_transport(const TArgs& g, int dtype, hipStream_t stream) {
 using namespace gc;
 
 extern "C" int gc_transport_step(const void* x0_prev, const void* x0_anchor_new, const int32_t* corr,
-                                 const float* weights, int B, int N, int H, int W, int C, const int32_t* anchors,
-                                 int a, int K, int dtype, void* x0_out, hipStream_t stream) {
+                                 const float* weights, const uint32_t* vis_bits, const int32_t* vis_list,
+                                 int64_t n_vis, int B, int N, int H, int W, int C, const int32_t* anchors, int a,
+                                 int K, int dtype, void* x0_out, hipStream_t stream) {
   clear_error();
   TArgs g;
-  int rc = prepare_transport(x0_prev, x0_anchor_new, corr, weights, B, N, H, W, C, anchors, a, K, dtype, x0_out,
-                             "gc_transport_step", &g);
+  int rc = prepare_transport(x0_prev, x0_anchor_new, corr, weights, vis_bits, vis_list, n_vis, B, N, H, W, C,
+                             anchors, a, K, dtype, x0_out, "gc_transport_step", &g);
   if (rc) return rc;
   if (g.n_threads == 0) return GC_OK;
   launch_transport<false>(g, dtype, stream);
@@ -385,14 +491,15 @@ extern "C" int gc_sampler_reconstruct(const void* x_t, const void* x0, void* x_n
 }
 
 extern "C" int gc_transport_reconstruct(const void* x0_prev, const void* x0_anchor_new, const int32_t* corr,
-                                        const float* weights, const void* x_t, int B, int N, int H, int W, int C,
+                                        const float* weights, const uint32_t* vis_bits, const int32_t* vis_list,
+                                        int64_t n_vis, const void* x_t, int B, int N, int H, int W, int C,
                                         const int32_t* anchors, int a, int K, int dtype, const gc_sampler* smp,
                                         double t, double t_next, void* x0_out, void* x_next, void* model_out,
                                         hipStream_t stream) {
   clear_error();
   TArgs g;
-  int rc = prepare_transport(x0_prev, x0_anchor_new, corr, weights, B, N, H, W, C, anchors, a, K, dtype, x0_out,
-                             "gc_transport_reconstruct", &g);
+  int rc = prepare_transport(x0_prev, x0_anchor_new, corr, weights, vis_bits, vis_list, n_vis, B, N, H, W, C,
+                             anchors, a, K, dtype, x0_out, "gc_transport_reconstruct", &g);
   if (rc) return rc;
   if (!x_t || !x_next) return fail(GC_ERR_ARG, "gc_transport_reconstruct: null x_t or x_next");
   rc = make_recon(smp, t, t_next, &g.r);

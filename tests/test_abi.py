@@ -26,7 +26,7 @@ A0, A1, A2, A3, A4, A5 = (0x10000000 * (i + 1) for i in range(6))
 def header_functions():
     src = open(HEADER).read()
     src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
-    return sorted(set(re.findall(r"^\s*(?:int|const char\*)\s+(gc_\w+)\s*\(", src, flags=re.M)))
+    return sorted(set(re.findall(r"^\s*(?:int|size_t|const char\*)\s+(gc_\w+)\s*\(", src, flags=re.M)))
 
 
 @pytest.fixture(scope="module")
@@ -63,8 +63,9 @@ def _err(L):
 def test_transport_validation(gc, L):
     anchors = (ctypes.c_int32 * 2)(0, 3)
 
-    def call(x0_prev=A0, new=A1, corr=A2, w=A3, B=1, N=6, H=8, W=8, C=16, anc=anchors, a=2, K=4, dt=1, out=A4):
-        return L.gc_transport_step(x0_prev, new, corr, w, B, N, H, W, C, anc, a, K, dt, out, None)
+    def call(x0_prev=A0, new=A1, corr=A2, w=A3, B=1, N=6, H=8, W=8, C=16, anc=anchors, a=2, K=4, dt=1, out=A4,
+             bits=None, lst=None, nv=0):
+        return L.gc_transport_step(x0_prev, new, corr, w, bits, lst, nv, B, N, H, W, C, anc, a, K, dt, out, None)
 
     assert call(x0_prev=None) == -1 and "null" in _err(L)
     assert call(a=0) == -1
@@ -85,6 +86,10 @@ def test_transport_validation(gc, L):
     assert call(corr=None) == -1               # targets exist, so the operator is required
     nine = (ctypes.c_int32 * 9)(*range(9))
     assert call(anc=nine, a=9, N=12) == -6
+    assert call(bits=A5) == -1                  # an index needs both the bits and the list
+    assert call(bits=A5, lst=A5 + 4096, nv=-1) == -1
+    assert call(bits=A5, lst=A5 + 4096, nv=1 * 4 * 64 + 1) == -1   # more visible tokens than targets
+    assert call(bits=A5 + 4, lst=A5 + 4096, nv=3) == -4
 
 
 def test_fused_validation(gc, L):
@@ -93,8 +98,8 @@ def test_fused_validation(gc, L):
     n = 1 * 6 * 8 * 8 * 16 * 2
 
     def call(xt=A5, smpp=ctypes.byref(smp), t=0.5, tn=0.4, out=A4, xn=A5 + n, mo=None):
-        return L.gc_transport_reconstruct(A0, A1, A2, A3, xt, 1, 6, 8, 8, 16, anchors, 2, 4, 1, smpp, t, tn,
-                                          out, xn, mo, None)
+        return L.gc_transport_reconstruct(A0, A1, A2, A3, None, None, 0, xt, 1, 6, 8, 8, 16, anchors, 2, 4, 1,
+                                          smpp, t, tn, out, xn, mo, None)
 
     assert call(t=0.0) == -1                   # sigma_t must be > 0
     assert call(tn=0.6) == -1                  # sigma_next must not exceed sigma_t
@@ -121,6 +126,12 @@ def test_reconstruct_and_build_validation(gc, L):
     assert L.gc_posmap_downsample(A0, 2, 32, 32, 8, A0 + 64, None) == -5
     assert L.gc_posmap_bbox(A0, 1, 4, 8, 8, 0.0, A1, None) == -1
     assert L.gc_posmap_bbox(A0, 1, 4, 8, 8, 0.01, A1 + 4, None) == -4
+    need = L.gc_index_workspace_bytes(1 << 20)
+    assert need >= 2 * 4 * 1024 and need % 256 == 0
+    assert L.gc_index_correspondence(A0, 1 << 20, 4, A1, A2, A3, A4, need - 1, None) == -6
+    assert L.gc_index_correspondence(A0, 1 << 20, 9, A1, A2, A3, A4, need, None) == -1
+    assert L.gc_index_correspondence(A0, 1 << 20, 4, A1, A0 + 64, A3, A4, need, None) == -5
+    assert L.gc_index_correspondence(A0, -1, 4, A1, A2, A3, A4, need, None) == -2
 
 
 def test_host_schedule_matches_oracle(gc):

@@ -373,3 +373,90 @@ def test_k1_transport_and_channel_widths(gc):
             corr, wts = _gpu_build(gc, w, P, A, K)
             x0_out = gc.gc_transport_step(to_dev(o["x0_prev"], dtype), to_dev(o["x0_new"], dtype), corr, wts, A)
             _check_x0(w, A, o, to_host(x0_out, dtype))
+
+
+# ---------------------------------------------------------------------------
+# visible-token index and the split launch
+# ---------------------------------------------------------------------------
+
+def _expected_index(corr_o):
+    a = corr_o.shape[-1]
+    vis = (corr_o.reshape(-1, a) != 0).any(-1)
+    n = vis.size
+    words = np.zeros((n + 31) // 32, np.uint32)
+    for i in np.flatnonzero(vis):
+        words[i >> 5] |= np.uint32(1) << np.uint32(i & 31)
+    return words, np.flatnonzero(vis).astype(np.int32)
+
+
+def _check_index(idx, corr_o):
+    words, lst = _expected_index(corr_o)
+    assert idx.n_vis == lst.size
+    np.testing.assert_array_equal(idx.vis_bits.cpu().numpy().view(np.uint32)[:words.size], words)
+    np.testing.assert_array_equal(idx.vis_list.cpu().numpy()[:lst.size], lst)
+
+
+@pytest.mark.parametrize("w", ALL, ids=lambda w: w.name)
+def test_index_parity(gc, w):
+    P = latent_maps(w.name)
+    for c in (0, 1):
+        A = anchors_of(w, c)
+        corr_o, _, _ = oracle.build(P, synth.batch_cameras(w), A, w.K, oracle.bbox(P, w.tol_frac))
+        corr, _ = _gpu_build(gc, w, P, A, w.K)
+        _check_index(gc.gc_index_correspondence(corr), corr_o)
+        if w.fixed_anchors:
+            break
+
+
+def test_index_edges(gc):
+    rs = np.random.default_rng(4)
+    for shape, density in [((1, 1, 3, 7, 3), 0.5), ((2, 3, 17, 33, 4), 0.3), ((1, 2, 40, 40, 2), 0.0),
+                           ((1, 5, 64, 64, 4), 1.0), ((3, 1, 11, 13, 5), 0.05)]:
+        corr_o = np.where(rs.random(shape) < density, rs.integers(1, 2 ** 28, size=shape), 0).astype(np.int32)
+        idx = gc.gc_index_correspondence(torch.from_numpy(corr_o).to(DEV))
+        _check_index(idx, corr_o)
+    empty = torch.empty((1, 0, 8, 8, 4), dtype=torch.int32, device=DEV)
+    assert gc.gc_index_correspondence(empty).n_vis == 0
+
+
+@pytest.mark.parametrize("w", ALL, ids=lambda w: w.name)
+def test_split_launch_equals_dense_and_oracle(gc, w):
+    P = latent_maps(w.name)
+    A = anchors_of(w, 1)
+    k = 4 if w.S > 4 else 0
+    o = _oracle_step(w, P, A, k)
+    corr, wts = _gpu_build(gc, w, P, A, o["K"])
+    idx = gc.gc_index_correspondence(corr)
+    smp = sampler_of(gc, w)
+    prev, new, xt = (to_dev(o[n], w.dtype) for n in ("x0_prev", "x0_new", "x_t"))
+    iv = torch.int16 if w.dtype == "bf16" else torch.int32
+    x0_d = gc.gc_transport_step(prev, new, corr, wts, A)
+    x0_s = gc.gc_transport_step(prev, new, corr, wts, A, index=idx)
+    assert torch.equal(x0_d.view(iv), x0_s.view(iv))
+    _check_x0(w, A, o, to_host(x0_s, w.dtype))
+    d = gc.gc_transport_reconstruct(prev, new, corr, wts, xt, A, smp, o["t"], o["tn"])
+    s_ = gc.gc_transport_reconstruct(prev, new, corr, wts, xt, A, smp, o["t"], o["tn"], index=idx)
+    for a_, b_ in zip(d, s_):
+        assert torch.equal(a_.view(iv), b_.view(iv))
+    assert torch.equal(s_[0].view(iv), x0_s.view(iv))
+    xn = synth.values(to_host(s_[1], w.dtype), w.dtype).astype(np.float64)
+    assert np.abs(xn - o["xn"]).max() <= TOL[w.dtype]
+
+
+def test_split_launch_without_visible_tokens(gc):
+    """An operator no anchor contributes to: the split launch has no gather
+    blocks and every target keeps its state."""
+    w = C2
+    P = latent_maps(w.name)
+    A = anchors_of(w, 0)
+    x0_prev, x0_new, x_t = latents(w, P, A, 2)
+    corr = torch.zeros((1, w.N - w.a, w.H, w.W, w.a), dtype=torch.int32, device=DEV)
+    wts = torch.zeros((1, w.N - w.a, w.H, w.W, w.a, 4), dtype=torch.float32, device=DEV)
+    idx = gc.gc_index_correspondence(corr)
+    assert idx.n_vis == 0
+    out = gc.gc_transport_step(to_dev(x0_prev, "f32"), to_dev(x0_new, "f32"), corr, wts, A, index=idx)
+    got = out.cpu().numpy()
+    targets = [v for v in range(w.N) if v not in A]
+    np.testing.assert_array_equal(got[:, targets], x0_prev[:, targets])
+    for s, u in enumerate(A):
+        np.testing.assert_array_equal(got[:, u], x0_new[:, s])
