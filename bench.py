@@ -44,6 +44,7 @@ def parse():
     ap.add_argument("--copy-probe", action="store_true",
                     help="also run a plain 1 GiB device copy (reference kernel for counter scaling)")
     ap.add_argument("--quiet", action="store_true")
+    ap.add_argument("--no-small", action="store_true", help="skip the launch-bound small-workload row")
     return ap.parse_args()
 
 
@@ -263,6 +264,11 @@ def main():
         rows["copy_1GiB_GBps"] = copy_gbps
         del src, dst
 
+    # ---- launch-bound small workloads: eager vs HIP-graph replay -------------
+    if not args.no_small:
+        for name in ("tiny_sphere_4v_32", "hunyuan_torus_6v_64"):
+            rows[f"small_{name}"] = small_workload(gc, synth, name)
+
     # ---- CPU baseline: the oracle on one asset ------------------------------
     cpu = None
     if not args.no_cpu_baseline:
@@ -293,6 +299,66 @@ def main():
         "rows": rows,
     }
     print(json.dumps(out), flush=True)
+
+
+def small_workload(gc, synth, name, steps=300):
+    """One cached step of a small workload, launched eagerly and replayed from
+    a HIP graph (the launch-bound regime): microseconds per step each way."""
+    import torch
+    w = synth.CONFIGS[name]
+    dev = torch.device("cuda:0")
+    hi = torch.from_numpy(synth.render_position_maps(w)).to(dev)
+    pos = gc.gc_posmap_downsample(hi, w.factor) if w.factor > 1 else hi
+    cams = gc.camera_tensor(synth.batch_cameras(w), dev)
+    bbox = gc.gc_posmap_bbox(pos, w.tol_frac)
+    tdt = torch.float32 if w.dtype == "f32" else torch.bfloat16
+    if w.fixed_anchors:
+        sets = [list(w.fixed_anchors)]
+    else:
+        sets = []
+        for c in range(w.N):
+            A = gc.gc_schedule_anchors(w.N, w.a, c)
+            if A not in sets:
+                sets.append(A)
+    smp = gc.Sampler(kind=gc.GC_DDIM if w.sampler == "ddim" else gc.GC_FLOW_EULER)
+    t, tn = w.ddim_single if w.ddim_single else gc.gc_sampler_step_times(smp, w.S, 2)
+    g = torch.Generator(device=dev).manual_seed(0)
+    shape = (w.B, w.N, w.H, w.W, w.C)
+    x0 = torch.randn(shape, generator=g, device=dev).to(tdt)
+    xt = torch.randn(shape, generator=g, device=dev).to(tdt)
+    s = torch.cuda.Stream()
+    calls = []
+    for A in sets:
+        corr, wts = gc.gc_build_correspondence(pos, cams, A, w.K, bbox)
+        idx = gc.gc_index_correspondence(corr)
+        new = torch.randn((w.B, len(A), w.H, w.W, w.C), generator=g, device=dev).to(tdt)
+        calls.append(gc.bind_transport_reconstruct(x0, new, corr, wts, xt, A, smp, torch.empty_like(x0),
+                                                   torch.empty_like(x0), index=idx, stream=s))
+    torch.cuda.synchronize()
+    reps = max(1, steps // len(calls))
+
+    def timed(fn, n):
+        fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(s)
+        for _ in range(n):
+            fn()
+        e1.record(s)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / n
+
+    def eager():
+        for c in calls:
+            c(t, tn)
+    eager_ms = timed(eager, reps) / len(calls)
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=s):
+        eager()
+    graph_ms = timed(graph.replay, reps) / len(calls)
+    V = w.B * (w.N - len(sets[0])) * w.H * w.W
+    return {"view_pixels_per_step": V, "eager_us_per_step": eager_ms * 1e3, "graph_us_per_step": graph_ms * 1e3,
+            "graph_view_pixels_per_s": V / (graph_ms * 1e-3)}
 
 
 def cpu_baseline(w, pos1, cams_np, x0_prev1, seconds):

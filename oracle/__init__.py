@@ -237,7 +237,9 @@ def trajectory(x_t0: np.ndarray, stub, pos: np.ndarray, cams, K: int, tol_frac: 
     the stored x0 is transported to the other views, and every view is then
     reconstructed.  x0(t) of all N views becomes the next reference.
 
-    Returns the list of per-step records (x_t, x0 state, anchors)."""
+    Returns the list of per-step records: anchors, the cached-step counter c
+    after the step, the stored x_t and x0 (storage dtype) and their unrounded
+    double values x_t_exact and x0_exact."""
     steps = S if steps is None else steps
     B, N = pos.shape[0], pos.shape[1]
     bb = bbox(pos, tol_frac)
@@ -251,6 +253,7 @@ def trajectory(x_t0: np.ndarray, stub, pos: np.ndarray, cams, K: int, tol_frac: 
         if full[k] or x0_store is None:
             x0_new = stub(k, list(range(N)))
             x0_state = x0_new
+            x0_exact = (x0_new if dtype == "f32" else _bf16_values(x0_new)).astype(np.float64)
             A = list(range(N))
         else:
             A = anchors(N, a, c)
@@ -260,9 +263,14 @@ def trajectory(x_t0: np.ndarray, stub, pos: np.ndarray, cams, K: int, tol_frac: 
                 corr, w, _ = build(pos, cams, A, K, bb)
                 cache[key] = (corr, w)
             corr, w = cache[key]
-            _, x0_state = transport(x0_store, stub(k, A), corr, w, A, dtype)
+            x0_exact, x0_state = transport(x0_store, stub(k, A), corr, w, A, dtype)
         xn, _ = reconstruct(x_t, x0_state, dtype, kind, t, tn)
         x_t = store(xn, dtype)
         x0_store = x0_state
-        out.append({"k": k, "anchors": A, "x_t": x_t, "x0": x0_state})
+        out.append({"k": k, "anchors": A, "c": c, "x_t": x_t, "x0": x0_state, "x_t_exact": xn,
+                    "x0_exact": x0_exact})
     return out
+
+
+def _bf16_values(bits: np.ndarray) -> np.ndarray:
+    return (np.asarray(bits, np.uint16).astype(np.uint32) << 16).view(np.float32)

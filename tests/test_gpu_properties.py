@@ -1,0 +1,147 @@
+"""Property-based parity (hypothesis): random small problems -- grid sizes
+that are not multiples of anything, 2-7 views, 1-4 anchors, K = 1..4, C = 4..16,
+float32 / bfloat16, orthographic or pinhole rigs with random poses (points
+behind a pinhole camera included), random background holes and tolerances --
+through the whole per-step path against the oracle, plus HIP-graph replays.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+from hypothesis import HealthCheck, given, settings, strategies as st
+
+import oracle
+import synth
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda:0"
+TOL = {"f32": 1e-5, "bf16": 2e-2}
+
+
+def to_dev(arr, dtype):
+    if dtype == "f32":
+        return torch.from_numpy(np.ascontiguousarray(arr)).to(DEV)
+    return torch.from_numpy(np.ascontiguousarray(arr).view(np.int16)).to(DEV).view(torch.bfloat16)
+
+
+def to_host(t, dtype):
+    return t.cpu().numpy() if dtype == "f32" else t.view(torch.int16).cpu().numpy().view(np.uint16)
+
+
+def random_rig(rs, N, H, W, pinhole):
+    cams = {"model": np.full(N, 0 if pinhole else 1, np.int32), "R": np.zeros((N, 3, 3), np.float32),
+            "t": np.zeros((N, 3), np.float32), "fx": np.zeros(N, np.float32), "fy": np.zeros(N, np.float32),
+            "cx": np.full(N, W / 2, np.float32), "cy": np.full(N, H / 2, np.float32)}
+    for v in range(N):
+        az, el = rs.uniform(0, 360), rs.uniform(-40, 40)
+        dist = rs.uniform(1.2, 4.0) if pinhole else 3.0      # pinhole rigs may sit inside the bound
+        R, t = synth.look_at_origin(az, el, dist)
+        if pinhole and rs.random() < 0.25:
+            F = np.diag([-1.0, 1.0, -1.0])        # turned away: the object is behind this camera
+            R, t = F @ R, F @ t
+        cams["R"][v], cams["t"][v] = R, t
+        if pinhole:
+            f = (W / 2) / math.tan(math.radians(rs.uniform(30, 60) / 2))
+            cams["fx"][v], cams["fy"][v] = f, f * H / W * rs.uniform(0.8, 1.2)
+        else:
+            cams["fx"][v], cams["fy"][v] = W / 2.4, H / 2.4
+    return cams
+
+
+@settings(max_examples=30, deadline=None, derandomize=True, suppress_health_check=list(HealthCheck))
+@given(seed=st.integers(0, 2 ** 31 - 1), H=st.integers(1, 40), W=st.integers(1, 40), N=st.integers(2, 7),
+       a_frac=st.floats(0.0, 1.0), K=st.integers(1, 4), C=st.sampled_from([4, 8, 12, 16]),
+       dtype=st.sampled_from(["f32", "bf16"]), pinhole=st.booleans(), tol=st.sampled_from([0.01, 0.03, 0.1]),
+       holes=st.floats(0.0, 0.3), sampler=st.sampled_from(["ddim", "flow"]))
+def test_random_problems_match_oracle(seed, H, W, N, a_frac, K, C, dtype, pinhole, tol, holes, sampler):
+    import paper_2608_13255_amd as gc
+    rs = np.random.default_rng(seed)
+    a = 1 + int(a_frac * (min(N, 4) - 1) + 0.5)
+    anchors = sorted(rs.choice(N, size=a, replace=False).tolist())
+    cams = random_rig(rs, N, H, W, pinhole)
+    prm = synth.sphere_params(synth.CONFIGS["tiny_sphere_4v_32"], int(seed % 7))
+    P = synth.raycast_radial(0.05, prm, cams, H, W)[None]
+    P[0][rs.random((N, H, W)) < holes] = np.nan
+    bcams = {k: v[None] for k, v in cams.items()}
+    bb = oracle.bbox(P, tol)
+    corr_o, wts_o, nvis_o = oracle.build(P, bcams, anchors, K, bb)
+    prev = synth.storage(rs.standard_normal((1, N, H, W, C)).astype(np.float32), dtype)
+    new = synth.storage(synth.values(prev, dtype)[:, anchors] + 0.1 * rs.standard_normal((1, a, H, W, C)).astype(np.float32), dtype)
+    xt = synth.storage(rs.standard_normal((1, N, H, W, C)).astype(np.float32), dtype)
+    if sampler == "ddim":
+        t, tn = int(rs.integers(1, 999)), None
+        tn = int(rs.integers(-1, t))
+        smp, pred = gc.Sampler(kind=gc.GC_DDIM, pred_out=gc.GC_PRED_EPS), "eps"
+        cond = max(1.0, 1 / math.sqrt(1 - oracle.alpha_bar(t)))
+    else:
+        t = float(rs.uniform(0.05, 1.0))
+        tn = float(rs.uniform(0.0, t))
+        smp, pred = gc.Sampler(kind=gc.GC_FLOW_EULER, pred_out=gc.GC_PRED_VEL), "vel"
+        cond = max(1.0, 1 / t)
+    x0_exact, x0_state = oracle.transport(prev, new, corr_o, wts_o, anchors, dtype)
+    xn_o, mo_o = oracle.reconstruct(xt, x0_state, dtype, sampler, t, tn, pred=pred)
+
+    Pd = torch.from_numpy(P).to(DEV)
+    bbd = gc.gc_posmap_bbox(Pd, tol)
+    np.testing.assert_array_equal(bbd.cpu().numpy()[:, 6].view(np.uint32), bb[:, 6].view(np.uint32))
+    corr, wts = gc.gc_build_correspondence(Pd, gc.camera_tensor(bcams, DEV), anchors, K, bbd)
+    np.testing.assert_array_equal(corr.cpu().numpy(), corr_o)
+    assert np.abs(wts.cpu().numpy() - wts_o).max(initial=0.0) <= 1e-6
+    idx = gc.gc_index_correspondence(corr)
+    assert idx.n_vis == int((nvis_o > 0).sum())
+    for index in (None, idx):
+        x0_out, x_next, mo = gc.gc_transport_reconstruct(to_dev(prev, dtype), to_dev(new, dtype), corr, wts,
+                                                         to_dev(xt, dtype), anchors, smp, t, tn, index=index)
+        x0h = to_host(x0_out, dtype)
+        assert np.abs(synth.values(x0h, dtype).astype(np.float64) - x0_exact).max() <= TOL[dtype]
+        assert np.abs(synth.values(to_host(x_next, dtype), dtype).astype(np.float64) - xn_o).max() <= TOL[dtype]
+        same = np.ones(x0h.shape, bool) if dtype == "f32" else (x0h == x0_state)
+        err = np.abs(synth.values(to_host(mo, dtype), dtype).astype(np.float64) - mo_o)[same]
+        assert err.max(initial=0.0) <= TOL[dtype] * cond
+
+
+def test_graph_replays_match_eager():
+    """Fused steps captured in a HIP graph and replayed several times, with
+    eager work and synchronisations between replays: every replay equals the
+    eager result bit for bit."""
+    import paper_2608_13255_amd as gc
+    from conftest import latent_maps
+    from synth.configs import C2
+    w = C2
+    P = torch.from_numpy(latent_maps(w.name)).to(DEV)
+    cams = gc.camera_tensor(synth.batch_cameras(w), DEV)
+    bb = gc.gc_posmap_bbox(P)
+    rs = np.random.default_rng(0)
+    sets = [gc.gc_schedule_anchors(w.N, w.a, c) for c in range(3)]
+    ops = {tuple(A): gc.gc_build_correspondence(P, cams, A, w.K, bb) for A in sets}
+    idx = {A: gc.gc_index_correspondence(ops[A][0]) for A in ops}
+    x0 = torch.from_numpy(rs.standard_normal((1, w.N, w.H, w.W, w.C)).astype(np.float32)).to(DEV)
+    news = [torch.from_numpy(rs.standard_normal((1, w.a, w.H, w.W, w.C)).astype(np.float32)).to(DEV) for _ in sets]
+    xt = torch.from_numpy(rs.standard_normal((1, w.N, w.H, w.W, w.C)).astype(np.float32)).to(DEV)
+    smp = gc.Sampler(kind=gc.GC_DDIM)
+    outs = [(torch.empty_like(x0), torch.empty_like(x0)) for _ in sets]
+    s = torch.cuda.Stream()
+    calls = [gc.bind_transport_reconstruct(x0, news[i], *ops[tuple(A)], xt, A, smp, outs[i][0], outs[i][1],
+                                           index=idx[tuple(A)], stream=s) for i, A in enumerate(sets)]
+    times = [(966, 932), (932, 899), (899, 866)]
+    with torch.cuda.stream(s):
+        for c, (t, tn) in zip(calls, times):
+            c(t, tn)
+    torch.cuda.synchronize()
+    eager = [(o.clone(), n.clone()) for o, n in outs]
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=s):
+        for c, (t, tn) in zip(calls, times):
+            c(t, tn)
+    for rep in range(4):
+        for o, n in outs:
+            o.fill_(float("nan"))
+            n.zero_()
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for (o, n), (eo, en) in zip(outs, eager):
+            assert torch.equal(o.view(torch.int32), eo.view(torch.int32)), rep
+            assert torch.equal(n.view(torch.int32), en.view(torch.int32)), rep
+        _ = (x0 * 2).sum().item()          # eager work between replays
