@@ -2,16 +2,14 @@
 // for one anchor set (once per asset and anchor set; the rotation has only a
 // few distinct sets, so the host caches one build per set).
 //
-// One thread per target token.  For each anchor the thread projects the
-// token's 3D point, tests the 2x2 footprint taps against the tolerance,
-// keeps the K nearest, forms the area weights and finally divides by the
-// number of anchors that see the token.  Every float operation is written in
-// a fixed order and the library is compiled without contraction, so the
-// tap choice (an integer decision taken in float) is reproducible exactly.
+// Every float operation is written in a fixed order and the library is
+// compiled without contraction, so the tap choice (an integer decision taken
+// in float) is reproducible exactly.
 //
-// Coverage statistics are reduced with wavefront ballots: each wave counts
-// its visible pairs / pixels / taps with a ballot + popcount and one lane
-// adds them to the asset's counters.
+// Visibility reductions use wavefront ballots: the anchors that see a token
+// are counted by a ballot over its lane group, and each wave counts its
+// visible pairs / tokens / taps with ballot + popcount before one lane adds
+// them to the asset's counters.
 #include "gc_common.h"
 
 namespace gc {
@@ -45,20 +43,33 @@ __device__ __forceinline__ uint32_t wave_sum(uint32_t v) {
   return v;
 }
 
-// grid: x = pixel blocks, y = b * NT + target slot.
+// One lane per (target token, anchor slot): a group of G = 4 or 8 adjacent
+// lanes serves one token (lanes with slot >= a idle).  Each lane projects the
+// token into its own anchor, tests the four footprint taps, keeps the K
+// nearest and forms that anchor's normalised area weights; the number of
+// anchors that see the token (n_vis) is a ballot over the lane group.  Words
+// and weights of one token are adjacent, so a group writes them coalesced.
+// grid: x = token blocks, y = b * NT + target slot; the block's anchor
+// cameras are staged in LDS.
+template <int G>
 __global__ __launch_bounds__(kBlock) void k_build(BuildArgs g) {
+  __shared__ gc_camera cam_lds[GC_MAX_ANCHORS];
   const int HW = g.H * g.W;
-  const int p = blockIdx.x * kBlock + threadIdx.x;
   const int bt = blockIdx.y;
   const int b = bt / g.NT;
   const int ti = bt - b * g.NT;
   const int v = g.target_view[ti];
-  const bool live = p < HW;
+  if (threadIdx.x < g.a) cam_lds[threadIdx.x] = g.cams[(int64_t)b * g.N + g.anchor_view[threadIdx.x]];
+  __syncthreads();
+
+  const int s = threadIdx.x & (G - 1);                   // anchor slot of this lane
+  const int p = blockIdx.x * (kBlock / G) + threadIdx.x / G;
+  const bool live = p < HW && s < g.a;
   const float tol2 = g.bbox[(int64_t)b * 8 + 6];
 
   float P[3] = {0.f, 0.f, 0.f};
   bool fg = false;
-  if (live) {
+  if (p < HW) {
     const float* pp = g.pos + (((int64_t)b * g.N + v) * HW + p) * 3;
     P[0] = pp[0];
     P[1] = pp[1];
@@ -66,137 +77,158 @@ __global__ __launch_bounds__(kBlock) void k_build(BuildArgs g) {
     fg = finite_f(P[0]) && finite_f(P[1]) && finite_f(P[2]);
   }
 
-  int32_t words[GC_MAX_ANCHORS];
-  float wts[GC_MAX_ANCHORS][4];   // per-anchor normalised weights by tap k
-  int n_vis = 0;
-  int n_taps = 0;
-  for (int s = 0; s < g.a; ++s) {
-    words[s] = 0;
-    for (int k = 0; k < 4; ++k) wts[s][k] = 0.0f;
-    if (!fg) continue;
+  int32_t word = 0;
+  float wk[4] = {0.f, 0.f, 0.f, 0.f};   // this anchor's normalised weight of tap k
+  int mask = 0;
+  if (live && fg) {
+    const gc_camera& cam = cam_lds[s];
     const int u = g.anchor_view[s];
-    const gc_camera cam = g.cams[(int64_t)b * g.N + u];
     const float* R = cam.R;
     const float xc = ((R[0] * P[0] + R[1] * P[1]) + R[2] * P[2]) + cam.t[0];
     const float yc = ((R[3] * P[0] + R[4] * P[1]) + R[5] * P[2]) + cam.t[1];
     const float zc = ((R[6] * P[0] + R[7] * P[1]) + R[8] * P[2]) + cam.t[2];
-    float px, py;
+    float px = 0.f, py = 0.f;
+    bool ok = true;
     if (cam.model == 0) {
-      if (!(zc > 0.0f)) continue;
-      px = cam.fx * (xc / zc) + cam.cx;
-      py = cam.fy * (yc / zc) + cam.cy;
+      ok = zc > 0.0f;
+      if (ok) {
+        px = cam.fx * (xc / zc) + cam.cx;
+        py = cam.fy * (yc / zc) + cam.cy;
+      }
     } else if (cam.model == 1) {
       px = cam.fx * xc + cam.cx;
       py = cam.fy * yc + cam.cy;
     } else {
-      continue;
+      ok = false;
     }
-    if (!(finite_f(px) && finite_f(py))) continue;
-    if (px < -2.0f || px > (float)g.W + 2.0f || py < -2.0f || py > (float)g.H + 2.0f) continue;
-    const float gx = px - 0.5f, gy = py - 0.5f;
-    const float fx0 = floorf(gx), fy0 = floorf(gy);
-    const float ax = gx - fx0, ay = gy - fy0;
-    const int x0 = (int)fx0, y0 = (int)fy0;
-    const float* src = g.pos + ((int64_t)b * g.N + u) * HW * 3;
-    bool valid[4];
-    float d2[4];
-    int nvalid = 0;
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      const int x = x0 + (k & 1), y = y0 + (k >> 1);
-      valid[k] = false;
-      d2[k] = 0.0f;
-      if (x < 0 || x >= g.W || y < 0 || y >= g.H) continue;
-      const float* Q = src + ((int64_t)y * g.W + x) * 3;
-      const float qx = Q[0], qy = Q[1], qz = Q[2];
-      if (!(finite_f(qx) && finite_f(qy) && finite_f(qz))) continue;
-      const float dx = qx - P[0], dy = qy - P[1], dz = qz - P[2];
-      const float dd = (dx * dx + dy * dy) + dz * dz;
-      if (!(dd <= tol2)) continue;
-      valid[k] = true;
-      d2[k] = dd;
-      ++nvalid;
-    }
-    if (nvalid == 0) continue;
-    bool sel[4] = {false, false, false, false};
-    if (nvalid <= g.K) {
-#pragma unroll
-      for (int k = 0; k < 4; ++k) sel[k] = valid[k];
-    } else {
-      for (int r = 0; r < g.K; ++r) {
-        int best = -1;
-#pragma unroll
-        for (int k = 0; k < 4; ++k) {
-          if (!valid[k] || sel[k]) continue;
-          if (best < 0 || d2[k] < d2[best]) best = k;
-        }
-        sel[best] = true;
-      }
-    }
-    const float wx[2] = {1.0f - ax, ax};
-    const float wy[2] = {1.0f - ay, ay};
-    float area[4];
-    float S = 0.0f;
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      area[k] = sel[k] ? wx[k & 1] * wy[k >> 1] : 0.0f;
-      S = S + area[k];
-    }
-    int mask = 0;
-    if (S > 0.0f) {
+    ok = ok && finite_f(px) && finite_f(py) && !(px < -2.0f || px > (float)g.W + 2.0f || py < -2.0f ||
+                                                  py > (float)g.H + 2.0f);
+    if (ok) {
+      const float gx = px - 0.5f, gy = py - 0.5f;
+      const float fx0 = floorf(gx), fy0 = floorf(gy);
+      const float ax = gx - fx0, ay = gy - fy0;
+      const int x0 = (int)fx0, y0 = (int)fy0;
+      const float* src = g.pos + ((int64_t)b * g.N + u) * HW * 3;
+      bool valid[4];
+      float d2[4];
+      int nvalid = 0;
 #pragma unroll
       for (int k = 0; k < 4; ++k) {
-        if (sel[k] && area[k] > 0.0f) {
-          wts[s][k] = area[k] / S;
-          mask |= 1 << k;
-        }
+        const int x = x0 + (k & 1), y = y0 + (k >> 1);
+        valid[k] = false;
+        d2[k] = 0.0f;
+        if (x < 0 || x >= g.W || y < 0 || y >= g.H) continue;
+        const float* Q = src + ((int64_t)y * g.W + x) * 3;
+        const float qx = Q[0], qy = Q[1], qz = Q[2];
+        if (!(finite_f(qx) && finite_f(qy) && finite_f(qz))) continue;
+        const float dx = qx - P[0], dy = qy - P[1], dz = qz - P[2];
+        const float dd = (dx * dx + dy * dy) + dz * dz;
+        if (!(dd <= tol2)) continue;
+        valid[k] = true;
+        d2[k] = dd;
+        ++nvalid;
       }
-    } else {
-      int best = -1;
+      if (nvalid > 0) {
+        bool sel[4] = {false, false, false, false};
+        if (nvalid <= g.K) {
 #pragma unroll
-      for (int k = 0; k < 4; ++k)
-        if (sel[k] && (best < 0 || d2[k] < d2[best])) best = k;
-      wts[s][best] = 1.0f;
-      mask = 1 << best;
+          for (int k = 0; k < 4; ++k) sel[k] = valid[k];
+        } else {
+          for (int r = 0; r < g.K; ++r) {
+            int best = -1;
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+              if (!valid[k] || sel[k]) continue;
+              if (best < 0 || d2[k] < d2[best]) best = k;
+            }
+            sel[best] = true;
+          }
+        }
+        const float wx[2] = {1.0f - ax, ax};
+        const float wy[2] = {1.0f - ay, ay};
+        float area[4];
+        float S = 0.0f;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          area[k] = sel[k] ? wx[k & 1] * wy[k >> 1] : 0.0f;
+          S = S + area[k];
+        }
+        if (S > 0.0f) {
+#pragma unroll
+          for (int k = 0; k < 4; ++k) {
+            if (sel[k] && area[k] > 0.0f) {
+              wk[k] = area[k] / S;
+              mask |= 1 << k;
+            }
+          }
+        } else {
+          int best = -1;
+#pragma unroll
+          for (int k = 0; k < 4; ++k)
+            if (sel[k] && (best < 0 || d2[k] < d2[best])) best = k;
+#pragma unroll
+          for (int k = 0; k < 4; ++k) wk[k] = k == best ? 1.0f : 0.0f;
+          mask = 1 << best;
+        }
+        word = (int32_t)((uint32_t)(x0 + 1) | ((uint32_t)(y0 + 1) << 12) | ((uint32_t)mask << 24));
+      }
     }
-    ++n_vis;
-    n_taps += __popc(mask);
-    words[s] = (int32_t)((uint32_t)(x0 + 1) | ((uint32_t)(y0 + 1) << 12) | ((uint32_t)mask << 24));
   }
+
+  // n_vis: anchors of this token that see it -- a ballot over the lane group
+  const unsigned long long seen = __ballot(word != 0);
+  const int lane = __lane_id();
+  const int gbase = lane & ~(G - 1);
+  const int n_vis = __popcll((seen >> gbase) & ((G == 64) ? ~0ull : ((1ull << G) - 1)));
 
   if (live) {
     const int64_t row = ((int64_t)b * g.NT + ti) * HW + p;
-    int32_t* cw = g.corr + row * g.a;
-    float* ww = g.weights + row * g.a * g.K;
+    g.corr[row * g.a + s] = word;
+    float out[4] = {0.f, 0.f, 0.f, 0.f};
     const float inv = n_vis > 0 ? (float)n_vis : 1.0f;
-    for (int s = 0; s < g.a; ++s) {
-      cw[s] = words[s];
-      const int mask = (int)(((uint32_t)words[s] >> 24) & 0xFu);
-      int j = 0;
+    int j = 0;
 #pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        if (mask & (1 << k)) {
-          ww[s * g.K + j] = wts[s][k] / inv;
-          ++j;
-        }
+    for (int k = 0; k < 4; ++k) {
+      if (mask & (1 << k)) {
+        // j-th kept tap -> slot j
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          if (q == j) out[q] = wk[k] / inv;
+        ++j;
       }
-      for (; j < g.K; ++j) ww[s * g.K + j] = 0.0f;
+    }
+    float* ww = g.weights + (row * g.a + s) * g.K;
+    if (g.K == 4) {   // 16-byte aligned: the weights base is, and each (token, slot) row is 16 bytes
+      *reinterpret_cast<float4*>(ww) = make_float4(out[0], out[1], out[2], out[3]);
+    } else {
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        if (q < g.K) ww[q] = out[q];
     }
   }
 
   if (g.stats) {
-    // blocks never straddle assets (grid y is per asset and target), so every
-    // lane of a wave adds to the same counters
-    const uint32_t c_pairs = wave_sum((uint32_t)n_vis);
-    const uint32_t c_pix = wave_count(live && n_vis > 0);
-    const uint32_t c_fg = wave_count(live && fg);
-    const uint32_t c_taps = wave_sum((uint32_t)n_taps);
-    if (__lane_id() == 0 && (c_pairs | c_pix | c_fg | c_taps)) {
-      uint32_t* st = g.stats + (int64_t)b * 4;
-      atomicAdd(st + 0, c_pairs);
-      atomicAdd(st + 1, c_pix);
-      atomicAdd(st + 2, c_fg);
-      atomicAdd(st + 3, c_taps);
+    // blocks never straddle assets (grid y is per asset and target): waves
+    // count with ballots, the block sums in LDS, one thread adds to the
+    // asset's counters
+    __shared__ uint32_t part[kBlock / 64][4];
+    const uint32_t c_pairs = (uint32_t)__popcll(seen);
+    const bool lead = (threadIdx.x & (G - 1)) == 0 && p < HW;
+    const uint32_t c_pix = wave_count(lead && n_vis > 0);
+    const uint32_t c_fg = wave_count(lead && fg);
+    const uint32_t c_taps = wave_sum(live ? (uint32_t)__popc(mask) : 0u);
+    const int wv = threadIdx.x / 64;
+    if (__lane_id() == 0) {
+      part[wv][0] = c_pairs;
+      part[wv][1] = c_pix;
+      part[wv][2] = c_fg;
+      part[wv][3] = c_taps;
+    }
+    __syncthreads();
+    if (threadIdx.x < 4) {
+      uint32_t sum = 0;
+      for (int w = 0; w < kBlock / 64; ++w) sum += part[w][threadIdx.x];
+      if (sum) atomicAdd(g.stats + (int64_t)b * 4 + threadIdx.x, sum);
     }
   }
 }
@@ -254,8 +286,13 @@ extern "C" int gc_build_correspondence(const float* pos, const gc_camera* cams, 
   g.NT = NT;
   if (stats) hipLaunchKernelGGL(k_zero_u32, dim3((4 * B + 255) / 256), dim3(256), 0, stream, stats, 4 * B);
   if (NT > 0) {
-    const unsigned bx = (unsigned)((HW + kBlock - 1) / kBlock);
-    hipLaunchKernelGGL(k_build, dim3(bx, B * NT), dim3(kBlock), 0, stream, g);
+    if (a <= 4) {
+      const unsigned bx = (unsigned)((HW + kBlock / 4 - 1) / (kBlock / 4));
+      hipLaunchKernelGGL(k_build<4>, dim3(bx, B * NT), dim3(kBlock), 0, stream, g);
+    } else {
+      const unsigned bx = (unsigned)((HW + kBlock / 8 - 1) / (kBlock / 8));
+      hipLaunchKernelGGL(k_build<8>, dim3(bx, B * NT), dim3(kBlock), 0, stream, g);
+    }
   }
   return after_launch(stream, "gc_build_correspondence");
 }
