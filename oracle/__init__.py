@@ -61,6 +61,11 @@ def lib():
         L.orc_full_steps.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, _u8p]
         L.orc_ddim_timesteps.argtypes = [ctypes.c_int, ctypes.c_int, _i32p]
         L.orc_store.argtypes = [_f64p, ctypes.c_int64, ctypes.c_int, _vp]
+        L.orc_unipc_coeffs.argtypes = [ctypes.c_int, ctypes.c_double, ctypes.c_double, _i32p, ctypes.c_int,
+                                       ctypes.c_int, ctypes.c_int, ctypes.c_int, _f64p]
+        L.orc_unipc_coeffs.restype = ctypes.c_int
+        L.orc_unipc_apply.argtypes = [_vp, _vp, _vp, _vp, _vp, ctypes.c_int64, ctypes.c_int, _f64p, _f64p, _f64p]
+        L.orc_unipc_apply.restype = ctypes.c_int
         for f in ("orc_downsample", "orc_bbox", "orc_build", "orc_transport", "orc_reconstruct",
                   "orc_anchors", "orc_full_steps", "orc_ddim_timesteps", "orc_store"):
             getattr(L, f).restype = ctypes.c_int
@@ -191,6 +196,31 @@ def alpha_bar(t: int, T: int = 1000, beta_start: float = 1e-4, beta_end: float =
     return lib().orc_alpha_bar(T, beta_start, beta_end, int(t))
 
 
+def unipc_coeffs(S: int, k: int, order: int = 2, corrector: bool = True, T: int = 1000,
+                 beta_start: float = 1e-4, beta_end: float = 0.02) -> np.ndarray:
+    """Coefficients of UniPC step k of an S-step trailing-timestep trajectory
+    (see oracle.c O8): [use_corrector, pc, pp, c_xprev, c_mk2, c_mk1, c_mk,
+    p_xc, p_mk1, p_mk]."""
+    ts = np.ascontiguousarray(ddim_timesteps(S, T), np.int32)
+    c = np.zeros(10, np.float64)
+    _check(lib().orc_unipc_coeffs(T, beta_start, beta_end, _p(ts, _i32p), S, k, order, int(corrector),
+                                  _p(c, _f64p)), "unipc_coeffs")
+    return c
+
+
+def unipc_apply(coeffs: np.ndarray, x_cur, x_prev, m_km2, m_km1, m_k, dtype: str):
+    """One UniPC update in double; returns (x_c, x_next) float64."""
+    sd = _storage_dtype(dtype)
+    arrs = [None if a is None else np.ascontiguousarray(a, sd) for a in (x_cur, x_prev, m_km2, m_km1, m_k)]
+    n = arrs[4].size
+    xc = np.empty(arrs[4].shape, np.float64)
+    xn = np.empty(arrs[4].shape, np.float64)
+    c = np.ascontiguousarray(coeffs, np.float64)
+    _check(lib().orc_unipc_apply(*[None if a is None else a.ctypes.data for a in arrs], n, DTYPES[dtype],
+                                 _p(c, _f64p), _p(xc, _f64p), _p(xn, _f64p)), "unipc_apply")
+    return xc, xn
+
+
 # --------------------------------------------------------------------------
 # schedule
 # --------------------------------------------------------------------------
@@ -269,6 +299,44 @@ def trajectory(x_t0: np.ndarray, stub, pos: np.ndarray, cams, K: int, tol_frac: 
         x0_store = x0_state
         out.append({"k": k, "anchors": A, "c": c, "x_t": x_t, "x0": x0_state, "x_t_exact": xn,
                     "x0_exact": x0_exact})
+    return out
+
+
+def trajectory_unipc(x_t0: np.ndarray, stub, pos: np.ndarray, cams, K: int, tol_frac: float, dtype: str, S: int,
+                     full: Sequence[int], a: int, order: int = 2, corrector: bool = True, steps: int = None):
+    """The cached loop with a UniPC data-prediction solver (see oracle.c O8):
+    the x0 store is the solver's history.  Per step: x0 of every view (from
+    the stub at a full step, by Eq. 1 at a cached step), then the UniPC
+    corrector + predictor.  Returns per-step records like trajectory()
+    plus the corrected sample x_c (exact and stored)."""
+    steps = S if steps is None else steps
+    B, N = pos.shape[0], pos.shape[1]
+    bb = bbox(pos, tol_frac)
+    cache = {}
+    x_t, x_prev, m1, m2 = x_t0, None, None, None
+    c = 0
+    out = []
+    for k in range(steps):
+        if full[k] or m1 is None:
+            mk = stub(k, list(range(N)))
+            mk_exact = (mk if dtype == "f32" else _bf16_values(mk)).astype(np.float64)
+            A = list(range(N))
+        else:
+            A = anchors(N, a, c)
+            c += 1
+            key = tuple(A)
+            if key not in cache:
+                corr, w, _ = build(pos, cams, A, K, bb)
+                cache[key] = (corr, w)
+            corr, w = cache[key]
+            mk_exact, mk = transport(m1, stub(k, A), corr, w, A, dtype)
+        co = unipc_coeffs(S, k, order, corrector)
+        xc, xn = unipc_apply(co, x_t, x_prev, m2, m1, mk, dtype)
+        xc_s = store(xc, dtype)
+        x_t = store(xn, dtype)
+        x_prev, m2, m1 = xc_s, m1, mk
+        out.append({"k": k, "anchors": A, "c": c, "x_t": x_t, "x0": mk, "x_c": xc_s, "x_t_exact": xn,
+                    "x0_exact": mk_exact, "x_c_exact": xc})
     return out
 
 

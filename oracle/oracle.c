@@ -549,3 +549,139 @@ int orc_ddim_timesteps(int T, int S, int32_t* out) {
   out[S] = -1;
   return 0;
 }
+
+/* ------------------------------------------------------------------ */
+/* O8: multistep (UniPC) sampler-consistent update                      */
+/* ------------------------------------------------------------------ */
+/*
+ * The reconstruction keeps the solver's history in the parameterisation it
+ * expects (Sec. 3.2, after Eq. 1).  For a multistep solver in data
+ * prediction, that history is the x0 of previous steps -- for a cached step,
+ * the transported x0 of every view.  This is the UniPC predictor-corrector
+ * (Zhao et al. 2023) with B(h) = expm1(h) ("bh2"), data prediction, on the
+ * DDIM noise schedule: alpha_t = sqrt(abar_t), sigma_t = sqrt(1 - abar_t),
+ * lambda_t = log(alpha_t / sigma_t).  At sampler step k (time s0 = t_k):
+ *   corrector (k >= 1, order pc = predictor order of step k-1):
+ *     x_c = (sigma_s0/sigma_p) x_prev - alpha_s0 (e^{-h} - 1) m_{k-1}
+ *           - alpha_s0 B_h (sum_j rho_c[j] D_j + rho_c[pc-1] (m_k - m_{k-1}))
+ *     with h = lambda_s0 - lambda_{t_{k-1}}, x_prev the corrected sample of
+ *     step k-1, D_1 = (m_{k-2} - m_{k-1}) / r_1 (pc = 2),
+ *     r_1 = (lambda_{t_{k-2}} - lambda_{t_{k-1}}) / h; rho_c = [1/2] for
+ *     pc = 1, else the solution of R rho = b (below);
+ *   predictor (order pp):
+ *     x_next = (sigma_n/sigma_s0) x_c - alpha_n (e^{-h'} - 1) m_k
+ *              - alpha_n B_h' rho_p D'_1
+ *     with h' = lambda_n - lambda_s0, D'_1 = (m_{k-1} - m_k) / r'_1,
+ *     r'_1 = (lambda_{t_{k-1}} - lambda_s0) / h', rho_p = 1/2 (pp = 2).
+ *   R[i][j] = r_j^i (r_last = 1), b_i = h_phi_{i+1} (i+1)! / B_h with
+ *   h_phi_1 = expm1(-h), h_phi_{i+1} = h_phi_i / (-h) - 1/(i+1)!.
+ *   Orders: pp = min(order, steps taken + 1, S - k) (warm-up and a
+ *   first-order last step).  The last step goes to sigma_n = 0, where the
+ *   predictor reduces to x_next = m_k.
+ * The whole update is linear in (x_prev, m_{k-2}, m_{k-1}, m_k) or, without a
+ * corrector, (x_k, m_{k-1}, m_k); orc_unipc_coeffs returns those
+ * coefficients in double, orc_unipc_apply applies them in double.
+ * coef layout: [0] use corrector, [1] pc, [2] pp,
+ *   corrector x_c = c[3] x_prev + c[4] m_{k-2} + c[5] m_{k-1} + c[6] m_k,
+ *   predictor x_next = c[7] x_c + c[8] m_{k-1} + c[9] m_k.
+ */
+static double unipc_lambda(int T, double bs, double be, int t) {
+  const double ab = orc_alpha_bar(T, bs, be, t);
+  return log(sqrt(ab)) - log(sqrt(1.0 - ab));
+}
+
+int orc_unipc_coeffs(int T, double beta_start, double beta_end, const int32_t* ts, int S, int k, int order,
+                     int corrector, double* c) {
+  if (order < 1 || order > 2 || k < 0 || k >= S) return -1;
+  for (int i = 0; i < 10; ++i) c[i] = 0.0;
+  /* predictor order at step j: warm-up and first-order final step */
+  int pp_k = order;
+  if (k + 1 < pp_k) pp_k = k + 1;
+  if (S - k < pp_k) pp_k = S - k;
+  const int t0 = ts[k];
+  const double ab0 = orc_alpha_bar(T, beta_start, beta_end, t0);
+  const double a0 = sqrt(ab0), s0 = sqrt(1.0 - ab0), l0 = log(a0) - log(s0);
+  /* corrector: back from step k-1 to step k */
+  if (corrector && k >= 1) {
+    int pc = order;
+    if (k < pc) pc = k;                    /* predictor order used at step k-1 */
+    if (S - (k - 1) < pc) pc = S - (k - 1);
+    const int tp = ts[k - 1];
+    const double abp = orc_alpha_bar(T, beta_start, beta_end, tp);
+    const double ap = sqrt(abp), sp = sqrt(1.0 - abp), lp = log(ap) - log(sp);
+    const double h = l0 - lp, hh = -h;
+    const double h_phi_1 = expm1(hh), B_h = expm1(hh);
+    double rho[2];
+    double r1 = 0.0;
+    if (pc == 1) {
+      rho[0] = 0.5;
+    } else {
+      const double lpp = unipc_lambda(T, beta_start, beta_end, ts[k - 2]);
+      r1 = (lpp - lp) / h;
+      /* R = [[1, 1], [r1, 1]], b_i = h_phi_{i+1} (i+1)! / B_h */
+      double h_phi_k = h_phi_1 / hh - 1.0;
+      const double b0 = h_phi_k * 1.0 / B_h;
+      h_phi_k = h_phi_k / hh - 1.0 / 2.0;
+      const double b1 = h_phi_k * 2.0 / B_h;
+      const double det = 1.0 * 1.0 - 1.0 * r1;
+      rho[0] = (b0 * 1.0 - 1.0 * b1) / det;
+      rho[1] = (1.0 * b1 - r1 * b0) / det;
+    }
+    c[0] = 1.0;
+    c[1] = pc;
+    c[3] = s0 / sp;
+    /* - a0 h_phi_1 m_{k-1} - a0 B_h rho_last (m_k - m_{k-1}) - a0 B_h rho_0 (m_{k-2} - m_{k-1}) / r1 */
+    const double rl = pc == 1 ? rho[0] : rho[1];
+    c[5] = -a0 * h_phi_1 + a0 * B_h * rl;
+    c[6] = -a0 * B_h * rl;
+    if (pc == 2) {
+      c[4] = -a0 * B_h * rho[0] / r1;
+      c[5] += a0 * B_h * rho[0] / r1;
+    }
+  }
+  if ((pp_k == 2 && k < 1) || (c[1] == 2 && k < 2)) return -1;   /* no history that far back */
+  c[2] = pp_k;
+  /* predictor: step k -> k+1 */
+  const int tn = ts[k + 1];
+  if (tn < 0) {              /* sigma_n = 0: x_next = m_k */
+    c[9] = 1.0;
+    return 0;
+  }
+  const double abn = orc_alpha_bar(T, beta_start, beta_end, tn);
+  const double an = sqrt(abn), sn = sqrt(1.0 - abn), ln = log(an) - log(sn);
+  const double h = ln - l0, hh = -h;
+  const double h_phi_1 = expm1(hh), B_h = expm1(hh);
+  c[7] = sn / s0;
+  c[9] = -an * h_phi_1;
+  if (pp_k == 2) {
+    const double lm = unipc_lambda(T, beta_start, beta_end, ts[k - 1]);
+    const double r1 = (lm - l0) / h;
+    /* - an B_h (1/2) (m_{k-1} - m_k) / r1 */
+    c[8] = -an * B_h * 0.5 / r1;
+    c[9] += an * B_h * 0.5 / r1;
+  }
+  return 0;
+}
+
+/* One UniPC update, elementwise in double.  x_cur is the sample the step
+ * starts from when there is no corrector; x_prev the previous corrected
+ * sample otherwise.  Outputs: x_c (the corrected sample, next step's x_prev)
+ * and x_next.  Any of m_km2 / x_prev may be null when its coefficient is 0. */
+int orc_unipc_apply(const void* x_cur, const void* x_prev, const void* m_km2, const void* m_km1, const void* m_k,
+                    int64_t n, int dtype, const double* c, double* x_c, double* x_next) {
+  if (dtype != ORC_F32 && dtype != ORC_BF16) return -3;
+  for (int64_t i = 0; i < n; ++i) {
+    const double mk = load_val(m_k, i, dtype);
+    const double mk1 = m_km1 ? load_val(m_km1, i, dtype) : 0.0;
+    double xc;
+    if (c[0] != 0.0) {
+      const double mk2 = m_km2 ? load_val(m_km2, i, dtype) : 0.0;
+      xc = c[3] * load_val(x_prev, i, dtype) + c[4] * mk2 + c[5] * mk1 + c[6] * mk;
+    } else {
+      xc = load_val(x_cur, i, dtype);
+    }
+    x_c[i] = xc;
+    x_next[i] = c[7] * xc + c[8] * mk1 + c[9] * mk;
+  }
+  return 0;
+}

@@ -460,3 +460,34 @@ def test_split_launch_without_visible_tokens(gc):
     np.testing.assert_array_equal(got[:, targets], x0_prev[:, targets])
     for s, u in enumerate(A):
         np.testing.assert_array_equal(got[:, u], x0_new[:, s])
+
+
+def test_patch_token_granularity(gc):
+    """DiT-style tokens (Sec. 3.2, applicability: an anchor can be a token-frame
+    slice): 2x2 latent patches become tokens with 4C channels; the token grid's
+    position maps are the latent maps area-downsampled by 2, and the same
+    calls run on the token grid."""
+    w = C2
+    P_lat = latent_maps(w.name)                               # [1, 6, 64, 64, 3]
+    P_tok_o = oracle.downsample(P_lat, 2)                     # [1, 6, 32, 32, 3]
+    P_tok = gc.gc_posmap_downsample(torch.from_numpy(P_lat).to(DEV), 2)
+    np.testing.assert_array_equal(P_tok.cpu().numpy().view(np.uint32), P_tok_o.view(np.uint32))
+    cams = synth.batch_cameras(w)
+    for k in ("fx", "fy", "cx", "cy"):                        # token-pixel units
+        cams[k] = (cams[k] / 2).astype(np.float32)
+    A = anchors_of(w, 0)
+    bb = oracle.bbox(P_tok_o, w.tol_frac)
+    corr_o, wts_o, _ = oracle.build(P_tok_o, cams, A, w.K, bb)
+    corr, wts = gc.gc_build_correspondence(P_tok, gc.camera_tensor(cams, DEV), A, w.K,
+                                           gc.gc_posmap_bbox(P_tok, w.tol_frac))
+    np.testing.assert_array_equal(corr.cpu().numpy(), corr_o)
+    rs = np.random.default_rng(9)
+    C = 4 * 16                                                # 2x2 patch of a 16-channel latent
+    prev = synth.storage(rs.standard_normal((1, w.N, 32, 32, C)).astype(np.float32), "bf16")
+    new = synth.storage(rs.standard_normal((1, w.a, 32, 32, C)).astype(np.float32), "bf16")
+    ex, st = oracle.transport(prev, new, corr_o, wts_o, A, "bf16")
+    idx = gc.gc_index_correspondence(corr)
+    out = gc.gc_transport_step(to_dev(prev, "bf16"), to_dev(new, "bf16"), corr, wts, A, index=idx)
+    got = synth.values(to_host(out, "bf16"), "bf16").astype(np.float64)
+    assert np.abs(got - ex).max() <= TOL["bf16"]
+    assert idx.n_vis > 0

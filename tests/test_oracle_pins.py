@@ -668,3 +668,90 @@ def test_all_anchor_trajectory_equals_plain_sampler(maps, kind, dtype):
     for r1, r2 in zip(cached, plain):
         np.testing.assert_array_equal(r1["x_t"], r2["x_t"])
         np.testing.assert_array_equal(r1["x0"], r2["x0"])
+
+
+# ---------------------------------------------------------------------------
+# O8 multistep (UniPC) update
+# ---------------------------------------------------------------------------
+
+def test_unipc_order1_predictor_is_ddim():
+    """UniPC of order 1 without the corrector is the DDIM step (closed form)."""
+    S = 10
+    ts = oracle.ddim_timesteps(S)
+    rs = np.random.default_rng(0)
+    x = rs.standard_normal(1024).astype(np.float32)
+    m = rs.standard_normal(1024).astype(np.float32)
+    for k in range(S):
+        co = oracle.unipc_coeffs(S, k, order=1, corrector=False)
+        _, xn = oracle.unipc_apply(co, x, None, None, None, m, "f32")
+        want, _ = oracle.reconstruct(x, m, "f32", "ddim", ts[k], ts[k + 1])
+        np.testing.assert_allclose(xn, want, rtol=0, atol=1e-12)
+
+
+def test_unipc_constant_history_is_ddim_chain():
+    """With the same x0 prediction at every step the multistep terms vanish:
+    the corrected sample equals the DDIM step from the previous corrected
+    sample, and the prediction equals the DDIM step from the corrected one."""
+    S = 12
+    ts = oracle.ddim_timesteps(S)
+    rs = np.random.default_rng(1)
+    m = rs.standard_normal(512).astype(np.float32)
+    xprev = rs.standard_normal(512).astype(np.float32)
+    for k in range(1, S):
+        co = oracle.unipc_coeffs(S, k, order=2, corrector=True)
+        assert co[0] == 1
+        xc, xn = oracle.unipc_apply(co, None, xprev, m, m, m, "f32")
+        want_c, _ = oracle.reconstruct(xprev, m, "f32", "ddim", ts[k - 1], ts[k])
+        np.testing.assert_allclose(xc, want_c, rtol=0, atol=1e-9)
+        want_n, _ = oracle.reconstruct(xc.astype(np.float32), m, "f32", "ddim", ts[k], ts[k + 1])
+        np.testing.assert_allclose(xn, want_n, rtol=0, atol=1e-6)
+
+
+def _unipc_error(S, order, corrector, c0=0.3, c1=0.7, t_check=99):
+    """Run UniPC on a 'model' whose x0 prediction is c0 + c1 * lambda_t (it
+    ignores x); the data-prediction ODE then has the exact solution
+    x_t = (sigma_t / sigma_s) x_s + sigma_t [e^lam (c0 + c1 (lam - 1))]_s^t.
+    Returns |x - x_exact| at timestep t_check."""
+    ts = oracle.ddim_timesteps(S)
+    lam = lambda t: 0.5 * math.log(oracle.alpha_bar(t) / (1 - oracle.alpha_bar(t)))
+    sig = lambda t: math.sqrt(1 - oracle.alpha_bar(t))
+    F = lambda L: math.exp(L) * (c0 + c1 * (L - 1))
+    x0_start = 0.2
+    t0 = ts[0]
+    exact = lambda t: sig(t) / sig(t0) * x0_start + sig(t) * (F(lam(t)) - F(lam(t0)))
+    xt = np.array([x0_start], np.float64)
+    xprev = m1 = m2 = None
+    for k in range(S):
+        mk = np.array([c0 + c1 * lam(ts[k])])
+        co = oracle.unipc_coeffs(S, k, order=order, corrector=corrector)
+        xc = co[7] * 0 + (co[3] * xprev[0] + co[4] * (m2[0] if m2 is not None else 0) + co[5] * m1[0] + co[6] * mk[0]
+                          if co[0] else xt[0])
+        if ts[k] == t_check:
+            return abs(xc - exact(t_check))
+        xn = co[7] * xc + co[8] * (m1[0] if m1 is not None else 0) + co[9] * mk[0]
+        xprev, m2, m1, xt = np.array([xc]), m1, mk, np.array([xn])
+    raise AssertionError("t_check not on the grid")
+
+
+def test_unipc_convergence_order():
+    """Against the exact solution: halving the step cuts the error ~4x with
+    the second-order solver and ~2x with DDIM (first order)."""
+    e2 = [_unipc_error(S, 2, True) for S in (10, 20, 40)]
+    e1 = [_unipc_error(S, 1, False) for S in (10, 20, 40)]
+    assert e2[0] / e2[1] > 3.0 and e2[1] / e2[2] > 3.0, e2
+    assert 1.5 < e1[0] / e1[1] < 2.6 and 1.5 < e1[1] / e1[2] < 2.6, e1
+    assert e2[2] < e1[2] / 10
+
+
+def test_unipc_orders_warm_up_and_final_step():
+    """Multistep orders: first order at step 0 (no history yet), first order on
+    the last step, the corrector taking the previous step's predictor order."""
+    S = 10
+    pp = [int(oracle.unipc_coeffs(S, k, order=2)[2]) for k in range(S)]
+    pc = [int(oracle.unipc_coeffs(S, k, order=2)[1]) for k in range(S)]
+    assert pp == [1] + [2] * (S - 2) + [1]
+    assert pc == [0, 1] + [2] * (S - 2)
+    assert oracle.unipc_coeffs(S, 0, order=2)[0] == 0        # no corrector before any history
+    # the last step lands on sigma = 0: the prediction is the clean estimate
+    co = oracle.unipc_coeffs(S, S - 1, order=2)
+    assert co[7] == 0 and co[8] == 0 and co[9] == 1
