@@ -29,7 +29,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 PEAK_HBM_GBS = 8000.0
-FUSED_KERNEL = "k_transport<1, 8, true, true>"   # bf16, 16-byte vectors, fused, split launch
+FUSED_KERNEL = "k_transport<1, 8, 1, true>"   # bf16, 16-byte vectors, fused reconstruction, split launch
 
 
 def parse():
@@ -250,6 +250,22 @@ def main():
     rows["reconstruct_only_ms"] = timed(lambda: gc.gc_sampler_reconstruct(buf["x_t"], buf["x0_out"], smp, tt, ttn,
                                                                           x_next=buf["x_next"]))
     rows["unfused_pair_ms"] = rows["transport_only_ms"] + rows["reconstruct_only_ms"]
+
+    # multistep variant: UniPC-2 with the corrector (DDIM noise schedule) fused with
+    # Eq. 1; it also reads x_prev and m_{k-2} and writes x_c (no x_t read)
+    ust = gc.gc_unipc_coeffs(gc.Sampler(kind=gc.GC_DDIM), w.S, kc, 2, True)
+    uplans = []
+    for b in ring[:2]:
+        uplans.append(gc.bind_transport_unipc(b["x0_prev"], b["x0_new"], corr0, wts0, A0, b["x0_out"],
+                                              torch.empty_like(b["x0_prev"]), b["x_next"], x_prev=b["x_t"].clone(),
+                                              m_km2=b["x0_prev"].clone(), index=index[anchor_sets[0]]))
+    uc = iter(range(1 << 30))
+    rows["unipc_fused_ms"] = timed(lambda: uplans[next(uc) % len(uplans)](ust))
+    nv0 = index[anchor_sets[0]].n_vis
+    ubytes = (B * (6 * N + a) * latent_view + 4 * ((n_tok + 31) // 32) + 4 * nv0 + 4 * a * nv0
+              + 4 * K * vis_pairs[anchor_sets[0]])
+    rows["unipc_fused_GBps"] = ubytes / (rows["unipc_fused_ms"] * 1e-3) / 1e9
+    del uplans
     rows["coverage_per_anchor_set"] = [round(cover[A], 4) for A in anchor_sets]
     rows["visible_pairs_per_anchor_set"] = [vis_pairs[A] for A in anchor_sets]
     rows["visible_tokens_per_anchor_set"] = [index[A].n_vis for A in anchor_sets]

@@ -15,6 +15,7 @@
  *   every cached step    gc_transport_step      Eq. 1: x0(v) = x0_prev(v) + G[dx0(A)]
  *                        gc_sampler_reconstruct sampler-consistent eps / v / velocity + x_t update
  *                        gc_transport_reconstruct  the two above fused in one pass
+ *                        gc_unipc_update, gc_transport_unipc  multistep (UniPC) variant
  *   host schedule        gc_schedule_anchors, gc_schedule_full_steps, gc_sampler_step_times
  *
  * Conventions shared by every call
@@ -282,6 +283,64 @@ int gc_transport_reconstruct(const void* x0_prev, const void* x0_anchor_new, con
                              const int32_t* anchors, int a, int K, int dtype, const gc_sampler* smp,
                              double t, double t_next, void* x0_out, void* x_next, void* model_out,
                              hipStream_t stream);
+
+/*
+ * Multistep (UniPC) sampler-consistent update.
+ * The reconstruction keeps the solver's history in the parameterisation it
+ * expects (Sec. 3.2, after Eq. 1).  For a multistep solver in data
+ * prediction -- UniPC with B(h) = expm1(h) (Zhao et al. 2023), the solver of
+ * the paper's headline operating point -- that history is the x0 of earlier
+ * steps, i.e. the x0 store: at a cached step the transported x0 of every
+ * view enters it directly.  One step k of an S-step trajectory on the DDIM
+ * noise schedule (alpha = sqrt(abar), sigma = sqrt(1 - abar), trailing
+ * timesteps, sigma = 0 after the last step) is linear in its inputs:
+ *   corrector (use_corrector):  x_c = c_xprev x_prev + c_mk2 m_{k-2} + c_mk1 m_{k-1} + c_mk m_k
+ *   otherwise:                  x_c = x_cur
+ *   predictor:                  x_next = p_xc x_c + p_mk1 m_{k-1} + p_mk m_k
+ * with m_j the x0 of step j, x_prev the corrected sample of step k-1 and
+ * x_cur the sample step k starts from.  Orders: first order at step 0 and on
+ * the last step, otherwise min(order, 2); the corrector uses the previous
+ * step's predictor order.  gc_unipc_coeffs computes the coefficients on the
+ * host in double; the kernels round them once to float.
+ */
+typedef struct gc_unipc_step {
+  int32_t use_corrector;
+  int32_t corrector_order;
+  int32_t predictor_order;
+  int32_t reserved;
+  double c_xprev, c_mk2, c_mk1, c_mk;
+  double p_xc, p_mk1, p_mk;
+} gc_unipc_step;
+
+/* smp: a GC_DDIM sampler (its T and betas define the schedule); order 1 or 2;
+ * corrector 0/1. */
+int gc_unipc_coeffs(const gc_sampler* smp, int S, int k, int order, int corrector, gc_unipc_step* out);
+
+/*
+ * The update over n_elems values (a full step: x0 of every view given).
+ *   x_cur   device [n] (required iff !use_corrector)
+ *   x_prev  device [n] (required iff use_corrector)
+ *   m_km2, m_km1  device [n], required iff a coefficient of theirs is non-zero
+ *   m_k     device [n]
+ *   x_c     device [n] output (the next step's x_prev); may be x_prev itself
+ *   x_next  device [n] output; may be x_cur itself
+ * n_elems a multiple of 4; other outputs must not overlap any input.
+ */
+int gc_unipc_update(const void* x_cur, const void* x_prev, const void* m_km2, const void* m_km1, const void* m_k,
+                    int64_t n_elems, int dtype, const gc_unipc_step* st, void* x_c, void* x_next,
+                    hipStream_t stream);
+
+/*
+ * A cached step with the UniPC update, fused: gc_transport_step (m_k =
+ * x0_out, m_{k-1} = x0_prev) followed by gc_unipc_update over all B*N views
+ * in one pass.  Arguments as for gc_transport_step and gc_unipc_update; all
+ * latents [B][N][H][W][C].  x_c may be x_prev, x_next may be x_cur.
+ */
+int gc_transport_unipc(const void* x0_prev, const void* x0_anchor_new, const int32_t* corr, const float* weights,
+                       const uint32_t* vis_bits, const int32_t* vis_list, int64_t n_vis, const void* x_cur,
+                       const void* x_prev, const void* m_km2, int B, int N, int H, int W, int C,
+                       const int32_t* anchors, int a, int K, int dtype, const gc_unipc_step* st, void* x0_out,
+                       void* x_c, void* x_next, hipStream_t stream);
 
 /*
  * Host schedule (no device work).

@@ -49,6 +49,15 @@ class _Sampler(ctypes.Structure):
                 ("reserved", ctypes.c_int32), ("beta_start", ctypes.c_double), ("beta_end", ctypes.c_double)]
 
 
+class UniPCStep(ctypes.Structure):
+    """gc_unipc_step: coefficients of one UniPC step (gc_unipc_coeffs)."""
+    _fields_ = [("use_corrector", ctypes.c_int32), ("corrector_order", ctypes.c_int32),
+                ("predictor_order", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("c_xprev", ctypes.c_double), ("c_mk2", ctypes.c_double), ("c_mk1", ctypes.c_double),
+                ("c_mk", ctypes.c_double), ("p_xc", ctypes.c_double), ("p_mk1", ctypes.c_double),
+                ("p_mk", ctypes.c_double)]
+
+
 @dataclass(frozen=True)
 class Sampler:
     """gc_sampler: kind GC_DDIM (linear betas over T steps) or GC_FLOW_EULER."""
@@ -92,6 +101,10 @@ def lib() -> ctypes.CDLL:
             "gc_transport_reconstruct": ([_vp, _vp, _vp, _vp, _vp, _vp, _i64, _vp, _i, _i, _i, _i, _i, _i32p, _i,
                                           _i, _i, ctypes.POINTER(_Sampler), ctypes.c_double, ctypes.c_double, _vp,
                                           _vp, _vp, _vp], _i),
+            "gc_unipc_coeffs": ([ctypes.POINTER(_Sampler), _i, _i, _i, _i, ctypes.POINTER(UniPCStep)], _i),
+            "gc_unipc_update": ([_vp, _vp, _vp, _vp, _vp, _i64, _i, ctypes.POINTER(UniPCStep), _vp, _vp, _vp], _i),
+            "gc_transport_unipc": ([_vp, _vp, _vp, _vp, _vp, _vp, _i64, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i32p,
+                                    _i, _i, _i, ctypes.POINTER(UniPCStep), _vp, _vp, _vp, _vp], _i),
             "gc_schedule_anchors": ([_i, _i, _i64, _i32p], _i),
             "gc_schedule_full_steps": ([_i, _i, _i, ctypes.POINTER(ctypes.c_uint8)], _i),
             "gc_sampler_step_times": ([ctypes.POINTER(_Sampler), _i, _i, ctypes.POINTER(ctypes.c_double),
@@ -374,6 +387,98 @@ def bind_transport_reconstruct(x0_prev: torch.Tensor, x0_anchor_new: torch.Tenso
     post = (_dev(x0_out, "x0_out"), _dev(x_next, "x_next"), _opt(model_out, "model_out"), _stream(stream))
     return BoundCall(lib().gc_transport_reconstruct, pre, sampler.c(), post,
                      (x0_prev, x0_anchor_new, corr, weights, x_t, x0_out, x_next, model_out, arr, index))
+
+
+def gc_unipc_coeffs(sampler: Sampler, S: int, k: int, order: int = 2, corrector: bool = True) -> UniPCStep:
+    st = UniPCStep()
+    smp = sampler.c()
+    _check(lib().gc_unipc_coeffs(ctypes.byref(smp), S, k, order, int(corrector), ctypes.byref(st)),
+           "gc_unipc_coeffs")
+    return st
+
+
+def gc_unipc_update(st: UniPCStep, m_k: torch.Tensor, x_cur: torch.Tensor = None, x_prev: torch.Tensor = None,
+                    m_km2: torch.Tensor = None, m_km1: torch.Tensor = None, x_c: torch.Tensor = None,
+                    x_next: torch.Tensor = None, stream=None):
+    """UniPC update over all elements (a full step); returns (x_c, x_next)."""
+    if x_c is None:
+        x_c = torch.empty_like(m_k)
+    if x_next is None:
+        x_next = torch.empty_like(m_k)
+    for name, t in (("x_cur", x_cur), ("x_prev", x_prev), ("m_km2", m_km2), ("m_km1", m_km1)):
+        if t is not None and (t.shape != m_k.shape or t.dtype != m_k.dtype):
+            raise ValueError(f"{name} must match m_k in shape and dtype")
+    _check(lib().gc_unipc_update(_opt(x_cur, "x_cur"), _opt(x_prev, "x_prev"), _opt(m_km2, "m_km2"),
+                                 _opt(m_km1, "m_km1"), _dev(m_k, "m_k"), m_k.numel(), dtype_code(m_k),
+                                 ctypes.byref(st), _dev(x_c, "x_c"), _dev(x_next, "x_next"), _stream(stream)),
+           "gc_unipc_update")
+    return x_c, x_next
+
+
+def gc_transport_unipc(x0_prev: torch.Tensor, x0_anchor_new: torch.Tensor, corr: torch.Tensor,
+                       weights: torch.Tensor, anchors: Sequence[int], st: UniPCStep, x_cur: torch.Tensor = None,
+                       x_prev: torch.Tensor = None, m_km2: torch.Tensor = None, x0_out: torch.Tensor = None,
+                       x_c: torch.Tensor = None, x_next: torch.Tensor = None, index: VisibleIndex = None,
+                       stream=None):
+    """Fused Eq. 1 + UniPC update; returns (x0_out, x_c, x_next)."""
+    B, N, H, W, C = _latent_shape(x0_prev)
+    arr, a = _anchors(anchors)
+    if tuple(x0_anchor_new.shape) != (B, a, H, W, C) or x0_anchor_new.dtype != x0_prev.dtype:
+        raise ValueError(f"x0_anchor_new must be [B, a={a}, H, W, C] of the same dtype as x0_prev")
+    for name, t in (("x_cur", x_cur), ("x_prev", x_prev), ("m_km2", m_km2)):
+        if t is not None and (t.shape != x0_prev.shape or t.dtype != x0_prev.dtype):
+            raise ValueError(f"{name} must match x0_prev in shape and dtype")
+    K = weights.shape[-1]
+    x0_out = torch.empty_like(x0_prev) if x0_out is None else x0_out
+    x_c = torch.empty_like(x0_prev) if x_c is None else x_c
+    x_next = torch.empty_like(x0_prev) if x_next is None else x_next
+    _check(lib().gc_transport_unipc(_dev(x0_prev, "x0_prev"), _dev(x0_anchor_new, "x0_anchor_new"),
+                                    _dev(corr, "corr") if corr.numel() else None,
+                                    _dev(weights, "weights") if weights.numel() else None, *_index_args(index),
+                                    _opt(x_cur, "x_cur"), _opt(x_prev, "x_prev"), _opt(m_km2, "m_km2"),
+                                    B, N, H, W, C, arr, a, K, dtype_code(x0_prev), ctypes.byref(st),
+                                    _dev(x0_out, "x0_out"), _dev(x_c, "x_c"), _dev(x_next, "x_next"),
+                                    _stream(stream)), "gc_transport_unipc")
+    return x0_out, x_c, x_next
+
+
+class BoundUniPC:
+    """A gc_transport_unipc call with its buffer arguments marshalled; the
+    object takes the step's coefficients and issues exactly one ctypes call."""
+    __slots__ = ("_fn", "_pre", "_post", "keep")
+
+    def __init__(self, fn, pre, post, keep):
+        self._fn, self._pre, self._post, self.keep = fn, pre, post, keep
+
+    def __call__(self, st: UniPCStep) -> None:
+        rc = self._fn(*self._pre, ctypes.byref(st), *self._post)
+        if rc != GC_OK:
+            _check(rc, "gc_transport_unipc")
+
+
+def bind_transport_unipc(x0_prev: torch.Tensor, x0_anchor_new: torch.Tensor, corr: torch.Tensor,
+                         weights: torch.Tensor, anchors: Sequence[int], x0_out: torch.Tensor, x_c: torch.Tensor,
+                         x_next: torch.Tensor, x_cur: torch.Tensor = None, x_prev: torch.Tensor = None,
+                         m_km2: torch.Tensor = None, index: VisibleIndex = None, stream=None) -> BoundUniPC:
+    """Marshal gc_transport_unipc's buffer arguments once (same shape checks
+    as gc_transport_unipc); the returned object takes a UniPCStep.  The
+    tensors must stay alive and unmoved while the object is used."""
+    B, N, H, W, C = _latent_shape(x0_prev)
+    arr, a = _anchors(anchors)
+    if tuple(x0_anchor_new.shape) != (B, a, H, W, C) or x0_anchor_new.dtype != x0_prev.dtype:
+        raise ValueError(f"x0_anchor_new must be [B, a={a}, H, W, C] of the same dtype as x0_prev")
+    for name, t in (("x_cur", x_cur), ("x_prev", x_prev), ("m_km2", m_km2), ("x0_out", x0_out), ("x_c", x_c),
+                    ("x_next", x_next)):
+        if t is not None and (t.shape != x0_prev.shape or t.dtype != x0_prev.dtype):
+            raise ValueError(f"{name} must match x0_prev in shape and dtype")
+    K = weights.shape[-1]
+    pre = (_dev(x0_prev, "x0_prev"), _dev(x0_anchor_new, "x0_anchor_new"),
+           _dev(corr, "corr") if corr.numel() else None, _dev(weights, "weights") if weights.numel() else None,
+           *_index_args(index), _opt(x_cur, "x_cur"), _opt(x_prev, "x_prev"), _opt(m_km2, "m_km2"),
+           B, N, H, W, C, arr, a, K, dtype_code(x0_prev))
+    post = (_dev(x0_out, "x0_out"), _dev(x_c, "x_c"), _dev(x_next, "x_next"), _stream(stream))
+    return BoundUniPC(lib().gc_transport_unipc, pre, post,
+                      (x0_prev, x0_anchor_new, corr, weights, x_cur, x_prev, m_km2, x0_out, x_c, x_next, arr, index))
 
 
 def gc_schedule_anchors(N: int, a: int, c: int) -> List[int]:

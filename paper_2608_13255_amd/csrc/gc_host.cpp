@@ -172,4 +172,77 @@ int gc_sampler_alpha_bar(const gc_sampler* smp, int t, double* abar) {
   return GC_OK;
 }
 
+// UniPC (bh2, data prediction) coefficients of step k.  Times: trailing
+// DDIM timesteps, the step after the last one at sigma = 0.
+int gc_unipc_coeffs(const gc_sampler* smp, int S, int k, int order, int corrector, gc_unipc_step* out) {
+  clear_error();
+  if (!smp || !out) return fail(GC_ERR_ARG, "unipc: null argument");
+  if (smp->kind != GC_DDIM) return fail(GC_ERR_ARG, "unipc: needs a GC_DDIM sampler for its noise schedule");
+  int rc = check_sampler(smp);
+  if (rc) return rc;
+  if (order < 1 || order > 2) return fail(GC_ERR_ARG, "unipc: order %d outside [1, 2]", order);
+  if (S < 1 || S > smp->T || k < 0 || k >= S) return fail(GC_ERR_ARG, "unipc: step %d outside [0, S=%d)", k, S);
+  auto tstep = [&](int j) { return j >= S ? -1 : (int)(std::floor((double)(S - j) * smp->T / S + 0.5) - 1.0); };
+  auto ab = [&](int t) { return alpha_bar(smp, t); };
+  auto lam = [&](int t) {
+    const double a = ab(t);
+    return 0.5 * std::log(a / (1.0 - a));   // log(alpha / sigma)
+  };
+  auto pred_order = [&](int j) {
+    int o = order;
+    if (j + 1 < o) o = j + 1;   // warm-up: no older x0 yet
+    if (S - j < o) o = S - j;   // first-order last step
+    return o;
+  };
+  std::memset(out, 0, sizeof(*out));
+  const int t0 = tstep(k);
+  const double a0 = std::sqrt(ab(t0)), s0 = std::sqrt(1.0 - ab(t0)), l0 = lam(t0);
+  if (corrector && k >= 1) {
+    const int pc = pred_order(k - 1);
+    const int tp = tstep(k - 1);
+    const double sp = std::sqrt(1.0 - ab(tp)), lp = lam(tp);
+    const double h = l0 - lp, hh = -h;
+    const double phi1 = std::expm1(hh), Bh = std::expm1(hh);
+    out->use_corrector = 1;
+    out->corrector_order = pc;
+    out->c_xprev = s0 / sp;
+    if (pc == 1) {
+      // x_c = s0/sp x_prev - a0 phi1 m_{k-1} - a0 Bh (1/2) (m_k - m_{k-1})
+      out->c_mk1 = -a0 * phi1 + 0.5 * a0 * Bh;
+      out->c_mk = -0.5 * a0 * Bh;
+    } else {
+      const double r1 = (lam(tstep(k - 2)) - lp) / h;
+      // rho solves [[1, 1], [r1, 1]] rho = (g1, g2), g_i = hphi_i i! / Bh
+      const double hphi2 = phi1 / hh - 1.0;
+      const double hphi3 = hphi2 / hh - 0.5;
+      const double g1 = hphi2 / Bh, g2 = 2.0 * hphi3 / Bh;
+      const double rho0 = (g1 - g2) / (1.0 - r1);
+      const double rho1 = g1 - rho0;
+      // ... - a0 Bh (rho0 (m_{k-2} - m_{k-1}) / r1 + rho1 (m_k - m_{k-1}))
+      out->c_mk2 = -a0 * Bh * rho0 / r1;
+      out->c_mk1 = -a0 * phi1 + a0 * Bh * (rho0 / r1 + rho1);
+      out->c_mk = -a0 * Bh * rho1;
+    }
+  }
+  const int pp = pred_order(k);
+  out->predictor_order = pp;
+  const int tn = tstep(k + 1);
+  if (tn < 0) {
+    out->p_mk = 1.0;   // sigma = 0: the sample is the clean estimate
+    return GC_OK;
+  }
+  const double an = std::sqrt(ab(tn)), sn = std::sqrt(1.0 - ab(tn)), ln = lam(tn);
+  const double h = ln - l0, hh = -h;
+  const double phi1 = std::expm1(hh), Bh = std::expm1(hh);
+  out->p_xc = sn / s0;
+  out->p_mk = -an * phi1;
+  if (pp == 2) {
+    const double r1 = (lam(tstep(k - 1)) - l0) / h;
+    // ... - an Bh (1/2) (m_{k-1} - m_k) / r1
+    out->p_mk1 = -0.5 * an * Bh / r1;
+    out->p_mk += 0.5 * an * Bh / r1;
+  }
+  return GC_OK;
+}
+
 }  // extern "C"

@@ -105,7 +105,17 @@ struct TArgs {
   int gblocks;         // gather blocks in front of the streaming blocks (multiple of kXcds)
   int32_t sorted_anchor[GC_MAX_ANCHORS];  // anchor views ascending, padded with INT_MAX
   Recon r;
+  // UniPC mode: x_t is x_cur; x_prev / m_km2 inputs, x_c output; coefficients in float
+  const void* x_prev;
+  const void* m_km2;
+  void* x_c;
+  int32_t u_corr, u_need_m1, u_need_m2;
+  float uc_xprev, uc_mk2, uc_mk1, uc_mk, up_xc, up_mk1, up_mk;
 };
+
+// What a step does after the transport: nothing, the sampler reconstruction
+// (DDIM / flow Euler), or the UniPC corrector + predictor.
+enum StepMode { kTransportOnly = 0, kReconstruct = 1, kUniPC = 2 };
 
 __device__ __forceinline__ int logical_block(int i, int n_blocks, int remap) {
   if (!remap) return i;
@@ -133,19 +143,38 @@ __device__ __forceinline__ void reconstruct_vec(const Recon& r, const float (&xt
   }
 }
 
+// UniPC corrector (or the start sample) and predictor, fixed float order:
+//   x_c = ((c_xprev x_prev + c_mk2 m_{k-2}) + c_mk1 m_{k-1}) + c_mk m_k   (corrector)
+//   x_next = (p_xc x_c + p_mk1 m_{k-1}) + p_mk m_k
+template <int VEC>
+__device__ __forceinline__ void unipc_vec(const TArgs& g, const float (&xin)[VEC], const float (&m2)[VEC],
+                                          const float (&m1)[VEC], const float (&mk)[VEC], float (&xc)[VEC],
+                                          float (&xn)[VEC]) {
+#pragma unroll
+  for (int e = 0; e < VEC; ++e) {
+    xc[e] = g.u_corr ? ((g.uc_xprev * xin[e] + g.uc_mk2 * m2[e]) + g.uc_mk1 * m1[e]) + g.uc_mk * mk[e] : xin[e];
+    xn[e] = (g.up_xc * xc[e] + g.up_mk1 * m1[e]) + g.up_mk * mk[e];
+  }
+}
+
 // What the caller of token_step knows about a target token.
 enum TokenMode { kAnchorRow = 0, kTargetCheck = 1, kTargetSeen = 2, kTargetUnseen = 3 };
 
 // One cached step for one (token, channel vector): Eq. 1 for a target token
 // (or the copy for an anchor row), then, when fused, the reconstruction.
-template <int DT, int VEC, bool FUSED>
+template <int DT, int VEC, int MODE>
 __device__ __forceinline__ void token_step(const TArgs& g, int b, int p, int cv, int s_self, int64_t crow,
                                            int64_t base, TokenMode mode) {
   using CD = Codec<DT, VEC>;
   using Raw = typename CD::Raw;
   // issue every load of data this thread owns before using any of it
-  Raw xtr;
-  if constexpr (FUSED) xtr = CD::load_stream(g.x_t, base);
+  Raw xtr, m2r, m1r;
+  if constexpr (MODE == kReconstruct) xtr = CD::load_stream(g.x_t, base);
+  if constexpr (MODE == kUniPC) {
+    xtr = CD::load_stream(g.u_corr ? g.x_prev : g.x_t, base);
+    if (g.u_need_m2) m2r = CD::load_stream(g.m_km2, base);
+    if (g.u_need_m1 && mode == kAnchorRow) m1r = CD::load_stream(g.x0_prev, base);
+  }
   Raw x0r;
   float x0f[VEC];
   if (mode == kAnchorRow) {
@@ -155,8 +184,10 @@ __device__ __forceinline__ void token_step(const TArgs& g, int b, int p, int cv,
   } else if (mode == kTargetUnseen) {
     x0r = CD::load_stream(g.x0_prev, base);   // no anchor sees this token: it keeps its own state
     CD::unpack(x0r, x0f);
+    if constexpr (MODE == kUniPC) m1r = x0r;
   } else {
     const Raw prevr = CD::load_stream(g.x0_prev, base);
+    if constexpr (MODE == kUniPC) m1r = prevr;
     const int32_t* cw = g.corr + crow * g.a;
     int32_t words[GC_MAX_ANCHORS];
     if (g.a == 4) {   // the common layout: one 16-byte load (rows are 16-byte aligned)
@@ -217,12 +248,23 @@ __device__ __forceinline__ void token_step(const TArgs& g, int b, int p, int cv,
     }
   }
   CD::store_stream(g.x0_out, base, x0r);
-  if constexpr (FUSED) {
+  if constexpr (MODE == kReconstruct) {
     float xtf[VEC], xn[VEC], mo[VEC];
     CD::unpack(xtr, xtf);
     reconstruct_vec<VEC>(g.r, xtf, x0f, xn, mo);
     CD::store_stream(g.x_next, base, CD::pack(xn));
     if (g.model_out) CD::store_stream(g.model_out, base, CD::pack(mo));
+  }
+  if constexpr (MODE == kUniPC) {
+    float xin[VEC], m2[VEC], m1[VEC], xc[VEC], xn[VEC];
+    CD::unpack(xtr, xin);
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) m2[e] = m1[e] = 0.0f;
+    if (g.u_need_m2) CD::unpack(m2r, m2);
+    if (g.u_need_m1) CD::unpack(m1r, m1);
+    unipc_vec<VEC>(g, xin, m2, m1, x0f, xc, xn);
+    CD::store_stream(g.x_c, base, CD::pack(xc));
+    CD::store_stream(g.x_next, base, CD::pack(xn));
   }
 }
 
@@ -231,7 +273,7 @@ __device__ __forceinline__ void token_step(const TArgs& g, int b, int p, int cv,
 // visible-token list and do all the gathering; the remaining blocks stream
 // every other token, skipping the visible ones by their bit.  Gather blocks go
 // first so that their dependent-load latency overlaps the streaming.
-template <int DT, int VEC, bool FUSED, bool SPLIT>
+template <int DT, int VEC, int MODE, bool SPLIT>
 __global__ __launch_bounds__(kBlock) void k_transport(TArgs g) {
   int i = blockIdx.x;
   if constexpr (SPLIT) {
@@ -257,7 +299,7 @@ __global__ __launch_bounds__(kBlock) void k_transport(TArgs g) {
 #pragma unroll
       for (int s = 0; s < GC_MAX_ANCHORS; ++s) v += g.sorted_anchor[s] <= v ? 1 : 0;
       const int64_t base = (((int64_t)b * g.N + v) * g.HW + p) * g.C + (int64_t)cv * VEC;
-      token_step<DT, VEC, FUSED>(g, b, p, cv, -1, tok, base, kTargetSeen);
+      token_step<DT, VEC, MODE>(g, b, p, cv, -1, tok, base, kTargetSeen);
       return;
     }
     i -= g.gblocks;
@@ -291,15 +333,15 @@ __global__ __launch_bounds__(kBlock) void k_transport(TArgs g) {
   }
   const int64_t base = ((int64_t)bv * g.HW + p) * g.C + (int64_t)cv * VEC;
   if (s_self >= 0) {
-    token_step<DT, VEC, FUSED>(g, b, p, cv, s_self, 0, base, kAnchorRow);
+    token_step<DT, VEC, MODE>(g, b, p, cv, s_self, 0, base, kAnchorRow);
     return;
   }
   const int64_t crow = ((int64_t)b * g.NT + (v - n_before)) * g.HW + p;
   if constexpr (SPLIT) {
     if ((g.vis_bits[crow >> 5] >> (crow & 31)) & 1u) return;   // a gather block owns this token
-    token_step<DT, VEC, FUSED>(g, b, p, cv, -1, crow, base, kTargetUnseen);
+    token_step<DT, VEC, MODE>(g, b, p, cv, -1, crow, base, kTargetUnseen);
   } else {
-    token_step<DT, VEC, FUSED>(g, b, p, cv, -1, crow, base, kTargetCheck);
+    token_step<DT, VEC, MODE>(g, b, p, cv, -1, crow, base, kTargetCheck);
   }
 }
 
@@ -316,6 +358,23 @@ __global__ __launch_bounds__(kBlock) void k_reconstruct(const void* __restrict__
   reconstruct_vec<VEC>(r, xtf, x0f, xn, mo);
   CD::store_stream(x_next, i * VEC, CD::pack(xn));
   if (model_out) CD::store_stream(model_out, i * VEC, CD::pack(mo));
+}
+
+template <int DT, int VEC>
+__global__ __launch_bounds__(kBlock) void k_unipc(TArgs g, const void* __restrict__ m_k, int64_t n_vec) {
+  using CD = Codec<DT, VEC>;
+  const int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+  if (i >= n_vec) return;
+  float xin[VEC], m2[VEC], m1[VEC], mk[VEC], xc[VEC], xn[VEC];
+  CD::unpack(CD::load_stream(g.u_corr ? g.x_prev : g.x_t, i * VEC), xin);
+#pragma unroll
+  for (int e = 0; e < VEC; ++e) m2[e] = m1[e] = 0.0f;
+  if (g.u_need_m2) CD::unpack(CD::load_stream(g.m_km2, i * VEC), m2);
+  if (g.u_need_m1) CD::unpack(CD::load_stream(g.x0_prev, i * VEC), m1);
+  CD::unpack(CD::load_stream(m_k, i * VEC), mk);
+  unipc_vec<VEC>(g, xin, m2, m1, mk, xc, xn);
+  CD::store_stream(g.x_c, i * VEC, CD::pack(xc));
+  CD::store_stream(g.x_next, i * VEC, CD::pack(xn));
 }
 
 int pick_vec(int dtype, int64_t c) { return dtype == GC_F32 ? 4 : (c % 8 == 0 ? 8 : 4); }
@@ -412,19 +471,19 @@ int prepare_transport(const void* x0_prev, const void* x0_new, const int32_t* co
   return GC_OK;
 }
 
-template <bool FUSED>
+template <int MODE>
 void launch_transport(const TArgs& g, int dtype, hipStream_t stream) {
   const int per = (g.n_blocks + kXcds - 1) / kXcds;
   const unsigned stream_blocks = g.remap ? (unsigned)(per * kXcds) : (unsigned)g.n_blocks;
   const bool split = g.vis_bits != nullptr;
   const dim3 grid(stream_blocks + (split ? (unsigned)g.gblocks : 0u));
   const int vec = g.C / g.CV;
-#define GC_LAUNCH(DT_, VEC_)                                                                        \
-  do {                                                                                              \
-    if (split)                                                                                      \
-      hipLaunchKernelGGL((k_transport<DT_, VEC_, FUSED, true>), grid, dim3(kBlock), 0, stream, g);  \
-    else                                                                                            \
-      hipLaunchKernelGGL((k_transport<DT_, VEC_, FUSED, false>), grid, dim3(kBlock), 0, stream, g); \
+#define GC_LAUNCH(DT_, VEC_)                                                                       \
+  do {                                                                                             \
+    if (split)                                                                                     \
+      hipLaunchKernelGGL((k_transport<DT_, VEC_, MODE, true>), grid, dim3(kBlock), 0, stream, g);  \
+    else                                                                                           \
+      hipLaunchKernelGGL((k_transport<DT_, VEC_, MODE, false>), grid, dim3(kBlock), 0, stream, g); \
   } while (0)
   if (dtype == GC_F32)
     GC_LAUNCH(GC_F32, 4);
@@ -433,6 +492,34 @@ void launch_transport(const TArgs& g, int dtype, hipStream_t stream) {
   else
     GC_LAUNCH(GC_BF16, 4);
 #undef GC_LAUNCH
+}
+
+// Validate UniPC coefficients / buffers and load them into g.
+int prepare_unipc(const gc_unipc_step* st, const void* x_cur, const void* x_prev, const void* m_km2,
+                  const void* m_km1, size_t nbytes, const char* who, TArgs* g) {
+  if (!st) return fail(GC_ERR_ARG, "%s: null coefficients", who);
+  g->u_corr = st->use_corrector ? 1 : 0;
+  g->u_need_m2 = (g->u_corr && st->c_mk2 != 0.0) ? 1 : 0;
+  g->u_need_m1 = ((g->u_corr && st->c_mk1 != 0.0) || st->p_mk1 != 0.0) ? 1 : 0;
+  if (g->u_corr && !x_prev) return fail(GC_ERR_ARG, "%s: the corrector needs x_prev", who);
+  if (!g->u_corr && !x_cur) return fail(GC_ERR_ARG, "%s: without the corrector x_cur is needed", who);
+  if (g->u_need_m2 && !m_km2) return fail(GC_ERR_ARG, "%s: the coefficients need m_{k-2}", who);
+  if (g->u_need_m1 && !m_km1) return fail(GC_ERR_ARG, "%s: the coefficients need m_{k-1}", who);
+  const void* ins[4] = {x_cur, x_prev, m_km2, m_km1};
+  for (const void* q : ins)
+    if (q && !aligned16(q)) return fail(GC_ERR_ALIGN, "%s: device pointers must be 16-byte aligned", who);
+  g->x_t = x_cur;
+  g->x_prev = x_prev;
+  g->m_km2 = m_km2;
+  g->uc_xprev = (float)st->c_xprev;
+  g->uc_mk2 = (float)st->c_mk2;
+  g->uc_mk1 = (float)st->c_mk1;
+  g->uc_mk = (float)st->c_mk;
+  g->up_xc = (float)st->p_xc;
+  g->up_mk1 = (float)st->p_mk1;
+  g->up_mk = (float)st->p_mk;
+  (void)nbytes;
+  return GC_OK;
 }
 
 }  // namespace
@@ -450,7 +537,7 @@ extern "C" int gc_transport_step(const void* x0_prev, const void* x0_anchor_new,
                              anchors, a, K, dtype, x0_out, "gc_transport_step", &g);
   if (rc) return rc;
   if (g.n_threads == 0) return GC_OK;
-  launch_transport<false>(g, dtype, stream);
+  launch_transport<kTransportOnly>(g, dtype, stream);
   return after_launch(stream, "gc_transport_step");
 }
 
@@ -523,6 +610,79 @@ extern "C" int gc_transport_reconstruct(const void* x0_prev, const void* x0_anch
   g.x_next = x_next;
   g.model_out = model_out;
   if (g.n_threads == 0) return GC_OK;
-  launch_transport<true>(g, dtype, stream);
+  launch_transport<kReconstruct>(g, dtype, stream);
   return after_launch(stream, "gc_transport_reconstruct");
+}
+
+extern "C" int gc_unipc_update(const void* x_cur, const void* x_prev, const void* m_km2, const void* m_km1,
+                               const void* m_k, int64_t n_elems, int dtype, const gc_unipc_step* st, void* x_c,
+                               void* x_next, hipStream_t stream) {
+  clear_error();
+  if (!m_k || !x_c || !x_next) return fail(GC_ERR_ARG, "gc_unipc_update: null pointer");
+  if (dtype != GC_F32 && dtype != GC_BF16) return fail(GC_ERR_DTYPE, "gc_unipc_update: unknown dtype %d", dtype);
+  if (n_elems < 0 || n_elems % 4)
+    return fail(GC_ERR_SHAPE, "gc_unipc_update: n_elems=%lld must be a non-negative multiple of 4", (long long)n_elems);
+  TArgs g;
+  std::memset(&g, 0, sizeof(g));
+  const size_t nb = (size_t)n_elems * dtype_bytes(dtype);
+  int rc = prepare_unipc(st, x_cur, x_prev, m_km2, m_km1, nb, "gc_unipc_update", &g);
+  if (rc) return rc;
+  g.x0_prev = m_km1;
+  g.x_c = x_c;
+  g.x_next = x_next;
+  if (!aligned16(m_k) || !aligned16(x_c) || !aligned16(x_next))
+    return fail(GC_ERR_ALIGN, "gc_unipc_update: device pointers must be 16-byte aligned");
+  const void* ins[5] = {x_cur, x_prev, m_km2, m_km1, m_k};
+  for (int i = 0; i < 5; ++i) {
+    if (!ins[i]) continue;
+    if ((ins[i] != x_cur && overlaps(x_next, nb, ins[i], nb)) || (ins[i] != x_prev && overlaps(x_c, nb, ins[i], nb)))
+      return fail(GC_ERR_ALIAS, "gc_unipc_update: outputs overlap inputs (only x_c == x_prev, x_next == x_cur)");
+  }
+  if (overlaps(x_c, nb, x_next, nb)) return fail(GC_ERR_ALIAS, "gc_unipc_update: x_c overlaps x_next");
+  if (n_elems == 0) return GC_OK;
+  const int vec = pick_vec(dtype, n_elems);
+  const int64_t n_vec = n_elems / vec;
+  const int64_t blocks = (n_vec + kBlock - 1) / kBlock;
+  if (blocks > 0x7fffffff) return fail(GC_ERR_CAPACITY, "gc_unipc_update: too many elements");
+  if (dtype == GC_F32)
+    hipLaunchKernelGGL((k_unipc<GC_F32, 4>), dim3((unsigned)blocks), dim3(kBlock), 0, stream, g, m_k, n_vec);
+  else if (vec == 8)
+    hipLaunchKernelGGL((k_unipc<GC_BF16, 8>), dim3((unsigned)blocks), dim3(kBlock), 0, stream, g, m_k, n_vec);
+  else
+    hipLaunchKernelGGL((k_unipc<GC_BF16, 4>), dim3((unsigned)blocks), dim3(kBlock), 0, stream, g, m_k, n_vec);
+  return after_launch(stream, "gc_unipc_update");
+}
+
+extern "C" int gc_transport_unipc(const void* x0_prev, const void* x0_anchor_new, const int32_t* corr,
+                                  const float* weights, const uint32_t* vis_bits, const int32_t* vis_list,
+                                  int64_t n_vis, const void* x_cur, const void* x_prev, const void* m_km2, int B,
+                                  int N, int H, int W, int C, const int32_t* anchors, int a, int K, int dtype,
+                                  const gc_unipc_step* st, void* x0_out, void* x_c, void* x_next,
+                                  hipStream_t stream) {
+  clear_error();
+  TArgs g;
+  int rc = prepare_transport(x0_prev, x0_anchor_new, corr, weights, vis_bits, vis_list, n_vis, B, N, H, W, C,
+                             anchors, a, K, dtype, x0_out, "gc_transport_unipc", &g);
+  if (rc) return rc;
+  if (!x_c || !x_next) return fail(GC_ERR_ARG, "gc_transport_unipc: null x_c or x_next");
+  const size_t es = (size_t)dtype_bytes(dtype);
+  const size_t n_all = (size_t)B * N * H * W * C * es, n_new = (size_t)B * a * H * W * C * es;
+  rc = prepare_unipc(st, x_cur, x_prev, m_km2, x0_prev, n_all, "gc_transport_unipc", &g);
+  if (rc) return rc;
+  if (!aligned16(x_c) || !aligned16(x_next)) return fail(GC_ERR_ALIGN, "gc_transport_unipc: outputs must be 16-byte aligned");
+  const void* ins[5] = {x0_prev, x0_anchor_new, x_cur, x_prev, m_km2};
+  const size_t lens[5] = {n_all, n_new, n_all, n_all, n_all};
+  for (int i = 0; i < 5; ++i) {
+    if (!ins[i]) continue;
+    if ((ins[i] != x_cur && overlaps(x_next, n_all, ins[i], lens[i])) ||
+        (ins[i] != x_prev && overlaps(x_c, n_all, ins[i], lens[i])) || overlaps(x0_out, n_all, ins[i], lens[i]))
+      return fail(GC_ERR_ALIAS, "gc_transport_unipc: outputs overlap inputs (only x_c == x_prev, x_next == x_cur)");
+  }
+  if (overlaps(x_c, n_all, x_next, n_all) || overlaps(x_c, n_all, x0_out, n_all) || overlaps(x_next, n_all, x0_out, n_all))
+    return fail(GC_ERR_ALIAS, "gc_transport_unipc: outputs overlap each other");
+  g.x_c = x_c;
+  g.x_next = x_next;
+  if (g.n_threads == 0) return GC_OK;
+  launch_transport<kUniPC>(g, dtype, stream);
+  return after_launch(stream, "gc_transport_unipc");
 }

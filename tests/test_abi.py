@@ -179,3 +179,47 @@ def test_product_never_touches_the_oracle():
             if f.endswith((".py", ".hip", ".cpp", ".h", "Makefile")) or f == "Makefile":
                 text = open(os.path.join(dirpath, f)).read()
                 assert not re.search(r"\boracle\b|\borc_\w+|liboracle|\bsynth\b", text), f
+
+
+def test_unipc_validation(gc, L):
+    ddim = gc.Sampler(kind=gc.GC_DDIM).c()
+    st = gc.UniPCStep()
+    assert ctypes.sizeof(st) == 72
+    flow = gc.Sampler(kind=gc.GC_FLOW_EULER).c()
+    assert L.gc_unipc_coeffs(ctypes.byref(flow), 10, 0, 2, 1, ctypes.byref(st)) == -1
+    assert L.gc_unipc_coeffs(ctypes.byref(ddim), 10, 0, 3, 1, ctypes.byref(st)) == -1
+    assert L.gc_unipc_coeffs(ctypes.byref(ddim), 10, 10, 2, 1, ctypes.byref(st)) == -1
+    assert L.gc_unipc_coeffs(ctypes.byref(ddim), 10, 5, 2, 1, None) == -1
+    assert L.gc_unipc_coeffs(ctypes.byref(ddim), 10, 5, 2, 1, ctypes.byref(st)) == 0
+    assert st.use_corrector == 1 and st.corrector_order == 2 and st.predictor_order == 2
+    assert st.c_mk2 != 0.0 and st.p_mk1 != 0.0
+    n = 64
+    nb = 4 * n
+
+    def upd(x_cur=A0, x_prev=A1, m2=A2, m1=A3, mk=A4, n_el=n, dt=0, stp=ctypes.byref(st), xc=A5, xn=A5 + nb):
+        return L.gc_unipc_update(x_cur, x_prev, m2, m1, mk, n_el, dt, stp, xc, xn, None)
+
+    assert upd(stp=None) == -1
+    assert upd(x_prev=None) == -1 and "x_prev" in _err(L)
+    assert upd(m2=None) == -1 and "m_{k-2}" in _err(L)
+    assert upd(m1=None) == -1
+    assert upd(n_el=66) == -2
+    assert upd(dt=7) == -3
+    assert upd(m2=A2 + 8) == -4
+    assert upd(xc=A4) == -5                     # x_c on m_k
+    assert upd(xn=A5 + 16) == -5                # x_next overlaps x_c
+    assert upd(n_el=0, xc=A1, xn=A0) == 0       # in place (x_c on x_prev, x_next on x_cur); n = 0 launches nothing
+    assert L.gc_unipc_coeffs(ctypes.byref(ddim), 10, 0, 2, 1, ctypes.byref(st)) == 0
+    assert st.use_corrector == 0 and st.predictor_order == 1 and st.p_mk1 == 0.0
+    assert upd(x_cur=None) == -1 and "x_cur" in _err(L)
+    anchors = (ctypes.c_int32 * 2)(0, 3)
+    big = 1 * 6 * 8 * 8 * 16 * 4
+
+    def fused(xc=A5, xn=A5 + big, x_cur=A4 + big, out=A4 + 2 * big):
+        return L.gc_transport_unipc(A0, A1, A2, A3, None, None, 0, x_cur, None, None, 1, 6, 8, 8, 16, anchors, 2, 4,
+                                    0, ctypes.byref(st), out, xc, xn, None)
+
+    assert fused(xc=None) == -1
+    assert fused(x_cur=None) == -1
+    assert fused(xn=A5 + 64) == -5              # x_next overlaps x_c
+    assert fused(out=A0 + 64) == -5             # x0_out overlaps x0_prev

@@ -483,8 +483,10 @@ def test_patch_token_granularity(gc):
     np.testing.assert_array_equal(corr.cpu().numpy(), corr_o)
     rs = np.random.default_rng(9)
     C = 4 * 16                                                # 2x2 patch of a 16-channel latent
-    prev = synth.storage(rs.standard_normal((1, w.N, 32, 32, C)).astype(np.float32), "bf16")
-    new = synth.storage(rs.standard_normal((1, w.a, 32, 32, C)).astype(np.float32), "bf16")
+    # std 0.5 keeps every transported value inside |x| < 8, the range the
+    # bfloat16 bar is stated for (half an ulp there is 2^-6)
+    prev = synth.storage(0.5 * rs.standard_normal((1, w.N, 32, 32, C)).astype(np.float32), "bf16")
+    new = synth.storage(0.5 * rs.standard_normal((1, w.a, 32, 32, C)).astype(np.float32), "bf16")
     ex, st = oracle.transport(prev, new, corr_o, wts_o, A, "bf16")
     idx = gc.gc_index_correspondence(corr)
     out = gc.gc_transport_step(to_dev(prev, "bf16"), to_dev(new, "bf16"), corr, wts, A, index=idx)

@@ -1,0 +1,149 @@
+"""Multistep (UniPC) sampler-consistent update on the GPU against the oracle.
+
+Bars as for the other sampler outputs: float32 1e-5, bfloat16 2e-2 against
+the oracle's unrounded double values (inputs identical; random inputs have
+std 0.5 so that outputs stay inside |x| < 8, the range the bars are stated
+for).  The fused cached
+step equals transport followed by the update bit for bit.  The trajectory
+test runs the paper's headline operating point on the Hunyuan-shaped
+workload: a = 2 of N = 6 views over 10 UniPC steps, four of them full
+(two-step head, one mid refresh, one tail).
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+from synth.configs import C2, C4, C5
+
+from conftest import latent_maps
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda:0"
+TOL = {"f32": 1e-5, "bf16": 2e-2}
+
+
+def to_dev(arr, dtype):
+    if dtype == "f32":
+        return torch.from_numpy(np.ascontiguousarray(arr)).to(DEV)
+    return torch.from_numpy(np.ascontiguousarray(arr).view(np.int16)).to(DEV).view(torch.bfloat16)
+
+
+def to_host(t, dtype):
+    return t.cpu().numpy() if dtype == "f32" else t.view(torch.int16).cpu().numpy().view(np.uint16)
+
+
+def vals(t, dtype):
+    return synth.values(to_host(t, dtype), dtype).astype(np.float64)
+
+
+@pytest.fixture(scope="module")
+def gc():
+    import paper_2608_13255_amd as gc
+    return gc
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("order,corrector", [(2, True), (1, True), (1, False), (2, False)])
+def test_unipc_update_parity(gc, dtype, order, corrector):
+    S = 10
+    rs = np.random.default_rng(order * 10 + int(corrector))
+    n = 4096 + 8
+    xs = [synth.storage(0.5 * rs.standard_normal(n).astype(np.float32), dtype) for _ in range(5)]
+    smp = gc.Sampler(kind=gc.GC_DDIM)
+    for k in range(S):
+        co = oracle.unipc_coeffs(S, k, order, corrector)
+        st = gc.gc_unipc_coeffs(smp, S, k, order, corrector)
+        x_cur, x_prev, m2, m1, mk = xs
+        xc_o, xn_o = oracle.unipc_apply(co, x_cur, x_prev, m2, m1, mk, dtype)
+        xc, xn = gc.gc_unipc_update(st, to_dev(mk, dtype), x_cur=to_dev(x_cur, dtype), x_prev=to_dev(x_prev, dtype),
+                                    m_km2=to_dev(m2, dtype), m_km1=to_dev(m1, dtype))
+        assert np.abs(vals(xc, dtype) - xc_o).max() <= TOL[dtype], k
+        assert np.abs(vals(xn, dtype) - xn_o).max() <= TOL[dtype], k
+
+
+@pytest.mark.parametrize("w", [C2, C4, C5], ids=lambda w: w.name)
+def test_transport_unipc_parity(gc, w):
+    P = latent_maps(w.name)
+    A = oracle.anchors(w.N, w.a, 1)
+    S, k = 10, 4
+    rs = np.random.default_rng(3)
+    shape = (w.B, w.N, w.H, w.W, w.C)
+    x_prev, m2, m1, xcur = (synth.storage(0.5 * rs.standard_normal(shape).astype(np.float32), w.dtype)
+                            for _ in range(4))
+    new = synth.storage(synth.values(m1, w.dtype)[:, A] + 0.1 * rs.standard_normal((w.B, w.a) + shape[2:]).astype(np.float32), w.dtype)
+    corr_o, wts_o, _ = oracle.build(P, synth.batch_cameras(w), A, w.K, oracle.bbox(P, w.tol_frac))
+    mk_exact, mk_state = oracle.transport(m1, new, corr_o, wts_o, A, w.dtype)
+    co = oracle.unipc_coeffs(S, k, 2, True)
+    xc_o, xn_o = oracle.unipc_apply(co, xcur, x_prev, m2, m1, mk_state, w.dtype)
+    Pd = torch.from_numpy(P).to(DEV)
+    corr, wts = gc.gc_build_correspondence(Pd, gc.camera_tensor(synth.batch_cameras(w), DEV), A, w.K,
+                                           gc.gc_posmap_bbox(Pd, w.tol_frac))
+    idx = gc.gc_index_correspondence(corr)
+    st = gc.gc_unipc_coeffs(gc.Sampler(kind=gc.GC_DDIM), S, k, 2, True)
+    args = [to_dev(a_, w.dtype) for a_ in (m1, new, xcur, x_prev, m2)]
+    iv = torch.int16 if w.dtype == "bf16" else torch.int32
+    outs = []
+    for index in (None, idx):
+        mk, xc, xn = gc.gc_transport_unipc(args[0], args[1], corr, wts, A, st, x_cur=args[2], x_prev=args[3],
+                                           m_km2=args[4], index=index)
+        assert np.abs(vals(mk, w.dtype) - mk_exact).max() <= TOL[w.dtype]
+        same = np.ones(shape, bool) if w.dtype == "f32" else to_host(mk, w.dtype) == mk_state
+        assert same.mean() > 0.999
+        assert np.abs(vals(xc, w.dtype) - xc_o)[same].max() <= TOL[w.dtype]
+        assert np.abs(vals(xn, w.dtype) - xn_o)[same].max() <= TOL[w.dtype]
+        outs.append((mk, xc, xn))
+    for a_, b_ in zip(*outs):                          # split launch == plain launch
+        assert torch.equal(a_.view(iv), b_.view(iv))
+    # fused == transport then update
+    mk2 = gc.gc_transport_step(args[0], args[1], corr, wts, A, index=idx)
+    xc2, xn2 = gc.gc_unipc_update(st, mk2, x_cur=args[2], x_prev=args[3], m_km2=args[4], m_km1=args[0])
+    assert torch.equal(mk2.view(iv), outs[0][0].view(iv))
+    assert torch.equal(xc2.view(iv), outs[0][1].view(iv)) and torch.equal(xn2.view(iv), outs[0][2].view(iv))
+
+
+def test_unipc_trajectory_headline_operating_point(gc):
+    from paper_2608_13255_amd.runner import GeoCacheRunner
+    w = synth.shrink(C2, S=10)
+    S = 10
+    P = latent_maps(C2.name)
+    cams = synth.batch_cameras(w)
+    full = GeoCacheRunner.full_steps("head_mid_tail", S)
+    assert [k for k in range(S) if full[k]] == [0, 1, 5, 9]
+    preds = {}
+
+    def stub_np(k, views):
+        key = (k, tuple(views))
+        if key not in preds:
+            preds[key] = synth.storage(synth.x0_state(w, P, k, views=views), w.dtype)
+        return preds[key]
+
+    xt0 = synth.storage(synth.eps_noise(w, 0), w.dtype)
+    ref = oracle.trajectory_unipc(xt0, stub_np, P, cams, w.K, w.tol_frac, w.dtype, S, full, w.a, order=2)
+    runner = GeoCacheRunner(torch.from_numpy(P).to(DEV), gc.camera_tensor(cams, DEV), w.a, w.K,
+                            gc.Sampler(kind=gc.GC_DDIM), S, full, w.tol_frac, unipc_order=2)
+
+    def predict(k, views):
+        return to_dev(stub_np(k, views), w.dtype)
+
+    for k in range(S):
+        if k == 0:
+            runner.start(to_dev(xt0, w.dtype))
+        else:
+            r1 = ref[k - 1]
+            r2 = ref[k - 2] if k >= 2 else None
+            runner.load_state_dict({"k": k, "c": r1["c"], "x_t": to_dev(r1["x_t"], w.dtype),
+                                    "x0": to_dev(r1["x0"], w.dtype),
+                                    "x0_km2": to_dev(r2["x0"], w.dtype) if r2 else None,
+                                    "x_c": to_dev(r1["x_c"], w.dtype)})
+        views = runner.step(predict)
+        assert views == ref[k]["anchors"], k
+        assert np.abs(vals(runner.x0, w.dtype) - ref[k]["x0_exact"]).max() <= TOL[w.dtype], k
+        assert np.abs(vals(runner.x_c, w.dtype) - ref[k]["x_c_exact"]).max() <= TOL[w.dtype], k
+        assert np.abs(vals(runner.x_t, w.dtype) - ref[k]["x_t_exact"]).max() <= TOL[w.dtype], k
+    runner.start(to_dev(xt0, w.dtype))
+    runner.run(predict)
+    drift = float(np.abs(vals(runner.x_t, w.dtype) - synth.values(ref[-1]["x_t"], w.dtype)).max())
+    print(f"UniPC-2 headline point: free-running drift after {S} steps: {drift:.3g}")
+    assert drift <= 1e-4
