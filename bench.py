@@ -18,6 +18,7 @@ The once-per-asset rows (area downsample, bbox, correspondence builds) and
 the unfused pair are timed too and reported under "rows".
 """
 import argparse
+import ctypes
 import hashlib
 import json
 import math
@@ -55,7 +56,7 @@ def log(args, *a):
 
 def kernel_source_hash():
     h = hashlib.sha256()
-    for f in ("gc_transport.hip", "gc_common.h"):
+    for f in ("gc_transport.hip", "gc_latent.h", "gc_common.h"):
         h.update(open(os.path.join(ROOT, "paper_2608_13255_amd", "csrc", f), "rb").read())
     return h.hexdigest()[:16]
 
@@ -266,6 +267,29 @@ def main():
               + 4 * K * vis_pairs[anchor_sets[0]])
     rows["unipc_fused_GBps"] = ubytes / (rows["unipc_fused_ms"] * 1e-3) / 1e9
     del uplans
+
+    # the same cached step with G_{A->v} computed on the fly (no stored operator);
+    # algorithmic bytes: the latents as above, 12 B of position per target token,
+    # the anchors' position maps once
+    L = gc.lib()
+    smp_c = smp.c()
+    arr0 = (ctypes.c_int32 * a)(*A0)
+    gargs = []
+    for b in ring[:2]:
+        gargs.append((b["x0_prev"].data_ptr(), b["x0_new"].data_ptr(), pos.data_ptr(), cams.data_ptr(), bbox.data_ptr(),
+                      b["x_t"].data_ptr(), B, N, H, W, C, arr0, a, K, gc.dtype_code(b["x0_prev"]), ctypes.byref(smp_c),
+                      tt, ttn, b["x0_out"].data_ptr(), b["x_next"].data_ptr(), None,
+                      torch.cuda.current_stream().cuda_stream))
+    gi = iter(range(1 << 30))
+
+    def geom_call():
+        rc = L.gc_transport_reconstruct_geom(*gargs[next(gi) % len(gargs)])
+        if rc != 0:
+            raise RuntimeError(L.gc_last_error().decode())
+
+    rows["geom_fused_ms"] = timed(geom_call)
+    gbytes = B * (4 * N + a) * latent_view + 12 * n_tok + 12 * B * a * HW
+    rows["geom_fused_GBps"] = gbytes / (rows["geom_fused_ms"] * 1e-3) / 1e9
     rows["coverage_per_anchor_set"] = [round(cover[A], 4) for A in anchor_sets]
     rows["visible_pairs_per_anchor_set"] = [vis_pairs[A] for A in anchor_sets]
     rows["visible_tokens_per_anchor_set"] = [index[A].n_vis for A in anchor_sets]

@@ -16,6 +16,8 @@
  *                        gc_sampler_reconstruct sampler-consistent eps / v / velocity + x_t update
  *                        gc_transport_reconstruct  the two above fused in one pass
  *                        gc_unipc_update, gc_transport_unipc  multistep (UniPC) variant
+ *                        gc_transport_step_geom, gc_transport_reconstruct_geom
+ *                                               the same with G_{A->v} computed on the fly
  *   host schedule        gc_schedule_anchors, gc_schedule_full_steps, gc_sampler_step_times
  *
  * Conventions shared by every call
@@ -341,6 +343,32 @@ int gc_transport_unipc(const void* x0_prev, const void* x0_anchor_new, const int
                        const void* x_prev, const void* m_km2, int B, int N, int H, int W, int C,
                        const int32_t* anchors, int a, int K, int dtype, const gc_unipc_step* st, void* x0_out,
                        void* x_c, void* x_next, hipStream_t stream);
+
+/*
+ * Cached step with the correspondence computed on the fly (Sec. 3.2: the
+ * operator depends on geometry alone).  Instead of a stored G_{A->v}, the
+ * kernel projects every target token into the anchor cameras and runs the
+ * same tap test, selection and weighting as gc_build_correspondence, then
+ * applies Eq. 1 (and, for the _reconstruct variant, the sampler step).  The
+ * outputs equal gc_build_correspondence + gc_transport_step (+ the sampler
+ * step of gc_transport_reconstruct) bit for bit.  Nothing is built or stored
+ * per anchor set, which suits anchor sets that do not repeat; the stored
+ * operator with its index is cheaper per step when they do.
+ *   pos    device float32 [B][N][H][W][3] latent-grid position maps (NaN = background)
+ *   cams   device gc_camera [B][N]
+ *   bbox   device float32 [B][8] from gc_posmap_bbox (element 6 = squared tolerance)
+ * Other arguments as for gc_transport_step / gc_transport_reconstruct.
+ * x0_out, x_next and model_out must not overlap any input (x_next may be
+ * x_t); latents and pos 16-byte aligned.
+ */
+int gc_transport_step_geom(const void* x0_prev, const void* x0_anchor_new, const float* pos, const gc_camera* cams,
+                           const float* bbox, int B, int N, int H, int W, int C, const int32_t* anchors, int a, int K,
+                           int dtype, void* x0_out, hipStream_t stream);
+int gc_transport_reconstruct_geom(const void* x0_prev, const void* x0_anchor_new, const float* pos,
+                                  const gc_camera* cams, const float* bbox, const void* x_t, int B, int N, int H,
+                                  int W, int C, const int32_t* anchors, int a, int K, int dtype,
+                                  const gc_sampler* smp, double t, double t_next, void* x0_out, void* x_next,
+                                  void* model_out, hipStream_t stream);
 
 /*
  * Host schedule (no device work).

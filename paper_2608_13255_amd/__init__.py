@@ -105,6 +105,11 @@ def lib() -> ctypes.CDLL:
             "gc_unipc_update": ([_vp, _vp, _vp, _vp, _vp, _i64, _i, ctypes.POINTER(UniPCStep), _vp, _vp, _vp], _i),
             "gc_transport_unipc": ([_vp, _vp, _vp, _vp, _vp, _vp, _i64, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i32p,
                                     _i, _i, _i, ctypes.POINTER(UniPCStep), _vp, _vp, _vp, _vp], _i),
+            "gc_transport_step_geom": ([_vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i32p, _i, _i, _i, _vp, _vp],
+                                       _i),
+            "gc_transport_reconstruct_geom": ([_vp, _vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i32p, _i, _i, _i,
+                                               ctypes.POINTER(_Sampler), ctypes.c_double, ctypes.c_double, _vp, _vp,
+                                               _vp, _vp], _i),
             "gc_schedule_anchors": ([_i, _i, _i64, _i32p], _i),
             "gc_schedule_full_steps": ([_i, _i, _i, ctypes.POINTER(ctypes.c_uint8)], _i),
             "gc_sampler_step_times": ([ctypes.POINTER(_Sampler), _i, _i, ctypes.POINTER(ctypes.c_double),
@@ -345,6 +350,61 @@ def gc_transport_reconstruct(x0_prev: torch.Tensor, x0_anchor_new: torch.Tensor,
                                           ctypes.byref(smp), float(t), float(t_next), _dev(x0_out, "x0_out"),
                                           _dev(x_next, "x_next"), _opt(model_out, "model_out"), _stream(stream)),
            "gc_transport_reconstruct")
+    return x0_out, x_next, model_out
+
+
+def _geom_inputs(x0_prev, x0_anchor_new, pos, cams, bbox, anchors):
+    B, N, H, W, C = _latent_shape(x0_prev)
+    arr, a = _anchors(anchors)
+    if tuple(x0_anchor_new.shape) != (B, a, H, W, C) or x0_anchor_new.dtype != x0_prev.dtype:
+        raise ValueError(f"x0_anchor_new must be [B, a={a}, H, W, C] of the same dtype as x0_prev")
+    if pos.dtype != torch.float32 or tuple(pos.shape) != (B, N, H, W, 3):
+        raise ValueError(f"pos must be float32 [B={B}, N={N}, H={H}, W={W}, 3]")
+    if cams.dtype != torch.uint8 or tuple(cams.shape) != (B, N, 68):
+        raise ValueError(f"cams must be uint8 [B={B}, N={N}, 68]")
+    if bbox.dtype != torch.float32 or tuple(bbox.shape) != (B, 8):
+        raise ValueError(f"bbox must be float32 [B={B}, 8]")
+    return (B, N, H, W, C), arr, a
+
+
+def gc_transport_step_geom(x0_prev: torch.Tensor, x0_anchor_new: torch.Tensor, pos: torch.Tensor,
+                           cams: torch.Tensor, bbox: torch.Tensor, anchors: Sequence[int], K: int,
+                           x0_out: torch.Tensor = None, stream=None) -> torch.Tensor:
+    """Eq. 1 with G_{A->v} computed on the fly from the position maps
+    (pos float32 [B, N, H, W, 3], cams from camera_tensor, bbox from
+    gc_posmap_bbox); equals gc_build_correspondence + gc_transport_step."""
+    (B, N, H, W, C), arr, a = _geom_inputs(x0_prev, x0_anchor_new, pos, cams, bbox, anchors)
+    if x0_out is None:
+        x0_out = torch.empty_like(x0_prev)
+    _check(lib().gc_transport_step_geom(_dev(x0_prev, "x0_prev"), _dev(x0_anchor_new, "x0_anchor_new"),
+                                        _dev(pos, "pos"), _dev(cams, "cams"), _dev(bbox, "bbox"), B, N, H, W, C, arr,
+                                        a, K, dtype_code(x0_prev), _dev(x0_out, "x0_out"), _stream(stream)),
+           "gc_transport_step_geom")
+    return x0_out
+
+
+def gc_transport_reconstruct_geom(x0_prev: torch.Tensor, x0_anchor_new: torch.Tensor, pos: torch.Tensor,
+                                  cams: torch.Tensor, bbox: torch.Tensor, x_t: torch.Tensor, anchors: Sequence[int],
+                                  K: int, sampler: Sampler, t: float, t_next: float, x0_out: torch.Tensor = None,
+                                  x_next: torch.Tensor = None, model_out: torch.Tensor = None, stream=None):
+    """gc_transport_reconstruct with G_{A->v} computed on the fly; returns
+    (x0_out, x_next, model_out or None)."""
+    (B, N, H, W, C), arr, a = _geom_inputs(x0_prev, x0_anchor_new, pos, cams, bbox, anchors)
+    if x_t.shape != x0_prev.shape or x_t.dtype != x0_prev.dtype:
+        raise ValueError("x_t must match x0_prev in shape and dtype")
+    if x0_out is None:
+        x0_out = torch.empty_like(x0_prev)
+    if x_next is None:
+        x_next = torch.empty_like(x_t)
+    if sampler.pred_out != GC_PRED_NONE and model_out is None:
+        model_out = torch.empty_like(x_t)
+    smp = sampler.c()
+    _check(lib().gc_transport_reconstruct_geom(_dev(x0_prev, "x0_prev"), _dev(x0_anchor_new, "x0_anchor_new"),
+                                               _dev(pos, "pos"), _dev(cams, "cams"), _dev(bbox, "bbox"),
+                                               _dev(x_t, "x_t"), B, N, H, W, C, arr, a, K, dtype_code(x0_prev),
+                                               ctypes.byref(smp), float(t), float(t_next), _dev(x0_out, "x0_out"),
+                                               _dev(x_next, "x_next"), _opt(model_out, "model_out"),
+                                               _stream(stream)), "gc_transport_reconstruct_geom")
     return x0_out, x_next, model_out
 
 

@@ -11,6 +11,7 @@
 // visible pairs / tokens / taps with ballot + popcount before one lane adds
 // them to the asset's counters.
 #include "gc_common.h"
+#include "gc_geometry.h"
 
 namespace gc {
 namespace {
@@ -81,98 +82,12 @@ __global__ __launch_bounds__(kBlock) void k_build(BuildArgs g) {
   float wk[4] = {0.f, 0.f, 0.f, 0.f};   // this anchor's normalised weight of tap k
   int mask = 0;
   if (live && fg) {
-    const gc_camera& cam = cam_lds[s];
-    const int u = g.anchor_view[s];
-    const float* R = cam.R;
-    const float xc = ((R[0] * P[0] + R[1] * P[1]) + R[2] * P[2]) + cam.t[0];
-    const float yc = ((R[3] * P[0] + R[4] * P[1]) + R[5] * P[2]) + cam.t[1];
-    const float zc = ((R[6] * P[0] + R[7] * P[1]) + R[8] * P[2]) + cam.t[2];
-    float px = 0.f, py = 0.f;
-    bool ok = true;
-    if (cam.model == 0) {
-      ok = zc > 0.0f;
-      if (ok) {
-        px = cam.fx * (xc / zc) + cam.cx;
-        py = cam.fy * (yc / zc) + cam.cy;
-      }
-    } else if (cam.model == 1) {
-      px = cam.fx * xc + cam.cx;
-      py = cam.fy * yc + cam.cy;
-    } else {
-      ok = false;
-    }
-    ok = ok && finite_f(px) && finite_f(py) && !(px < -2.0f || px > (float)g.W + 2.0f || py < -2.0f ||
-                                                  py > (float)g.H + 2.0f);
-    if (ok) {
-      const float gx = px - 0.5f, gy = py - 0.5f;
-      const float fx0 = floorf(gx), fy0 = floorf(gy);
-      const float ax = gx - fx0, ay = gy - fy0;
-      const int x0 = (int)fx0, y0 = (int)fy0;
-      const float* src = g.pos + ((int64_t)b * g.N + u) * HW * 3;
-      bool valid[4];
-      float d2[4];
-      int nvalid = 0;
+    const AnchorTaps at = anchor_taps(P, cam_lds[s], g.pos + ((int64_t)b * g.N + g.anchor_view[s]) * HW * 3, g.H,
+                                      g.W, g.K, tol2);
+    word = at.word;
+    mask = at.mask;
 #pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        const int x = x0 + (k & 1), y = y0 + (k >> 1);
-        valid[k] = false;
-        d2[k] = 0.0f;
-        if (x < 0 || x >= g.W || y < 0 || y >= g.H) continue;
-        const float* Q = src + ((int64_t)y * g.W + x) * 3;
-        const float qx = Q[0], qy = Q[1], qz = Q[2];
-        if (!(finite_f(qx) && finite_f(qy) && finite_f(qz))) continue;
-        const float dx = qx - P[0], dy = qy - P[1], dz = qz - P[2];
-        const float dd = (dx * dx + dy * dy) + dz * dz;
-        if (!(dd <= tol2)) continue;
-        valid[k] = true;
-        d2[k] = dd;
-        ++nvalid;
-      }
-      if (nvalid > 0) {
-        bool sel[4] = {false, false, false, false};
-        if (nvalid <= g.K) {
-#pragma unroll
-          for (int k = 0; k < 4; ++k) sel[k] = valid[k];
-        } else {
-          for (int r = 0; r < g.K; ++r) {
-            int best = -1;
-#pragma unroll
-            for (int k = 0; k < 4; ++k) {
-              if (!valid[k] || sel[k]) continue;
-              if (best < 0 || d2[k] < d2[best]) best = k;
-            }
-            sel[best] = true;
-          }
-        }
-        const float wx[2] = {1.0f - ax, ax};
-        const float wy[2] = {1.0f - ay, ay};
-        float area[4];
-        float S = 0.0f;
-#pragma unroll
-        for (int k = 0; k < 4; ++k) {
-          area[k] = sel[k] ? wx[k & 1] * wy[k >> 1] : 0.0f;
-          S = S + area[k];
-        }
-        if (S > 0.0f) {
-#pragma unroll
-          for (int k = 0; k < 4; ++k) {
-            if (sel[k] && area[k] > 0.0f) {
-              wk[k] = area[k] / S;
-              mask |= 1 << k;
-            }
-          }
-        } else {
-          int best = -1;
-#pragma unroll
-          for (int k = 0; k < 4; ++k)
-            if (sel[k] && (best < 0 || d2[k] < d2[best])) best = k;
-#pragma unroll
-          for (int k = 0; k < 4; ++k) wk[k] = k == best ? 1.0f : 0.0f;
-          mask = 1 << best;
-        }
-        word = (int32_t)((uint32_t)(x0 + 1) | ((uint32_t)(y0 + 1) << 12) | ((uint32_t)mask << 24));
-      }
-    }
+    for (int k = 0; k < 4; ++k) wk[k] = at.wk[k];
   }
 
   // n_vis: anchors of this token that see it -- a ballot over the lane group

@@ -1,0 +1,304 @@
+// Cached step with the correspondence computed on the fly: Eq. 1 (and the
+// sampler reconstruction) reading the position maps and cameras directly
+// instead of a stored G_{A->v}.  The operator depends on geometry alone
+// (Sec. 3.2, correspondence operator), so it can be rebuilt inside the step
+// from 12 bytes of position per target token plus the anchors' position
+// taps; nothing has to be built or stored per anchor set.  That pays when
+// anchor sets do not repeat (e.g. chosen adaptively); with the rotation's
+// few repeating sets the stored operator and its visible-token index are
+// cheaper per step.
+//
+// Work mapping: a group of G = 4 (a <= 4) or 8 adjacent lanes serves one
+// token.  On a target token lane s evaluates anchor slot s exactly as the
+// builder does (same device function, same float order), n_vis is a ballot
+// over the group, and the group's lanes read every anchor's word and
+// weights from each other with cross-lane permutes; lane j then gathers and
+// blends the channel vectors j, j + G, ...  Weights are the builder's
+// stored values (w_k / n_vis in float), so the result equals
+// gc_build_correspondence followed by gc_transport_step bit for bit.
+// Anchor rows copy the new prediction.  Blocks never straddle a view and
+// are dealt to XCDs in contiguous slices, as in the stored-operator kernel.
+#include "gc_common.h"
+#include "gc_geometry.h"
+#include "gc_latent.h"
+
+namespace gc {
+namespace {
+
+constexpr int kBlock = 256;
+
+enum GeomMode { kGeomTransport = 0, kGeomReconstruct = 1 };
+
+struct GArgs {
+  const void* x0_prev;
+  const void* x0_new;
+  const float* pos;
+  const gc_camera* cams;
+  const float* bbox;
+  const void* x_t;
+  void* x0_out;
+  void* x_next;
+  void* model_out;
+  int N, H, W, HW, C, a, K, CV;
+  int bpv;        // blocks per view: ceil(HW / tokens per block)
+  int n_blocks;   // B * N * bpv
+  int32_t anchor_view[GC_MAX_ANCHORS];
+  Recon r;
+};
+
+template <int DT, int VEC, int MODE, int G>
+__global__ __launch_bounds__(kBlock) void k_transport_geom(GArgs g) {
+  using CD = Codec<DT, VEC>;
+  using Raw = typename CD::Raw;
+  constexpr int kTok = kBlock / G;   // tokens per block
+  __shared__ gc_camera cam_lds[GC_MAX_ANCHORS];
+  const int lb = logical_block((int)blockIdx.x, g.n_blocks, 1);
+  if (lb >= g.n_blocks) return;   // XCD padding: whole block
+  const int bv = __builtin_amdgcn_readfirstlane(lb / g.bpv);   // b * N + v
+  const int b = __builtin_amdgcn_readfirstlane(bv / g.N);
+  const int v = bv - b * g.N;
+  int s_self = -1;
+#pragma unroll
+  for (int s = 0; s < GC_MAX_ANCHORS; ++s)
+    if (s < g.a && g.anchor_view[s] == v) s_self = s;
+  const int lane_g = (int)threadIdx.x & (G - 1);
+  const int p = (lb - bv * g.bpv) * kTok + (int)threadIdx.x / G;
+  const bool tok_ok = p < g.HW;
+  const int64_t tbase = ((int64_t)bv * g.HW + p) * g.C;   // this token's first element
+
+  if (s_self >= 0) {   // anchor row (block-uniform): the store takes the new prediction
+    if (!tok_ok) return;
+    const int64_t nbase = (((int64_t)b * g.a + s_self) * g.HW + p) * g.C;
+    for (int c = lane_g; c < g.CV; c += G) {
+      const int64_t e = tbase + (int64_t)c * VEC;
+      Raw xtr;
+      if constexpr (MODE == kGeomReconstruct) xtr = CD::load_stream(g.x_t, e);
+      const Raw x0r = CD::load(g.x0_new, nbase + (int64_t)c * VEC);
+      CD::store_stream(g.x0_out, e, x0r);
+      if constexpr (MODE == kGeomReconstruct) {
+        float xtf[VEC], x0f[VEC], xn[VEC], mo[VEC];
+        CD::unpack(xtr, xtf);
+        CD::unpack(x0r, x0f);
+        reconstruct_vec<VEC>(g.r, xtf, x0f, xn, mo);
+        CD::store_stream(g.x_next, e, CD::pack(xn));
+        if (g.model_out) CD::store_stream(g.model_out, e, CD::pack(mo));
+      }
+    }
+    return;
+  }
+
+  // target token: lane s of the group evaluates anchor slot s
+  if (threadIdx.x < g.a) cam_lds[threadIdx.x] = g.cams[(int64_t)b * g.N + g.anchor_view[threadIdx.x]];
+  __syncthreads();
+  float P[3] = {0.f, 0.f, 0.f};
+  bool fg = false;
+  if (tok_ok) {
+    const float* pp = g.pos + ((int64_t)bv * g.HW + p) * 3;
+    P[0] = pp[0];
+    P[1] = pp[1];
+    P[2] = pp[2];
+    fg = finite_f(P[0]) && finite_f(P[1]) && finite_f(P[2]);
+  }
+  AnchorTaps at;
+  at.word = 0;
+  at.mask = 0;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) at.wk[k] = 0.0f;
+  if (tok_ok && fg && lane_g < g.a)
+    at = anchor_taps(P, cam_lds[lane_g], g.pos + ((int64_t)b * g.N + g.anchor_view[lane_g]) * g.HW * 3, g.H, g.W,
+                     g.K, g.bbox[(int64_t)b * 8 + 6]);
+  // every lane reaches the ballot and the permutes below (no early exit)
+  const unsigned long long seen = __ballot(at.word != 0);
+  const int gbase = __lane_id() & ~(G - 1);
+  const int n_vis = __popcll((seen >> gbase) & ((1ull << G) - 1));
+  const float inv = n_vis > 0 ? (float)n_vis : 1.0f;
+  const int rounds = (g.CV + G - 1) / G;
+  for (int r = 0; r < rounds; ++r) {
+    const int c = r * G + lane_g;
+    const bool act = tok_ok && c < g.CV;
+    const int64_t e = tbase + (int64_t)c * VEC;
+    Raw xtr, prevr;
+    if (act) {
+      if constexpr (MODE == kGeomReconstruct) xtr = CD::load_stream(g.x_t, e);
+      prevr = CD::load_stream(g.x0_prev, e);
+    }
+    float acc[VEC];
+#pragma unroll
+    for (int q = 0; q < VEC; ++q) acc[q] = 0.0f;
+    for (int s = 0; s < g.a; ++s) {
+      const uint32_t w = (uint32_t)__shfl(at.word, gbase + s);
+      float wk[4];
+#pragma unroll
+      for (int k = 0; k < 4; ++k) wk[k] = __shfl(at.wk[k], gbase + s);
+      if (!act || !w) continue;
+      const int x0 = (int)(w & 0xfffu) - 1;
+      const int y0 = (int)((w >> 12) & 0xfffu) - 1;
+      const uint32_t mask = (w >> 24) & 0xfu;
+      const int64_t new_view = ((int64_t)b * g.a + s) * g.HW;
+      const int64_t old_view = ((int64_t)b * g.N + g.anchor_view[s]) * g.HW;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        if (!(mask & (1u << k))) continue;
+        const int q = (y0 + (k >> 1)) * g.W + x0 + (k & 1);
+        const float wt = wk[k] / inv;   // the builder's stored weight
+        float nf[VEC], of[VEC];
+        CD::unpack(CD::load(g.x0_new, (new_view + q) * g.C + (int64_t)c * VEC), nf);
+        CD::unpack(CD::load(g.x0_prev, (old_view + q) * g.C + (int64_t)c * VEC), of);
+#pragma unroll
+        for (int q2 = 0; q2 < VEC; ++q2) acc[q2] = acc[q2] + wt * (nf[q2] - of[q2]);
+      }
+    }
+    if (!act) continue;
+    Raw x0r;
+    float x0f[VEC];
+    if (n_vis == 0) {
+      x0r = prevr;   // no anchor sees this token: it keeps its own state
+    } else {
+      float prevf[VEC], y[VEC];
+      CD::unpack(prevr, prevf);
+#pragma unroll
+      for (int q = 0; q < VEC; ++q) y[q] = prevf[q] + acc[q];
+      x0r = CD::pack(y);
+    }
+    CD::store_stream(g.x0_out, e, x0r);
+    if constexpr (MODE == kGeomReconstruct) {
+      float xtf[VEC], xn[VEC], mo[VEC];
+      CD::unpack(x0r, x0f);   // the reconstruction reads x0 as stored
+      CD::unpack(xtr, xtf);
+      reconstruct_vec<VEC>(g.r, xtf, x0f, xn, mo);
+      CD::store_stream(g.x_next, e, CD::pack(xn));
+      if (g.model_out) CD::store_stream(g.model_out, e, CD::pack(mo));
+    }
+  }
+}
+
+int prepare_geom(const void* x0_prev, const void* x0_new, const float* pos, const gc_camera* cams, const float* bbox,
+                 int B, int N, int H, int W, int C, const int32_t* anchors, int a, int K, int dtype, void* x0_out,
+                 const char* who, GArgs* g) {
+  if (!x0_prev || !x0_new || !pos || !cams || !bbox || !anchors || !x0_out)
+    return fail(GC_ERR_ARG, "%s: null pointer", who);
+  if (dtype != GC_F32 && dtype != GC_BF16) return fail(GC_ERR_DTYPE, "%s: unknown dtype %d", who, dtype);
+  if (B < 1 || N < 1 || H < 1 || W < 1 || C < 1)
+    return fail(GC_ERR_SHAPE, "%s: bad shape B=%d N=%d H=%d W=%d C=%d", who, B, N, H, W, C);
+  if (C % 4) return fail(GC_ERR_SHAPE, "%s: C=%d is not a multiple of 4", who, C);
+  if (C > GC_MAX_CHANNELS) return fail(GC_ERR_CAPACITY, "%s: C=%d exceeds %d", who, C, GC_MAX_CHANNELS);
+  if (N > GC_MAX_VIEWS) return fail(GC_ERR_CAPACITY, "%s: N=%d exceeds %d", who, N, GC_MAX_VIEWS);
+  if (H > GC_MAX_GRID || W > GC_MAX_GRID) return fail(GC_ERR_CAPACITY, "%s: grid %dx%d exceeds %d", who, H, W, GC_MAX_GRID);
+  if (a < 1 || a > N) return fail(GC_ERR_ARG, "%s: a=%d outside [1, N=%d]", who, a, N);
+  if (a > GC_MAX_ANCHORS) return fail(GC_ERR_CAPACITY, "%s: a=%d exceeds %d", who, a, GC_MAX_ANCHORS);
+  if (K < 1 || K > 4) return fail(GC_ERR_ARG, "%s: K=%d outside [1, 4]", who, K);
+  if (!aligned16(x0_prev) || !aligned16(x0_new) || !aligned16(x0_out) || !aligned16(pos))
+    return fail(GC_ERR_ALIGN, "%s: latents and position maps must be 16-byte aligned", who);
+  std::memset(g, 0, sizeof(*g));
+  bool is_anchor[GC_MAX_VIEWS] = {};
+  for (int s = 0; s < a; ++s) {
+    const int u = anchors[s];
+    if (u < 0 || u >= N) return fail(GC_ERR_ARG, "%s: anchor %d outside [0, %d)", who, u, N);
+    if (is_anchor[u]) return fail(GC_ERR_ARG, "%s: anchor %d listed twice", who, u);
+    is_anchor[u] = true;
+    g->anchor_view[s] = u;
+  }
+  const size_t es = (size_t)dtype_bytes(dtype);
+  const size_t HW = (size_t)H * W;
+  const size_t n_all = (size_t)B * N * HW * C * es, n_new = (size_t)B * a * HW * C * es;
+  if (overlaps(x0_out, n_all, x0_prev, n_all) || overlaps(x0_out, n_all, x0_new, n_new) ||
+      overlaps(x0_out, n_all, pos, (size_t)B * N * HW * 12) || overlaps(x0_out, n_all, cams, (size_t)B * N * sizeof(gc_camera)) ||
+      overlaps(x0_out, n_all, bbox, (size_t)B * 32))
+    return fail(GC_ERR_ALIAS, "%s: x0_out overlaps an input", who);
+  g->x0_prev = x0_prev;
+  g->x0_new = x0_new;
+  g->pos = pos;
+  g->cams = cams;
+  g->bbox = bbox;
+  g->x0_out = x0_out;
+  g->N = N;
+  g->H = H;
+  g->W = W;
+  g->HW = (int)HW;
+  g->C = C;
+  g->a = a;
+  g->K = K;
+  g->CV = C / pick_vec(dtype, C);
+  const int tok = a <= 4 ? kBlock / 4 : kBlock / 8;
+  g->bpv = (int)(((int64_t)HW + tok - 1) / tok);
+  const int64_t nb = (int64_t)B * N * g->bpv;
+  if (nb > (int64_t)0x7fffffff - kXcds) return fail(GC_ERR_CAPACITY, "%s: problem too large for one launch", who);
+  g->n_blocks = (int)nb;
+  return GC_OK;
+}
+
+template <int MODE>
+void launch_geom(const GArgs& g, int dtype, hipStream_t stream) {
+  const int per = (g.n_blocks + kXcds - 1) / kXcds;
+  const dim3 grid((unsigned)(per * kXcds));
+  const int vec = g.C / g.CV;
+#define GC_LAUNCH_GEOM(DT_, VEC_)                                                                         \
+  do {                                                                                                    \
+    if (g.a <= 4)                                                                                         \
+      hipLaunchKernelGGL((k_transport_geom<DT_, VEC_, MODE, 4>), grid, dim3(kBlock), 0, stream, g);       \
+    else                                                                                                  \
+      hipLaunchKernelGGL((k_transport_geom<DT_, VEC_, MODE, 8>), grid, dim3(kBlock), 0, stream, g);       \
+  } while (0)
+  if (dtype == GC_F32)
+    GC_LAUNCH_GEOM(GC_F32, 4);
+  else if (vec == 8)
+    GC_LAUNCH_GEOM(GC_BF16, 8);
+  else
+    GC_LAUNCH_GEOM(GC_BF16, 4);
+#undef GC_LAUNCH_GEOM
+}
+
+}  // namespace
+}  // namespace gc
+
+using namespace gc;
+
+extern "C" int gc_transport_step_geom(const void* x0_prev, const void* x0_anchor_new, const float* pos,
+                                      const gc_camera* cams, const float* bbox, int B, int N, int H, int W, int C,
+                                      const int32_t* anchors, int a, int K, int dtype, void* x0_out,
+                                      hipStream_t stream) {
+  clear_error();
+  GArgs g;
+  int rc = prepare_geom(x0_prev, x0_anchor_new, pos, cams, bbox, B, N, H, W, C, anchors, a, K, dtype, x0_out,
+                        "gc_transport_step_geom", &g);
+  if (rc) return rc;
+  launch_geom<kGeomTransport>(g, dtype, stream);
+  return after_launch(stream, "gc_transport_step_geom");
+}
+
+extern "C" int gc_transport_reconstruct_geom(const void* x0_prev, const void* x0_anchor_new, const float* pos,
+                                             const gc_camera* cams, const float* bbox, const void* x_t, int B, int N,
+                                             int H, int W, int C, const int32_t* anchors, int a, int K, int dtype,
+                                             const gc_sampler* smp, double t, double t_next, void* x0_out,
+                                             void* x_next, void* model_out, hipStream_t stream) {
+  clear_error();
+  GArgs g;
+  int rc = prepare_geom(x0_prev, x0_anchor_new, pos, cams, bbox, B, N, H, W, C, anchors, a, K, dtype, x0_out,
+                        "gc_transport_reconstruct_geom", &g);
+  if (rc) return rc;
+  if (!x_t || !x_next) return fail(GC_ERR_ARG, "gc_transport_reconstruct_geom: null x_t or x_next");
+  rc = make_recon(smp, t, t_next, &g.r);
+  if (rc) return rc;
+  if ((g.r.pred != GC_PRED_NONE) != (model_out != nullptr))
+    return fail(GC_ERR_ARG, "gc_transport_reconstruct_geom: model_out must be given iff pred_out != GC_PRED_NONE");
+  if (!aligned16(x_t) || !aligned16(x_next) || (model_out && !aligned16(model_out)))
+    return fail(GC_ERR_ALIGN, "gc_transport_reconstruct_geom: device pointers must be 16-byte aligned");
+  const size_t es = (size_t)dtype_bytes(dtype);
+  const size_t HW = (size_t)H * W;
+  const size_t n_all = (size_t)B * N * HW * C * es, n_new = (size_t)B * a * HW * C * es;
+  const void* ins[6] = {x0_prev, x0_anchor_new, x0_out, pos, cams, bbox};
+  const size_t lens[6] = {n_all, n_new, n_all, (size_t)B * N * HW * 12, (size_t)B * N * sizeof(gc_camera),
+                          (size_t)B * 32};
+  for (int i = 0; i < 6; ++i) {
+    if (overlaps(x_next, n_all, ins[i], lens[i]) || overlaps(model_out, n_all, ins[i], lens[i]))
+      return fail(GC_ERR_ALIAS, "gc_transport_reconstruct_geom: x_next/model_out overlap an input or x0_out");
+  }
+  if (overlaps(x_t, n_all, x0_out, n_all) || (x_next != x_t && overlaps(x_next, n_all, x_t, n_all)) ||
+      overlaps(model_out, n_all, x_t, n_all) || overlaps(model_out, n_all, x_next, n_all))
+    return fail(GC_ERR_ALIAS, "gc_transport_reconstruct_geom: outputs overlap x_t (only x_next == x_t is allowed)");
+  g.x_t = x_t;
+  g.x_next = x_next;
+  g.model_out = model_out;
+  launch_geom<kGeomReconstruct>(g, dtype, stream);
+  return after_launch(stream, "gc_transport_reconstruct_geom");
+}

@@ -17,69 +17,12 @@
 // (its own x0_prev and x_t, every output) is read and written with
 // nontemporal hints; only the gathered anchor tiles go through L2 normally.
 #include "gc_common.h"
+#include "gc_latent.h"
 
 namespace gc {
 namespace {
 
 constexpr int kBlock = 256;
-constexpr int kXcds = 8;
-
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
-template <int BYTES> struct RawT;
-template <> struct RawT<16> { using type = uint4; using nt = u32x4; };
-template <> struct RawT<8> { using type = uint2; using nt = u32x2; };
-
-// Storage codec for VEC elements of dtype DT packed in one raw vector.
-template <int DT, int VEC> struct Codec {
-  static constexpr int kBytes = VEC * (DT == GC_F32 ? 4 : 2);
-  using Raw = typename RawT<kBytes>::type;
-  using NT = typename RawT<kBytes>::nt;
-
-  // cached load: anchor tiles gathered by several target tokens
-  __device__ __forceinline__ static Raw load(const void* base, int64_t elem) {
-    return *reinterpret_cast<const Raw*>(static_cast<const char*>(base) + elem * (DT == GC_F32 ? 4 : 2));
-  }
-  // streamed load / store: data touched exactly once per step.  The
-  // nontemporal hint keeps it from displacing the gathered anchor tiles in L2.
-  __device__ __forceinline__ static Raw load_stream(const void* base, int64_t elem) {
-    const NT* p = reinterpret_cast<const NT*>(static_cast<const char*>(base) + elem * (DT == GC_F32 ? 4 : 2));
-    const NT v = __builtin_nontemporal_load(p);
-    Raw r;
-    __builtin_memcpy(&r, &v, sizeof(Raw));
-    return r;
-  }
-  __device__ __forceinline__ static void store_stream(void* base, int64_t elem, const Raw& r) {
-    NT v;
-    __builtin_memcpy(&v, &r, sizeof(Raw));
-    __builtin_nontemporal_store(v, reinterpret_cast<NT*>(static_cast<char*>(base) + elem * (DT == GC_F32 ? 4 : 2)));
-  }
-  __device__ __forceinline__ static void unpack(const Raw& r, float (&f)[VEC]) {
-    const uint32_t* w = reinterpret_cast<const uint32_t*>(&r);
-    if constexpr (DT == GC_F32) {
-#pragma unroll
-      for (int e = 0; e < VEC; ++e) f[e] = __uint_as_float(w[e]);
-    } else {
-#pragma unroll
-      for (int e = 0; e < VEC / 2; ++e) {
-        f[2 * e] = bf16_bits_to_f(w[e] & 0xffffu);
-        f[2 * e + 1] = bf16_bits_to_f(w[e] >> 16);
-      }
-    }
-  }
-  __device__ __forceinline__ static Raw pack(const float (&f)[VEC]) {
-    Raw r;
-    uint32_t* w = reinterpret_cast<uint32_t*>(&r);
-    if constexpr (DT == GC_F32) {
-#pragma unroll
-      for (int e = 0; e < VEC; ++e) w[e] = __float_as_uint(f[e]);
-    } else {
-#pragma unroll
-      for (int e = 0; e < VEC / 2; ++e) w[e] = f_to_bf16_bits(f[2 * e]) | (f_to_bf16_bits(f[2 * e + 1]) << 16);
-    }
-    return r;
-  }
-};
 
 struct TArgs {
   const void* x0_prev;
@@ -116,32 +59,6 @@ struct TArgs {
 // What a step does after the transport: nothing, the sampler reconstruction
 // (DDIM / flow Euler), or the UniPC corrector + predictor.
 enum StepMode { kTransportOnly = 0, kReconstruct = 1, kUniPC = 2 };
-
-__device__ __forceinline__ int logical_block(int i, int n_blocks, int remap) {
-  if (!remap) return i;
-  const int per = (n_blocks + kXcds - 1) / kXcds;   // grid is padded to kXcds * per
-  return (i % kXcds) * per + i / kXcds;
-}
-
-template <int VEC>
-__device__ __forceinline__ void reconstruct_vec(const Recon& r, const float (&xt)[VEC], const float (&x0)[VEC],
-                                                float (&xn)[VEC], float (&mo)[VEC]) {
-  if (r.kind == GC_DDIM) {
-#pragma unroll
-    for (int e = 0; e < VEC; ++e) {
-      const float eps = (xt[e] - r.a_t * x0[e]) * r.inv_s_t;
-      xn[e] = r.a_n * x0[e] + r.s_n * eps;
-      mo[e] = r.pred == GC_PRED_V ? r.a_t * eps - r.s_t * x0[e] : eps;
-    }
-  } else {
-#pragma unroll
-    for (int e = 0; e < VEC; ++e) {
-      const float vel = (xt[e] - x0[e]) * r.inv_sigma;
-      xn[e] = xt[e] + r.dsigma * vel;
-      mo[e] = vel;
-    }
-  }
-}
 
 // UniPC corrector (or the start sample) and predictor, fixed float order:
 //   x_c = ((c_xprev x_prev + c_mk2 m_{k-2}) + c_mk1 m_{k-1}) + c_mk m_k   (corrector)
@@ -377,7 +294,6 @@ __global__ __launch_bounds__(kBlock) void k_unipc(TArgs g, const void* __restric
   CD::store_stream(g.x_next, i * VEC, CD::pack(xn));
 }
 
-int pick_vec(int dtype, int64_t c) { return dtype == GC_F32 ? 4 : (c % 8 == 0 ? 8 : 4); }
 
 // Validation shared by the transport entry points; fills g (except the
 // reconstruction coefficients and the fused-only pointers).

@@ -223,3 +223,34 @@ def test_unipc_validation(gc, L):
     assert fused(x_cur=None) == -1
     assert fused(xn=A5 + 64) == -5              # x_next overlaps x_c
     assert fused(out=A0 + 64) == -5             # x0_out overlaps x0_prev
+
+
+def test_geom_validation(gc, L):
+    anchors = (ctypes.c_int32 * 2)(0, 3)
+    n = 1 * 6 * 8 * 8 * 16 * 2
+
+    def step(prev=A0, new=A1, pos=A2, cams=A3, bbox=A4, C=16, a=2, K=4, dt=1, out=A5, anc=anchors):
+        return L.gc_transport_step_geom(prev, new, pos, cams, bbox, 1, 6, 8, 8, C, anc, a, K, dt, out, None)
+
+    assert step(pos=None) == -1 and "null" in _err(L)
+    assert step(cams=None) == -1
+    assert step(K=0) == -1
+    assert step(a=9) == -1
+    assert step(C=6) == -2
+    assert step(dt=5) == -3
+    assert step(pos=A2 + 4) == -4
+    assert step(out=A0 + 32) == -5                # x0_out overlaps x0_prev
+    assert step(out=A2 + 64) == -5                # x0_out overlaps the position maps
+    dup = (ctypes.c_int32 * 2)(1, 1)
+    assert step(anc=dup) == -1 and "twice" in _err(L)
+    smp = gc.Sampler(kind=gc.GC_FLOW_EULER).c()
+
+    def fused(xt=A5 + 4 * n, xn=A5 + 8 * n, mo=None, t=0.5, tn=0.4):
+        return L.gc_transport_reconstruct_geom(A0, A1, A2, A3, A4, xt, 1, 6, 8, 8, 16, anchors, 2, 4, 1,
+                                               ctypes.byref(smp), t, tn, A5, xn, mo, None)
+
+    assert fused(xt=None) == -1
+    assert fused(t=0.0) == -1
+    assert fused(mo=A5 + 12 * n) == -1            # model_out without a prediction output
+    assert fused(xn=A5 + 64) == -5                # x_next overlaps x0_out
+    assert fused(xt=A5 + 64) == -5                # x_t overlaps x0_out
