@@ -66,6 +66,17 @@ def lib():
         L.orc_unipc_coeffs.restype = ctypes.c_int
         L.orc_unipc_apply.argtypes = [_vp, _vp, _vp, _vp, _vp, ctypes.c_int64, ctypes.c_int, _f64p, _f64p, _f64p]
         L.orc_unipc_apply.restype = ctypes.c_int
+        _u32p = ctypes.POINTER(ctypes.c_uint32)
+        _u64p = ctypes.POINTER(ctypes.c_uint64)
+        L.orc_cov_init.argtypes = [_f32p, ctypes.c_int64, _u8p]
+        L.orc_cov_update.argtypes = [_u8p, ctypes.c_int, ctypes.c_int, ctypes.c_int64, _i32p, ctypes.c_int,
+                                     ctypes.c_int, _u8p, _u32p]
+        L.orc_cov_gains.argtypes = [_u8p, _u8p, ctypes.c_int, ctypes.c_int, ctypes.c_int64, _u8p, _u64p]
+        L.orc_cov_select.argtypes = [_u8p, _u8p, ctypes.c_int, ctypes.c_int, ctypes.c_int64, ctypes.c_int, _i32p,
+                                     ctypes.c_int, _i32p]
+        L.orc_refresh_due.argtypes = [_u32p, ctypes.c_int, ctypes.c_int, ctypes.c_double]
+        for f in ("orc_cov_init", "orc_cov_update", "orc_cov_gains", "orc_cov_select", "orc_refresh_due"):
+            getattr(L, f).restype = ctypes.c_int
         for f in ("orc_downsample", "orc_bbox", "orc_build", "orc_transport", "orc_reconstruct",
                   "orc_anchors", "orc_full_steps", "orc_ddim_timesteps", "orc_store"):
             getattr(L, f).restype = ctypes.c_int
@@ -338,6 +349,80 @@ def trajectory_unipc(x_t0: np.ndarray, stub, pos: np.ndarray, cams, K: int, tol_
         out.append({"k": k, "anchors": A, "c": c, "x_t": x_t, "x0": mk, "x_c": xc_s, "x_t_exact": xn,
                     "x0_exact": mk_exact, "x_c_exact": xc})
     return out
+
+
+# --------------------------------------------------------------------------
+# token staleness and the coverage-driven schedule (see oracle.c O9)
+# --------------------------------------------------------------------------
+
+def coverage_pairs(pos: np.ndarray, cams, K: int, bbox_arr: np.ndarray) -> np.ndarray:
+    """seen[u][b][v][h][w] (uint8 0/1): anchor u alone sees token (v, h, w)
+    -- a non-zero O3 word of the build for the anchor set {u}."""
+    B, N, H, W, _ = pos.shape
+    seen = np.zeros((N, B, N, H, W), np.uint8)
+    for u in range(N):
+        corr, _, _ = build(pos, cams, [u], K, bbox_arr)
+        targets = [v for v in range(N) if v != u]
+        for ti, v in enumerate(targets):
+            seen[u, :, v] = corr[:, ti, :, :, 0] != 0
+    return seen
+
+
+def coverage_init(pos: np.ndarray) -> np.ndarray:
+    """Staleness state [B][N][H][W] uint8: 0 for foreground, 255 for background."""
+    pos = np.ascontiguousarray(pos, np.float32)
+    out = np.empty(pos.shape[:-1], np.uint8)
+    _check(lib().orc_cov_init(_p(pos, _f32p), out.size, _p(out, _u8p)), "cov_init")
+    return out
+
+
+def coverage_update(stale: np.ndarray, seen: np.ndarray, anchors: Sequence[int], R: int):
+    """One step with anchor set `anchors` (all views for a full step):
+    returns (new staleness, stats uint32 [B][N][4] = foreground tokens,
+    tokens with staleness >= R, sum, max)."""
+    B, N = stale.shape[:2]
+    HW = int(np.prod(stale.shape[2:]))
+    st = np.ascontiguousarray(stale, np.uint8).copy()
+    sn = np.ascontiguousarray(seen, np.uint8)
+    A = np.ascontiguousarray(anchors, np.int32)
+    stats = np.zeros((B, N, 4), np.uint32)
+    _check(lib().orc_cov_update(_p(sn, _u8p), B, N, HW, _p(A, _i32p), A.size, R, _p(st, _u8p),
+                                stats.ctypes.data_as(ctypes.POINTER(ctypes.c_uint32))), "cov_update")
+    return st, stats
+
+
+def coverage_gains(stale: np.ndarray, seen: np.ndarray, chosen: Sequence[int]) -> np.ndarray:
+    """Weighted coverage gain of every view given the chosen views (uint64 [N])."""
+    B, N = stale.shape[:2]
+    HW = int(np.prod(stale.shape[2:]))
+    ch = np.zeros(N, np.uint8)
+    ch[list(chosen)] = 1
+    g = np.zeros(N, np.uint64)
+    _check(lib().orc_cov_gains(_p(np.ascontiguousarray(seen, np.uint8), _u8p),
+                               _p(np.ascontiguousarray(stale, np.uint8), _u8p), B, N, HW, _p(ch, _u8p),
+                               g.ctypes.data_as(ctypes.POINTER(ctypes.c_uint64))), "cov_gains")
+    return g
+
+
+def coverage_select(stale: np.ndarray, seen: np.ndarray, a: int, forced: Sequence[int] = ()) -> List[int]:
+    """Greedy weighted maximum coverage: forced views first, then a views in all; sorted."""
+    B, N = stale.shape[:2]
+    HW = int(np.prod(stale.shape[2:]))
+    f = np.ascontiguousarray(list(forced) or [0], np.int32)
+    out = np.empty(a, np.int32)
+    _check(lib().orc_cov_select(_p(np.ascontiguousarray(seen, np.uint8), _u8p),
+                                _p(np.ascontiguousarray(stale, np.uint8), _u8p), B, N, HW, a, _p(f, _i32p),
+                                len(forced), _p(out, _i32p)), "cov_select")
+    return out.tolist()
+
+
+def refresh_due(stats: np.ndarray, tau: float) -> bool:
+    st = np.ascontiguousarray(stats, np.uint32)
+    B, N = st.shape[:2]
+    rc = lib().orc_refresh_due(st.ctypes.data_as(ctypes.POINTER(ctypes.c_uint32)), B, N, tau)
+    if rc < 0:
+        raise ValueError("oracle refresh_due rejected its arguments")
+    return bool(rc)
 
 
 def _bf16_values(bits: np.ndarray) -> np.ndarray:

@@ -685,3 +685,128 @@ int orc_unipc_apply(const void* x_cur, const void* x_prev, const void* m_km2, co
   }
   return 0;
 }
+
+/* ===================================================================== */
+/* O9: token staleness and the coverage-driven schedule                   */
+/* ===================================================================== */
+/* Sec. 3.2 (invalid matches): a token no anchor sees keeps its state and
+ * misses that step's denoising until the next full step.  The limitations
+ * section names adaptive anchor selection and visibility-aware refresh as
+ * the remedy for regions few anchors observe; the paper defines neither, so
+ * the definitions below are this implementation's reading:
+ *   - staleness of token (b, v, p): the number of consecutive steps in which
+ *     it received neither a fresh prediction (v an anchor, or a full step)
+ *     nor a transported increment (some anchor of the step sees it),
+ *     saturating at 254; background tokens (non-finite position) hold 255
+ *     and are never counted;
+ *   - per-view statistics after an update: foreground tokens, tokens with
+ *     staleness >= R, the sum and the maximum of the staleness;
+ *   - anchor selection: greedy weighted maximum coverage.  A candidate view
+ *     u covers (b, v, p) when v = u or u sees it; a token counts with weight
+ *     1 + staleness while no chosen view covers it.  Forced views are
+ *     chosen first, then the candidate with the largest gain (ties: the
+ *     lower view) until a views are chosen; the result is sorted;
+ *   - refresh: due when (tokens with staleness >= R) / (foreground tokens)
+ *     over all assets and views exceeds tau.
+ * seen[u][b][v][p] (0/1) is whether anchor u alone sees token p of view v:
+ * a non-zero O3 word for the anchor set {u}; seen[u][b][u][.] = 0.  Whether
+ * a set A sees a token is the OR over u in A, since O3 tests each anchor on
+ * its own. */
+
+#define ORC_BG 255u
+#define ORC_STALE_MAX 254u
+
+int orc_cov_init(const float* pos, int64_t n_tok, uint8_t* stale) {
+  if (n_tok < 0) return -2;
+  for (int64_t i = 0; i < n_tok; ++i) {
+    const float* P = pos + i * 3;
+    stale[i] = (isfinite(P[0]) && isfinite(P[1]) && isfinite(P[2])) ? 0u : (uint8_t)ORC_BG;
+  }
+  return 0;
+}
+
+static int covers(const uint8_t* seen, int B, int N, int64_t HW, int u, int b, int v, int64_t p) {
+  if (u == v) return 1;
+  return seen[(((int64_t)u * B + b) * N + v) * HW + p] != 0;
+}
+
+int orc_cov_update(const uint8_t* seen, int B, int N, int64_t HW, const int32_t* anchors, int a, int R,
+                   uint8_t* stale, uint32_t* stats) {
+  if (B < 1 || N < 1 || HW < 0 || a < 1 || a > N || R < 1) return -2;
+  for (int b = 0; b < B; ++b) {
+    for (int v = 0; v < N; ++v) {
+      uint32_t n_fg = 0, n_ge = 0, sum = 0, mx = 0;
+      for (int64_t p = 0; p < HW; ++p) {
+        uint8_t* s = stale + ((int64_t)b * N + v) * HW + p;
+        if (*s == ORC_BG) continue;
+        int fresh = 0;
+        for (int j = 0; j < a; ++j) fresh |= covers(seen, B, N, HW, anchors[j], b, v, p);
+        if (fresh) *s = 0;
+        else if (*s < ORC_STALE_MAX) *s = (uint8_t)(*s + 1);
+        n_fg += 1;
+        n_ge += *s >= (uint32_t)R;
+        sum += *s;
+        if (*s > mx) mx = *s;
+      }
+      uint32_t* o = stats + ((int64_t)b * N + v) * 4;
+      o[0] = n_fg;
+      o[1] = n_ge;
+      o[2] = sum;
+      o[3] = mx;
+    }
+  }
+  return 0;
+}
+
+int orc_cov_gains(const uint8_t* seen, const uint8_t* stale, int B, int N, int64_t HW, const uint8_t* chosen,
+                  uint64_t* gains) {
+  if (B < 1 || N < 1 || HW < 0) return -2;
+  for (int u = 0; u < N; ++u) gains[u] = 0;
+  for (int b = 0; b < B; ++b)
+    for (int v = 0; v < N; ++v)
+      for (int64_t p = 0; p < HW; ++p) {
+        const uint8_t s = stale[((int64_t)b * N + v) * HW + p];
+        if (s == ORC_BG) continue;
+        int covered = 0;
+        for (int u = 0; u < N; ++u) covered |= chosen[u] && covers(seen, B, N, HW, u, b, v, p);
+        if (covered) continue;
+        for (int u = 0; u < N; ++u)
+          if (!chosen[u] && covers(seen, B, N, HW, u, b, v, p)) gains[u] += 1u + s;
+      }
+  return 0;
+}
+
+int orc_cov_select(const uint8_t* seen, const uint8_t* stale, int B, int N, int64_t HW, int a,
+                   const int32_t* forced, int n_forced, int32_t* out) {
+  if (B < 1 || N < 1 || N > 64 || a < 1 || a > N || n_forced < 0 || n_forced > a) return -2;
+  uint8_t chosen[64] = {0};
+  uint64_t gains[64];
+  int n = 0;
+  for (int j = 0; j < n_forced; ++j) {
+    if (forced[j] < 0 || forced[j] >= N || chosen[forced[j]]) return -1;
+    chosen[forced[j]] = 1;
+    ++n;
+  }
+  while (n < a) {
+    orc_cov_gains(seen, stale, B, N, HW, chosen, gains);
+    int best = -1;
+    for (int u = 0; u < N; ++u)
+      if (!chosen[u] && (best < 0 || gains[u] > gains[best])) best = u;
+    chosen[best] = 1;
+    ++n;
+  }
+  int j = 0;
+  for (int u = 0; u < N; ++u)
+    if (chosen[u]) out[j++] = u;
+  return 0;
+}
+
+int orc_refresh_due(const uint32_t* stats, int B, int N, double tau) {
+  if (B < 1 || N < 1) return -2;
+  uint64_t fg = 0, ge = 0;
+  for (int64_t i = 0; i < (int64_t)B * N; ++i) {
+    fg += stats[i * 4 + 0];
+    ge += stats[i * 4 + 1];
+  }
+  return fg > 0 && (double)ge > tau * (double)fg;
+}

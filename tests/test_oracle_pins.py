@@ -16,7 +16,7 @@ import oracle
 import synth
 from synth.configs import C1, C2, C3, C4, C5
 
-from conftest import ulp_diff
+from conftest import latent_maps, ulp_diff
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
 
@@ -755,3 +755,127 @@ def test_unipc_orders_warm_up_and_final_step():
     # the last step lands on sigma = 0: the prediction is the clean estimate
     co = oracle.unipc_coeffs(S, S - 1, order=2)
     assert co[7] == 0 and co[8] == 0 and co[9] == 1
+
+
+# ---------------------------------------------------------------------------
+# O9 token staleness and the coverage-driven schedule
+# ---------------------------------------------------------------------------
+
+def _toy_coverage():
+    """1 asset, 3 views of 1 x 4 tokens; token 2 of view 1 is background.
+    Anchor 0 sees tokens 0, 1 of view 1; anchor 1 sees tokens 2, 3 of view 2
+    and token 0 of view 0; anchor 2 sees nothing."""
+    pos = np.zeros((1, 3, 1, 4, 3), np.float32)
+    pos[0, 1, 0, 2] = np.nan
+    seen = np.zeros((3, 1, 3, 1, 4), np.uint8)
+    seen[0, 0, 1, 0, [0, 1]] = 1
+    seen[1, 0, 2, 0, [2, 3]] = 1
+    seen[1, 0, 0, 0, 0] = 1
+    return pos, seen
+
+
+def test_coverage_hand_sequence():
+    pos, seen = _toy_coverage()
+    st = oracle.coverage_init(pos)
+    assert st.reshape(3, 4).tolist() == [[0, 0, 0, 0], [0, 0, 255, 0], [0, 0, 0, 0]]
+    # step with A = {0}: view 0 fresh; view 1 tokens 0, 1 seen; the rest miss a step
+    st, stats = oracle.coverage_update(st, seen, [0], R=2)
+    assert st.reshape(3, 4).tolist() == [[0, 0, 0, 0], [0, 0, 255, 1], [1, 1, 1, 1]]
+    assert stats[0].tolist() == [[4, 0, 0, 0], [3, 0, 1, 1], [4, 0, 4, 1]]
+    # A = {1}: view 1 fresh, view 0 token 0 and view 2 tokens 2, 3 seen
+    st, stats = oracle.coverage_update(st, seen, [1], R=2)
+    assert st.reshape(3, 4).tolist() == [[0, 1, 1, 1], [0, 0, 255, 0], [2, 2, 0, 0]]
+    assert stats[0].tolist() == [[4, 0, 3, 1], [3, 0, 0, 0], [4, 2, 4, 2]]
+    # A = {2} twice: view 2 fresh; views 0 and 1 age
+    st, _ = oracle.coverage_update(st, seen, [2], R=2)
+    st, stats = oracle.coverage_update(st, seen, [2], R=2)
+    assert st.reshape(3, 4).tolist() == [[2, 3, 3, 3], [2, 2, 255, 2], [0, 0, 0, 0]]
+    assert stats[0].tolist() == [[4, 4, 11, 3], [3, 3, 6, 2], [4, 0, 0, 0]]
+    # a full step (every view an anchor) resets every foreground token
+    st, stats = oracle.coverage_update(st, seen, [0, 1, 2], R=1)
+    assert st.reshape(3, 4).tolist() == [[0, 0, 0, 0], [0, 0, 255, 0], [0, 0, 0, 0]]
+    assert stats[0, :, 1].tolist() == [0, 0, 0]
+
+
+def test_coverage_gains_and_greedy_by_hand():
+    pos, seen = _toy_coverage()
+    st = np.array([[2, 3, 3, 3], [2, 2, 255, 2], [0, 0, 0, 0]], np.uint8).reshape(1, 3, 1, 4)
+    # weights 1 + staleness: view 0: 3 4 4 4; view 1: 3 3 - 3; view 2: 1 1 1 1
+    # u = 0: own view (15) + view 1 tokens 0, 1 (6) = 21; u = 1: own (9) + view 0
+    # token 0 (3) + view 2 tokens 2, 3 (2) = 14; u = 2: own (4)
+    assert oracle.coverage_gains(st, seen, []).tolist() == [21, 14, 4]
+    # after choosing 0: u = 1 adds view 1 token 3 (3) and view 2 tokens 2, 3 (2)
+    assert oracle.coverage_gains(st, seen, [0]).tolist() == [0, 5, 4]
+    assert oracle.coverage_select(st, seen, 2) == [0, 1]
+    assert oracle.coverage_select(st, seen, 2, forced=[2]) == [0, 2]
+    assert oracle.coverage_select(st, seen, 3) == [0, 1, 2]
+    with pytest.raises(ValueError):
+        oracle.coverage_select(st, seen, 2, forced=[1, 1])
+
+
+def _weighted_coverage(st, seen, S):
+    B, N = st.shape[:2]
+    w = np.where(st == 255, 0, 1 + st.astype(np.int64))
+    cov = np.zeros(st.shape, bool)
+    for u in S:
+        cov[:, u] = True
+        cov |= seen[u].astype(bool)
+    return int((w * cov).sum())
+
+
+def test_coverage_greedy_against_brute_force():
+    """Greedy picks the best single view first, and its set reaches at least
+    (1 - 1/e) of the best weighted coverage over all a-subsets (the classical
+    bound for greedy maximum coverage) on random small instances."""
+    import itertools
+    rs = np.random.default_rng(4)
+    for trial in range(12):
+        N, a, H, W = 6, 2 + trial % 2, 5, 7
+        st = rs.integers(0, 6, (2, N, H, W)).astype(np.uint8)
+        st[rs.random(st.shape) < 0.1] = 255
+        seen = (rs.random((N, 2, N, H, W)) < 0.3).astype(np.uint8)
+        for u in range(N):
+            seen[u, :, u] = 0
+        g = oracle.coverage_gains(st, seen, [])
+        single = [_weighted_coverage(st, seen, [u]) for u in range(N)]
+        assert g.tolist() == single
+        S = oracle.coverage_select(st, seen, a)
+        assert int(np.argmax(single)) in S
+        best = max(_weighted_coverage(st, seen, c) for c in itertools.combinations(range(N), a))
+        assert _weighted_coverage(st, seen, S) >= (1 - 1 / np.e) * best
+
+
+def test_coverage_saturates_and_keeps_background():
+    pos, seen = _toy_coverage()
+    st = oracle.coverage_init(pos)
+    for _ in range(300):
+        st, stats = oracle.coverage_update(st, seen, [2], R=1)
+    assert st[0, 0].max() == 254 and st[0, 1, 0, 2] == 255
+    assert stats[0, 0].tolist() == [4, 4, 4 * 254, 254]
+
+
+def test_coverage_pairs_or_equals_set_visibility():
+    """A set sees a token iff one of its anchors does on its own: the OR of
+    the single-anchor pairs equals n_vis > 0 of the set's own build."""
+    P = latent_maps("hunyuan_torus_6v_64")
+    w = synth.CONFIGS["hunyuan_torus_6v_64"]
+    cams = synth.batch_cameras(w)
+    bb = oracle.bbox(P, w.tol_frac)
+    seen = oracle.coverage_pairs(P, cams, w.K, bb)
+    for u in range(w.N):
+        assert not seen[u, :, u].any()
+    for c in range(3):
+        A = oracle.anchors(w.N, w.a, c)
+        _, _, nvis = oracle.build(P, cams, A, w.K, bb)
+        targets = [v for v in range(w.N) if v not in A]
+        for ti, v in enumerate(targets):
+            np.testing.assert_array_equal(np.any(seen[A][:, :, v], axis=0), nvis[:, ti] > 0)
+
+
+def test_refresh_due():
+    stats = np.zeros((2, 3, 4), np.uint32)
+    stats[..., 0] = 100
+    stats[0, 1, 1] = 30                        # 30 of 600 foreground tokens stale >= R
+    assert oracle.refresh_due(stats, 0.04)
+    assert not oracle.refresh_due(stats, 0.05)
+    assert not oracle.refresh_due(np.zeros((1, 1, 4), np.uint32), 0.0)
