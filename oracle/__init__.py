@@ -75,7 +75,10 @@ def lib():
         L.orc_cov_select.argtypes = [_u8p, _u8p, ctypes.c_int, ctypes.c_int, ctypes.c_int64, ctypes.c_int, _i32p,
                                      ctypes.c_int, _i32p]
         L.orc_refresh_due.argtypes = [_u32p, ctypes.c_int, ctypes.c_int, ctypes.c_double]
-        for f in ("orc_cov_init", "orc_cov_update", "orc_cov_gains", "orc_cov_select", "orc_refresh_due"):
+        L.orc_cov_score.argtypes = [_u8p, _u8p, ctypes.c_int, ctypes.c_int, ctypes.c_int64, _i32p, ctypes.c_int,
+                                    ctypes.c_int, _u64p]
+        for f in ("orc_cov_init", "orc_cov_update", "orc_cov_gains", "orc_cov_select", "orc_refresh_due",
+                  "orc_cov_score"):
             getattr(L, f).restype = ctypes.c_int
         for f in ("orc_downsample", "orc_bbox", "orc_build", "orc_transport", "orc_reconstruct",
                   "orc_anchors", "orc_full_steps", "orc_ddim_timesteps", "orc_store"):
@@ -416,6 +419,29 @@ def coverage_select(stale: np.ndarray, seen: np.ndarray, a: int, forced: Sequenc
     return out.tolist()
 
 
+def coverage_score(stale: np.ndarray, seen: np.ndarray, sets: Sequence[Sequence[int]]) -> np.ndarray:
+    """Weighted coverage (1 + staleness over covered foreground tokens) of each candidate set (uint64 [M])."""
+    B, N = stale.shape[:2]
+    HW = int(np.prod(stale.shape[2:]))
+    S = np.ascontiguousarray(sets, np.int32)
+    M, a = S.shape
+    out = np.zeros(M, np.uint64)
+    _check(lib().orc_cov_score(_p(np.ascontiguousarray(seen, np.uint8), _u8p),
+                               _p(np.ascontiguousarray(stale, np.uint8), _u8p), B, N, HW, _p(S, _i32p), M, a,
+                               out.ctypes.data_as(ctypes.POINTER(ctypes.c_uint64))), "cov_score")
+    return out
+
+
+def rotation_sets(N: int, a: int) -> List[List[int]]:
+    """The rotation's distinct anchor sets, in order of first appearance."""
+    out = []
+    for c in range(N):
+        A = anchors(N, a, c)
+        if A not in out:
+            out.append(A)
+    return out
+
+
 def refresh_due(stats: np.ndarray, tau: float) -> bool:
     st = np.ascontiguousarray(stats, np.uint32)
     B, N = st.shape[:2]
@@ -423,6 +449,66 @@ def refresh_due(stats: np.ndarray, tau: float) -> bool:
     if rc < 0:
         raise ValueError("oracle refresh_due rejected its arguments")
     return bool(rc)
+
+
+def trajectory_adaptive(x_t0: np.ndarray, stub, pos: np.ndarray, cams, K: int, tol_frac: float, dtype: str,
+                        kind: str, S: int, full: Sequence[int], a: int, policy: str = "coverage", max_gap: int = 0,
+                        tau: float = None, R: int = 2, steps: int = None):
+    """The cached loop of trajectory() with the coverage-driven schedule
+    (see oracle.c O9): a step is full when the schedule says so, on the first
+    step, or when refresh_due(stats of the previous step, tau); a cached
+    step's anchors come from coverage_select (policy "coverage", views whose
+    anchor gap reached max_gap forced first, longest gap first, then lower
+    view), from the rotation (policy "rotate"), or from the rotation's
+    distinct sets, the one with the largest coverage_score (policy
+    "rotation_coverage", ties to the earlier set).  After every step the
+    staleness is updated with the step's views (all views when full) and
+    each view's gap (cached steps since it was last an anchor) advances.
+    Records as trajectory() plus full, stale, stats and gap after the step."""
+    steps = S if steps is None else steps
+    B, N = pos.shape[0], pos.shape[1]
+    bb = bbox(pos, tol_frac)
+    seen = coverage_pairs(pos, cams, K, bb)
+    stale = coverage_init(pos)
+    stats = None
+    gap = [0] * N
+    cache = {}
+    x_t, x0_store, c = x_t0, None, 0
+    out = []
+    for k in range(steps):
+        t, tn = step_times(kind, S, k)
+        is_full = bool(full[k]) or x0_store is None or (tau is not None and stats is not None
+                                                        and refresh_due(stats, tau))
+        if is_full:
+            A = list(range(N))
+            x0_state = stub(k, A)
+            x0_exact = (x0_state if dtype == "f32" else _bf16_values(x0_state)).astype(np.float64)
+        else:
+            if policy == "rotate":
+                A = anchors(N, a, c)
+            elif policy == "rotation_coverage":
+                cands = rotation_sets(N, a)
+                sc = coverage_score(stale, seen, cands)
+                A = cands[int(np.argmax(sc))]           # first maximum: ties go to the earlier set
+            else:
+                due = [v for v in range(N) if max_gap and gap[v] >= max_gap]
+                due = sorted(due, key=lambda v: (-gap[v], v))[:a]
+                A = coverage_select(stale, seen, a, forced=due)
+            c += 1
+            key = tuple(A)
+            if key not in cache:
+                corr, w, _ = build(pos, cams, A, K, bb)
+                cache[key] = (corr, w)
+            corr, w = cache[key]
+            x0_exact, x0_state = transport(x0_store, stub(k, A), corr, w, A, dtype)
+        xn, _ = reconstruct(x_t, x0_state, dtype, kind, t, tn)
+        x_t = store(xn, dtype)
+        x0_store = x0_state
+        stale, stats = coverage_update(stale, seen, A, R)
+        gap = [0 if (is_full or v in A) else g + 1 for v, g in enumerate(gap)]
+        out.append({"k": k, "anchors": A, "full": is_full, "c": c, "x_t": x_t, "x0": x0_state, "x_t_exact": xn,
+                    "x0_exact": x0_exact, "stale": stale.copy(), "stats": stats.copy(), "gap": list(gap)})
+    return out
 
 
 def _bf16_values(bits: np.ndarray) -> np.ndarray:

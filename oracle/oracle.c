@@ -801,6 +801,32 @@ int orc_cov_select(const uint8_t* seen, const uint8_t* stale, int B, int N, int6
   return 0;
 }
 
+/* Weighted coverage of candidate sets: score[m] = sum over foreground tokens
+ * covered by set m (sets[m][0..a-1]) of 1 + staleness.  Choosing, among the
+ * rotation's own sets, the one that covers the most keeps the rotation's
+ * evenly spread anchors while following where the stale tokens are. */
+int orc_cov_score(const uint8_t* seen, const uint8_t* stale, int B, int N, int64_t HW, const int32_t* sets, int M,
+                  int a, uint64_t* score) {
+  if (B < 1 || N < 1 || HW < 0 || M < 1 || a < 1 || a > N) return -2;
+  for (int m = 0; m < M; ++m) {
+    score[m] = 0;
+    for (int j = 0; j < a; ++j)
+      if (sets[m * a + j] < 0 || sets[m * a + j] >= N) return -1;
+  }
+  for (int b = 0; b < B; ++b)
+    for (int v = 0; v < N; ++v)
+      for (int64_t p = 0; p < HW; ++p) {
+        const uint8_t s = stale[((int64_t)b * N + v) * HW + p];
+        if (s == ORC_BG) continue;
+        for (int m = 0; m < M; ++m) {
+          int covered = 0;
+          for (int j = 0; j < a; ++j) covered |= covers(seen, B, N, HW, sets[m * a + j], b, v, p);
+          if (covered) score[m] += 1u + s;
+        }
+      }
+  return 0;
+}
+
 int orc_refresh_due(const uint32_t* stats, int B, int N, double tau) {
   if (B < 1 || N < 1) return -2;
   uint64_t fg = 0, ge = 0;

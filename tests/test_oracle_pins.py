@@ -879,3 +879,26 @@ def test_refresh_due():
     assert oracle.refresh_due(stats, 0.04)
     assert not oracle.refresh_due(stats, 0.05)
     assert not oracle.refresh_due(np.zeros((1, 1, 4), np.uint32), 0.0)
+
+
+def test_coverage_score_hand_and_brute_force():
+    pos, seen = _toy_coverage()
+    st = np.array([[2, 3, 3, 3], [2, 2, 255, 2], [0, 0, 0, 0]], np.uint8).reshape(1, 3, 1, 4)
+    # {0}: 21 (as the gain above); {1, 2}: own views 9 + 4, view 0 token 0 (3) = 16
+    assert oracle.coverage_score(st, seen, [[0, 0], [1, 2]]).tolist() == [21, 16]
+    rs = np.random.default_rng(8)
+    for trial in range(6):
+        N, a = 7, 3
+        st = rs.integers(0, 9, (2, N, 4, 6)).astype(np.uint8)
+        st[rs.random(st.shape) < 0.1] = 255
+        seen = (rs.random((N, 2, N, 4, 6)) < 0.25).astype(np.uint8)
+        for u in range(N):
+            seen[u, :, u] = 0
+        sets = [list(rs.choice(N, a, replace=False)) for _ in range(5)]
+        assert oracle.coverage_score(st, seen, sets).tolist() == [_weighted_coverage(st, seen, S) for S in sets]
+
+
+def test_rotation_sets():
+    assert oracle.rotation_sets(12, 4) == [[0, 3, 6, 9], [1, 4, 7, 10], [2, 5, 8, 11]]
+    assert oracle.rotation_sets(6, 2) == [[0, 3], [1, 4], [2, 5]]
+    assert len(oracle.rotation_sets(10, 3)) == 10
