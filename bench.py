@@ -41,6 +41,7 @@ def parse():
     ap.add_argument("--config", default="stress_torusknot_12v_128x16_b8")
     ap.add_argument("--ring", type=int, default=3, help="buffer sets cycled through (defeats the LLC)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-coverage", action="store_true", help="skip the coverage-schedule rows")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--copy-probe", action="store_true",
                     help="also run a plain 1 GiB device copy (reference kernel for counter scaling)")
@@ -309,6 +310,10 @@ def main():
         for name in ("tiny_sphere_4v_32", "hunyuan_torus_6v_64"):
             rows[f"small_{name}"] = small_workload(gc, synth, name)
 
+    # ---- coverage-driven schedule: staleness under each anchor policy --------
+    if not args.no_coverage:
+        rows["coverage"] = coverage_rows(gc, w, pos, cams, bbox, full)
+
     # ---- CPU baseline: the oracle on one asset ------------------------------
     cpu = None
     if not args.no_cpu_baseline:
@@ -339,6 +344,57 @@ def main():
         "rows": rows,
     }
     print(json.dumps(out), flush=True)
+
+
+def coverage_rows(gc, w, pos, cams, bbox, full, R=2):
+    """One whole trajectory of the schedule alone (no latents) per anchor
+    policy: per-step staleness of the foreground tokens after the step
+    (mean, fraction stale for >= R steps, max) and the policy's cost per
+    cached step (selection or scoring + the staleness update + the host
+    read-backs it needs)."""
+    import numpy as np
+    import torch
+    N, a = w.N, w.a
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    pairs = gc.gc_coverage_pairs(pos, cams, bbox)
+    torch.cuda.synchronize()
+    out = {"pairs_ms": (time.perf_counter() - t0) * 1e3, "R": R}
+    rot_sets = []
+    for c in range(N):
+        A = gc.gc_schedule_anchors(N, a, c)
+        if A not in rot_sets:
+            rot_sets.append(A)
+    ws = torch.empty(gc.gc_coverage_workspace_bytes(), dtype=torch.uint8, device=pos.device)
+    max_gap = -(-N // a)
+    for policy in ("rotate", "rotation_coverage", "coverage"):
+        stale = gc.gc_coverage_init(pos)
+        gap, c, rec, cost = [0] * N, 0, [], []
+        for k in range(w.S):
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            if full[k] or k == 0:
+                A = list(range(N))
+            elif policy == "rotate":
+                A = gc.gc_schedule_anchors(N, a, c)
+            elif policy == "rotation_coverage":
+                sc = gc.gc_coverage_score(pairs, stale, rot_sets).cpu().tolist()
+                A = rot_sets[sc.index(max(sc))]
+            else:
+                due = sorted([v for v in range(N) if gap[v] >= max_gap], key=lambda v: (-gap[v], v))[:a]
+                A = gc.gc_coverage_select(pairs, stale, a, forced=due, workspace=ws).cpu().tolist()
+            st = gc.gc_coverage_update(pairs, stale, A, R).cpu().numpy().astype(np.int64)
+            if not (full[k] or k == 0):
+                cost.append(time.perf_counter() - t0)
+                c += 1
+            gap = [0 if (full[k] or v in A) else g + 1 for v, g in enumerate(gap)]
+            fg = st[..., 0].sum()
+            rec.append((st[..., 2].sum() / fg, st[..., 1].sum() / fg, st[..., 3].max()))
+        r = np.array(rec, np.float64)
+        out[policy] = {"mean_staleness": round(float(r[:, 0].mean()), 5),
+                       "frac_stale_ge_R": round(float(r[:, 1].mean()), 5), "max_staleness": int(r[:, 2].max()),
+                       "ms_per_cached_step": round(float(np.median(cost)) * 1e3, 4)}
+    return out
 
 
 def small_workload(gc, synth, name, steps=300):

@@ -18,6 +18,9 @@
  *                        gc_unipc_update, gc_transport_unipc  multistep (UniPC) variant
  *                        gc_transport_step_geom, gc_transport_reconstruct_geom
  *                                               the same with G_{A->v} computed on the fly
+ *   coverage schedule    gc_coverage_pairs, gc_coverage_init, gc_coverage_update, gc_coverage_select,
+ *                        gc_coverage_score, gc_schedule_refresh_due
+ *                                               token staleness, adaptive anchors and refresh
  *   host schedule        gc_schedule_anchors, gc_schedule_full_steps, gc_sampler_step_times
  *
  * Conventions shared by every call
@@ -369,6 +372,68 @@ int gc_transport_reconstruct_geom(const void* x0_prev, const void* x0_anchor_new
                                   int W, int C, const int32_t* anchors, int a, int K, int dtype,
                                   const gc_sampler* smp, double t, double t_next, void* x0_out, void* x_next,
                                   void* model_out, hipStream_t stream);
+
+/*
+ * Token staleness and the coverage-driven schedule.
+ * A token no anchor sees keeps its state and misses that step's denoising
+ * until the next full step (Sec. 3.2, invalid matches); the paper's
+ * limitations section names adaptive anchor selection and visibility-aware
+ * refresh as the remedy for regions few anchors observe but defines neither.
+ * This library's reading:
+ *   staleness  uint8 per token [B][N][H][W]: consecutive steps without a fresh
+ *              prediction (its view an anchor, or a full step) or a
+ *              transported increment (some anchor of the step sees it),
+ *              saturating at 254; 255 marks background (non-finite position)
+ *              and is never counted;
+ *   selection  greedy weighted maximum coverage: view u covers token (b, v, p)
+ *              when v = u or anchor u sees it; an uncovered foreground token
+ *              weighs 1 + its staleness.  Forced views are taken first, then
+ *              the view with the largest gain (ties: the lower view) until a
+ *              views are chosen; the set is written in ascending order;
+ *   refresh    a full step is due when, over all assets and views, the tokens
+ *              with staleness >= R exceed the fraction tau of the foreground.
+ * Visibility comes from single-anchor pairs: bit (u, b, v, p) is set when
+ * anchor u alone has an in-tolerance tap for token p of view v -- the tap
+ * test of gc_build_correspondence, which examines each anchor on its own, so
+ * a set sees a token iff one of its anchors does.
+ *
+ * gc_coverage_pair_words: uint32 words of the pair bits, N * B * N * ceil(H*W/32);
+ *   layout [u][b][v][ceil(H*W/32)], token p at bit p % 32 of word p / 32, the
+ *   bits of view u in row (u, b, u) zero.
+ * gc_coverage_pairs: pos [B][N][H][W][3], cams device gc_camera [B][N], bbox
+ *   device [B][8] (gc_posmap_bbox) -> pair_bits (once per asset batch).
+ * gc_coverage_init: staleness 0 for foreground tokens, 255 for background.
+ * gc_coverage_update: one step with the anchor set anchors (host [a]; all N
+ *   views for a full step) -> staleness updated in place and stats
+ *   (device uint32 [B][N][4]: foreground tokens, tokens with staleness >= R,
+ *   sum and maximum of the staleness), recomputed by the call.
+ * gc_coverage_select: the anchor set of the next cached step, written to
+ *   anchors_out (device int32 [a], ascending); forced: host [n_forced] views
+ *   that must be in it.  a <= GC_MAX_ANCHORS.  workspace: caller-owned device
+ *   memory of gc_coverage_workspace_bytes(), 16-byte aligned; it holds the
+ *   running gains, so concurrent calls need separate workspaces.  Enqueues
+ *   2 (a - n_forced) + 2 small launches and never synchronises.
+ * gc_coverage_score: scores (device uint64 [M], overwritten) = the weighted
+ *   coverage, sum of 1 + staleness over the foreground tokens it covers, of
+ *   each candidate set sets (host int32 [M][a]); M <= 64.  Choosing the
+ *   rotation's set with the largest score keeps the rotation's evenly spread
+ *   anchors while following where the stale tokens are.
+ * gc_schedule_refresh_due: host; stats as written by gc_coverage_update and
+ *   copied to the host; *due = 1 when a full step is due.
+ */
+int64_t gc_coverage_pair_words(int B, int N, int H, int W);
+int gc_coverage_pairs(const float* pos, const gc_camera* cams, const float* bbox, int B, int N, int H, int W,
+                      uint32_t* pair_bits, hipStream_t stream);
+int gc_coverage_init(const float* pos, int B, int N, int H, int W, uint8_t* stale, hipStream_t stream);
+int gc_coverage_update(const uint32_t* pair_bits, int B, int N, int H, int W, const int32_t* anchors, int a, int R,
+                       uint8_t* stale, uint32_t* stats, hipStream_t stream);
+size_t gc_coverage_workspace_bytes(void);
+int gc_coverage_select(const uint32_t* pair_bits, const uint8_t* stale, int B, int N, int H, int W, int a,
+                       const int32_t* forced, int n_forced, int32_t* anchors_out, void* workspace, size_t ws_bytes,
+                       hipStream_t stream);
+int gc_coverage_score(const uint32_t* pair_bits, const uint8_t* stale, int B, int N, int H, int W, const int32_t* sets,
+                      int M, int a, uint64_t* scores, hipStream_t stream);
+int gc_schedule_refresh_due(const uint32_t* stats, int B, int N, double tau, int* due);
 
 /*
  * Host schedule (no device work).

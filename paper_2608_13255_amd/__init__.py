@@ -110,6 +110,14 @@ def lib() -> ctypes.CDLL:
             "gc_transport_reconstruct_geom": ([_vp, _vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i32p, _i, _i, _i,
                                                ctypes.POINTER(_Sampler), ctypes.c_double, ctypes.c_double, _vp, _vp,
                                                _vp, _vp], _i),
+            "gc_coverage_pair_words": ([_i, _i, _i, _i], _i64),
+            "gc_coverage_pairs": ([_vp, _vp, _vp, _i, _i, _i, _i, _vp, _vp], _i),
+            "gc_coverage_init": ([_vp, _i, _i, _i, _i, _vp, _vp], _i),
+            "gc_coverage_update": ([_vp, _i, _i, _i, _i, _i32p, _i, _i, _vp, _vp, _vp], _i),
+            "gc_coverage_workspace_bytes": ([], ctypes.c_size_t),
+            "gc_coverage_select": ([_vp, _vp, _i, _i, _i, _i, _i, _i32p, _i, _vp, _vp, ctypes.c_size_t, _vp], _i),
+            "gc_schedule_refresh_due": ([_vp, _i, _i, ctypes.c_double, ctypes.POINTER(ctypes.c_int)], _i),
+            "gc_coverage_score": ([_vp, _vp, _i, _i, _i, _i, _i32p, _i, _i, _vp, _vp], _i),
             "gc_schedule_anchors": ([_i, _i, _i64, _i32p], _i),
             "gc_schedule_full_steps": ([_i, _i, _i, ctypes.POINTER(ctypes.c_uint8)], _i),
             "gc_sampler_step_times": ([ctypes.POINTER(_Sampler), _i, _i, ctypes.POINTER(ctypes.c_double),
@@ -539,6 +547,107 @@ def bind_transport_unipc(x0_prev: torch.Tensor, x0_anchor_new: torch.Tensor, cor
     post = (_dev(x0_out, "x0_out"), _dev(x_c, "x_c"), _dev(x_next, "x_next"), _stream(stream))
     return BoundUniPC(lib().gc_transport_unipc, pre, post,
                       (x0_prev, x0_anchor_new, corr, weights, x_cur, x_prev, m_km2, x0_out, x_c, x_next, arr, index))
+
+
+# --------------------------------------------------------------------------
+# token staleness and the coverage-driven schedule
+# --------------------------------------------------------------------------
+
+def gc_coverage_pairs(pos: torch.Tensor, cams: torch.Tensor, bbox: torch.Tensor, out: torch.Tensor = None,
+                      stream=None) -> torch.Tensor:
+    """Single-anchor visibility bits: int32 [N, B, N, ceil(H*W/32)] (uint32
+    words; bit p % 32 of word p / 32 of row (u, b, v): anchor u sees token p
+    of view v)."""
+    if pos.dtype != torch.float32 or pos.dim() != 5 or pos.shape[-1] != 3:
+        raise ValueError("pos must be float32 [B, N, H, W, 3]")
+    B, N, H, W, _ = pos.shape
+    if cams.dtype != torch.uint8 or tuple(cams.shape) != (B, N, 68):
+        raise ValueError(f"cams must be uint8 [B={B}, N={N}, 68]")
+    wpr = (H * W + 31) // 32
+    if out is None:
+        out = torch.empty((N, B, N, wpr), dtype=torch.int32, device=pos.device)
+    if tuple(out.shape) != (N, B, N, wpr) or out.element_size() != 4:
+        raise ValueError(f"out must be a 32-bit [{N}, {B}, {N}, {wpr}] tensor")
+    _check(lib().gc_coverage_pairs(_dev(pos, "pos"), _dev(cams, "cams"), _dev(bbox, "bbox"), B, N, H, W,
+                                   _dev(out, "pair_bits"), _stream(stream)), "gc_coverage_pairs")
+    return out
+
+
+def gc_coverage_init(pos: torch.Tensor, out: torch.Tensor = None, stream=None) -> torch.Tensor:
+    """Staleness uint8 [B, N, H, W]: 0 for foreground tokens, 255 for background."""
+    B, N, H, W, _ = pos.shape
+    if out is None:
+        out = torch.empty((B, N, H, W), dtype=torch.uint8, device=pos.device)
+    _check(lib().gc_coverage_init(_dev(pos, "pos"), B, N, H, W, _dev(out, "stale"), _stream(stream)),
+           "gc_coverage_init")
+    return out
+
+
+def gc_coverage_update(pair_bits: torch.Tensor, stale: torch.Tensor, anchors: Sequence[int], R: int,
+                       stats: torch.Tensor = None, stream=None) -> torch.Tensor:
+    """One step with anchor set `anchors` (every view for a full step):
+    staleness updated in place; returns stats int32 [B, N, 4] (foreground,
+    staleness >= R, sum, max)."""
+    if stale.dtype != torch.uint8 or stale.dim() != 4:
+        raise ValueError("stale must be uint8 [B, N, H, W]")
+    B, N, H, W = stale.shape
+    arr = (ctypes.c_int32 * len(anchors))(*anchors)
+    if stats is None:
+        stats = torch.empty((B, N, 4), dtype=torch.int32, device=stale.device)
+    if tuple(stats.shape) != (B, N, 4) or stats.element_size() != 4:
+        raise ValueError(f"stats must be a 32-bit [{B}, {N}, 4] tensor")
+    _check(lib().gc_coverage_update(_dev(pair_bits, "pair_bits"), B, N, H, W, arr, len(anchors), R,
+                                    _dev(stale, "stale"), _dev(stats, "stats"), _stream(stream)),
+           "gc_coverage_update")
+    return stats
+
+
+def gc_coverage_workspace_bytes() -> int:
+    return int(lib().gc_coverage_workspace_bytes())
+
+
+def gc_coverage_select(pair_bits: torch.Tensor, stale: torch.Tensor, a: int, forced: Sequence[int] = (),
+                       out: torch.Tensor = None, workspace: torch.Tensor = None, stream=None) -> torch.Tensor:
+    """Anchor set of the next cached step (greedy weighted maximum coverage):
+    device int32 [a], ascending.  Enqueued only: read it after a sync."""
+    B, N, H, W = stale.shape
+    if out is None:
+        out = torch.empty(a, dtype=torch.int32, device=stale.device)
+    if workspace is None:
+        workspace = torch.empty(gc_coverage_workspace_bytes(), dtype=torch.uint8, device=stale.device)
+    farr = (ctypes.c_int32 * max(len(forced), 1))(*forced)
+    _check(lib().gc_coverage_select(_dev(pair_bits, "pair_bits"), _dev(stale, "stale"), B, N, H, W, a, farr,
+                                    len(forced), _dev(out, "anchors_out"), _dev(workspace, "workspace"),
+                                    workspace.numel() * workspace.element_size(), _stream(stream)),
+           "gc_coverage_select")
+    return out
+
+
+def gc_coverage_score(pair_bits: torch.Tensor, stale: torch.Tensor, sets: Sequence[Sequence[int]],
+                      out: torch.Tensor = None, stream=None) -> torch.Tensor:
+    """Weighted coverage of each candidate set: device int64 [M] (uint64 values)."""
+    B, N, H, W = stale.shape
+    M, a = len(sets), len(sets[0])
+    if any(len(S) != a for S in sets):
+        raise ValueError("candidate sets must have the same size")
+    flat = (ctypes.c_int32 * (M * a))(*[int(u) for S in sets for u in S])
+    if out is None:
+        out = torch.empty(M, dtype=torch.int64, device=stale.device)
+    _check(lib().gc_coverage_score(_dev(pair_bits, "pair_bits"), _dev(stale, "stale"), B, N, H, W, flat, M, a,
+                                   _dev(out, "scores"), _stream(stream)), "gc_coverage_score")
+    return out
+
+
+def gc_schedule_refresh_due(stats_host, tau: float) -> bool:
+    """stats as returned by gc_coverage_update, on the host (numpy or CPU tensor)."""
+    import numpy as np
+    st = np.ascontiguousarray(stats_host.numpy() if isinstance(stats_host, torch.Tensor) else stats_host)
+    if st.dtype.itemsize != 4 or st.ndim != 3 or st.shape[2] != 4:
+        raise ValueError("stats must be 32-bit [B, N, 4]")
+    due = ctypes.c_int()
+    _check(lib().gc_schedule_refresh_due(st.ctypes.data, st.shape[0], st.shape[1], float(tau), ctypes.byref(due)),
+           "gc_schedule_refresh_due")
+    return bool(due.value)
 
 
 def gc_schedule_anchors(N: int, a: int, c: int) -> List[int]:

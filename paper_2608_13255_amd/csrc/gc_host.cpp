@@ -161,6 +161,20 @@ int gc_sampler_step_times(const gc_sampler* smp, int S, int k, double* t, double
   return GC_OK;
 }
 
+int gc_schedule_refresh_due(const uint32_t* stats, int B, int N, double tau, int* due) {
+  clear_error();
+  if (!stats || !due) return fail(GC_ERR_ARG, "refresh: null pointer");
+  if (B < 1 || N < 1) return fail(GC_ERR_SHAPE, "refresh: bad shape B=%d N=%d", B, N);
+  if (!(tau >= 0.0 && tau <= 1.0)) return fail(GC_ERR_ARG, "refresh: tau outside [0, 1]");
+  uint64_t fg = 0, stale = 0;
+  for (int64_t i = 0; i < (int64_t)B * N; ++i) {
+    fg += stats[i * 4 + 0];
+    stale += stats[i * 4 + 1];
+  }
+  *due = fg > 0 && (double)stale > tau * (double)fg;
+  return GC_OK;
+}
+
 int gc_sampler_alpha_bar(const gc_sampler* smp, int t, double* abar) {
   clear_error();
   if (!smp || !abar) return fail(GC_ERR_ARG, "null argument");

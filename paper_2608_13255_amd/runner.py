@@ -18,9 +18,10 @@ from typing import Callable, Dict, List, Optional, Sequence, Tuple
 import torch
 
 from . import (GC_FULL_HEAD_MID_TAIL, GC_FULL_PERIODIC, Sampler, VisibleIndex, gc_build_correspondence,
+               gc_coverage_init, gc_coverage_pairs, gc_coverage_score, gc_coverage_select, gc_coverage_update,
                gc_index_correspondence, gc_posmap_bbox, gc_sampler_reconstruct, gc_sampler_step_times,
-               gc_schedule_anchors, gc_schedule_full_steps, gc_transport_reconstruct, gc_transport_unipc,
-               gc_unipc_coeffs, gc_unipc_update)
+               gc_schedule_anchors, gc_schedule_full_steps, gc_schedule_refresh_due, gc_transport_reconstruct,
+               gc_transport_reconstruct_geom, gc_transport_unipc, gc_unipc_coeffs, gc_unipc_update)
 
 Predict = Callable[[int, List[int]], torch.Tensor]
 
@@ -28,11 +29,26 @@ Predict = Callable[[int, List[int]], torch.Tensor]
 class GeoCacheRunner:
     def __init__(self, pos: torch.Tensor, cams: torch.Tensor, a: int, K: int, sampler: Sampler, S: int,
                  full: Sequence[int], tol_frac: float = 0.01, use_index: bool = True, unipc_order: int = 0,
-                 unipc_corrector: bool = True, stream=None):
+                 unipc_corrector: bool = True, anchor_policy: str = "rotate", max_gap: int = 0,
+                 refresh_tau: Optional[float] = None, refresh_R: int = 2, geom: bool = False, stream=None):
         """pos: device float32 [B, N, H, W, 3] latent-grid position maps;
         cams: device gc_camera tensor [B, N, 68]; full[k] = 1 for full-view steps.
         unipc_order 1 or 2 runs the UniPC multistep solver on the sampler's
-        DDIM noise schedule instead of the sampler's own step."""
+        DDIM noise schedule instead of the sampler's own step.
+
+        anchor_policy "coverage" picks each cached step's anchors by greedy
+        weighted maximum coverage of the stale tokens (gc_coverage_select);
+        views that have not been anchors for max_gap cached steps (0: off)
+        are forced into the set, longest gap first.  "rotation_coverage"
+        takes, among the rotation's distinct sets, the one with the largest
+        weighted coverage (gc_coverage_score; ties to the earlier set).  refresh_tau makes a
+        step full when the fraction of foreground tokens stale for refresh_R
+        or more steps exceeds it.  geom computes the correspondence inside
+        each step instead of building and caching one per anchor set."""
+        if anchor_policy not in ("rotate", "coverage", "rotation_coverage"):
+            raise ValueError("anchor_policy must be 'rotate', 'coverage' or 'rotation_coverage'")
+        if unipc_order and geom:
+            raise ValueError("the on-the-fly transport has no UniPC variant")
         self.pos, self.cams, self.a, self.K = pos, cams, a, K
         self.sampler, self.S = sampler, S
         self.full = list(full)
@@ -44,6 +60,19 @@ class GeoCacheRunner:
         self.bbox = gc_posmap_bbox(pos, tol_frac, stream=stream)
         self._ops: Dict[Tuple[int, ...], Tuple[torch.Tensor, torch.Tensor, Optional[VisibleIndex]]] = {}
         self.unipc_order, self.unipc_corrector = unipc_order, unipc_corrector
+        self.anchor_policy, self.max_gap = anchor_policy, max_gap
+        self.refresh_tau, self.refresh_R, self.geom = refresh_tau, refresh_R, geom
+        self.tracking = anchor_policy != "rotate" or refresh_tau is not None
+        self.rotation_sets: List[List[int]] = []
+        for c in range(self.N):
+            A = gc_schedule_anchors(self.N, a, c)
+            if A not in self.rotation_sets:
+                self.rotation_sets.append(A)
+        self.pairs = gc_coverage_pairs(pos, cams, self.bbox, stream=stream) if self.tracking else None
+        self.stale: Optional[torch.Tensor] = None
+        self.stats_host = None                        # per-view staleness statistics after the last step
+        self.gap: List[int] = [0] * self.N            # cached steps since each view was last an anchor
+        self.last_full = False
         self.k = 0
         self.c = 0
         self.x_t: Optional[torch.Tensor] = None
@@ -67,6 +96,39 @@ class GeoCacheRunner:
     def start(self, x_t: torch.Tensor) -> None:
         self.x_t, self.x0, self.k, self.c = x_t, None, 0, 0
         self.x0_km2, self.x_c = None, None
+        if self.tracking:
+            self.stale = gc_coverage_init(self.pos, stream=self.stream)
+            self.stats_host = None
+        self.gap = [0] * self.N
+        self.last_full = False
+
+    def _is_full(self, k: int) -> bool:
+        if self.full[k] or self.x0 is None:
+            return True
+        return (self.refresh_tau is not None and self.stats_host is not None
+                and gc_schedule_refresh_due(self.stats_host, self.refresh_tau))
+
+    def _anchors(self) -> List[int]:
+        """Anchor set of the next cached step (advances the cached-step counter)."""
+        c = self.c
+        self.c += 1
+        if self.anchor_policy == "rotate":
+            return gc_schedule_anchors(self.N, self.a, c)
+        if self.anchor_policy == "rotation_coverage":
+            sc = gc_coverage_score(self.pairs, self.stale, self.rotation_sets, stream=self.stream).cpu().tolist()
+            return list(self.rotation_sets[sc.index(max(sc))])
+        due = [v for v in range(self.N) if self.max_gap and self.gap[v] >= self.max_gap]
+        due = sorted(due, key=lambda v: (-self.gap[v], v))[:self.a]
+        sel = gc_coverage_select(self.pairs, self.stale, self.a, forced=due, stream=self.stream)
+        return [int(v) for v in sel.cpu().tolist()]
+
+    def _after(self, views: List[int], full: bool) -> None:
+        """Staleness and anchor gaps after a step with the given views."""
+        self.last_full = full
+        self.gap = [0 if (full or v in views) else g + 1 for v, g in enumerate(self.gap)]
+        if self.tracking:
+            stats = gc_coverage_update(self.pairs, self.stale, views, self.refresh_R, stream=self.stream)
+            self.stats_host = stats.cpu()
 
     def step(self, predict: Predict) -> List[int]:
         """Run sampler step k; returns the views the denoiser was asked for."""
@@ -76,17 +138,23 @@ class GeoCacheRunner:
         if self.unipc_order:
             return self._step_unipc(predict)
         t, tn = gc_sampler_step_times(self.sampler, self.S, k)
-        if self.full[k] or self.x0 is None:
+        full = self._is_full(k)
+        if full:
             views = list(range(self.N))
             x0 = predict(k, views).contiguous()
             x_next, _ = gc_sampler_reconstruct(self.x_t, x0, self.sampler, t, tn, stream=self.stream)
         else:
-            views = gc_schedule_anchors(self.N, self.a, self.c)
-            self.c += 1
-            corr, wts, idx = self.operator(views)
-            x0, x_next, _ = gc_transport_reconstruct(self.x0, predict(k, views).contiguous(), corr, wts, self.x_t,
-                                                     views, self.sampler, t, tn, index=idx, stream=self.stream)
+            views = self._anchors()
+            new = predict(k, views).contiguous()
+            if self.geom:
+                x0, x_next, _ = gc_transport_reconstruct_geom(self.x0, new, self.pos, self.cams, self.bbox, self.x_t,
+                                                              views, self.K, self.sampler, t, tn, stream=self.stream)
+            else:
+                corr, wts, idx = self.operator(views)
+                x0, x_next, _ = gc_transport_reconstruct(self.x0, new, corr, wts, self.x_t, views, self.sampler, t,
+                                                         tn, index=idx, stream=self.stream)
         self.x0, self.x_t = x0, x_next
+        self._after(views, full)
         self.k += 1
         return views
 
@@ -94,19 +162,20 @@ class GeoCacheRunner:
         k = self.k
         st = gc_unipc_coeffs(self.sampler, self.S, k, self.unipc_order, self.unipc_corrector)
         m2 = self.x0_km2 if st.use_corrector and st.c_mk2 != 0.0 else None
-        if self.full[k] or self.x0 is None:
+        full = self._is_full(k)
+        if full:
             views = list(range(self.N))
             mk = predict(k, views).contiguous()
             x_c, x_next = gc_unipc_update(st, mk, x_cur=self.x_t, x_prev=self.x_c if st.use_corrector else None,
                                           m_km2=m2, m_km1=self.x0, stream=self.stream)
         else:
-            views = gc_schedule_anchors(self.N, self.a, self.c)
-            self.c += 1
+            views = self._anchors()
             corr, wts, idx = self.operator(views)
             mk, x_c, x_next = gc_transport_unipc(self.x0, predict(k, views).contiguous(), corr, wts, views, st,
                                                  x_cur=self.x_t, x_prev=self.x_c if st.use_corrector else None,
                                                  m_km2=m2, index=idx, stream=self.stream)
         self.x0_km2, self.x0, self.x_c, self.x_t = self.x0, mk, x_c, x_next
+        self._after(views, full)
         self.k += 1
         return views
 
@@ -118,10 +187,16 @@ class GeoCacheRunner:
         """Loop state for checkpoint / resume (tensors are cloned)."""
         cl = lambda t: None if t is None else t.clone()
         return {"k": self.k, "c": self.c, "x_t": cl(self.x_t), "x0": cl(self.x0), "x0_km2": cl(self.x0_km2),
-                "x_c": cl(self.x_c)}
+                "x_c": cl(self.x_c), "stale": cl(self.stale), "stats": cl(self.stats_host), "gap": list(self.gap)}
 
     def load_state_dict(self, st: dict) -> None:
         cl = lambda t: None if t is None else t.clone()
         self.k, self.c = int(st["k"]), int(st["c"])
         self.x_t, self.x0 = cl(st["x_t"]), cl(st["x0"])
         self.x0_km2, self.x_c = cl(st.get("x0_km2")), cl(st.get("x_c"))
+        if self.tracking:
+            if st.get("stale") is None:
+                raise ValueError("this runner tracks staleness: the state needs 'stale'")
+            self.stale = cl(st["stale"])
+            self.stats_host = cl(st.get("stats"))
+        self.gap = list(st.get("gap", [0] * self.N))

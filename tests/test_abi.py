@@ -26,7 +26,7 @@ A0, A1, A2, A3, A4, A5 = (0x10000000 * (i + 1) for i in range(6))
 def header_functions():
     src = open(HEADER).read()
     src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
-    return sorted(set(re.findall(r"^\s*(?:int|size_t|const char\*)\s+(gc_\w+)\s*\(", src, flags=re.M)))
+    return sorted(set(re.findall(r"^\s*(?:int64_t|int|size_t|const char\*)\s+(gc_\w+)\s*\(", src, flags=re.M)))
 
 
 @pytest.fixture(scope="module")
