@@ -2,7 +2,9 @@
 that are not multiples of anything, 2-7 views, 1-4 anchors, K = 1..4, C = 4..16,
 float32 / bfloat16, orthographic or pinhole rigs with random poses (points
 behind a pinhole camera included), random background holes and tolerances --
-through the whole per-step path against the oracle, plus HIP-graph replays.
+through the whole per-step path against the oracle (the on-the-fly operator
+bit for bit against the stored one, the coverage visibility bits against the
+oracle's), plus HIP-graph replays.
 """
 import math
 
@@ -90,15 +92,29 @@ def test_random_problems_match_oracle(seed, H, W, N, a_frac, K, C, dtype, pinhol
     assert np.abs(wts.cpu().numpy() - wts_o).max(initial=0.0) <= 1e-6
     idx = gc.gc_index_correspondence(corr)
     assert idx.n_vis == int((nvis_o > 0).sum())
+    outs = []
     for index in (None, idx):
         x0_out, x_next, mo = gc.gc_transport_reconstruct(to_dev(prev, dtype), to_dev(new, dtype), corr, wts,
                                                          to_dev(xt, dtype), anchors, smp, t, tn, index=index)
+        outs.append((x0_out, x_next, mo))
         x0h = to_host(x0_out, dtype)
         assert np.abs(synth.values(x0h, dtype).astype(np.float64) - x0_exact).max() <= TOL[dtype]
         assert np.abs(synth.values(to_host(x_next, dtype), dtype).astype(np.float64) - xn_o).max() <= TOL[dtype]
         same = np.ones(x0h.shape, bool) if dtype == "f32" else (x0h == x0_state)
         err = np.abs(synth.values(to_host(mo, dtype), dtype).astype(np.float64) - mo_o)[same]
         assert err.max(initial=0.0) <= TOL[dtype] * cond
+    # the on-the-fly operator equals the stored one bit for bit
+    cams_d = gc.camera_tensor(bcams, DEV)
+    geo = gc.gc_transport_reconstruct_geom(to_dev(prev, dtype), to_dev(new, dtype), Pd, cams_d, bbd,
+                                           to_dev(xt, dtype), anchors, K, smp, t, tn)
+    iv = torch.int32 if dtype == "f32" else torch.int16
+    for g_, r_ in zip(geo, outs[0]):
+        assert torch.equal(g_.view(iv), r_.view(iv))
+    # single-anchor visibility bits equal the oracle's
+    bits = gc.gc_coverage_pairs(Pd, cams_d, bbd).cpu().numpy().view(np.uint32)
+    unpacked = np.unpackbits(np.ascontiguousarray(bits).view(np.uint8), axis=-1, bitorder="little")
+    unpacked = unpacked.reshape(N, 1, N, -1)[..., :H * W].reshape(N, 1, N, H, W)
+    np.testing.assert_array_equal(unpacked, oracle.coverage_pairs(P, bcams, K, bb))
 
 
 def test_graph_replays_match_eager():
