@@ -27,7 +27,7 @@ _LIB = None
 DTYPES = {"f32": 0, "bf16": 1}
 PRED = {"none": 0, "eps": 1, "v": 2, "vel": 3}
 KIND = {"ddim": 0, "flow": 1}
-FULL_RULE = {"periodic": 0, "head_mid_tail": 1}
+FULL_RULE = {"periodic": 0, "head_mid_tail": 1, "head_tail_e": 2}
 
 _i32p = ctypes.POINTER(ctypes.c_int32)
 _f32p = ctypes.POINTER(ctypes.c_float)

@@ -535,6 +535,13 @@ int orc_full_steps(int rule, int S, int E, uint8_t* out) {
     if (S > 1) out[1] = 1;
     out[S / 2] = 1;
     out[S - 1] = 1;
+  } else if (rule == 2) {
+    /* Sec. 4.1, configurations: E full-view refresh steps at the end of the
+     * trajectory, after the two-step head of the drift-bounding schedule */
+    if (E < 0 || E > S) return -1;
+    out[0] = 1;
+    if (S > 1) out[1] = 1;
+    for (int k = S - E; k < S; ++k) out[k] = 1;
   } else {
     return -1;
   }

@@ -645,6 +645,13 @@ def test_full_step_sets():
     assert [k for k, f in enumerate(oracle.full_steps("head_mid_tail", 50)) if f] == [0, 1, 25, 49]
     # the paper's Hunyuan operating point: 10 steps, four of them full
     assert sum(oracle.full_steps("head_mid_tail", 10)) == 4
+    # "a=2, E=5, S=10": the two-step head and E = 5 refresh steps at the end
+    assert [k for k, f in enumerate(oracle.full_steps("head_tail_e", 10, 5)) if f] == [0, 1, 5, 6, 7, 8, 9]
+    assert [k for k, f in enumerate(oracle.full_steps("head_tail_e", 30, 1)) if f] == [0, 1, 29]
+    assert [k for k, f in enumerate(oracle.full_steps("head_tail_e", 8, 0)) if f] == [0, 1]
+    assert all(oracle.full_steps("head_tail_e", 6, 6))
+    with pytest.raises(ValueError):
+        oracle.full_steps("head_tail_e", 10, 11)
 
 
 @pytest.mark.parametrize("kind,dtype", [("ddim", "f32"), ("flow", "bf16")])
