@@ -95,6 +95,7 @@ extern "C" {
 /* full-step rules for gc_schedule_full_steps */
 #define GC_FULL_PERIODIC 0      /* steps 0, E, 2E, ... */
 #define GC_FULL_HEAD_MID_TAIL 1 /* steps 0, 1, floor(S/2), S-1 */
+#define GC_FULL_HEAD_TAIL_E 2   /* steps 0, 1 and the last E steps */
 
 /*
  * A pinhole or orthographic camera (68 bytes, 4-byte aligned).
@@ -446,7 +447,9 @@ int gc_schedule_refresh_due(const uint32_t* stats, int B, int N, double tau, int
  * gc_schedule_full_steps: is_full_out[k] = 1 for the full-view steps of an
  * S-step trajectory (Sec. 3.2, drift-bounding schedule; Sec. 4.1,
  * configurations): GC_FULL_PERIODIC every E-th step, GC_FULL_HEAD_MID_TAIL
- * steps {0, 1, floor(S/2), S-1}.  Step 0 is always full.
+ * steps {0, 1, floor(S/2), S-1}, GC_FULL_HEAD_TAIL_E steps {0, 1} and the last
+ * E steps (E full-view refresh steps at the end, 0 <= E <= S).  Step 0 is
+ * always full.
  *
  * gc_sampler_step_times: (t, t_next) of step k of an S-step trajectory.
  * DDIM: trailing timesteps t_k = round((S-k) T / S) - 1 and t_S = -1.

@@ -27,7 +27,7 @@ GC_OK = 0
 GC_F32, GC_BF16 = 0, 1
 GC_DDIM, GC_FLOW_EULER = 0, 1
 GC_PRED_NONE, GC_PRED_EPS, GC_PRED_V, GC_PRED_VEL = 0, 1, 2, 3
-GC_FULL_PERIODIC, GC_FULL_HEAD_MID_TAIL = 0, 1
+GC_FULL_PERIODIC, GC_FULL_HEAD_MID_TAIL, GC_FULL_HEAD_TAIL_E = 0, 1, 2
 GC_MAX_VIEWS, GC_MAX_ANCHORS, GC_MAX_GRID = 64, 8, 4094
 ERRORS = {-1: "GC_ERR_ARG", -2: "GC_ERR_SHAPE", -3: "GC_ERR_DTYPE", -4: "GC_ERR_ALIGN",
           -5: "GC_ERR_ALIAS", -6: "GC_ERR_CAPACITY", -7: "GC_ERR_HIP"}

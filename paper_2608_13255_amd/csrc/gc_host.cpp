@@ -136,6 +136,11 @@ int gc_schedule_full_steps(int rule, int S, int E, uint8_t* is_full_out) {
     if (S > 1) is_full_out[1] = 1;
     is_full_out[S / 2] = 1;
     is_full_out[S - 1] = 1;
+  } else if (rule == GC_FULL_HEAD_TAIL_E) {
+    if (E < 0 || E > S) return fail(GC_ERR_ARG, "head + tail full steps need 0 <= E <= S (got E=%d, S=%d)", E, S);
+    is_full_out[0] = 1;
+    if (S > 1) is_full_out[1] = 1;
+    for (int k = S - E; k < S; ++k) is_full_out[k] = 1;
   } else {
     return fail(GC_ERR_ARG, "unknown full-step rule %d", rule);
   }

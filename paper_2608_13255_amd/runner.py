@@ -17,7 +17,7 @@ from typing import Callable, Dict, List, Optional, Sequence, Tuple
 
 import torch
 
-from . import (GC_FULL_HEAD_MID_TAIL, GC_FULL_PERIODIC, Sampler, VisibleIndex, gc_build_correspondence,
+from . import (GC_FULL_HEAD_MID_TAIL, GC_FULL_HEAD_TAIL_E, GC_FULL_PERIODIC, Sampler, VisibleIndex, gc_build_correspondence,
                gc_coverage_init, gc_coverage_pairs, gc_coverage_score, gc_coverage_select, gc_coverage_update,
                gc_index_correspondence, gc_posmap_bbox, gc_sampler_reconstruct, gc_sampler_step_times,
                gc_schedule_anchors, gc_schedule_full_steps, gc_schedule_refresh_due, gc_transport_reconstruct,
@@ -82,7 +82,12 @@ class GeoCacheRunner:
 
     @staticmethod
     def full_steps(rule: str, S: int, E: int = 0) -> List[int]:
-        return gc_schedule_full_steps(GC_FULL_PERIODIC if rule == "periodic" else GC_FULL_HEAD_MID_TAIL, S, E)
+        """rule "periodic" (every E-th step), "head_mid_tail" ({0, 1, S/2, S-1}) or
+        "head_tail_e" ({0, 1} and the last E steps)."""
+        codes = {"periodic": GC_FULL_PERIODIC, "head_mid_tail": GC_FULL_HEAD_MID_TAIL, "head_tail_e": GC_FULL_HEAD_TAIL_E}
+        if rule not in codes:
+            raise ValueError(f"unknown full-step rule {rule!r}")
+        return gc_schedule_full_steps(codes[rule], S, E)
 
     def operator(self, anchors: Sequence[int]):
         """(corr, weights, index) of an anchor set, built on first use."""

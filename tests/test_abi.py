@@ -145,7 +145,9 @@ def test_host_schedule_matches_oracle(gc):
                 seen |= set(gc.gc_schedule_anchors(N, a, c))
             assert seen == set(range(N))
     for rule, name, S, E in [(0, "periodic", 30, 5), (0, "periodic", 30, 4), (1, "head_mid_tail", 30, 0),
-                             (1, "head_mid_tail", 50, 0), (1, "head_mid_tail", 10, 0), (0, "periodic", 1, 3)]:
+                             (1, "head_mid_tail", 50, 0), (1, "head_mid_tail", 10, 0), (0, "periodic", 1, 3),
+                             (2, "head_tail_e", 10, 5), (2, "head_tail_e", 30, 1), (2, "head_tail_e", 8, 0),
+                             (2, "head_tail_e", 6, 6), (2, "head_tail_e", 1, 1)]:
         assert gc.gc_schedule_full_steps(rule, S, E) == oracle.full_steps(name, S, E)
     ddim = gc.Sampler(kind=gc.GC_DDIM)
     flow = gc.Sampler(kind=gc.GC_FLOW_EULER)
@@ -161,6 +163,8 @@ def test_host_schedule_matches_oracle(gc):
         gc.gc_schedule_anchors(6, 7, 0)
     with pytest.raises(gc.GeoCacheError):
         gc.gc_schedule_full_steps(5, 10, 1)
+    with pytest.raises(gc.GeoCacheError):
+        gc.gc_schedule_full_steps(2, 10, 11)
 
 
 def test_product_fails_loudly_without_library(tmp_path):
