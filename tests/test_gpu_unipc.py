@@ -103,14 +103,18 @@ def test_transport_unipc_parity(gc, w):
     assert torch.equal(xc2.view(iv), outs[0][1].view(iv)) and torch.equal(xn2.view(iv), outs[0][2].view(iv))
 
 
-def test_unipc_trajectory_headline_operating_point(gc):
+@pytest.mark.parametrize("rule,E,expect", [("head_mid_tail", 0, [0, 1, 5, 9]),
+                                           ("head_tail_e", 5, [0, 1, 5, 6, 7, 8, 9])])
+def test_unipc_trajectory_headline_operating_point(gc, rule, E, expect):
+    """a = 2 of N = 6 over 10 UniPC steps: the schedule section's four full
+    steps, and the configurations' "a=2, E=5, S=10" point."""
     from paper_2608_13255_amd.runner import GeoCacheRunner
     w = synth.shrink(C2, S=10)
     S = 10
     P = latent_maps(C2.name)
     cams = synth.batch_cameras(w)
-    full = GeoCacheRunner.full_steps("head_mid_tail", S)
-    assert [k for k in range(S) if full[k]] == [0, 1, 5, 9]
+    full = GeoCacheRunner.full_steps(rule, S, E)
+    assert [k for k in range(S) if full[k]] == expect
     preds = {}
 
     def stub_np(k, views):
