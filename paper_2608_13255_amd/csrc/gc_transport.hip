@@ -412,7 +412,7 @@ void launch_transport(const TArgs& g, int dtype, hipStream_t stream) {
 
 // Validate UniPC coefficients / buffers and load them into g.
 int prepare_unipc(const gc_unipc_step* st, const void* x_cur, const void* x_prev, const void* m_km2,
-                  const void* m_km1, size_t nbytes, const char* who, TArgs* g) {
+                  const void* m_km1, const char* who, TArgs* g) {
   if (!st) return fail(GC_ERR_ARG, "%s: null coefficients", who);
   g->u_corr = st->use_corrector ? 1 : 0;
   g->u_need_m2 = (g->u_corr && st->c_mk2 != 0.0) ? 1 : 0;
@@ -434,7 +434,6 @@ int prepare_unipc(const gc_unipc_step* st, const void* x_cur, const void* x_prev
   g->up_xc = (float)st->p_xc;
   g->up_mk1 = (float)st->p_mk1;
   g->up_mk = (float)st->p_mk;
-  (void)nbytes;
   return GC_OK;
 }
 
@@ -541,7 +540,7 @@ extern "C" int gc_unipc_update(const void* x_cur, const void* x_prev, const void
   TArgs g;
   std::memset(&g, 0, sizeof(g));
   const size_t nb = (size_t)n_elems * dtype_bytes(dtype);
-  int rc = prepare_unipc(st, x_cur, x_prev, m_km2, m_km1, nb, "gc_unipc_update", &g);
+  int rc = prepare_unipc(st, x_cur, x_prev, m_km2, m_km1, "gc_unipc_update", &g);
   if (rc) return rc;
   g.x0_prev = m_km1;
   g.x_c = x_c;
@@ -583,7 +582,7 @@ extern "C" int gc_transport_unipc(const void* x0_prev, const void* x0_anchor_new
   if (!x_c || !x_next) return fail(GC_ERR_ARG, "gc_transport_unipc: null x_c or x_next");
   const size_t es = (size_t)dtype_bytes(dtype);
   const size_t n_all = (size_t)B * N * H * W * C * es, n_new = (size_t)B * a * H * W * C * es;
-  rc = prepare_unipc(st, x_cur, x_prev, m_km2, x0_prev, n_all, "gc_transport_unipc", &g);
+  rc = prepare_unipc(st, x_cur, x_prev, m_km2, x0_prev, "gc_transport_unipc", &g);
   if (rc) return rc;
   if (!aligned16(x_c) || !aligned16(x_next)) return fail(GC_ERR_ALIGN, "gc_transport_unipc: outputs must be 16-byte aligned");
   const void* ins[5] = {x0_prev, x0_anchor_new, x_cur, x_prev, m_km2};
