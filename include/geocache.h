@@ -204,10 +204,10 @@ int gc_build_correspondence(const float* pos, const gc_camera* cams, int B, int 
 /*
  * Visible-token index of a correspondence operator (once per asset and
  * anchor set).  A token's row of G_{A->v} is non-zero iff at least one anchor
- * sees it (Sec. 3.2: rows with no in-tolerance tap are zero).  The index lets
- * the per-step calls split their work: the visible tokens, listed compactly,
- * get the gathering; every other token is streamed and recognised by one bit
- * instead of its a correspondence words.
+ * sees it (Sec. 3.2: a token with no tap inside the tolerance has an all-zero
+ * row).  The index lets the per-step calls split their work: the visible
+ * tokens, listed compactly, get the gathering; every other token is streamed
+ * and recognised by one bit instead of its a correspondence words.
  *   corr       device int32 [n_tokens][a] words from gc_build_correspondence,
  *              n_tokens = B * (N - a) * H * W (at most 2^31 - 1)
  *   vis_bits   device uint32 [ceil(n_tokens / 32)] output: bit (i & 31) of word
@@ -350,8 +350,9 @@ int gc_transport_unipc(const void* x0_prev, const void* x0_anchor_new, const int
 
 /*
  * Cached step with the correspondence computed on the fly (Sec. 3.2: the
- * operator depends on geometry alone).  Instead of a stored G_{A->v}, the
- * kernel projects every target token into the anchor cameras and runs the
+ * operator is a function of the position maps and cameras only).  Instead of
+ * a stored G_{A->v}, the kernel projects every target token into the anchor
+ * cameras and runs the
  * same tap test, selection and weighting as gc_build_correspondence, then
  * applies Eq. 1 (and, for the _reconstruct variant, the sampler step).  The
  * outputs equal gc_build_correspondence + gc_transport_step (+ the sampler

@@ -1,9 +1,10 @@
 // Cached step with the correspondence computed on the fly: Eq. 1 (and the
 // sampler reconstruction) reading the position maps and cameras directly
-// instead of a stored G_{A->v}.  The operator depends on geometry alone
-// (Sec. 3.2, correspondence operator), so it can be rebuilt inside the step
-// from 12 bytes of position per target token plus the anchors' position
-// taps; nothing has to be built or stored per anchor set.  That pays when
+// instead of a stored G_{A->v}.  The operator is a function of the position
+// maps and cameras only (Sec. 3.2, correspondence operator), so it can be
+// rebuilt inside the step from 12 bytes of position per target token plus
+// the anchors' position taps; nothing has to be built or stored per anchor
+// set.  That pays when
 // anchor sets do not repeat (e.g. chosen adaptively); with the rotation's
 // few repeating sets the stored operator and its visible-token index are
 // cheaper per step.

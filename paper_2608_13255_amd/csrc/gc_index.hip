@@ -2,8 +2,9 @@
 // anchor set).
 //
 // G_{A->v} has a non-zero row only for tokens some anchor sees (Sec. 3.2:
-// rows with no in-tolerance tap are zero).  The per-step kernel splits its
-// work on that: blocks over a compact list of the visible tokens do the
+// a token with no tap inside the tolerance has an all-zero row).  The
+// per-step kernel splits its work on that: blocks over a compact list of the
+// visible tokens do the
 // gathers, and blocks over all tokens stream everything else, skipping
 // visible tokens by a one-bit-per-token mask instead of reading their words.
 //
