@@ -161,3 +161,70 @@ def test_graph_replays_match_eager():
             assert torch.equal(o.view(torch.int32), eo.view(torch.int32)), rep
             assert torch.equal(n.view(torch.int32), en.view(torch.int32)), rep
         _ = (x0 * 2).sum().item()          # eager work between replays
+
+
+def test_graph_replays_other_paths():
+    """The on-the-fly step, the fused UniPC step and the coverage update +
+    greedy selection captured in one HIP graph: every replay (with eager
+    work, state resets and synchronisations between replays) equals the
+    eager result bit for bit."""
+    import paper_2608_13255_amd as gc
+    from conftest import latent_maps
+    from synth.configs import C4
+    w = C4
+    P = torch.from_numpy(latent_maps(w.name)).to(DEV)
+    cams = gc.camera_tensor(synth.batch_cameras(w), DEV)
+    bb = gc.gc_posmap_bbox(P, w.tol_frac)
+    rs = np.random.default_rng(5)
+    shape = (1, w.N, w.H, w.W, w.C)
+    bf = lambda sh: torch.from_numpy(rs.standard_normal(sh).astype(np.float32)).to(DEV).to(torch.bfloat16)
+    A0, A1 = gc.gc_schedule_anchors(w.N, w.a, 0), gc.gc_schedule_anchors(w.N, w.a, 1)
+    corr1, wts1 = gc.gc_build_correspondence(P, cams, A1, w.K, bb)
+    idx1 = gc.gc_index_correspondence(corr1)
+    x0, xt, xprev, m2 = bf(shape), bf(shape), bf(shape), bf(shape)
+    new0, new1 = bf((1, w.a, w.H, w.W, w.C)), bf((1, w.a, w.H, w.W, w.C))
+    smp = gc.Sampler(kind=gc.GC_DDIM, pred_out=gc.GC_PRED_EPS)
+    st = gc.gc_unipc_coeffs(gc.Sampler(kind=gc.GC_DDIM), 30, 6, 2, True)
+    outs = {k: torch.empty_like(x0) for k in ("g0", "g1", "g2", "u0", "u1", "u2")}
+    pairs = gc.gc_coverage_pairs(P, cams, bb)
+    stale0 = gc.gc_coverage_init(P)
+    for A in (A0, A1, A0):
+        gc.gc_coverage_update(pairs, stale0, A, 2)
+    stale = stale0.clone()
+    stats = torch.empty((1, w.N, 4), dtype=torch.int32, device=DEV)
+    sel = torch.empty(w.a, dtype=torch.int32, device=DEV)
+    ws = torch.empty(gc.gc_coverage_workspace_bytes(), dtype=torch.uint8, device=DEV)
+    s = torch.cuda.Stream()
+    torch.cuda.synchronize()
+
+    def step():
+        gc.gc_transport_reconstruct_geom(x0, new0, P, cams, bb, xt, A0, w.K, smp, 700, 666, x0_out=outs["g0"],
+                                         x_next=outs["g1"], model_out=outs["g2"], stream=s)
+        gc.gc_transport_unipc(x0, new1, corr1, wts1, A1, st, x_prev=xprev, m_km2=m2, x0_out=outs["u0"],
+                              x_c=outs["u1"], x_next=outs["u2"], index=idx1, stream=s)
+        gc.gc_coverage_update(pairs, stale, A1, 2, stats=stats, stream=s)
+        gc.gc_coverage_select(pairs, stale, w.a, forced=[w.N - 1], out=sel, workspace=ws, stream=s)
+
+    with torch.cuda.stream(s):
+        step()
+    torch.cuda.synchronize()
+    eager = {k: v.clone() for k, v in outs.items()}
+    eager_stale, eager_stats, eager_sel = stale.clone(), stats.clone(), sel.clone()
+    g = torch.cuda.CUDAGraph()
+    stale.copy_(stale0)
+    torch.cuda.synchronize()
+    with torch.cuda.graph(g, stream=s):
+        step()
+    for rep in range(4):
+        stale.copy_(stale0)
+        for v in outs.values():
+            v.fill_(float("nan"))
+        stats.fill_(-1)
+        sel.fill_(-1)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for k, v in outs.items():
+            assert torch.equal(v.view(torch.int16), eager[k].view(torch.int16)), (rep, k)
+        assert torch.equal(stale, eager_stale) and torch.equal(stats, eager_stats) and torch.equal(sel, eager_sel), rep
+        _ = (x0.float() * 2).sum().item()  # eager work between replays
