@@ -17,6 +17,12 @@ namespace gc {
 namespace {
 
 constexpr int kBlock = 256;
+// Launch size of the builder, in blocks per CU (256 CUs).  The coverage
+// counters cost one device-scope atomic per block and counter, and atomics
+// on one address serialise, so a build that counts uses fewer, longer
+// blocks; one that does not uses enough blocks to hide its load latency.
+constexpr int kBuildBlocksPerCU = 16;
+constexpr int kBuildBlocksPerCUStats = 4;
 
 struct BuildArgs {
   const float* pos;
@@ -50,8 +56,11 @@ __device__ __forceinline__ uint32_t wave_sum(uint32_t v) {
 // nearest and forms that anchor's normalised area weights; the number of
 // anchors that see the token (n_vis) is a ballot over the lane group.  Words
 // and weights of one token are adjacent, so a group writes them coalesced.
-// grid: x = token blocks, y = b * NT + target slot; the block's anchor
-// cameras are staged in LDS.
+// grid: y = b * NT + target slot; x = blocks that stride over the view's
+// token chunks (kBlock / G tokens each).  A block counts its visible pairs /
+// tokens / foreground tokens / taps over all its chunks and adds them to
+// the asset's counters once: few blocks per asset keep the same-address
+// atomics from serialising.  The block's anchor cameras are staged in LDS.
 template <int G>
 __global__ __launch_bounds__(kBlock) void k_build(BuildArgs g) {
   __shared__ gc_camera cam_lds[GC_MAX_ANCHORS];
@@ -64,74 +73,83 @@ __global__ __launch_bounds__(kBlock) void k_build(BuildArgs g) {
   __syncthreads();
 
   const int s = threadIdx.x & (G - 1);                   // anchor slot of this lane
-  const int p = blockIdx.x * (kBlock / G) + threadIdx.x / G;
-  const bool live = p < HW && s < g.a;
   const float tol2 = g.bbox[(int64_t)b * 8 + 6];
+  const int n_chunks = (HW + kBlock / G - 1) / (kBlock / G);
+  uint32_t c_pairs = 0, c_pix = 0, c_fg = 0;   // wave totals (uniform across the wave)
+  uint32_t taps_lane = 0;                       // this lane's kept taps, summed over the wave at the end
+  for (int chunk = blockIdx.x; chunk < n_chunks; chunk += gridDim.x) {
+    const int p = chunk * (kBlock / G) + threadIdx.x / G;
+    const bool live = p < HW && s < g.a;
 
-  float P[3] = {0.f, 0.f, 0.f};
-  bool fg = false;
-  if (p < HW) {
-    const float* pp = g.pos + (((int64_t)b * g.N + v) * HW + p) * 3;
-    P[0] = pp[0];
-    P[1] = pp[1];
-    P[2] = pp[2];
-    fg = finite_f(P[0]) && finite_f(P[1]) && finite_f(P[2]);
-  }
+    float P[3] = {0.f, 0.f, 0.f};
+    bool fg = false;
+    if (p < HW) {
+      const float* pp = g.pos + (((int64_t)b * g.N + v) * HW + p) * 3;
+      P[0] = pp[0];
+      P[1] = pp[1];
+      P[2] = pp[2];
+      fg = finite_f(P[0]) && finite_f(P[1]) && finite_f(P[2]);
+    }
 
-  int32_t word = 0;
-  float wk[4] = {0.f, 0.f, 0.f, 0.f};   // this anchor's normalised weight of tap k
-  int mask = 0;
-  if (live && fg) {
-    const AnchorTaps at = anchor_taps(P, cam_lds[s], g.pos + ((int64_t)b * g.N + g.anchor_view[s]) * HW * 3, g.H,
-                                      g.W, g.K, tol2);
-    word = at.word;
-    mask = at.mask;
+    int32_t word = 0;
+    float wk[4] = {0.f, 0.f, 0.f, 0.f};   // this anchor's normalised weight of tap k
+    int mask = 0;
+    if (live && fg) {
+      const AnchorTaps at = anchor_taps(P, cam_lds[s], g.pos + ((int64_t)b * g.N + g.anchor_view[s]) * HW * 3, g.H,
+                                        g.W, g.K, tol2);
+      word = at.word;
+      mask = at.mask;
 #pragma unroll
-    for (int k = 0; k < 4; ++k) wk[k] = at.wk[k];
-  }
+      for (int k = 0; k < 4; ++k) wk[k] = at.wk[k];
+    }
 
-  // n_vis: anchors of this token that see it -- a ballot over the lane group
-  const unsigned long long seen = __ballot(word != 0);
-  const int lane = __lane_id();
-  const int gbase = lane & ~(G - 1);
-  const int n_vis = __popcll((seen >> gbase) & ((G == 64) ? ~0ull : ((1ull << G) - 1)));
+    // n_vis: anchors of this token that see it -- a ballot over the lane group
+    const unsigned long long seen = __ballot(word != 0);
+    const int lane = __lane_id();
+    const int gbase = lane & ~(G - 1);
+    const int n_vis = __popcll((seen >> gbase) & ((G == 64) ? ~0ull : ((1ull << G) - 1)));
 
-  if (live) {
-    const int64_t row = ((int64_t)b * g.NT + ti) * HW + p;
-    g.corr[row * g.a + s] = word;
-    float out[4] = {0.f, 0.f, 0.f, 0.f};
-    const float inv = n_vis > 0 ? (float)n_vis : 1.0f;
-    int j = 0;
+    if (live) {
+      const int64_t row = ((int64_t)b * g.NT + ti) * HW + p;
+      g.corr[row * g.a + s] = word;
+      float out[4] = {0.f, 0.f, 0.f, 0.f};
+      const float inv = n_vis > 0 ? (float)n_vis : 1.0f;
+      int j = 0;
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      if (mask & (1 << k)) {
-        // j-th kept tap -> slot j
+      for (int k = 0; k < 4; ++k) {
+        if (mask & (1 << k)) {
+          // j-th kept tap -> slot j
+#pragma unroll
+          for (int q = 0; q < 4; ++q)
+            if (q == j) out[q] = wk[k] / inv;
+          ++j;
+        }
+      }
+      float* ww = g.weights + (row * g.a + s) * g.K;
+      if (g.K == 4) {   // 16-byte aligned: the weights base is, and each (token, slot) row is 16 bytes
+        *reinterpret_cast<float4*>(ww) = make_float4(out[0], out[1], out[2], out[3]);
+      } else {
 #pragma unroll
         for (int q = 0; q < 4; ++q)
-          if (q == j) out[q] = wk[k] / inv;
-        ++j;
+          if (q < g.K) ww[q] = out[q];
       }
     }
-    float* ww = g.weights + (row * g.a + s) * g.K;
-    if (g.K == 4) {   // 16-byte aligned: the weights base is, and each (token, slot) row is 16 bytes
-      *reinterpret_cast<float4*>(ww) = make_float4(out[0], out[1], out[2], out[3]);
-    } else {
-#pragma unroll
-      for (int q = 0; q < 4; ++q)
-        if (q < g.K) ww[q] = out[q];
+
+    if (g.stats) {
+      const bool lead = (threadIdx.x & (G - 1)) == 0 && p < HW;
+      c_pairs += (uint32_t)__popcll(seen);
+      c_pix += wave_count(lead && n_vis > 0);
+      c_fg += wave_count(lead && fg);
+      taps_lane += live ? (uint32_t)__popc(mask) : 0u;
     }
   }
 
   if (g.stats) {
-    // blocks never straddle assets (grid y is per asset and target): waves
-    // count with ballots, the block sums in LDS, one thread adds to the
-    // asset's counters
+    // blocks never straddle assets (grid y is per asset and target): the
+    // block sums its waves' totals in LDS, one thread per counter adds them
+    // to the asset's counters
     __shared__ uint32_t part[kBlock / 64][4];
-    const uint32_t c_pairs = (uint32_t)__popcll(seen);
-    const bool lead = (threadIdx.x & (G - 1)) == 0 && p < HW;
-    const uint32_t c_pix = wave_count(lead && n_vis > 0);
-    const uint32_t c_fg = wave_count(lead && fg);
-    const uint32_t c_taps = wave_sum(live ? (uint32_t)__popc(mask) : 0u);
+    const uint32_t c_taps = wave_sum(taps_lane);
     const int wv = threadIdx.x / 64;
     if (__lane_id() == 0) {
       part[wv][0] = c_pairs;
@@ -201,13 +219,17 @@ extern "C" int gc_build_correspondence(const float* pos, const gc_camera* cams, 
   g.NT = NT;
   if (stats) hipLaunchKernelGGL(k_zero_u32, dim3((4 * B + 255) / 256), dim3(256), 0, stream, stats, 4 * B);
   if (NT > 0) {
-    if (a <= 4) {
-      const unsigned bx = (unsigned)((HW + kBlock / 4 - 1) / (kBlock / 4));
-      hipLaunchKernelGGL(k_build<4>, dim3(bx, B * NT), dim3(kBlock), 0, stream, g);
-    } else {
-      const unsigned bx = (unsigned)((HW + kBlock / 8 - 1) / (kBlock / 8));
-      hipLaunchKernelGGL(k_build<8>, dim3(bx, B * NT), dim3(kBlock), 0, stream, g);
-    }
+    // x-blocks per (asset, target), from the launch size above
+    const int tok = a <= 4 ? kBlock / 4 : kBlock / 8;
+    const int64_t chunks = ((int64_t)HW + tok - 1) / tok;
+    const int64_t per_cu = stats ? kBuildBlocksPerCUStats : kBuildBlocksPerCU;
+    int64_t bx = (per_cu * 256 + (int64_t)B * NT - 1) / ((int64_t)B * NT);
+    if (bx > chunks) bx = chunks;
+    if (bx < 1) bx = 1;
+    if (a <= 4)
+      hipLaunchKernelGGL(k_build<4>, dim3((unsigned)bx, B * NT), dim3(kBlock), 0, stream, g);
+    else
+      hipLaunchKernelGGL(k_build<8>, dim3((unsigned)bx, B * NT), dim3(kBlock), 0, stream, g);
   }
   return after_launch(stream, "gc_build_correspondence");
 }
