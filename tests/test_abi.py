@@ -258,3 +258,25 @@ def test_geom_validation(gc, L):
     assert fused(mo=A5 + 12 * n) == -1            # model_out without a prediction output
     assert fused(xn=A5 + 64) == -5                # x_next overlaps x0_out
     assert fused(xt=A5 + 64) == -5                # x_t overlaps x0_out
+
+
+def test_error_message_is_per_thread(gc, L):
+    """gc_last_error() reports the calling thread's last failure, also while
+    another thread fails differently at the same time."""
+    import threading
+    bad = {}
+    barrier = threading.Barrier(2)
+    anchors = (ctypes.c_int32 * 2)(0, 3)
+
+    def worker(name, K, dt, rc_want, text):
+        barrier.wait()
+        for _ in range(500):
+            rc = L.gc_transport_step(A0, A1, A2, A3, None, None, 0, 1, 6, 8, 8, 16, anchors, 2, K, dt, A4, None)
+            msg = L.gc_last_error().decode()
+            if rc != rc_want or text not in msg:
+                bad[name] = (rc, msg)
+
+    t1 = threading.Thread(target=worker, args=("K", 5, 1, -1, "K=5"))
+    t2 = threading.Thread(target=worker, args=("dtype", 4, 7, -3, "dtype"))
+    t1.start(); t2.start(); t1.join(); t2.join()
+    assert not bad, bad
