@@ -361,8 +361,9 @@ def coverage_rows(gc, w, pos, cams, bbox, full, R=2):
     """One whole trajectory of the schedule alone (no latents) per anchor
     policy: per-step staleness of the foreground tokens after the step
     (mean, fraction stale for >= R steps, max) and the policy's cost per
-    cached step (selection or scoring + the staleness update + the host
-    read-backs it needs)."""
+    cached step: wall time of the selection or scoring, the staleness update
+    and the host read-backs it needs (the anchors, the counters), and the
+    device time from the first launch to the update's end (HIP events)."""
     import numpy as np
     import torch
     N, a = w.N, w.a
@@ -380,23 +381,28 @@ def coverage_rows(gc, w, pos, cams, bbox, full, R=2):
     max_gap = -(-N // a)
     for policy in ("rotate", "rotation_coverage", "coverage"):
         stale = gc.gc_coverage_init(pos)
-        gap, c, rec, cost = [0] * N, 0, [], []
+        gap, c, rec, cost, dev_ms = [0] * N, 0, [], [], []
         for k in range(w.S):
             torch.cuda.synchronize()
             t0 = time.perf_counter()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
             if full[k] or k == 0:
                 A = list(range(N))
             elif policy == "rotate":
                 A = gc.gc_schedule_anchors(N, a, c)
             elif policy == "rotation_coverage":
-                sc = gc.gc_coverage_score(pairs, stale, rot_sets).cpu().tolist()
+                sc = gc.gc_coverage_score(pairs, stale, rot_sets, workspace=ws).cpu().tolist()
                 A = rot_sets[sc.index(max(sc))]
             else:
                 due = sorted([v for v in range(N) if gap[v] >= max_gap], key=lambda v: (-gap[v], v))[:a]
                 A = gc.gc_coverage_select(pairs, stale, a, forced=due, workspace=ws).cpu().tolist()
-            st = gc.gc_coverage_update(pairs, stale, A, R).cpu().numpy().astype(np.int64)
+            st = gc.gc_coverage_update(pairs, stale, A, R)
+            e1.record()
+            st = st.cpu().numpy().astype(np.int64)
             if not (full[k] or k == 0):
                 cost.append(time.perf_counter() - t0)
+                dev_ms.append(e0.elapsed_time(e1))
                 c += 1
             gap = [0 if (full[k] or v in A) else g + 1 for v, g in enumerate(gap)]
             fg = st[..., 0].sum()
@@ -404,7 +410,8 @@ def coverage_rows(gc, w, pos, cams, bbox, full, R=2):
         r = np.array(rec, np.float64)
         out[policy] = {"mean_staleness": round(float(r[:, 0].mean()), 5),
                        "frac_stale_ge_R": round(float(r[:, 1].mean()), 5), "max_staleness": int(r[:, 2].max()),
-                       "ms_per_cached_step": round(float(np.median(cost)) * 1e3, 4)}
+                       "ms_per_cached_step": round(float(np.median(cost)) * 1e3, 4),
+                       "device_ms_per_cached_step": round(float(np.median(dev_ms)), 4)}
     return out
 
 

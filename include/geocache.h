@@ -401,7 +401,9 @@ int gc_transport_reconstruct_geom(const void* x0_prev, const void* x0_anchor_new
  *
  * gc_coverage_pair_words: uint32 words of the pair bits, N * B * N * ceil(H*W/32);
  *   layout [u][b][v][ceil(H*W/32)], token p at bit p % 32 of word p / 32, the
- *   bits of view u in row (u, b, u) zero.
+ *   bits of view u in row (u, b, u) zero.  The update, selection and scoring
+ *   calls read neither the padding bits past H*W nor the rows (u, b, u) (a
+ *   view covers its own tokens), so other producers may leave them unset.
  * gc_coverage_pairs: pos [B][N][H][W][3], cams device gc_camera [B][N], bbox
  *   device [B][8] (gc_posmap_bbox) -> pair_bits (once per asset batch).
  * gc_coverage_init: staleness 0 for foreground tokens, 255 for background.
@@ -412,12 +414,14 @@ int gc_transport_reconstruct_geom(const void* x0_prev, const void* x0_anchor_new
  * gc_coverage_select: the anchor set of the next cached step, written to
  *   anchors_out (device int32 [a], ascending); forced: host [n_forced] views
  *   that must be in it.  a <= GC_MAX_ANCHORS.  workspace: caller-owned device
- *   memory of gc_coverage_workspace_bytes(), 16-byte aligned; it holds the
- *   running gains, so concurrent calls need separate workspaces.  Enqueues
- *   2 (a - n_forced) + 2 small launches and never synchronises.
+ *   memory of gc_coverage_workspace_bytes(), 16-byte aligned; it holds
+ *   per-block partial gains and the chosen set, so concurrent calls need
+ *   separate workspaces.  Enqueues 2 (a - n_forced) + 2 launches and never
+ *   synchronises.
  * gc_coverage_score: scores (device uint64 [M], overwritten) = the weighted
  *   coverage, sum of 1 + staleness over the foreground tokens it covers, of
- *   each candidate set sets (host int32 [M][a]); M <= 64.  Choosing the
+ *   each candidate set sets (host int32 [M][a]); M <= 64.  workspace as for
+ *   gc_coverage_select (per-block partial sums; no atomics).  Choosing the
  *   rotation's set with the largest score keeps the rotation's evenly spread
  *   anchors while following where the stale tokens are.
  * gc_schedule_refresh_due: host; stats as written by gc_coverage_update and
@@ -434,7 +438,7 @@ int gc_coverage_select(const uint32_t* pair_bits, const uint8_t* stale, int B, i
                        const int32_t* forced, int n_forced, int32_t* anchors_out, void* workspace, size_t ws_bytes,
                        hipStream_t stream);
 int gc_coverage_score(const uint32_t* pair_bits, const uint8_t* stale, int B, int N, int H, int W, const int32_t* sets,
-                      int M, int a, uint64_t* scores, hipStream_t stream);
+                      int M, int a, uint64_t* scores, void* workspace, size_t ws_bytes, hipStream_t stream);
 int gc_schedule_refresh_due(const uint32_t* stats, int B, int N, double tau, int* due);
 
 /*

@@ -117,7 +117,7 @@ def lib() -> ctypes.CDLL:
             "gc_coverage_workspace_bytes": ([], ctypes.c_size_t),
             "gc_coverage_select": ([_vp, _vp, _i, _i, _i, _i, _i, _i32p, _i, _vp, _vp, ctypes.c_size_t, _vp], _i),
             "gc_schedule_refresh_due": ([_vp, _i, _i, ctypes.c_double, ctypes.POINTER(ctypes.c_int)], _i),
-            "gc_coverage_score": ([_vp, _vp, _i, _i, _i, _i, _i32p, _i, _i, _vp, _vp], _i),
+            "gc_coverage_score": ([_vp, _vp, _i, _i, _i, _i, _i32p, _i, _i, _vp, _vp, ctypes.c_size_t, _vp], _i),
             "gc_schedule_anchors": ([_i, _i, _i64, _i32p], _i),
             "gc_schedule_full_steps": ([_i, _i, _i, ctypes.POINTER(ctypes.c_uint8)], _i),
             "gc_sampler_step_times": ([ctypes.POINTER(_Sampler), _i, _i, ctypes.POINTER(ctypes.c_double),
@@ -624,7 +624,7 @@ def gc_coverage_select(pair_bits: torch.Tensor, stale: torch.Tensor, a: int, for
 
 
 def gc_coverage_score(pair_bits: torch.Tensor, stale: torch.Tensor, sets: Sequence[Sequence[int]],
-                      out: torch.Tensor = None, stream=None) -> torch.Tensor:
+                      out: torch.Tensor = None, workspace: torch.Tensor = None, stream=None) -> torch.Tensor:
     """Weighted coverage of each candidate set: device int64 [M] (uint64 values)."""
     B, N, H, W = stale.shape
     M, a = len(sets), len(sets[0])
@@ -633,8 +633,12 @@ def gc_coverage_score(pair_bits: torch.Tensor, stale: torch.Tensor, sets: Sequen
     flat = (ctypes.c_int32 * (M * a))(*[int(u) for S in sets for u in S])
     if out is None:
         out = torch.empty(M, dtype=torch.int64, device=stale.device)
+    if workspace is None:
+        workspace = torch.empty(gc_coverage_workspace_bytes(), dtype=torch.uint8, device=stale.device)
     _check(lib().gc_coverage_score(_dev(pair_bits, "pair_bits"), _dev(stale, "stale"), B, N, H, W, flat, M, a,
-                                   _dev(out, "scores"), _stream(stream)), "gc_coverage_score")
+                                   _dev(out, "scores"), _dev(workspace, "workspace"),
+                                   workspace.numel() * workspace.element_size(), _stream(stream)),
+           "gc_coverage_score")
     return out
 
 

@@ -30,7 +30,6 @@ namespace {
 
 constexpr int kBlock = 256;
 constexpr uint8_t kBackground = 255;
-constexpr uint8_t kStaleMax = 254;
 
 __device__ __forceinline__ uint32_t wave_add(uint32_t v) {
   for (int o = 32; o > 0; o >>= 1) v += (uint32_t)__shfl_xor((int)v, o);
@@ -40,10 +39,6 @@ __device__ __forceinline__ uint32_t wave_add(uint32_t v) {
 __device__ __forceinline__ uint32_t wave_max(uint32_t v) {
   for (int o = 32; o > 0; o >>= 1) v = max(v, (uint32_t)__shfl_xor((int)v, o));
   return v;
-}
-
-__device__ __forceinline__ bool pair_bit(const uint32_t* bits, int B, int N, int wpr, int u, int b, int v, int p) {
-  return (bits[(((int64_t)u * B + b) * N + v) * wpr + (p >> 5)] >> (p & 31)) & 1u;
 }
 
 // grid: x = token chunks of kBlock, y = (u * B + b) * N + v.  A wave's
@@ -86,106 +81,239 @@ __global__ void k_fill_u32(uint32_t* __restrict__ p, int n, uint32_t v) {
   if (i < n) p[i] = v;
 }
 
-// grid: x = token chunks, y = b * N + v.  stats[b][v] = foreground tokens,
-// tokens with staleness >= R, sum, max (after the update).
-__global__ __launch_bounds__(kBlock) void k_cov_update(const uint32_t* __restrict__ bits, int B, int N, int HW,
-                                                       int wpr, uint64_t anchor_mask, int R, uint8_t* __restrict__ stale,
-                                                       uint32_t* __restrict__ stats) {
-  const int bv = blockIdx.y;
-  const int b = bv / N, v = bv % N;
-  const int p = blockIdx.x * kBlock + (int)threadIdx.x;
-  bool fg = false;
-  uint32_t s = 0;
-  if (p < HW) {
-    uint8_t* sp = stale + (int64_t)bv * HW + p;
-    s = *sp;
-    fg = s != kBackground;
-    if (fg) {
-      bool fresh = (anchor_mask >> v) & 1ull;
-      for (uint64_t m = anchor_mask; m && !fresh; m &= m - 1) fresh = pair_bit(bits, B, N, wpr, __ffsll((long long)m) - 1, b, v, p);
-      s = fresh ? 0u : (s < kStaleMax ? s + 1u : (uint32_t)kStaleMax);
-      *sp = (uint8_t)s;
+// The token kernels give each lane one pair word: 32 consecutive tokens of
+// a row, the staleness bytes of those tokens (two 16-byte loads, or bytewise
+// when the rows are not 16-byte aligned) and, per view, one coalesced uint32
+// of the pair bits.  A 64-lane wave covers 2048 tokens of one (asset, view)
+// row: an item.  Per-item sums go through one wave sum each.
+
+__device__ __forceinline__ uint32_t pair_word(const uint32_t* __restrict__ bits, int B, int N, int wpr, int u, int b,
+                                              int v, int wi) {
+  return bits[(((int64_t)u * B + b) * N + v) * wpr + wi];
+}
+
+// Tokens of word wi of view v that the views in mask cover: all of them when
+// v is in the set, else those some view of the set sees.
+__device__ __forceinline__ uint32_t set_covers(const uint32_t* __restrict__ bits, int B, int N, int wpr,
+                                               unsigned long long mask, int b, int v, int wi) {
+  if ((mask >> v) & 1ull) return ~0u;
+  uint32_t acc = 0u;
+  for (; mask; mask &= mask - 1) acc |= pair_word(bits, B, N, wpr, __ffsll((long long)mask) - 1, b, v, wi);
+  return acc;
+}
+
+// Bits of word wi that are tokens of the row (the last word may be partial).
+__device__ __forceinline__ uint32_t valid_bits(int HW, int wi) {
+  const int n = HW - wi * 32;
+  return n >= 32 ? ~0u : (n <= 0 ? 0u : (1u << n) - 1u);
+}
+
+// Staleness bytes of tokens t0 .. t0 + 31 of a row, four per register (token
+// t0 + 4k + j in byte j of d[k]); tokens past the row read as background.
+// VEC: the row starts 16-byte aligned and holds a multiple of 16 tokens.
+template <bool VEC>
+__device__ __forceinline__ void load_word_bytes(const uint8_t* __restrict__ row, int HW, int t0, uint32_t (&d)[8]) {
+  if constexpr (VEC) {
+    const uint4 bg = make_uint4(~0u, ~0u, ~0u, ~0u);
+    const uint4 lo = t0 < HW ? *reinterpret_cast<const uint4*>(row + t0) : bg;
+    const uint4 hi = t0 + 16 < HW ? *reinterpret_cast<const uint4*>(row + t0 + 16) : bg;
+    d[0] = lo.x; d[1] = lo.y; d[2] = lo.z; d[3] = lo.w;
+    d[4] = hi.x; d[5] = hi.y; d[6] = hi.z; d[7] = hi.w;
+  } else {
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      uint32_t x = 0u;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int t = t0 + 4 * k + j;
+        x |= (t < HW ? (uint32_t)row[t] : 0xffu) << (8 * j);
+      }
+      d[k] = x;
     }
   }
-  if (!fg) s = 0;
-  __shared__ uint32_t part[kBlock / 64][4];
-  const uint32_t c_fg = (uint32_t)__popcll(__ballot(fg));
-  const uint32_t c_ge = (uint32_t)__popcll(__ballot(fg && s >= (uint32_t)R));
-  const uint32_t c_sum = wave_add(s);
-  const uint32_t c_max = wave_max(s);
-  const int wv = threadIdx.x / 64;
-  if (__lane_id() == 0) {
-    part[wv][0] = c_fg;
-    part[wv][1] = c_ge;
-    part[wv][2] = c_sum;
-    part[wv][3] = c_max;
+}
+
+template <bool VEC>
+__device__ __forceinline__ void store_word_bytes(uint8_t* __restrict__ row, int HW, int t0, const uint32_t (&d)[8]) {
+  if constexpr (VEC) {
+    if (t0 < HW) *reinterpret_cast<uint4*>(row + t0) = make_uint4(d[0], d[1], d[2], d[3]);
+    if (t0 + 16 < HW) *reinterpret_cast<uint4*>(row + t0 + 16) = make_uint4(d[4], d[5], d[6], d[7]);
+  } else {
+#pragma unroll
+    for (int k = 0; k < 8; ++k)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int t = t0 + 4 * k + j;
+        if (t < HW) row[t] = (uint8_t)(d[k] >> (8 * j));
+      }
   }
-  __syncthreads();
-  if (threadIdx.x < 4) {
-    uint32_t acc = 0;
-    for (int i = 0; i < kBlock / 64; ++i) acc = threadIdx.x == 3 ? max(acc, part[i][3]) : acc + part[i][threadIdx.x];
-    uint32_t* o = stats + (int64_t)bv * 4 + threadIdx.x;
-    if (threadIdx.x == 3)
+}
+
+// Bytewise (x + 1) mod 256: the token weight 1 + staleness, 0 for background.
+__device__ __forceinline__ uint32_t bytes_plus_one(uint32_t x) {
+  return ((x & 0x7f7f7f7fu) + 0x01010101u) ^ (x & 0x80808080u);
+}
+
+// 0x80 in each byte of x that is not zero, 0 elsewhere.
+__device__ __forceinline__ uint32_t bytes_nonzero(uint32_t x) {
+  return (((x & 0x7f7f7f7fu) + 0x7f7f7f7fu) | x) & 0x80808080u;
+}
+
+// Bits 4k .. 4k + 3 of sel as bytes 0 / 1 (nibble bit j moves to bit 8 j:
+// the product's partial terms land on distinct bits, so nothing carries).
+__device__ __forceinline__ uint32_t nibble_bytes(uint32_t sel, int k) {
+  return (((sel >> (4 * k)) & 0xfu) * 0x00204081u) & 0x01010101u;
+}
+
+// Sum of the weight bytes w of the tokens whose bit is set in sel.
+__device__ __forceinline__ uint32_t weighted_count(const uint32_t (&w)[8], uint32_t sel) {
+  uint32_t acc = 0u;
+#pragma unroll
+  for (int k = 0; k < 8; ++k) acc = __builtin_amdgcn_udot4(w[k], nibble_bytes(sel, k), acc, false);
+  return acc;
+}
+
+// grid: x = one-wave blocks striding over the items of one (asset, view), y
+// = b * N + v.  stats[b][v] = foreground tokens, tokens with staleness >= R,
+// sum, max (after the update); each block adds its totals once.
+template <bool VEC>
+__global__ __launch_bounds__(64) void k_cov_update(const uint32_t* __restrict__ bits, int B, int N, int HW, int wpr,
+                                                   unsigned long long anchor_mask, int R, uint8_t* __restrict__ stale,
+                                                   uint32_t* __restrict__ stats) {
+  const int bv = blockIdx.y;
+  const int b = bv / N, v = bv % N;
+  const int lane = (int)threadIdx.x;
+  uint8_t* row = stale + (int64_t)bv * HW;
+  uint32_t c_fg = 0, c_ge = 0, c_sum = 0, c_max = 0;   // this lane's totals
+  for (int wi = blockIdx.x * 64 + lane; wi - lane < wpr; wi += gridDim.x * 64) {
+    if (wi >= wpr) continue;
+    const uint32_t fresh = set_covers(bits, B, N, wpr, anchor_mask, b, v, wi) & valid_bits(HW, wi);
+    uint32_t d[8];
+    load_word_bytes<VEC>(row, HW, wi * 32, d);
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const uint32_t s = d[k];
+      const uint32_t fg = bytes_nonzero(~s);                       // s != 255
+      const uint32_t inc = bytes_nonzero(~(s | 0x01010101u)) >> 7;   // s < 254
+      const uint32_t fgm = (fg >> 7) * 0xffu;
+      const uint32_t zero = nibble_bytes(fresh, k) * 0xffu & fgm;
+      const uint32_t n = (s + inc) & ~zero;
+      d[k] = n;
+      const uint32_t nf = n & fgm;                                   // background reads 0
+      c_fg += (uint32_t)__popc(fg);
+      c_sum = __builtin_amdgcn_udot4(nf, 0x01010101u, c_sum, false);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const uint32_t x = (nf >> (8 * j)) & 0xffu;
+        c_ge += x >= (uint32_t)R ? 1u : 0u;
+        c_max = max(c_max, x);
+      }
+    }
+    store_word_bytes<VEC>(row, HW, wi * 32, d);
+  }
+  c_fg = wave_add(c_fg);
+  c_ge = wave_add(c_ge);
+  c_sum = wave_add(c_sum);
+  c_max = wave_max(c_max);
+  if (lane < 4) {
+    const uint32_t acc = lane == 0 ? c_fg : lane == 1 ? c_ge : lane == 2 ? c_sum : c_max;
+    uint32_t* o = stats + (int64_t)bv * 4 + lane;
+    if (lane == 3)
       atomicMax(o, acc);
     else if (acc)
       atomicAdd(o, acc);
   }
 }
 
-// Selection state in the workspace.
+// Reductions over all tokens (selection gains, set scores) run on at most
+// kRedBlocks one-wave blocks that stride over the items; lane u of a block
+// keeps candidate u's total, written as one partial row of the workspace at
+// the end, and one small block adds the rows up.  No global atomics: the
+// per-candidate counters would otherwise take an atomic from every block.
+constexpr int kRedBlocks = 2048;
+constexpr int kMaxSets = 64;       // candidate sets per gc_coverage_score call
+
+// Workspace layout: per-block partial sums, candidate-major (the reducer's
+// loads are coalesced), then the selection state.
 struct SelState {
-  unsigned long long gains[GC_MAX_VIEWS];
-  unsigned long long chosen;   // bit u: view u chosen
+  unsigned long long part[GC_MAX_VIEWS][kRedBlocks];   // part[u][block]: gains or scores
+  unsigned long long chosen;                           // bit u: view u chosen
 };
 
-__global__ void k_sel_begin(SelState* st, unsigned long long forced, int N) {
-  const int u = threadIdx.x;
-  if (u < N) st->gains[u] = 0ull;
-  if (u == 0) st->chosen = forced;
+int red_blocks(int64_t n_items) { return (int)(n_items < kRedBlocks ? n_items : kRedBlocks); }
+
+// 1024 threads: wave w sums candidate u = w, w + 16, ... over the first nblk
+// blocks' partials (coalesced, then a wave sum) into out[u] (LDS).
+__device__ __forceinline__ void sum_partials(const SelState* st, int n, int nblk, unsigned long long* out) {
+  const int wv = threadIdx.x / 64, lane = __lane_id();
+  for (int u = wv; u < n; u += 16) {
+    unsigned long long acc = 0ull;
+#pragma unroll 4
+    for (int i = lane; i < nblk; i += 64) acc += st->part[u][i];
+    for (int o = 32; o > 0; o >>= 1) acc += (unsigned long long)__shfl_xor((long long)acc, o);
+    if (lane == 0) out[u] = acc;
+  }
 }
 
-// grid: x = token chunks, y = b * N + v.  Gains of every unchosen view.
-__global__ __launch_bounds__(kBlock) void k_sel_gains(const uint32_t* __restrict__ bits,
-                                                      const uint8_t* __restrict__ stale, int B, int N, int HW, int wpr,
-                                                      SelState* st) {
-  __shared__ uint32_t g_lds[GC_MAX_VIEWS];
-  const int bv = blockIdx.y;
-  const int b = bv / N, v = bv % N;
-  const int p = blockIdx.x * kBlock + (int)threadIdx.x;
+__global__ void k_sel_begin(SelState* st, unsigned long long forced) {
+  if (threadIdx.x == 0) st->chosen = forced;
+}
+
+// Per token: weight 1 + staleness if no chosen view covers it (0 for
+// background), added to every unchosen candidate that covers it.  Items
+// whose view is chosen are covered throughout and add nothing.
+template <bool VEC>
+__global__ __launch_bounds__(64) void k_sel_gains(const uint32_t* __restrict__ bits, const uint8_t* __restrict__ stale,
+                                                  int B, int N, int HW, int wpr, SelState* st) {
   const unsigned long long chosen = st->chosen;
-  if ((int)threadIdx.x < N) g_lds[threadIdx.x] = 0u;
-  __syncthreads();
-  uint32_t w = 0;
-  if (p < HW) {
-    const uint8_t s = stale[(int64_t)bv * HW + p];
-    if (s != kBackground) {
-      bool covered = (chosen >> v) & 1ull;
-      for (unsigned long long m = chosen; m && !covered; m &= m - 1)
-        covered = pair_bit(bits, B, N, wpr, __ffsll((long long)m) - 1, b, v, p);
-      w = covered ? 0u : 1u + s;
+  const int lane = (int)threadIdx.x;
+  const int cpr = (wpr + 63) / 64;   // items per (asset, view)
+  const int64_t n_items = (int64_t)B * N * cpr;
+  unsigned long long mine = 0ull;    // lane u: candidate u's total
+  for (int64_t it = blockIdx.x; it < n_items; it += gridDim.x) {
+    const int bv = (int)(it / cpr);
+    const int b = bv / N, v = bv - b * N;
+    if ((chosen >> v) & 1ull) continue;   // uniform
+    const int wi = (int)(it - (int64_t)bv * cpr) * 64 + lane;
+    uint32_t w[8];
+    load_word_bytes<VEC>(stale + (int64_t)bv * HW, HW, wi * 32, w);
+#pragma unroll
+    for (int k = 0; k < 8; ++k) w[k] = bytes_plus_one(w[k]);
+    const bool in = wi < wpr;
+    const uint32_t live = in ? valid_bits(HW, wi) & ~set_covers(bits, B, N, wpr, chosen, b, v, wi) : 0u;
+    for (int u0 = 0; u0 < N; u0 += 8) {   // uniform; the group's words are loaded together
+      uint32_t wd[8];
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        const int u = u0 + q;
+        wd[q] = (u >= N || ((chosen >> u) & 1ull) || !in) ? 0u : (u == v ? ~0u : pair_word(bits, B, N, wpr, u, b, v, wi));
+      }
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        const int u = u0 + q;
+        if (u >= N) break;
+        const uint32_t g = wave_add(weighted_count(w, wd[q] & live));
+        if (lane == u) mine += g;
+      }
     }
   }
-  for (int u = 0; u < N; ++u) {   // uniform loop: every lane reaches the shuffles
-    if ((chosen >> u) & 1ull) continue;
-    const bool hit = w && (u == v || (p < HW && pair_bit(bits, B, N, wpr, u, b, v, p)));
-    const uint32_t sum = wave_add(hit ? w : 0u);
-    if (__lane_id() == 0 && sum) atomicAdd(&g_lds[u], sum);
-  }
-  __syncthreads();
-  if ((int)threadIdx.x < N && g_lds[threadIdx.x]) atomicAdd(&st->gains[threadIdx.x], (unsigned long long)g_lds[threadIdx.x]);
+  if (lane < N) st->part[lane][blockIdx.x] = mine;
 }
 
-// one thread: take the unchosen view with the largest gain (ties: lower
-// view), then clear the gains for the next round
-__global__ void k_sel_pick(SelState* st, int N) {
+// 1024 threads: each view's gain is the sum of the blocks' partials; then
+// the unchosen view with the largest gain (ties: lower view) is chosen.
+__global__ __launch_bounds__(1024) void k_sel_pick(SelState* st, int N, int nblk) {
+  __shared__ unsigned long long gain[GC_MAX_VIEWS];
+  sum_partials(st, N, nblk, gain);
+  __syncthreads();
   if (threadIdx.x != 0) return;
+  const unsigned long long chosen = st->chosen;
   int best = -1;
-  for (int u = 0; u < N; ++u) {
-    if ((st->chosen >> u) & 1ull) continue;
-    if (best < 0 || st->gains[u] > st->gains[best]) best = u;
+  for (int c = 0; c < N; ++c) {
+    if ((chosen >> c) & 1ull) continue;
+    if (best < 0 || gain[c] > gain[best]) best = c;
   }
-  if (best >= 0) st->chosen |= 1ull << best;
-  for (int u = 0; u < N; ++u) st->gains[u] = 0ull;
+  if (best >= 0) st->chosen = chosen | (1ull << best);
 }
 
 __global__ void k_sel_finish(const SelState* st, int N, int32_t* out) {
@@ -195,46 +323,49 @@ __global__ void k_sel_finish(const SelState* st, int N, int32_t* out) {
     if ((st->chosen >> u) & 1ull) out[j++] = u;
 }
 
-// Candidate sets as view masks (at most kMaxSets per call).
-constexpr int kMaxSets = 64;
+// Candidate sets as view masks.
 struct SetMasks {
   unsigned long long m[kMaxSets];
 };
 
-__global__ void k_fill_u64(unsigned long long* __restrict__ p, int n) {
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < n) p[i] = 0ull;
+// score[m] partials: 1 + staleness over the foreground tokens set m covers.
+template <bool VEC>
+__global__ __launch_bounds__(64) void k_cov_score(const uint32_t* __restrict__ bits, const uint8_t* __restrict__ stale,
+                                                  int B, int N, int HW, int wpr, SetMasks sets, int M, SelState* st) {
+  const int lane = (int)threadIdx.x;
+  const int cpr = (wpr + 63) / 64;
+  const int64_t n_items = (int64_t)B * N * cpr;
+  unsigned long long mine = 0ull;   // lane m: set m's total
+  for (int64_t it = blockIdx.x; it < n_items; it += gridDim.x) {
+    const int bv = (int)(it / cpr);
+    const int b = bv / N, v = bv - b * N;
+    const int wi = (int)(it - (int64_t)bv * cpr) * 64 + lane;
+    uint32_t w[8];
+    load_word_bytes<VEC>(stale + (int64_t)bv * HW, HW, wi * 32, w);
+#pragma unroll
+    for (int k = 0; k < 8; ++k) w[k] = bytes_plus_one(w[k]);
+    const bool in = wi < wpr;
+    const uint32_t vm = in ? valid_bits(HW, wi) : 0u;
+    for (int m = 0; m < M; ++m) {   // uniform
+      const uint32_t cov = in ? set_covers(bits, B, N, wpr, sets.m[m], b, v, wi) & vm : 0u;
+      const uint32_t g = wave_add(weighted_count(w, cov));
+      if (lane == m) mine += g;
+    }
+  }
+  if (lane < M) st->part[lane][blockIdx.x] = mine;
 }
 
-// grid: x = token chunks, y = b * N + v.  score[m] += 1 + staleness over the
-// foreground tokens set m covers.
-__global__ __launch_bounds__(kBlock) void k_cov_score(const uint32_t* __restrict__ bits,
-                                                      const uint8_t* __restrict__ stale, int B, int N, int HW, int wpr,
-                                                      SetMasks sets, int M, unsigned long long* __restrict__ score) {
-  __shared__ uint32_t s_lds[kMaxSets];
-  const int bv = blockIdx.y;
-  const int b = bv / N, v = bv % N;
-  const int p = blockIdx.x * kBlock + (int)threadIdx.x;
-  if ((int)threadIdx.x < M) s_lds[threadIdx.x] = 0u;
+__global__ __launch_bounds__(1024) void k_score_final(const SelState* st, int M, int nblk,
+                                                      unsigned long long* __restrict__ score) {
+  __shared__ unsigned long long sum[kMaxSets];
+  sum_partials(st, M, nblk, sum);
   __syncthreads();
-  uint32_t w = 0;
-  if (p < HW) {
-    const uint8_t s = stale[(int64_t)bv * HW + p];
-    w = s == kBackground ? 0u : 1u + s;
-  }
-  for (int m = 0; m < M; ++m) {   // uniform loop: every lane reaches the shuffles
-    bool covered = false;
-    if (w) {
-      covered = (sets.m[m] >> v) & 1ull;
-      for (unsigned long long q = sets.m[m]; q && !covered; q &= q - 1)
-        covered = pair_bit(bits, B, N, wpr, __ffsll((long long)q) - 1, b, v, p);
-    }
-    const uint32_t sum = wave_add(covered ? w : 0u);
-    if (__lane_id() == 0 && sum) atomicAdd(&s_lds[m], sum);
-  }
-  __syncthreads();
-  if ((int)threadIdx.x < M && s_lds[threadIdx.x]) atomicAdd(&score[threadIdx.x], (unsigned long long)s_lds[threadIdx.x]);
+  if ((int)threadIdx.x < M) score[threadIdx.x] = sum[threadIdx.x];
 }
+
+// The staleness rows start 16-byte aligned: the token kernels then move
+// each lane's 32 bytes with two 16-byte accesses.
+bool rows_aligned(const uint8_t* stale, size_t HW) { return ((uintptr_t)stale & 15u) == 0 && HW % 16 == 0; }
 
 int check_grid(int B, int N, int H, int W, const char* who) {
   if (B < 1 || N < 1 || H < 1 || W < 1) return fail(GC_ERR_SHAPE, "%s: bad shape B=%d N=%d H=%d W=%d", who, B, N, H, W);
@@ -307,9 +438,16 @@ extern "C" int gc_coverage_update(const uint32_t* pair_bits, int B, int N, int H
   if (!aligned16(pair_bits) || !aligned16(stats)) return fail(GC_ERR_ALIGN, "gc_coverage_update: pair_bits and stats must be 16-byte aligned");
   const int wpr = (int)((HW + 31) / 32);
   hipLaunchKernelGGL(k_fill_u32, dim3((unsigned)((B * N * 4 + 255) / 256)), dim3(256), 0, stream, stats, B * N * 4, 0u);
-  const dim3 grid((unsigned)((HW + kBlock - 1) / kBlock), (unsigned)(B * N));
-  hipLaunchKernelGGL(k_cov_update, grid, dim3(kBlock), 0, stream, pair_bits, B, N, (int)HW, wpr, (uint64_t)mask, R, stale,
-                     stats);
+  // one-wave blocks, at most one per 2048-token item and about kRedBlocks in
+  // all: each adds its totals to its view's counters once
+  const int64_t cpr = ((int64_t)wpr + 63) / 64;
+  int64_t bpr = (kRedBlocks + (int64_t)B * N - 1) / ((int64_t)B * N);
+  if (bpr > cpr) bpr = cpr;
+  const dim3 grid((unsigned)bpr, (unsigned)(B * N));
+  if (rows_aligned(stale, HW))
+    hipLaunchKernelGGL(k_cov_update<true>, grid, dim3(64), 0, stream, pair_bits, B, N, (int)HW, wpr, mask, R, stale, stats);
+  else
+    hipLaunchKernelGGL(k_cov_update<false>, grid, dim3(64), 0, stream, pair_bits, B, N, (int)HW, wpr, mask, R, stale, stats);
   return after_launch(stream, "gc_coverage_update");
 }
 
@@ -344,20 +482,25 @@ extern "C" int gc_coverage_select(const uint32_t* pair_bits, const uint8_t* stal
     return fail(GC_ERR_ALIAS, "gc_coverage_select: workspace / anchors_out overlap an input");
   SelState* st = static_cast<SelState*>(workspace);
   const int wpr = (int)((HW + 31) / 32);
-  hipLaunchKernelGGL(k_sel_begin, dim3(1), dim3(64), 0, stream, st, mask, N);
-  const dim3 grid((unsigned)((HW + kBlock - 1) / kBlock), (unsigned)(B * N));
+  const int nblk = red_blocks((int64_t)B * N * ((wpr + 63) / 64));
+  const bool vec = rows_aligned(stale, HW);
+  hipLaunchKernelGGL(k_sel_begin, dim3(1), dim3(64), 0, stream, st, mask);
   for (int r = n_forced; r < a; ++r) {
-    hipLaunchKernelGGL(k_sel_gains, grid, dim3(kBlock), 0, stream, pair_bits, stale, B, N, (int)HW, wpr, st);
-    hipLaunchKernelGGL(k_sel_pick, dim3(1), dim3(64), 0, stream, st, N);
+    if (vec)
+      hipLaunchKernelGGL(k_sel_gains<true>, dim3(nblk), dim3(64), 0, stream, pair_bits, stale, B, N, (int)HW, wpr, st);
+    else
+      hipLaunchKernelGGL(k_sel_gains<false>, dim3(nblk), dim3(64), 0, stream, pair_bits, stale, B, N, (int)HW, wpr, st);
+    hipLaunchKernelGGL(k_sel_pick, dim3(1), dim3(1024), 0, stream, st, N, nblk);
   }
   hipLaunchKernelGGL(k_sel_finish, dim3(1), dim3(64), 0, stream, st, N, anchors_out);
   return after_launch(stream, "gc_coverage_select");
 }
 
 extern "C" int gc_coverage_score(const uint32_t* pair_bits, const uint8_t* stale, int B, int N, int H, int W,
-                                 const int32_t* sets, int M, int a, uint64_t* scores, hipStream_t stream) {
+                                 const int32_t* sets, int M, int a, uint64_t* scores, void* workspace, size_t ws_bytes,
+                                 hipStream_t stream) {
   clear_error();
-  if (!pair_bits || !stale || !sets || !scores) return fail(GC_ERR_ARG, "gc_coverage_score: null pointer");
+  if (!pair_bits || !stale || !sets || !scores || !workspace) return fail(GC_ERR_ARG, "gc_coverage_score: null pointer");
   int rc = check_grid(B, N, H, W, "gc_coverage_score");
   if (rc) return rc;
   if (M < 1 || M > kMaxSets) return fail(GC_ERR_CAPACITY, "gc_coverage_score: M=%d outside [1, %d]", M, kMaxSets);
@@ -372,13 +515,25 @@ extern "C" int gc_coverage_score(const uint32_t* pair_bits, const uint8_t* stale
     }
   const size_t HW = (size_t)H * W;
   const size_t n_tok = (size_t)B * N * HW, nb = (size_t)gc_coverage_pair_words(B, N, H, W) * 4;
-  if (overlaps(scores, (size_t)M * 8, pair_bits, nb) || overlaps(scores, (size_t)M * 8, stale, n_tok))
-    return fail(GC_ERR_ALIAS, "gc_coverage_score: scores overlap an input");
-  if (!aligned16(pair_bits) || ((uintptr_t)scores & 7u)) return fail(GC_ERR_ALIGN, "gc_coverage_score: pair_bits 16-byte, scores 8-byte aligned");
+  if (ws_bytes < gc_coverage_workspace_bytes())
+    return fail(GC_ERR_CAPACITY, "gc_coverage_score: workspace of %zu bytes, %zu needed", ws_bytes, gc_coverage_workspace_bytes());
+  const size_t ws = gc_coverage_workspace_bytes();
+  if (overlaps(scores, (size_t)M * 8, pair_bits, nb) || overlaps(scores, (size_t)M * 8, stale, n_tok) ||
+      overlaps(workspace, ws, pair_bits, nb) || overlaps(workspace, ws, stale, n_tok) ||
+      overlaps(workspace, ws, scores, (size_t)M * 8))
+    return fail(GC_ERR_ALIAS, "gc_coverage_score: scores / workspace overlap an input or each other");
+  if (!aligned16(pair_bits) || !aligned16(workspace) || ((uintptr_t)scores & 7u))
+    return fail(GC_ERR_ALIGN, "gc_coverage_score: pair_bits and workspace 16-byte, scores 8-byte aligned");
   const int wpr = (int)((HW + 31) / 32);
-  hipLaunchKernelGGL(k_fill_u64, dim3(1), dim3(64), 0, stream, reinterpret_cast<unsigned long long*>(scores), M);
-  const dim3 grid((unsigned)((HW + kBlock - 1) / kBlock), (unsigned)(B * N));
-  hipLaunchKernelGGL(k_cov_score, grid, dim3(kBlock), 0, stream, pair_bits, stale, B, N, (int)HW, wpr, masks, M,
+  SelState* st = static_cast<SelState*>(workspace);
+  const int nblk = red_blocks((int64_t)B * N * ((wpr + 63) / 64));
+  if (rows_aligned(stale, HW))
+    hipLaunchKernelGGL(k_cov_score<true>, dim3(nblk), dim3(64), 0, stream, pair_bits, stale, B, N, (int)HW, wpr, masks,
+                       M, st);
+  else
+    hipLaunchKernelGGL(k_cov_score<false>, dim3(nblk), dim3(64), 0, stream, pair_bits, stale, B, N, (int)HW, wpr, masks,
+                       M, st);
+  hipLaunchKernelGGL(k_score_final, dim3(1), dim3(1024), 0, stream, st, M, nblk,
                      reinterpret_cast<unsigned long long*>(scores));
   return after_launch(stream, "gc_coverage_score");
 }

@@ -19,6 +19,7 @@ import torch
 
 from . import (GC_FULL_HEAD_MID_TAIL, GC_FULL_HEAD_TAIL_E, GC_FULL_PERIODIC, Sampler, VisibleIndex, gc_build_correspondence,
                gc_coverage_init, gc_coverage_pairs, gc_coverage_score, gc_coverage_select, gc_coverage_update,
+               gc_coverage_workspace_bytes,
                gc_index_correspondence, gc_posmap_bbox, gc_sampler_reconstruct, gc_sampler_step_times,
                gc_schedule_anchors, gc_schedule_full_steps, gc_schedule_refresh_due, gc_transport_reconstruct,
                gc_transport_reconstruct_geom, gc_transport_unipc, gc_unipc_coeffs, gc_unipc_update)
@@ -69,6 +70,8 @@ class GeoCacheRunner:
             if A not in self.rotation_sets:
                 self.rotation_sets.append(A)
         self.pairs = gc_coverage_pairs(pos, cams, self.bbox, stream=stream) if self.tracking else None
+        self._ws = (torch.empty(gc_coverage_workspace_bytes(), dtype=torch.uint8, device=pos.device)
+                    if self.tracking else None)
         self.stale: Optional[torch.Tensor] = None
         self.stats_host = None                        # per-view staleness statistics after the last step
         self.gap: List[int] = [0] * self.N            # cached steps since each view was last an anchor
@@ -120,11 +123,12 @@ class GeoCacheRunner:
         if self.anchor_policy == "rotate":
             return gc_schedule_anchors(self.N, self.a, c)
         if self.anchor_policy == "rotation_coverage":
-            sc = gc_coverage_score(self.pairs, self.stale, self.rotation_sets, stream=self.stream).cpu().tolist()
+            sc = gc_coverage_score(self.pairs, self.stale, self.rotation_sets, workspace=self._ws,
+                                   stream=self.stream).cpu().tolist()
             return list(self.rotation_sets[sc.index(max(sc))])
         due = [v for v in range(self.N) if self.max_gap and self.gap[v] >= self.max_gap]
         due = sorted(due, key=lambda v: (-self.gap[v], v))[:self.a]
-        sel = gc_coverage_select(self.pairs, self.stale, self.a, forced=due, stream=self.stream)
+        sel = gc_coverage_select(self.pairs, self.stale, self.a, forced=due, workspace=self._ws, stream=self.stream)
         return [int(v) for v in sel.cpu().tolist()]
 
     def _after(self, views: List[int], full: bool) -> None:
