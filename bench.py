@@ -362,8 +362,10 @@ def coverage_rows(gc, w, pos, cams, bbox, full, R=2):
     policy: per-step staleness of the foreground tokens after the step
     (mean, fraction stale for >= R steps, max) and the policy's cost per
     cached step: wall time of the selection or scoring, the staleness update
-    and the host read-backs it needs (the anchors, the counters), and the
-    device time from the first launch to the update's end (HIP events)."""
+    and the host read-backs it needs (the anchors, the counters), and device
+    time (HIP events around the selection's launches and around the update's,
+    summed: the kernels and the gaps between back-to-back launches, not the
+    read-backs)."""
     import numpy as np
     import torch
     N, a = w.N, w.a
@@ -385,24 +387,31 @@ def coverage_rows(gc, w, pos, cams, bbox, full, R=2):
         for k in range(w.S):
             torch.cuda.synchronize()
             t0 = time.perf_counter()
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0, e1, e2, e3 = (torch.cuda.Event(enable_timing=True) for _ in range(4))
             e0.record()
             if full[k] or k == 0:
                 A = list(range(N))
             elif policy == "rotate":
                 A = gc.gc_schedule_anchors(N, a, c)
             elif policy == "rotation_coverage":
-                sc = gc.gc_coverage_score(pairs, stale, rot_sets, workspace=ws).cpu().tolist()
+                sc = gc.gc_coverage_score(pairs, stale, rot_sets, workspace=ws)
+                e1.record()
+                sc = sc.cpu().tolist()
                 A = rot_sets[sc.index(max(sc))]
             else:
                 due = sorted([v for v in range(N) if gap[v] >= max_gap], key=lambda v: (-gap[v], v))[:a]
-                A = gc.gc_coverage_select(pairs, stale, a, forced=due, workspace=ws).cpu().tolist()
+                A = gc.gc_coverage_select(pairs, stale, a, forced=due, workspace=ws)
+                e1.record()
+                A = A.cpu().tolist()
+            if full[k] or k == 0 or policy == "rotate":
+                e1.record()   # no selection launches
+            e2.record()
             st = gc.gc_coverage_update(pairs, stale, A, R)
-            e1.record()
+            e3.record()
             st = st.cpu().numpy().astype(np.int64)
             if not (full[k] or k == 0):
                 cost.append(time.perf_counter() - t0)
-                dev_ms.append(e0.elapsed_time(e1))
+                dev_ms.append(e0.elapsed_time(e1) + e2.elapsed_time(e3))
                 c += 1
             gap = [0 if (full[k] or v in A) else g + 1 for v, g in enumerate(gap)]
             fg = st[..., 0].sum()

@@ -416,8 +416,8 @@ int gc_transport_reconstruct_geom(const void* x0_prev, const void* x0_anchor_new
  *   that must be in it.  a <= GC_MAX_ANCHORS.  workspace: caller-owned device
  *   memory of gc_coverage_workspace_bytes(), 16-byte aligned; it holds
  *   per-block partial gains and the chosen set, so concurrent calls need
- *   separate workspaces.  Enqueues 2 (a - n_forced) + 2 launches and never
- *   synchronises.
+ *   separate workspaces.  Enqueues 2 (a - n_forced) launches (one when every
+ *   view is forced) and never synchronises.
  * gc_coverage_score: scores (device uint64 [M], overwritten) = the weighted
  *   coverage, sum of 1 + staleness over the foreground tokens it covers, of
  *   each candidate set sets (host int32 [M][a]); M <= 64.  workspace as for

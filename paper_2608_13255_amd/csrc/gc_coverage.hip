@@ -255,8 +255,10 @@ __device__ __forceinline__ void sum_partials(const SelState* st, int n, int nblk
   }
 }
 
-__global__ void k_sel_begin(SelState* st, unsigned long long forced) {
-  if (threadIdx.x == 0) st->chosen = forced;
+// The views chosen before this round: the forced ones in the first round,
+// else the set the previous round's pick left in the workspace.
+__device__ __forceinline__ unsigned long long chosen_so_far(const SelState* st, unsigned long long forced, int first) {
+  return first ? forced : st->chosen;
 }
 
 // Per token: weight 1 + staleness if no chosen view covers it (0 for
@@ -264,8 +266,9 @@ __global__ void k_sel_begin(SelState* st, unsigned long long forced) {
 // whose view is chosen are covered throughout and add nothing.
 template <bool VEC>
 __global__ __launch_bounds__(64) void k_sel_gains(const uint32_t* __restrict__ bits, const uint8_t* __restrict__ stale,
-                                                  int B, int N, int HW, int wpr, SelState* st) {
-  const unsigned long long chosen = st->chosen;
+                                                  int B, int N, int HW, int wpr, SelState* st,
+                                                  unsigned long long forced, int first) {
+  const unsigned long long chosen = chosen_so_far(st, forced, first);
   const int lane = (int)threadIdx.x;
   const int cpr = (wpr + 63) / 64;   // items per (asset, view)
   const int64_t n_items = (int64_t)B * N * cpr;
@@ -300,27 +303,36 @@ __global__ __launch_bounds__(64) void k_sel_gains(const uint32_t* __restrict__ b
   if (lane < N) st->part[lane][blockIdx.x] = mine;
 }
 
+// The views of mask in ascending order.
+__device__ __forceinline__ void write_set(unsigned long long mask, int N, int32_t* out) {
+  int j = 0;
+  for (int u = 0; u < N; ++u)
+    if ((mask >> u) & 1ull) out[j++] = u;
+}
+
 // 1024 threads: each view's gain is the sum of the blocks' partials; then
-// the unchosen view with the largest gain (ties: lower view) is chosen.
-__global__ __launch_bounds__(1024) void k_sel_pick(SelState* st, int N, int nblk) {
+// the unchosen view with the largest gain (ties: lower view) is chosen.  The
+// last round writes the set to out.
+__global__ __launch_bounds__(1024) void k_sel_pick(SelState* st, int N, int nblk, unsigned long long forced, int first,
+                                                   int32_t* out) {
   __shared__ unsigned long long gain[GC_MAX_VIEWS];
   sum_partials(st, N, nblk, gain);
   __syncthreads();
   if (threadIdx.x != 0) return;
-  const unsigned long long chosen = st->chosen;
+  unsigned long long chosen = chosen_so_far(st, forced, first);
   int best = -1;
   for (int c = 0; c < N; ++c) {
     if ((chosen >> c) & 1ull) continue;
     if (best < 0 || gain[c] > gain[best]) best = c;
   }
-  if (best >= 0) st->chosen = chosen | (1ull << best);
+  if (best >= 0) chosen |= 1ull << best;
+  st->chosen = chosen;
+  if (out) write_set(chosen, N, out);
 }
 
-__global__ void k_sel_finish(const SelState* st, int N, int32_t* out) {
-  if (threadIdx.x != 0) return;
-  int j = 0;
-  for (int u = 0; u < N; ++u)
-    if ((st->chosen >> u) & 1ull) out[j++] = u;
+// the forced views are the whole set: no round runs
+__global__ void k_sel_forced(unsigned long long forced, int N, int32_t* out) {
+  if (threadIdx.x == 0) write_set(forced, N, out);
 }
 
 // Candidate sets as view masks.
@@ -484,15 +496,18 @@ extern "C" int gc_coverage_select(const uint32_t* pair_bits, const uint8_t* stal
   const int wpr = (int)((HW + 31) / 32);
   const int nblk = red_blocks((int64_t)B * N * ((wpr + 63) / 64));
   const bool vec = rows_aligned(stale, HW);
-  hipLaunchKernelGGL(k_sel_begin, dim3(1), dim3(64), 0, stream, st, mask);
+  if (n_forced == a) hipLaunchKernelGGL(k_sel_forced, dim3(1), dim3(64), 0, stream, mask, N, anchors_out);
   for (int r = n_forced; r < a; ++r) {
+    const int first = r == n_forced;
+    int32_t* out = r == a - 1 ? anchors_out : nullptr;
     if (vec)
-      hipLaunchKernelGGL(k_sel_gains<true>, dim3(nblk), dim3(64), 0, stream, pair_bits, stale, B, N, (int)HW, wpr, st);
+      hipLaunchKernelGGL(k_sel_gains<true>, dim3(nblk), dim3(64), 0, stream, pair_bits, stale, B, N, (int)HW, wpr, st,
+                         mask, first);
     else
-      hipLaunchKernelGGL(k_sel_gains<false>, dim3(nblk), dim3(64), 0, stream, pair_bits, stale, B, N, (int)HW, wpr, st);
-    hipLaunchKernelGGL(k_sel_pick, dim3(1), dim3(1024), 0, stream, st, N, nblk);
+      hipLaunchKernelGGL(k_sel_gains<false>, dim3(nblk), dim3(64), 0, stream, pair_bits, stale, B, N, (int)HW, wpr, st,
+                         mask, first);
+    hipLaunchKernelGGL(k_sel_pick, dim3(1), dim3(1024), 0, stream, st, N, nblk, mask, first, out);
   }
-  hipLaunchKernelGGL(k_sel_finish, dim3(1), dim3(64), 0, stream, st, N, anchors_out);
   return after_launch(stream, "gc_coverage_select");
 }
 
