@@ -31,14 +31,32 @@ namespace {
 constexpr int kBlock = 256;
 constexpr uint8_t kBackground = 255;
 
+// Wave-wide sum and maximum, returned wave-uniform; every lane of the wave
+// must be active.  Within each row of 16 lanes, DPP moves pair lane i with i
+// xor 1, i xor 2, 7 - i (within 8) and 15 - i, so every lane ends with its
+// row's total; the four row totals are then read into scalar registers.
+constexpr int kDppXor1 = 0xb1;          // quad_perm [1, 0, 3, 2]
+constexpr int kDppXor2 = 0x4e;          // quad_perm [2, 3, 0, 1]
+constexpr int kDppHalfMirror = 0x141;   // row_half_mirror
+constexpr int kDppMirror = 0x140;       // row_mirror
+
 __device__ __forceinline__ uint32_t wave_add(uint32_t v) {
-  for (int o = 32; o > 0; o >>= 1) v += (uint32_t)__shfl_xor((int)v, o);
-  return v;
+  int x = (int)v;
+  x += __builtin_amdgcn_mov_dpp(x, kDppXor1, 0xf, 0xf, false);
+  x += __builtin_amdgcn_mov_dpp(x, kDppXor2, 0xf, 0xf, false);
+  x += __builtin_amdgcn_mov_dpp(x, kDppHalfMirror, 0xf, 0xf, false);
+  x += __builtin_amdgcn_mov_dpp(x, kDppMirror, 0xf, 0xf, false);
+  return (uint32_t)__builtin_amdgcn_readlane(x, 0) + (uint32_t)__builtin_amdgcn_readlane(x, 16) +
+         (uint32_t)__builtin_amdgcn_readlane(x, 32) + (uint32_t)__builtin_amdgcn_readlane(x, 48);
 }
 
 __device__ __forceinline__ uint32_t wave_max(uint32_t v) {
-  for (int o = 32; o > 0; o >>= 1) v = max(v, (uint32_t)__shfl_xor((int)v, o));
-  return v;
+  v = max(v, (uint32_t)__builtin_amdgcn_mov_dpp((int)v, kDppXor1, 0xf, 0xf, false));
+  v = max(v, (uint32_t)__builtin_amdgcn_mov_dpp((int)v, kDppXor2, 0xf, 0xf, false));
+  v = max(v, (uint32_t)__builtin_amdgcn_mov_dpp((int)v, kDppHalfMirror, 0xf, 0xf, false));
+  v = max(v, (uint32_t)__builtin_amdgcn_mov_dpp((int)v, kDppMirror, 0xf, 0xf, false));
+  return max(max((uint32_t)__builtin_amdgcn_readlane((int)v, 0), (uint32_t)__builtin_amdgcn_readlane((int)v, 16)),
+             max((uint32_t)__builtin_amdgcn_readlane((int)v, 32), (uint32_t)__builtin_amdgcn_readlane((int)v, 48)));
 }
 
 // grid: x = token chunks of kBlock, y = (u * B + b) * N + v.  A wave's
@@ -284,15 +302,15 @@ __global__ __launch_bounds__(64) void k_sel_gains(const uint32_t* __restrict__ b
     for (int k = 0; k < 8; ++k) w[k] = bytes_plus_one(w[k]);
     const bool in = wi < wpr;
     const uint32_t live = in ? valid_bits(HW, wi) & ~set_covers(bits, B, N, wpr, chosen, b, v, wi) : 0u;
-    for (int u0 = 0; u0 < N; u0 += 8) {   // uniform; the group's words are loaded together
-      uint32_t wd[8];
+    for (int u0 = 0; u0 < N; u0 += 16) {   // uniform; the group's words are loaded together
+      uint32_t wd[16];
 #pragma unroll
-      for (int q = 0; q < 8; ++q) {
+      for (int q = 0; q < 16; ++q) {
         const int u = u0 + q;
         wd[q] = (u >= N || ((chosen >> u) & 1ull) || !in) ? 0u : (u == v ? ~0u : pair_word(bits, B, N, wpr, u, b, v, wi));
       }
 #pragma unroll
-      for (int q = 0; q < 8; ++q) {
+      for (int q = 0; q < 16; ++q) {
         const int u = u0 + q;
         if (u >= N) break;
         const uint32_t g = wave_add(weighted_count(w, wd[q] & live));
