@@ -230,6 +230,20 @@ def main():
     bytes_per_launch = float(np.mean([algo_bytes(A) for A in used]))
     achieved = bytes_per_launch / (avg_kernel_ms * 1e-3) / 1e9
 
+    # ---- per-step distribution (outside the timed region) ---------------------
+    # each step between its own pair of events; the events' own cost widens
+    # the gaps a little, so the median sits slightly above the timed mean
+    n_dist = min(100, max(10, args.steps))
+    evs = [ev() for _ in range(n_dist + 1)]
+    torch.cuda.synchronize()
+    evs[0].record()
+    for i in range(n_dist):
+        step(args.warmup + args.steps + i)
+        evs[i + 1].record()
+    torch.cuda.synchronize()
+    per_step_us = np.array([evs[i].elapsed_time(evs[i + 1]) * 1e3 for i in range(n_dist)])
+    rows["step_us_p10_p50_p90"] = [round(float(np.percentile(per_step_us, q)), 2) for q in (10, 50, 90)]
+
     # ---- unfused pair and full step, for the record -------------------------
     def timed(fn, n=20):
         fn()
@@ -522,9 +536,19 @@ def cpu_baseline(w, pos1, cams_np, x0_prev1, seconds):
         if el >= seconds:
             break
     vp = reps * (w.N - w.a) * w.H * w.W
+    model = "unknown CPU"
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    visible = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else os.cpu_count()
     return {"value": vp / el, "unit": "view-pixels/s", "cores": 1, "kind": "oracle",
             "sample": f"{reps} cached steps of 1 of {w.B} assets ({w.N} views, {w.H}x{w.W}x{w.C} {w.dtype}, "
-                      f"a={w.a}, K={w.K}), transport + reconstruction, {el:.1f}s on one host thread"}
+                      f"a={w.a}, K={w.K}), transport + reconstruction, {el:.1f}s on one host thread",
+            "host": f"{model}; {visible} CPUs visible to the process"}
 
 
 if __name__ == "__main__":
