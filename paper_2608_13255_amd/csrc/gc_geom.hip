@@ -17,8 +17,14 @@
 // blends the channel vectors j, j + G, ...  Weights are the builder's
 // stored values (w_k / n_vis in float), so the result equals
 // gc_build_correspondence followed by gc_transport_step bit for bit.
-// Anchor rows copy the new prediction.  Blocks never straddle a view and
-// are dealt to XCDs in contiguous slices, as in the stored-operator kernel.
+//
+// Split launch: the target-view blocks, whose dependent loads (position,
+// the anchors' position taps, then the latent taps) set the pace, come
+// first; the anchor rows, which only copy the new prediction and stream the
+// sampler step, follow as dense blocks of one lane per channel vector and
+// fill the machine while the last target blocks finish.  Each part is dealt
+// to the XCDs in contiguous slices, so an XCD gathers from few assets'
+// anchor views, and blocks never straddle a view.
 #include "gc_common.h"
 #include "gc_geometry.h"
 #include "gc_latent.h"
@@ -40,10 +46,15 @@ struct GArgs {
   void* x0_out;
   void* x_next;
   void* model_out;
-  int N, H, W, HW, C, a, K, CV;
-  int bpv;        // blocks per view: ceil(HW / tokens per block)
-  int n_blocks;   // B * N * bpv
-  int32_t anchor_view[GC_MAX_ANCHORS];
+  int N, H, W, HW, C, a, K, CV, NT;
+  int cv_shift;     // log2(CV) when CV is a power of two, else -1
+  int bpv_t;        // target blocks per target view: ceil(HW / tokens per block)
+  int n_tblocks;    // B * NT * bpv_t
+  int tgrid;        // target part of the grid, padded to a multiple of kXcds
+  int bpv_a;        // anchor-row blocks per anchor view: ceil(HW * CV / kBlock)
+  int n_ablocks;    // B * a * bpv_a
+  int32_t anchor_view[GC_MAX_ANCHORS];     // view of anchor slot s
+  int32_t sorted_anchor[GC_MAX_ANCHORS];   // anchor views ascending, padded with INT_MAX
   Recon r;
 };
 
@@ -51,42 +62,53 @@ template <int DT, int VEC, int MODE, int G>
 __global__ __launch_bounds__(kBlock) void k_transport_geom(GArgs g) {
   using CD = Codec<DT, VEC>;
   using Raw = typename CD::Raw;
-  constexpr int kTok = kBlock / G;   // tokens per block
+  constexpr int kTok = kBlock / G;   // target tokens per block
   __shared__ gc_camera cam_lds[GC_MAX_ANCHORS];
-  const int lb = logical_block((int)blockIdx.x, g.n_blocks, 1);
-  if (lb >= g.n_blocks) return;   // XCD padding: whole block
-  const int bv = __builtin_amdgcn_readfirstlane(lb / g.bpv);   // b * N + v
-  const int b = __builtin_amdgcn_readfirstlane(bv / g.N);
-  const int v = bv - b * g.N;
-  int s_self = -1;
-#pragma unroll
-  for (int s = 0; s < GC_MAX_ANCHORS; ++s)
-    if (s < g.a && g.anchor_view[s] == v) s_self = s;
-  const int lane_g = (int)threadIdx.x & (G - 1);
-  const int p = (lb - bv * g.bpv) * kTok + (int)threadIdx.x / G;
-  const bool tok_ok = p < g.HW;
-  const int64_t tbase = ((int64_t)bv * g.HW + p) * g.C;   // this token's first element
-
-  if (s_self >= 0) {   // anchor row (block-uniform): the store takes the new prediction
-    if (!tok_ok) return;
-    const int64_t nbase = (((int64_t)b * g.a + s_self) * g.HW + p) * g.C;
-    for (int c = lane_g; c < g.CV; c += G) {
-      const int64_t e = tbase + (int64_t)c * VEC;
-      Raw xtr;
-      if constexpr (MODE == kGeomReconstruct) xtr = CD::load_stream(g.x_t, e);
-      const Raw x0r = CD::load(g.x0_new, nbase + (int64_t)c * VEC);
-      CD::store_stream(g.x0_out, e, x0r);
-      if constexpr (MODE == kGeomReconstruct) {
-        float xtf[VEC], x0f[VEC], xn[VEC], mo[VEC];
-        CD::unpack(xtr, xtf);
-        CD::unpack(x0r, x0f);
-        reconstruct_vec<VEC>(g.r, xtf, x0f, xn, mo);
-        CD::store_stream(g.x_next, e, CD::pack(xn));
-        if (g.model_out) CD::store_stream(g.model_out, e, CD::pack(mo));
-      }
+  if ((int)blockIdx.x >= g.tgrid) {
+    // anchor row: one lane per (token, channel vector); the store takes the
+    // new prediction
+    const int lb = logical_block((int)blockIdx.x - g.tgrid, g.n_ablocks, 1);
+    if (lb >= g.n_ablocks) return;
+    const int bs = __builtin_amdgcn_readfirstlane(lb / g.bpv_a);   // b * a + s
+    const int b = __builtin_amdgcn_readfirstlane(bs / g.a);
+    const int s = bs - b * g.a;
+    const int t = (lb - bs * g.bpv_a) * kBlock + (int)threadIdx.x;
+    if (t >= g.HW * g.CV) return;
+    int p, c;
+    if (g.cv_shift >= 0) {
+      p = t >> g.cv_shift;
+      c = t & (g.CV - 1);
+    } else {
+      p = t / g.CV;
+      c = t - p * g.CV;
+    }
+    const int64_t e = (((int64_t)b * g.N + g.anchor_view[s]) * g.HW + p) * g.C + (int64_t)c * VEC;
+    Raw xtr;
+    if constexpr (MODE == kGeomReconstruct) xtr = CD::load_stream(g.x_t, e);
+    const Raw x0r = CD::load(g.x0_new, ((int64_t)bs * g.HW + p) * g.C + (int64_t)c * VEC);
+    CD::store_stream(g.x0_out, e, x0r);
+    if constexpr (MODE == kGeomReconstruct) {
+      float xtf[VEC], x0f[VEC], xn[VEC], mo[VEC];
+      CD::unpack(xtr, xtf);
+      CD::unpack(x0r, x0f);
+      reconstruct_vec<VEC>(g.r, xtf, x0f, xn, mo);
+      CD::store_stream(g.x_next, e, CD::pack(xn));
+      if (g.model_out) CD::store_stream(g.model_out, e, CD::pack(mo));
     }
     return;
   }
+  const int lb = logical_block((int)blockIdx.x, g.n_tblocks, 1);
+  if (lb >= g.n_tblocks) return;   // XCD padding: whole block
+  const int bt = __builtin_amdgcn_readfirstlane(lb / g.bpv_t);   // b * NT + target slot
+  const int b = __builtin_amdgcn_readfirstlane(bt / g.NT);
+  int v = bt - b * g.NT;                                          // target slot -> view
+#pragma unroll
+  for (int s = 0; s < GC_MAX_ANCHORS; ++s) v += g.sorted_anchor[s] <= v ? 1 : 0;
+  const int bv = b * g.N + v;
+  const int lane_g = (int)threadIdx.x & (G - 1);
+  const int p = (lb - bt * g.bpv_t) * kTok + (int)threadIdx.x / G;
+  const bool tok_ok = p < g.HW;
+  const int64_t tbase = ((int64_t)bv * g.HW + p) * g.C;   // this token's first element
 
   // target token: lane s of the group evaluates anchor slot s
   if (threadIdx.x < g.a) cam_lds[threadIdx.x] = g.cams[(int64_t)b * g.N + g.anchor_view[threadIdx.x]];
@@ -220,18 +242,28 @@ int prepare_geom(const void* x0_prev, const void* x0_new, const float* pos, cons
   g->a = a;
   g->K = K;
   g->CV = C / pick_vec(dtype, C);
+  g->NT = N - a;
+  g->cv_shift = (g->CV & (g->CV - 1)) == 0 ? __builtin_ctz((unsigned)g->CV) : -1;
+  int n_sorted = 0;
+  for (int u = 0; u < N; ++u)
+    if (is_anchor[u]) g->sorted_anchor[n_sorted++] = u;
+  for (int s = n_sorted; s < GC_MAX_ANCHORS; ++s) g->sorted_anchor[s] = INT32_MAX;
   const int tok = a <= 4 ? kBlock / 4 : kBlock / 8;
-  g->bpv = (int)(((int64_t)HW + tok - 1) / tok);
-  const int64_t nb = (int64_t)B * N * g->bpv;
-  if (nb > (int64_t)0x7fffffff - kXcds) return fail(GC_ERR_CAPACITY, "%s: problem too large for one launch", who);
-  g->n_blocks = (int)nb;
+  g->bpv_t = (int)(((int64_t)HW + tok - 1) / tok);
+  g->bpv_a = (int)(((int64_t)HW * g->CV + kBlock - 1) / kBlock);
+  const int64_t nt = (int64_t)B * g->NT * g->bpv_t, na = (int64_t)B * a * g->bpv_a;
+  const int64_t tgrid = (nt + kXcds - 1) / kXcds * kXcds, agrid = (na + kXcds - 1) / kXcds * kXcds;
+  if (tgrid + agrid > (int64_t)0x7fffffff) return fail(GC_ERR_CAPACITY, "%s: problem too large for one launch", who);
+  g->n_tblocks = (int)nt;
+  g->tgrid = (int)tgrid;
+  g->n_ablocks = (int)na;
   return GC_OK;
 }
 
 template <int MODE>
 void launch_geom(const GArgs& g, int dtype, hipStream_t stream) {
-  const int per = (g.n_blocks + kXcds - 1) / kXcds;
-  const dim3 grid((unsigned)(per * kXcds));
+  const int agrid = (g.n_ablocks + kXcds - 1) / kXcds * kXcds;
+  const dim3 grid((unsigned)(g.tgrid + agrid));
   const int vec = g.C / g.CV;
 #define GC_LAUNCH_GEOM(DT_, VEC_)                                                                         \
   do {                                                                                                    \
