@@ -9,11 +9,13 @@
 // few repeating sets the stored operator and its visible-token index are
 // cheaper per step.
 //
-// Work mapping: a group of G = 4 (a <= 4) or 8 adjacent lanes serves one
-// token.  On a target token lane s evaluates anchor slot s exactly as the
-// builder does (same device function, same float order), n_vis is a ballot
-// over the group, and the group's lanes read every anchor's word and
-// weights from each other with cross-lane permutes; lane j then gathers and
+// Work mapping: a group of G adjacent lanes serves one target token, G the
+// number of channel vectors rounded up to a power of two (at most 8), so
+// that every lane of the group has latent work.  Lane j of the group
+// evaluates anchor slots j, j + G, ... exactly as the builder does (same
+// device function, same float order); n_vis is a ballot over the group, and
+// the group's lanes read every anchor's word and weights from each other
+// with cross-lane permutes, in ascending slot order; lane j then gathers and
 // blends the channel vectors j, j + G, ...  Weights are the builder's
 // stored values (w_k / n_vis in float), so the result equals
 // gc_build_correspondence followed by gc_transport_step bit for bit.
@@ -47,6 +49,7 @@ struct GArgs {
   void* x_next;
   void* model_out;
   int N, H, W, HW, C, a, K, CV, NT;
+  int G;            // lanes per target token (geom_group)
   int cv_shift;     // log2(CV) when CV is a power of two, else -1
   int bpv_t;        // target blocks per target view: ceil(HW / tokens per block)
   int n_tblocks;    // B * NT * bpv_t
@@ -58,11 +61,15 @@ struct GArgs {
   Recon r;
 };
 
-template <int DT, int VEC, int MODE, int G>
+// G lanes per target token; AMAX (4 or 8) bounds the anchor count, so each
+// lane evaluates up to AMAX / G anchor slots.
+template <int DT, int VEC, int MODE, int G, int AMAX>
 __global__ __launch_bounds__(kBlock) void k_transport_geom(GArgs g) {
   using CD = Codec<DT, VEC>;
   using Raw = typename CD::Raw;
   constexpr int kTok = kBlock / G;   // target tokens per block
+  constexpr int kApl = AMAX / G;     // anchor slots per lane
+  static_assert(kApl >= 1 && kApl * G == AMAX, "G must divide AMAX");
   __shared__ gc_camera cam_lds[GC_MAX_ANCHORS];
   if ((int)blockIdx.x >= g.tgrid) {
     // anchor row: one lane per (token, channel vector); the store takes the
@@ -110,7 +117,7 @@ __global__ __launch_bounds__(kBlock) void k_transport_geom(GArgs g) {
   const bool tok_ok = p < g.HW;
   const int64_t tbase = ((int64_t)bv * g.HW + p) * g.C;   // this token's first element
 
-  // target token: lane s of the group evaluates anchor slot s
+  // target token: lane j of the group evaluates anchor slots j, j + G, ...
   if (threadIdx.x < g.a) cam_lds[threadIdx.x] = g.cams[(int64_t)b * g.N + g.anchor_view[threadIdx.x]];
   __syncthreads();
   float P[3] = {0.f, 0.f, 0.f};
@@ -122,18 +129,23 @@ __global__ __launch_bounds__(kBlock) void k_transport_geom(GArgs g) {
     P[2] = pp[2];
     fg = finite_f(P[0]) && finite_f(P[1]) && finite_f(P[2]);
   }
-  AnchorTaps at;
-  at.word = 0;
-  at.mask = 0;
+  AnchorTaps at[kApl];
 #pragma unroll
-  for (int k = 0; k < 4; ++k) at.wk[k] = 0.0f;
-  if (tok_ok && fg && lane_g < g.a)
-    at = anchor_taps(P, cam_lds[lane_g], g.pos + ((int64_t)b * g.N + g.anchor_view[lane_g]) * g.HW * 3, g.H, g.W,
-                     g.K, g.bbox[(int64_t)b * 8 + 6]);
-  // every lane reaches the ballot and the permutes below (no early exit)
-  const unsigned long long seen = __ballot(at.word != 0);
+  for (int j = 0; j < kApl; ++j) {
+    at[j].word = 0;
+    at[j].mask = 0;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) at[j].wk[k] = 0.0f;
+    const int s = j * G + lane_g;
+    if (tok_ok && fg && s < g.a)
+      at[j] = anchor_taps(P, cam_lds[s], g.pos + ((int64_t)b * g.N + g.anchor_view[s]) * g.HW * 3, g.H, g.W, g.K,
+                          g.bbox[(int64_t)b * 8 + 6]);
+  }
+  // every lane reaches the ballots and the permutes below (no early exit)
   const int gbase = __lane_id() & ~(G - 1);
-  const int n_vis = __popcll((seen >> gbase) & ((1ull << G) - 1));
+  int n_vis = 0;
+#pragma unroll
+  for (int j = 0; j < kApl; ++j) n_vis += __popcll((__ballot(at[j].word != 0) >> gbase) & ((1ull << G) - 1));
   const float inv = n_vis > 0 ? (float)n_vis : 1.0f;
   const int rounds = (g.CV + G - 1) / G;
   for (int r = 0; r < rounds; ++r) {
@@ -148,27 +160,39 @@ __global__ __launch_bounds__(kBlock) void k_transport_geom(GArgs g) {
     float acc[VEC];
 #pragma unroll
     for (int q = 0; q < VEC; ++q) acc[q] = 0.0f;
-    for (int s = 0; s < g.a; ++s) {
-      const uint32_t w = (uint32_t)__shfl(at.word, gbase + s);
-      float wk[4];
 #pragma unroll
-      for (int k = 0; k < 4; ++k) wk[k] = __shfl(at.wk[k], gbase + s);
-      if (!act || !w) continue;
-      const int x0 = (int)(w & 0xfffu) - 1;
-      const int y0 = (int)((w >> 12) & 0xfffu) - 1;
-      const uint32_t mask = (w >> 24) & 0xfu;
-      const int64_t new_view = ((int64_t)b * g.a + s) * g.HW;
-      const int64_t old_view = ((int64_t)b * g.N + g.anchor_view[s]) * g.HW;
+    for (int j = 0; j < kApl; ++j) {
+      for (int q = 0; q < G; ++q) {   // anchor slot s = j G + q: ascending, as the stored operator sums
+        const int s = j * G + q;
+        if (s >= g.a) break;
+        uint32_t w;
+        float wk[4];
+        if constexpr (G == 1) {
+          w = (uint32_t)at[j].word;
 #pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        if (!(mask & (1u << k))) continue;
-        const int q = (y0 + (k >> 1)) * g.W + x0 + (k & 1);
-        const float wt = wk[k] / inv;   // the builder's stored weight
-        float nf[VEC], of[VEC];
-        CD::unpack(CD::load(g.x0_new, (new_view + q) * g.C + (int64_t)c * VEC), nf);
-        CD::unpack(CD::load(g.x0_prev, (old_view + q) * g.C + (int64_t)c * VEC), of);
+          for (int k = 0; k < 4; ++k) wk[k] = at[j].wk[k];
+        } else {
+          w = (uint32_t)__shfl(at[j].word, gbase + q);
 #pragma unroll
-        for (int q2 = 0; q2 < VEC; ++q2) acc[q2] = acc[q2] + wt * (nf[q2] - of[q2]);
+          for (int k = 0; k < 4; ++k) wk[k] = __shfl(at[j].wk[k], gbase + q);
+        }
+        if (!act || !w) continue;
+        const int x0 = (int)(w & 0xfffu) - 1;
+        const int y0 = (int)((w >> 12) & 0xfffu) - 1;
+        const uint32_t mask = (w >> 24) & 0xfu;
+        const int64_t new_view = ((int64_t)b * g.a + s) * g.HW;
+        const int64_t old_view = ((int64_t)b * g.N + g.anchor_view[s]) * g.HW;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          if (!(mask & (1u << k))) continue;
+          const int qq = (y0 + (k >> 1)) * g.W + x0 + (k & 1);
+          const float wt = wk[k] / inv;   // the builder's stored weight
+          float nf[VEC], of[VEC];
+          CD::unpack(CD::load(g.x0_new, (new_view + qq) * g.C + (int64_t)c * VEC), nf);
+          CD::unpack(CD::load(g.x0_prev, (old_view + qq) * g.C + (int64_t)c * VEC), of);
+#pragma unroll
+          for (int q2 = 0; q2 < VEC; ++q2) acc[q2] = acc[q2] + wt * (nf[q2] - of[q2]);
+        }
       }
     }
     if (!act) continue;
@@ -194,6 +218,10 @@ __global__ __launch_bounds__(kBlock) void k_transport_geom(GArgs g) {
     }
   }
 }
+
+// Lanes per target token: the channel vectors rounded up to a power of two,
+// at most 8 (more vectors take several rounds).
+int geom_group(int CV) { return CV <= 1 ? 1 : CV <= 2 ? 2 : CV <= 4 ? 4 : 8; }
 
 int prepare_geom(const void* x0_prev, const void* x0_new, const float* pos, const gc_camera* cams, const float* bbox,
                  int B, int N, int H, int W, int C, const int32_t* anchors, int a, int K, int dtype, void* x0_out,
@@ -248,7 +276,8 @@ int prepare_geom(const void* x0_prev, const void* x0_new, const float* pos, cons
   for (int u = 0; u < N; ++u)
     if (is_anchor[u]) g->sorted_anchor[n_sorted++] = u;
   for (int s = n_sorted; s < GC_MAX_ANCHORS; ++s) g->sorted_anchor[s] = INT32_MAX;
-  const int tok = a <= 4 ? kBlock / 4 : kBlock / 8;
+  g->G = geom_group(g->CV);
+  const int tok = kBlock / g->G;
   g->bpv_t = (int)(((int64_t)HW + tok - 1) / tok);
   g->bpv_a = (int)(((int64_t)HW * g->CV + kBlock - 1) / kBlock);
   const int64_t nt = (int64_t)B * g->NT * g->bpv_t, na = (int64_t)B * a * g->bpv_a;
@@ -265,12 +294,33 @@ void launch_geom(const GArgs& g, int dtype, hipStream_t stream) {
   const int agrid = (g.n_ablocks + kXcds - 1) / kXcds * kXcds;
   const dim3 grid((unsigned)(g.tgrid + agrid));
   const int vec = g.C / g.CV;
-#define GC_LAUNCH_GEOM(DT_, VEC_)                                                                         \
-  do {                                                                                                    \
-    if (g.a <= 4)                                                                                         \
-      hipLaunchKernelGGL((k_transport_geom<DT_, VEC_, MODE, 4>), grid, dim3(kBlock), 0, stream, g);       \
-    else                                                                                                  \
-      hipLaunchKernelGGL((k_transport_geom<DT_, VEC_, MODE, 8>), grid, dim3(kBlock), 0, stream, g);       \
+#define GC_GEOM_K(DT_, VEC_, G_, AMAX_) \
+  hipLaunchKernelGGL((k_transport_geom<DT_, VEC_, MODE, G_, AMAX_>), grid, dim3(kBlock), 0, stream, g)
+#define GC_LAUNCH_GEOM(DT_, VEC_)                  \
+  do {                                             \
+    const bool small = g.a <= 4;                   \
+    switch (g.G) {                                 \
+      case 1:                                      \
+        if (small)                                 \
+          GC_GEOM_K(DT_, VEC_, 1, 4);              \
+        else                                       \
+          GC_GEOM_K(DT_, VEC_, 1, 8);              \
+        break;                                     \
+      case 2:                                      \
+        if (small)                                 \
+          GC_GEOM_K(DT_, VEC_, 2, 4);              \
+        else                                       \
+          GC_GEOM_K(DT_, VEC_, 2, 8);              \
+        break;                                     \
+      case 4:                                      \
+        if (small)                                 \
+          GC_GEOM_K(DT_, VEC_, 4, 4);              \
+        else                                       \
+          GC_GEOM_K(DT_, VEC_, 4, 8);              \
+        break;                                     \
+      default:                                     \
+        GC_GEOM_K(DT_, VEC_, 8, 8);                \
+    }                                              \
   } while (0)
   if (dtype == GC_F32)
     GC_LAUNCH_GEOM(GC_F32, 4);
@@ -279,6 +329,7 @@ void launch_geom(const GArgs& g, int dtype, hipStream_t stream) {
   else
     GC_LAUNCH_GEOM(GC_BF16, 4);
 #undef GC_LAUNCH_GEOM
+#undef GC_GEOM_K
 }
 
 }  // namespace
