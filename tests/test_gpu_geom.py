@@ -6,10 +6,10 @@ equal gc_build_correspondence followed by gc_transport_step /
 gc_transport_reconstruct bit for bit (x0_out, x_next, model_out), and the
 transported x0 must meet the oracle's bar (float32 1e-5, bfloat16 2e-2
 against its unrounded values; unseen tokens and anchor rows bit-exact).
-Covered: every workload at full size, both lane-group sizes (a <= 4 and
-a > 4), K in {1, 2, 4}, ragged grids (a partial last block per view),
-channel counts whose vectors do not fill a lane group or need two rounds,
-background positions, a = N.
+Covered: every workload at full size, every lane-group size G in {1, 2, 4,
+8} with a <= 4 and a > 4, K in {1, 2, 4}, ragged grids (a partial last
+block per view), channel counts whose vectors do not fill a lane group or
+need two rounds, background positions, a = N.
 """
 import numpy as np
 import pytest
@@ -113,14 +113,19 @@ def test_geom_equals_stored_operator(gc, w):
         compare(gc, w, P, synth.batch_cameras(w), A, w.K, prev, new, xt, w.dtype, smp, t, tn)
 
 
-@pytest.mark.parametrize("a", [5, 8])
-def test_geom_eight_lane_groups(gc, a):
-    """a > 4 anchors: one lane per anchor in groups of 8."""
+@pytest.mark.parametrize("a,C,dtype", [(5, 16, "bf16"), (8, 16, "bf16"), (6, 16, "f32"), (5, 64, "bf16"),
+                                       (7, 4, "f32"), (3, 8, "f32")])
+def test_geom_many_anchors_every_group_size(gc, a, C, dtype):
+    """Lanes per target token G = channel vectors (rounded up to a power of
+    two, at most 8); each lane evaluates anchor slots j, j + G, ...:
+    (5 | 8, 16 bf16): G = 2, up to four slots per lane; (6, 16 f32): G = 4,
+    two slots; (5, 64 bf16): G = 8, one slot; (7, 4 f32): G = 1, every slot
+    in one lane; (3, 8 f32): G = 2 with a slot past a in the second lane."""
     w = synth.shrink(C5, B=2, a=a)
     P = latent_maps(C5.name, B=2)
     A = oracle.anchors(w.N, a, 1)
-    prev, new, xt = inputs(w, P, A, 0, C=16, dtype="bf16", seed=a)
-    compare(gc, w, P, synth.batch_cameras(w), A, 4, prev, new, xt, "bf16", sampler_of(gc, w), 0.6, 0.58)
+    prev, new, xt = inputs(w, P, A, 0, C=C, dtype=dtype, seed=a * 100 + C)
+    compare(gc, w, P, synth.batch_cameras(w), A, 4, prev, new, xt, dtype, sampler_of(gc, w), 0.6, 0.58)
 
 
 @pytest.mark.parametrize("K", [1, 2])
