@@ -141,8 +141,24 @@ def main():
             stats[A] = st
         e3.record()
         torch.cuda.synchronize()
-    rows["downsample_ms"] = e0.elapsed_time(e1)
-    rows["downsample_GBps"] = hi_d.numel() * 4 / (e0.elapsed_time(e1) * 1e-3) / 1e9 if w.factor > 1 else None
+    if w.factor > 1:
+        # ten back-to-back launches into a preallocated output (the render maps
+        # are larger than the last-level cache, so every launch reads HBM)
+        ds_out = torch.empty_like(pos)
+        torch.cuda.synchronize()
+        d0, d1 = ev(), ev()
+        d0.record()
+        for _ in range(10):
+            gc.gc_posmap_downsample(hi_d, w.factor, pos_lat=ds_out)
+        d1.record()
+        torch.cuda.synchronize()
+        assert torch.equal(ds_out.view(torch.int32), pos.view(torch.int32))
+        rows["downsample_ms"] = d0.elapsed_time(d1) / 10
+        rows["downsample_GBps"] = (hi_d.numel() + pos.numel()) * 4 / (rows["downsample_ms"] * 1e-3) / 1e9
+        del ds_out
+    else:
+        rows["downsample_ms"] = e0.elapsed_time(e1)
+        rows["downsample_GBps"] = None
     rows["bbox_ms"] = e1.elapsed_time(e2)
     rows["build_ms_per_anchor_set"] = e2.elapsed_time(e3) / len(anchor_sets)
     rows["anchor_sets"] = len(anchor_sets)

@@ -51,68 +51,57 @@ __global__ __launch_bounds__(kBlock) void k_downsample(const float* __restrict__
   }
 }
 
-// Tiled variant for f = 8: a block handles kTilePix consecutive latent
-// pixels of one latent row.  All threads first copy the block's 8 render-row
-// segments into LDS with coalesced 16-byte loads (each segment is contiguous
-// in the render map); then one thread per latent pixel folds its 8 x 8
-// samples from LDS in the same row-major order as the direct kernel.
-constexpr int kTilePix = 64;
-constexpr int kTileF = 8;
-constexpr int kTileFloats = kTileF * kTilePix * kTileF * 3;   // 12288 floats = 48 KiB
-static_assert(kTileFloats % (4 * 256) == 0, "tile must split evenly over the block");
-
-__global__ __launch_bounds__(kBlock) void k_downsample_f8(const float* __restrict__ hi, int64_t n_maps, int Hr,
-                                                          int Wr, int H, int W, float* __restrict__ lo) {
-  __shared__ f32x4 tile[kTileFloats / 4];
-  const int tiles_per_row = (W + kTilePix - 1) / kTilePix;
-  const int64_t row_id = blockIdx.x / tiles_per_row;          // m * H + j
-  const int i0 = (int)(blockIdx.x - row_id * tiles_per_row) * kTilePix;
-  const int np = min(kTilePix, W - i0);                       // latent pixels in this tile
-  const int64_t m = row_id / H;
-  const int j = (int)(row_id - m * H);
-  const int seg4 = np * kTileF * 3 / 4;                       // float4s per render-row segment
-  constexpr int kPer = kTileFloats / 4 / kBlock;              // 12 float4 per thread for a full tile
-  f32x4 v[kPer];
-  // issue every load of the tile before the first LDS write
-#pragma unroll
-  for (int r = 0; r < kPer; ++r) {
-    const int q = threadIdx.x + r * kBlock;
-    if (q < kTileF * seg4) {
-      const int dy = q / seg4, c = q - dy * seg4;
-      const f32x4* src = reinterpret_cast<const f32x4*>(hi + ((m * Hr + (int64_t)j * kTileF + dy) * Wr +
-                                                              (int64_t)i0 * kTileF) * 3);
-      v[r] = __builtin_nontemporal_load(src + c);
-    }
-  }
-#pragma unroll
-  for (int r = 0; r < kPer; ++r) {
-    const int q = threadIdx.x + r * kBlock;
-    if (q < kTileF * seg4) {
-      const int dy = q / seg4, c = q - dy * seg4;
-      tile[dy * (kTilePix * kTileF * 3 / 4) + c] = v[r];
-    }
-  }
-  __syncthreads();
-  const int t = threadIdx.x;
-  if (t >= np) return;
-  const float* ts = reinterpret_cast<const float*>(tile);
+// Vector variant for f = 4 and 8: one thread per latent pixel, each of its F
+// render rows read as 3F/4 aligned 16-byte vectors (the pixel's segment of a
+// render row is 3F contiguous floats at a multiple of 48 bytes), kRows rows
+// in flight per step.  The strided vectors of one wave tile a contiguous run
+// of the render row, so L2 serves the lines neighbouring lanes share (plain
+// loads: a nontemporal hint makes those lines miss and halves the rate);
+// no LDS and no barrier, and each thread folds its samples in the same
+// row-major order as the direct kernel.
+template <int F>
+__global__ __launch_bounds__(kBlock) void k_downsample_vec(const float* __restrict__ hi, int64_t n_pix, int Hr,
+                                                           int Wr, int H, int W, float* __restrict__ lo) {
+  constexpr int kRow4 = 3 * F / 4;          // vectors per render-row segment
+  constexpr int kRows = 4;                  // rows loaded together
+  static_assert(F % 4 == 0, "F must be a multiple of 4");
+  const int64_t gid = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+  if (gid >= n_pix) return;
+  const int i = (int)(gid % W);
+  const int64_t mj = gid / W;
+  const int j = (int)(mj % H);
+  const int64_t m = mj / H;
+  const f32x4* src = reinterpret_cast<const f32x4*>(hi + ((m * Hr + (int64_t)j * F) * Wr + (int64_t)i * F) * 3);
+  const int64_t rs = (int64_t)Wr * 3 / 4;   // vectors per render row
   int n_fg = 0;
   double sx = 0.0, sy = 0.0, sz = 0.0;
-  for (int dy = 0; dy < kTileF; ++dy) {
-    const float* row = ts + dy * (kTilePix * kTileF * 3) + t * kTileF * 3;
+  for (int dy0 = 0; dy0 < F; dy0 += kRows) {
+    float buf[kRows][3 * F];
 #pragma unroll
-    for (int dx = 0; dx < kTileF; ++dx) {
-      const float x = row[3 * dx], y = row[3 * dx + 1], z = row[3 * dx + 2];
-      if (finite_f(x) && finite_f(y) && finite_f(z)) {
-        n_fg += 1;
-        sx += (double)x;
-        sy += (double)y;
-        sz += (double)z;
+    for (int r = 0; r < kRows; ++r)
+#pragma unroll
+      for (int c = 0; c < kRow4; ++c) {
+        const f32x4 q = src[(int64_t)(dy0 + r) * rs + c];
+        buf[r][4 * c] = q.x;
+        buf[r][4 * c + 1] = q.y;
+        buf[r][4 * c + 2] = q.z;
+        buf[r][4 * c + 3] = q.w;
       }
-    }
+#pragma unroll
+    for (int r = 0; r < kRows; ++r)
+#pragma unroll
+      for (int dx = 0; dx < F; ++dx) {
+        const float x = buf[r][3 * dx], y = buf[r][3 * dx + 1], z = buf[r][3 * dx + 2];
+        if (finite_f(x) && finite_f(y) && finite_f(z)) {
+          n_fg += 1;
+          sx += (double)x;
+          sy += (double)y;
+          sz += (double)z;
+        }
+      }
   }
-  float* o = lo + ((m * H + j) * (int64_t)W + i0 + t) * 3;
-  if (2 * n_fg < kTileF * kTileF) {
+  float* o = lo + gid * 3;
+  if (2 * n_fg < F * F) {
     const float qnan = __uint_as_float(0x7fc00000u);
     o[0] = qnan;
     o[1] = qnan;
@@ -261,10 +250,11 @@ extern "C" int gc_posmap_downsample(const float* pos_hi, int64_t n_maps, int Hr,
   if (n_pix == 0) return GC_OK;
   const int64_t blocks = (n_pix + kBlock - 1) / kBlock;
   if (blocks > 0x7fffffff) return fail(GC_ERR_CAPACITY, "downsample: too many latent pixels");
-  if (f == kTileF) {
-    const int64_t tblocks = n_maps * H * (int64_t)((W + kTilePix - 1) / kTilePix);
-    if (tblocks > 0x7fffffff) return fail(GC_ERR_CAPACITY, "downsample: too many latent rows");
-    hipLaunchKernelGGL(k_downsample_f8, dim3((unsigned)tblocks), dim3(kBlock), 0, stream, pos_hi, n_maps, Hr, Wr, H,
+  if (f == 8) {
+    hipLaunchKernelGGL(k_downsample_vec<8>, dim3((unsigned)blocks), dim3(kBlock), 0, stream, pos_hi, n_pix, Hr, Wr, H,
+                       W, pos_lat);
+  } else if (f == 4) {
+    hipLaunchKernelGGL(k_downsample_vec<4>, dim3((unsigned)blocks), dim3(kBlock), 0, stream, pos_hi, n_pix, Hr, Wr, H,
                        W, pos_lat);
   } else {
     hipLaunchKernelGGL(k_downsample, dim3((unsigned)blocks), dim3(kBlock), 0, stream, pos_hi, n_pix, Hr, Wr, f, H,
