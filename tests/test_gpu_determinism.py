@@ -1,0 +1,139 @@
+"""Determinism of every device entry point on the stress workload (12
+views, 128 x 128 x 16 bfloat16, 8 assets, 4 anchors, K = 4).
+
+Each call runs twice, into output buffers pre-filled with different bytes,
+and the two results must agree bit for bit.  A difference means either a
+race (the design uses no float atomics: every float sum has a fixed order)
+or an output element the call does not write; every output here is fully
+defined by its contract, except the visible-token list past n_vis."""
+import pytest
+import torch
+
+import synth
+from synth.configs import C5
+
+from conftest import latent_maps
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda:0"
+FILL = (0xA5, 0x3C)
+
+
+@pytest.fixture(scope="module")
+def gc():
+    import paper_2608_13255_amd as gc
+    return gc
+
+
+@pytest.fixture(scope="module")
+def setup(gc):
+    w = C5
+    P = torch.from_numpy(latent_maps(w.name)).to(DEV)
+    cams = gc.camera_tensor(synth.batch_cameras(w), DEV)
+    bbox = gc.gc_posmap_bbox(P, w.tol_frac)
+    A = gc.gc_schedule_anchors(w.N, w.a, 1)
+    g = torch.Generator(device=DEV).manual_seed(5)
+    shape = (w.B, w.N, w.H, w.W, w.C)
+    lat = {k: (0.5 * torch.randn(shape, device=DEV, generator=g)).to(torch.bfloat16)
+           for k in ("x0_prev", "x_t", "x_prev", "m_km2")}
+    lat["x0_new"] = (0.5 * torch.randn((w.B, w.a, w.H, w.W, w.C), device=DEV, generator=g)).to(torch.bfloat16)
+    return w, P, cams, bbox, A, lat
+
+
+def filled(like, r, shape=None, dtype=None):
+    """An output buffer (shaped like `like`, or shape/dtype) with every byte FILL[r]."""
+    t = torch.empty(shape if shape is not None else like.shape, dtype=dtype or like.dtype, device=DEV)
+    t.view(-1).view(torch.uint8).fill_(FILL[r])
+    return t
+
+
+def bits(t):
+    if t.dtype in (torch.bfloat16, torch.float16):
+        return t.view(torch.int16).cpu()
+    if t.dtype == torch.float32:
+        return t.view(torch.int32).cpu()
+    return t.cpu()
+
+
+def same(outs):
+    for x, y in zip(outs[0], outs[1]):
+        assert torch.equal(bits(x), bits(y))
+
+
+def test_build_and_index(gc, setup):
+    w, P, cams, bbox, A, _ = setup
+    B, N, H, W, a, K = w.B, w.N, w.H, w.W, w.a, w.K
+    outs = []
+    for r in range(2):
+        corr = filled(None, r, (B, N - a, H, W, a), torch.int32)
+        wts = filled(None, r, (B, N - a, H, W, a, K), torch.float32)
+        st = filled(None, r, (B, 4), torch.int32)
+        gc.gc_build_correspondence(P, cams, A, K, bbox, corr=corr, weights=wts, stats=st)
+        idx = gc.gc_index_correspondence(corr)
+        outs.append((corr, wts, st, idx.vis_bits, idx.vis_list[:idx.n_vis]))
+    same(outs)
+
+
+def test_step_kernels(gc, setup):
+    w, P, cams, bbox, A, lat = setup
+    corr, wts = gc.gc_build_correspondence(P, cams, A, w.K, bbox)
+    idx = gc.gc_index_correspondence(corr)
+    smp = gc.Sampler(kind=gc.GC_FLOW_EULER, pred_out=gc.GC_PRED_VEL)
+    t, tn = gc.gc_sampler_step_times(smp, w.S, 7)
+    ust = gc.gc_unipc_coeffs(gc.Sampler(kind=gc.GC_DDIM), w.S, 7, 2, True)
+    x = lat["x0_prev"]
+    outs = []
+    for r in range(2):
+        o = []
+        for index in (None, idx):   # plain and split launch
+            x0 = filled(x, r)
+            o.append(gc.gc_transport_step(x, lat["x0_new"], corr, wts, A, x0_out=x0, index=index))
+            x0, xn, mo = filled(x, r), filled(x, r), filled(x, r)
+            gc.gc_transport_reconstruct(x, lat["x0_new"], corr, wts, lat["x_t"], A, smp, t, tn, x0_out=x0,
+                                        x_next=xn, model_out=mo, index=index)
+            o += [x0, xn, mo]
+            x0, xc, xn = filled(x, r), filled(x, r), filled(x, r)
+            gc.gc_transport_unipc(x, lat["x0_new"], corr, wts, A, ust, x_prev=lat["x_prev"], m_km2=lat["m_km2"],
+                                  x0_out=x0, x_c=xc, x_next=xn, index=index)
+            o += [x0, xc, xn]
+        xn, mo = filled(x, r), filled(x, r)
+        gc.gc_sampler_reconstruct(lat["x_t"], x, smp, t, tn, x_next=xn, model_out=mo)
+        o += [xn, mo]
+        x0 = filled(x, r)
+        o.append(gc.gc_transport_step_geom(x, lat["x0_new"], P, cams, bbox, A, w.K, x0_out=x0))
+        x0, xn, mo = filled(x, r), filled(x, r), filled(x, r)
+        gc.gc_transport_reconstruct_geom(x, lat["x0_new"], P, cams, bbox, lat["x_t"], A, w.K, smp, t, tn,
+                                         x0_out=x0, x_next=xn, model_out=mo)
+        o += [x0, xn, mo]
+        outs.append(o)
+    same(outs)
+
+
+def test_coverage_kernels(gc, setup):
+    w, P, cams, bbox, A, _ = setup
+    B, N, H, W = w.B, w.N, w.H, w.W
+    wpr = (H * W + 31) // 32
+    rot = []
+    for c in range(N):
+        S = gc.gc_schedule_anchors(N, w.a, c)
+        if S not in rot:
+            rot.append(S)
+    outs = []
+    for r in range(2):
+        pairs = filled(None, r, (N, B, N, wpr), torch.int32)
+        gc.gc_coverage_pairs(P, cams, bbox, out=pairs)
+        stale = filled(None, r, (B, N, H, W), torch.uint8)
+        gc.gc_coverage_init(P, out=stale)
+        ws = filled(None, r, (gc.gc_coverage_workspace_bytes(),), torch.uint8)
+        o = [pairs]
+        for step in range(6):
+            st = filled(None, r, (B, N, 4), torch.int32)
+            gc.gc_coverage_update(pairs, stale, gc.gc_schedule_anchors(N, w.a, step), 2, stats=st)
+            sel = filled(None, r, (w.a,), torch.int32)
+            gc.gc_coverage_select(pairs, stale, w.a, forced=[step % N], out=sel, workspace=ws)
+            sc = filled(None, r, (len(rot),), torch.int64)
+            gc.gc_coverage_score(pairs, stale, rot, out=sc, workspace=ws)
+            o += [st, sel, sc]
+        o.append(stale)
+        outs.append(o)
+    same(outs)
