@@ -11,9 +11,9 @@
 // not a multiple of 8), so every latent access is one 16-byte (or 8-byte)
 // load/store, consecutive lanes touch consecutive addresses, and the threads
 // of one pixel share its correspondence words and weights through L1.
-// Blocks are remapped so that each of the 8 XCDs processes one contiguous
-// slice of the (asset, view, pixel) space: an XCD then gathers from only its
-// own assets' anchor views, which fit its L2.  Data each thread touches once
+// Blocks that gather are remapped so that each of the 8 XCDs processes one
+// contiguous slice of the (asset, view, pixel) space: an XCD then gathers
+// from only its own assets' anchor views, which fit its L2.  Data each thread touches once
 // (its own x0_prev and x_t, every output) is read and written with
 // nontemporal hints; only the gathered anchor tiles go through L2 normally.
 #include "gc_common.h"
@@ -225,7 +225,10 @@ __global__ __launch_bounds__(kBlock) void k_transport(TArgs g) {
   // Blocks never straddle a view, so the (asset, view) split and the view's
   // role (anchor slot or target slot) are wave-uniform scalar values; only
   // the chunk -> (token, channel vector) split is per lane.
-  const int lb = logical_block(i, g.n_blocks, g.remap);
+  // The split launch's streaming blocks gather nothing: they run in the
+  // hardware's round-robin order over the XCDs (measured faster than one
+  // contiguous slice per XCD); the dense launch keeps the slices.
+  const int lb = logical_block(i, g.n_blocks, SPLIT ? 0 : g.remap);
   if (lb >= g.n_blocks) return;
   const int bv = __builtin_amdgcn_readfirstlane(lb / g.bpv);   // b * N + v
   const int t = (lb - bv * g.bpv) * kBlock + (int)threadIdx.x;
