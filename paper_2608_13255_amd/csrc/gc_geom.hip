@@ -4,21 +4,22 @@
 // maps and cameras only (Sec. 3.2, correspondence operator), so it can be
 // rebuilt inside the step from 12 bytes of position per target token plus
 // the anchors' position taps; nothing has to be built or stored per anchor
-// set.  That pays when
-// anchor sets do not repeat (e.g. chosen adaptively); with the rotation's
-// few repeating sets the stored operator and its visible-token index are
-// cheaper per step.
+// set.  That pays when anchor sets do not repeat (e.g. chosen adaptively);
+// with the rotation's few repeating sets the stored operator and its
+// visible-token index are cheaper per step.
 //
-// Work mapping: a group of G adjacent lanes serves one target token, G the
-// number of channel vectors rounded up to a power of two (at most 8), so
-// that every lane of the group has latent work.  Lane j of the group
-// evaluates anchor slots j, j + G, ... exactly as the builder does (same
-// device function, same float order); n_vis is a ballot over the group, and
-// the group's lanes read every anchor's word and weights from each other
-// with cross-lane permutes, in ascending slot order; lane j then gathers and
-// blends the channel vectors j, j + G, ...  Weights are the builder's
-// stored values (w_k / n_vis in float), so the result equals
-// gc_build_correspondence followed by gc_transport_step bit for bit.
+// Work mapping: in a target-view block a group of G adjacent lanes serves
+// one target token, G the number of channel vectors rounded up to a power of
+// two (at most 8).  Lane j of the group evaluates anchor slots j, j + G, ...
+// exactly as the builder does (same device function, same float order), and
+// n_vis is a ballot over the group.  The block then ranks its tokens, the
+// visible ones (some anchor sees them) first and the others after them,
+// keeps the visible tokens' words and weights in LDS, and hands out one
+// (token, channel vector) item per lane in that order: the gathers fill
+// whole waves while the other waves only stream, as in the stored-operator
+// split launch.  A visible item blends its anchors in ascending slot order
+// with the builder's stored weights (w_k / n_vis in float), so the result
+// equals gc_build_correspondence followed by gc_transport_step bit for bit.
 //
 // Split launch: the target-view blocks, whose dependent loads (position,
 // the anchors' position taps, then the latent taps) set the pace, come
@@ -115,7 +116,6 @@ __global__ __launch_bounds__(kBlock) void k_transport_geom(GArgs g) {
   const int lane_g = (int)threadIdx.x & (G - 1);
   const int p = (lb - bt * g.bpv_t) * kTok + (int)threadIdx.x / G;
   const bool tok_ok = p < g.HW;
-  const int64_t tbase = ((int64_t)bv * g.HW + p) * g.C;   // this token's first element
 
   // target token: lane j of the group evaluates anchor slots j, j + G, ...
   if (threadIdx.x < g.a) cam_lds[threadIdx.x] = g.cams[(int64_t)b * g.N + g.anchor_view[threadIdx.x]];
@@ -141,42 +141,83 @@ __global__ __launch_bounds__(kBlock) void k_transport_geom(GArgs g) {
       at[j] = anchor_taps(P, cam_lds[s], g.pos + ((int64_t)b * g.N + g.anchor_view[s]) * g.HW * 3, g.H, g.W, g.K,
                           g.bbox[(int64_t)b * 8 + 6]);
   }
-  // every lane reaches the ballots and the permutes below (no early exit)
+  // n_vis: a ballot over the group (every lane reaches the ballots)
   const int gbase = __lane_id() & ~(G - 1);
   int n_vis = 0;
 #pragma unroll
   for (int j = 0; j < kApl; ++j) n_vis += __popcll((__ballot(at[j].word != 0) >> gbase) & ((1ull << G) - 1));
-  const float inv = n_vis > 0 ? (float)n_vis : 1.0f;
-  const int rounds = (g.CV + G - 1) / G;
-  for (int r = 0; r < rounds; ++r) {
-    const int c = r * G + lane_g;
-    const bool act = tok_ok && c < g.CV;
-    const int64_t e = tbase + (int64_t)c * VEC;
-    Raw xtr, prevr;
-    if (act) {
-      if constexpr (MODE == kGeomReconstruct) xtr = CD::load_stream(g.x_t, e);
-      prevr = CD::load_stream(g.x0_prev, e);
-    }
-    float acc[VEC];
+
+  // Compaction: the block's visible tokens first (ascending), then the other
+  // tokens (ascending); the visible tokens' words and weights go to LDS.  The
+  // latent phase gives each lane one (token, channel vector) item in that
+  // order, so the gathering and the streaming fall into separate waves.
+  __shared__ int32_t s_tok[kTok];
+  __shared__ int32_t s_nvis[kTok];
+  __shared__ int32_t s_word[kTok][AMAX + 1];       // +1: no bank conflicts between consecutive tokens
+  __shared__ float s_wk[kTok][AMAX * 4 + 1];
+  __shared__ int32_t s_count[kBlock / 64][2];      // per wave: visible tokens, live tokens
+  const bool vis = tok_ok && n_vis > 0;
+  const bool lead = lane_g == 0;
+  const unsigned long long bvis = __ballot(lead && vis);
+  const unsigned long long blive = __ballot(lead && tok_ok);
+  const int wv = (int)threadIdx.x / 64;
+  if (__lane_id() == 0) {
+    s_count[wv][0] = __popcll(bvis);
+    s_count[wv][1] = __popcll(blive);
+  }
+  __syncthreads();
+  int off_v = 0, off_l = 0, nv = 0, nl = 0;
 #pragma unroll
-    for (int q = 0; q < VEC; ++q) acc[q] = 0.0f;
+  for (int q = 0; q < kBlock / 64; ++q) {
+    const int cv_ = s_count[q][0], cl_ = s_count[q][1];
+    off_v += q < wv ? cv_ : 0;
+    off_l += q < wv ? cl_ : 0;
+    nv += cv_;
+    nl += cl_;
+  }
+  if (tok_ok) {
+    const unsigned long long below = (1ull << gbase) - 1;   // the groups before this one in the wave
+    const int rv = off_v + __popcll(bvis & below);
+    const int rl = off_l + __popcll(blive & below);
+    if (lead) s_tok[vis ? rv : nv + (rl - rv)] = p;
+    if (vis) {
 #pragma unroll
-    for (int j = 0; j < kApl; ++j) {
-      for (int q = 0; q < G; ++q) {   // anchor slot s = j G + q: ascending, as the stored operator sums
-        const int s = j * G + q;
-        if (s >= g.a) break;
-        uint32_t w;
-        float wk[4];
-        if constexpr (G == 1) {
-          w = (uint32_t)at[j].word;
+      for (int j = 0; j < kApl; ++j) {
+        const int s = j * G + lane_g;
+        if (s < g.a) {
+          s_word[rv][s] = at[j].word;
 #pragma unroll
-          for (int k = 0; k < 4; ++k) wk[k] = at[j].wk[k];
-        } else {
-          w = (uint32_t)__shfl(at[j].word, gbase + q);
-#pragma unroll
-          for (int k = 0; k < 4; ++k) wk[k] = __shfl(at[j].wk[k], gbase + q);
+          for (int k = 0; k < 4; ++k) s_wk[rv][s * 4 + k] = at[j].wk[k];
         }
-        if (!act || !w) continue;
+      }
+      if (lead) s_nvis[rv] = n_vis;
+    }
+  }
+  __syncthreads();
+
+  const int n_items = nl * g.CV;
+  for (int it = (int)threadIdx.x; it < n_items; it += kBlock) {
+    int slot, c;
+    if (g.cv_shift >= 0) {
+      slot = it >> g.cv_shift;
+      c = it & (g.CV - 1);
+    } else {
+      slot = it / g.CV;
+      c = it - slot * g.CV;
+    }
+    const int64_t e = ((int64_t)bv * g.HW + s_tok[slot]) * g.C + (int64_t)c * VEC;
+    Raw xtr, prevr;
+    if constexpr (MODE == kGeomReconstruct) xtr = CD::load_stream(g.x_t, e);
+    prevr = CD::load_stream(g.x0_prev, e);
+    Raw x0r;
+    if (slot < nv) {
+      const float inv = (float)s_nvis[slot];
+      float acc[VEC];
+#pragma unroll
+      for (int q = 0; q < VEC; ++q) acc[q] = 0.0f;
+      for (int s = 0; s < g.a; ++s) {   // ascending slots, as the stored operator sums
+        const uint32_t w = (uint32_t)s_word[slot][s];
+        if (!w) continue;
         const int x0 = (int)(w & 0xfffu) - 1;
         const int y0 = (int)((w >> 12) & 0xfffu) - 1;
         const uint32_t mask = (w >> 24) & 0xfu;
@@ -186,7 +227,7 @@ __global__ __launch_bounds__(kBlock) void k_transport_geom(GArgs g) {
         for (int k = 0; k < 4; ++k) {
           if (!(mask & (1u << k))) continue;
           const int qq = (y0 + (k >> 1)) * g.W + x0 + (k & 1);
-          const float wt = wk[k] / inv;   // the builder's stored weight
+          const float wt = s_wk[slot][s * 4 + k] / inv;   // the builder's stored weight
           float nf[VEC], of[VEC];
           CD::unpack(CD::load(g.x0_new, (new_view + qq) * g.C + (int64_t)c * VEC), nf);
           CD::unpack(CD::load(g.x0_prev, (old_view + qq) * g.C + (int64_t)c * VEC), of);
@@ -194,22 +235,17 @@ __global__ __launch_bounds__(kBlock) void k_transport_geom(GArgs g) {
           for (int q2 = 0; q2 < VEC; ++q2) acc[q2] = acc[q2] + wt * (nf[q2] - of[q2]);
         }
       }
-    }
-    if (!act) continue;
-    Raw x0r;
-    float x0f[VEC];
-    if (n_vis == 0) {
-      x0r = prevr;   // no anchor sees this token: it keeps its own state
-    } else {
       float prevf[VEC], y[VEC];
       CD::unpack(prevr, prevf);
 #pragma unroll
       for (int q = 0; q < VEC; ++q) y[q] = prevf[q] + acc[q];
       x0r = CD::pack(y);
+    } else {
+      x0r = prevr;   // no anchor sees this token: it keeps its own state
     }
     CD::store_stream(g.x0_out, e, x0r);
     if constexpr (MODE == kGeomReconstruct) {
-      float xtf[VEC], xn[VEC], mo[VEC];
+      float xtf[VEC], x0f[VEC], xn[VEC], mo[VEC];
       CD::unpack(x0r, x0f);   // the reconstruction reads x0 as stored
       CD::unpack(xtr, xtf);
       reconstruct_vec<VEC>(g.r, xtf, x0f, xn, mo);
@@ -220,7 +256,7 @@ __global__ __launch_bounds__(kBlock) void k_transport_geom(GArgs g) {
 }
 
 // Lanes per target token: the channel vectors rounded up to a power of two,
-// at most 8 (more vectors take several rounds).
+// at most 8 (with more vectors a lane takes several items).
 int geom_group(int CV) { return CV <= 1 ? 1 : CV <= 2 ? 2 : CV <= 4 ? 4 : 8; }
 
 int prepare_geom(const void* x0_prev, const void* x0_new, const float* pos, const gc_camera* cams, const float* bbox,
