@@ -224,6 +224,12 @@ def main():
         plans[(i % len(ring), A)](t, tn)
         return A
 
+    # device warm-up before the W warmup steps: about 90 ms of the same step,
+    # so that the GPU's clocks have left their idle state (the first tens of
+    # milliseconds after an idle host phase run measurably slower)
+    for i in range(2000):
+        step(i)
+    torch.cuda.synchronize()
     for i in range(args.warmup):
         step(i)
     torch.cuda.synchronize()

@@ -46,7 +46,6 @@ struct TArgs {
   int64_t n_tokens;    // B * NT * HW
   int n_vis;
   int gblocks;         // gather blocks in front of the streaming blocks (multiple of kXcds)
-  int bits_uniform;    // 1: each streaming wave's target tokens lie in one vis_bits word
   int32_t sorted_anchor[GC_MAX_ANCHORS];  // anchor views ascending, padded with INT_MAX
   Recon r;
   // UniPC mode: x_t is x_cur; x_prev / m_km2 inputs, x_c output; coefficients in float
@@ -259,11 +258,7 @@ __global__ __launch_bounds__(kBlock) void k_transport(TArgs g) {
   }
   const int64_t crow = ((int64_t)b * g.NT + (v - n_before)) * g.HW + p;
   if constexpr (SPLIT) {
-    // when the wave's tokens share one word, it is read once, wave-uniform,
-    // through the scalar cache (shorter latency before the data loads)
-    const uint32_t word =
-        g.bits_uniform ? g.vis_bits[__builtin_amdgcn_readfirstlane((int)(crow >> 5))] : g.vis_bits[crow >> 5];
-    if ((word >> (crow & 31)) & 1u) return;   // a gather block owns this token
+    if ((g.vis_bits[crow >> 5] >> (crow & 31)) & 1u) return;   // a gather block owns this token
     token_step<DT, VEC, MODE>(g, b, p, cv, -1, crow, base, kTargetUnseen);
   } else {
     token_step<DT, VEC, MODE>(g, b, p, cv, -1, crow, base, kTargetCheck);
@@ -378,10 +373,6 @@ int prepare_transport(const void* x0_prev, const void* x0_new, const int32_t* co
     g->vis_bits = vis_bits;
     g->vis_list = vis_list;
     g->n_vis = (int)n_vis;
-    // A streaming wave covers 64 / CV consecutive tokens of one view starting
-    // at a multiple of 64 / CV; with CV a power of two >= 2 and rows of a
-    // multiple of 32 tokens that range lies inside one 32-token word.
-    g->bits_uniform = (g->cv_shift >= 1 && HW % 32 == 0) ? 1 : 0;
     const int64_t gb = ((int64_t)n_vis * g->CV + kBlock - 1) / kBlock;
     g->gblocks = (int)((gb + kXcds - 1) / kXcds * kXcds);
     if ((int64_t)g->gblocks + nb > (int64_t)0x7fffffff - kXcds)
