@@ -190,8 +190,11 @@ int gc_posmap_bbox(const float* pos, int B, int N, int H, int W, float tol_frac,
  *   corr     device int32 [B][N-a][H][W][a] output, target views in ascending
  *            view order: word = (x0+1) | (y0+1) << 12 | mask << 24, mask bit k
  *            set for each kept tap; 0 iff anchor s contributes nothing
- *   weights  device float [B][N-a][H][W][a][K] output: final weight of the j-th
- *            tap set in the word (ascending k), 0 beyond
+ *   weights  device float [B][N-a][H][W][a][K] output, written for the pairs
+ *            whose word is non-zero: final weight of the j-th tap set in the
+ *            word (ascending k), 0 beyond.  The weights of a pair whose word is
+ *            0 are not written (no transport call reads them), so the buffer
+ *            keeps whatever it held there.
  *   stats    nullable device uint32 [B][4] output (zeroed by the call):
  *            {visible (pixel, anchor) pairs, target pixels seen by >= 1 anchor,
  *             foreground target pixels, kept taps}

@@ -112,6 +112,11 @@ __global__ __launch_bounds__(kBlock) void k_build(BuildArgs g) {
     if (live) {
       const int64_t row = ((int64_t)b * g.NT + ti) * HW + p;
       g.corr[row * g.a + s] = word;
+    }
+    // weights only for pairs the anchor sees: the transport reads a pair's
+    // weights only when its word is non-zero (most pairs' words are zero)
+    if (live && word != 0) {
+      const int64_t row = ((int64_t)b * g.NT + ti) * HW + p;
       float out[4] = {0.f, 0.f, 0.f, 0.f};
       const float inv = n_vis > 0 ? (float)n_vis : 1.0f;
       int j = 0;

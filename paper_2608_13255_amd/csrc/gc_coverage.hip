@@ -312,9 +312,10 @@ __global__ __launch_bounds__(64) void k_sel_gains(const uint32_t* __restrict__ b
 #pragma unroll
       for (int q = 0; q < 16; ++q) {
         const int u = u0 + q;
-        if (u >= N) break;
-        const uint32_t g = wave_add(weighted_count(w, wd[q] & live));
-        if (lane == u) mine += g;
+        if (u < N) {   // uniform
+          const uint32_t g = wave_add(weighted_count(w, wd[q] & live));
+          if (lane == u) mine += g;
+        }
       }
     }
   }

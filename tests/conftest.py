@@ -40,3 +40,13 @@ def ulp_diff(a: np.ndarray, b: np.ndarray) -> np.ndarray:
     ia = np.asarray(a, np.float32).view(np.int32).astype(np.int64)
     ib = np.asarray(b, np.float32).view(np.int32).astype(np.int64)
     return np.abs(ia - ib)
+
+
+def visible_weights(corr, wts):
+    """The builder writes the weights of (token, anchor) pairs with a non-zero
+    word only; this zeroes the others (whatever the buffer held), which is what
+    the oracle stores there."""
+    import numpy as np
+    corr = corr.cpu().numpy() if hasattr(corr, "cpu") else corr
+    wts = wts.cpu().numpy() if hasattr(wts, "cpu") else wts
+    return np.where((corr != 0)[..., None], wts, np.float32(0))

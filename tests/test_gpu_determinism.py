@@ -5,7 +5,8 @@ Each call runs twice, into output buffers pre-filled with different bytes,
 and the two results must agree bit for bit.  A difference means either a
 race (the design uses no float atomics: every float sum has a fixed order)
 or an output element the call does not write; every output here is fully
-defined by its contract, except the visible-token list past n_vis."""
+defined by its contract, except the visible-token list past n_vis and the
+weights of pairs whose word is zero."""
 import pytest
 import torch
 
@@ -70,7 +71,8 @@ def test_build_and_index(gc, setup):
         st = filled(None, r, (B, 4), torch.int32)
         gc.gc_build_correspondence(P, cams, A, K, bbox, corr=corr, weights=wts, stats=st)
         idx = gc.gc_index_correspondence(corr)
-        outs.append((corr, wts, st, idx.vis_bits, idx.vis_list[:idx.n_vis]))
+        seen = (corr != 0).unsqueeze(-1).expand_as(wts)   # weights are written for these pairs only
+        outs.append((corr, wts[seen], st, idx.vis_bits, idx.vis_list[:idx.n_vis]))
     same(outs)
 
 

@@ -15,7 +15,7 @@ import oracle
 import synth
 from synth.configs import C2
 
-from conftest import latent_maps
+from conftest import latent_maps, visible_weights
 from test_gpu_properties import random_rig
 
 pytestmark = pytest.mark.gpu
@@ -68,7 +68,7 @@ def full_check(gc, P, bcams, anchors, K, C, dtype, rs, tol_frac=0.03, geom=True,
     bbd = gc.gc_posmap_bbox(Pd, tol_frac)
     corr, wts = gc.gc_build_correspondence(Pd, cams_d, anchors, K, bbd)
     np.testing.assert_array_equal(corr.cpu().numpy(), corr_o)
-    assert np.abs(wts.cpu().numpy() - wts_o).max(initial=0.0) <= 1e-6
+    assert np.abs(visible_weights(corr, wts) - wts_o).max(initial=0.0) <= 1e-6
     idx = gc.gc_index_correspondence(corr)
     assert idx.n_vis == int((nvis_o > 0).sum())
     smp = gc.Sampler(kind=gc.GC_FLOW_EULER)

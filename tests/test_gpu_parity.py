@@ -20,7 +20,7 @@ import oracle
 import synth
 from synth.configs import C1, C2, C3, C4, C5
 
-from conftest import latent_maps
+from conftest import latent_maps, visible_weights
 
 pytestmark = pytest.mark.gpu
 
@@ -144,7 +144,7 @@ def _build_both(gc, w, P, A, K):
     Pd = torch.from_numpy(P).to(DEV)
     bbd = gc.gc_posmap_bbox(Pd, w.tol_frac)
     corr, wts = gc.gc_build_correspondence(Pd, cams, A, K, bbd, stats=stats)
-    return (corr_o, wts_o, nvis_o), (corr.cpu().numpy(), wts.cpu().numpy(), stats.cpu().numpy())
+    return (corr_o, wts_o, nvis_o), (corr.cpu().numpy(), visible_weights(corr, wts), stats.cpu().numpy())
 
 
 @pytest.mark.parametrize("w", ALL, ids=lambda w: w.name)
@@ -155,6 +155,7 @@ def test_correspondence_parity(gc, w, K):
         A = anchors_of(w, c)
         (corr_o, wts_o, nvis_o), (corr, wts, stats) = _build_both(gc, w, P, A, K)
         np.testing.assert_array_equal(corr, corr_o)
+        # weights of visible pairs (the oracle stores 0 for the others)
         assert np.abs(wts.astype(np.float64) - wts_o).max() <= 1e-6
         # the words decide which weights are zero: they must agree exactly
         np.testing.assert_array_equal(wts == 0, wts_o == 0)
@@ -171,6 +172,26 @@ def test_correspondence_parity(gc, w, K):
             assert stats[b, 3] == taps[b].sum()
         if w.fixed_anchors:
             break
+
+
+def test_weights_written_for_visible_pairs_only(gc):
+    """The builder writes a pair's weights iff its word is non-zero: every
+    other weight keeps the buffer's previous bytes; the written ones equal a
+    build into a fresh buffer."""
+    w = C5
+    P = latent_maps(w.name)
+    A = anchors_of(w, 1)
+    Pd = torch.from_numpy(P).to(DEV)
+    cams = gc.camera_tensor(synth.batch_cameras(w), DEV)
+    bbd = gc.gc_posmap_bbox(Pd, w.tol_frac)
+    corr, wts = gc.gc_build_correspondence(Pd, cams, A, w.K, bbd)
+    pre = torch.full_like(wts, -7.25)
+    corr2, wts2 = gc.gc_build_correspondence(Pd, cams, A, w.K, bbd, weights=pre)
+    assert torch.equal(corr2, corr)
+    seen = (corr != 0).unsqueeze(-1).expand_as(wts)
+    assert torch.equal(wts2[seen], wts[seen])
+    assert bool((wts2[~seen] == -7.25).all())
+    assert 0 < int(seen.sum()) < seen.numel()
 
 
 def test_correspondence_ragged_grid_and_all_anchor_set(gc):
@@ -191,7 +212,7 @@ def test_correspondence_ragged_grid_and_all_anchor_set(gc):
             corr, wts = gc.gc_build_correspondence(Pd, gc.camera_tensor(bcams, DEV), A, K,
                                                    gc.gc_posmap_bbox(Pd, 0.01))
             np.testing.assert_array_equal(corr.cpu().numpy(), corr_o)
-            assert np.abs(wts.cpu().numpy() - wts_o).max() <= 1e-6
+            assert np.abs(visible_weights(corr, wts) - wts_o).max() <= 1e-6
     Pd = torch.from_numpy(P).to(DEV)
     corr, wts = gc.gc_build_correspondence(Pd, gc.camera_tensor(bcams, DEV), [0, 1, 2, 3], 4,
                                            gc.gc_posmap_bbox(Pd, 0.01))

@@ -16,6 +16,8 @@ from hypothesis import HealthCheck, given, settings, strategies as st
 import oracle
 import synth
 
+from conftest import visible_weights
+
 pytestmark = pytest.mark.gpu
 DEV = "cuda:0"
 TOL = {"f32": 1e-5, "bf16": 2e-2}
@@ -89,7 +91,7 @@ def test_random_problems_match_oracle(seed, H, W, N, a_frac, K, C, dtype, pinhol
     np.testing.assert_array_equal(bbd.cpu().numpy()[:, 6].view(np.uint32), bb[:, 6].view(np.uint32))
     corr, wts = gc.gc_build_correspondence(Pd, gc.camera_tensor(bcams, DEV), anchors, K, bbd)
     np.testing.assert_array_equal(corr.cpu().numpy(), corr_o)
-    assert np.abs(wts.cpu().numpy() - wts_o).max(initial=0.0) <= 1e-6
+    assert np.abs(visible_weights(corr, wts) - wts_o).max(initial=0.0) <= 1e-6
     idx = gc.gc_index_correspondence(corr)
     assert idx.n_vis == int((nvis_o > 0).sum())
     outs = []
