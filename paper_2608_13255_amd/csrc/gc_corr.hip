@@ -69,7 +69,11 @@ __global__ __launch_bounds__(kBlock) void k_build(BuildArgs g) {
   const int b = bt / g.NT;
   const int ti = bt - b * g.NT;
   const int v = g.target_view[ti];
-  if (threadIdx.x < g.a) cam_lds[threadIdx.x] = g.cams[(int64_t)b * g.N + g.anchor_view[threadIdx.x]];
+  __shared__ int32_t view_lds[GC_MAX_ANCHORS];   // a lane's own slot: from LDS, not a per-lane kernel-argument load
+  if (threadIdx.x < g.a) {
+    view_lds[threadIdx.x] = g.anchor_view[threadIdx.x];
+    cam_lds[threadIdx.x] = g.cams[(int64_t)b * g.N + g.anchor_view[threadIdx.x]];
+  }
   __syncthreads();
 
   const int s = threadIdx.x & (G - 1);                   // anchor slot of this lane
@@ -95,7 +99,7 @@ __global__ __launch_bounds__(kBlock) void k_build(BuildArgs g) {
     float wk[4] = {0.f, 0.f, 0.f, 0.f};   // this anchor's normalised weight of tap k
     int mask = 0;
     if (live && fg) {
-      const AnchorTaps at = anchor_taps(P, cam_lds[s], g.pos + ((int64_t)b * g.N + g.anchor_view[s]) * HW * 3, g.H,
+      const AnchorTaps at = anchor_taps(P, cam_lds[s], g.pos + ((int64_t)b * g.N + view_lds[s]) * HW * 3, g.H,
                                         g.W, g.K, tol2);
       word = at.word;
       mask = at.mask;

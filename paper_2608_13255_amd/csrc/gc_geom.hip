@@ -118,7 +118,12 @@ __global__ __launch_bounds__(kBlock) void k_transport_geom(GArgs g) {
   const bool tok_ok = p < g.HW;
 
   // target token: lane j of the group evaluates anchor slots j, j + G, ...
-  if (threadIdx.x < g.a) cam_lds[threadIdx.x] = g.cams[(int64_t)b * g.N + g.anchor_view[threadIdx.x]];
+  __shared__ int32_t view_lds[GC_MAX_ANCHORS];   // anchor views in LDS: a per-lane index into the kernel
+                                                  // arguments would be a memory load ordered after the taps
+  if (threadIdx.x < g.a) {
+    view_lds[threadIdx.x] = g.anchor_view[threadIdx.x];
+    cam_lds[threadIdx.x] = g.cams[(int64_t)b * g.N + g.anchor_view[threadIdx.x]];
+  }
   __syncthreads();
   float P[3] = {0.f, 0.f, 0.f};
   bool fg = false;
@@ -129,18 +134,27 @@ __global__ __launch_bounds__(kBlock) void k_transport_geom(GArgs g) {
     P[2] = pp[2];
     fg = finite_f(P[0]) && finite_f(P[1]) && finite_f(P[2]);
   }
+  // all of the lane's slots are projected first and all their tap loads are
+  // issued together (a lane without a slot, or a background token, loads the
+  // grid's corner taps of slot 0's map and ignores them)
+  AnchorProj pj[kApl];
+  TapPos tp[kApl];
   AnchorTaps at[kApl];
 #pragma unroll
-  for (int j = 0; j < kApl; ++j) {
-    at[j].word = 0;
-    at[j].mask = 0;
-#pragma unroll
-    for (int k = 0; k < 4; ++k) at[j].wk[k] = 0.0f;
+  for (int j = 0; j < kApl; ++j) {   // branch-free: a lane without the slot keeps the result unused
     const int s = j * G + lane_g;
-    if (tok_ok && fg && s < g.a)
-      at[j] = anchor_taps(P, cam_lds[s], g.pos + ((int64_t)b * g.N + g.anchor_view[s]) * g.HW * 3, g.H, g.W, g.K,
-                          g.bbox[(int64_t)b * 8 + 6]);
+    pj[j] = anchor_project(P, cam_lds[s < g.a ? s : 0], g.H, g.W);
+    pj[j].ok = pj[j].ok && tok_ok && fg && s < g.a;
   }
+#pragma unroll
+  for (int j = 0; j < kApl; ++j) {
+    const int s = j * G + lane_g;
+    const int sc = s < g.a ? s : 0;
+    tp[j] = anchor_tap_positions(pj[j], g.pos + ((int64_t)b * g.N + view_lds[sc]) * g.HW * 3, g.H, g.W);
+  }
+  const float tol2 = g.bbox[(int64_t)b * 8 + 6];
+#pragma unroll
+  for (int j = 0; j < kApl; ++j) at[j] = anchor_select(P, pj[j], tp[j], g.H, g.W, g.K, tol2);
   // n_vis: a ballot over the group (every lane reaches the ballots)
   const int gbase = __lane_id() & ~(G - 1);
   int n_vis = 0;

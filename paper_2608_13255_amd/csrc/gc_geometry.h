@@ -17,15 +17,26 @@ struct AnchorTaps {
   float wk[4];    // this anchor's normalised weight of tap k (before the division by n_vis)
 };
 
-// P: the target token's 3D point (finite); cam: the anchor's camera;
-// src: the anchor view's position map [H][W][3]; tol2: squared tolerance.
-__device__ __forceinline__ AnchorTaps anchor_taps(const float (&P)[3], const gc_camera& cam, const float* src, int H,
-                                                  int W, int K, float tol2) {
-  AnchorTaps o;
-  o.word = 0;
-  o.mask = 0;
-#pragma unroll
-  for (int k = 0; k < 4; ++k) o.wk[k] = 0.0f;
+// The operator for one pair runs in three steps so that callers can keep
+// several anchors' tap loads in flight: anchor_project (arithmetic only),
+// anchor_tap_positions (the four loads, all issued together) and
+// anchor_select (the tests, the selection and the weights).  anchor_taps
+// composes them for one anchor.
+
+struct AnchorProj {
+  bool ok;          // the projection lands within two pixels of the grid
+  int x0, y0;       // the footprint's top-left tap
+  float ax, ay;     // bilinear fractions
+};
+
+// P: the target token's 3D point (finite); cam: the anchor's camera.
+__device__ __forceinline__ AnchorProj anchor_project(const float (&P)[3], const gc_camera& cam, int H, int W) {
+  AnchorProj o;
+  o.ok = false;
+  o.x0 = 0;
+  o.y0 = 0;
+  o.ax = 0.0f;
+  o.ay = 0.0f;
   const float* R = cam.R;
   const float xc = ((R[0] * P[0] + R[1] * P[1]) + R[2] * P[2]) + cam.t[0];
   const float yc = ((R[3] * P[0] + R[4] * P[1]) + R[5] * P[2]) + cam.t[1];
@@ -49,8 +60,48 @@ __device__ __forceinline__ AnchorTaps anchor_taps(const float (&P)[3], const gc_
   if (!ok) return o;
   const float gx = px - 0.5f, gy = py - 0.5f;
   const float fx0 = floorf(gx), fy0 = floorf(gy);
-  const float ax = gx - fx0, ay = gy - fy0;
-  const int x0 = (int)fx0, y0 = (int)fy0;
+  o.ok = true;
+  o.ax = gx - fx0;
+  o.ay = gy - fy0;
+  o.x0 = (int)fx0;
+  o.y0 = (int)fy0;
+  return o;
+}
+
+// Positions of the four taps (x0 + (k & 1), y0 + (k >> 1)) of the anchor
+// view's map src [H][W][3].  Every load reads a pixel clamped onto the grid,
+// so all four are issued without a branch; anchor_select ignores the taps
+// that are off the grid (and all of them when the projection failed).
+struct TapPos {
+  float q[4][3];
+};
+
+__device__ __forceinline__ TapPos anchor_tap_positions(const AnchorProj& pj, const float* src, int H, int W) {
+  TapPos t;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const int x = min(max(pj.x0 + (k & 1), 0), W - 1);
+    const int y = min(max(pj.y0 + (k >> 1), 0), H - 1);
+    const float* Q = src + ((int64_t)y * W + x) * 3;
+    t.q[k][0] = Q[0];
+    t.q[k][1] = Q[1];
+    t.q[k][2] = Q[2];
+  }
+  return t;
+}
+
+// The per-tap tolerance test, the K nearest valid taps and their normalised
+// area weights; tol2: squared tolerance.
+__device__ __forceinline__ AnchorTaps anchor_select(const float (&P)[3], const AnchorProj& pj, const TapPos& tp, int H,
+                                                    int W, int K, float tol2) {
+  AnchorTaps o;
+  o.word = 0;
+  o.mask = 0;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) o.wk[k] = 0.0f;
+  if (!pj.ok) return o;
+  const int x0 = pj.x0, y0 = pj.y0;
+  const float ax = pj.ax, ay = pj.ay;
   bool valid[4];
   float d2[4];
   int nvalid = 0;
@@ -60,8 +111,7 @@ __device__ __forceinline__ AnchorTaps anchor_taps(const float (&P)[3], const gc_
     valid[k] = false;
     d2[k] = 0.0f;
     if (x < 0 || x >= W || y < 0 || y >= H) continue;
-    const float* Q = src + ((int64_t)y * W + x) * 3;
-    const float qx = Q[0], qy = Q[1], qz = Q[2];
+    const float qx = tp.q[k][0], qy = tp.q[k][1], qz = tp.q[k][2];
     if (!(finite_f(qx) && finite_f(qy) && finite_f(qz))) continue;
     const float dx = qx - P[0], dy = qy - P[1], dz = qz - P[2];
     const float dd = (dx * dx + dy * dy) + dz * dz;
@@ -114,6 +164,15 @@ __device__ __forceinline__ AnchorTaps anchor_taps(const float (&P)[3], const gc_
   }
   o.word = (int32_t)((uint32_t)(x0 + 1) | ((uint32_t)(y0 + 1) << 12) | ((uint32_t)o.mask << 24));
   return o;
+}
+
+// P: the target token's 3D point (finite); cam: the anchor's camera;
+// src: the anchor view's position map [H][W][3]; tol2: squared tolerance.
+__device__ __forceinline__ AnchorTaps anchor_taps(const float (&P)[3], const gc_camera& cam, const float* src, int H,
+                                                  int W, int K, float tol2) {
+  const AnchorProj pj = anchor_project(P, cam, H, W);
+  const TapPos tp = anchor_tap_positions(pj, src, H, W);
+  return anchor_select(P, pj, tp, H, W, K, tol2);
 }
 
 }  // namespace gc
