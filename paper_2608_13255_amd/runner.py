@@ -17,12 +17,12 @@ from typing import Callable, Dict, List, Optional, Sequence, Tuple
 
 import torch
 
-from . import (GC_FULL_HEAD_MID_TAIL, GC_FULL_HEAD_TAIL_E, GC_FULL_PERIODIC, Sampler, VisibleIndex, gc_build_correspondence,
-               gc_coverage_init, gc_coverage_pairs, gc_coverage_score, gc_coverage_select, gc_coverage_update,
-               gc_coverage_workspace_bytes,
-               gc_index_correspondence, gc_posmap_bbox, gc_sampler_reconstruct, gc_sampler_step_times,
-               gc_schedule_anchors, gc_schedule_full_steps, gc_schedule_refresh_due, gc_transport_reconstruct,
-               gc_transport_reconstruct_geom, gc_transport_unipc, gc_unipc_coeffs, gc_unipc_update)
+from . import (GC_FULL_HEAD_MID_TAIL, GC_FULL_HEAD_TAIL_E, GC_FULL_PERIODIC, Sampler, VisibleIndex,
+               gc_build_correspondence, gc_coverage_init, gc_coverage_pairs, gc_coverage_score, gc_coverage_select,
+               gc_coverage_update, gc_coverage_workspace_bytes, gc_index_correspondence, gc_posmap_bbox,
+               gc_sampler_reconstruct, gc_sampler_step_times, gc_schedule_anchors, gc_schedule_full_steps,
+               gc_schedule_refresh_due, gc_transport_reconstruct, gc_transport_reconstruct_geom, gc_transport_unipc,
+               gc_unipc_coeffs, gc_unipc_update)
 
 Predict = Callable[[int, List[int]], torch.Tensor]
 
@@ -42,10 +42,11 @@ class GeoCacheRunner:
         views that have not been anchors for max_gap cached steps (0: off)
         are forced into the set, longest gap first.  "rotation_coverage"
         takes, among the rotation's distinct sets, the one with the largest
-        weighted coverage (gc_coverage_score; ties to the earlier set).  refresh_tau makes a
-        step full when the fraction of foreground tokens stale for refresh_R
-        or more steps exceeds it.  geom computes the correspondence inside
-        each step instead of building and caching one per anchor set."""
+        weighted coverage (gc_coverage_score; ties to the earlier set).
+        refresh_tau makes a step full when the fraction of foreground tokens
+        stale for refresh_R or more steps exceeds it.  geom computes the
+        correspondence inside each step instead of building and caching one
+        per anchor set."""
         if anchor_policy not in ("rotate", "coverage", "rotation_coverage"):
             raise ValueError("anchor_policy must be 'rotate', 'coverage' or 'rotation_coverage'")
         if unipc_order and geom:
