@@ -357,6 +357,9 @@ def main():
     rows["coverage_per_anchor_set"] = [round(cover[A], 4) for A in anchor_sets]
     rows["visible_pairs_per_anchor_set"] = [vis_pairs[A] for A in anchor_sets]
     rows["visible_tokens_per_anchor_set"] = [index[A].n_vis for A in anchor_sets]
+    # target tokens by the number of anchors that see them (0 .. a), per anchor set
+    rows["n_vis_histogram_per_anchor_set"] = [
+        torch.bincount((ops[A][0] != 0).sum(-1).flatten(), minlength=a + 1).tolist() for A in anchor_sets]
 
     copy_gbps = None
     if args.copy_probe:
