@@ -480,9 +480,13 @@ def coverage_rows(gc, w, pos, cams, bbox, full, R=2):
     return out
 
 
+GRAPH_STEPS = 24   # cached steps captured per graph (rounded up to whole rotations)
+
+
 def config_row(gc, synth, name, steps=300):
     """One cached step of another workload, launched eagerly and replayed
-    from a HIP graph: microseconds per step each way, transported
+    from a HIP graph holding a run of consecutive steps (one per anchor set
+    of the rotation, repeated): microseconds per step each way, transported
     view-pixels/s and algorithmic GB/s at the faster of the two.  These
     working sets fit in the 256 MB last-level cache, so their GB/s is not an
     HBM figure; the smaller ones are launch-bound."""
@@ -541,10 +545,14 @@ def config_row(gc, synth, name, steps=300):
         for c in calls:
             c(t, tn)
     eager_ms = timed(eager, reps) / len(calls)
+    # A captured denoising loop holds many consecutive steps; a graph of one
+    # step per replay would time the replay call's own host overhead instead.
+    rounds = -(-GRAPH_STEPS // len(calls))
     graph = torch.cuda.CUDAGraph()
     with torch.cuda.graph(graph, stream=s):
-        eager()
-    graph_ms = timed(graph.replay, reps) / len(calls)
+        for _ in range(rounds):
+            eager()
+    graph_ms = timed(graph.replay, max(1, reps // rounds)) / (len(calls) * rounds)
     V = n_tok
     best = min(eager_ms, graph_ms)
     return {"view_pixels_per_step": V, "eager_us_per_step": eager_ms * 1e3, "graph_us_per_step": graph_ms * 1e3,

@@ -36,6 +36,7 @@ namespace gc {
 namespace {
 
 constexpr int kBlock = 256;
+static_assert(GC_MAX_VIEWS <= 256 && GC_MAX_ANCHORS <= 8, "view_bytes holds one byte per anchor slot");
 
 enum GeomMode { kGeomTransport = 0, kGeomReconstruct = 1 };
 
@@ -59,6 +60,7 @@ struct GArgs {
   int n_ablocks;    // B * a * bpv_a
   int32_t anchor_view[GC_MAX_ANCHORS];     // view of anchor slot s
   int32_t sorted_anchor[GC_MAX_ANCHORS];   // anchor views ascending, padded with INT_MAX
+  uint64_t view_bytes;                     // byte s: view of anchor slot s
   Recon r;
 };
 
@@ -117,44 +119,61 @@ __global__ __launch_bounds__(kBlock) void k_transport_geom(GArgs g) {
   const int p = (lb - bt * g.bpv_t) * kTok + (int)threadIdx.x / G;
   const bool tok_ok = p < g.HW;
 
-  // target token: lane j of the group evaluates anchor slots j, j + G, ...
-  __shared__ int32_t view_lds[GC_MAX_ANCHORS];   // anchor views in LDS: a per-lane index into the kernel
-                                                  // arguments would be a memory load ordered after the taps
-  if (threadIdx.x < g.a) {
-    view_lds[threadIdx.x] = g.anchor_view[threadIdx.x];
-    cam_lds[threadIdx.x] = g.cams[(int64_t)b * g.N + g.anchor_view[threadIdx.x]];
-  }
-  __syncthreads();
+  // the token's position is loaded first, so its latency overlaps the
+  // camera setup and its barrier
   float P[3] = {0.f, 0.f, 0.f};
-  bool fg = false;
   if (tok_ok) {
     const float* pp = g.pos + ((int64_t)bv * g.HW + p) * 3;
     P[0] = pp[0];
     P[1] = pp[1];
     P[2] = pp[2];
-    fg = finite_f(P[0]) && finite_f(P[1]) && finite_f(P[2]);
   }
+  // target token: lane j of the group evaluates anchor slots j, j + G, ...
+  __shared__ int32_t view_lds[GC_MAX_ANCHORS];   // anchor views in LDS: a per-lane index into the kernel
+                                                  // arguments would be a memory load ordered after the taps
+  if (threadIdx.x < g.a) {
+    // the slot's view by a shift of a scalar argument: indexing anchor_view
+    // per lane would be a memory load in front of the camera load
+    const int u = (int)((g.view_bytes >> (8 * threadIdx.x)) & 0xffu);
+    view_lds[threadIdx.x] = u;
+    cam_lds[threadIdx.x] = g.cams[(int64_t)b * g.N + u];
+  }
+  __syncthreads();
+  const bool fg = tok_ok && finite_f(P[0]) && finite_f(P[1]) && finite_f(P[2]);
   // all of the lane's slots are projected first and all their tap loads are
   // issued together (a lane without a slot, or a background token, loads the
-  // grid's corner taps of slot 0's map and ignores them)
+  // grid's corner taps of slot 0's map and ignores them); a wave in which no
+  // projection succeeded (all background, mostly) skips the loads
   AnchorProj pj[kApl];
-  TapPos tp[kApl];
   AnchorTaps at[kApl];
+  bool any_ok = false;
 #pragma unroll
   for (int j = 0; j < kApl; ++j) {   // branch-free: a lane without the slot keeps the result unused
     const int s = j * G + lane_g;
     pj[j] = anchor_project(P, cam_lds[s < g.a ? s : 0], g.H, g.W);
     pj[j].ok = pj[j].ok && tok_ok && fg && s < g.a;
+    any_ok = any_ok || pj[j].ok;
   }
+  if (__ballot(any_ok)) {
+    TapPos tp[kApl];
 #pragma unroll
-  for (int j = 0; j < kApl; ++j) {
-    const int s = j * G + lane_g;
-    const int sc = s < g.a ? s : 0;
-    tp[j] = anchor_tap_positions(pj[j], g.pos + ((int64_t)b * g.N + view_lds[sc]) * g.HW * 3, g.H, g.W);
+    for (int j = 0; j < kApl; ++j) {
+      const int s = j * G + lane_g;
+      const int sc = s < g.a ? s : 0;
+      tp[j] = anchor_tap_positions(pj[j], g.pos + ((int64_t)b * g.N + view_lds[sc]) * g.HW * 3, g.H, g.W);
+    }
+    const float tol2 = g.bbox[(int64_t)b * 8 + 6];
+#pragma unroll
+    for (int j = 0; j < kApl; ++j) at[j] = anchor_select(P, pj[j], tp[j], g.H, g.W, g.K, tol2);
+  } else {
+#pragma unroll
+    for (int j = 0; j < kApl; ++j) {
+      at[j].word = 0;
+      at[j].mask = 0;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) at[j].wk[k] = 0.0f;
+    }
   }
-  const float tol2 = g.bbox[(int64_t)b * 8 + 6];
-#pragma unroll
-  for (int j = 0; j < kApl; ++j) at[j] = anchor_select(P, pj[j], tp[j], g.H, g.W, g.K, tol2);
   // n_vis: a ballot over the group (every lane reaches the ballots)
   const int gbase = __lane_id() & ~(G - 1);
   int n_vis = 0;
@@ -298,6 +317,7 @@ int prepare_geom(const void* x0_prev, const void* x0_new, const float* pos, cons
     if (is_anchor[u]) return fail(GC_ERR_ARG, "%s: anchor %d listed twice", who, u);
     is_anchor[u] = true;
     g->anchor_view[s] = u;
+    g->view_bytes |= (uint64_t)u << (8 * s);
   }
   const size_t es = (size_t)dtype_bytes(dtype);
   const size_t HW = (size_t)H * W;
