@@ -105,6 +105,9 @@ def main():
     cams_np = synth.batch_cameras(w)
     log(args, f"[bench] rendered {hi.shape} in {time.time() - t0:.1f}s")
     hi_d = torch.from_numpy(hi).to(dev)
+    # the oracle's baseline takes asset 0's render and computes everything
+    # else itself (nothing it reads comes from the HIP path)
+    hi0 = None if args.no_cpu_baseline else hi[:1].copy()
     del hi
     cams = gc.camera_tensor(cams_np, dev)
 
@@ -177,7 +180,14 @@ def main():
             gc.gc_build_correspondence(pos, cams, list(A), K, bbox, corr=ops[A][0], weights=ops[A][1], stats=stats[A])
     b1.record()
     torch.cuda.synchronize()
-    rows["build_ms_per_anchor_set"] = b0.elapsed_time(b1) / (10 * len(anchor_sets))
+    rows["build_ms_per_anchor_set"] = b0.elapsed_time(b1) / (10 * len(anchor_sets))   # with the counters
+    b0.record()
+    for _ in range(10):
+        for A in anchor_sets:
+            gc.gc_build_correspondence(pos, cams, list(A), K, bbox, corr=ops[A][0], weights=ops[A][1])
+    b1.record()
+    torch.cuda.synchronize()
+    rows["build_no_counters_ms_per_anchor_set"] = b0.elapsed_time(b1) / (10 * len(anchor_sets))
     rows["anchor_sets"] = len(anchor_sets)
     index = {}
     e4, e5 = ev(), ev()
@@ -186,7 +196,28 @@ def main():
         index[A] = gc.gc_index_correspondence(ops[A][0])
     e5.record()
     torch.cuda.synchronize()
-    rows["index_ms_per_anchor_set"] = e4.elapsed_time(e5) / len(anchor_sets)
+    # the binding allocates the index and reads the visible count back (one
+    # synchronisation); the device part alone: ten back-to-back launches per
+    # set into preallocated buffers
+    rows["index_with_readback_ms_per_anchor_set"] = e4.elapsed_time(e5) / len(anchor_sets)
+    corr0 = ops[anchor_sets[0]][0]
+    n_tok = corr0.numel() // corr0.shape[-1]
+    ws = torch.empty(int(gc.lib().gc_index_workspace_bytes(n_tok)), dtype=torch.uint8, device=dev)
+    bits_i = torch.empty((n_tok + 31) // 32, dtype=torch.int32, device=dev)
+    lst_i = torch.empty(n_tok, dtype=torch.int32, device=dev)
+    nv_i = torch.empty(1, dtype=torch.int32, device=dev)
+    torch.cuda.synchronize()
+    e4.record()
+    for _ in range(10):
+        for A in anchor_sets:
+            rc = gc.lib().gc_index_correspondence(ops[A][0].data_ptr(), n_tok, corr0.shape[-1], bits_i.data_ptr(),
+                                                  lst_i.data_ptr(), nv_i.data_ptr(), ws.data_ptr(), ws.numel(),
+                                                  torch.cuda.current_stream().cuda_stream)
+            assert rc == 0, gc.lib().gc_last_error()
+    e5.record()
+    torch.cuda.synchronize()
+    rows["index_device_ms_per_anchor_set"] = e4.elapsed_time(e5) / (10 * len(anchor_sets))
+    del ws, bits_i, lst_i, nv_i
     vis_pairs = {A: int(stats[A][:, 0].sum().item()) for A in anchor_sets}
     cover = {A: float(stats[A][:, 1].sum().item()) / max(1, float(stats[A][:, 2].sum().item())) for A in anchor_sets}
     del hi_d
@@ -375,7 +406,8 @@ def main():
     if not args.no_small:
         for name in synth.CONFIGS:
             if name != w.name:
-                rows[f"config_{name}"] = config_row(gc, synth, name)
+                rows[f"config_{name}"] = config_row(gc, synth, name,
+                                                    oracle_seconds=None if args.no_cpu_baseline else 1.0)
 
     # ---- coverage-driven schedule: staleness under each anchor policy --------
     if not args.no_coverage:
@@ -384,7 +416,7 @@ def main():
     # ---- CPU baseline: the oracle on one asset ------------------------------
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(w, pos[:1].cpu().numpy(), cams_np, x0_prev_np[:1], args.cpu_seconds)
+        cpu = cpu_baseline(w, hi0, cams_np, cached_steps[0] - 1, args.cpu_seconds)
 
     traffic = read_traffic(w.name)
     out = {
@@ -483,17 +515,20 @@ def coverage_rows(gc, w, pos, cams, bbox, full, R=2):
 GRAPH_STEPS = 24   # cached steps captured per graph (rounded up to whole rotations)
 
 
-def config_row(gc, synth, name, steps=300):
+def config_row(gc, synth, name, steps=300, oracle_seconds=None):
     """One cached step of another workload, launched eagerly and replayed
     from a HIP graph holding a run of consecutive steps (one per anchor set
     of the rotation, repeated): microseconds per step each way, transported
     view-pixels/s and algorithmic GB/s at the faster of the two.  These
     working sets fit in the 256 MB last-level cache, so their GB/s is not an
-    HBM figure; the smaller ones are launch-bound."""
+    HBM figure; the smaller ones are launch-bound.  With oracle_seconds, the
+    oracle's cached step on the same workload is timed beside it (one host
+    thread, from the seeded render on its own)."""
     import torch
     w = synth.CONFIGS[name]
     dev = torch.device("cuda:0")
-    hi = torch.from_numpy(synth.render_position_maps(w)).to(dev)
+    hi_np = synth.render_position_maps(w)
+    hi = torch.from_numpy(hi_np).to(dev)
     pos = gc.gc_posmap_downsample(hi, w.factor) if w.factor > 1 else hi
     cams = gc.camera_tensor(synth.batch_cameras(w), dev)
     bbox = gc.gc_posmap_bbox(pos, w.tol_frac)
@@ -555,19 +590,57 @@ def config_row(gc, synth, name, steps=300):
     graph_ms = timed(graph.replay, max(1, reps // rounds)) / (len(calls) * rounds)
     V = n_tok
     best = min(eager_ms, graph_ms)
-    return {"view_pixels_per_step": V, "eager_us_per_step": eager_ms * 1e3, "graph_us_per_step": graph_ms * 1e3,
-            "view_pixels_per_s": V / (best * 1e-3),
-            "algorithmic_GBps": sum(step_bytes) / len(step_bytes) / (best * 1e-3) / 1e9}
+    row = {"view_pixels_per_step": V, "eager_us_per_step": eager_ms * 1e3, "graph_us_per_step": graph_ms * 1e3,
+           "view_pixels_per_s": V / (best * 1e-3),
+           "algorithmic_GBps": sum(step_bytes) / len(step_bytes) / (best * 1e-3) / 1e9}
+    if oracle_seconds:
+        vps = oracle_step_rate(w, hi_np, oracle_seconds)
+        row["oracle_view_pixels_per_s"] = vps
+        row["gpu_over_oracle"] = row["view_pixels_per_s"] / vps
+    return row
 
 
-def cpu_baseline(w, pos1, cams_np, x0_prev1, seconds):
+def oracle_step_rate(w, hi_np, seconds):
+    """The oracle's cached step (transport + reconstruction) over all assets
+    of a workload, single-threaded, repeated for about `seconds` seconds:
+    transported view-pixels/s.  Every input is computed from the seeded
+    render by the oracle and the generators."""
+    import numpy as np
+
+    import oracle
+    import synth
+    A = list(w.fixed_anchors) if w.fixed_anchors else oracle.anchors(w.N, w.a, 0)
+    t, tn = w.ddim_single if w.ddim_single else oracle.step_times(w.sampler, w.S, 2)
+    pos = oracle.downsample(hi_np, w.factor) if w.factor > 1 else hi_np
+    cams = synth.batch_cameras(w)
+    corr, wts, _ = oracle.build(pos, cams, list(A), w.K, oracle.bbox(pos, w.tol_frac))
+    rs = np.random.default_rng(7)
+    prev = synth.storage(rs.standard_normal((w.B, w.N, w.H, w.W, w.C)).astype(np.float32), w.dtype)
+    new = synth.storage(rs.standard_normal((w.B, len(A), w.H, w.W, w.C)).astype(np.float32), w.dtype)
+    xt = synth.storage(rs.standard_normal((w.B, w.N, w.H, w.W, w.C)).astype(np.float32), w.dtype)
+    reps = 0
+    t0 = time.perf_counter()
+    while True:
+        _, st = oracle.transport(prev, new, corr, wts, list(A), w.dtype)
+        oracle.reconstruct(xt, st, w.dtype, w.sampler, t, tn)
+        reps += 1
+        el = time.perf_counter() - t0
+        if el >= seconds:
+            break
+    return reps * w.B * (w.N - len(A)) * w.H * w.W / el
+
+
+def cpu_baseline(w, hi0, cams_np, step, seconds):
     """The oracle's cached step (transport + reconstruction) on one asset,
-    single-threaded, repeated for about `seconds` seconds."""
+    single-threaded, repeated for about `seconds` seconds.  hi0: asset 0's
+    render-resolution position maps; the oracle downsamples them itself."""
     import numpy as np
 
     import oracle
     import synth
 
+    pos1 = oracle.downsample(hi0, w.factor) if w.factor > 1 else hi0
+    x0_prev1 = synth.x0_state(w, pos1, step)
     cams1 = {k: v[:1] for k, v in cams_np.items()}
     A = oracle.anchors(w.N, w.a, 0)
     bb = oracle.bbox(pos1, w.tol_frac)
