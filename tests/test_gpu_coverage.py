@@ -80,7 +80,7 @@ def test_update_sequence_bit_exact(gc, key):
     w, P = workload(key)
     Pd, cams, bb = device_inputs(gc, w, P)
     bits = gc.gc_coverage_pairs(Pd, cams, bb)
-    seen = unpack_pairs(bits, w.H, w.W)
+    seen = oracle.coverage_pairs(P, synth.batch_cameras(w), w.K, oracle.bbox(P, w.tol_frac))   # the oracle's own
     stale = gc.gc_coverage_init(Pd)
     st_o = oracle.coverage_init(P)
     np.testing.assert_array_equal(stale.cpu().numpy(), st_o)
@@ -106,7 +106,7 @@ def test_select_and_score_match_oracle(gc, key):
     w, P = workload(key)
     Pd, cams, bb = device_inputs(gc, w, P)
     bits = gc.gc_coverage_pairs(Pd, cams, bb)
-    seen = unpack_pairs(bits, w.H, w.W)
+    seen = oracle.coverage_pairs(P, synth.batch_cameras(w), w.K, oracle.bbox(P, w.tol_frac))   # the oracle's own
     rs = np.random.default_rng(7)
     ws = torch.empty(gc.gc_coverage_workspace_bytes(), dtype=torch.uint8, device=DEV)
     for trial in range(4):
