@@ -12,6 +12,7 @@
  *                        gc_posmap_bbox         per-asset bbox and squared tolerance
  *                        gc_build_correspondence   G_{A->v} for one anchor set
  *                        gc_index_correspondence   visible-token index of G_{A->v}
+ *                        gc_index_foreground       foreground-token index of the position maps
  *   every cached step    gc_transport_step      Eq. 1: x0(v) = x0_prev(v) + G[dx0(A)]
  *                        gc_sampler_reconstruct sampler-consistent eps / v / velocity + x_t update
  *                        gc_transport_reconstruct  the two above fused in one pass
@@ -62,7 +63,7 @@
 extern "C" {
 #endif
 
-#define GC_ABI_VERSION 1
+#define GC_ABI_VERSION 2
 
 /* limits */
 #define GC_MAX_VIEWS 64     /* views per asset */
@@ -228,6 +229,29 @@ int gc_index_correspondence(const int32_t* corr, int64_t n_tokens, int a, uint32
                             int32_t* n_vis, void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 /*
+ * Foreground index of latent-grid position maps (once per asset batch; it
+ * does not depend on the anchor set).  Only a token with a finite position
+ * can pass the operator's tolerance test (Sec. 3.2: the test compares 3D
+ * points), so the on-the-fly step (gc_transport_*_geom) can evaluate the
+ * operator for the listed tokens only and stream every other one.
+ *   pos        device float32 [n_tokens][3], n_tokens = B * N * H * W (at
+ *              most 2^31 - 1); a token is foreground iff its three
+ *              components are finite
+ *   fg_bits    device uint32 [ceil(n_tokens / 32)] output: bit (i & 31) of
+ *              word i >> 5 is set iff token i is foreground
+ *   fg_recs    device int32 [n_tokens][4] output (capacity): the first *n_fg
+ *              records are {i, x, y, z} for the foreground tokens i in
+ *              ascending order, x, y, z being the position's float bit patterns
+ *   n_fg       device int32 [1] output
+ *   workspace  device scratch of at least gc_index_workspace_bytes(n_tokens)
+ *              bytes, as for gc_index_correspondence
+ * All pointers 16-byte aligned; outputs must not overlap pos or each other.
+ * The result is deterministic.  n_tokens = 0 is legal (n_fg = 0).
+ */
+int gc_index_foreground(const float* pos, int64_t n_tokens, uint32_t* fg_bits, int32_t* fg_recs, int32_t* n_fg,
+                        void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
  * Delta transport, Eq. 1 (Sec. 3.2, delta transport and loop order), for one
  * cached step:
  *   anchor view u = anchors[s]:  x0_out(u) = x0_anchor_new(s)          (copy)
@@ -365,18 +389,29 @@ int gc_transport_unipc(const void* x0_prev, const void* x0_anchor_new, const int
  *   pos    device float32 [B][N][H][W][3] latent-grid position maps (NaN = background)
  *   cams   device gc_camera [B][N]
  *   bbox   device float32 [B][8] from gc_posmap_bbox (element 6 = squared tolerance)
+ *   fg_bits, fg_recs, n_fg
+ *          optional foreground index of pos from gc_index_foreground (n_fg
+ *          read back to the host); fg_bits and fg_recs null and n_fg 0 for the
+ *          blocked launch.  With the index, only the listed tokens of the
+ *          target views run the operator and every other token is streamed;
+ *          the result is bit-identical either way.  A record whose token lies
+ *          outside [0, B*N*H*W) is ignored.  The index is used when B * a <= 64
+ *          (the launch stages every (asset, anchor) camera); otherwise the
+ *          blocked launch runs.
  * Other arguments as for gc_transport_step / gc_transport_reconstruct.
  * x0_out, x_next and model_out must not overlap any input (x_next may be
- * x_t); latents and pos 16-byte aligned.
+ * x_t); latents, pos, fg_bits and fg_recs 16-byte aligned.
  */
 int gc_transport_step_geom(const void* x0_prev, const void* x0_anchor_new, const float* pos, const gc_camera* cams,
-                           const float* bbox, int B, int N, int H, int W, int C, const int32_t* anchors, int a, int K,
-                           int dtype, void* x0_out, hipStream_t stream);
+                           const float* bbox, const uint32_t* fg_bits, const int32_t* fg_recs, int64_t n_fg, int B,
+                           int N, int H, int W, int C, const int32_t* anchors, int a, int K, int dtype, void* x0_out,
+                           hipStream_t stream);
 int gc_transport_reconstruct_geom(const void* x0_prev, const void* x0_anchor_new, const float* pos,
-                                  const gc_camera* cams, const float* bbox, const void* x_t, int B, int N, int H,
-                                  int W, int C, const int32_t* anchors, int a, int K, int dtype,
-                                  const gc_sampler* smp, double t, double t_next, void* x0_out, void* x_next,
-                                  void* model_out, hipStream_t stream);
+                                  const gc_camera* cams, const float* bbox, const uint32_t* fg_bits,
+                                  const int32_t* fg_recs, int64_t n_fg, const void* x_t, int B, int N, int H, int W,
+                                  int C, const int32_t* anchors, int a, int K, int dtype, const gc_sampler* smp,
+                                  double t, double t_next, void* x0_out, void* x_next, void* model_out,
+                                  hipStream_t stream);
 
 /*
  * Token staleness and the coverage-driven schedule.

@@ -21,6 +21,7 @@ import torch
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libgeocache.so")
+ABI_VERSION = 2   # GC_ABI_VERSION the binding is written for
 
 # constants mirrored from include/geocache.h
 GC_OK = 0
@@ -94,6 +95,7 @@ def lib() -> ctypes.CDLL:
             "gc_build_correspondence": ([_vp, _vp, _i, _i, _i, _i, _i32p, _i, _i, _vp, _vp, _vp, _vp, _vp], _i),
             "gc_index_workspace_bytes": ([_i64], ctypes.c_size_t),
             "gc_index_correspondence": ([_vp, _i64, _i, _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp], _i),
+            "gc_index_foreground": ([_vp, _i64, _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp], _i),
             "gc_transport_step": ([_vp, _vp, _vp, _vp, _vp, _vp, _i64, _i, _i, _i, _i, _i, _i32p, _i, _i, _i, _vp,
                                    _vp], _i),
             "gc_sampler_reconstruct": ([_vp, _vp, _vp, _vp, _i64, _i, ctypes.POINTER(_Sampler), ctypes.c_double,
@@ -105,11 +107,11 @@ def lib() -> ctypes.CDLL:
             "gc_unipc_update": ([_vp, _vp, _vp, _vp, _vp, _i64, _i, ctypes.POINTER(UniPCStep), _vp, _vp, _vp], _i),
             "gc_transport_unipc": ([_vp, _vp, _vp, _vp, _vp, _vp, _i64, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i32p,
                                     _i, _i, _i, ctypes.POINTER(UniPCStep), _vp, _vp, _vp, _vp], _i),
-            "gc_transport_step_geom": ([_vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i32p, _i, _i, _i, _vp, _vp],
-                                       _i),
-            "gc_transport_reconstruct_geom": ([_vp, _vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i32p, _i, _i, _i,
-                                               ctypes.POINTER(_Sampler), ctypes.c_double, ctypes.c_double, _vp, _vp,
-                                               _vp, _vp], _i),
+            "gc_transport_step_geom": ([_vp, _vp, _vp, _vp, _vp, _vp, _vp, _i64, _i, _i, _i, _i, _i, _i32p, _i, _i,
+                                        _i, _vp, _vp], _i),
+            "gc_transport_reconstruct_geom": ([_vp, _vp, _vp, _vp, _vp, _vp, _vp, _i64, _vp, _i, _i, _i, _i, _i,
+                                               _i32p, _i, _i, _i, ctypes.POINTER(_Sampler), ctypes.c_double,
+                                               ctypes.c_double, _vp, _vp, _vp, _vp], _i),
             "gc_coverage_pair_words": ([_i, _i, _i, _i], _i64),
             "gc_coverage_pairs": ([_vp, _vp, _vp, _i, _i, _i, _i, _vp, _vp], _i),
             "gc_coverage_init": ([_vp, _i, _i, _i, _i, _vp, _vp], _i),
@@ -128,8 +130,8 @@ def lib() -> ctypes.CDLL:
             f = getattr(L, name)
             f.argtypes = args
             f.restype = res
-        if L.gc_abi_version() != 1:
-            raise ImportError(f"libgeocache ABI {L.gc_abi_version()} != 1")
+        if L.gc_abi_version() != ABI_VERSION:
+            raise ImportError(f"libgeocache ABI {L.gc_abi_version()} != {ABI_VERSION}")
         _LIB = L
     return _LIB
 
@@ -281,6 +283,45 @@ def gc_index_correspondence(corr: torch.Tensor, workspace: torch.Tensor = None, 
     return VisibleIndex(bits, lst, int(nv.item()))
 
 
+@dataclass
+class ForegroundIndex:
+    """Output of gc_index_foreground: fg_bits (int32 view of the uint32
+    words), fg_recs (int32 [capacity, 4] records {token, x, y, z}) and the
+    host count n_fg."""
+    fg_bits: torch.Tensor
+    fg_recs: torch.Tensor
+    n_fg: int
+
+
+def gc_index_foreground(pos: torch.Tensor, workspace: torch.Tensor = None, stream=None) -> ForegroundIndex:
+    """Foreground index of position maps (float32 [..., 3], e.g. [B, N, H, W, 3]),
+    once per asset batch.  Reads the foreground count back to the host (one
+    synchronisation)."""
+    if pos.dtype != torch.float32 or pos.dim() < 1 or pos.shape[-1] != 3:
+        raise ValueError("pos must be float32 [..., 3]")
+    n_tok = int(pos.numel() // 3)
+    dev = pos.device
+    need = int(lib().gc_index_workspace_bytes(n_tok))
+    if workspace is None:
+        workspace = torch.empty(need, dtype=torch.uint8, device=dev)
+    if workspace.numel() * workspace.element_size() < need:
+        raise ValueError(f"workspace must hold at least {need} bytes")
+    bits = torch.empty(max(1, (n_tok + 31) // 32), dtype=torch.int32, device=dev)
+    recs = torch.empty((max(1, n_tok), 4), dtype=torch.int32, device=dev)
+    nf = torch.empty(1, dtype=torch.int32, device=dev)
+    _check(lib().gc_index_foreground(_dev(pos, "pos") if n_tok else None, n_tok, _dev(bits, "fg_bits"),
+                                     _dev(recs, "fg_recs"), _dev(nf, "n_fg"), _dev(workspace, "workspace"),
+                                     workspace.numel() * workspace.element_size(), _stream(stream)),
+           "gc_index_foreground")
+    return ForegroundIndex(bits, recs, int(nf.item()))
+
+
+def _fg_args(fg_index: Optional[ForegroundIndex]):
+    if fg_index is None:
+        return None, None, 0
+    return _dev(fg_index.fg_bits, "fg_bits"), _dev(fg_index.fg_recs, "fg_recs"), int(fg_index.n_fg)
+
+
 def _index_args(index: Optional[VisibleIndex]):
     if index is None:
         return None, None, 0
@@ -377,16 +418,19 @@ def _geom_inputs(x0_prev, x0_anchor_new, pos, cams, bbox, anchors):
 
 def gc_transport_step_geom(x0_prev: torch.Tensor, x0_anchor_new: torch.Tensor, pos: torch.Tensor,
                            cams: torch.Tensor, bbox: torch.Tensor, anchors: Sequence[int], K: int,
-                           x0_out: torch.Tensor = None, stream=None) -> torch.Tensor:
+                           x0_out: torch.Tensor = None, fg_index: ForegroundIndex = None, stream=None) -> torch.Tensor:
     """Eq. 1 with G_{A->v} computed on the fly from the position maps
     (pos float32 [B, N, H, W, 3], cams from camera_tensor, bbox from
-    gc_posmap_bbox); equals gc_build_correspondence + gc_transport_step."""
+    gc_posmap_bbox); equals gc_build_correspondence + gc_transport_step.
+    `fg_index` (gc_index_foreground of pos) selects the foreground launch."""
     (B, N, H, W, C), arr, a = _geom_inputs(x0_prev, x0_anchor_new, pos, cams, bbox, anchors)
     if x0_out is None:
         x0_out = torch.empty_like(x0_prev)
+    fb, fr, nf = _fg_args(fg_index)
     _check(lib().gc_transport_step_geom(_dev(x0_prev, "x0_prev"), _dev(x0_anchor_new, "x0_anchor_new"),
-                                        _dev(pos, "pos"), _dev(cams, "cams"), _dev(bbox, "bbox"), B, N, H, W, C, arr,
-                                        a, K, dtype_code(x0_prev), _dev(x0_out, "x0_out"), _stream(stream)),
+                                        _dev(pos, "pos"), _dev(cams, "cams"), _dev(bbox, "bbox"), fb, fr, nf, B, N, H,
+                                        W, C, arr, a, K, dtype_code(x0_prev), _dev(x0_out, "x0_out"),
+                                        _stream(stream)),
            "gc_transport_step_geom")
     return x0_out
 
@@ -394,9 +438,11 @@ def gc_transport_step_geom(x0_prev: torch.Tensor, x0_anchor_new: torch.Tensor, p
 def gc_transport_reconstruct_geom(x0_prev: torch.Tensor, x0_anchor_new: torch.Tensor, pos: torch.Tensor,
                                   cams: torch.Tensor, bbox: torch.Tensor, x_t: torch.Tensor, anchors: Sequence[int],
                                   K: int, sampler: Sampler, t: float, t_next: float, x0_out: torch.Tensor = None,
-                                  x_next: torch.Tensor = None, model_out: torch.Tensor = None, stream=None):
+                                  x_next: torch.Tensor = None, model_out: torch.Tensor = None,
+                                  fg_index: ForegroundIndex = None, stream=None):
     """gc_transport_reconstruct with G_{A->v} computed on the fly; returns
-    (x0_out, x_next, model_out or None)."""
+    (x0_out, x_next, model_out or None).  `fg_index` (gc_index_foreground of
+    pos) selects the foreground launch."""
     (B, N, H, W, C), arr, a = _geom_inputs(x0_prev, x0_anchor_new, pos, cams, bbox, anchors)
     if x_t.shape != x0_prev.shape or x_t.dtype != x0_prev.dtype:
         raise ValueError("x_t must match x0_prev in shape and dtype")
@@ -407,8 +453,9 @@ def gc_transport_reconstruct_geom(x0_prev: torch.Tensor, x0_anchor_new: torch.Te
     if sampler.pred_out != GC_PRED_NONE and model_out is None:
         model_out = torch.empty_like(x_t)
     smp = sampler.c()
+    fb, fr, nf = _fg_args(fg_index)
     _check(lib().gc_transport_reconstruct_geom(_dev(x0_prev, "x0_prev"), _dev(x0_anchor_new, "x0_anchor_new"),
-                                               _dev(pos, "pos"), _dev(cams, "cams"), _dev(bbox, "bbox"),
+                                               _dev(pos, "pos"), _dev(cams, "cams"), _dev(bbox, "bbox"), fb, fr, nf,
                                                _dev(x_t, "x_t"), B, N, H, W, C, arr, a, K, dtype_code(x0_prev),
                                                ctypes.byref(smp), float(t), float(t_next), _dev(x0_out, "x0_out"),
                                                _dev(x_next, "x_next"), _opt(model_out, "model_out"),

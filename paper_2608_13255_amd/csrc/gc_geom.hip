@@ -21,13 +21,25 @@
 // with the builder's stored weights (w_k / n_vis in float), so the result
 // equals gc_build_correspondence followed by gc_transport_step bit for bit.
 //
-// Split launch: the target-view blocks, whose dependent loads (position,
-// the anchors' position taps, then the latent taps) set the pace, come
-// first; the anchor rows, which only copy the new prediction and stream the
-// sampler step, follow as dense blocks of one lane per channel vector and
-// fill the machine while the last target blocks finish.  Each part is dealt
-// to the XCDs in contiguous slices, so an XCD gathers from few assets'
-// anchor views, and blocks never straddle a view.
+// Blocked launch (no foreground index): the target-view blocks, whose
+// dependent loads (position, the anchors' position taps, then the latent
+// taps) set the pace, come first; the anchor rows, which only copy the new
+// prediction and stream the sampler step, follow as dense blocks of one lane
+// per channel vector and fill the machine while the last target blocks
+// finish.  Each part is dealt to the XCDs in contiguous slices, so an XCD
+// gathers from few assets' anchor views, and blocks never straddle a view.
+//
+// Foreground launch (with gc_index_foreground's index of the position
+// maps): only a token with a finite position can be seen by an anchor, so
+// the geometry runs in blocks over the compact list of foreground tokens,
+// whose records carry each token's position (one 16-byte load gives a lane
+// both), while every other token -- the background of the target views and
+// all of the anchor rows -- is streamed by blocks in the hardware's
+// round-robin order that skip the listed target tokens by their bit.  The
+// list covers all views; a record of an anchor view is skipped.  A block of
+// the list may straddle views and assets, so it stages the cameras of every
+// (asset, anchor slot) in LDS (B * a <= kMaxCamLds; beyond that the blocked
+// launch runs, with the same result).
 #include "gc_common.h"
 #include "gc_geometry.h"
 #include "gc_latent.h"
@@ -62,7 +74,17 @@ struct GArgs {
   int32_t sorted_anchor[GC_MAX_ANCHORS];   // anchor views ascending, padded with INT_MAX
   uint64_t view_bytes;                     // byte s: view of anchor slot s
   Recon r;
+  // foreground launch
+  const uint32_t* fg_bits;   // bit per token of [B][N][H][W]: finite position
+  const int4* fg_recs;       // [n_fg] {token, x, y, z}, ascending token
+  int n_fg;
+  int B;
+  int gblocks;               // list blocks in front of the streaming blocks (multiple of kXcds)
+  int bpv_s;                 // streaming blocks per view: ceil(HW * CV / kBlock)
+  int n_sblocks;             // B * N * bpv_s
 };
+
+constexpr int kMaxCamLds = 64;   // (asset, anchor slot) cameras a list block can stage
 
 // G lanes per target token; AMAX (4 or 8) bounds the anchor count, so each
 // lane evaluates up to AMAX / G anchor slots.
@@ -288,13 +310,242 @@ __global__ __launch_bounds__(kBlock) void k_transport_geom(GArgs g) {
   }
 }
 
+// Stores a token's channel vector: x0 as given and, when reconstructing, the
+// sampler step from x_t and that x0 as stored.
+template <int DT, int VEC, int MODE>
+__device__ __forceinline__ void finish_item(const GArgs& g, int64_t e, const typename Codec<DT, VEC>::Raw& x0r,
+                                            const typename Codec<DT, VEC>::Raw& xtr) {
+  using CD = Codec<DT, VEC>;
+  CD::store_stream(g.x0_out, e, x0r);
+  if constexpr (MODE == kGeomReconstruct) {
+    float xtf[VEC], x0f[VEC], xn[VEC], mo[VEC];
+    CD::unpack(x0r, x0f);   // the reconstruction reads x0 as stored
+    CD::unpack(xtr, xtf);
+    reconstruct_vec<VEC>(g.r, xtf, x0f, xn, mo);
+    CD::store_stream(g.x_next, e, CD::pack(xn));
+    if (g.model_out) CD::store_stream(g.model_out, e, CD::pack(mo));
+  }
+}
+
+// Foreground launch: g.gblocks list blocks (G lanes per listed token), then
+// g.n_sblocks streaming blocks (one lane per token and channel vector).
+template <int DT, int VEC, int MODE, int G, int AMAX>
+__global__ __launch_bounds__(kBlock) void k_transport_geom_fg(GArgs g) {
+  using CD = Codec<DT, VEC>;
+  using Raw = typename CD::Raw;
+  constexpr int kTok = kBlock / G;   // listed tokens per block
+  constexpr int kApl = AMAX / G;     // anchor slots per lane
+  static_assert(kApl >= 1 && kApl * G == AMAX, "G must divide AMAX");
+  const int i = (int)blockIdx.x;
+  if (i >= g.gblocks) {
+    // streaming: anchor rows take the new prediction; a target token that is
+    // listed belongs to a list block; any other keeps its own state
+    const int lb = i - g.gblocks;
+    if (lb >= g.n_sblocks) return;
+    const int bv = __builtin_amdgcn_readfirstlane(lb / g.bpv_s);   // b * N + v
+    const int t = (lb - bv * g.bpv_s) * kBlock + (int)threadIdx.x;
+    if (t >= g.HW * g.CV) return;
+    const int b = __builtin_amdgcn_readfirstlane(bv / g.N);
+    const int v = bv - b * g.N;
+    int s_self = -1;
+#pragma unroll
+    for (int s = 0; s < GC_MAX_ANCHORS; ++s) s_self = s < g.a && g.anchor_view[s] == v ? s : s_self;
+    int p, c;
+    if (g.cv_shift >= 0) {
+      p = t >> g.cv_shift;
+      c = t & (g.CV - 1);
+    } else {
+      p = t / g.CV;
+      c = t - p * g.CV;
+    }
+    const int64_t e = ((int64_t)bv * g.HW + p) * g.C + (int64_t)c * VEC;
+    Raw xtr{};
+    if (s_self >= 0) {
+      if constexpr (MODE == kGeomReconstruct) xtr = CD::load_stream(g.x_t, e);
+      const Raw x0r = CD::load(g.x0_new, (((int64_t)b * g.a + s_self) * g.HW + p) * g.C + (int64_t)c * VEC);
+      finish_item<DT, VEC, MODE>(g, e, x0r, xtr);
+      return;
+    }
+    const int64_t tk = (int64_t)bv * g.HW + p;
+    if ((g.fg_bits[tk >> 5] >> (tk & 31)) & 1u) return;
+    if constexpr (MODE == kGeomReconstruct) xtr = CD::load_stream(g.x_t, e);
+    finish_item<DT, VEC, MODE>(g, e, CD::load_stream(g.x0_prev, e), xtr);
+    return;
+  }
+
+  // list block: an XCD-contiguous slice of the foreground list
+  const int per = g.gblocks / kXcds;
+  const int lb = (i % kXcds) * per + i / kXcds;
+  const int lane_g = (int)threadIdx.x & (G - 1);
+  const int r = lb * kTok + (int)threadIdx.x / G;
+  const int64_t n_all = (int64_t)g.B * g.N * g.HW;
+  int4 rec = make_int4(-1, 0, 0, 0);
+  if (r < g.n_fg) rec = g.fg_recs[r];   // loaded first: its latency overlaps the camera setup
+  __shared__ gc_camera cam_lds[kMaxCamLds];     // camera of (asset b, anchor slot s) at b * a + s
+  __shared__ int32_t view_lds[GC_MAX_ANCHORS];  // anchor views (a per-lane index into the arguments is a load)
+  for (int q = (int)threadIdx.x; q < g.B * g.a; q += kBlock) {
+    const int bb = q / g.a, s = q - bb * g.a;
+    cam_lds[q] = g.cams[(int64_t)bb * g.N + (int)((g.view_bytes >> (8 * s)) & 0xffu)];
+  }
+  if (threadIdx.x < g.a) view_lds[threadIdx.x] = (int)((g.view_bytes >> (8 * threadIdx.x)) & 0xffu);
+  __syncthreads();
+  // records come from the caller: a token outside the maps is ignored
+  const int tokg = rec.x >= 0 && (int64_t)rec.x < n_all ? rec.x : -1;
+  const int bv = tokg >= 0 ? tokg / g.HW : 0;
+  const int b = bv / g.N;
+  const int v = bv - b * g.N;
+  bool anchor_row = false;
+#pragma unroll
+  for (int s = 0; s < GC_MAX_ANCHORS; ++s) anchor_row = anchor_row || (s < g.a && g.anchor_view[s] == v);
+  const bool tok_ok = tokg >= 0 && !anchor_row;   // a target token of the list
+  const float P[3] = {__int_as_float(rec.y), __int_as_float(rec.z), __int_as_float(rec.w)};
+  const bool fg = tok_ok && finite_f(P[0]) && finite_f(P[1]) && finite_f(P[2]);
+
+  // the operator, as in the blocked launch: lane j of the group evaluates
+  // anchor slots j, j + G, ...; a wave in which no projection succeeded skips
+  // the tap loads
+  AnchorProj pj[kApl];
+  AnchorTaps at[kApl];
+  bool any_ok = false;
+#pragma unroll
+  for (int j = 0; j < kApl; ++j) {   // branch-free: a lane without the slot keeps the result unused
+    const int s = j * G + lane_g;
+    pj[j] = anchor_project(P, cam_lds[b * g.a + (s < g.a ? s : 0)], g.H, g.W);
+    pj[j].ok = pj[j].ok && fg && s < g.a;
+    any_ok = any_ok || pj[j].ok;
+  }
+  if (__ballot(any_ok)) {
+    TapPos tp[kApl];
+#pragma unroll
+    for (int j = 0; j < kApl; ++j) {
+      const int s = j * G + lane_g;
+      const int sc = s < g.a ? s : 0;
+      tp[j] = anchor_tap_positions(pj[j], g.pos + ((int64_t)b * g.N + view_lds[sc]) * g.HW * 3, g.H, g.W);
+    }
+    const float tol2 = g.bbox[(int64_t)b * 8 + 6];
+#pragma unroll
+    for (int j = 0; j < kApl; ++j) at[j] = anchor_select(P, pj[j], tp[j], g.H, g.W, g.K, tol2);
+  } else {
+#pragma unroll
+    for (int j = 0; j < kApl; ++j) {
+      at[j].word = 0;
+      at[j].mask = 0;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) at[j].wk[k] = 0.0f;
+    }
+  }
+  const int gbase = __lane_id() & ~(G - 1);
+  int n_vis = 0;
+#pragma unroll
+  for (int j = 0; j < kApl; ++j) n_vis += __popcll((__ballot(at[j].word != 0) >> gbase) & ((1ull << G) - 1));
+
+  // the block's visible tokens first, then its other listed target tokens;
+  // one (token, channel vector) item per lane in that order
+  __shared__ int32_t s_tok[kTok];
+  __shared__ int32_t s_nvis[kTok];
+  __shared__ int32_t s_word[kTok][AMAX + 1];       // +1: no bank conflicts between consecutive tokens
+  __shared__ float s_wk[kTok][AMAX * 4 + 1];
+  __shared__ int32_t s_count[kBlock / 64][2];      // per wave: visible tokens, listed target tokens
+  const bool vis = tok_ok && n_vis > 0;
+  const bool lead = lane_g == 0;
+  const unsigned long long bvis = __ballot(lead && vis);
+  const unsigned long long blive = __ballot(lead && tok_ok);
+  const int wv = (int)threadIdx.x / 64;
+  if (__lane_id() == 0) {
+    s_count[wv][0] = __popcll(bvis);
+    s_count[wv][1] = __popcll(blive);
+  }
+  __syncthreads();
+  int off_v = 0, off_l = 0, nv = 0, nl = 0;
+#pragma unroll
+  for (int q = 0; q < kBlock / 64; ++q) {
+    const int cv_ = s_count[q][0], cl_ = s_count[q][1];
+    off_v += q < wv ? cv_ : 0;
+    off_l += q < wv ? cl_ : 0;
+    nv += cv_;
+    nl += cl_;
+  }
+  if (tok_ok) {
+    const unsigned long long below = (1ull << gbase) - 1;   // the groups before this one in the wave
+    const int rv = off_v + __popcll(bvis & below);
+    const int rl = off_l + __popcll(blive & below);
+    if (lead) s_tok[vis ? rv : nv + (rl - rv)] = tokg;
+    if (vis) {
+#pragma unroll
+      for (int j = 0; j < kApl; ++j) {
+        const int s = j * G + lane_g;
+        if (s < g.a) {
+          s_word[rv][s] = at[j].word;
+#pragma unroll
+          for (int k = 0; k < 4; ++k) s_wk[rv][s * 4 + k] = at[j].wk[k];
+        }
+      }
+      if (lead) s_nvis[rv] = n_vis;
+    }
+  }
+  __syncthreads();
+
+  const int n_items = nl * g.CV;
+  for (int it = (int)threadIdx.x; it < n_items; it += kBlock) {
+    int slot, c;
+    if (g.cv_shift >= 0) {
+      slot = it >> g.cv_shift;
+      c = it & (g.CV - 1);
+    } else {
+      slot = it / g.CV;
+      c = it - slot * g.CV;
+    }
+    const int tk = s_tok[slot];
+    const int64_t e = (int64_t)tk * g.C + (int64_t)c * VEC;   // latents are [B][N][H][W][C]
+    Raw xtr{};
+    if constexpr (MODE == kGeomReconstruct) xtr = CD::load_stream(g.x_t, e);
+    const Raw prevr = CD::load_stream(g.x0_prev, e);
+    Raw x0r;
+    if (slot < nv) {
+      const int ib = tk / g.HW / g.N;
+      const float inv = (float)s_nvis[slot];
+      float acc[VEC];
+#pragma unroll
+      for (int q = 0; q < VEC; ++q) acc[q] = 0.0f;
+      for (int s = 0; s < g.a; ++s) {   // ascending slots, as the stored operator sums
+        const uint32_t w = (uint32_t)s_word[slot][s];
+        if (!w) continue;
+        const int x0 = (int)(w & 0xfffu) - 1;
+        const int y0 = (int)((w >> 12) & 0xfffu) - 1;
+        const uint32_t mask = (w >> 24) & 0xfu;
+        const int64_t new_view = ((int64_t)ib * g.a + s) * g.HW;
+        const int64_t old_view = ((int64_t)ib * g.N + g.anchor_view[s]) * g.HW;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          if (!(mask & (1u << k))) continue;
+          const int qq = (y0 + (k >> 1)) * g.W + x0 + (k & 1);
+          const float wt = s_wk[slot][s * 4 + k] / inv;   // the builder's stored weight
+          float nf[VEC], of[VEC];
+          CD::unpack(CD::load(g.x0_new, (new_view + qq) * g.C + (int64_t)c * VEC), nf);
+          CD::unpack(CD::load(g.x0_prev, (old_view + qq) * g.C + (int64_t)c * VEC), of);
+#pragma unroll
+          for (int q2 = 0; q2 < VEC; ++q2) acc[q2] = acc[q2] + wt * (nf[q2] - of[q2]);
+        }
+      }
+      float prevf[VEC], y[VEC];
+      CD::unpack(prevr, prevf);
+#pragma unroll
+      for (int q = 0; q < VEC; ++q) y[q] = prevf[q] + acc[q];
+      x0r = CD::pack(y);
+    } else {
+      x0r = prevr;   // no anchor sees this token: it keeps its own state
+    }
+    finish_item<DT, VEC, MODE>(g, e, x0r, xtr);
+  }
+}
+
 // Lanes per target token: the channel vectors rounded up to a power of two,
 // at most 8 (with more vectors a lane takes several items).
 int geom_group(int CV) { return CV <= 1 ? 1 : CV <= 2 ? 2 : CV <= 4 ? 4 : 8; }
 
 int prepare_geom(const void* x0_prev, const void* x0_new, const float* pos, const gc_camera* cams, const float* bbox,
-                 int B, int N, int H, int W, int C, const int32_t* anchors, int a, int K, int dtype, void* x0_out,
-                 const char* who, GArgs* g) {
+                 const uint32_t* fg_bits, const int32_t* fg_recs, int64_t n_fg, int B, int N, int H, int W, int C,
+                 const int32_t* anchors, int a, int K, int dtype, void* x0_out, const char* who, GArgs* g) {
   if (!x0_prev || !x0_new || !pos || !cams || !bbox || !anchors || !x0_out)
     return fail(GC_ERR_ARG, "%s: null pointer", who);
   if (dtype != GC_F32 && dtype != GC_BF16) return fail(GC_ERR_DTYPE, "%s: unknown dtype %d", who, dtype);
@@ -309,6 +560,19 @@ int prepare_geom(const void* x0_prev, const void* x0_new, const float* pos, cons
   if (K < 1 || K > 4) return fail(GC_ERR_ARG, "%s: K=%d outside [1, 4]", who, K);
   if (!aligned16(x0_prev) || !aligned16(x0_new) || !aligned16(x0_out) || !aligned16(pos))
     return fail(GC_ERR_ALIGN, "%s: latents and position maps must be 16-byte aligned", who);
+  // optional foreground index: both pointers null (and n_fg 0) for the blocked launch
+  const int64_t n_tok_all = (int64_t)B * N * H * W;
+  if (!fg_bits && (fg_recs || n_fg != 0))
+    return fail(GC_ERR_ARG, "%s: fg_recs / n_fg given without fg_bits", who);
+  if (fg_bits) {
+    if (n_fg < 0 || n_fg > n_tok_all)
+      return fail(GC_ERR_ARG, "%s: n_fg=%lld outside [0, B*N*H*W=%lld]", who, (long long)n_fg, (long long)n_tok_all);
+    if (n_fg > 0 && !fg_recs) return fail(GC_ERR_ARG, "%s: null fg_recs with n_fg > 0", who);
+    if (n_tok_all > 0x7fffffffLL)
+      return fail(GC_ERR_CAPACITY, "%s: B*N*H*W=%lld exceeds 2^31-1 (foreground index)", who, (long long)n_tok_all);
+    if (!aligned16(fg_bits) || (fg_recs && !aligned16(fg_recs)))
+      return fail(GC_ERR_ALIGN, "%s: fg_bits and fg_recs must be 16-byte aligned", who);
+  }
   std::memset(g, 0, sizeof(*g));
   bool is_anchor[GC_MAX_VIEWS] = {};
   for (int s = 0; s < a; ++s) {
@@ -324,7 +588,9 @@ int prepare_geom(const void* x0_prev, const void* x0_new, const float* pos, cons
   const size_t n_all = (size_t)B * N * HW * C * es, n_new = (size_t)B * a * HW * C * es;
   if (overlaps(x0_out, n_all, x0_prev, n_all) || overlaps(x0_out, n_all, x0_new, n_new) ||
       overlaps(x0_out, n_all, pos, (size_t)B * N * HW * 12) || overlaps(x0_out, n_all, cams, (size_t)B * N * sizeof(gc_camera)) ||
-      overlaps(x0_out, n_all, bbox, (size_t)B * 32))
+      overlaps(x0_out, n_all, bbox, (size_t)B * 32) ||
+      overlaps(x0_out, n_all, fg_bits, (size_t)(n_tok_all + 31) / 32 * 4) ||
+      overlaps(x0_out, n_all, fg_recs, (size_t)n_fg * 16))
     return fail(GC_ERR_ALIAS, "%s: x0_out overlaps an input", who);
   g->x0_prev = x0_prev;
   g->x0_new = x0_new;
@@ -356,16 +622,36 @@ int prepare_geom(const void* x0_prev, const void* x0_new, const float* pos, cons
   g->n_tblocks = (int)nt;
   g->tgrid = (int)tgrid;
   g->n_ablocks = (int)na;
+  g->B = B;
+  if (fg_bits && (int64_t)B * a <= kMaxCamLds) {   // the foreground launch
+    const int64_t gb = (n_fg + tok - 1) / tok;
+    const int64_t bpv_s = ((int64_t)HW * g->CV + kBlock - 1) / kBlock;
+    const int64_t ns = (int64_t)B * N * bpv_s;
+    const int64_t gblocks = (gb + kXcds - 1) / kXcds * kXcds;
+    if (gblocks + ns > (int64_t)0x7fffffff) return fail(GC_ERR_CAPACITY, "%s: problem too large for one launch", who);
+    g->fg_bits = fg_bits;
+    g->fg_recs = reinterpret_cast<const int4*>(fg_recs);
+    g->n_fg = (int)n_fg;
+    g->gblocks = (int)gblocks;
+    g->bpv_s = (int)bpv_s;
+    g->n_sblocks = (int)ns;
+  }
   return GC_OK;
 }
 
 template <int MODE>
 void launch_geom(const GArgs& g, int dtype, hipStream_t stream) {
   const int agrid = (g.n_ablocks + kXcds - 1) / kXcds * kXcds;
-  const dim3 grid((unsigned)(g.tgrid + agrid));
+  const bool fg = g.fg_bits != nullptr;
+  const dim3 grid((unsigned)(fg ? g.gblocks + g.n_sblocks : g.tgrid + agrid));
   const int vec = g.C / g.CV;
-#define GC_GEOM_K(DT_, VEC_, G_, AMAX_) \
-  hipLaunchKernelGGL((k_transport_geom<DT_, VEC_, MODE, G_, AMAX_>), grid, dim3(kBlock), 0, stream, g)
+#define GC_GEOM_K(DT_, VEC_, G_, AMAX_)                                                                       \
+  do {                                                                                                      \
+    if (fg)                                                                                                 \
+      hipLaunchKernelGGL((k_transport_geom_fg<DT_, VEC_, MODE, G_, AMAX_>), grid, dim3(kBlock), 0, stream, g); \
+    else                                                                                                    \
+      hipLaunchKernelGGL((k_transport_geom<DT_, VEC_, MODE, G_, AMAX_>), grid, dim3(kBlock), 0, stream, g);    \
+  } while (0)
 #define GC_LAUNCH_GEOM(DT_, VEC_)                  \
   do {                                             \
     const bool small = g.a <= 4;                   \
@@ -408,27 +694,29 @@ void launch_geom(const GArgs& g, int dtype, hipStream_t stream) {
 using namespace gc;
 
 extern "C" int gc_transport_step_geom(const void* x0_prev, const void* x0_anchor_new, const float* pos,
-                                      const gc_camera* cams, const float* bbox, int B, int N, int H, int W, int C,
+                                      const gc_camera* cams, const float* bbox, const uint32_t* fg_bits,
+                                      const int32_t* fg_recs, int64_t n_fg, int B, int N, int H, int W, int C,
                                       const int32_t* anchors, int a, int K, int dtype, void* x0_out,
                                       hipStream_t stream) {
   clear_error();
   GArgs g;
-  int rc = prepare_geom(x0_prev, x0_anchor_new, pos, cams, bbox, B, N, H, W, C, anchors, a, K, dtype, x0_out,
-                        "gc_transport_step_geom", &g);
+  int rc = prepare_geom(x0_prev, x0_anchor_new, pos, cams, bbox, fg_bits, fg_recs, n_fg, B, N, H, W, C, anchors, a,
+                        K, dtype, x0_out, "gc_transport_step_geom", &g);
   if (rc) return rc;
   launch_geom<kGeomTransport>(g, dtype, stream);
   return after_launch(stream, "gc_transport_step_geom");
 }
 
 extern "C" int gc_transport_reconstruct_geom(const void* x0_prev, const void* x0_anchor_new, const float* pos,
-                                             const gc_camera* cams, const float* bbox, const void* x_t, int B, int N,
+                                             const gc_camera* cams, const float* bbox, const uint32_t* fg_bits,
+                                             const int32_t* fg_recs, int64_t n_fg, const void* x_t, int B, int N,
                                              int H, int W, int C, const int32_t* anchors, int a, int K, int dtype,
                                              const gc_sampler* smp, double t, double t_next, void* x0_out,
                                              void* x_next, void* model_out, hipStream_t stream) {
   clear_error();
   GArgs g;
-  int rc = prepare_geom(x0_prev, x0_anchor_new, pos, cams, bbox, B, N, H, W, C, anchors, a, K, dtype, x0_out,
-                        "gc_transport_reconstruct_geom", &g);
+  int rc = prepare_geom(x0_prev, x0_anchor_new, pos, cams, bbox, fg_bits, fg_recs, n_fg, B, N, H, W, C, anchors, a,
+                        K, dtype, x0_out, "gc_transport_reconstruct_geom", &g);
   if (rc) return rc;
   if (!x_t || !x_next) return fail(GC_ERR_ARG, "gc_transport_reconstruct_geom: null x_t or x_next");
   rc = make_recon(smp, t, t_next, &g.r);
@@ -440,10 +728,11 @@ extern "C" int gc_transport_reconstruct_geom(const void* x0_prev, const void* x0
   const size_t es = (size_t)dtype_bytes(dtype);
   const size_t HW = (size_t)H * W;
   const size_t n_all = (size_t)B * N * HW * C * es, n_new = (size_t)B * a * HW * C * es;
-  const void* ins[6] = {x0_prev, x0_anchor_new, x0_out, pos, cams, bbox};
-  const size_t lens[6] = {n_all, n_new, n_all, (size_t)B * N * HW * 12, (size_t)B * N * sizeof(gc_camera),
-                          (size_t)B * 32};
-  for (int i = 0; i < 6; ++i) {
+  const void* ins[8] = {x0_prev, x0_anchor_new, x0_out, pos, cams, bbox, fg_bits, fg_recs};
+  const size_t lens[8] = {n_all, n_new, n_all, (size_t)B * N * HW * 12, (size_t)B * N * sizeof(gc_camera),
+                          (size_t)B * 32, ((size_t)B * N * HW + 31) / 32 * 4, (size_t)n_fg * 16};
+  for (int i = 0; i < 8; ++i) {
+    if (!ins[i]) continue;   // the optional index: a null pointer overlaps nothing (nor a null model_out)
     if (overlaps(x_next, n_all, ins[i], lens[i]) || overlaps(model_out, n_all, ins[i], lens[i]))
       return fail(GC_ERR_ALIAS, "gc_transport_reconstruct_geom: x_next/model_out overlap an input or x0_out");
   }

@@ -1,19 +1,24 @@
-// Visible-token index of a correspondence operator (once per asset and
-// anchor set).
+// Token indexes that let the per-step kernels split their work into
+// gathering blocks over a compact list and streaming blocks over everything
+// else, which recognise the listed tokens by one bit each.
 //
-// G_{A->v} has a non-zero row only for tokens some anchor sees (Sec. 3.2:
-// a token with no tap inside the tolerance has an all-zero row).  The
-// per-step kernel splits its work on that: blocks over a compact list of the
-// visible tokens do the
-// gathers, and blocks over all tokens stream everything else, skipping
-// visible tokens by a one-bit-per-token mask instead of reading their words.
+// Visible-token index of a correspondence operator (once per asset and
+// anchor set).  G_{A->v} has a non-zero row only for tokens some anchor sees
+// (Sec. 3.2: a token with no tap inside the tolerance has an all-zero row);
+// the list holds those tokens.
+//
+// Foreground index of the position maps (once per asset batch).  Only a
+// token with a finite position can be seen by an anchor (the operator's
+// tolerance test needs its 3D point), so the on-the-fly step evaluates the
+// operator for foreground tokens only; the list holds each one's token index
+// and position, so that one 16-byte load gives a lane both.
 //
 // Three passes, deterministic (the list is in ascending token order):
-//   count    per 1024-token chunk, visible tokens (ballot + popcount);
+//   count    per 1024-token chunk, listed tokens (ballot + popcount);
 //            also writes the bitmask (one 64-bit ballot per wave)
-//   scan     exclusive prefix over the chunk counts, total -> n_vis
-//   scatter  each chunk writes its visible tokens at its offset, ranked
-//            inside the chunk by (round, wave, mbcnt of the ballot)
+//   scan     exclusive prefix over the chunk counts, total -> list length
+//   scatter  each chunk writes its tokens at its offset, ranked inside the
+//            chunk by (round, wave, mbcnt of the ballot)
 #include "gc_common.h"
 
 namespace gc {
@@ -24,28 +29,48 @@ constexpr int kRounds = 4;                 // tokens per block = kRounds * kBloc
 constexpr int kChunk = kRounds * kBlock;
 constexpr int kWaves = kBlock / 64;
 
-__device__ __forceinline__ bool token_visible(const int32_t* __restrict__ corr, int64_t tok, int64_t n_tokens,
-                                              int a) {
-  if (tok >= n_tokens) return false;
-  const int32_t* w = corr + tok * a;
-  if (a == 4) {
-    const int4 q = *reinterpret_cast<const int4*>(w);
-    return (q.x | q.y | q.z | q.w) != 0;
+// Listed tokens of the visible-token index: a non-zero correspondence row.
+struct VisiblePred {
+  const int32_t* corr;
+  int a;
+  __device__ __forceinline__ bool operator()(int64_t tok) const {
+    const int32_t* w = corr + tok * a;
+    if (a == 4) {
+      const int4 q = *reinterpret_cast<const int4*>(w);
+      return (q.x | q.y | q.z | q.w) != 0;
+    }
+    int32_t any = 0;
+    for (int s = 0; s < a; ++s) any |= w[s];
+    return any != 0;
   }
-  int32_t any = 0;
-  for (int s = 0; s < a; ++s) any |= w[s];
-  return any != 0;
-}
+  // list entry: the token index
+  __device__ __forceinline__ void write(int32_t* list, int32_t at, int64_t tok) const { list[at] = (int32_t)tok; }
+};
 
-__global__ __launch_bounds__(kBlock) void k_index_count(const int32_t* __restrict__ corr, int64_t n_tokens, int a,
-                                                        uint32_t* __restrict__ bits, int64_t n_words,
-                                                        int32_t* __restrict__ counts) {
+// Listed tokens of the foreground index: all three position components finite.
+struct ForegroundPred {
+  const float* pos;
+  __device__ __forceinline__ bool operator()(int64_t tok) const {
+    const float* q = pos + tok * 3;
+    return finite_f(q[0]) && finite_f(q[1]) && finite_f(q[2]);
+  }
+  // list entry: {token, x, y, z} (positions as float bit patterns), 16 bytes
+  __device__ __forceinline__ void write(int32_t* list, int32_t at, int64_t tok) const {
+    const float* q = pos + tok * 3;
+    *reinterpret_cast<int4*>(list + (int64_t)at * 4) =
+        make_int4((int32_t)tok, __float_as_int(q[0]), __float_as_int(q[1]), __float_as_int(q[2]));
+  }
+};
+
+template <class Pred>
+__global__ __launch_bounds__(kBlock) void k_index_count(Pred pred, int64_t n_tokens, uint32_t* __restrict__ bits,
+                                                        int64_t n_words, int32_t* __restrict__ counts) {
   __shared__ int32_t wave_cnt[kWaves];
   const int wv = threadIdx.x / 64;
   int32_t total = 0;
   for (int r = 0; r < kRounds; ++r) {
     const int64_t tok = (int64_t)blockIdx.x * kChunk + r * kBlock + threadIdx.x;
-    const unsigned long long m = __ballot(token_visible(corr, tok, n_tokens, a));
+    const unsigned long long m = __ballot(tok < n_tokens && pred(tok));
     if (__lane_id() == 0) {
       const int64_t w0 = ((int64_t)blockIdx.x * kChunk + r * kBlock + wv * 64) >> 5;
       if (w0 < n_words) bits[w0] = (uint32_t)m;
@@ -85,15 +110,15 @@ __global__ __launch_bounds__(kBlock) void k_index_scan(const int32_t* __restrict
   if (threadIdx.x == 0) *n_vis = carry;
 }
 
-__global__ __launch_bounds__(kBlock) void k_index_scatter(const int32_t* __restrict__ corr, int64_t n_tokens, int a,
-                                                          const int32_t* __restrict__ offsets,
+template <class Pred>
+__global__ __launch_bounds__(kBlock) void k_index_scatter(Pred pred, int64_t n_tokens, const int32_t* __restrict__ offsets,
                                                           int32_t* __restrict__ list) {
   __shared__ int32_t wave_cnt[kWaves];
   const int wv = threadIdx.x / 64;
   int32_t pos = offsets[blockIdx.x];
   for (int r = 0; r < kRounds; ++r) {
     const int64_t tok = (int64_t)blockIdx.x * kChunk + r * kBlock + threadIdx.x;
-    const bool vis = token_visible(corr, tok, n_tokens, a);
+    const bool vis = tok < n_tokens && pred(tok);
     const unsigned long long m = __ballot(vis);
     if (__lane_id() == 0) wave_cnt[wv] = __popcll(m);
     __syncthreads();
@@ -101,7 +126,7 @@ __global__ __launch_bounds__(kBlock) void k_index_scatter(const int32_t* __restr
     for (int w = 0; w < wv; ++w) before += wave_cnt[w];
     const int32_t rank = (int32_t)__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
                                                             __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
-    if (vis) list[pos + before + rank] = (int32_t)tok;
+    if (vis) pred.write(list, pos + before + rank, tok);
     int32_t round_total = 0;
     for (int w = 0; w < kWaves; ++w) round_total += wave_cnt[w];
     __syncthreads();
@@ -145,11 +170,45 @@ extern "C" int gc_index_correspondence(const int32_t* corr, int64_t n_tokens, in
   int32_t* counts = static_cast<int32_t*>(workspace);
   int32_t* offsets = counts + nb;
   if (nb > 0)
-    hipLaunchKernelGGL(k_index_count, dim3((unsigned)nb), dim3(kBlock), 0, stream, corr, n_tokens, a, vis_bits,
-                       n_words, counts);
+    hipLaunchKernelGGL(k_index_count<VisiblePred>, dim3((unsigned)nb), dim3(kBlock), 0, stream,
+                       VisiblePred{corr, a}, n_tokens, vis_bits, n_words, counts);
   hipLaunchKernelGGL(k_index_scan, dim3(1), dim3(kBlock), 0, stream, counts, nb, offsets, n_vis);
   if (nb > 0)
-    hipLaunchKernelGGL(k_index_scatter, dim3((unsigned)nb), dim3(kBlock), 0, stream, corr, n_tokens, a, offsets,
-                       vis_list);
+    hipLaunchKernelGGL(k_index_scatter<VisiblePred>, dim3((unsigned)nb), dim3(kBlock), 0, stream,
+                       VisiblePred{corr, a}, n_tokens, offsets, vis_list);
   return after_launch(stream, "gc_index_correspondence");
+}
+
+extern "C" int gc_index_foreground(const float* pos, int64_t n_tokens, uint32_t* fg_bits, int32_t* fg_recs,
+                                   int32_t* n_fg, void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  clear_error();
+  if (!n_fg || !workspace) return fail(GC_ERR_ARG, "foreground index: null n_fg or workspace");
+  if (n_tokens < 0) return fail(GC_ERR_SHAPE, "foreground index: n_tokens=%lld is negative", (long long)n_tokens);
+  if (n_tokens > 0x7fffffffLL)
+    return fail(GC_ERR_CAPACITY, "foreground index: n_tokens=%lld exceeds 2^31-1", (long long)n_tokens);
+  if (n_tokens > 0 && (!pos || !fg_bits || !fg_recs)) return fail(GC_ERR_ARG, "foreground index: null pointer");
+  if ((pos && !aligned16(pos)) || (fg_bits && !aligned16(fg_bits)) || (fg_recs && !aligned16(fg_recs)) ||
+      !aligned16(workspace))
+    return fail(GC_ERR_ALIGN, "foreground index: pointers must be 16-byte aligned");
+  if (workspace_bytes < gc_index_workspace_bytes(n_tokens))
+    return fail(GC_ERR_CAPACITY, "foreground index: workspace of %zu bytes is below the %zu required", workspace_bytes,
+                gc_index_workspace_bytes(n_tokens));
+  const int64_t n_words = (n_tokens + 31) / 32;
+  const size_t np = (size_t)n_tokens * 12, nr = (size_t)n_tokens * 16, nbits = (size_t)n_words * 4;
+  if (overlaps(fg_bits, nbits, pos, np) || overlaps(fg_recs, nr, pos, np) || overlaps(fg_recs, nr, fg_bits, nbits) ||
+      overlaps(n_fg, 4, fg_recs, nr) || overlaps(n_fg, 4, fg_bits, nbits) || overlaps(n_fg, 4, pos, np) ||
+      overlaps(workspace, workspace_bytes, pos, np) || overlaps(workspace, workspace_bytes, fg_recs, nr) ||
+      overlaps(workspace, workspace_bytes, fg_bits, nbits) || overlaps(workspace, workspace_bytes, n_fg, 4))
+    return fail(GC_ERR_ALIAS, "foreground index: buffers overlap");
+  const int64_t nb = n_tokens > 0 ? (n_tokens + kChunk - 1) / kChunk : 0;
+  int32_t* counts = static_cast<int32_t*>(workspace);
+  int32_t* offsets = counts + nb;
+  if (nb > 0)
+    hipLaunchKernelGGL(k_index_count<ForegroundPred>, dim3((unsigned)nb), dim3(kBlock), 0, stream,
+                       ForegroundPred{pos}, n_tokens, fg_bits, n_words, counts);
+  hipLaunchKernelGGL(k_index_scan, dim3(1), dim3(kBlock), 0, stream, counts, nb, offsets, n_fg);
+  if (nb > 0)
+    hipLaunchKernelGGL(k_index_scatter<ForegroundPred>, dim3((unsigned)nb), dim3(kBlock), 0, stream,
+                       ForegroundPred{pos}, n_tokens, offsets, fg_recs);
+  return after_launch(stream, "gc_index_foreground");
 }

@@ -19,8 +19,8 @@ import torch
 
 from . import (GC_FULL_HEAD_MID_TAIL, GC_FULL_HEAD_TAIL_E, GC_FULL_PERIODIC, Sampler, VisibleIndex,
                gc_build_correspondence, gc_coverage_init, gc_coverage_pairs, gc_coverage_score, gc_coverage_select,
-               gc_coverage_update, gc_coverage_workspace_bytes, gc_index_correspondence, gc_posmap_bbox,
-               gc_sampler_reconstruct, gc_sampler_step_times, gc_schedule_anchors, gc_schedule_full_steps,
+               gc_coverage_update, gc_coverage_workspace_bytes, gc_index_correspondence, gc_index_foreground,
+               gc_posmap_bbox, gc_sampler_reconstruct, gc_sampler_step_times, gc_schedule_anchors, gc_schedule_full_steps,
                gc_schedule_refresh_due, gc_transport_reconstruct, gc_transport_reconstruct_geom, gc_transport_unipc,
                gc_unipc_coeffs, gc_unipc_update)
 
@@ -46,7 +46,8 @@ class GeoCacheRunner:
         refresh_tau makes a step full when the fraction of foreground tokens
         stale for refresh_R or more steps exceeds it.  geom computes the
         correspondence inside each step instead of building and caching one
-        per anchor set."""
+        per anchor set; with use_index it uses the position maps' foreground
+        index (built once here)."""
         if anchor_policy not in ("rotate", "coverage", "rotation_coverage"):
             raise ValueError("anchor_policy must be 'rotate', 'coverage' or 'rotation_coverage'")
         if unipc_order and geom:
@@ -60,6 +61,7 @@ class GeoCacheRunner:
         self.use_index = use_index
         self.stream = stream
         self.bbox = gc_posmap_bbox(pos, tol_frac, stream=stream)
+        self.fg_index = gc_index_foreground(pos, stream=stream) if geom and use_index else None
         self._ops: Dict[Tuple[int, ...], Tuple[torch.Tensor, torch.Tensor, Optional[VisibleIndex]]] = {}
         self.unipc_order, self.unipc_corrector = unipc_order, unipc_corrector
         self.anchor_policy, self.max_gap = anchor_policy, max_gap
@@ -158,7 +160,8 @@ class GeoCacheRunner:
             new = predict(k, views).contiguous()
             if self.geom:
                 x0, x_next, _ = gc_transport_reconstruct_geom(self.x0, new, self.pos, self.cams, self.bbox, self.x_t,
-                                                              views, self.K, self.sampler, t, tn, stream=self.stream)
+                                                              views, self.K, self.sampler, t, tn,
+                                                              fg_index=self.fg_index, stream=self.stream)
             else:
                 corr, wts, idx = self.operator(views)
                 x0, x_next, _ = gc_transport_reconstruct(self.x0, new, corr, wts, self.x_t, views, self.sampler, t,

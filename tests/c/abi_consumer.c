@@ -99,7 +99,7 @@ int main(void) {
   HIP_OK(hipMemcpy(d_new, x0_new, n_lat / NV * 4, hipMemcpyHostToDevice));
   HIP_OK(hipMemcpy(d_xt, x_t, n_lat * 4, hipMemcpyHostToDevice));
 
-  CHECK(gc_abi_version() == 1, "abi version %d", gc_abi_version());
+  CHECK(gc_abi_version() == GC_ABI_VERSION, "abi version %d", gc_abi_version());
   const int32_t anchors[1] = {0};
   int rc = gc_posmap_bbox(d_pos, 1, NV, H, W, 0.01f, d_bbox, 0);
   CHECK(rc == GC_OK, "bbox rc=%d %s", rc, gc_last_error());

@@ -20,7 +20,11 @@ LIBSO = os.path.join(ROOT, "paper_2608_13255_amd", "libgeocache.so")
 
 # fake, never-dereferenced device addresses: every call below fails validation
 # before anything is launched
-A0, A1, A2, A3, A4, A5 = (0x10000000 * (i + 1) for i in range(6))
+A0, A1, A2, A3, A4, A5, A6, A7 = (0x10000000 * (i + 1) for i in range(8))
+
+
+def header_abi_version():
+    return int(re.search(r"#define GC_ABI_VERSION (\d+)", open(HEADER).read()).group(1))
 
 
 def header_functions():
@@ -37,6 +41,7 @@ def gc():
 
 @pytest.fixture(scope="module")
 def L(gc):
+    assert gc.ABI_VERSION == header_abi_version()
     return gc.lib()
 
 
@@ -48,7 +53,7 @@ def test_exports_match_header(L):
     assert exported == declared
     for name in declared:
         assert getattr(L, name) is not None
-    assert L.gc_abi_version() == 1
+    assert L.gc_abi_version() == header_abi_version()
 
 
 def test_struct_layouts(gc):
@@ -132,6 +137,17 @@ def test_reconstruct_and_build_validation(gc, L):
     assert L.gc_index_correspondence(A0, 1 << 20, 9, A1, A2, A3, A4, need, None) == -1
     assert L.gc_index_correspondence(A0, 1 << 20, 4, A1, A0 + 64, A3, A4, need, None) == -5
     assert L.gc_index_correspondence(A0, -1, 4, A1, A2, A3, A4, need, None) == -2
+    # foreground index of position maps: pos, bits, records, count, workspace
+    n = 1 << 20
+    assert L.gc_index_foreground(A0, n, A1, A2, A3, A4, need - 1, None) == -6
+    assert L.gc_index_foreground(A0, n, A1, A2, None, A4, need, None) == -1
+    assert L.gc_index_foreground(None, n, A1, A2, A3, A4, need, None) == -1
+    assert L.gc_index_foreground(A0, -1, A1, A2, A3, A4, need, None) == -2
+    assert L.gc_index_foreground(A0, 1 << 31, A1, A2, A3, A4, need, None) == -6
+    assert L.gc_index_foreground(A0, n, A1, A2 + 8, A3, A4, need, None) == -4
+    assert L.gc_index_foreground(A0, n, A1, A0 + 64, A3, A4, need, None) == -5   # records overlap the maps
+    assert L.gc_index_foreground(A0, n, A1, A2, A2 + 16, A4, need, None) == -5   # count inside the records
+    assert L.gc_index_foreground(A0, n, A1, A2, A3, A1 + 16, need, None) == -5   # workspace over the bits
 
 
 def test_host_schedule_matches_oracle(gc):
@@ -233,8 +249,10 @@ def test_geom_validation(gc, L):
     anchors = (ctypes.c_int32 * 2)(0, 3)
     n = 1 * 6 * 8 * 8 * 16 * 2
 
-    def step(prev=A0, new=A1, pos=A2, cams=A3, bbox=A4, C=16, a=2, K=4, dt=1, out=A5, anc=anchors):
-        return L.gc_transport_step_geom(prev, new, pos, cams, bbox, 1, 6, 8, 8, C, anc, a, K, dt, out, None)
+    def step(prev=A0, new=A1, pos=A2, cams=A3, bbox=A4, C=16, a=2, K=4, dt=1, out=A5, anc=anchors, fb=None, fr=None,
+             nf=0):
+        return L.gc_transport_step_geom(prev, new, pos, cams, bbox, fb, fr, nf, 1, 6, 8, 8, C, anc, a, K, dt, out,
+                                        None)
 
     assert step(pos=None) == -1 and "null" in _err(L)
     assert step(cams=None) == -1
@@ -247,10 +265,20 @@ def test_geom_validation(gc, L):
     assert step(out=A2 + 64) == -5                # x0_out overlaps the position maps
     dup = (ctypes.c_int32 * 2)(1, 1)
     assert step(anc=dup) == -1 and "twice" in _err(L)
+    # the optional foreground index (6 * 8 * 8 = 384 tokens)
+    assert step(fr=A6) == -1 and "without fg_bits" in _err(L)
+    assert step(nf=3) == -1
+    assert step(fb=A6, nf=385) == -1 and "n_fg" in _err(L)
+    assert step(fb=A6, nf=-1) == -1
+    assert step(fb=A6, nf=5) == -1 and "fg_recs" in _err(L)
+    assert step(fb=A6 + 4, fr=A7, nf=5) == -4
+    assert step(fb=A6, fr=A7 + 8, nf=5) == -4
+    assert step(fb=A6, fr=A7, nf=5, out=A7 - 64) == -5     # x0_out overlaps the records
+    assert step(fb=A6, fr=A7, nf=5, out=A6 - 64) == -5     # x0_out overlaps the bits
     smp = gc.Sampler(kind=gc.GC_FLOW_EULER).c()
 
-    def fused(xt=A5 + 4 * n, xn=A5 + 8 * n, mo=None, t=0.5, tn=0.4):
-        return L.gc_transport_reconstruct_geom(A0, A1, A2, A3, A4, xt, 1, 6, 8, 8, 16, anchors, 2, 4, 1,
+    def fused(xt=A5 + 4 * n, xn=A5 + 8 * n, mo=None, t=0.5, tn=0.4, fb=None, fr=None, nf=0):
+        return L.gc_transport_reconstruct_geom(A0, A1, A2, A3, A4, fb, fr, nf, xt, 1, 6, 8, 8, 16, anchors, 2, 4, 1,
                                                ctypes.byref(smp), t, tn, A5, xn, mo, None)
 
     assert fused(xt=None) == -1
@@ -258,6 +286,8 @@ def test_geom_validation(gc, L):
     assert fused(mo=A5 + 12 * n) == -1            # model_out without a prediction output
     assert fused(xn=A5 + 64) == -5                # x_next overlaps x0_out
     assert fused(xt=A5 + 64) == -5                # x_t overlaps x0_out
+    assert fused(fb=A6, fr=A7, nf=5, xn=A7 - 64) == -5   # x_next overlaps the records
+    assert fused(fb=A6, nf=2) == -1
 
 
 def test_error_message_is_per_thread(gc, L):

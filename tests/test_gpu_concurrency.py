@@ -1,7 +1,8 @@
 """The library keeps no state between calls (error messages are per thread):
 two host threads, each with its own HIP stream, buffers and coverage
 workspace, issue cached steps concurrently -- the stored operator with its
-index, the on-the-fly step, the fused UniPC step and a coverage update +
+index, the on-the-fly step (blocked and foreground launches), the fused
+UniPC step and a coverage update +
 greedy selection -- and every result equals the same call run alone, bit
 for bit.  ctypes releases the interpreter lock around each foreign call, so
 the two threads' calls overlap on the host as well as on the device."""
@@ -38,6 +39,7 @@ def test_two_threads_two_streams(gc):
     smp = gc.Sampler(kind=gc.GC_DDIM, pred_out=gc.GC_PRED_EPS)
     st = gc.gc_unipc_coeffs(gc.Sampler(kind=gc.GC_DDIM), w.S, 6, 2, True)
     pairs = gc.gc_coverage_pairs(P, cams, bb)
+    fgi = gc.gc_index_foreground(P)
     shape = (1, w.N, w.H, w.W, w.C)
 
     def make(seed, c):
@@ -49,7 +51,8 @@ def test_two_threads_two_streams(gc):
                    xprev=bf(shape), m2=bf(shape), new=bf((1, w.a, w.H, w.W, w.C)),
                    ws=torch.empty(gc.gc_coverage_workspace_bytes(), dtype=torch.uint8, device=DEV),
                    stale0=gc.gc_coverage_init(P), stream=torch.cuda.Stream())
-        job["out"] = {k: torch.empty_like(job["x0"]) for k in ("f0", "f1", "f2", "g0", "g1", "g2", "u0", "u1", "u2")}
+        job["out"] = {k: torch.empty_like(job["x0"])
+                      for k in ("f0", "f1", "f2", "g0", "g1", "g2", "h0", "h1", "h2", "u0", "u1", "u2")}
         job["stale"] = job["stale0"].clone()
         job["stats"] = torch.empty((1, w.N, 4), dtype=torch.int32, device=DEV)
         job["sel"] = torch.empty(w.a, dtype=torch.int32, device=DEV)
@@ -62,6 +65,9 @@ def test_two_threads_two_streams(gc):
                                         x0_out=o["f0"], x_next=o["f1"], model_out=o["f2"], index=j["idx"], stream=s)
             gc.gc_transport_reconstruct_geom(j["x0"], j["new"], P, cams, bb, j["xt"], j["A"], w.K, smp, 700, 666,
                                              x0_out=o["g0"], x_next=o["g1"], model_out=o["g2"], stream=s)
+            gc.gc_transport_reconstruct_geom(j["x0"], j["new"], P, cams, bb, j["xt"], j["A"], w.K, smp, 700, 666,
+                                             x0_out=o["h0"], x_next=o["h1"], model_out=o["h2"], fg_index=fgi,
+                                             stream=s)
             gc.gc_transport_unipc(j["x0"], j["new"], j["corr"], j["wts"], j["A"], st, x_prev=j["xprev"],
                                   m_km2=j["m2"], x0_out=o["u0"], x_c=o["u1"], x_next=o["u2"], index=j["idx"],
                                   stream=s)

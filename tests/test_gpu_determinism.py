@@ -5,8 +5,8 @@ Each call runs twice, into output buffers pre-filled with different bytes,
 and the two results must agree bit for bit.  A difference means either a
 race (the design uses no float atomics: every float sum has a fixed order)
 or an output element the call does not write; every output here is fully
-defined by its contract, except the visible-token list past n_vis and the
-weights of pairs whose word is zero."""
+defined by its contract, except the visible-token and foreground lists past
+their lengths and the weights of pairs whose word is zero."""
 import pytest
 import torch
 
@@ -84,6 +84,8 @@ def test_step_kernels(gc, setup):
     t, tn = gc.gc_sampler_step_times(smp, w.S, 7)
     ust = gc.gc_unipc_coeffs(gc.Sampler(kind=gc.GC_DDIM), w.S, 7, 2, True)
     x = lat["x0_prev"]
+    ws = torch.empty(int(gc.lib().gc_index_workspace_bytes(P.numel() // 3)), dtype=torch.uint8, device=DEV)
+    nf_d = [torch.empty(1, dtype=torch.int32, device=DEV) for _ in range(2)]
     outs = []
     for r in range(2):
         o = []
@@ -107,6 +109,19 @@ def test_step_kernels(gc, setup):
         gc.gc_transport_reconstruct_geom(x, lat["x0_new"], P, cams, bbox, lat["x_t"], A, w.K, smp, t, tn,
                                          x0_out=x0, x_next=xn, model_out=mo)
         o += [x0, xn, mo]
+        # the foreground launch, with the index rebuilt into pre-filled buffers
+        fb = filled(None, r, ((P.numel() // 3 + 31) // 32,), torch.int32)
+        fr = filled(None, r, (P.numel() // 3, 4), torch.int32)
+        rc = gc.lib().gc_index_foreground(P.data_ptr(), P.numel() // 3, fb.data_ptr(), fr.data_ptr(),
+                                          nf_d[r].data_ptr(), ws.data_ptr(), ws.numel(),
+                                          torch.cuda.current_stream().cuda_stream)
+        assert rc == 0, gc.lib().gc_last_error()
+        n_fg = int(nf_d[r].item())
+        fgi = gc.ForegroundIndex(fb, fr, n_fg)
+        x0, xn, mo = filled(x, r), filled(x, r), filled(x, r)
+        gc.gc_transport_reconstruct_geom(x, lat["x0_new"], P, cams, bbox, lat["x_t"], A, w.K, smp, t, tn,
+                                         x0_out=x0, x_next=xn, model_out=mo, fg_index=fgi)
+        o += [x0, xn, mo, fb, fr[:n_fg]]
         outs.append(o)
     same(outs)
 

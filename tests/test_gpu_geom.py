@@ -10,6 +10,14 @@ Covered: every workload at full size, every lane-group size G in {1, 2, 4,
 8} with a <= 4 and a > 4, K in {1, 2, 4}, ragged grids (a partial last
 block per view), channel counts whose vectors do not fill a lane group or
 need two rounds, background positions, a = N.
+
+Every case also runs the foreground launch (with gc_index_foreground's index
+of the position maps), which must give the same bits, and checks that index
+against its definition: a bit per token set iff its three position
+components are finite, and the foreground tokens' {token, x, y, z} records
+in ascending order.  Separately: all-background maps (an empty list), more
+(asset, anchor) cameras than the launch stages (B * a > 64: the blocked
+launch runs), and token counts that end inside a 32-bit word and a chunk.
 """
 import numpy as np
 import pytest
@@ -72,6 +80,28 @@ def inputs(w, P, A, k, C=None, dtype=None, seed=None):
     return prev, new, xt
 
 
+def expected_foreground(P):
+    """The foreground index by its definition: (bit words as uint32, records
+    int32 [n_fg, 4])."""
+    flat = np.ascontiguousarray(P, np.float32).reshape(-1, 3)
+    fg = np.isfinite(flat).all(-1)
+    n = fg.size
+    words = np.packbits(np.concatenate([fg, np.zeros((-n) % 32, bool)]).astype(np.uint8), bitorder="little")
+    words = words.view(np.uint32) if words.size else np.zeros(0, np.uint32)
+    tok = np.nonzero(fg)[0].astype(np.int32)
+    recs = np.concatenate([tok[:, None], flat[tok].view(np.int32)], 1) if tok.size else np.zeros((0, 4), np.int32)
+    return words, recs
+
+
+def check_foreground_index(gc, Pd, P):
+    fgi = gc.gc_index_foreground(Pd)
+    words, recs = expected_foreground(P)
+    assert fgi.n_fg == recs.shape[0]
+    np.testing.assert_array_equal(fgi.fg_bits.cpu().numpy().view(np.uint32)[:words.size], words)
+    np.testing.assert_array_equal(fgi.fg_recs[:fgi.n_fg].cpu().numpy(), recs)
+    return fgi
+
+
 def compare(gc, w, P, cams_np, A, K, prev, new, xt, dtype, smp, t, tn, oracle_check=True):
     Pd = torch.from_numpy(np.ascontiguousarray(P)).to(DEV)
     cams = gc.camera_tensor(cams_np, DEV)
@@ -86,6 +116,12 @@ def compare(gc, w, P, cams_np, A, K, prev, new, xt, dtype, smp, t, tn, oracle_ch
     r0, r1, r2 = gc.gc_transport_reconstruct(prev_d, new_d, corr, wts, xt_d, A, smp, t, tn)
     g0, g1, g2 = gc.gc_transport_reconstruct_geom(prev_d, new_d, Pd, cams, bb, xt_d, A, K, smp, t, tn)
     assert torch.equal(bits(g0), bits(r0)) and torch.equal(bits(g1), bits(r1)) and torch.equal(bits(g2), bits(r2))
+    # the foreground launch: the same bits
+    fgi = check_foreground_index(gc, Pd, P)
+    got_fg = gc.gc_transport_step_geom(prev_d, new_d, Pd, cams, bb, A, K, fg_index=fgi)
+    assert torch.equal(bits(got_fg), bits(ref))
+    f0, f1, f2 = gc.gc_transport_reconstruct_geom(prev_d, new_d, Pd, cams, bb, xt_d, A, K, smp, t, tn, fg_index=fgi)
+    assert torch.equal(bits(f0), bits(r0)) and torch.equal(bits(f1), bits(r1)) and torch.equal(bits(f2), bits(r2))
     if oracle_check:
         corr_o, wts_o, nvis_o = oracle.build(P, cams_np, A, K, oracle.bbox(P, w.tol_frac))
         ex, state = oracle.transport(prev, new, corr_o, wts_o, A, dtype)
@@ -173,3 +209,37 @@ def test_geom_all_views_anchors(gc):
     prev, new, xt = inputs(w, P, A, 0, C=4, dtype="f32", seed=3)
     got = compare(gc, w, P, synth.batch_cameras(w), A, 4, prev, new, xt, "f32", sampler_of(gc, w), 800, 760)
     np.testing.assert_array_equal(got.cpu().numpy(), new)
+
+
+def test_geom_foreground_all_background(gc):
+    """Position maps with no finite sample: the foreground list is empty and
+    every target token keeps its state; both launches agree."""
+    w = synth.shrink(C2, B=2)
+    P = np.full((2, w.N, 24, 40, 3), np.nan, np.float32)
+    A = oracle.anchors(w.N, w.a, 0)
+    prev, new, xt = inputs(w, P, A, 0, C=8, dtype="bf16", seed=11)
+    got = compare(gc, w, P, synth.batch_cameras(w), A, w.K, prev, new, xt, "bf16", sampler_of(gc, w), 600, 560)
+    targets = [v for v in range(w.N) if v not in A]
+    np.testing.assert_array_equal(to_host(got, "bf16")[:, targets], prev[:, targets])
+
+
+def test_geom_foreground_many_cameras_falls_back(gc):
+    """B * a = 22 * 3 = 66 (asset, anchor) cameras exceed what the foreground
+    launch stages: the blocked launch runs and the bits are the same."""
+    w = synth.shrink(C1, B=22, a=3)
+    P = latent_maps(C1.name, B=22)
+    A = [0, 1, 3]
+    prev, new, xt = inputs(w, P, A, 0, C=4, dtype="f32", seed=22)
+    compare(gc, w, P, synth.batch_cameras(w), A, 4, prev, new, xt, "f32", sampler_of(gc, w), 800, 760,
+            oracle_check=False)
+
+
+@pytest.mark.parametrize("shape", [(1, 3, 7, 9), (2, 5, 33, 31), (1, 1, 1, 1), (3, 4, 32, 33), (1, 2, 1, 1100)])
+def test_foreground_index_ragged(gc, shape):
+    """Token counts that end inside a 32-bit word and inside a 1024-token
+    chunk, single tokens, random holes."""
+    rs = np.random.default_rng(sum(shape))
+    P = rs.standard_normal(shape + (3,)).astype(np.float32)
+    P[rs.random(shape) < 0.4] = np.nan
+    P[..., 1][rs.random(shape) < 0.1] = np.inf     # one non-finite component is enough
+    check_foreground_index(gc, torch.from_numpy(P).to(DEV), P)
