@@ -166,7 +166,8 @@ def test_graph_replays_match_eager():
 
 
 def test_graph_replays_other_paths():
-    """The on-the-fly step, the fused UniPC step and the coverage update +
+    """The on-the-fly step (blocked and foreground launches), the fused UniPC
+    step and the coverage update +
     greedy selection captured in one HIP graph: every replay (with eager
     work, state resets and synchronisations between replays) equals the
     eager result bit for bit."""
@@ -187,7 +188,8 @@ def test_graph_replays_other_paths():
     new0, new1 = bf((1, w.a, w.H, w.W, w.C)), bf((1, w.a, w.H, w.W, w.C))
     smp = gc.Sampler(kind=gc.GC_DDIM, pred_out=gc.GC_PRED_EPS)
     st = gc.gc_unipc_coeffs(gc.Sampler(kind=gc.GC_DDIM), 30, 6, 2, True)
-    outs = {k: torch.empty_like(x0) for k in ("g0", "g1", "g2", "u0", "u1", "u2")}
+    outs = {k: torch.empty_like(x0) for k in ("g0", "g1", "g2", "h0", "h1", "h2", "u0", "u1", "u2")}
+    fgi = gc.gc_index_foreground(P)
     pairs = gc.gc_coverage_pairs(P, cams, bb)
     stale0 = gc.gc_coverage_init(P)
     for A in (A0, A1, A0):
@@ -202,6 +204,8 @@ def test_graph_replays_other_paths():
     def step():
         gc.gc_transport_reconstruct_geom(x0, new0, P, cams, bb, xt, A0, w.K, smp, 700, 666, x0_out=outs["g0"],
                                          x_next=outs["g1"], model_out=outs["g2"], stream=s)
+        gc.gc_transport_reconstruct_geom(x0, new1, P, cams, bb, xt, A1, w.K, smp, 700, 666, x0_out=outs["h0"],
+                                         x_next=outs["h1"], model_out=outs["h2"], fg_index=fgi, stream=s)
         gc.gc_transport_unipc(x0, new1, corr1, wts1, A1, st, x_prev=xprev, m_km2=m2, x0_out=outs["u0"],
                               x_c=outs["u1"], x_next=outs["u2"], index=idx1, stream=s)
         gc.gc_coverage_update(pairs, stale, A1, 2, stats=stats, stream=s)
