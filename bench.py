@@ -188,6 +188,10 @@ def main():
     b1.record()
     torch.cuda.synchronize()
     rows["build_no_counters_ms_per_anchor_set"] = b0.elapsed_time(b1) / (10 * len(anchor_sets))
+    # (target token, anchor) pairs the builder decides per second
+    n_pairs = B * (N - a) * HW * a
+    rows["build_pairs_per_s"] = n_pairs / (rows["build_no_counters_ms_per_anchor_set"] * 1e-3)
+    rows["build_with_counters_pairs_per_s"] = n_pairs / (rows["build_ms_per_anchor_set"] * 1e-3)
     rows["anchor_sets"] = len(anchor_sets)
     index = {}
     e4, e5 = ev(), ev()
