@@ -17,7 +17,7 @@
  *                        gc_sampler_reconstruct sampler-consistent eps / v / velocity + x_t update
  *                        gc_transport_reconstruct  the two above fused in one pass
  *                        gc_unipc_update, gc_transport_unipc  multistep (UniPC) variant
- *                        gc_transport_step_geom, gc_transport_reconstruct_geom
+ *                        gc_transport_step_geom, gc_transport_reconstruct_geom, gc_transport_unipc_geom
  *                                               the same with G_{A->v} computed on the fly
  *   coverage schedule    gc_coverage_pairs, gc_coverage_init, gc_coverage_update, gc_coverage_select,
  *                        gc_coverage_score, gc_schedule_refresh_due
@@ -412,6 +412,21 @@ int gc_transport_reconstruct_geom(const void* x0_prev, const void* x0_anchor_new
                                   int C, const int32_t* anchors, int a, int K, int dtype, const gc_sampler* smp,
                                   double t, double t_next, void* x0_out, void* x_next, void* model_out,
                                   hipStream_t stream);
+
+/*
+ * The multistep variant of the on-the-fly step: Eq. 1 with G_{A->v} computed
+ * on the fly, then the UniPC corrector + predictor on the x0 history
+ * (gc_transport_unipc's update), in one pass.  Equals gc_build_correspondence
+ * + gc_transport_unipc bit for bit.  Arguments as for gc_transport_unipc and
+ * gc_transport_reconstruct_geom: m_{k-1} is x0_prev; x_c may be x_prev and
+ * x_next may be x_cur, no other output may overlap an input or another
+ * output.
+ */
+int gc_transport_unipc_geom(const void* x0_prev, const void* x0_anchor_new, const float* pos, const gc_camera* cams,
+                            const float* bbox, const uint32_t* fg_bits, const int32_t* fg_recs, int64_t n_fg,
+                            const void* x_cur, const void* x_prev, const void* m_km2, int B, int N, int H, int W,
+                            int C, const int32_t* anchors, int a, int K, int dtype, const gc_unipc_step* st,
+                            void* x0_out, void* x_c, void* x_next, hipStream_t stream);
 
 /*
  * Token staleness and the coverage-driven schedule.

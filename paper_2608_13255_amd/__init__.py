@@ -112,6 +112,8 @@ def lib() -> ctypes.CDLL:
             "gc_transport_reconstruct_geom": ([_vp, _vp, _vp, _vp, _vp, _vp, _vp, _i64, _vp, _i, _i, _i, _i, _i,
                                                _i32p, _i, _i, _i, ctypes.POINTER(_Sampler), ctypes.c_double,
                                                ctypes.c_double, _vp, _vp, _vp, _vp], _i),
+            "gc_transport_unipc_geom": ([_vp, _vp, _vp, _vp, _vp, _vp, _vp, _i64, _vp, _vp, _vp, _i, _i, _i, _i, _i,
+                                         _i32p, _i, _i, _i, ctypes.POINTER(UniPCStep), _vp, _vp, _vp, _vp], _i),
             "gc_coverage_pair_words": ([_i, _i, _i, _i], _i64),
             "gc_coverage_pairs": ([_vp, _vp, _vp, _i, _i, _i, _i, _vp, _vp], _i),
             "gc_coverage_init": ([_vp, _i, _i, _i, _i, _vp, _vp], _i),
@@ -554,6 +556,31 @@ def gc_transport_unipc(x0_prev: torch.Tensor, x0_anchor_new: torch.Tensor, corr:
                                     B, N, H, W, C, arr, a, K, dtype_code(x0_prev), ctypes.byref(st),
                                     _dev(x0_out, "x0_out"), _dev(x_c, "x_c"), _dev(x_next, "x_next"),
                                     _stream(stream)), "gc_transport_unipc")
+    return x0_out, x_c, x_next
+
+
+def gc_transport_unipc_geom(x0_prev: torch.Tensor, x0_anchor_new: torch.Tensor, pos: torch.Tensor,
+                            cams: torch.Tensor, bbox: torch.Tensor, anchors: Sequence[int], K: int, st: UniPCStep,
+                            x_cur: torch.Tensor = None, x_prev: torch.Tensor = None, m_km2: torch.Tensor = None,
+                            x0_out: torch.Tensor = None, x_c: torch.Tensor = None, x_next: torch.Tensor = None,
+                            fg_index: ForegroundIndex = None, stream=None):
+    """gc_transport_unipc with G_{A->v} computed on the fly; returns
+    (x0_out, x_c, x_next).  `fg_index` (gc_index_foreground of pos) selects
+    the foreground launch."""
+    (B, N, H, W, C), arr, a = _geom_inputs(x0_prev, x0_anchor_new, pos, cams, bbox, anchors)
+    for name, t in (("x_cur", x_cur), ("x_prev", x_prev), ("m_km2", m_km2)):
+        if t is not None and (t.shape != x0_prev.shape or t.dtype != x0_prev.dtype):
+            raise ValueError(f"{name} must match x0_prev in shape and dtype")
+    x0_out = torch.empty_like(x0_prev) if x0_out is None else x0_out
+    x_c = torch.empty_like(x0_prev) if x_c is None else x_c
+    x_next = torch.empty_like(x0_prev) if x_next is None else x_next
+    fb, fr, nf = _fg_args(fg_index)
+    _check(lib().gc_transport_unipc_geom(_dev(x0_prev, "x0_prev"), _dev(x0_anchor_new, "x0_anchor_new"),
+                                         _dev(pos, "pos"), _dev(cams, "cams"), _dev(bbox, "bbox"), fb, fr, nf,
+                                         _opt(x_cur, "x_cur"), _opt(x_prev, "x_prev"), _opt(m_km2, "m_km2"),
+                                         B, N, H, W, C, arr, a, K, dtype_code(x0_prev), ctypes.byref(st),
+                                         _dev(x0_out, "x0_out"), _dev(x_c, "x_c"), _dev(x_next, "x_next"),
+                                         _stream(stream)), "gc_transport_unipc_geom")
     return x0_out, x_c, x_next
 
 

@@ -50,7 +50,9 @@ namespace {
 constexpr int kBlock = 256;
 static_assert(GC_MAX_VIEWS <= 256 && GC_MAX_ANCHORS <= 8, "view_bytes holds one byte per anchor slot");
 
-enum GeomMode { kGeomTransport = 0, kGeomReconstruct = 1 };
+// What a step does after the transport: nothing, the sampler reconstruction,
+// or the UniPC corrector + predictor on the x0 history.
+enum GeomMode { kGeomTransport = 0, kGeomReconstruct = 1, kGeomUniPC = 2 };
 
 struct GArgs {
   const void* x0_prev;
@@ -74,6 +76,11 @@ struct GArgs {
   int32_t sorted_anchor[GC_MAX_ANCHORS];   // anchor views ascending, padded with INT_MAX
   uint64_t view_bytes;                     // byte s: view of anchor slot s
   Recon r;
+  // UniPC mode: x_t is x_cur; x_prev / m_km2 inputs, x_c output
+  const void* x_prev;
+  const void* m_km2;
+  void* x_c;
+  UniCoef u;
   // foreground launch
   const uint32_t* fg_bits;   // bit per token of [B][N][H][W]: finite position
   const int4* fg_recs;       // [n_fg] {token, x, y, z}, ascending token
@@ -85,6 +92,56 @@ struct GArgs {
 };
 
 constexpr int kMaxCamLds = 64;   // (asset, anchor slot) cameras a list block can stage
+
+// An item's own inputs besides its x0_prev: x_t for the reconstruction; for
+// UniPC x_prev (corrector) or x_cur, m_{k-2}, and m_{k-1} (an anchor row
+// loads its x0_prev here; a target token's is the x0_prev it reads anyway).
+template <int DT, int VEC> struct Side {
+  typename Codec<DT, VEC>::Raw xin, m2, m1;
+};
+
+template <int DT, int VEC, int MODE>
+__device__ __forceinline__ Side<DT, VEC> load_side(const GArgs& g, int64_t e, bool anchor_row) {
+  using CD = Codec<DT, VEC>;
+  Side<DT, VEC> sd{};
+  if constexpr (MODE == kGeomReconstruct) sd.xin = CD::load_stream(g.x_t, e);
+  if constexpr (MODE == kGeomUniPC) {
+    sd.xin = CD::load_stream(g.u.corr ? g.x_prev : g.x_t, e);
+    if (g.u.need_m2) sd.m2 = CD::load_stream(g.m_km2, e);
+    if (anchor_row && g.u.need_m1) sd.m1 = CD::load_stream(g.x0_prev, e);
+  }
+  return sd;
+}
+
+// Stores a token's channel vector: x0 as given, then (reconstruction) the
+// sampler step from x_t and that x0 as stored, or (UniPC) the corrector and
+// predictor with m_k = that x0 as stored.
+template <int DT, int VEC, int MODE>
+__device__ __forceinline__ void finish_item(const GArgs& g, int64_t e, const typename Codec<DT, VEC>::Raw& x0r,
+                                            const Side<DT, VEC>& sd) {
+  using CD = Codec<DT, VEC>;
+  CD::store_stream(g.x0_out, e, x0r);
+  if constexpr (MODE == kGeomReconstruct) {
+    float xtf[VEC], x0f[VEC], xn[VEC], mo[VEC];
+    CD::unpack(x0r, x0f);   // the reconstruction reads x0 as stored
+    CD::unpack(sd.xin, xtf);
+    reconstruct_vec<VEC>(g.r, xtf, x0f, xn, mo);
+    CD::store_stream(g.x_next, e, CD::pack(xn));
+    if (g.model_out) CD::store_stream(g.model_out, e, CD::pack(mo));
+  }
+  if constexpr (MODE == kGeomUniPC) {
+    float xin[VEC], m2[VEC], m1[VEC], mk[VEC], xc[VEC], xn[VEC];
+    CD::unpack(sd.xin, xin);
+    CD::unpack(x0r, mk);
+#pragma unroll
+    for (int q = 0; q < VEC; ++q) m2[q] = m1[q] = 0.0f;
+    if (g.u.need_m2) CD::unpack(sd.m2, m2);
+    if (g.u.need_m1) CD::unpack(sd.m1, m1);
+    unipc_vec<VEC>(g.u, xin, m2, m1, mk, xc, xn);
+    CD::store_stream(g.x_c, e, CD::pack(xc));
+    CD::store_stream(g.x_next, e, CD::pack(xn));
+  }
+}
 
 // G lanes per target token; AMAX (4 or 8) bounds the anchor count, so each
 // lane evaluates up to AMAX / G anchor slots.
@@ -115,18 +172,9 @@ __global__ __launch_bounds__(kBlock) void k_transport_geom(GArgs g) {
       c = t - p * g.CV;
     }
     const int64_t e = (((int64_t)b * g.N + g.anchor_view[s]) * g.HW + p) * g.C + (int64_t)c * VEC;
-    Raw xtr;
-    if constexpr (MODE == kGeomReconstruct) xtr = CD::load_stream(g.x_t, e);
+    const Side<DT, VEC> sd = load_side<DT, VEC, MODE>(g, e, true);
     const Raw x0r = CD::load(g.x0_new, ((int64_t)bs * g.HW + p) * g.C + (int64_t)c * VEC);
-    CD::store_stream(g.x0_out, e, x0r);
-    if constexpr (MODE == kGeomReconstruct) {
-      float xtf[VEC], x0f[VEC], xn[VEC], mo[VEC];
-      CD::unpack(xtr, xtf);
-      CD::unpack(x0r, x0f);
-      reconstruct_vec<VEC>(g.r, xtf, x0f, xn, mo);
-      CD::store_stream(g.x_next, e, CD::pack(xn));
-      if (g.model_out) CD::store_stream(g.model_out, e, CD::pack(mo));
-    }
+    finish_item<DT, VEC, MODE>(g, e, x0r, sd);
     return;
   }
   const int lb = logical_block((int)blockIdx.x, g.n_tblocks, 1);
@@ -261,9 +309,9 @@ __global__ __launch_bounds__(kBlock) void k_transport_geom(GArgs g) {
       c = it - slot * g.CV;
     }
     const int64_t e = ((int64_t)bv * g.HW + s_tok[slot]) * g.C + (int64_t)c * VEC;
-    Raw xtr, prevr;
-    if constexpr (MODE == kGeomReconstruct) xtr = CD::load_stream(g.x_t, e);
-    prevr = CD::load_stream(g.x0_prev, e);
+    Side<DT, VEC> sd = load_side<DT, VEC, MODE>(g, e, false);
+    const Raw prevr = CD::load_stream(g.x0_prev, e);
+    sd.m1 = prevr;   // m_{k-1}: the token's own stored x0
     Raw x0r;
     if (slot < nv) {
       const float inv = (float)s_nvis[slot];
@@ -298,32 +346,7 @@ __global__ __launch_bounds__(kBlock) void k_transport_geom(GArgs g) {
     } else {
       x0r = prevr;   // no anchor sees this token: it keeps its own state
     }
-    CD::store_stream(g.x0_out, e, x0r);
-    if constexpr (MODE == kGeomReconstruct) {
-      float xtf[VEC], x0f[VEC], xn[VEC], mo[VEC];
-      CD::unpack(x0r, x0f);   // the reconstruction reads x0 as stored
-      CD::unpack(xtr, xtf);
-      reconstruct_vec<VEC>(g.r, xtf, x0f, xn, mo);
-      CD::store_stream(g.x_next, e, CD::pack(xn));
-      if (g.model_out) CD::store_stream(g.model_out, e, CD::pack(mo));
-    }
-  }
-}
-
-// Stores a token's channel vector: x0 as given and, when reconstructing, the
-// sampler step from x_t and that x0 as stored.
-template <int DT, int VEC, int MODE>
-__device__ __forceinline__ void finish_item(const GArgs& g, int64_t e, const typename Codec<DT, VEC>::Raw& x0r,
-                                            const typename Codec<DT, VEC>::Raw& xtr) {
-  using CD = Codec<DT, VEC>;
-  CD::store_stream(g.x0_out, e, x0r);
-  if constexpr (MODE == kGeomReconstruct) {
-    float xtf[VEC], x0f[VEC], xn[VEC], mo[VEC];
-    CD::unpack(x0r, x0f);   // the reconstruction reads x0 as stored
-    CD::unpack(xtr, xtf);
-    reconstruct_vec<VEC>(g.r, xtf, x0f, xn, mo);
-    CD::store_stream(g.x_next, e, CD::pack(xn));
-    if (g.model_out) CD::store_stream(g.model_out, e, CD::pack(mo));
+    finish_item<DT, VEC, MODE>(g, e, x0r, sd);
   }
 }
 
@@ -359,17 +382,18 @@ __global__ __launch_bounds__(kBlock) void k_transport_geom_fg(GArgs g) {
       c = t - p * g.CV;
     }
     const int64_t e = ((int64_t)bv * g.HW + p) * g.C + (int64_t)c * VEC;
-    Raw xtr{};
     if (s_self >= 0) {
-      if constexpr (MODE == kGeomReconstruct) xtr = CD::load_stream(g.x_t, e);
+      const Side<DT, VEC> sd = load_side<DT, VEC, MODE>(g, e, true);
       const Raw x0r = CD::load(g.x0_new, (((int64_t)b * g.a + s_self) * g.HW + p) * g.C + (int64_t)c * VEC);
-      finish_item<DT, VEC, MODE>(g, e, x0r, xtr);
+      finish_item<DT, VEC, MODE>(g, e, x0r, sd);
       return;
     }
     const int64_t tk = (int64_t)bv * g.HW + p;
     if ((g.fg_bits[tk >> 5] >> (tk & 31)) & 1u) return;
-    if constexpr (MODE == kGeomReconstruct) xtr = CD::load_stream(g.x_t, e);
-    finish_item<DT, VEC, MODE>(g, e, CD::load_stream(g.x0_prev, e), xtr);
+    Side<DT, VEC> sd = load_side<DT, VEC, MODE>(g, e, false);
+    const Raw prevr = CD::load_stream(g.x0_prev, e);
+    sd.m1 = prevr;
+    finish_item<DT, VEC, MODE>(g, e, prevr, sd);
     return;
   }
 
@@ -497,9 +521,9 @@ __global__ __launch_bounds__(kBlock) void k_transport_geom_fg(GArgs g) {
     }
     const int tk = s_tok[slot];
     const int64_t e = (int64_t)tk * g.C + (int64_t)c * VEC;   // latents are [B][N][H][W][C]
-    Raw xtr{};
-    if constexpr (MODE == kGeomReconstruct) xtr = CD::load_stream(g.x_t, e);
+    Side<DT, VEC> sd = load_side<DT, VEC, MODE>(g, e, false);
     const Raw prevr = CD::load_stream(g.x0_prev, e);
+    sd.m1 = prevr;   // m_{k-1}: the token's own stored x0
     Raw x0r;
     if (slot < nv) {
       const int ib = tk / g.HW / g.N;
@@ -535,7 +559,7 @@ __global__ __launch_bounds__(kBlock) void k_transport_geom_fg(GArgs g) {
     } else {
       x0r = prevr;   // no anchor sees this token: it keeps its own state
     }
-    finish_item<DT, VEC, MODE>(g, e, x0r, xtr);
+    finish_item<DT, VEC, MODE>(g, e, x0r, sd);
   }
 }
 
@@ -744,4 +768,49 @@ extern "C" int gc_transport_reconstruct_geom(const void* x0_prev, const void* x0
   g.model_out = model_out;
   launch_geom<kGeomReconstruct>(g, dtype, stream);
   return after_launch(stream, "gc_transport_reconstruct_geom");
+}
+
+extern "C" int gc_transport_unipc_geom(const void* x0_prev, const void* x0_anchor_new, const float* pos,
+                                       const gc_camera* cams, const float* bbox, const uint32_t* fg_bits,
+                                       const int32_t* fg_recs, int64_t n_fg, const void* x_cur, const void* x_prev,
+                                       const void* m_km2, int B, int N, int H, int W, int C, const int32_t* anchors,
+                                       int a, int K, int dtype, const gc_unipc_step* st, void* x0_out, void* x_c,
+                                       void* x_next, hipStream_t stream) {
+  clear_error();
+  GArgs g;
+  int rc = prepare_geom(x0_prev, x0_anchor_new, pos, cams, bbox, fg_bits, fg_recs, n_fg, B, N, H, W, C, anchors, a,
+                        K, dtype, x0_out, "gc_transport_unipc_geom", &g);
+  if (rc) return rc;
+  if (!st) return fail(GC_ERR_ARG, "gc_transport_unipc_geom: null coefficients");
+  if (!x_c || !x_next) return fail(GC_ERR_ARG, "gc_transport_unipc_geom: null x_c or x_next");
+  g.u = make_unicoef(*st);
+  if (g.u.corr && !x_prev) return fail(GC_ERR_ARG, "gc_transport_unipc_geom: the corrector needs x_prev");
+  if (!g.u.corr && !x_cur) return fail(GC_ERR_ARG, "gc_transport_unipc_geom: without the corrector x_cur is needed");
+  if (g.u.need_m2 && !m_km2) return fail(GC_ERR_ARG, "gc_transport_unipc_geom: the coefficients need m_{k-2}");
+  // m_{k-1} is x0_prev, the previous step's stored x0
+  const void* al[5] = {x_cur, x_prev, m_km2, x_c, x_next};
+  for (const void* q : al)
+    if (q && !aligned16(q)) return fail(GC_ERR_ALIGN, "gc_transport_unipc_geom: device pointers must be 16-byte aligned");
+  const size_t es = (size_t)dtype_bytes(dtype);
+  const size_t HW = (size_t)H * W;
+  const size_t n_all = (size_t)B * N * HW * C * es, n_new = (size_t)B * a * HW * C * es;
+  const void* ins[10] = {x0_prev, x0_anchor_new, x_cur, x_prev, m_km2, pos, cams, bbox, fg_bits, fg_recs};
+  const size_t lens[10] = {n_all, n_new, n_all, n_all, n_all, (size_t)B * N * HW * 12, (size_t)B * N * sizeof(gc_camera),
+                           (size_t)B * 32, ((size_t)B * N * HW + 31) / 32 * 4, (size_t)n_fg * 16};
+  for (int i = 0; i < 10; ++i) {
+    if (!ins[i]) continue;
+    if ((ins[i] != x_cur && overlaps(x_next, n_all, ins[i], lens[i])) ||
+        (ins[i] != x_prev && overlaps(x_c, n_all, ins[i], lens[i])) || overlaps(x0_out, n_all, ins[i], lens[i]))
+      return fail(GC_ERR_ALIAS,
+                  "gc_transport_unipc_geom: outputs overlap inputs (only x_c == x_prev, x_next == x_cur)");
+  }
+  if (overlaps(x_c, n_all, x_next, n_all) || overlaps(x_c, n_all, x0_out, n_all) || overlaps(x_next, n_all, x0_out, n_all))
+    return fail(GC_ERR_ALIAS, "gc_transport_unipc_geom: outputs overlap each other");
+  g.x_t = x_cur;
+  g.x_prev = x_prev;
+  g.m_km2 = m_km2;
+  g.x_c = x_c;
+  g.x_next = x_next;
+  launch_geom<kGeomUniPC>(g, dtype, stream);
+  return after_launch(stream, "gc_transport_unipc_geom");
 }

@@ -1,7 +1,7 @@
 // Device helpers of the per-step kernels: the latent storage codec
 // (float32 / bfloat16 vectors, cached or nontemporal access), the sampler
-// step from x_t and x0 (Sec. 3.2, the paragraph after Eq. 1), and the
-// XCD-aware block order.
+// step from x_t and x0 (Sec. 3.2, the paragraph after Eq. 1), the UniPC
+// update on the x0 history, and the XCD-aware block order.
 #pragma once
 
 #include "gc_common.h"
@@ -94,6 +94,42 @@ __device__ __forceinline__ void reconstruct_vec(const Recon& r, const float (&xt
       xn[e] = xt[e] + r.dsigma * vel;
       mo[e] = vel;
     }
+  }
+}
+
+// UniPC coefficients of one step (gc_unipc_coeffs, computed in double),
+// rounded once to float, and which of the history inputs they read.
+struct UniCoef {
+  int32_t corr, need_m1, need_m2;
+  float c_xprev, c_mk2, c_mk1, c_mk, p_xc, p_mk1, p_mk;
+};
+
+inline UniCoef make_unicoef(const gc_unipc_step& st) {
+  UniCoef u;
+  u.corr = st.use_corrector ? 1 : 0;
+  u.need_m2 = (u.corr && st.c_mk2 != 0.0) ? 1 : 0;
+  u.need_m1 = ((u.corr && st.c_mk1 != 0.0) || st.p_mk1 != 0.0) ? 1 : 0;
+  u.c_xprev = (float)st.c_xprev;
+  u.c_mk2 = (float)st.c_mk2;
+  u.c_mk1 = (float)st.c_mk1;
+  u.c_mk = (float)st.c_mk;
+  u.p_xc = (float)st.p_xc;
+  u.p_mk1 = (float)st.p_mk1;
+  u.p_mk = (float)st.p_mk;
+  return u;
+}
+
+// UniPC corrector (or the start sample) and predictor, fixed float order:
+//   x_c = ((c_xprev x_prev + c_mk2 m_{k-2}) + c_mk1 m_{k-1}) + c_mk m_k   (corrector)
+//   x_next = (p_xc x_c + p_mk1 m_{k-1}) + p_mk m_k
+template <int VEC>
+__device__ __forceinline__ void unipc_vec(const UniCoef& u, const float (&xin)[VEC], const float (&m2)[VEC],
+                                          const float (&m1)[VEC], const float (&mk)[VEC], float (&xc)[VEC],
+                                          float (&xn)[VEC]) {
+#pragma unroll
+  for (int e = 0; e < VEC; ++e) {
+    xc[e] = u.corr ? ((u.c_xprev * xin[e] + u.c_mk2 * m2[e]) + u.c_mk1 * m1[e]) + u.c_mk * mk[e] : xin[e];
+    xn[e] = (u.p_xc * xc[e] + u.p_mk1 * m1[e]) + u.p_mk * mk[e];
   }
 }
 

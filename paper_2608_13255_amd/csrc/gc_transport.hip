@@ -52,27 +52,12 @@ struct TArgs {
   const void* x_prev;
   const void* m_km2;
   void* x_c;
-  int32_t u_corr, u_need_m1, u_need_m2;
-  float uc_xprev, uc_mk2, uc_mk1, uc_mk, up_xc, up_mk1, up_mk;
+  UniCoef u;
 };
 
 // What a step does after the transport: nothing, the sampler reconstruction
 // (DDIM / flow Euler), or the UniPC corrector + predictor.
 enum StepMode { kTransportOnly = 0, kReconstruct = 1, kUniPC = 2 };
-
-// UniPC corrector (or the start sample) and predictor, fixed float order:
-//   x_c = ((c_xprev x_prev + c_mk2 m_{k-2}) + c_mk1 m_{k-1}) + c_mk m_k   (corrector)
-//   x_next = (p_xc x_c + p_mk1 m_{k-1}) + p_mk m_k
-template <int VEC>
-__device__ __forceinline__ void unipc_vec(const TArgs& g, const float (&xin)[VEC], const float (&m2)[VEC],
-                                          const float (&m1)[VEC], const float (&mk)[VEC], float (&xc)[VEC],
-                                          float (&xn)[VEC]) {
-#pragma unroll
-  for (int e = 0; e < VEC; ++e) {
-    xc[e] = g.u_corr ? ((g.uc_xprev * xin[e] + g.uc_mk2 * m2[e]) + g.uc_mk1 * m1[e]) + g.uc_mk * mk[e] : xin[e];
-    xn[e] = (g.up_xc * xc[e] + g.up_mk1 * m1[e]) + g.up_mk * mk[e];
-  }
-}
 
 // What the caller of token_step knows about a target token.
 enum TokenMode { kAnchorRow = 0, kTargetCheck = 1, kTargetSeen = 2, kTargetUnseen = 3 };
@@ -88,9 +73,9 @@ __device__ __forceinline__ void token_step(const TArgs& g, int b, int p, int cv,
   Raw xtr, m2r, m1r;
   if constexpr (MODE == kReconstruct) xtr = CD::load_stream(g.x_t, base);
   if constexpr (MODE == kUniPC) {
-    xtr = CD::load_stream(g.u_corr ? g.x_prev : g.x_t, base);
-    if (g.u_need_m2) m2r = CD::load_stream(g.m_km2, base);
-    if (g.u_need_m1 && mode == kAnchorRow) m1r = CD::load_stream(g.x0_prev, base);
+    xtr = CD::load_stream(g.u.corr ? g.x_prev : g.x_t, base);
+    if (g.u.need_m2) m2r = CD::load_stream(g.m_km2, base);
+    if (g.u.need_m1 && mode == kAnchorRow) m1r = CD::load_stream(g.x0_prev, base);
   }
   Raw x0r;
   float x0f[VEC];
@@ -177,9 +162,9 @@ __device__ __forceinline__ void token_step(const TArgs& g, int b, int p, int cv,
     CD::unpack(xtr, xin);
 #pragma unroll
     for (int e = 0; e < VEC; ++e) m2[e] = m1[e] = 0.0f;
-    if (g.u_need_m2) CD::unpack(m2r, m2);
-    if (g.u_need_m1) CD::unpack(m1r, m1);
-    unipc_vec<VEC>(g, xin, m2, m1, x0f, xc, xn);
+    if (g.u.need_m2) CD::unpack(m2r, m2);
+    if (g.u.need_m1) CD::unpack(m1r, m1);
+    unipc_vec<VEC>(g.u, xin, m2, m1, x0f, xc, xn);
     CD::store_stream(g.x_c, base, CD::pack(xc));
     CD::store_stream(g.x_next, base, CD::pack(xn));
   }
@@ -286,13 +271,13 @@ __global__ __launch_bounds__(kBlock) void k_unipc(TArgs g, const void* __restric
   const int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x;
   if (i >= n_vec) return;
   float xin[VEC], m2[VEC], m1[VEC], mk[VEC], xc[VEC], xn[VEC];
-  CD::unpack(CD::load_stream(g.u_corr ? g.x_prev : g.x_t, i * VEC), xin);
+  CD::unpack(CD::load_stream(g.u.corr ? g.x_prev : g.x_t, i * VEC), xin);
 #pragma unroll
   for (int e = 0; e < VEC; ++e) m2[e] = m1[e] = 0.0f;
-  if (g.u_need_m2) CD::unpack(CD::load_stream(g.m_km2, i * VEC), m2);
-  if (g.u_need_m1) CD::unpack(CD::load_stream(g.x0_prev, i * VEC), m1);
+  if (g.u.need_m2) CD::unpack(CD::load_stream(g.m_km2, i * VEC), m2);
+  if (g.u.need_m1) CD::unpack(CD::load_stream(g.x0_prev, i * VEC), m1);
   CD::unpack(CD::load_stream(m_k, i * VEC), mk);
-  unipc_vec<VEC>(g, xin, m2, m1, mk, xc, xn);
+  unipc_vec<VEC>(g.u, xin, m2, m1, mk, xc, xn);
   CD::store_stream(g.x_c, i * VEC, CD::pack(xc));
   CD::store_stream(g.x_next, i * VEC, CD::pack(xn));
 }
@@ -417,26 +402,17 @@ void launch_transport(const TArgs& g, int dtype, hipStream_t stream) {
 int prepare_unipc(const gc_unipc_step* st, const void* x_cur, const void* x_prev, const void* m_km2,
                   const void* m_km1, const char* who, TArgs* g) {
   if (!st) return fail(GC_ERR_ARG, "%s: null coefficients", who);
-  g->u_corr = st->use_corrector ? 1 : 0;
-  g->u_need_m2 = (g->u_corr && st->c_mk2 != 0.0) ? 1 : 0;
-  g->u_need_m1 = ((g->u_corr && st->c_mk1 != 0.0) || st->p_mk1 != 0.0) ? 1 : 0;
-  if (g->u_corr && !x_prev) return fail(GC_ERR_ARG, "%s: the corrector needs x_prev", who);
-  if (!g->u_corr && !x_cur) return fail(GC_ERR_ARG, "%s: without the corrector x_cur is needed", who);
-  if (g->u_need_m2 && !m_km2) return fail(GC_ERR_ARG, "%s: the coefficients need m_{k-2}", who);
-  if (g->u_need_m1 && !m_km1) return fail(GC_ERR_ARG, "%s: the coefficients need m_{k-1}", who);
+  g->u = make_unicoef(*st);
+  if (g->u.corr && !x_prev) return fail(GC_ERR_ARG, "%s: the corrector needs x_prev", who);
+  if (!g->u.corr && !x_cur) return fail(GC_ERR_ARG, "%s: without the corrector x_cur is needed", who);
+  if (g->u.need_m2 && !m_km2) return fail(GC_ERR_ARG, "%s: the coefficients need m_{k-2}", who);
+  if (g->u.need_m1 && !m_km1) return fail(GC_ERR_ARG, "%s: the coefficients need m_{k-1}", who);
   const void* ins[4] = {x_cur, x_prev, m_km2, m_km1};
   for (const void* q : ins)
     if (q && !aligned16(q)) return fail(GC_ERR_ALIGN, "%s: device pointers must be 16-byte aligned", who);
   g->x_t = x_cur;
   g->x_prev = x_prev;
   g->m_km2 = m_km2;
-  g->uc_xprev = (float)st->c_xprev;
-  g->uc_mk2 = (float)st->c_mk2;
-  g->uc_mk1 = (float)st->c_mk1;
-  g->uc_mk = (float)st->c_mk;
-  g->up_xc = (float)st->p_xc;
-  g->up_mk1 = (float)st->p_mk1;
-  g->up_mk = (float)st->p_mk;
   return GC_OK;
 }
 

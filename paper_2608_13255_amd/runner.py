@@ -22,7 +22,7 @@ from . import (GC_FULL_HEAD_MID_TAIL, GC_FULL_HEAD_TAIL_E, GC_FULL_PERIODIC, Sam
                gc_coverage_update, gc_coverage_workspace_bytes, gc_index_correspondence, gc_index_foreground,
                gc_posmap_bbox, gc_sampler_reconstruct, gc_sampler_step_times, gc_schedule_anchors, gc_schedule_full_steps,
                gc_schedule_refresh_due, gc_transport_reconstruct, gc_transport_reconstruct_geom, gc_transport_unipc,
-               gc_unipc_coeffs, gc_unipc_update)
+               gc_transport_unipc_geom, gc_unipc_coeffs, gc_unipc_update)
 
 Predict = Callable[[int, List[int]], torch.Tensor]
 
@@ -50,8 +50,6 @@ class GeoCacheRunner:
         index (built once here)."""
         if anchor_policy not in ("rotate", "coverage", "rotation_coverage"):
             raise ValueError("anchor_policy must be 'rotate', 'coverage' or 'rotation_coverage'")
-        if unipc_order and geom:
-            raise ValueError("the on-the-fly transport has no UniPC variant")
         self.pos, self.cams, self.a, self.K = pos, cams, a, K
         self.sampler, self.S = sampler, S
         self.full = list(full)
@@ -183,10 +181,16 @@ class GeoCacheRunner:
                                           m_km2=m2, m_km1=self.x0, stream=self.stream)
         else:
             views = self._anchors()
-            corr, wts, idx = self.operator(views)
-            mk, x_c, x_next = gc_transport_unipc(self.x0, predict(k, views).contiguous(), corr, wts, views, st,
-                                                 x_cur=self.x_t, x_prev=self.x_c if st.use_corrector else None,
-                                                 m_km2=m2, index=idx, stream=self.stream)
+            new = predict(k, views).contiguous()
+            x_prev = self.x_c if st.use_corrector else None
+            if self.geom:
+                mk, x_c, x_next = gc_transport_unipc_geom(self.x0, new, self.pos, self.cams, self.bbox, views, self.K,
+                                                          st, x_cur=self.x_t, x_prev=x_prev, m_km2=m2,
+                                                          fg_index=self.fg_index, stream=self.stream)
+            else:
+                corr, wts, idx = self.operator(views)
+                mk, x_c, x_next = gc_transport_unipc(self.x0, new, corr, wts, views, st, x_cur=self.x_t,
+                                                     x_prev=x_prev, m_km2=m2, index=idx, stream=self.stream)
         self.x0_km2, self.x0, self.x_c, self.x_t = self.x0, mk, x_c, x_next
         self._after(views, full)
         self.k += 1

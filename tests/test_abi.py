@@ -290,6 +290,33 @@ def test_geom_validation(gc, L):
     assert fused(fb=A6, nf=2) == -1
 
 
+def test_unipc_geom_validation(gc, L):
+    anchors = (ctypes.c_int32 * 2)(0, 3)
+    n = 1 * 6 * 8 * 8 * 16 * 2
+    st = gc.UniPCStep()
+    rc = L.gc_unipc_coeffs(ctypes.byref(gc.Sampler(kind=gc.GC_DDIM).c()), 10, 4, 2, 1, ctypes.byref(st))
+    assert rc == 0 and st.use_corrector == 1 and st.c_mk2 != 0.0
+
+    def call(xcur=A5 + 4 * n, xprev=A5 + 8 * n, m2=A5 + 12 * n, xc=A5 + 16 * n, xn=A5 + 20 * n, out=A5, s=st,
+             fb=None, fr=None, nf=0, pos=A2):
+        return L.gc_transport_unipc_geom(A0, A1, pos, A3, A4, fb, fr, nf, xcur, xprev, m2, 1, 6, 8, 8, 16, anchors, 2,
+                                         4, 1, ctypes.byref(s) if s is not None else None, out, xc, xn, None)
+
+    assert call(s=None) == -1 and "coefficients" in _err(L)
+    assert call(xprev=None) == -1 and "corrector" in _err(L)
+    assert call(m2=None) == -1 and "m_{k-2}" in _err(L)
+    assert call(xc=None) == -1
+    assert call(pos=None) == -1
+    assert call(xc=A5 + 16 * n + 4) == -4
+    assert call(xn=A0 + 64) == -5               # x_next overlaps x0_prev
+    assert call(xc=A5 + 4 * n) == -5            # x_c over x_cur (only x_prev allowed)
+    assert call(xn=A5 + 8 * n) == -5            # x_next over x_prev (only x_cur allowed)
+    assert call(xc=A5 + 20 * n) == -5           # x_c over x_next
+    assert call(out=A2) == -5                   # x0_out over the position maps
+    assert call(fb=A6, nf=3) == -1              # records missing
+    assert call(fb=A6, fr=A7, nf=5, xn=A7 - 64) == -5
+
+
 def test_error_message_is_per_thread(gc, L):
     """gc_last_error() reports the calling thread's last failure, also while
     another thread fails differently at the same time."""

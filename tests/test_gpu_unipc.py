@@ -151,3 +151,78 @@ def test_unipc_trajectory_headline_operating_point(gc, rule, E, expect):
     drift = float(np.abs(vals(runner.x_t, w.dtype) - synth.values(ref[-1]["x_t"], w.dtype)).max())
     print(f"UniPC-2 headline point: free-running drift after {S} steps: {drift:.3g}")
     assert drift <= 1e-4
+
+
+@pytest.mark.parametrize("w", [C2, C4, C5], ids=lambda w: w.name)
+@pytest.mark.parametrize("order,corrector,k", [(2, True, 4), (1, True, 1), (2, False, 5), (1, False, 0), (2, True, 9)])
+def test_transport_unipc_geom_equals_stored(gc, w, order, corrector, k):
+    """gc_transport_unipc_geom (blocked and foreground launches) equals
+    gc_build_correspondence + gc_transport_unipc bit for bit, for every
+    combination of the corrector and the history terms the coefficients
+    read; then with x_c written over x_prev and x_next over x_cur."""
+    if w is C5:
+        w = synth.shrink(C5, B=2)
+    P = latent_maps(w.name, B=w.B)
+    B = P.shape[0]
+    A = oracle.anchors(w.N, w.a, 2)
+    S = 10
+    g = torch.Generator(device=DEV).manual_seed(order * 10 + k)
+    tdt = torch.float32 if w.dtype == "f32" else torch.bfloat16
+    shape = (B, w.N, w.H, w.W, w.C)
+    lat = {n: (0.5 * torch.randn(shape, device=DEV, generator=g)).to(tdt) for n in ("m1", "xcur", "xprev", "m2")}
+    new = (0.5 * torch.randn((B, w.a, w.H, w.W, w.C), device=DEV, generator=g)).to(tdt)
+    Pd = torch.from_numpy(P).to(DEV)
+    cams = gc.camera_tensor(synth.batch_cameras(w), DEV)
+    bb = gc.gc_posmap_bbox(Pd, w.tol_frac)
+    corr, wts = gc.gc_build_correspondence(Pd, cams, A, w.K, bb)
+    fgi = gc.gc_index_foreground(Pd)
+    st = gc.gc_unipc_coeffs(gc.Sampler(kind=gc.GC_DDIM), S, k, order, corrector)
+    x_prev = lat["xprev"] if st.use_corrector else None
+    m2 = lat["m2"] if st.use_corrector and st.c_mk2 != 0.0 else None
+    iv = torch.int16 if w.dtype == "bf16" else torch.int32
+    ref = gc.gc_transport_unipc(lat["m1"], new, corr, wts, A, st, x_cur=lat["xcur"], x_prev=x_prev, m_km2=m2)
+    for fg in (None, fgi):
+        got = gc.gc_transport_unipc_geom(lat["m1"], new, Pd, cams, bb, A, w.K, st, x_cur=lat["xcur"], x_prev=x_prev,
+                                         m_km2=m2, fg_index=fg)
+        for a_, b_ in zip(got, ref):
+            assert torch.equal(a_.view(iv), b_.view(iv)), fg is not None
+    # in place: x_c over x_prev (with the corrector), x_next over x_cur
+    xc_buf = x_prev.clone() if x_prev is not None else torch.empty_like(lat["m1"])
+    xn_buf = lat["xcur"].clone()
+    _, xc, xn = gc.gc_transport_unipc_geom(lat["m1"], new, Pd, cams, bb, A, w.K, st, x_cur=xn_buf,
+                                           x_prev=xc_buf if x_prev is not None else None, m_km2=m2, x_c=xc_buf,
+                                           x_next=xn_buf, fg_index=fgi)
+    assert xc.data_ptr() == xc_buf.data_ptr() and xn.data_ptr() == xn_buf.data_ptr()
+    assert torch.equal(xc.view(iv), ref[1].view(iv)) and torch.equal(xn.view(iv), ref[2].view(iv))
+
+
+def test_unipc_runner_geom_equals_stored(gc):
+    """A whole UniPC-2 trajectory (10 steps, four full) with the operator
+    computed on the fly (foreground launch) equals the stored operator's,
+    bit for bit, also under the coverage policy."""
+    from paper_2608_13255_amd.runner import GeoCacheRunner
+    w = synth.shrink(C4, S=10)
+    P_np = latent_maps(C4.name)
+    P = torch.from_numpy(P_np).to(DEV)
+    cams = gc.camera_tensor(synth.batch_cameras(w), DEV)
+    full = GeoCacheRunner.full_steps("head_mid_tail", 10)
+    preds = {}
+
+    def predict(k, views):
+        key = (k, tuple(views))
+        if key not in preds:
+            preds[key] = to_dev(synth.storage(synth.x0_state(w, P_np, k, views=views), w.dtype), w.dtype)
+        return preds[key]
+
+    xt0 = to_dev(synth.storage(synth.eps_noise(w, 0), w.dtype), w.dtype)
+    for policy in ("rotate", "coverage"):
+        res = []
+        for geom in (False, True):
+            r = GeoCacheRunner(P, cams, w.a, w.K, gc.Sampler(kind=gc.GC_DDIM), 10, full, w.tol_frac, unipc_order=2,
+                               anchor_policy=policy, geom=geom)
+            r.start(xt0.clone())
+            hist = [r.step(predict) for _ in range(10)]
+            res.append((hist, r.x_t.clone(), r.x0.clone(), r.x_c.clone()))
+        assert res[0][0] == res[1][0], policy
+        for a_, b_ in zip(res[0][1:], res[1][1:]):
+            assert torch.equal(a_.view(torch.int16), b_.view(torch.int16)), policy
