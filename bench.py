@@ -403,6 +403,19 @@ def main():
     fg_targets = int(torch.isfinite(pos[:, targets0]).all(-1).sum().item())
     gbytes_fg = B * (4 * N + a) * latent_view + n_tok // 8 + 16 * fg_targets + 12 * B * a * HW
     rows["geom_fg_fused_GBps"] = gbytes_fg / (rows["geom_fg_fused_ms"] * 1e-3) / 1e9
+    # the on-the-fly UniPC-2 step (foreground launch), the multistep row's inputs
+    ubufs = [(b, b["x_t"].clone(), b["x0_prev"].clone(), torch.empty_like(b["x0_prev"])) for b in ring[:2]]
+    ui = iter(range(1 << 30))
+
+    def unipc_geom_call():
+        b, xp, m2, xc = ubufs[next(ui) % len(ubufs)]
+        gc.gc_transport_unipc_geom(b["x0_prev"], b["x0_new"], pos, cams, bbox, A0, K, ust, x_prev=xp, m_km2=m2,
+                                   x0_out=b["x0_out"], x_c=xc, x_next=b["x_next"], fg_index=fgi)
+
+    rows["unipc_geom_fg_fused_ms"] = timed(unipc_geom_call)
+    ugbytes = B * (6 * N + a) * latent_view + n_tok // 8 + 16 * fg_targets + 12 * B * a * HW
+    rows["unipc_geom_fg_fused_GBps"] = ugbytes / (rows["unipc_geom_fg_fused_ms"] * 1e-3) / 1e9
+    del ubufs
     # K = 1 (the paper's ablation finds one tap as good as four): the same step
     # with a one-tap operator
     corr1, wts1 = gc.gc_build_correspondence(pos, cams, A0, 1, bbox)
