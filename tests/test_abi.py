@@ -56,6 +56,15 @@ def test_exports_match_header(L):
     assert L.gc_abi_version() == header_abi_version()
 
 
+def test_binding_types_every_entry_point(L):
+    """The Python binding declares argument and result types for every
+    function the header declares (ctypes would otherwise pass them untyped)."""
+    for name in header_functions():
+        f = getattr(L, name)
+        assert f.argtypes is not None, name
+        assert f.restype is not None, name
+
+
 def test_struct_layouts(gc):
     assert gc.CAMERA_DTYPE.itemsize == 68
     assert ctypes.sizeof(gc._Sampler) == 32
