@@ -1,6 +1,6 @@
-// Cached step with the correspondence computed on the fly: Eq. 1 (and the
-// sampler reconstruction) reading the position maps and cameras directly
-// instead of a stored G_{A->v}.  The operator is a function of the position
+// Cached step with the correspondence computed on the fly: Eq. 1 (and then
+// the sampler reconstruction or the UniPC update) reading the position maps
+// and cameras directly instead of a stored G_{A->v}.  The operator is a function of the position
 // maps and cameras only (Sec. 3.2, correspondence operator), so it can be
 // rebuilt inside the step from 12 bytes of position per target token plus
 // the anchors' position taps; nothing has to be built or stored per anchor
@@ -19,7 +19,8 @@
 // whole waves while the other waves only stream, as in the stored-operator
 // split launch.  A visible item blends its anchors in ascending slot order
 // with the builder's stored weights (w_k / n_vis in float), so the result
-// equals gc_build_correspondence followed by gc_transport_step bit for bit.
+// equals gc_build_correspondence followed by gc_transport_step (or the fused
+// reconstruction / UniPC calls) bit for bit.
 //
 // Blocked launch (no foreground index): the target-view blocks, whose
 // dependent loads (position, the anchors' position taps, then the latent
