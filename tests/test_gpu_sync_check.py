@@ -31,6 +31,11 @@ xt = torch.randn((1, 6, 64, 64, 4), generator=g).cuda()
 smp = gc.Sampler(kind=gc.GC_DDIM, pred_out=gc.GC_PRED_EPS)
 outs = list(gc.gc_transport_reconstruct(prev, new, corr, wts, xt, A, smp, 700, 660, index=idx))
 outs += list(gc.gc_transport_reconstruct_geom(prev, new, P, cams, bb, xt, A, 4, smp, 700, 660))
+fgi = gc.gc_index_foreground(P)
+outs += list(gc.gc_transport_reconstruct_geom(prev, new, P, cams, bb, xt, A, 4, smp, 700, 660, fg_index=fgi))
+ust = gc.gc_unipc_coeffs(gc.Sampler(kind=gc.GC_DDIM), 10, 4, 2, True)
+outs += list(gc.gc_transport_unipc_geom(prev, new, P, cams, bb, A, 4, ust, x_prev=xt, m_km2=prev, fg_index=fgi))
+outs += [fgi.fg_bits, fgi.fg_recs[:fgi.n_fg]]
 pairs = gc.gc_coverage_pairs(P, cams, bb)
 stale = gc.gc_coverage_init(P)
 stats = gc.gc_coverage_update(pairs, stale, A, 2)
