@@ -1,21 +1,27 @@
 // Per-step kernels: delta transport (Eq. 1), sampler-consistent
-// reconstruction, and the two fused into one pass.
+// reconstruction, the two fused into one pass, and the multistep variant
+// (Eq. 1 fused with the UniPC corrector + predictor on the x0 history).
 //
-// All three are HBM-streaming: each latent element is read and written once;
-// the only reuse is the gather of anchor taps, which neighbouring target
-// tokens share and which stays in L2.  No MFMA: nothing here is a dense
-// contraction.
+// All of them are HBM-streaming: each latent element is read and written
+// once; the only reuse is the gather of anchor taps, which neighbouring
+// target tokens share and which stays in L2.  No MFMA: nothing here is a
+// dense contraction.
 //
 // Work mapping: one thread per (asset, view, pixel, channel vector); a
 // channel vector is 16 bytes (4 floats or 8 bfloat16; 4 bfloat16 when C is
 // not a multiple of 8), so every latent access is one 16-byte (or 8-byte)
 // load/store, consecutive lanes touch consecutive addresses, and the threads
 // of one pixel share its correspondence words and weights through L1.
-// Blocks that gather are remapped so that each of the 8 XCDs processes one
-// contiguous slice of the (asset, view, pixel) space: an XCD then gathers
-// from only its own assets' anchor views, which fit its L2.  Data each thread touches once
-// (its own x0_prev and x_t, every output) is read and written with
-// nontemporal hints; only the gathered anchor tiles go through L2 normally.
+//
+// Dense launch (no visible-token index): every block tiles (asset, view)
+// rows and each target thread reads its token's words.  Split launch (with
+// gc_index_correspondence's index): gather blocks over the compact list of
+// visible tokens come first, in XCD-contiguous slices so that an XCD gathers
+// from only its own assets' anchor views, which fit its L2; streaming blocks
+// over all rows follow in the hardware's round-robin order and skip the
+// visible tokens by their bit.  Data each thread touches once (its own
+// x0_prev and x_t, every output) is read and written with nontemporal hints;
+// only the gathered anchor tiles go through L2 normally.
 #include "gc_common.h"
 #include "gc_latent.h"
 
