@@ -394,7 +394,9 @@ int gc_transport_unipc(const void* x0_prev, const void* x0_anchor_new, const int
  *          read back to the host); fg_bits and fg_recs null and n_fg 0 for the
  *          blocked launch.  With the index, only the listed tokens of the
  *          target views run the operator and every other token is streamed;
- *          the result is bit-identical either way.  A record whose token lies
+ *          the result is bit-identical either way.  The index must be the one
+ *          built from these position maps: a target token whose bit is set is
+ *          written only through its record.  A record whose token lies
  *          outside [0, B*N*H*W) is ignored.  The index is used when B * a <= 64
  *          (the launch stages every (asset, anchor) camera); otherwise the
  *          blocked launch runs.
