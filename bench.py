@@ -669,15 +669,33 @@ def oracle_step_rate(w, hi_np, seconds):
     new = synth.storage(rs.standard_normal((w.B, len(A), w.H, w.W, w.C)).astype(np.float32), w.dtype)
     xt = synth.storage(rs.standard_normal((w.B, w.N, w.H, w.W, w.C)).astype(np.float32), w.dtype)
     reps = 0
-    t0 = time.perf_counter()
-    while True:
-        _, st = oracle.transport(prev, new, corr, wts, list(A), w.dtype)
-        oracle.reconstruct(xt, st, w.dtype, w.sampler, t, tn)
-        reps += 1
-        el = time.perf_counter() - t0
-        if el >= seconds:
-            break
+    with one_core():
+        t0 = time.perf_counter()
+        while True:
+            _, st = oracle.transport(prev, new, corr, wts, list(A), w.dtype)
+            oracle.reconstruct(xt, st, w.dtype, w.sampler, t, tn)
+            reps += 1
+            el = time.perf_counter() - t0
+            if el >= seconds:
+                break
     return reps * w.B * (w.N - len(A)) * w.H * w.W / el
+
+
+class one_core:
+    """Pins the calling thread to one host core while the oracle is timed
+    (the oracle is single-threaded); restores the previous affinity."""
+
+    def __enter__(self):
+        self.saved = None
+        if hasattr(os, "sched_getaffinity"):
+            self.saved = os.sched_getaffinity(0)
+            os.sched_setaffinity(0, {min(self.saved)})
+        return self
+
+    def __exit__(self, *exc):
+        if self.saved is not None:
+            os.sched_setaffinity(0, self.saved)
+        return False
 
 
 def cpu_baseline(w, hi0, cams_np, step, seconds):
@@ -700,14 +718,15 @@ def cpu_baseline(w, hi0, cams_np, step, seconds):
     xt = synth.storage(0.5 * x0_prev1, w.dtype)
     t, tn = oracle.step_times(w.sampler, w.S, 2)
     reps = 0
-    t0 = time.perf_counter()
-    while True:
-        _, st = oracle.transport(prev, new, corr, wts, A, w.dtype)
-        oracle.reconstruct(xt, st, w.dtype, w.sampler, t, tn)
-        reps += 1
-        el = time.perf_counter() - t0
-        if el >= seconds:
-            break
+    with one_core():
+        t0 = time.perf_counter()
+        while True:
+            _, st = oracle.transport(prev, new, corr, wts, A, w.dtype)
+            oracle.reconstruct(xt, st, w.dtype, w.sampler, t, tn)
+            reps += 1
+            el = time.perf_counter() - t0
+            if el >= seconds:
+                break
     vp = reps * (w.N - w.a) * w.H * w.W
     model = "unknown CPU"
     try:
@@ -720,7 +739,7 @@ def cpu_baseline(w, hi0, cams_np, step, seconds):
     visible = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else os.cpu_count()
     return {"value": vp / el, "unit": "view-pixels/s", "cores": 1, "kind": "oracle",
             "sample": f"{reps} cached steps of 1 of {w.B} assets ({w.N} views, {w.H}x{w.W}x{w.C} {w.dtype}, "
-                      f"a={w.a}, K={w.K}), transport + reconstruction, {el:.1f}s on one host thread",
+                      f"a={w.a}, K={w.K}), transport + reconstruction, {el:.1f}s on one host thread pinned to one core",
             "host": f"{model}; {visible} CPUs visible to the process"}
 
 
