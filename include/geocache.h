@@ -99,7 +99,11 @@ extern "C" {
 #define GC_FULL_HEAD_TAIL_E 2   /* steps 0, 1 and the last E steps */
 
 /*
- * A pinhole or orthographic camera (68 bytes, 4-byte aligned).
+ * A pinhole or orthographic camera (68 bytes, 4-byte aligned): the view
+ * camera into which the correspondence operator projects a target token's 3D
+ * point to find the anchor pixels that may see it (Sec. 3.2, correspondence
+ * operator).  The paper states no camera model; these two cover its
+ * renderers' perspective views and the orthographic rigs of the tests.
  * World -> camera: x_c = R * X + t, R row-major; camera axes x right, y down,
  * z forward.  Intrinsics are in latent-pixel units; pixel i spans [i, i+1).
  *   model 0 (pinhole):      u = fx * (x_c / z_c) + cx,  v = fy * (y_c / z_c) + cy,
@@ -266,7 +270,10 @@ int gc_index_foreground(const float* pos, int64_t n_tokens, uint32_t* fg_bits, i
  *                  optional index of corr from gc_index_correspondence (n_vis
  *                  read back to the host); both null for the plain launch.
  *                  With the index the visible tokens are processed by their own
- *                  blocks; the result is bit-identical either way.
+ *                  blocks; the result is bit-identical either way.  The index
+ *                  needs n_vis * CV <= 2^31 - 2048, CV being the channel
+ *                  vectors per token (C/4 for float32; C/8 for bfloat16 when 8
+ *                  divides C, else C/4); larger counts fail with GC_ERR_CAPACITY.
  *   x0_out         device [B][N][H][W][C]  output; must not overlap x0_prev or x0_anchor_new
  */
 int gc_transport_step(const void* x0_prev, const void* x0_anchor_new, const int32_t* corr,
@@ -299,7 +306,11 @@ int gc_sampler_reconstruct(const void* x_t, const void* x0, void* x_next, void* 
 
 /*
  * gc_transport_step followed by gc_sampler_reconstruct over all B*N views, in
- * one pass (one read of every input, one write of every output).  The
+ * one pass (one read of every input, one write of every output): the cached
+ * step of the loop order (Sec. 3.2: transport the anchors' increment, then
+ * reconstruct every view for the sampler) as one multi-view, multi-asset
+ * kernel, the remedy the paper names for a loop that has become launch-bound
+ * (Sec. 5, limitations).  The
  * optional index (vis_bits, vis_list, n_vis) is as for gc_transport_step.  The
  * reconstruction consumes x0_out as stored (rounded to the dtype), so the
  * result is bit-identical to the two separate calls.
@@ -399,7 +410,10 @@ int gc_transport_unipc(const void* x0_prev, const void* x0_anchor_new, const int
  *          written only through its record.  A record whose token lies
  *          outside [0, B*N*H*W) is ignored.  The index is used when B * a <= 64
  *          (the launch stages every (asset, anchor) camera); otherwise the
- *          blocked launch runs.
+ *          blocked launch runs.  It needs n_fg <= 2^31 - 2048 / G, G being
+ *          the channel vectors per token (as for gc_transport_step) rounded
+ *          up to a power of two, at most 8; larger counts fail with
+ *          GC_ERR_CAPACITY.
  * Other arguments as for gc_transport_step / gc_transport_reconstruct.
  * x0_out, x_next and model_out must not overlap any input (x_next may be
  * x_t); latents, pos, fg_bits and fg_recs 16-byte aligned.

@@ -653,6 +653,9 @@ int prepare_geom(const void* x0_prev, const void* x0_new, const float* pos, cons
     const int64_t bpv_s = ((int64_t)HW * g->CV + kBlock - 1) / kBlock;
     const int64_t ns = (int64_t)B * N * bpv_s;
     const int64_t gblocks = (gb + kXcds - 1) / kXcds * kXcds;
+    // a list lane's record index (block * tokens per block + lane / G) is a 32-bit int
+    if (gblocks * tok > (int64_t)0x7fffffff)
+      return fail(GC_ERR_CAPACITY, "%s: n_fg=%lld exceeds the list part's 2^31 records", who, (long long)n_fg);
     if (gblocks + ns > (int64_t)0x7fffffff) return fail(GC_ERR_CAPACITY, "%s: problem too large for one launch", who);
     g->fg_bits = fg_bits;
     g->fg_recs = reinterpret_cast<const int4*>(fg_recs);

@@ -365,7 +365,12 @@ int prepare_transport(const void* x0_prev, const void* x0_new, const int32_t* co
     g->vis_list = vis_list;
     g->n_vis = (int)n_vis;
     const int64_t gb = ((int64_t)n_vis * g->CV + kBlock - 1) / kBlock;
-    g->gblocks = (int)((gb + kXcds - 1) / kXcds * kXcds);
+    const int64_t gblocks = (gb + kXcds - 1) / kXcds * kXcds;
+    // a gather lane's item index (block * kBlock + lane) is a 32-bit int
+    if (gblocks * kBlock > (int64_t)0x7fffffff)
+      return fail(GC_ERR_CAPACITY, "%s: n_vis=%lld times %d channel vectors exceeds the gather part's 2^31 lanes", who,
+                  (long long)n_vis, g->CV);
+    g->gblocks = (int)gblocks;
     if ((int64_t)g->gblocks + nb > (int64_t)0x7fffffff - kXcds)
       return fail(GC_ERR_CAPACITY, "%s: problem too large for one launch", who);
   }

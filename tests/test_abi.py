@@ -346,3 +346,38 @@ def test_error_message_is_per_thread(gc, L):
     t2 = threading.Thread(target=worker, args=("dtype", 4, 7, -3, "dtype"))
     t1.start(); t2.start(); t1.join(); t2.join()
     assert not bad, bad
+
+
+def test_index_lane_counts_fit_32_bits(gc, L):
+    """The split launches number their gather / list lanes in 32 bits; index
+    sizes whose lane count would exceed 2^31 - 1 are rejected on the host
+    (GC_ERR_CAPACITY) before anything is launched, and sizes at the limit
+    pass that check (the calls below then stop at a missing x_t instead)."""
+    P = [(i + 1) << 40 for i in range(10)]       # fake addresses, 1 TiB apart: nothing overlaps
+    one = (ctypes.c_int32 * 1)(0)
+    # float32, C = 256: 64 channel vectors per token; 4 views of 4094^2 tokens, one anchor
+    B, N, H, W, C = 1, 4, 4094, 4094, 256
+    smp = gc.Sampler(kind=gc.GC_FLOW_EULER).c()
+
+    def step(nv):
+        return L.gc_transport_step(P[0], P[1], P[2], P[3], P[4], P[5], nv, B, N, H, W, C, one, 1, 4, 0, P[6], None)
+
+    def fused(nv):
+        return L.gc_transport_reconstruct(P[0], P[1], P[2], P[3], P[4], P[5], nv, None, B, N, H, W, C, one, 1, 4, 0,
+                                          ctypes.byref(smp), 0.5, 0.4, P[6], P[7], None, None)
+
+    assert step(2 ** 25) == -6 and "2^31" in _err(L)          # 2^25 * 64 lanes
+    assert step(2 ** 25 - 31) == -6                            # rounds up to 2^31 lanes
+    assert fused(2 ** 25 - 31) == -6
+    assert fused(2 ** 25 - 32) == -1 and "x_t" in _err(L)      # 2^31 - 2048 lanes: accepted
+    # the foreground launch: 8 lanes per record (C = 32 float32), 32 records per block
+    B, N, H, W, C = 19, 31, 1019, 3578, 32
+    n_tok = B * N * H * W
+    assert 2 ** 31 - 256 < n_tok < 2 ** 31
+
+    def geom(nf):
+        return L.gc_transport_reconstruct_geom(P[0], P[1], P[2], P[3], P[4], P[5], P[6], nf, None, B, N, H, W, C,
+                                               one, 1, 4, 0, ctypes.byref(smp), 0.5, 0.4, P[7], P[8], None, None)
+
+    assert geom(n_tok) == -6 and "n_fg" in _err(L)
+    assert geom(2 ** 31 - 256) == -1 and "x_t" in _err(L)
