@@ -22,7 +22,8 @@
  *   coverage schedule    gc_coverage_pairs, gc_coverage_init, gc_coverage_update, gc_coverage_select,
  *                        gc_coverage_score, gc_schedule_refresh_due
  *                                               token staleness, adaptive anchors and refresh
- *   host schedule        gc_schedule_anchors, gc_schedule_full_steps, gc_sampler_step_times
+ *   host schedule        gc_schedule_anchors, gc_schedule_full_steps, gc_sampler_step_times,
+ *                        gc_schedule_forced_views, gc_schedule_advance_gaps
  *
  * Conventions shared by every call
  *   - Every call returns GC_OK (0) or a negative GC_ERR_* code and never
@@ -63,7 +64,7 @@
 extern "C" {
 #endif
 
-#define GC_ABI_VERSION 2
+#define GC_ABI_VERSION 3
 
 /* limits */
 #define GC_MAX_VIEWS 64     /* views per asset */
@@ -509,6 +510,24 @@ int gc_coverage_select(const uint32_t* pair_bits, const uint8_t* stale, int B, i
 int gc_coverage_score(const uint32_t* pair_bits, const uint8_t* stale, int B, int N, int H, int W, const int32_t* sets,
                       int M, int a, uint64_t* scores, void* workspace, size_t ws_bytes, hipStream_t stream);
 int gc_schedule_refresh_due(const uint32_t* stats, int B, int N, double tau, int* due);
+
+/*
+ * Anchor gaps of the coverage-driven schedule (host; no device work).  The
+ * limitations section (Sec. 5) names adaptive anchor selection as the remedy
+ * for regions few anchors observe; a purely greedy choice can starve a view,
+ * so a caller may force views whose gap -- cached steps since the view was
+ * last an anchor (or predicted by a full step) -- reached max_gap, as
+ * gc_coverage_select's forced list.
+ * gc_schedule_forced_views: gap host int32 [N] (>= 0); writes to forced_out
+ *   (host int32, room for a) the views with gap >= max_gap, the longest gap
+ *   first, equal gaps in ascending view order, at most a of them, and their
+ *   number to *n_forced.  max_gap = 0 forces nothing.
+ * gc_schedule_advance_gaps: gap host int32 [N], updated in place after a step
+ *   whose denoiser predicted views[0..n_views): those views (every view when
+ *   full != 0) go to 0, the others grow by one (saturating at INT32_MAX).
+ */
+int gc_schedule_forced_views(const int32_t* gap, int N, int a, int max_gap, int32_t* forced_out, int* n_forced);
+int gc_schedule_advance_gaps(int32_t* gap, int N, const int32_t* views, int n_views, int full);
 
 /*
  * Host schedule (no device work).

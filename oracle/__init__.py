@@ -7,8 +7,10 @@ imports it and shares no code with it.
 Thin numpy/ctypes marshalling over oracle.c (plain single-threaded C, double
 precision for continuous outputs, float where a float decides an integer).
 Every arithmetic step lives in oracle.c and cites the paper there; this file
-adds only the trajectory loop, which strings the C steps together in the
-order of Sec. 3.2 ("Loop order") and Sec. 3.2 ("Drift-bounding schedule").
+adds only the trajectory loops, which string the C steps together in the
+order of Sec. 3.2 ("Loop order") and Sec. 3.2 ("Drift-bounding schedule"),
+and the integer rule of the coverage schedule's anchor gaps (forced_views,
+advance_gaps; Sec. 5, adaptive anchor selection).
 
 Latent arrays are float32 for dtype "f32" and uint16 bfloat16 bit patterns
 for dtype "bf16".
@@ -451,38 +453,48 @@ def refresh_due(stats: np.ndarray, tau: float) -> bool:
     return bool(rc)
 
 
-def trajectory_adaptive(x_t0: np.ndarray, stub, pos: np.ndarray, cams, K: int, tol_frac: float, dtype: str,
-                        kind: str, S: int, full: Sequence[int], a: int, policy: str = "coverage", max_gap: int = 0,
-                        tau: float = None, R: int = 2, steps: int = None):
-    """The cached loop of trajectory() with the coverage-driven schedule
-    (see oracle.c O9): a step is full when the schedule says so, on the first
-    step, or when refresh_due(stats of the previous step, tau); a cached
-    step's anchors come from coverage_select (policy "coverage", views whose
-    anchor gap reached max_gap forced first, longest gap first, then lower
-    view), from the rotation (policy "rotate"), or from the rotation's
-    distinct sets, the one with the largest coverage_score (policy
-    "rotation_coverage", ties to the earlier set).  After every step the
-    staleness is updated with the step's views (all views when full) and
-    each view's gap (cached steps since it was last an anchor) advances.
-    Records as trajectory() plus full, stale, stats and gap after the step."""
-    steps = S if steps is None else steps
-    B, N = pos.shape[0], pos.shape[1]
-    bb = bbox(pos, tol_frac)
-    seen = coverage_pairs(pos, cams, K, bb)
-    stale = coverage_init(pos)
-    stats = None
-    gap = [0] * N
-    cache = {}
-    x_t, x0_store, c = x_t0, None, 0
+def forced_views(gap: Sequence[int], a: int, max_gap: int) -> List[int]:
+    """Views that must be anchors of the next cached step (the limitations
+    section's adaptive anchor selection, as read in oracle.c O9): every view
+    whose gap -- cached steps since it was last an anchor -- has reached
+    max_gap (max_gap 0: no view is forced), the longest gap first, equal gaps
+    in ascending view order, at most a of them."""
+    if max_gap <= 0:
+        return []
+    due = [v for v in range(len(gap)) if gap[v] >= max_gap]
+    due.sort(key=lambda v: (-gap[v], v))
+    return due[:a]
+
+
+def advance_gaps(gap: Sequence[int], views: Sequence[int], full: bool) -> List[int]:
+    """Every view's gap after a step: 0 for the step's anchors (every view at
+    a full step, which predicts all of them), one more for the others."""
+    return [0 if (full or v in views) else g + 1 for v, g in enumerate(gap)]
+
+
+def schedule_adaptive(seen: np.ndarray, stale0: np.ndarray, full: Sequence[int], a: int, policy: str = "coverage",
+                      max_gap: int = 0, tau: float = None, R: int = 2, steps: int = None):
+    """The coverage-driven schedule alone (see oracle.c O9); it depends on
+    the visibility pairs and the staleness only, never on latent values.
+    Step k is full when full[k] says so, on the first step, or when
+    refresh_due(stats of the previous step, tau).  A cached step's anchors
+    come from the rotation over the cached-step counter (policy "rotate"),
+    from the rotation's distinct sets, the one with the largest
+    coverage_score (policy "rotation_coverage", ties to the earlier set), or
+    from coverage_select with forced_views first (policy "coverage").  After
+    every step the staleness is updated with the step's views (all views
+    when full) and the gaps advance.  seen: [N][B][N][H][W] pairs (as from
+    coverage_pairs); stale0: the initial staleness (coverage_init).
+    Returns per-step records: k, anchors, full, c (cached steps so far),
+    stale, stats and gap after the step."""
+    N = stale0.shape[1]
+    steps = len(full) if steps is None else steps
+    stale, stats, gap, c = stale0, None, [0] * N, 0
     out = []
     for k in range(steps):
-        t, tn = step_times(kind, S, k)
-        is_full = bool(full[k]) or x0_store is None or (tau is not None and stats is not None
-                                                        and refresh_due(stats, tau))
+        is_full = bool(full[k]) or k == 0 or (tau is not None and stats is not None and refresh_due(stats, tau))
         if is_full:
             A = list(range(N))
-            x0_state = stub(k, A)
-            x0_exact = (x0_state if dtype == "f32" else _bf16_values(x0_state)).astype(np.float64)
         else:
             if policy == "rotate":
                 A = anchors(N, a, c)
@@ -491,10 +503,36 @@ def trajectory_adaptive(x_t0: np.ndarray, stub, pos: np.ndarray, cams, K: int, t
                 sc = coverage_score(stale, seen, cands)
                 A = cands[int(np.argmax(sc))]           # first maximum: ties go to the earlier set
             else:
-                due = [v for v in range(N) if max_gap and gap[v] >= max_gap]
-                due = sorted(due, key=lambda v: (-gap[v], v))[:a]
-                A = coverage_select(stale, seen, a, forced=due)
+                A = coverage_select(stale, seen, a, forced=forced_views(gap, a, max_gap))
             c += 1
+        stale, stats = coverage_update(stale, seen, A, R)
+        gap = advance_gaps(gap, A, is_full)
+        out.append({"k": k, "anchors": list(A), "full": is_full, "c": c, "stale": stale.copy(),
+                    "stats": stats.copy(), "gap": list(gap)})
+    return out
+
+
+def trajectory_adaptive(x_t0: np.ndarray, stub, pos: np.ndarray, cams, K: int, tol_frac: float, dtype: str,
+                        kind: str, S: int, full: Sequence[int], a: int, policy: str = "coverage", max_gap: int = 0,
+                        tau: float = None, R: int = 2, steps: int = None):
+    """The cached loop of trajectory() with the coverage-driven schedule of
+    schedule_adaptive() (the visibility pairs from this geometry's own
+    builds).  Records as trajectory() plus full, stale, stats and gap after
+    the step."""
+    steps = S if steps is None else steps
+    bb = bbox(pos, tol_frac)
+    seen = coverage_pairs(pos, cams, K, bb)
+    sched = schedule_adaptive(seen, coverage_init(pos), full, a, policy, max_gap, tau, R, steps)
+    cache = {}
+    x_t, x0_store = x_t0, None
+    out = []
+    for d in sched:
+        k, A, is_full = d["k"], d["anchors"], d["full"]
+        t, tn = step_times(kind, S, k)
+        if is_full:
+            x0_state = stub(k, A)
+            x0_exact = (x0_state if dtype == "f32" else _bf16_values(x0_state)).astype(np.float64)
+        else:
             key = tuple(A)
             if key not in cache:
                 corr, w, _ = build(pos, cams, A, K, bb)
@@ -504,10 +542,9 @@ def trajectory_adaptive(x_t0: np.ndarray, stub, pos: np.ndarray, cams, K: int, t
         xn, _ = reconstruct(x_t, x0_state, dtype, kind, t, tn)
         x_t = store(xn, dtype)
         x0_store = x0_state
-        stale, stats = coverage_update(stale, seen, A, R)
-        gap = [0 if (is_full or v in A) else g + 1 for v, g in enumerate(gap)]
-        out.append({"k": k, "anchors": A, "full": is_full, "c": c, "x_t": x_t, "x0": x0_state, "x_t_exact": xn,
-                    "x0_exact": x0_exact, "stale": stale.copy(), "stats": stats.copy(), "gap": list(gap)})
+        out.append({"k": k, "anchors": A, "full": is_full, "c": d["c"], "x_t": x_t, "x0": x0_state,
+                    "x_t_exact": xn, "x0_exact": x0_exact, "stale": d["stale"], "stats": d["stats"],
+                    "gap": d["gap"]})
     return out
 
 

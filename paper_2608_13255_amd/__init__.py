@@ -21,7 +21,7 @@ import torch
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libgeocache.so")
-ABI_VERSION = 2   # GC_ABI_VERSION the binding is written for
+ABI_VERSION = 3   # GC_ABI_VERSION the binding is written for
 
 # constants mirrored from include/geocache.h
 GC_OK = 0
@@ -122,6 +122,8 @@ def lib() -> ctypes.CDLL:
             "gc_coverage_select": ([_vp, _vp, _i, _i, _i, _i, _i, _i32p, _i, _vp, _vp, ctypes.c_size_t, _vp], _i),
             "gc_schedule_refresh_due": ([_vp, _i, _i, ctypes.c_double, ctypes.POINTER(ctypes.c_int)], _i),
             "gc_coverage_score": ([_vp, _vp, _i, _i, _i, _i, _i32p, _i, _i, _vp, _vp, ctypes.c_size_t, _vp], _i),
+            "gc_schedule_forced_views": ([_i32p, _i, _i, _i, _i32p, ctypes.POINTER(ctypes.c_int)], _i),
+            "gc_schedule_advance_gaps": ([_i32p, _i, _i32p, _i, _i], _i),
             "gc_schedule_anchors": ([_i, _i, _i64, _i32p], _i),
             "gc_schedule_full_steps": ([_i, _i, _i, ctypes.POINTER(ctypes.c_uint8)], _i),
             "gc_sampler_step_times": ([ctypes.POINTER(_Sampler), _i, _i, ctypes.POINTER(ctypes.c_double),
@@ -726,6 +728,25 @@ def gc_schedule_refresh_due(stats_host, tau: float) -> bool:
     _check(lib().gc_schedule_refresh_due(st.ctypes.data, st.shape[0], st.shape[1], float(tau), ctypes.byref(due)),
            "gc_schedule_refresh_due")
     return bool(due.value)
+
+
+def gc_schedule_forced_views(gap: Sequence[int], a: int, max_gap: int) -> List[int]:
+    """Views whose anchor gap reached max_gap, longest gap first (ties: lower view), at most a."""
+    N = len(gap)
+    g = (ctypes.c_int32 * max(N, 1))(*[int(x) for x in gap])
+    out = (ctypes.c_int32 * max(a, 1))()
+    n = ctypes.c_int()
+    _check(lib().gc_schedule_forced_views(g, N, a, max_gap, out, ctypes.byref(n)), "gc_schedule_forced_views")
+    return list(out[:n.value])
+
+
+def gc_schedule_advance_gaps(gap: Sequence[int], views: Sequence[int], full: bool) -> List[int]:
+    """The anchor gaps after a step that predicted `views` (all views if full)."""
+    N = len(gap)
+    g = (ctypes.c_int32 * max(N, 1))(*[int(x) for x in gap])
+    arr, n = _anchors(views)
+    _check(lib().gc_schedule_advance_gaps(g, N, arr, n, int(bool(full))), "gc_schedule_advance_gaps")
+    return list(g[:N])
 
 
 def gc_schedule_anchors(N: int, a: int, c: int) -> List[int]:

@@ -180,6 +180,45 @@ int gc_schedule_refresh_due(const uint32_t* stats, int B, int N, double tau, int
   return GC_OK;
 }
 
+int gc_schedule_forced_views(const int32_t* gap, int N, int a, int max_gap, int32_t* forced_out, int* n_forced) {
+  clear_error();
+  if (!gap || !forced_out || !n_forced) return fail(GC_ERR_ARG, "forced views: null pointer");
+  if (N < 1 || N > GC_MAX_VIEWS) return fail(GC_ERR_CAPACITY, "forced views: N=%d outside [1, %d]", N, GC_MAX_VIEWS);
+  if (a < 1 || a > N) return fail(GC_ERR_ARG, "forced views: a=%d outside [1, N=%d]", a, N);
+  if (max_gap < 0) return fail(GC_ERR_ARG, "forced views: max_gap=%d is negative", max_gap);
+  for (int v = 0; v < N; ++v)
+    if (gap[v] < 0) return fail(GC_ERR_ARG, "forced views: gap[%d]=%d is negative", v, gap[v]);
+  *n_forced = 0;
+  if (max_gap == 0) return GC_OK;
+  // a rounds of "the due view with the longest gap, the lowest such view"
+  bool taken[GC_MAX_VIEWS] = {};
+  for (int r = 0; r < a; ++r) {
+    int best = -1;
+    for (int v = 0; v < N; ++v)
+      if (!taken[v] && gap[v] >= max_gap && (best < 0 || gap[v] > gap[best])) best = v;
+    if (best < 0) break;
+    taken[best] = true;
+    forced_out[(*n_forced)++] = best;
+  }
+  return GC_OK;
+}
+
+int gc_schedule_advance_gaps(int32_t* gap, int N, const int32_t* views, int n_views, int full) {
+  clear_error();
+  if (!gap || (n_views > 0 && !views)) return fail(GC_ERR_ARG, "advance gaps: null pointer");
+  if (N < 1 || N > GC_MAX_VIEWS) return fail(GC_ERR_CAPACITY, "advance gaps: N=%d outside [1, %d]", N, GC_MAX_VIEWS);
+  if (n_views < 0 || n_views > N) return fail(GC_ERR_ARG, "advance gaps: n_views=%d outside [0, N=%d]", n_views, N);
+  bool fresh[GC_MAX_VIEWS] = {};
+  for (int i = 0; i < n_views; ++i) {
+    if (views[i] < 0 || views[i] >= N) return fail(GC_ERR_ARG, "advance gaps: view %d outside [0, %d)", views[i], N);
+    fresh[views[i]] = true;
+  }
+  for (int v = 0; v < N; ++v)
+    if (gap[v] < 0) return fail(GC_ERR_ARG, "advance gaps: gap[%d]=%d is negative", v, gap[v]);
+  for (int v = 0; v < N; ++v) gap[v] = (full || fresh[v]) ? 0 : (gap[v] == INT32_MAX ? INT32_MAX : gap[v] + 1);
+  return GC_OK;
+}
+
 int gc_sampler_alpha_bar(const gc_sampler* smp, int t, double* abar) {
   clear_error();
   if (!smp || !abar) return fail(GC_ERR_ARG, "null argument");

@@ -20,9 +20,10 @@ import torch
 from . import (GC_FULL_HEAD_MID_TAIL, GC_FULL_HEAD_TAIL_E, GC_FULL_PERIODIC, Sampler, VisibleIndex,
                gc_build_correspondence, gc_coverage_init, gc_coverage_pairs, gc_coverage_score, gc_coverage_select,
                gc_coverage_update, gc_coverage_workspace_bytes, gc_index_correspondence, gc_index_foreground,
-               gc_posmap_bbox, gc_sampler_reconstruct, gc_sampler_step_times, gc_schedule_anchors, gc_schedule_full_steps,
-               gc_schedule_refresh_due, gc_transport_reconstruct, gc_transport_reconstruct_geom, gc_transport_unipc,
-               gc_transport_unipc_geom, gc_unipc_coeffs, gc_unipc_update)
+               gc_posmap_bbox, gc_sampler_reconstruct, gc_sampler_step_times, gc_schedule_advance_gaps,
+               gc_schedule_anchors, gc_schedule_forced_views, gc_schedule_full_steps, gc_schedule_refresh_due,
+               gc_transport_reconstruct, gc_transport_reconstruct_geom, gc_transport_unipc, gc_transport_unipc_geom,
+               gc_unipc_coeffs, gc_unipc_update)
 
 Predict = Callable[[int, List[int]], torch.Tensor]
 
@@ -127,15 +128,14 @@ class GeoCacheRunner:
             sc = gc_coverage_score(self.pairs, self.stale, self.rotation_sets, workspace=self._ws,
                                    stream=self.stream).cpu().tolist()
             return list(self.rotation_sets[sc.index(max(sc))])
-        due = [v for v in range(self.N) if self.max_gap and self.gap[v] >= self.max_gap]
-        due = sorted(due, key=lambda v: (-self.gap[v], v))[:self.a]
+        due = gc_schedule_forced_views(self.gap, self.a, self.max_gap)
         sel = gc_coverage_select(self.pairs, self.stale, self.a, forced=due, workspace=self._ws, stream=self.stream)
         return [int(v) for v in sel.cpu().tolist()]
 
     def _after(self, views: List[int], full: bool) -> None:
         """Staleness and anchor gaps after a step with the given views."""
         self.last_full = full
-        self.gap = [0 if (full or v in views) else g + 1 for v, g in enumerate(self.gap)]
+        self.gap = gc_schedule_advance_gaps(self.gap, views, full)
         if self.tracking:
             stats = gc_coverage_update(self.pairs, self.stale, views, self.refresh_R, stream=self.stream)
             self.stats_host = stats.cpu()

@@ -381,3 +381,40 @@ def test_index_lane_counts_fit_32_bits(gc, L):
 
     assert geom(n_tok) == -6 and "n_fg" in _err(L)
     assert geom(2 ** 31 - 256) == -1 and "x_t" in _err(L)
+
+
+def test_forced_views_and_gaps_host_calls(gc, L):
+    """The library's forced-view rule and gap counter (the runner's only
+    source for them) on the hand-derived toy cases, against the oracle's own
+    rule on random gaps, and their argument checks."""
+    assert gc.gc_schedule_forced_views([0, 1, 1], 1, 1) == [1]
+    assert gc.gc_schedule_forced_views([1, 0, 2], 3, 1) == [2, 0]
+    assert gc.gc_schedule_forced_views([3, 3, 3], 2, 2) == [0, 1]
+    assert gc.gc_schedule_forced_views([5, 5, 5], 3, 0) == []
+    assert gc.gc_schedule_advance_gaps([1, 0, 2], [2], False) == [2, 1, 0]
+    assert gc.gc_schedule_advance_gaps([1, 0, 2], [], True) == [0, 0, 0]
+    assert gc.gc_schedule_advance_gaps([2 ** 31 - 1, 0], [1], False) == [2 ** 31 - 1, 0]
+    rs = np.random.default_rng(3)
+    for _ in range(300):
+        N = int(rs.integers(1, 13))
+        a = int(rs.integers(1, N + 1))
+        gap = [int(x) for x in rs.integers(0, 5, N)]
+        mg = int(rs.integers(0, 4))
+        assert gc.gc_schedule_forced_views(gap, a, mg) == oracle.forced_views(gap, a, mg)
+        views = sorted(set(int(x) for x in rs.integers(0, N, int(rs.integers(0, N + 1)))))
+        full = bool(rs.integers(0, 2))
+        assert gc.gc_schedule_advance_gaps(gap, views, full) == oracle.advance_gaps(gap, views, full)
+    g = (ctypes.c_int32 * 3)(0, 1, 2)
+    out = (ctypes.c_int32 * 3)()
+    n = ctypes.c_int()
+    assert L.gc_schedule_forced_views(None, 3, 1, 1, out, ctypes.byref(n)) == -1
+    assert L.gc_schedule_forced_views(g, 3, 4, 1, out, ctypes.byref(n)) == -1
+    assert L.gc_schedule_forced_views(g, 65, 1, 1, out, ctypes.byref(n)) == -6
+    assert L.gc_schedule_forced_views(g, 3, 1, -1, out, ctypes.byref(n)) == -1
+    neg = (ctypes.c_int32 * 3)(0, -1, 2)
+    assert L.gc_schedule_forced_views(neg, 3, 1, 1, out, ctypes.byref(n)) == -1
+    v = (ctypes.c_int32 * 1)(3)
+    assert L.gc_schedule_advance_gaps(g, 3, v, 1, 0) == -1 and "view 3" in _err(L)
+    assert L.gc_schedule_advance_gaps(g, 3, None, 1, 0) == -1
+    assert L.gc_schedule_advance_gaps(g, 3, v, 4, 0) == -1
+    assert list(g) == [0, 1, 2]                 # a rejected call leaves the gaps alone

@@ -909,3 +909,201 @@ def test_rotation_sets():
     assert oracle.rotation_sets(12, 4) == [[0, 3, 6, 9], [1, 4, 7, 10], [2, 5, 8, 11]]
     assert oracle.rotation_sets(6, 2) == [[0, 3], [1, 4], [2, 5]]
     assert len(oracle.rotation_sets(10, 3)) == 10
+
+
+# ---------------------------------------------------------------------------
+# O7/O8/O9 loop level: the oracle's own trajectory and schedule functions
+# ---------------------------------------------------------------------------
+# Each pin takes the oracle module (or a planted-mutation copy of its
+# loop-level functions) so that test_planted_loop_mutations_fail_pins can
+# show every planted mistake failing one of them.
+
+def _lam(t):
+    ab = oracle.alpha_bar(t)
+    return 0.5 * math.log(ab / (1 - ab))
+
+
+def _pin_unipc_trajectory_exact_ode(orc):
+    """oracle.trajectory_unipc, every step full, on a model whose x0 is
+    c0 + c1 * lambda_t: the data-prediction ODE has the exact solution
+    x_t = (sigma_t / sigma_s) x_s + sigma_t [e^lam (c0 + c1 (lam - 1))]_s^t,
+    and halving the step must cut the error of the corrected sample by the
+    solver's order: third order for order 2 with the corrector (the corrector
+    raises the order by one), second order for order 1 with it, first order
+    (DDIM) without."""
+    c0, c1, x_start, t_check = 0.3, 0.7, 0.2, 99
+    sig = lambda t: math.sqrt(1 - oracle.alpha_bar(t))
+    F = lambda L: math.exp(L) * (c0 + c1 * (L - 1))
+
+    def err(S, order, corr):
+        ts = oracle.ddim_timesteps(S)
+        exact = sig(t_check) / sig(ts[0]) * x_start + sig(t_check) * (F(_lam(t_check)) - F(_lam(ts[0])))
+        k = ts.index(t_check)
+        pos = np.zeros((1, 2, 1, 4, 3), np.float32)
+        xt0 = np.full((1, 2, 1, 4, 4), x_start, np.float32)
+        stub = lambda kk, views: np.full((1, len(views), 1, 4, 4), c0 + c1 * _lam(ts[kk]), np.float32)
+        recs = orc.trajectory_unipc(xt0, stub, pos, None, 4, 0.01, "f32", S, [1] * S, 1, order, corr, steps=k + 1)
+        got = recs[k]["x_c_exact"] if corr else recs[k - 1]["x_t_exact"]
+        return float(np.abs(got - exact).max())
+
+    e2c = [err(S, 2, True) for S in (10, 20, 40)]
+    e1c = [err(S, 1, True) for S in (10, 20, 40)]
+    e1 = [err(S, 1, False) for S in (10, 20, 40)]
+    assert e2c[0] / e2c[1] > 6 and e2c[1] / e2c[2] > 6, e2c
+    assert e1c[0] / e1c[1] > 3 and e1c[1] / e1c[2] > 3, e1c
+    assert all(1.5 < e1[i] / e1[i + 1] < 2.6 for i in range(2)), e1
+    assert e2c[2] < 1e-5
+
+
+def _pin_unipc_history_by_hand(orc):
+    """A mixed full / cached trajectory whose x0 history is known by hand:
+    three views that see nothing of each other (all background), so at a
+    cached step the anchor takes its new prediction and every other view
+    keeps its stored x0 (Sec. 3.2, invalid matches).  Each view's prediction
+    at step k is the constant 1 + k/8 + u/64; the anchor of cached step c is
+    view c mod 3.  The expected corrected samples and predictions follow
+    from the UniPC recurrence on those scalars (coefficients from
+    oracle.unipc_coeffs, pinned above), with x_c and x_t stored as float32
+    between steps."""
+    S, N = 6, 3
+    full = [1, 0, 0, 1, 0, 0]
+    p = lambda k, u: 1.0 + k / 8 + u / 64
+    # x0 store after each step, by hand: m0 = p0; m1 = (p1[0], m0[1], m0[2]);
+    # m2 = (m1[0], p2[1], m1[2]); m3 = p3; m4 = (m3[0], m3[1], p4[2]);
+    # m5 = (p5[0], m4[1], m4[2])
+    m = [[p(0, 0), p(0, 1), p(0, 2)],
+         [p(1, 0), p(0, 1), p(0, 2)],
+         [p(1, 0), p(2, 1), p(0, 2)],
+         [p(3, 0), p(3, 1), p(3, 2)],
+         [p(3, 0), p(3, 1), p(4, 2)],
+         [p(5, 0), p(3, 1), p(4, 2)]]
+    anchors = [[0, 1, 2], [0], [1], [0, 1, 2], [2], [0]]
+    pos = np.full((1, N, 1, 4, 3), np.nan, np.float32)
+    cams = batch(ortho_cams(np.eye(3), [0, 0, 0], 1.0, [(2, 0.5)] * N))
+    x_start = np.array([0.25, -0.5, 0.75], np.float32)
+    xt0 = np.ascontiguousarray(np.broadcast_to(x_start[None, :, None, None, None], (1, N, 1, 4, 4)))
+
+    def stub(k, views):
+        return np.ascontiguousarray(np.broadcast_to(
+            np.array([p(k, u) for u in views], np.float32)[None, :, None, None, None], (1, len(views), 1, 4, 4)))
+
+    recs = orc.trajectory_unipc(xt0, stub, pos, cams, 4, 0.01, "f32", S, full, 1, 2, True)
+    assert [r["anchors"] for r in recs] == anchors
+    x = [float(v) for v in x_start]
+    xprev = [None] * N
+    for k, r in enumerate(recs):
+        co = oracle.unipc_coeffs(S, k, 2, True)
+        for u in range(N):
+            m2 = m[k - 2][u] if k >= 2 else 0.0
+            m1 = m[k - 1][u] if k >= 1 else 0.0
+            mk = m[k][u]
+            xc = co[3] * xprev[u] + co[4] * m2 + co[5] * m1 + co[6] * mk if co[0] else x[u]
+            xn = co[7] * xc + co[8] * m1 + co[9] * mk
+            assert np.all(r["x0"][0, u] == np.float32(mk)), (k, u)
+            np.testing.assert_allclose(r["x_c_exact"][0, u], xc, rtol=0, atol=1e-12, err_msg=f"x_c k={k} u={u}")
+            np.testing.assert_allclose(r["x_t_exact"][0, u], xn, rtol=0, atol=1e-12, err_msg=f"x_t k={k} u={u}")
+            xprev[u] = float(np.float32(xc))
+            x[u] = float(np.float32(xn))
+
+
+def _pin_forced_views_by_hand(orc):
+    """The coverage schedule's forced views and anchor gaps on the toy scene
+    (three views of 1 x 4 tokens; _toy_coverage), derived by hand.
+
+    a = 1, max_gap = 1, step 0 full: step 1 forces nothing (all gaps 0) and
+    the greedy takes view 0 (gains 6, 6, 4: the tie goes to the lower view);
+    from then on the views whose gap reached 1 are forced, the longest gap
+    first and equal gaps to the lower view: 1 (gaps 0 1 1), 2 (1 0 2),
+    0 (2 1 0), 1, 2.
+
+    a = 1, max_gap = 2, steps 0 and 3 full: step 1 greedy 0 (tie), step 2
+    greedy 1 (gains 6, 9, 8 with weights 1 + staleness), step 3 full resets
+    every gap, so steps 4 and 5 repeat steps 1 and 2, and step 6 forces
+    view 2 (gap 2).
+
+    a = 2, max_gap = 1: step 1 greedy {0, then 2} (after 0, view 1 adds 3 and
+    view 2 adds 4); step 2 forces view 1 and the greedy adds 0 (3 against 2);
+    step 3 forces view 2 and the greedy adds 0 (6 against 4)."""
+    pos, seen = _toy_coverage()
+    st0 = orc.coverage_init(pos)
+    cases = [
+        (1, 1, [1, 0, 0, 0, 0, 0, 0],
+         [[0, 1, 2], [0], [1], [2], [0], [1], [2]],
+         [[0, 0, 0], [0, 1, 1], [1, 0, 2], [2, 1, 0], [0, 2, 1], [1, 0, 2], [2, 1, 0]]),
+        (1, 2, [1, 0, 0, 1, 0, 0, 0],
+         [[0, 1, 2], [0], [1], [0, 1, 2], [0], [1], [2]],
+         [[0, 0, 0], [0, 1, 1], [1, 0, 2], [0, 0, 0], [0, 1, 1], [1, 0, 2], [2, 1, 0]]),
+        (2, 1, [1, 0, 0, 0],
+         [[0, 1, 2], [0, 2], [0, 1], [0, 2]],
+         [[0, 0, 0], [0, 1, 0], [0, 0, 1], [0, 1, 0]]),
+    ]
+    for a, max_gap, full, want_a, want_gap in cases:
+        recs = orc.schedule_adaptive(seen, st0, full, a, "coverage", max_gap=max_gap, R=2)
+        assert [r["anchors"] for r in recs] == want_a, (a, max_gap)
+        assert [r["gap"] for r in recs] == want_gap, (a, max_gap)
+        assert [r["full"] for r in recs] == [bool(f) for f in full]
+    assert orc.forced_views([0, 1, 1], 1, 1) == [1]
+    assert orc.forced_views([1, 0, 2], 3, 1) == [2, 0]
+    assert orc.forced_views([3, 3, 3], 2, 2) == [0, 1]
+    assert orc.forced_views([5, 5, 5], 3, 0) == []
+    assert orc.advance_gaps([1, 0, 2], [2], False) == [2, 1, 0]
+    assert orc.advance_gaps([1, 0, 2], [], True) == [0, 0, 0]
+
+
+def test_unipc_trajectory_exact_ode():
+    _pin_unipc_trajectory_exact_ode(oracle)
+
+
+def test_unipc_trajectory_history_by_hand():
+    _pin_unipc_history_by_hand(oracle)
+
+
+def test_forced_views_and_gaps_by_hand():
+    _pin_forced_views_by_hand(oracle)
+
+
+def _mutant(fn_name, old, new):
+    """A copy of the oracle's loop-level Python functions with one planted
+    mistake (a source replacement in fn_name); the copies call each other."""
+    import inspect
+    import types
+    ns = dict(vars(oracle))
+    for fn in ("forced_views", "advance_gaps", "schedule_adaptive", "trajectory_unipc"):
+        src = inspect.getsource(getattr(oracle, fn))
+        if fn == fn_name:
+            assert old in src, f"the planted mistake no longer matches {fn}"
+            src = src.replace(old, new)
+        exec(compile(src, f"<mutant {fn}>", "exec"), ns)
+    return types.SimpleNamespace(**ns)
+
+
+@pytest.mark.parametrize("fn,old,new", [
+    # the multistep history shifted wrongly: m_{k-1} and m_{k-2} swapped
+    ("trajectory_unipc", "x_prev, m2, m1 = xc_s, m1, mk", "x_prev, m2, m1 = xc_s, mk, m1"),
+    # a cached step transporting onto the x0 of step k-2 instead of k-1
+    ("trajectory_unipc", "transport(m1, stub(k, A)", "transport(m2 if m2 is not None else m1, stub(k, A)"),
+    # the corrected sample not carried to the next step
+    ("trajectory_unipc", "x_prev, m2, m1 = xc_s, m1, mk", "x_prev, m2, m1 = x_t, m1, mk"),
+    # a full step not resetting the anchor gaps
+    ("schedule_adaptive", "gap = advance_gaps(gap, A, is_full)",
+     "gap = advance_gaps(gap, A, is_full) if not is_full else gap"),
+    # equal gaps going to the higher view
+    ("forced_views", "due.sort(key=lambda v: (-gap[v], v))", "due.sort(key=lambda v: (-gap[v], -v))"),
+    # the forced list not capped at a
+    ("forced_views", "return due[:a]", "return due[:a + 1]"),
+])
+def test_planted_loop_mutations_fail_pins(fn, old, new):
+    """Every planted mistake in the loop-level functions fails at least one
+    of the pins above (and the unmutated copy passes them all)."""
+    pins = (_pin_unipc_trajectory_exact_ode, _pin_unipc_history_by_hand, _pin_forced_views_by_hand)
+    clean = _mutant(fn, old, old)
+    for pin in pins:
+        pin(clean)
+    bad = _mutant(fn, old, new)
+    failed = []
+    for pin in pins:
+        try:
+            pin(bad)
+        except (AssertionError, ValueError, IndexError):
+            failed.append(pin.__name__)
+    assert failed, f"no pin caught the planted mistake in {fn}"
