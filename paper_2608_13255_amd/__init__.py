@@ -153,6 +153,34 @@ def _stream(stream) -> Optional[int]:
     return int(stream)
 
 
+def _side_stream(stream) -> Optional[torch.cuda.Stream]:
+    """The stream of an explicit `stream` argument when it is not torch's
+    current stream (None otherwise)."""
+    if stream is None:
+        return None
+    cur = torch.cuda.current_stream()
+    s = stream if isinstance(stream, torch.cuda.Stream) else torch.cuda.ExternalStream(int(stream))
+    return None if s.cuda_stream == cur.cuda_stream else s
+
+
+def _keep(stream, tensors) -> None:
+    """Tensors this binding allocated and handed to work on a side stream:
+    tell torch's caching allocator, so that their memory is not given to
+    current-stream work before the side stream's kernels are done with it."""
+    s = _side_stream(stream)
+    if s is not None:
+        for t in tensors:
+            t.record_stream(s)
+
+
+def _after_side(stream) -> None:
+    """Order torch's current stream (and so a following host read-back)
+    after the work just enqueued on a side stream."""
+    s = _side_stream(stream)
+    if s is not None:
+        torch.cuda.current_stream().wait_stream(s)
+
+
 def _dev(t: torch.Tensor, name: str) -> int:
     if not isinstance(t, torch.Tensor):
         raise TypeError(f"{name} must be a torch.Tensor")
@@ -205,10 +233,13 @@ def gc_posmap_downsample(pos_hi: torch.Tensor, f: int, pos_lat: torch.Tensor = N
     Hr, Wr = pos_hi.shape[-3], pos_hi.shape[-2]
     lead = tuple(pos_hi.shape[:-3])
     n = int(np.prod(lead)) if lead else 1
+    fresh = []
     if pos_lat is None:
         pos_lat = torch.empty(lead + (Hr // f, Wr // f, 3), dtype=torch.float32, device=pos_hi.device)
+        fresh.append(pos_lat)
     _check(lib().gc_posmap_downsample(_dev(pos_hi, "pos_hi"), n, Hr, Wr, f, _dev(pos_lat, "pos_lat"),
                                       _stream(stream)), "gc_posmap_downsample")
+    _keep(stream, fresh)
     return pos_lat
 
 
@@ -217,10 +248,13 @@ def gc_posmap_bbox(pos: torch.Tensor, tol_frac: float = 0.01, bbox: torch.Tensor
     if pos.dtype != torch.float32 or pos.dim() != 5 or pos.shape[-1] != 3:
         raise ValueError("pos must be float32 [B, N, H, W, 3]")
     B, N, H, W, _ = pos.shape
+    fresh = []
     if bbox is None:
         bbox = torch.empty((B, 8), dtype=torch.float32, device=pos.device)
+        fresh.append(bbox)
     _check(lib().gc_posmap_bbox(_dev(pos, "pos"), B, N, H, W, float(tol_frac), _dev(bbox, "bbox"),
                                 _stream(stream)), "gc_posmap_bbox")
+    _keep(stream, fresh)
     return bbox
 
 
@@ -238,10 +272,13 @@ def gc_build_correspondence(pos: torch.Tensor, cams: torch.Tensor, anchors: Sequ
     arr, a = _anchors(anchors)
     NT = N - a
     dev = pos.device
+    fresh = []
     if corr is None:
         corr = torch.empty((B, NT, H, W, a), dtype=torch.int32, device=dev)
+        fresh.append(corr)
     if weights is None:
         weights = torch.empty((B, NT, H, W, a, K), dtype=torch.float32, device=dev)
+        fresh.append(weights)
     if tuple(corr.shape) != (B, NT, H, W, a) or corr.dtype != torch.int32:
         raise ValueError("corr must be int32 [B, N-a, H, W, a]")
     if tuple(weights.shape) != (B, NT, H, W, a, K) or weights.dtype != torch.float32:
@@ -252,6 +289,7 @@ def gc_build_correspondence(pos: torch.Tensor, cams: torch.Tensor, anchors: Sequ
                                          _dev(bbox, "bbox"), _dev(corr, "corr") if corr.numel() else None,
                                          _dev(weights, "weights") if weights.numel() else None,
                                          _opt(stats, "stats"), _stream(stream)), "gc_build_correspondence")
+    _keep(stream, fresh)
     return corr, weights
 
 
@@ -284,6 +322,8 @@ def gc_index_correspondence(corr: torch.Tensor, workspace: torch.Tensor = None, 
                                          _dev(lst, "vis_list"), _dev(nv, "n_vis"), _dev(workspace, "workspace"),
                                          workspace.numel() * workspace.element_size(), _stream(stream)),
            "gc_index_correspondence")
+    _keep(stream, (bits, lst))
+    _after_side(stream)          # the count is read on the current stream
     return VisibleIndex(bits, lst, int(nv.item()))
 
 
@@ -317,6 +357,8 @@ def gc_index_foreground(pos: torch.Tensor, workspace: torch.Tensor = None, strea
                                      _dev(recs, "fg_recs"), _dev(nf, "n_fg"), _dev(workspace, "workspace"),
                                      workspace.numel() * workspace.element_size(), _stream(stream)),
            "gc_index_foreground")
+    _keep(stream, (bits, recs))
+    _after_side(stream)          # the count is read on the current stream
     return ForegroundIndex(bits, recs, int(nf.item()))
 
 
@@ -355,6 +397,7 @@ def gc_transport_step(x0_prev: torch.Tensor, x0_anchor_new: torch.Tensor, corr: 
                                    _dev(weights, "weights") if weights.numel() else None, *_index_args(index),
                                    B, N, H, W, C, arr, a, K, dtype_code(x0_prev), _dev(x0_out, "x0_out"),
                                    _stream(stream)), "gc_transport_step")
+    _keep(stream, (x0_out,))
     return x0_out
 
 
@@ -372,6 +415,7 @@ def gc_sampler_reconstruct(x_t: torch.Tensor, x0: torch.Tensor, sampler: Sampler
                                         _opt(model_out, "model_out"), x_t.numel(), dtype_code(x_t),
                                         ctypes.byref(smp), float(t), float(t_next), _stream(stream)),
            "gc_sampler_reconstruct")
+    _keep(stream, [t for t in (x_next, model_out) if t is not None])
     return x_next, model_out
 
 
@@ -403,6 +447,7 @@ def gc_transport_reconstruct(x0_prev: torch.Tensor, x0_anchor_new: torch.Tensor,
                                           ctypes.byref(smp), float(t), float(t_next), _dev(x0_out, "x0_out"),
                                           _dev(x_next, "x_next"), _opt(model_out, "model_out"), _stream(stream)),
            "gc_transport_reconstruct")
+    _keep(stream, [t for t in (x0_out, x_next, model_out) if t is not None])
     return x0_out, x_next, model_out
 
 
@@ -436,6 +481,7 @@ def gc_transport_step_geom(x0_prev: torch.Tensor, x0_anchor_new: torch.Tensor, p
                                         W, C, arr, a, K, dtype_code(x0_prev), _dev(x0_out, "x0_out"),
                                         _stream(stream)),
            "gc_transport_step_geom")
+    _keep(stream, (x0_out,))
     return x0_out
 
 
@@ -464,6 +510,7 @@ def gc_transport_reconstruct_geom(x0_prev: torch.Tensor, x0_anchor_new: torch.Te
                                                ctypes.byref(smp), float(t), float(t_next), _dev(x0_out, "x0_out"),
                                                _dev(x_next, "x_next"), _opt(model_out, "model_out"),
                                                _stream(stream)), "gc_transport_reconstruct_geom")
+    _keep(stream, [t for t in (x0_out, x_next, model_out) if t is not None])
     return x0_out, x_next, model_out
 
 
@@ -531,6 +578,7 @@ def gc_unipc_update(st: UniPCStep, m_k: torch.Tensor, x_cur: torch.Tensor = None
                                  _opt(m_km1, "m_km1"), _dev(m_k, "m_k"), m_k.numel(), dtype_code(m_k),
                                  ctypes.byref(st), _dev(x_c, "x_c"), _dev(x_next, "x_next"), _stream(stream)),
            "gc_unipc_update")
+    _keep(stream, (x_c, x_next))
     return x_c, x_next
 
 
@@ -558,6 +606,7 @@ def gc_transport_unipc(x0_prev: torch.Tensor, x0_anchor_new: torch.Tensor, corr:
                                     B, N, H, W, C, arr, a, K, dtype_code(x0_prev), ctypes.byref(st),
                                     _dev(x0_out, "x0_out"), _dev(x_c, "x_c"), _dev(x_next, "x_next"),
                                     _stream(stream)), "gc_transport_unipc")
+    _keep(stream, (x0_out, x_c, x_next))
     return x0_out, x_c, x_next
 
 
@@ -583,6 +632,7 @@ def gc_transport_unipc_geom(x0_prev: torch.Tensor, x0_anchor_new: torch.Tensor, 
                                          B, N, H, W, C, arr, a, K, dtype_code(x0_prev), ctypes.byref(st),
                                          _dev(x0_out, "x0_out"), _dev(x_c, "x_c"), _dev(x_next, "x_next"),
                                          _stream(stream)), "gc_transport_unipc_geom")
+    _keep(stream, (x0_out, x_c, x_next))
     return x0_out, x_c, x_next
 
 
@@ -646,6 +696,7 @@ def gc_coverage_pairs(pos: torch.Tensor, cams: torch.Tensor, bbox: torch.Tensor,
         raise ValueError(f"out must be a 32-bit [{N}, {B}, {N}, {wpr}] tensor")
     _check(lib().gc_coverage_pairs(_dev(pos, "pos"), _dev(cams, "cams"), _dev(bbox, "bbox"), B, N, H, W,
                                    _dev(out, "pair_bits"), _stream(stream)), "gc_coverage_pairs")
+    _keep(stream, (out,))
     return out
 
 
@@ -656,6 +707,7 @@ def gc_coverage_init(pos: torch.Tensor, out: torch.Tensor = None, stream=None) -
         out = torch.empty((B, N, H, W), dtype=torch.uint8, device=pos.device)
     _check(lib().gc_coverage_init(_dev(pos, "pos"), B, N, H, W, _dev(out, "stale"), _stream(stream)),
            "gc_coverage_init")
+    _keep(stream, (out,))
     return out
 
 
@@ -675,6 +727,7 @@ def gc_coverage_update(pair_bits: torch.Tensor, stale: torch.Tensor, anchors: Se
     _check(lib().gc_coverage_update(_dev(pair_bits, "pair_bits"), B, N, H, W, arr, len(anchors), R,
                                     _dev(stale, "stale"), _dev(stats, "stats"), _stream(stream)),
            "gc_coverage_update")
+    _keep(stream, (stats,))
     return stats
 
 
@@ -696,6 +749,7 @@ def gc_coverage_select(pair_bits: torch.Tensor, stale: torch.Tensor, a: int, for
                                     len(forced), _dev(out, "anchors_out"), _dev(workspace, "workspace"),
                                     workspace.numel() * workspace.element_size(), _stream(stream)),
            "gc_coverage_select")
+    _keep(stream, (out, workspace))
     return out
 
 
@@ -715,6 +769,7 @@ def gc_coverage_score(pair_bits: torch.Tensor, stale: torch.Tensor, sets: Sequen
                                    _dev(out, "scores"), _dev(workspace, "workspace"),
                                    workspace.numel() * workspace.element_size(), _stream(stream)),
            "gc_coverage_score")
+    _keep(stream, (out, workspace))
     return out
 
 

@@ -13,6 +13,7 @@ the listed views as a device tensor [B, len(views), H, W, C].
 """
 from __future__ import annotations
 
+import contextlib
 from typing import Callable, Dict, List, Optional, Sequence, Tuple
 
 import torch
@@ -58,9 +59,9 @@ class GeoCacheRunner:
             raise ValueError("full must have one entry per sampler step")
         self.B, self.N = pos.shape[0], pos.shape[1]
         self.use_index = use_index
+        if stream is not None and not isinstance(stream, torch.cuda.Stream):
+            stream = torch.cuda.ExternalStream(int(stream))
         self.stream = stream
-        self.bbox = gc_posmap_bbox(pos, tol_frac, stream=stream)
-        self.fg_index = gc_index_foreground(pos, stream=stream) if geom and use_index else None
         self._ops: Dict[Tuple[int, ...], Tuple[torch.Tensor, torch.Tensor, Optional[VisibleIndex]]] = {}
         self.unipc_order, self.unipc_corrector = unipc_order, unipc_corrector
         self.anchor_policy, self.max_gap = anchor_policy, max_gap
@@ -71,9 +72,12 @@ class GeoCacheRunner:
             A = gc_schedule_anchors(self.N, a, c)
             if A not in self.rotation_sets:
                 self.rotation_sets.append(A)
-        self.pairs = gc_coverage_pairs(pos, cams, self.bbox, stream=stream) if self.tracking else None
-        self._ws = (torch.empty(gc_coverage_workspace_bytes(), dtype=torch.uint8, device=pos.device)
-                    if self.tracking else None)
+        with self._on_stream():
+            self.bbox = gc_posmap_bbox(pos, tol_frac, stream=stream)
+            self.fg_index = gc_index_foreground(pos, stream=stream) if geom and use_index else None
+            self.pairs = gc_coverage_pairs(pos, cams, self.bbox, stream=stream) if self.tracking else None
+            self._ws = (torch.empty(gc_coverage_workspace_bytes(), dtype=torch.uint8, device=pos.device)
+                        if self.tracking else None)
         self.stale: Optional[torch.Tensor] = None
         self.stats_host = None                        # per-view staleness statistics after the last step
         self.gap: List[int] = [0] * self.N            # cached steps since each view was last an anchor
@@ -84,6 +88,12 @@ class GeoCacheRunner:
         self.x0: Optional[torch.Tensor] = None
         self.x0_km2: Optional[torch.Tensor] = None   # UniPC: x0 of step k-2
         self.x_c: Optional[torch.Tensor] = None      # UniPC: corrected sample of step k-1
+
+    def _on_stream(self):
+        """Every device call, allocation and read-back of the runner happens
+        with its stream current, so they are ordered on it (with stream=None,
+        on torch's current stream)."""
+        return torch.cuda.stream(self.stream) if self.stream is not None else contextlib.nullcontext()
 
     @staticmethod
     def full_steps(rule: str, S: int, E: int = 0) -> List[int]:
@@ -104,6 +114,12 @@ class GeoCacheRunner:
         return self._ops[key]
 
     def start(self, x_t: torch.Tensor) -> None:
+        """x_t: the initial state; work that produced it on another stream
+        must be complete or ordered before this runner's stream."""
+        with self._on_stream():
+            self._start(x_t)
+
+    def _start(self, x_t: torch.Tensor) -> None:
         self.x_t, self.x0, self.k, self.c = x_t, None, 0, 0
         self.x0_km2, self.x_c = None, None
         if self.tracking:
@@ -141,9 +157,14 @@ class GeoCacheRunner:
             self.stats_host = stats.cpu()
 
     def step(self, predict: Predict) -> List[int]:
-        """Run sampler step k; returns the views the denoiser was asked for."""
+        """Run sampler step k; returns the views the denoiser was asked for.
+        predict runs with the runner's stream current."""
         if self.x_t is None:
             raise RuntimeError("call start() first")
+        with self._on_stream():
+            return self._step(predict)
+
+    def _step(self, predict: Predict) -> List[int]:
         k = self.k
         if self.unipc_order:
             return self._step_unipc(predict)
@@ -201,12 +222,17 @@ class GeoCacheRunner:
             self.step(predict)
 
     def state_dict(self) -> dict:
-        """Loop state for checkpoint / resume (tensors are cloned)."""
+        """Loop state for checkpoint / resume (tensors are cloned on the runner's stream)."""
         cl = lambda t: None if t is None else t.clone()
-        return {"k": self.k, "c": self.c, "x_t": cl(self.x_t), "x0": cl(self.x0), "x0_km2": cl(self.x0_km2),
-                "x_c": cl(self.x_c), "stale": cl(self.stale), "stats": cl(self.stats_host), "gap": list(self.gap)}
+        with self._on_stream():
+            return {"k": self.k, "c": self.c, "x_t": cl(self.x_t), "x0": cl(self.x0), "x0_km2": cl(self.x0_km2),
+                    "x_c": cl(self.x_c), "stale": cl(self.stale), "stats": cl(self.stats_host), "gap": list(self.gap)}
 
     def load_state_dict(self, st: dict) -> None:
+        with self._on_stream():
+            self._load_state_dict(st)
+
+    def _load_state_dict(self, st: dict) -> None:
         cl = lambda t: None if t is None else t.clone()
         self.k, self.c = int(st["k"]), int(st["c"])
         self.x_t, self.x0 = cl(st["x_t"]), cl(st["x0"])

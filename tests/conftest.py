@@ -50,3 +50,50 @@ def visible_weights(corr, wts):
     corr = corr.cpu().numpy() if hasattr(corr, "cpu") else corr
     wts = wts.cpu().numpy() if hasattr(wts, "cpu") else wts
     return np.where((corr != 0)[..., None], wts, np.float32(0))
+
+
+def stored_x0_slack(got, want, dtype):
+    """Elementwise |got - want| (float64) of two stored x0 arrays (float32
+    values, or bfloat16 bit patterns as uint16).  A model output is computed
+    by each side from its own stored x0, so the two outputs may differ by the
+    closed form's x0 coefficient times this difference on top of the bar.
+    The stored values are usually equal or one ulp apart, but not always in
+    ulps: where Eq. 1's sum cancels to nearly zero the float sum's absolute
+    error (far below the x0 bar) can exceed the result itself."""
+    import numpy as np
+    if dtype == "f32":
+        return np.abs(np.asarray(got, np.float32).astype(np.float64) - np.asarray(want, np.float32).astype(np.float64))
+    va = (np.asarray(got, np.uint16).astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    vb = (np.asarray(want, np.uint16).astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    return np.abs(va - vb)
+
+
+def x0_coef(sampler: str, pred: str, t: float) -> float:
+    """|d model_out / d x0| of the reconstruction's closed forms at step time
+    t: eps = (x_t - sqrt(abar) x0) / sqrt(1 - abar) -> sqrt(abar) / sqrt(1 - abar);
+    v = sqrt(abar) eps - sqrt(1 - abar) x0 -> 1 / sqrt(1 - abar);
+    velocity = (x_t - x0) / sigma -> 1 / sigma."""
+    import math
+    import oracle
+    if sampler == "ddim":
+        ab = oracle.alpha_bar(int(t))
+        return math.sqrt(ab) / math.sqrt(1 - ab) if pred == "eps" else 1 / math.sqrt(1 - ab)
+    return 1.0 / t
+
+
+def storage_ulps(got, want, dtype):
+    """Elementwise distance in storage ulps between two stored latent arrays
+    (float32 values, or bfloat16 bit patterns as uint16); +0 and -0 are 0
+    apart."""
+    import numpy as np
+    if dtype == "f32":
+        i = np.asarray(got, np.float32).view(np.int32).astype(np.int64)
+        j = np.asarray(want, np.float32).view(np.int32).astype(np.int64)
+        i = np.where(i < 0, -(i & 0x7FFFFFFF), i)
+        j = np.where(j < 0, -(j & 0x7FFFFFFF), j)
+    else:
+        h = np.asarray(got, np.uint16).astype(np.int64)
+        k = np.asarray(want, np.uint16).astype(np.int64)
+        i = np.where(h & 0x8000, -(h & 0x7FFF), h)
+        j = np.where(k & 0x8000, -(k & 0x7FFF), k)
+    return np.abs(i - j)

@@ -218,3 +218,41 @@ def test_adaptive_free_running_geom_and_resume(gc):
     hist2 = [r2.step(predict) for _ in range(w.S - 13)]
     assert hist2 == outs[0][0][13:]
     assert torch.equal(r2.x_t.view(torch.int16), outs[0][1].view(torch.int16))
+
+
+@pytest.mark.parametrize("geom,unipc", [(False, 0), (True, 0), (False, 2)], ids=["stored", "geom", "unipc"])
+def test_runner_on_a_side_stream_matches_default_stream(gc, geom, unipc):
+    """A runner given its own (non-blocking) torch stream produces the
+    default-stream trajectory bit for bit: its read-backs (the visible and
+    foreground counts, the selected anchors, the staleness statistics) and
+    the tensors the binding allocates are ordered on that stream.  The
+    coverage policy with refresh exercises every read-back."""
+    from paper_2608_13255_amd.runner import GeoCacheRunner
+    w, P = workload("syncmvd")
+    preds = {}
+
+    def predict(k, views):
+        key = (k, tuple(views))
+        if key not in preds:
+            preds[key] = to_dev(synth.storage(synth.x0_state(w, P, k, views=views), w.dtype), w.dtype)
+        return preds[key]
+
+    xt0 = to_dev(synth.storage(synth.eps_noise(w, 0), w.dtype), w.dtype)
+    full = GeoCacheRunner.full_steps(w.full_rule, w.S, w.full_E)
+    smp = gc.Sampler(kind=gc.GC_DDIM)
+    torch.cuda.synchronize()
+    outs = []
+    for side in (None, torch.cuda.Stream()):
+        Pd, cams, _ = device_inputs(gc, w, P)
+        torch.cuda.synchronize()
+        r = GeoCacheRunner(Pd, cams, w.a, w.K, smp, w.S, full, w.tol_frac, anchor_policy="coverage", max_gap=3,
+                           refresh_tau=0.01, refresh_R=2, geom=geom, unipc_order=unipc, stream=side)
+        r.start(xt0.clone() if side is None else xt0)
+        hist = [r.step(predict) for _ in range(w.S)]
+        with torch.cuda.stream(side) if side is not None else torch.cuda.stream(torch.cuda.current_stream()):
+            res = (hist, r.x_t.clone(), r.x0.clone(), r.stale.clone())
+        torch.cuda.synchronize()
+        outs.append(res)
+    assert outs[0][0] == outs[1][0]
+    for a_, b_ in zip(outs[0][1:], outs[1][1:]):
+        assert torch.equal(a_.view(torch.uint8), b_.view(torch.uint8))

@@ -5,9 +5,12 @@ driving the kernels) against the oracle's trajectory.
     state after the previous step, and its step must match the oracle's next
     state to the per-step bar (float32 1e-5, bfloat16 2e-2 against the
     oracle's unrounded values);
-  * free-running: the GPU runs the whole trajectory on its own; rounding
-    differences may accumulate, so the final state is held to a drift bound
-    (float32 1e-4, bfloat16 0.1) and the drift is reported;
+  * free-running: the GPU runs the whole trajectory on its own and its
+    final state is compared with the oracle's free-running trajectory
+    element by element in storage ulps.  Rounding differences could
+    accumulate; measured, they do not: the float32 workloads end at most one
+    ulp apart (1.19e-7) and the bfloat16 one bit-identical, so the bound is
+    2 float32 ulps and 1 bfloat16 ulp, and the drift is printed;
   * checkpoint/resume: a runner restored from a mid-trajectory state
     finishes bit-identical to the uninterrupted run.
 """
@@ -19,12 +22,12 @@ import oracle
 import synth
 from synth.configs import C2, C3, C4
 
-from conftest import latent_maps
+from conftest import latent_maps, storage_ulps
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda:0"
 TOL = {"f32": 1e-5, "bf16": 2e-2}
-DRIFT = {"f32": 1e-4, "bf16": 0.1}
+DRIFT_ULPS = {"f32": 2, "bf16": 1}
 
 
 def to_dev(arr, dtype):
@@ -87,8 +90,9 @@ def test_trajectory_teacher_forced_and_free_running(w):
     runner.run(predict)
     xt = synth.values(to_host(runner.x_t, w.dtype), w.dtype).astype(np.float64)
     drift = float(np.abs(xt - synth.values(ref[-1]["x_t"], w.dtype)).max())
-    print(f"{w.name}: free-running drift after {w.S} steps: {drift:.3g}")
-    assert drift <= DRIFT[w.dtype]
+    ulps = int(storage_ulps(to_host(runner.x_t, w.dtype), ref[-1]["x_t"], w.dtype).max())
+    print(f"{w.name}: free-running drift after {w.S} steps: {drift:.3g} ({ulps} ulps)")
+    assert ulps <= DRIFT_ULPS[w.dtype]
 
 
 def test_checkpoint_resume_is_bit_identical():

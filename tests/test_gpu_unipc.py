@@ -17,7 +17,7 @@ import oracle
 import synth
 from synth.configs import C2, C4, C5
 
-from conftest import latent_maps
+from conftest import latent_maps, storage_ulps, stored_x0_slack
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda:0"
@@ -89,10 +89,12 @@ def test_transport_unipc_parity(gc, w):
         mk, xc, xn = gc.gc_transport_unipc(args[0], args[1], corr, wts, A, st, x_cur=args[2], x_prev=args[3],
                                            m_km2=args[4], index=index)
         assert np.abs(vals(mk, w.dtype) - mk_exact).max() <= TOL[w.dtype]
-        same = np.ones(shape, bool) if w.dtype == "f32" else to_host(mk, w.dtype) == mk_state
-        assert same.mean() > 0.999
-        assert np.abs(vals(xc, w.dtype) - xc_o)[same].max() <= TOL[w.dtype]
-        assert np.abs(vals(xn, w.dtype) - xn_o)[same].max() <= TOL[w.dtype]
+        # x_c and x_next depend on the stored m_k, which the two sides may round to neighbouring
+        # values: the bar plus the update's m_k coefficient times that difference, every element
+        slack = stored_x0_slack(to_host(mk, w.dtype), mk_state, w.dtype)
+        c_mk = co[6] if co[0] else 0.0
+        assert (np.abs(vals(xc, w.dtype) - xc_o) <= TOL[w.dtype] + abs(c_mk) * slack).all()
+        assert (np.abs(vals(xn, w.dtype) - xn_o) <= TOL[w.dtype] + abs(co[7] * c_mk + co[9]) * slack).all()
         outs.append((mk, xc, xn))
     for a_, b_ in zip(*outs):                          # split launch == plain launch
         assert torch.equal(a_.view(iv), b_.view(iv))
@@ -149,8 +151,9 @@ def test_unipc_trajectory_headline_operating_point(gc, rule, E, expect):
     runner.start(to_dev(xt0, w.dtype))
     runner.run(predict)
     drift = float(np.abs(vals(runner.x_t, w.dtype) - synth.values(ref[-1]["x_t"], w.dtype)).max())
-    print(f"UniPC-2 headline point: free-running drift after {S} steps: {drift:.3g}")
-    assert drift <= 1e-4
+    ulps = int(storage_ulps(to_host(runner.x_t, w.dtype), ref[-1]["x_t"], w.dtype).max())
+    print(f"UniPC-2 headline point: free-running drift after {S} steps: {drift:.3g} ({ulps} ulps)")
+    assert ulps <= 2          # measured: bit-identical to the oracle's free-running trajectory
 
 
 @pytest.mark.parametrize("w", [C2, C4, C5], ids=lambda w: w.name)
