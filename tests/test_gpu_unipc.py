@@ -151,9 +151,12 @@ def test_unipc_trajectory_headline_operating_point(gc, rule, E, expect):
     runner.start(to_dev(xt0, w.dtype))
     runner.run(predict)
     drift = float(np.abs(vals(runner.x_t, w.dtype) - synth.values(ref[-1]["x_t"], w.dtype)).max())
-    ulps = int(storage_ulps(to_host(runner.x_t, w.dtype), ref[-1]["x_t"], w.dtype).max())
-    print(f"UniPC-2 headline point: free-running drift after {S} steps: {drift:.3g} ({ulps} ulps)")
-    assert ulps <= 2          # measured: bit-identical to the oracle's free-running trajectory
+    print(f"UniPC-2 headline point: free-running drift after {S} steps: {drift:.3g}")
+    # measured: bit-identical to the oracle's free-running trajectory
+    if w.dtype == "f32":
+        assert drift <= 1e-6
+    else:
+        assert storage_ulps(to_host(runner.x_t, w.dtype), ref[-1]["x_t"], w.dtype).max() <= 1
 
 
 @pytest.mark.parametrize("w", [C2, C4, C5], ids=lambda w: w.name)
