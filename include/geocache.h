@@ -12,6 +12,7 @@
  *                        gc_posmap_bbox         per-asset bbox and squared tolerance
  *                        gc_build_correspondence   G_{A->v} for one anchor set
  *                        gc_index_correspondence   visible-token index of G_{A->v}
+ *                        gc_index_correspondence_noalloc   the same without a workspace argument
  *                        gc_index_foreground       foreground-token index of the position maps
  *   every cached step    gc_transport_step      Eq. 1: x0(v) = x0_prev(v) + G[dx0(A)]
  *                        gc_sampler_reconstruct sampler-consistent eps / v / velocity + x_t update
@@ -71,6 +72,7 @@ extern "C" {
 #define GC_MAX_ANCHORS 8    /* anchors per cached step */
 #define GC_MAX_GRID 4094    /* latent H and W (12-bit packed tap coordinates) */
 #define GC_MAX_CHANNELS 256 /* latent channels */
+#define GC_NOALLOC_SCRATCH_BYTES (1 << 20) /* library-held scratch of gc_index_correspondence_noalloc, per GPU */
 
 /* status codes */
 #define GC_OK 0
@@ -232,6 +234,26 @@ int gc_build_correspondence(const float* pos, const gc_camera* cams, int B, int 
 size_t gc_index_workspace_bytes(int64_t n_tokens);
 int gc_index_correspondence(const int32_t* corr, int64_t n_tokens, int a, uint32_t* vis_bits, int32_t* vis_list,
                             int32_t* n_vis, void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * gc_index_correspondence without a workspace argument, for callers that
+ * cannot allocate device memory: code under HIP graph capture, tight serving
+ * loops, harnesses that forbid hipMalloc.  The per-chunk counts and offsets
+ * go to a scratch array of GC_NOALLOC_SCRATCH_BYTES that the library holds on
+ * every GPU it runs on until the process ends (its address is looked up once
+ * per device, on the first call with that device current); the call itself
+ * allocates nothing.  Arguments, outputs and result are those of
+ * gc_index_correspondence; the current device must be the one that owns the
+ * buffers and the stream.  n_tokens is at most 134217728 (the scratch holds
+ * 2 * ceil(n_tokens / 1024) int32); larger counts fail with GC_ERR_CAPACITY
+ * before anything is launched.  Every call on one GPU shares that GPU's
+ * scratch: calls that overlap in time on one GPU (concurrent streams or host
+ * threads) race and must be serialised by the caller.  The scratch keeps the
+ * last call's contents; every call writes all of the part it reads, so
+ * nothing has to be cleared between calls.
+ */
+int gc_index_correspondence_noalloc(const int32_t* corr, int64_t n_tokens, int a, uint32_t* vis_bits,
+                                    int32_t* vis_list, int32_t* n_vis, hipStream_t stream);
 
 /*
  * Foreground index of latent-grid position maps (once per asset batch; it

@@ -30,6 +30,7 @@ GC_DDIM, GC_FLOW_EULER = 0, 1
 GC_PRED_NONE, GC_PRED_EPS, GC_PRED_V, GC_PRED_VEL = 0, 1, 2, 3
 GC_FULL_PERIODIC, GC_FULL_HEAD_MID_TAIL, GC_FULL_HEAD_TAIL_E = 0, 1, 2
 GC_MAX_VIEWS, GC_MAX_ANCHORS, GC_MAX_GRID = 64, 8, 4094
+GC_NOALLOC_SCRATCH_BYTES = 1 << 20
 ERRORS = {-1: "GC_ERR_ARG", -2: "GC_ERR_SHAPE", -3: "GC_ERR_DTYPE", -4: "GC_ERR_ALIGN",
           -5: "GC_ERR_ALIAS", -6: "GC_ERR_CAPACITY", -7: "GC_ERR_HIP"}
 
@@ -95,6 +96,7 @@ def lib() -> ctypes.CDLL:
             "gc_build_correspondence": ([_vp, _vp, _i, _i, _i, _i, _i32p, _i, _i, _vp, _vp, _vp, _vp, _vp], _i),
             "gc_index_workspace_bytes": ([_i64], ctypes.c_size_t),
             "gc_index_correspondence": ([_vp, _i64, _i, _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp], _i),
+            "gc_index_correspondence_noalloc": ([_vp, _i64, _i, _vp, _vp, _vp, _vp], _i),
             "gc_index_foreground": ([_vp, _i64, _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp], _i),
             "gc_transport_step": ([_vp, _vp, _vp, _vp, _vp, _vp, _i64, _i, _i, _i, _i, _i, _i32p, _i, _i, _i, _vp,
                                    _vp], _i),
@@ -324,6 +326,26 @@ def gc_index_correspondence(corr: torch.Tensor, workspace: torch.Tensor = None, 
            "gc_index_correspondence")
     _keep(stream, (bits, lst))
     _after_side(stream)          # the count is read on the current stream
+    return VisibleIndex(bits, lst, int(nv.item()))
+
+
+def gc_index_correspondence_noalloc(corr: torch.Tensor, stream=None) -> VisibleIndex:
+    """gc_index_correspondence with the library's own scratch instead of a
+    workspace (the C call allocates nothing; this wrapper allocates the
+    outputs).  Reads the visible count back to the host."""
+    if corr.dtype != torch.int32 or corr.dim() != 5:
+        raise ValueError("corr must be int32 [B, N-a, H, W, a]")
+    a = corr.shape[-1]
+    n_tok = int(corr.numel() // a) if a else 0
+    dev = corr.device
+    bits = torch.empty(max(1, (n_tok + 31) // 32), dtype=torch.int32, device=dev)
+    lst = torch.empty(max(1, n_tok), dtype=torch.int32, device=dev)
+    nv = torch.empty(1, dtype=torch.int32, device=dev)
+    _check(lib().gc_index_correspondence_noalloc(_dev(corr, "corr") if n_tok else None, n_tok, a,
+                                                 _dev(bits, "vis_bits"), _dev(lst, "vis_list"), _dev(nv, "n_vis"),
+                                                 _stream(stream)), "gc_index_correspondence_noalloc")
+    _keep(stream, (bits, lst))
+    _after_side(stream)
     return VisibleIndex(bits, lst, int(nv.item()))
 
 

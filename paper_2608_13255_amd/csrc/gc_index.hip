@@ -19,7 +19,14 @@
 //   scan     exclusive prefix over the chunk counts, total -> list length
 //   scatter  each chunk writes its tokens at its offset, ranked inside the
 //            chunk by (round, wave, mbcnt of the ballot)
+#include <mutex>
+
 #include "gc_common.h"
+
+// Scratch of gc_index_correspondence_noalloc (per-chunk counts and offsets),
+// one copy per GPU for the life of the process.  Host code never uses this
+// name as an address: it takes the device address from hipGetSymbolAddress.
+static __device__ __align__(256) unsigned char scratch[GC_NOALLOC_SCRATCH_BYTES];
 
 namespace gc {
 namespace {
@@ -145,29 +152,35 @@ extern "C" size_t gc_index_workspace_bytes(int64_t n_tokens) {
   return (size_t)(((2 * nb * 4) + 255) / 256 * 256);
 }
 
-extern "C" int gc_index_correspondence(const int32_t* corr, int64_t n_tokens, int a, uint32_t* vis_bits,
-                                       int32_t* vis_list, int32_t* n_vis, void* workspace, size_t workspace_bytes,
-                                       hipStream_t stream) {
-  clear_error();
-  if (!n_vis || !workspace) return fail(GC_ERR_ARG, "index: null n_vis or workspace");
-  if (n_tokens < 0) return fail(GC_ERR_SHAPE, "index: n_tokens=%lld is negative", (long long)n_tokens);
-  if (n_tokens > 0x7fffffffLL) return fail(GC_ERR_CAPACITY, "index: n_tokens=%lld exceeds 2^31-1", (long long)n_tokens);
-  if (a < 1 || a > GC_MAX_ANCHORS) return fail(GC_ERR_ARG, "index: a=%d outside [1, %d]", a, GC_MAX_ANCHORS);
-  if (n_tokens > 0 && (!corr || !vis_bits || !vis_list)) return fail(GC_ERR_ARG, "index: null pointer");
-  if ((corr && !aligned16(corr)) || (vis_bits && !aligned16(vis_bits)) || (vis_list && !aligned16(vis_list)) ||
-      !aligned16(workspace))
-    return fail(GC_ERR_ALIGN, "index: pointers must be 16-byte aligned");
-  if (workspace_bytes < gc_index_workspace_bytes(n_tokens))
-    return fail(GC_ERR_CAPACITY, "index: workspace of %zu bytes is below the %zu required", workspace_bytes,
-                gc_index_workspace_bytes(n_tokens));
+namespace gc {
+namespace {
+
+// Validation of the visible-token index's own arguments (everything but
+// the scratch memory).
+int check_visible_index(const int32_t* corr, int64_t n_tokens, int a, const uint32_t* vis_bits,
+                        const int32_t* vis_list, const int32_t* n_vis, const char* who) {
+  if (!n_vis) return fail(GC_ERR_ARG, "%s: null n_vis", who);
+  if (n_tokens < 0) return fail(GC_ERR_SHAPE, "%s: n_tokens=%lld is negative", who, (long long)n_tokens);
+  if (n_tokens > 0x7fffffffLL) return fail(GC_ERR_CAPACITY, "%s: n_tokens=%lld exceeds 2^31-1", who, (long long)n_tokens);
+  if (a < 1 || a > GC_MAX_ANCHORS) return fail(GC_ERR_ARG, "%s: a=%d outside [1, %d]", who, a, GC_MAX_ANCHORS);
+  if (n_tokens > 0 && (!corr || !vis_bits || !vis_list)) return fail(GC_ERR_ARG, "%s: null pointer", who);
+  if ((corr && !aligned16(corr)) || (vis_bits && !aligned16(vis_bits)) || (vis_list && !aligned16(vis_list)))
+    return fail(GC_ERR_ALIGN, "%s: pointers must be 16-byte aligned", who);
   const int64_t n_words = (n_tokens + 31) / 32;
   const size_t nc = (size_t)n_tokens * a * 4, nl = (size_t)n_tokens * 4, nbits = (size_t)n_words * 4;
   if (overlaps(vis_bits, nbits, corr, nc) || overlaps(vis_list, nl, corr, nc) || overlaps(vis_list, nl, vis_bits, nbits) ||
-      overlaps(n_vis, 4, vis_list, nl) || overlaps(n_vis, 4, vis_bits, nbits) || overlaps(workspace, workspace_bytes, corr, nc) ||
-      overlaps(workspace, workspace_bytes, vis_list, nl) || overlaps(workspace, workspace_bytes, vis_bits, nbits))
-    return fail(GC_ERR_ALIAS, "index: buffers overlap");
+      overlaps(n_vis, 4, vis_list, nl) || overlaps(n_vis, 4, vis_bits, nbits))
+    return fail(GC_ERR_ALIAS, "%s: buffers overlap", who);
+  return GC_OK;
+}
+
+// The three passes; counts_offsets: 2 * ceil(n_tokens / kChunk) int32 of
+// device scratch, fully written before it is read.
+void launch_visible_index(const int32_t* corr, int64_t n_tokens, int a, uint32_t* vis_bits, int32_t* vis_list,
+                          int32_t* n_vis, int32_t* counts_offsets, hipStream_t stream) {
+  const int64_t n_words = (n_tokens + 31) / 32;
   const int64_t nb = n_tokens > 0 ? (n_tokens + kChunk - 1) / kChunk : 0;
-  int32_t* counts = static_cast<int32_t*>(workspace);
+  int32_t* counts = counts_offsets;
   int32_t* offsets = counts + nb;
   if (nb > 0)
     hipLaunchKernelGGL(k_index_count<VisiblePred>, dim3((unsigned)nb), dim3(kBlock), 0, stream,
@@ -176,7 +189,68 @@ extern "C" int gc_index_correspondence(const int32_t* corr, int64_t n_tokens, in
   if (nb > 0)
     hipLaunchKernelGGL(k_index_scatter<VisiblePred>, dim3((unsigned)nb), dim3(kBlock), 0, stream,
                        VisiblePred{corr, a}, n_tokens, offsets, vis_list);
-  return after_launch(stream, "gc_index_correspondence");
+}
+
+// Device address of this library's scratch array on the current device,
+// looked up once per device (with that device current) and kept.
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+int scratch_on_current_device(void** out, const char* who) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(GC_ERR_HIP, "%s: hipGetDevice: %s", who, hipGetErrorString(e));
+  if (dev < 0 || dev >= kMaxDevices) return fail(GC_ERR_CAPACITY, "%s: device %d beyond %d", who, dev, kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p)
+      return fail(GC_ERR_HIP, "%s: hipGetSymbolAddress of the scratch array: %s", who, hipGetErrorString(e));
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return GC_OK;
+}
+
+}  // namespace
+}  // namespace gc
+
+extern "C" int gc_index_correspondence(const int32_t* corr, int64_t n_tokens, int a, uint32_t* vis_bits,
+                                       int32_t* vis_list, int32_t* n_vis, void* workspace, size_t workspace_bytes,
+                                       hipStream_t stream) {
+  clear_error();
+  const char* who = "gc_index_correspondence";
+  if (!workspace) return fail(GC_ERR_ARG, "%s: null workspace", who);
+  int rc = check_visible_index(corr, n_tokens, a, vis_bits, vis_list, n_vis, who);
+  if (rc) return rc;
+  if (!aligned16(workspace)) return fail(GC_ERR_ALIGN, "%s: pointers must be 16-byte aligned", who);
+  if (workspace_bytes < gc_index_workspace_bytes(n_tokens))
+    return fail(GC_ERR_CAPACITY, "%s: workspace of %zu bytes is below the %zu required", who, workspace_bytes,
+                gc_index_workspace_bytes(n_tokens));
+  const size_t nc = (size_t)n_tokens * a * 4, nl = (size_t)n_tokens * 4, nbits = (size_t)(n_tokens + 31) / 32 * 4;
+  if (overlaps(workspace, workspace_bytes, corr, nc) || overlaps(workspace, workspace_bytes, vis_list, nl) ||
+      overlaps(workspace, workspace_bytes, vis_bits, nbits) || overlaps(workspace, workspace_bytes, n_vis, 4))
+    return fail(GC_ERR_ALIAS, "%s: buffers overlap", who);
+  launch_visible_index(corr, n_tokens, a, vis_bits, vis_list, n_vis, static_cast<int32_t*>(workspace), stream);
+  return after_launch(stream, who);
+}
+
+extern "C" int gc_index_correspondence_noalloc(const int32_t* corr, int64_t n_tokens, int a, uint32_t* vis_bits,
+                                               int32_t* vis_list, int32_t* n_vis, hipStream_t stream) {
+  clear_error();
+  const char* who = "gc_index_correspondence_noalloc";
+  int rc = check_visible_index(corr, n_tokens, a, vis_bits, vis_list, n_vis, who);
+  if (rc) return rc;
+  if (gc_index_workspace_bytes(n_tokens) > GC_NOALLOC_SCRATCH_BYTES)
+    return fail(GC_ERR_CAPACITY, "%s: n_tokens=%lld needs %zu bytes of scratch, above the library's %d", who,
+                (long long)n_tokens, gc_index_workspace_bytes(n_tokens), GC_NOALLOC_SCRATCH_BYTES);
+  void* ws = nullptr;
+  rc = scratch_on_current_device(&ws, who);
+  if (rc) return rc;
+  launch_visible_index(corr, n_tokens, a, vis_bits, vis_list, n_vis, static_cast<int32_t*>(ws), stream);
+  return after_launch(stream, who);
 }
 
 extern "C" int gc_index_foreground(const float* pos, int64_t n_tokens, uint32_t* fg_bits, int32_t* fg_recs,

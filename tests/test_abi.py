@@ -418,3 +418,25 @@ def test_forced_views_and_gaps_host_calls(gc, L):
     assert L.gc_schedule_advance_gaps(g, 3, None, 1, 0) == -1
     assert L.gc_schedule_advance_gaps(g, 3, v, 4, 0) == -1
     assert list(g) == [0, 1, 2]                 # a rejected call leaves the gaps alone
+
+
+def test_noalloc_index_validation(gc, L):
+    """gc_index_correspondence_noalloc checks its arguments and its scratch
+    limit (GC_NOALLOC_SCRATCH_BYTES: 2 * ceil(n / 1024) int32, so at most
+    134217728 tokens) on the host, before it touches a device."""
+    nv = (ctypes.c_int32 * 1)()
+
+    def call(corr=A0, n=4096, a=4, bits=A1, lst=A2, nvp=A3):
+        return L.gc_index_correspondence_noalloc(corr, n, a, bits, lst, nvp, None)
+
+    assert gc.GC_NOALLOC_SCRATCH_BYTES == 1 << 20
+    big = 134217728
+    far = [(i + 1) << 40 for i in range(4)]     # 1 TiB apart: nothing overlaps
+    assert call(corr=far[0], bits=far[1], lst=far[2], nvp=far[3], n=big + 1) == -6 and "scratch" in _err(L)
+    assert int(L.gc_index_workspace_bytes(big)) == 1 << 20
+    assert call(nvp=None) == -1
+    assert call(a=9) == -1
+    assert call(n=-1) == -2
+    assert call(corr=A0 + 4) == -4
+    assert call(lst=A1 + 64) == -5             # list overlaps the bits
+    assert call(n=2 ** 31) == -6
