@@ -9,13 +9,19 @@ the 256 MB last-level cache cannot serve a step from the previous one.
 
 Reported (one JSON line):
   value      transported view-pixels per second, B * (N - a) * H * W per step
-  roofline   the fused kernel's algorithmic bytes per launch over its average
-             launch duration (HIP events on the launch stream bracketing the K
-             back-to-back launches of the timed region), against 8 TB/s
+  roofline   the fused kernel's algorithmic bytes per launch (the latents read
+             and written, a correspondence word per (target token, anchor) and
+             the K weights of every visible pair) over its average launch
+             duration (HIP events on the launch stream bracketing the K
+             back-to-back launches of the timed region), against 8 TB/s; beside
+             it the practical ceiling, a plain nontemporal 16-byte copy kernel
+             (ceiling/)
   cpu_baseline  the oracle's transport + reconstruction on one asset, timed
              single-threaded on the host
-The once-per-asset rows (area downsample, bbox, correspondence builds) and
-the unfused pair are timed too and reported under "rows".
+The once-per-asset rows (area downsample, bbox, correspondence builds), the
+unfused pair, the plain copy / read / write kernels and the other workloads
+(cache-resident, and from HBM after a flush) are timed too and reported
+under "rows".  --cold WORKLOAD runs only that workload's from-HBM steps.
 """
 import argparse
 import ctypes
@@ -47,12 +53,82 @@ def parse():
                     help="also run a plain 1 GiB device copy (reference kernel for counter scaling)")
     ap.add_argument("--quiet", action="store_true")
     ap.add_argument("--no-small", action="store_true", help="skip the rows of the other workloads")
+    ap.add_argument("--cold", metavar="WORKLOAD",
+                    help="only the from-HBM steps of one workload's row (each after an L2 / LLC flush); for "
+                         "kernel traces and counter passes of that workload's fused kernel")
     return ap.parse_args()
 
 
 def log(args, *a):
     if not args.quiet:
         print(*a, file=sys.stderr, flush=True)
+
+
+def load_ceiling():
+    """ceiling/libceiling.so: plain copy / read / write kernels with the
+    per-step kernels' access shape (built by build())."""
+    path = os.path.join(ROOT, "ceiling", "libceiling.so")
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is missing: build it (python -c 'import __graft_entry__ as g; g.build()')")
+    L = ctypes.CDLL(path)
+    vp, i64, ci = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int
+    L.ceil_copy.argtypes = [vp, vp, i64, ci, vp]
+    L.ceil_read.argtypes = [vp, i64, vp, ci, vp]
+    L.ceil_write.argtypes = [vp, i64, ctypes.c_uint32, ci, vp]
+    for f in (L.ceil_copy, L.ceil_read, L.ceil_write):
+        f.restype = ci
+    return L
+
+
+class Flush:
+    """Evicts earlier data from L2 and the 256 MB last-level cache: one plain
+    read of a 1 GiB buffer, on the given stream (outside any timed region)."""
+
+    def __init__(self, torch, dev):
+        self.L = load_ceiling()
+        self.n16 = (1 << 30) // 16
+        self.buf = torch.ones(1 << 28, dtype=torch.int32, device=dev)
+        self.sink = torch.empty(((self.n16 + 255) // 256) * 4, dtype=torch.int32, device=dev)
+
+    def __call__(self, stream_handle):
+        rc = self.L.ceil_read(self.buf.data_ptr(), self.n16, self.sink.data_ptr(), 0, stream_handle)
+        if rc != 0:
+            raise RuntimeError(f"ceil_read failed ({rc})")
+
+
+def ceiling_rows(torch, dev):
+    """GB/s (bytes read + written) of the plain streaming kernels over 1 GiB,
+    cached and nontemporal, ten back-to-back launches each: the practical
+    ceiling the per-step kernels are compared with."""
+    L = load_ceiling()
+    n16 = (1 << 30) // 16
+    a = torch.ones(1 << 28, dtype=torch.int32, device=dev)
+    b = torch.zeros_like(a)
+    sink = torch.empty(((n16 + 255) // 256) * 4, dtype=torch.int32, device=dev)
+    s = torch.cuda.current_stream().cuda_stream
+
+    def timed(call, n=10):
+        for _ in range(2):
+            if call() != 0:
+                raise RuntimeError("ceiling kernel launch failed")
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(n):
+            call()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / n
+
+    out = {}
+    for nt, tag in ((0, ""), (1, "_nt")):
+        out["copy" + tag + "_GBps"] = 2 * (1 << 30) / (timed(lambda: L.ceil_copy(a.data_ptr(), b.data_ptr(), n16, nt, s)) * 1e-3) / 1e9
+        out["read" + tag + "_GBps"] = (1 << 30) / (timed(lambda: L.ceil_read(a.data_ptr(), n16, sink.data_ptr(), nt, s)) * 1e-3) / 1e9
+        out["write" + tag + "_GBps"] = (1 << 30) / (timed(lambda: L.ceil_write(b.data_ptr(), n16, 7, nt, s)) * 1e-3) / 1e9
+    ms = timed(lambda: (b.copy_(a), 0)[1])
+    out["torch_copy_GBps"] = 2 * (1 << 30) / (ms * 1e-3) / 1e9
+    del a, b, sink
+    return out
 
 
 def kernel_source_hash():
@@ -90,6 +166,14 @@ def main():
 
     import paper_2608_13255_amd as gc
     import synth
+
+    if args.cold:
+        torch.cuda.set_device(0)
+        if args.copy_probe:
+            copy_probe(torch, torch.device("cuda:0"))
+        row = config_row(gc, synth, args.cold, cold_steps=max(args.steps, 10), warm=False)
+        print(json.dumps({"workload": args.cold, "cold_steps": max(args.steps, 10), **row}), flush=True)
+        return
 
     w = synth.CONFIGS[args.config]
     dev = torch.device("cuda:0")
@@ -254,8 +338,14 @@ def main():
     n_tok = B * (N - a) * HW
 
     def algo_bytes(A):
-        # latents: read x0_prev, x0_anchor_new, x_t, write x0_out, x_next; index: one bit per
-        # target token + the list of visible tokens; their words; the weights of visible pairs
+        # what one cached step must move (the definition of the per-step unit): read
+        # x0_prev, x0_anchor_new, x_t, write x0_out, x_next; a correspondence word per
+        # (target token, anchor); the K weights of every visible (token, anchor) pair
+        return B * (4 * N + a) * latent_view + 4 * n_tok * a + 4 * K * vis_pairs[A]
+
+    def index_bytes(A):
+        # what the split launch reads of the operator instead of every word: a bit per
+        # target token, the list of visible tokens and their words
         nv = index[A].n_vis
         return (B * (4 * N + a) * latent_view + 4 * ((n_tok + 31) // 32) + 4 * nv + 4 * a * nv
                 + 4 * K * vis_pairs[A])
@@ -303,6 +393,8 @@ def main():
     avg_kernel_ms = ms_per_step
     bytes_per_launch = float(np.mean([algo_bytes(A) for A in used]))
     achieved = bytes_per_launch / (avg_kernel_ms * 1e-3) / 1e9
+    rows["index_bytes_per_launch"] = float(np.mean([index_bytes(A) for A in used]))
+    rows["index_bytes_GBps"] = rows["index_bytes_per_launch"] / (avg_kernel_ms * 1e-3) / 1e9
 
     # ---- per-step distribution (outside the timed region) ---------------------
     # each step between its own pair of events; the events' own cost widens
@@ -317,6 +409,18 @@ def main():
     torch.cuda.synchronize()
     per_step_us = np.array([evs[i].elapsed_time(evs[i + 1]) * 1e3 for i in range(n_dist)])
     rows["step_us_p10_p50_p90"] = [round(float(np.percentile(per_step_us, q)), 2) for q in (10, 50, 90)]
+    # the same steps on one buffer set (262 MB, about the size of the last-level
+    # cache): what the LLC can serve of a step that re-reads the last one's
+    # buffers, against the ring's every-step-from-HBM figure above
+    torch.cuda.synchronize()
+    r0, r1 = ev(), ev()
+    r0.record()
+    for i in range(args.steps):
+        A = tuple(gc.gc_schedule_anchors(N, a, i))
+        plans[(0, A)](*gc.gc_sampler_step_times(smp, w.S, cached_steps[i % len(cached_steps)]))
+    r1.record()
+    torch.cuda.synchronize()
+    rows["step_us_one_buffer_set"] = r0.elapsed_time(r1) / args.steps * 1e3
 
     # ---- unfused pair and full step, for the record -------------------------
     def timed(fn, n=20):
@@ -433,15 +537,10 @@ def main():
     rows["n_vis_histogram_per_anchor_set"] = [
         torch.bincount((ops[A][0] != 0).sum(-1).flatten(), minlength=a + 1).tolist() for A in anchor_sets]
 
-    copy_gbps = None
     if args.copy_probe:
-        src = torch.empty(1 << 28, dtype=torch.float32, device=dev)
-        dst = torch.empty_like(src)
-        src.fill_(1.0)
-        ms = timed(lambda: dst.copy_(src), n=10)
-        copy_gbps = 2 * src.numel() * 4 / (ms * 1e-3) / 1e9
-        rows["copy_1GiB_GBps"] = copy_gbps
-        del src, dst
+        copy_probe(torch, dev)
+    # the practical ceiling: plain streaming kernels with the step's access shape
+    rows["ceiling"] = ceiling_rows(torch, dev)
 
     # ---- the other workloads: eager vs HIP-graph replay ------------------------
     if not args.no_small:
@@ -479,11 +578,25 @@ def main():
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
                      "frac": achieved / PEAK_HBM_GBS,
                      "traffic": traffic, "kernel": FUSED_KERNEL, "algorithmic_bytes_per_launch": bytes_per_launch,
-                     "avg_launch_us": avg_kernel_ms * 1e3},
+                     "avg_launch_us": avg_kernel_ms * 1e3,
+                     "copy_ceiling_GBps": rows["ceiling"]["copy_nt_GBps"],
+                     "frac_of_copy_ceiling": achieved / rows["ceiling"]["copy_nt_GBps"]},
         "cpu_baseline": cpu,
         "rows": rows,
     }
     print(json.dumps(out), flush=True)
+
+
+def copy_probe(torch, dev):
+    """A plain 1 GiB device-to-device copy (torch's), the reference dispatch
+    whose FETCH_SIZE / WRITE_SIZE readings scale the counters of the other
+    kernels in the same rocprofv3 run."""
+    src = torch.ones(1 << 28, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    for _ in range(11):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    del src, dst
 
 
 def coverage_rows(gc, w, pos, cams, bbox, full, R=2):
@@ -565,15 +678,20 @@ def coverage_rows(gc, w, pos, cams, bbox, full, R=2):
 GRAPH_STEPS = 24   # cached steps captured per graph (rounded up to whole rotations)
 
 
-def config_row(gc, synth, name, steps=300, oracle_seconds=None):
-    """One cached step of another workload, launched eagerly and replayed
-    from a HIP graph holding a run of consecutive steps (one per anchor set
-    of the rotation, repeated): microseconds per step each way, transported
-    view-pixels/s and algorithmic GB/s at the faster of the two.  These
-    working sets fit in the 256 MB last-level cache, so their GB/s is not an
-    HBM figure; the smaller ones are launch-bound.  With oracle_seconds, the
-    oracle's cached step on the same workload is timed beside it (one host
-    thread, from the seeded render on its own)."""
+def config_row(gc, synth, name, steps=300, oracle_seconds=None, cold_steps=30, warm=True):
+    """One cached step of another workload, three ways: launched eagerly and
+    replayed from a HIP graph holding a run of consecutive steps (one per
+    anchor set of the rotation, repeated) -- these working sets fit in the
+    256 MB last-level cache and are re-read every step, so those GB/s are
+    cache-resident figures and the smaller workloads are launch-bound -- and
+    from HBM: each of cold_steps steps between its own pair of events after a
+    1 GiB read that evicts the step's data from L2 and the LLC (the events
+    add their own cost to these short steps).  Algorithmic bytes per step are
+    the latents, a correspondence word per (target token, anchor) and the
+    weights of the visible pairs.  With oracle_seconds, the oracle's cached
+    step on the same workload is timed beside it (one host thread, from the
+    seeded render on its own).  warm=False runs the HBM steps only."""
+    import numpy as np
     import torch
     w = synth.CONFIGS[name]
     dev = torch.device("cuda:0")
@@ -607,12 +725,14 @@ def config_row(gc, synth, name, steps=300, oracle_seconds=None):
         corr, wts = gc.gc_build_correspondence(pos, cams, A, w.K, bbox, stats=st)
         idx = gc.gc_index_correspondence(corr)
         pairs = int(st[:, 0].sum().item())
-        step_bytes.append(w.B * (4 * w.N + len(A)) * w.H * w.W * w.C * es + 4 * ((n_tok + 31) // 32) + 4 * idx.n_vis
-                          + 4 * len(A) * idx.n_vis + 4 * w.K * pairs)
+        step_bytes.append(w.B * (4 * w.N + len(A)) * w.H * w.W * w.C * es + 4 * n_tok * len(A) + 4 * w.K * pairs)
         new = torch.randn((w.B, len(A), w.H, w.W, w.C), generator=g, device=dev).to(tdt)
         calls.append(gc.bind_transport_reconstruct(x0, new, corr, wts, xt, A, smp, torch.empty_like(x0),
                                                    torch.empty_like(x0), index=idx, stream=s))
     torch.cuda.synchronize()
+    V = n_tok
+    mean_bytes = sum(step_bytes) / len(step_bytes)
+    row = {"view_pixels_per_step": V, "algorithmic_bytes_per_step": mean_bytes}
     reps = max(1, steps // len(calls))
 
     def timed(fn, n):
@@ -629,24 +749,43 @@ def config_row(gc, synth, name, steps=300, oracle_seconds=None):
     def eager():
         for c in calls:
             c(t, tn)
-    eager_ms = timed(eager, reps) / len(calls)
-    # A captured denoising loop holds many consecutive steps; a graph of one
-    # step per replay would time the replay call's own host overhead instead.
-    rounds = -(-GRAPH_STEPS // len(calls))
-    graph = torch.cuda.CUDAGraph()
-    with torch.cuda.graph(graph, stream=s):
-        for _ in range(rounds):
-            eager()
-    graph_ms = timed(graph.replay, max(1, reps // rounds)) / (len(calls) * rounds)
-    V = n_tok
-    best = min(eager_ms, graph_ms)
-    row = {"view_pixels_per_step": V, "eager_us_per_step": eager_ms * 1e3, "graph_us_per_step": graph_ms * 1e3,
-           "view_pixels_per_s": V / (best * 1e-3),
-           "algorithmic_GBps": sum(step_bytes) / len(step_bytes) / (best * 1e-3) / 1e9}
+    if warm:
+        eager_ms = timed(eager, reps) / len(calls)
+        # A captured denoising loop holds many consecutive steps; a graph of one
+        # step per replay would time the replay call's own host overhead instead.
+        rounds = -(-GRAPH_STEPS // len(calls))
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph, stream=s):
+            for _ in range(rounds):
+                eager()
+        graph_ms = timed(graph.replay, max(1, reps // rounds)) / (len(calls) * rounds)
+        best = min(eager_ms, graph_ms)
+        row.update({"eager_us_per_step": eager_ms * 1e3, "graph_us_per_step": graph_ms * 1e3,
+                    "view_pixels_per_s": V / (best * 1e-3),
+                    "cache_resident_algorithmic_GBps": mean_bytes / (best * 1e-3) / 1e9})
+    # from HBM: each step after a flush of L2 and the LLC, between its own events
+    flush = Flush(torch, dev)
+    calls[0](t, tn)
+    torch.cuda.synchronize()
+    cold = []
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    for i in range(cold_steps):
+        flush(s.cuda_stream)
+        e0.record(s)
+        calls[i % len(calls)](t, tn)
+        e1.record(s)
+        torch.cuda.synchronize()
+        cold.append(e0.elapsed_time(e1))
+    p50 = float(np.median(cold))
+    row.update({"hbm_us_per_step_p10_p50_p90": [round(float(np.percentile(cold, q)) * 1e3, 2) for q in (10, 50, 90)],
+                "hbm_view_pixels_per_s": V / (p50 * 1e-3),
+                "hbm_algorithmic_GBps": mean_bytes / (p50 * 1e-3) / 1e9,
+                "hbm_frac_of_peak": mean_bytes / (p50 * 1e-3) / 1e9 / PEAK_HBM_GBS})
+    del flush
     if oracle_seconds:
         vps = oracle_step_rate(w, hi_np, oracle_seconds)
         row["oracle_view_pixels_per_s"] = vps
-        row["gpu_over_oracle"] = row["view_pixels_per_s"] / vps
+        row["gpu_over_oracle"] = row.get("view_pixels_per_s", row["hbm_view_pixels_per_s"]) / vps
     return row
 
 
