@@ -603,11 +603,11 @@ def coverage_rows(gc, w, pos, cams, bbox, full, R=2):
     """One whole trajectory of the schedule alone (no latents) per anchor
     policy: per-step staleness of the foreground tokens after the step
     (mean, fraction stale for >= R steps, max) and the policy's cost per
-    cached step: wall time of the selection or scoring, the staleness update
-    and the host read-backs it needs (the anchors, the counters), and device
-    time (HIP events around the selection's launches and around the update's,
-    summed: the kernels and the gaps between back-to-back launches, not the
-    read-backs)."""
+    cached step two ways: the wall time of the trajectory's step (selection
+    or scoring, the staleness update and the host read-backs of the anchors
+    and counters), and the device time of the same launches captured in a
+    HIP graph and replayed back to back (what they cost the GPU when the host
+    is not in the way)."""
     import numpy as np
     import torch
     N, a = w.N, w.a
@@ -634,44 +634,63 @@ def coverage_rows(gc, w, pos, cams, bbox, full, R=2):
     max_gap = -(-N // a)
     for policy in ("rotate", "rotation_coverage", "coverage"):
         stale = gc.gc_coverage_init(pos)
-        gap, c, rec, cost, dev_ms = [0] * N, 0, [], [], []
+        gap, c, rec, cost = [0] * N, 0, [], []
         for k in range(w.S):
             torch.cuda.synchronize()
             t0 = time.perf_counter()
-            e0, e1, e2, e3 = (torch.cuda.Event(enable_timing=True) for _ in range(4))
-            e0.record()
             if full[k] or k == 0:
                 A = list(range(N))
             elif policy == "rotate":
                 A = gc.gc_schedule_anchors(N, a, c)
             elif policy == "rotation_coverage":
-                sc = gc.gc_coverage_score(pairs, stale, rot_sets, workspace=ws)
-                e1.record()
-                sc = sc.cpu().tolist()
+                sc = gc.gc_coverage_score(pairs, stale, rot_sets, workspace=ws).cpu().tolist()
                 A = rot_sets[sc.index(max(sc))]
             else:
-                due = sorted([v for v in range(N) if gap[v] >= max_gap], key=lambda v: (-gap[v], v))[:a]
-                A = gc.gc_coverage_select(pairs, stale, a, forced=due, workspace=ws)
-                e1.record()
-                A = A.cpu().tolist()
-            if full[k] or k == 0 or policy == "rotate":
-                e1.record()   # no selection launches
-            e2.record()
+                due = gc.gc_schedule_forced_views(gap, a, max_gap)
+                A = gc.gc_coverage_select(pairs, stale, a, forced=due, workspace=ws).cpu().tolist()
             st = gc.gc_coverage_update(pairs, stale, A, R)
-            e3.record()
             st = st.cpu().numpy().astype(np.int64)
             if not (full[k] or k == 0):
                 cost.append(time.perf_counter() - t0)
-                dev_ms.append(e0.elapsed_time(e1) + e2.elapsed_time(e3))
                 c += 1
-            gap = [0 if (full[k] or v in A) else g + 1 for v, g in enumerate(gap)]
+            gap = gc.gc_schedule_advance_gaps(gap, A, bool(full[k] or k == 0))
             fg = st[..., 0].sum()
             rec.append((st[..., 2].sum() / fg, st[..., 1].sum() / fg, st[..., 3].max()))
         r = np.array(rec, np.float64)
+        # the policy's launches for one cached step, captured and replayed back to back
+        sgr = torch.cuda.Stream()
+        stats_buf = torch.empty((w.B, N, 4), dtype=torch.int32, device=pos.device)
+        sel_buf = torch.empty(a, dtype=torch.int32, device=pos.device)
+        score_buf = torch.empty(len(rot_sets), dtype=torch.int64, device=pos.device)
+        A0 = rot_sets[0]
+        torch.cuda.synchronize()
+
+        def policy_step():
+            if policy == "rotation_coverage":
+                gc.gc_coverage_score(pairs, stale, rot_sets, out=score_buf, workspace=ws, stream=sgr)
+            elif policy == "coverage":
+                gc.gc_coverage_select(pairs, stale, a, out=sel_buf, workspace=ws, stream=sgr)
+            gc.gc_coverage_update(pairs, stale, A0, R, stats=stats_buf, stream=sgr)
+
+        reps = 20
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph, stream=sgr):
+            for _ in range(reps):
+                policy_step()
+        g0, g1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        with torch.cuda.stream(sgr):    # replay() launches on the current stream: the events' stream
+            graph.replay()
+            torch.cuda.synchronize()
+            g0.record(sgr)
+            for _ in range(5):
+                graph.replay()
+            g1.record(sgr)
+        torch.cuda.synchronize()
         out[policy] = {"mean_staleness": round(float(r[:, 0].mean()), 5),
                        "frac_stale_ge_R": round(float(r[:, 1].mean()), 5), "max_staleness": int(r[:, 2].max()),
                        "ms_per_cached_step": round(float(np.median(cost)) * 1e3, 4),
-                       "device_ms_per_cached_step": round(float(np.median(dev_ms)), 4)}
+                       "device_ms_per_cached_step": round(g0.elapsed_time(g1) / (5 * reps), 4)}
+        del graph
     return out
 
 
@@ -736,13 +755,16 @@ def config_row(gc, synth, name, steps=300, oracle_seconds=None, cold_steps=30, w
     reps = max(1, steps // len(calls))
 
     def timed(fn, n):
-        fn()
-        torch.cuda.synchronize()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record(s)
-        for _ in range(n):
+        # with s current: the bound calls launch on s, and graph.replay() on the
+        # current stream, so the events on s bracket the launches either way
+        with torch.cuda.stream(s):
             fn()
-        e1.record(s)
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(s)
+            for _ in range(n):
+                fn()
+            e1.record(s)
         torch.cuda.synchronize()
         return e0.elapsed_time(e1) / n
 

@@ -507,15 +507,21 @@ int gc_transport_unipc_geom(const void* x0_prev, const void* x0_anchor_new, cons
  *   anchors_out (device int32 [a], ascending); forced: host [n_forced] views
  *   that must be in it.  a <= GC_MAX_ANCHORS.  workspace: caller-owned device
  *   memory of gc_coverage_workspace_bytes(), 16-byte aligned; it holds
- *   per-block partial gains and the chosen set, so concurrent calls need
- *   separate workspaces.  Enqueues 2 (a - n_forced) launches (one when every
- *   view is forced) and never synchronises.
+ *   the coverage histogram (or per-block partial gains), so concurrent calls
+ *   need separate workspaces.  With N <= 12 it enqueues three launches
+ *   whatever a is: the histogram over the tokens' cover masks (own view and
+ *   the views that see them) of the weights 1 + staleness, then one block
+ *   that takes its subset sums Y and runs every round, the gain of u given
+ *   the chosen set S being Y[all \ S] - Y[all \ (S + u)]; with more views,
+ *   2 (a - n_forced) launches.  One launch when every view is forced.  Never
+ *   synchronises.
  * gc_coverage_score: scores (device uint64 [M], overwritten) = the weighted
  *   coverage, sum of 1 + staleness over the foreground tokens it covers, of
  *   each candidate set sets (host int32 [M][a]); M <= 64.  workspace as for
  *   gc_coverage_select (per-block partial sums; no atomics).  Choosing the
  *   rotation's set with the largest score keeps the rotation's evenly spread
- *   anchors while following where the stale tokens are.
+ *   anchors while following where the stale tokens are.  With N <= 12 a set's
+ *   score is Y[all] - Y[all \ S] from the same histogram (three launches).
  * gc_schedule_refresh_due: host; stats as written by gc_coverage_update and
  *   copied to the host; *due = 1 when a full step is due.
  */

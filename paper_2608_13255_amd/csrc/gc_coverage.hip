@@ -94,11 +94,6 @@ __global__ void k_cov_init(const float* __restrict__ pos, int64_t n_tok, uint8_t
   stale[i] = (finite_f(P[0]) && finite_f(P[1]) && finite_f(P[2])) ? 0 : kBackground;
 }
 
-__global__ void k_fill_u32(uint32_t* __restrict__ p, int n, uint32_t v) {
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < n) p[i] = v;
-}
-
 // The token kernels give each lane one pair word: 32 consecutive tokens of
 // a row, the staleness bytes of those tokens (two 16-byte loads, or bytewise
 // when the rows are not 16-byte aligned) and, per view, one coalesced uint32
@@ -191,20 +186,22 @@ __device__ __forceinline__ uint32_t weighted_count(const uint32_t (&w)[8], uint3
   return acc;
 }
 
-// grid: x = one-wave blocks striding over the items of one (asset, view), y
-// = b * N + v.  stats[b][v] = foreground tokens, tokens with staleness >= R,
-// sum, max (after the update); each block adds its totals once.
+// One block per (asset, view) row (blockIdx.x = b * N + v); its lanes
+// stride over the row's pair words.  stats[b][v] = foreground tokens, tokens
+// with staleness >= R, sum, max (after the update), reduced in the block and
+// written once: no atomics, and no zeroing launch in front.
+constexpr int kRowBlock = 512;
+
 template <bool VEC>
-__global__ __launch_bounds__(64) void k_cov_update(const uint32_t* __restrict__ bits, int B, int N, int HW, int wpr,
-                                                   unsigned long long anchor_mask, int R, uint8_t* __restrict__ stale,
-                                                   uint32_t* __restrict__ stats) {
-  const int bv = blockIdx.y;
+__global__ __launch_bounds__(kRowBlock) void k_cov_update(const uint32_t* __restrict__ bits, int B, int N, int HW,
+                                                          int wpr, unsigned long long anchor_mask, int R,
+                                                          uint8_t* __restrict__ stale, uint32_t* __restrict__ stats) {
+  __shared__ uint32_t part[kRowBlock / 64][4];
+  const int bv = blockIdx.x;
   const int b = bv / N, v = bv % N;
-  const int lane = (int)threadIdx.x;
   uint8_t* row = stale + (int64_t)bv * HW;
   uint32_t c_fg = 0, c_ge = 0, c_sum = 0, c_max = 0;   // this lane's totals
-  for (int wi = blockIdx.x * 64 + lane; wi - lane < wpr; wi += gridDim.x * 64) {
-    if (wi >= wpr) continue;
+  for (int wi = (int)threadIdx.x; wi < wpr; wi += kRowBlock) {
     const uint32_t fresh = set_covers(bits, B, N, wpr, anchor_mask, b, v, wi) & valid_bits(HW, wi);
     uint32_t d[8];
     load_word_bytes<VEC>(row, HW, wi * 32, d);
@@ -229,17 +226,224 @@ __global__ __launch_bounds__(64) void k_cov_update(const uint32_t* __restrict__ 
     }
     store_word_bytes<VEC>(row, HW, wi * 32, d);
   }
+  // every lane reaches the wave reductions (none returned early)
   c_fg = wave_add(c_fg);
   c_ge = wave_add(c_ge);
   c_sum = wave_add(c_sum);
   c_max = wave_max(c_max);
-  if (lane < 4) {
-    const uint32_t acc = lane == 0 ? c_fg : lane == 1 ? c_ge : lane == 2 ? c_sum : c_max;
-    uint32_t* o = stats + (int64_t)bv * 4 + lane;
-    if (lane == 3)
-      atomicMax(o, acc);
-    else if (acc)
-      atomicAdd(o, acc);
+  const int wv = (int)threadIdx.x / 64;
+  if (__lane_id() == 0) {
+    part[wv][0] = c_fg;
+    part[wv][1] = c_ge;
+    part[wv][2] = c_sum;
+    part[wv][3] = c_max;
+  }
+  __syncthreads();
+  if (threadIdx.x < 4) {
+    const int k = (int)threadIdx.x;
+    uint32_t acc = 0u;
+    for (int q = 0; q < kRowBlock / 64; ++q) acc = k == 3 ? max(acc, part[q][k]) : acc + part[q][k];
+    stats[(int64_t)bv * 4 + k] = acc;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Selection and scores through the coverage histogram (N <= kHistViews).
+// Every foreground token has a cover mask: bit v for its own view v and bit
+// u for every view u that sees it.  H[m], the summed weight 1 + staleness of
+// the tokens whose mask is m, decides both: with Y[X] the sum of H[m] over
+// the masks m that are subsets of X (the subset sums of H) and U all views,
+//   gain(u | S) = Y[U \ S] - Y[U \ (S + u)]   (the uncovered weight u covers)
+//   score(S)    = Y[U] - Y[U \ S]             (the weight S covers)
+// as exact integer sums.  Two launches: H and a block counter are cleared,
+// then one kernel makes the pass over the tokens -- each block builds its
+// histogram in LDS and adds its non-zero bins to H with integer atomics --
+// and its last block to finish (the counter's ticket) takes the subset sums
+// and runs every greedy round, or scores every set, with two lookups per
+// candidate.  No block waits for another.
+constexpr int kHistViews = 12;
+constexpr int kHistBins = 1 << kHistViews;
+constexpr int kHistThreads = 1024;                // 4 lanes per pair word, 8 tokens each
+constexpr int kHistBlocks = 256;                  // blocks of the token pass (more for huge inputs)
+constexpr int64_t kHistMaxWords = 1 << 16;        // words per block: 2^21 tokens * 255 < 2^32 per LDS bin
+
+struct HistState {
+  unsigned long long H[kHistBins];
+  unsigned int ticket;                            // blocks of the token pass that have added their bins
+};
+
+__global__ void k_hist_clear(HistState* __restrict__ hs, int nb) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < nb) hs->H[i] = 0ull;
+  if (i == 0) hs->ticket = 0u;
+}
+
+// Staleness bytes of tokens t0 .. t0 + 7 of a row, four per register;
+// tokens past the row read as background.  VEC: 16-byte aligned rows of a
+// multiple of 16 tokens (t0, a multiple of 8, then has all 8 in the row).
+template <bool VEC>
+__device__ __forceinline__ void load_8_bytes(const uint8_t* __restrict__ row, int HW, int t0, uint32_t (&d)[2]) {
+  if constexpr (VEC) {
+    const uint2 q = t0 < HW ? *reinterpret_cast<const uint2*>(row + t0) : make_uint2(~0u, ~0u);
+    d[0] = q.x;
+    d[1] = q.y;
+  } else {
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+      uint32_t x = 0u;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int t = t0 + 4 * k + j;
+        x |= (t < HW ? (uint32_t)row[t] : 0xffu) << (8 * j);
+      }
+      d[k] = x;
+    }
+  }
+}
+
+// Y = the subset sums of H (read with agent-scope atomic loads, after the
+// blocks' atomics), left in y (LDS), by 1024 threads holding four
+// consecutive masks each: the passes over bits 0 and 1 stay in registers,
+// bits 2..7 pair lanes of a wave, bits 8..11 pair waves through LDS.
+__device__ __forceinline__ void subset_sums(HistState* __restrict__ hs, int N, unsigned long long* y) {
+  const int nb = 1 << N;
+  const int t = (int)threadIdx.x;
+  unsigned long long r[4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k)
+    r[k] = 4 * t + k < nb ? __hip_atomic_load(&hs->H[4 * t + k], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0ull;
+  r[1] += r[0];
+  r[3] += r[2];
+  if (N > 1) {
+    r[2] += r[0];
+    r[3] += r[1];
+  }
+  const int lane = __lane_id();
+  for (int q = 2; q < N && q < 8; ++q) {   // uniform
+    const int d = 1 << (q - 2);
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const unsigned long long o = (unsigned long long)__shfl_xor((long long)r[k], d);
+      if (lane & d) r[k] += o;
+    }
+  }
+  for (int q = 8; q < N; ++q) {   // uniform
+    const int d = 1 << (q - 2);   // partner thread t ^ d, a whole number of waves away
+#pragma unroll
+    for (int k = 0; k < 4; ++k) y[4 * t + k] = r[k];
+    __syncthreads();
+    if (t & d) {
+#pragma unroll
+      for (int k = 0; k < 4; ++k) r[k] += y[4 * (t ^ d) + k];
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int k = 0; k < 4; ++k) y[4 * t + k] = r[k];
+  __syncthreads();
+}
+
+// The views of mask in ascending order.
+__device__ __forceinline__ void write_set(unsigned long long mask, int N, int32_t* out) {
+  int j = 0;
+  for (int u = 0; u < N; ++u)
+    if ((mask >> u) & 1ull) out[j++] = u;
+}
+
+// Candidate sets as view masks.
+constexpr int kMaxSets = 64;       // candidate sets per gc_coverage_score call
+struct SetMasks {
+  unsigned long long m[kMaxSets];
+};
+
+// The pass over the tokens (lane group of 4 per pair word, 8 tokens per
+// lane; blocks stride over the words of every (asset, view) row), then in
+// the last block: SCORE == false, forced views first and a - n_forced greedy
+// rounds (largest gain, ties to the lower view; wave 0, lane u evaluating
+// candidate u), the set to out; SCORE == true, score[m] for the M sets.
+template <bool VEC, bool SCORE>
+__global__ __launch_bounds__(kHistThreads) void k_cov_hist(const uint32_t* __restrict__ bits,
+                                                           const uint8_t* __restrict__ stale, int B, int N, int HW,
+                                                           int wpr, int64_t n_words, HistState* __restrict__ hs, int a,
+                                                           unsigned long long forced, int32_t* __restrict__ out,
+                                                           SetMasks sets, int M, unsigned long long* __restrict__ score) {
+  __shared__ unsigned long long y[kHistBins];     // the last block's subset sums
+  __shared__ uint32_t h[kHistBins];               // this block's histogram
+  __shared__ int last;
+  const int nb = 1 << N;
+  for (int i = (int)threadIdx.x; i < nb; i += kHistThreads) h[i] = 0u;
+  __syncthreads();
+  const int sub = (int)threadIdx.x & 3;           // which 8 tokens of the word
+  for (int64_t wg = ((int64_t)blockIdx.x * kHistThreads + threadIdx.x) >> 2; wg < n_words;
+       wg += (int64_t)gridDim.x * (kHistThreads / 4)) {
+    const int bv = (int)(wg / wpr);
+    const int wi = (int)(wg - (int64_t)bv * wpr);
+    const int b = bv / N, v = bv - b * N;
+    uint32_t w[2];   // weights 1 + staleness of the lane's 8 tokens (0: background and past the row)
+    load_8_bytes<VEC>(stale + (int64_t)bv * HW, HW, wi * 32 + 8 * sub, w);
+    w[0] = bytes_plus_one(w[0]);
+    w[1] = bytes_plus_one(w[1]);
+    if (!(w[0] | w[1])) continue;
+    uint32_t pb[kHistViews];   // the other views' pair bits of these 8 tokens
+#pragma unroll
+    for (int u = 0; u < kHistViews; ++u)
+      pb[u] = (u < N && u != v) ? (pair_word(bits, B, N, wpr, u, b, v, wi) >> (8 * sub)) & 0xffu : 0u;
+    // neighbouring tokens mostly share a mask: runs of one mask go to LDS as one add
+    uint32_t run_m = 0u, run_w = 0u;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const uint32_t wt = (w[j >> 2] >> (8 * (j & 3))) & 0xffu;
+      uint32_t m = 1u << v;
+#pragma unroll
+      for (int u = 0; u < kHistViews; ++u) m |= ((pb[u] >> j) & 1u) << u;
+      if (wt) {
+        if (m == run_m) {
+          run_w += wt;
+        } else {
+          if (run_w) atomicAdd(&h[run_m], run_w);
+          run_m = m;
+          run_w = wt;
+        }
+      }
+    }
+    if (run_w) atomicAdd(&h[run_m], run_w);
+  }
+  __syncthreads();
+  for (int i = (int)threadIdx.x; i < nb; i += kHistThreads)
+    if (h[i]) atomicAdd(&hs->H[i], (unsigned long long)h[i]);
+  // The last block to add its bins computes the result (no block waits).
+  // The barrier waits for this block's bin atomics; one acquire-release
+  // ticket per block orders them before the last block's reads of H.
+  __syncthreads();
+  if (threadIdx.x == 0)
+    last = __hip_atomic_fetch_add(&hs->ticket, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT) == gridDim.x - 1;
+  __syncthreads();
+  if (!last) return;
+  subset_sums(hs, N, y);
+  const unsigned all = (1u << N) - 1u;
+  if constexpr (SCORE) {
+    if ((int)threadIdx.x < M) score[threadIdx.x] = y[all] - y[all & ~(unsigned)sets.m[threadIdx.x]];
+  } else {
+    if (threadIdx.x >= 64) return;
+    const int u = (int)threadIdx.x;
+    unsigned chosen = (unsigned)forced;
+    for (int n = __popc(chosen); n < a; ++n) {
+      const unsigned free_views = all & ~chosen;
+      const bool cand = u < N && !((chosen >> u) & 1u);
+      unsigned long long g = cand ? y[free_views] - y[free_views & ~(1u << u)] : 0ull;
+      int best = cand ? u : 64;
+      // wave arg-max: the larger gain, on equal gains the lower view
+      for (int o = 32; o > 0; o >>= 1) {
+        const unsigned long long og = (unsigned long long)__shfl_xor((long long)g, o);
+        const int ob = __shfl_xor(best, o);
+        if (ob < 64 && (best == 64 || og > g || (og == g && ob < best))) {
+          g = og;
+          best = ob;
+        }
+      }
+      chosen |= 1u << best;
+    }
+    if (u == 0) write_set(chosen, N, out);
   }
 }
 
@@ -249,7 +453,6 @@ __global__ __launch_bounds__(64) void k_cov_update(const uint32_t* __restrict__ 
 // the end, and one small block adds the rows up.  No global atomics: the
 // per-candidate counters would otherwise take an atomic from every block.
 constexpr int kRedBlocks = 2048;
-constexpr int kMaxSets = 64;       // candidate sets per gc_coverage_score call
 
 // Workspace layout: per-block partial sums, candidate-major (the reducer's
 // loads are coalesced), then the selection state.
@@ -322,13 +525,6 @@ __global__ __launch_bounds__(64) void k_sel_gains(const uint32_t* __restrict__ b
   if (lane < N) st->part[lane][blockIdx.x] = mine;
 }
 
-// The views of mask in ascending order.
-__device__ __forceinline__ void write_set(unsigned long long mask, int N, int32_t* out) {
-  int j = 0;
-  for (int u = 0; u < N; ++u)
-    if ((mask >> u) & 1ull) out[j++] = u;
-}
-
 // 1024 threads: each view's gain is the sum of the blocks' partials; then
 // the unchosen view with the largest gain (ties: lower view) is chosen.  The
 // last round writes the set to out.
@@ -353,11 +549,6 @@ __global__ __launch_bounds__(1024) void k_sel_pick(SelState* st, int N, int nblk
 __global__ void k_sel_forced(unsigned long long forced, int N, int32_t* out) {
   if (threadIdx.x == 0) write_set(forced, N, out);
 }
-
-// Candidate sets as view masks.
-struct SetMasks {
-  unsigned long long m[kMaxSets];
-};
 
 // score[m] partials: 1 + staleness over the foreground tokens set m covers.
 template <bool VEC>
@@ -393,6 +584,30 @@ __global__ __launch_bounds__(1024) void k_score_final(const SelState* st, int M,
   __syncthreads();
   if ((int)threadIdx.x < M) score[threadIdx.x] = sum[threadIdx.x];
 }
+
+// The histogram path: clear H and the ticket, then the pass over the tokens
+// with the last block's rounds (select) or scores (score).
+template <bool SCORE>
+void launch_hist(const uint32_t* bits, const uint8_t* stale, int B, int N, size_t HW, HistState* hs, bool vec, int a,
+                 unsigned long long forced, int32_t* out, const SetMasks& sets, int M, unsigned long long* score,
+                 hipStream_t stream) {
+  const int wpr = (int)((HW + 31) / 32);
+  const int64_t n_words = (int64_t)B * N * wpr;
+  int64_t nblk = (n_words * 4 + kHistThreads - 1) / kHistThreads;
+  if (nblk > kHistBlocks) nblk = kHistBlocks;
+  const int64_t need = (n_words + kHistMaxWords - 1) / kHistMaxWords;
+  if (nblk < need) nblk = need;
+  hipLaunchKernelGGL(k_hist_clear, dim3((unsigned)(((1 << N) + 255) / 256)), dim3(256), 0, stream, hs, 1 << N);
+  if (vec)
+    hipLaunchKernelGGL((k_cov_hist<true, SCORE>), dim3((unsigned)nblk), dim3(kHistThreads), 0, stream, bits, stale, B,
+                       N, (int)HW, wpr, n_words, hs, a, forced, out, sets, M, score);
+  else
+    hipLaunchKernelGGL((k_cov_hist<false, SCORE>), dim3((unsigned)nblk), dim3(kHistThreads), 0, stream, bits, stale, B,
+                       N, (int)HW, wpr, n_words, hs, a, forced, out, sets, M, score);
+}
+
+// The histogram path serves N <= kHistViews (its grid stays below 2^31 blocks for any legal size).
+bool hist_path(int N) { return N <= kHistViews; }
 
 // The staleness rows start 16-byte aligned: the token kernels then move
 // each lane's 32 bytes with two 16-byte accesses.
@@ -468,21 +683,21 @@ extern "C" int gc_coverage_update(const uint32_t* pair_bits, int B, int N, int H
     return fail(GC_ERR_ALIAS, "gc_coverage_update: stale, stats and pair_bits must not overlap");
   if (!aligned16(pair_bits) || !aligned16(stats)) return fail(GC_ERR_ALIGN, "gc_coverage_update: pair_bits and stats must be 16-byte aligned");
   const int wpr = (int)((HW + 31) / 32);
-  hipLaunchKernelGGL(k_fill_u32, dim3((unsigned)((B * N * 4 + 255) / 256)), dim3(256), 0, stream, stats, B * N * 4, 0u);
-  // one-wave blocks, at most one per 2048-token item and about kRedBlocks in
-  // all: each adds its totals to its view's counters once
-  const int64_t cpr = ((int64_t)wpr + 63) / 64;
-  int64_t bpr = (kRedBlocks + (int64_t)B * N - 1) / ((int64_t)B * N);
-  if (bpr > cpr) bpr = cpr;
-  const dim3 grid((unsigned)bpr, (unsigned)(B * N));
+  // one block per (asset, view) row; each writes its row's statistics
+  const dim3 grid((unsigned)(B * N));
   if (rows_aligned(stale, HW))
-    hipLaunchKernelGGL(k_cov_update<true>, grid, dim3(64), 0, stream, pair_bits, B, N, (int)HW, wpr, mask, R, stale, stats);
+    hipLaunchKernelGGL(k_cov_update<true>, grid, dim3(kRowBlock), 0, stream, pair_bits, B, N, (int)HW, wpr, mask, R,
+                       stale, stats);
   else
-    hipLaunchKernelGGL(k_cov_update<false>, grid, dim3(64), 0, stream, pair_bits, B, N, (int)HW, wpr, mask, R, stale, stats);
+    hipLaunchKernelGGL(k_cov_update<false>, grid, dim3(kRowBlock), 0, stream, pair_bits, B, N, (int)HW, wpr, mask, R,
+                       stale, stats);
   return after_launch(stream, "gc_coverage_update");
 }
 
-extern "C" size_t gc_coverage_workspace_bytes(void) { return (sizeof(SelState) + 255) / 256 * 256; }
+extern "C" size_t gc_coverage_workspace_bytes(void) {
+  const size_t n = sizeof(SelState) > sizeof(HistState) ? sizeof(SelState) : sizeof(HistState);
+  return (n + 255) / 256 * 256;
+}
 
 extern "C" int gc_coverage_select(const uint32_t* pair_bits, const uint8_t* stale, int B, int N, int H, int W, int a,
                                   const int32_t* forced, int n_forced, int32_t* anchors_out, void* workspace,
@@ -515,8 +730,18 @@ extern "C" int gc_coverage_select(const uint32_t* pair_bits, const uint8_t* stal
   const int wpr = (int)((HW + 31) / 32);
   const int nblk = red_blocks((int64_t)B * N * ((wpr + 63) / 64));
   const bool vec = rows_aligned(stale, HW);
-  if (n_forced == a) hipLaunchKernelGGL(k_sel_forced, dim3(1), dim3(64), 0, stream, mask, N, anchors_out);
-  for (int r = n_forced; r < a; ++r) {
+  if (n_forced == a) {
+    hipLaunchKernelGGL(k_sel_forced, dim3(1), dim3(64), 0, stream, mask, N, anchors_out);
+    return after_launch(stream, "gc_coverage_select");
+  }
+  if (hist_path(N)) {   // the coverage histogram: two launches for every round
+    SetMasks none;
+    std::memset(&none, 0, sizeof(none));
+    launch_hist<false>(pair_bits, stale, B, N, HW, static_cast<HistState*>(workspace), vec, a, mask, anchors_out, none, 0,
+                       nullptr, stream);
+    return after_launch(stream, "gc_coverage_select");
+  }
+  for (int r = n_forced; r < a; ++r) {   // more views: one pass over the tokens per round
     const int first = r == n_forced;
     int32_t* out = r == a - 1 ? anchors_out : nullptr;
     if (vec)
@@ -559,6 +784,11 @@ extern "C" int gc_coverage_score(const uint32_t* pair_bits, const uint8_t* stale
   if (!aligned16(pair_bits) || !aligned16(workspace) || ((uintptr_t)scores & 7u))
     return fail(GC_ERR_ALIGN, "gc_coverage_score: pair_bits and workspace 16-byte, scores 8-byte aligned");
   const int wpr = (int)((HW + 31) / 32);
+  if (hist_path(N)) {
+    launch_hist<true>(pair_bits, stale, B, N, HW, static_cast<HistState*>(workspace), rows_aligned(stale, HW), a, 0ull,
+                      nullptr, masks, M, reinterpret_cast<unsigned long long*>(scores), stream);
+    return after_launch(stream, "gc_coverage_score");
+  }
   SelState* st = static_cast<SelState*>(workspace);
   const int nblk = red_blocks((int64_t)B * N * ((wpr + 63) / 64));
   if (rows_aligned(stale, HW))

@@ -79,7 +79,7 @@ class GeoCacheRunner:
             self._ws = (torch.empty(gc_coverage_workspace_bytes(), dtype=torch.uint8, device=pos.device)
                         if self.tracking else None)
         self.stale: Optional[torch.Tensor] = None
-        self.stats_host = None                        # per-view staleness statistics after the last step
+        self.stats_host = None                        # per-view staleness statistics after the last step (refresh rule)
         self.gap: List[int] = [0] * self.N            # cached steps since each view was last an anchor
         self.last_full = False
         self.k = 0
@@ -154,7 +154,8 @@ class GeoCacheRunner:
         self.gap = gc_schedule_advance_gaps(self.gap, views, full)
         if self.tracking:
             stats = gc_coverage_update(self.pairs, self.stale, views, self.refresh_R, stream=self.stream)
-            self.stats_host = stats.cpu()
+            # the host reads the statistics back only for the refresh rule
+            self.stats_host = stats.cpu() if self.refresh_tau is not None else None
 
     def step(self, predict: Predict) -> List[int]:
         """Run sampler step k; returns the views the denoiser was asked for.

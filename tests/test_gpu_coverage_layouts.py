@@ -7,7 +7,9 @@ distinguish:
   * ragged rows (1961 tokens: bytewise accesses, a partial last word);
   * a staleness tensor that starts one byte past an aligned address
     (bytewise accesses although the rows are whole words);
-  * more 2048-token items than reduction blocks (blocks stride over items).
+  * more 2048-token items than reduction blocks (blocks stride over items);
+  * 12 views (the coverage-histogram path at its largest) and 14 views (the
+    per-round passes that serve more views), aligned and ragged.
 Visibility bits are drawn at random rather than from geometry, with random
 garbage in each row's padding bits, which every call ignores, and in the
 rows (u, b, u), which the view itself covers anyway.  Staleness values cover
@@ -59,6 +61,9 @@ CASES = {
     "ragged_rows": (3, 2, 6, 37, 53, 0),
     "unaligned_pointer": (4, 2, 5, 32, 32, 1),
     "more_items_than_blocks": (5, 1, 5, 1024, 1024, 0),
+    "twelve_views": (6, 2, 12, 24, 40, 0),        # the largest view count of the histogram path
+    "fourteen_views": (7, 2, 14, 16, 24, 0),      # beyond it: one pass over the tokens per round
+    "fourteen_views_ragged": (8, 1, 14, 13, 29, 3),
 }
 
 
