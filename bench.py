@@ -603,11 +603,11 @@ def coverage_rows(gc, w, pos, cams, bbox, full, R=2):
     """One whole trajectory of the schedule alone (no latents) per anchor
     policy: per-step staleness of the foreground tokens after the step
     (mean, fraction stale for >= R steps, max) and the policy's cost per
-    cached step two ways: the wall time of the trajectory's step (selection
-    or scoring, the staleness update and the host read-backs of the anchors
-    and counters), and the device time of the same launches captured in a
-    HIP graph and replayed back to back (what they cost the GPU when the host
-    is not in the way)."""
+    cached step two ways: the wall time of the trajectory's step (the
+    staleness update fused with the next step's selection or scoring, and
+    the host read-backs of the anchors and counters), and the device time of
+    the same launches captured in a HIP graph and replayed back to back (what
+    they cost the GPU when the host is not in the way)."""
     import numpy as np
     import torch
     N, a = w.N, w.a
@@ -634,7 +634,7 @@ def coverage_rows(gc, w, pos, cams, bbox, full, R=2):
     max_gap = -(-N // a)
     for policy in ("rotate", "rotation_coverage", "coverage"):
         stale = gc.gc_coverage_init(pos)
-        gap, c, rec, cost = [0] * N, 0, [], []
+        gap, c, rec, cost, nxt = [0] * N, 0, [], [], None
         for k in range(w.S):
             torch.cuda.synchronize()
             t0 = time.perf_counter()
@@ -643,17 +643,24 @@ def coverage_rows(gc, w, pos, cams, bbox, full, R=2):
             elif policy == "rotate":
                 A = gc.gc_schedule_anchors(N, a, c)
             elif policy == "rotation_coverage":
-                sc = gc.gc_coverage_score(pairs, stale, rot_sets, workspace=ws).cpu().tolist()
+                sc = nxt.cpu().tolist()   # scored by the last step's fused update
                 A = rot_sets[sc.index(max(sc))]
             else:
-                due = gc.gc_schedule_forced_views(gap, a, max_gap)
-                A = gc.gc_coverage_select(pairs, stale, a, forced=due, workspace=ws).cpu().tolist()
-            st = gc.gc_coverage_update(pairs, stale, A, R)
+                A = nxt.cpu().tolist()    # chosen by the last step's fused update
+            gap = gc.gc_schedule_advance_gaps(gap, A, bool(full[k] or k == 0))
+            # the update, fused with the next cached step's choice (unused if that step is full)
+            if policy == "rotation_coverage":
+                st, nxt = gc.gc_coverage_update_score(pairs, stale, A, R, rot_sets, workspace=ws)
+            elif policy == "coverage":
+                st, nxt = gc.gc_coverage_update_select(pairs, stale, A, R, a,
+                                                       forced=gc.gc_schedule_forced_views(gap, a, max_gap),
+                                                       workspace=ws)
+            else:
+                st = gc.gc_coverage_update(pairs, stale, A, R)
             st = st.cpu().numpy().astype(np.int64)
             if not (full[k] or k == 0):
                 cost.append(time.perf_counter() - t0)
                 c += 1
-            gap = gc.gc_schedule_advance_gaps(gap, A, bool(full[k] or k == 0))
             fg = st[..., 0].sum()
             rec.append((st[..., 2].sum() / fg, st[..., 1].sum() / fg, st[..., 3].max()))
         r = np.array(rec, np.float64)
@@ -667,10 +674,13 @@ def coverage_rows(gc, w, pos, cams, bbox, full, R=2):
 
         def policy_step():
             if policy == "rotation_coverage":
-                gc.gc_coverage_score(pairs, stale, rot_sets, out=score_buf, workspace=ws, stream=sgr)
+                gc.gc_coverage_update_score(pairs, stale, A0, R, rot_sets, stats=stats_buf, out=score_buf,
+                                            workspace=ws, stream=sgr)
             elif policy == "coverage":
-                gc.gc_coverage_select(pairs, stale, a, out=sel_buf, workspace=ws, stream=sgr)
-            gc.gc_coverage_update(pairs, stale, A0, R, stats=stats_buf, stream=sgr)
+                gc.gc_coverage_update_select(pairs, stale, A0, R, a, stats=stats_buf, out=sel_buf, workspace=ws,
+                                             stream=sgr)
+            else:
+                gc.gc_coverage_update(pairs, stale, A0, R, stats=stats_buf, stream=sgr)
 
         reps = 20
         graph = torch.cuda.CUDAGraph()

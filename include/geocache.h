@@ -506,22 +506,32 @@ int gc_transport_unipc_geom(const void* x0_prev, const void* x0_anchor_new, cons
  * gc_coverage_select: the anchor set of the next cached step, written to
  *   anchors_out (device int32 [a], ascending); forced: host [n_forced] views
  *   that must be in it.  a <= GC_MAX_ANCHORS.  workspace: caller-owned device
- *   memory of gc_coverage_workspace_bytes(), 16-byte aligned; it holds
- *   the coverage histogram (or per-block partial gains), so concurrent calls
- *   need separate workspaces.  With N <= 12 it enqueues three launches
- *   whatever a is: the histogram over the tokens' cover masks (own view and
- *   the views that see them) of the weights 1 + staleness, then one block
- *   that takes its subset sums Y and runs every round, the gain of u given
- *   the chosen set S being Y[all \ S] - Y[all \ (S + u)]; with more views,
+ *   memory of gc_coverage_workspace_bytes(), 16-byte aligned, any contents;
+ *   it holds the coverage histogram (or per-block partial gains), so
+ *   concurrent calls need separate workspaces.  With N <= 12 it enqueues two
+ *   launches whatever a is: one that clears the histogram, then the pass over
+ *   the tokens that builds it -- the weights 1 + staleness summed per cover
+ *   mask (the token's own view and the views that see it) -- whose last block
+ *   takes its subset sums Y and runs every round, the gain of u given the
+ *   chosen set S being Y[all \ S] - Y[all \ (S + u)]; with more views,
  *   2 (a - n_forced) launches.  One launch when every view is forced.  Never
  *   synchronises.
  * gc_coverage_score: scores (device uint64 [M], overwritten) = the weighted
  *   coverage, sum of 1 + staleness over the foreground tokens it covers, of
  *   each candidate set sets (host int32 [M][a]); M <= 64.  workspace as for
- *   gc_coverage_select (per-block partial sums; no atomics).  Choosing the
- *   rotation's set with the largest score keeps the rotation's evenly spread
- *   anchors while following where the stale tokens are.  With N <= 12 a set's
- *   score is Y[all] - Y[all \ S] from the same histogram (three launches).
+ *   gc_coverage_select.  Choosing the rotation's set with the largest score
+ *   keeps the rotation's evenly spread anchors while following where the
+ *   stale tokens are.  With N <= 12 a set's score is Y[all] - Y[all \ S]
+ *   from the same histogram (two launches).
+ * gc_coverage_update_select: gc_coverage_update with anchors, a, R, stale,
+ *   stats, then gc_coverage_select of a_next views (forced, n_forced,
+ *   anchors_out, workspace) on the updated staleness -- the end of one step
+ *   and the choice for the next in one pass over the tokens when N <= 12
+ *   (two launches; the statistics are summed with integer atomics, so the
+ *   result is the same as the two calls').  With more views, the two calls'
+ *   launches.  stats must not overlap the workspace or anchors_out.
+ * gc_coverage_update_score: gc_coverage_update, then gc_coverage_score of
+ *   the M sets of a_set views on the updated staleness, fused as above.
  * gc_schedule_refresh_due: host; stats as written by gc_coverage_update and
  *   copied to the host; *due = 1 when a full step is due.
  */
@@ -537,6 +547,12 @@ int gc_coverage_select(const uint32_t* pair_bits, const uint8_t* stale, int B, i
                        hipStream_t stream);
 int gc_coverage_score(const uint32_t* pair_bits, const uint8_t* stale, int B, int N, int H, int W, const int32_t* sets,
                       int M, int a, uint64_t* scores, void* workspace, size_t ws_bytes, hipStream_t stream);
+int gc_coverage_update_select(const uint32_t* pair_bits, int B, int N, int H, int W, const int32_t* anchors, int a,
+                              int R, uint8_t* stale, uint32_t* stats, int a_next, const int32_t* forced, int n_forced,
+                              int32_t* anchors_out, void* workspace, size_t ws_bytes, hipStream_t stream);
+int gc_coverage_update_score(const uint32_t* pair_bits, int B, int N, int H, int W, const int32_t* anchors, int a,
+                             int R, uint8_t* stale, uint32_t* stats, const int32_t* sets, int M, int a_set,
+                             uint64_t* scores, void* workspace, size_t ws_bytes, hipStream_t stream);
 int gc_schedule_refresh_due(const uint32_t* stats, int B, int N, double tau, int* due);
 
 /*

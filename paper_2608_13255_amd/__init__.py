@@ -124,6 +124,10 @@ def lib() -> ctypes.CDLL:
             "gc_coverage_select": ([_vp, _vp, _i, _i, _i, _i, _i, _i32p, _i, _vp, _vp, ctypes.c_size_t, _vp], _i),
             "gc_schedule_refresh_due": ([_vp, _i, _i, ctypes.c_double, ctypes.POINTER(ctypes.c_int)], _i),
             "gc_coverage_score": ([_vp, _vp, _i, _i, _i, _i, _i32p, _i, _i, _vp, _vp, ctypes.c_size_t, _vp], _i),
+            "gc_coverage_update_select": ([_vp, _i, _i, _i, _i, _i32p, _i, _i, _vp, _vp, _i, _i32p, _i, _vp, _vp,
+                                           ctypes.c_size_t, _vp], _i),
+            "gc_coverage_update_score": ([_vp, _i, _i, _i, _i, _i32p, _i, _i, _vp, _vp, _i32p, _i, _i, _vp, _vp,
+                                          ctypes.c_size_t, _vp], _i),
             "gc_schedule_forced_views": ([_i32p, _i, _i, _i, _i32p, ctypes.POINTER(ctypes.c_int)], _i),
             "gc_schedule_advance_gaps": ([_i32p, _i, _i32p, _i, _i], _i),
             "gc_schedule_anchors": ([_i, _i, _i64, _i32p], _i),
@@ -793,6 +797,68 @@ def gc_coverage_score(pair_bits: torch.Tensor, stale: torch.Tensor, sets: Sequen
            "gc_coverage_score")
     _keep(stream, (out, workspace))
     return out
+
+
+def _stats_out(stale: torch.Tensor, stats: Optional[torch.Tensor]) -> torch.Tensor:
+    B, N = stale.shape[:2]
+    if stats is None:
+        stats = torch.empty((B, N, 4), dtype=torch.int32, device=stale.device)
+    if tuple(stats.shape) != (B, N, 4) or stats.element_size() != 4:
+        raise ValueError(f"stats must be a 32-bit [{B}, {N}, 4] tensor")
+    return stats
+
+
+def gc_coverage_update_select(pair_bits: torch.Tensor, stale: torch.Tensor, anchors: Sequence[int], R: int,
+                              a_next: int, forced: Sequence[int] = (), stats: torch.Tensor = None,
+                              out: torch.Tensor = None, workspace: torch.Tensor = None, stream=None):
+    """gc_coverage_update with `anchors`, then gc_coverage_select of `a_next`
+    views on the updated staleness, in one pass over the tokens; returns
+    (stats int32 [B, N, 4], selection device int32 [a_next])."""
+    if stale.dtype != torch.uint8 or stale.dim() != 4:
+        raise ValueError("stale must be uint8 [B, N, H, W]")
+    B, N, H, W = stale.shape
+    arr = (ctypes.c_int32 * len(anchors))(*anchors)
+    stats = _stats_out(stale, stats)
+    if out is None:
+        out = torch.empty(a_next, dtype=torch.int32, device=stale.device)
+    if workspace is None:
+        workspace = torch.empty(gc_coverage_workspace_bytes(), dtype=torch.uint8, device=stale.device)
+    farr = (ctypes.c_int32 * max(len(forced), 1))(*forced)
+    _check(lib().gc_coverage_update_select(_dev(pair_bits, "pair_bits"), B, N, H, W, arr, len(anchors), R,
+                                           _dev(stale, "stale"), _dev(stats, "stats"), a_next, farr, len(forced),
+                                           _dev(out, "anchors_out"), _dev(workspace, "workspace"),
+                                           workspace.numel() * workspace.element_size(), _stream(stream)),
+           "gc_coverage_update_select")
+    _keep(stream, (stats, out, workspace))
+    return stats, out
+
+
+def gc_coverage_update_score(pair_bits: torch.Tensor, stale: torch.Tensor, anchors: Sequence[int], R: int,
+                             sets: Sequence[Sequence[int]], stats: torch.Tensor = None, out: torch.Tensor = None,
+                             workspace: torch.Tensor = None, stream=None):
+    """gc_coverage_update with `anchors`, then gc_coverage_score of `sets` on
+    the updated staleness, in one pass over the tokens; returns (stats int32
+    [B, N, 4], scores device int64 [M])."""
+    if stale.dtype != torch.uint8 or stale.dim() != 4:
+        raise ValueError("stale must be uint8 [B, N, H, W]")
+    B, N, H, W = stale.shape
+    arr = (ctypes.c_int32 * len(anchors))(*anchors)
+    M, a_set = len(sets), len(sets[0])
+    if any(len(S) != a_set for S in sets):
+        raise ValueError("candidate sets must have the same size")
+    flat = (ctypes.c_int32 * (M * a_set))(*[int(u) for S in sets for u in S])
+    stats = _stats_out(stale, stats)
+    if out is None:
+        out = torch.empty(M, dtype=torch.int64, device=stale.device)
+    if workspace is None:
+        workspace = torch.empty(gc_coverage_workspace_bytes(), dtype=torch.uint8, device=stale.device)
+    _check(lib().gc_coverage_update_score(_dev(pair_bits, "pair_bits"), B, N, H, W, arr, len(anchors), R,
+                                          _dev(stale, "stale"), _dev(stats, "stats"), flat, M, a_set,
+                                          _dev(out, "scores"), _dev(workspace, "workspace"),
+                                          workspace.numel() * workspace.element_size(), _stream(stream)),
+           "gc_coverage_update_score")
+    _keep(stream, (stats, out, workspace))
+    return stats, out
 
 
 def gc_schedule_refresh_due(stats_host, tau: float) -> bool:

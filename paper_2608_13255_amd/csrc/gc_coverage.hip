@@ -272,9 +272,11 @@ struct HistState {
   unsigned int ticket;                            // blocks of the token pass that have added their bins
 };
 
-__global__ void k_hist_clear(HistState* __restrict__ hs, int nb) {
+// Clears H, the ticket and (the fused update) the statistics.
+__global__ void k_hist_clear(HistState* __restrict__ hs, int nb, uint32_t* __restrict__ stats, int n_stats) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i < nb) hs->H[i] = 0ull;
+  if (i < n_stats) stats[i] = 0u;
   if (i == 0) hs->ticket = 0u;
 }
 
@@ -301,46 +303,55 @@ __device__ __forceinline__ void load_8_bytes(const uint8_t* __restrict__ row, in
   }
 }
 
-// Y = the subset sums of H (read with agent-scope atomic loads, after the
-// blocks' atomics), left in y (LDS), by 1024 threads holding four
-// consecutive masks each: the passes over bits 0 and 1 stay in registers,
-// bits 2..7 pair lanes of a wave, bits 8..11 pair waves through LDS.
-__device__ __forceinline__ void subset_sums(HistState* __restrict__ hs, int N, unsigned long long* y) {
+// Y = the subset sums of H, left in y (LDS, indexed by mask).  The calling
+// block has acquired the other blocks' additions to H (the ticket), so plain
+// loads see them.  256 threads each hold 16 masks that differ in four bits
+// and add along those bits in registers: bits 0-3 (masks 16t .. 16t + 15),
+// then, after a transpose through y, bits 4-7, then bits 8-11; the passes
+// over bits at or above N are skipped (their masks are never read).
+__device__ __forceinline__ void subset_sums(const HistState* __restrict__ hs, int N, unsigned long long* y) {
   const int nb = 1 << N;
   const int t = (int)threadIdx.x;
-  unsigned long long r[4];
+  unsigned long long r[16];
+  auto sum4 = [&r]() {
 #pragma unroll
-  for (int k = 0; k < 4; ++k)
-    r[k] = 4 * t + k < nb ? __hip_atomic_load(&hs->H[4 * t + k], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0ull;
-  r[1] += r[0];
-  r[3] += r[2];
-  if (N > 1) {
-    r[2] += r[0];
-    r[3] += r[1];
-  }
-  const int lane = __lane_id();
-  for (int q = 2; q < N && q < 8; ++q) {   // uniform
-    const int d = 1 << (q - 2);
+    for (int bit = 0; bit < 4; ++bit)
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      const unsigned long long o = (unsigned long long)__shfl_xor((long long)r[k], d);
-      if (lane & d) r[k] += o;
+      for (int j = 0; j < 16; ++j)
+        if ((j >> bit) & 1) r[j] += r[j ^ (1 << bit)];
+  };
+  if (t < kHistBins / 16) {
+    const int m0 = 16 * t;
+    if (m0 < nb) {   // nb >= 16 whenever N >= 4; a smaller nb fills one partial row
+      const ulonglong2* src = reinterpret_cast<const ulonglong2*>(hs->H + m0);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const ulonglong2 q = 2 * j < nb - m0 ? src[j] : make_ulonglong2(0ull, 0ull);
+        r[2 * j] = q.x;
+        r[2 * j + 1] = 2 * j + 1 < nb - m0 ? q.y : 0ull;
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < 16; ++j) r[j] = 0ull;
     }
+    sum4();
+#pragma unroll
+    for (int j = 0; j < 16; ++j) y[m0 + j] = r[j];
   }
-  for (int q = 8; q < N; ++q) {   // uniform
-    const int d = 1 << (q - 2);   // partner thread t ^ d, a whole number of waves away
-#pragma unroll
-    for (int k = 0; k < 4; ++k) y[4 * t + k] = r[k];
-    __syncthreads();
-    if (t & d) {
-#pragma unroll
-      for (int k = 0; k < 4; ++k) r[k] += y[4 * (t ^ d) + k];
-    }
-    __syncthreads();
-  }
-#pragma unroll
-  for (int k = 0; k < 4; ++k) y[4 * t + k] = r[k];
   __syncthreads();
+  for (int ph = 1; ph < 3 && 4 * ph < N; ++ph) {   // uniform
+    const int sh = 4 * ph;                          // this pass's four bits: sh .. sh + 3
+    const int low = t & ((1 << sh) - 1);            // bits below sh
+    const int high = (t >> sh) << (sh + 4);         // bits above sh + 3
+    if (t < kHistBins / 16) {
+#pragma unroll
+      for (int j = 0; j < 16; ++j) r[j] = y[high | (j << sh) | low];
+      sum4();
+#pragma unroll
+      for (int j = 0; j < 16; ++j) y[high | (j << sh) | low] = r[j];
+    }
+    __syncthreads();
+  }
 }
 
 // The views of mask in ascending order.
@@ -361,33 +372,119 @@ struct SetMasks {
 // the last block: SCORE == false, forced views first and a - n_forced greedy
 // rounds (largest gain, ties to the lower view; wave 0, lane u evaluating
 // candidate u), the set to out; SCORE == true, score[m] for the M sets.
-template <bool VEC, bool SCORE>
+// Staleness bytes of a lane's 8 tokens written back (VEC as for load_8_bytes).
+template <bool VEC>
+__device__ __forceinline__ void store_8_bytes(uint8_t* __restrict__ row, int HW, int t0, const uint32_t (&d)[2]) {
+  if constexpr (VEC) {
+    if (t0 < HW) *reinterpret_cast<uint2*>(row + t0) = make_uint2(d[0], d[1]);
+  } else {
+#pragma unroll
+    for (int k = 0; k < 2; ++k)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int t = t0 + 4 * k + j;
+        if (t < HW) row[t] = (uint8_t)(d[k] >> (8 * j));
+      }
+  }
+}
+
+// The per-step staleness rule on four tokens' bytes s (token j in byte j):
+// background (255) stays; a token whose byte of fresh_bytes is 0xff becomes
+// 0; any other foreground token adds 1, saturating at 254.
+__device__ __forceinline__ uint32_t stale_step(uint32_t s, uint32_t fresh_bytes) {
+  const uint32_t fgm = (bytes_nonzero(~s) >> 7) * 0xffu;          // 0xff per foreground byte
+  const uint32_t inc = bytes_nonzero(~(s | 0x01010101u)) >> 7;     // s < 254
+  return (s + inc) & ~(fresh_bytes & fgm);
+}
+
+// The pass over the tokens (lane group of 4 per pair word, 8 tokens per
+// lane; each wave takes 16 consecutive words per round, blocks stride over
+// the words of every (asset, view) row), then in the last block: SCORE ==
+// false, forced views first and a - n_forced greedy rounds, the set to out;
+// SCORE == true, score[m] for the M sets.  UPDATE: the pass first applies
+// one step of the staleness rule with the anchor set anchor_mask to the
+// lane's tokens (stored back) and adds their statistics to stats (cleared
+// by k_hist_clear) -- the per-row sums of one wave with one atomic each --
+// so the histogram, and the selection or scores, are those of the updated
+// staleness.
+template <bool VEC, bool SCORE, bool UPDATE>
 __global__ __launch_bounds__(kHistThreads) void k_cov_hist(const uint32_t* __restrict__ bits,
-                                                           const uint8_t* __restrict__ stale, int B, int N, int HW,
+                                                           uint8_t* __restrict__ stale, int B, int N, int HW,
                                                            int wpr, int64_t n_words, HistState* __restrict__ hs, int a,
                                                            unsigned long long forced, int32_t* __restrict__ out,
-                                                           SetMasks sets, int M, unsigned long long* __restrict__ score) {
+                                                           SetMasks sets, int M, unsigned long long* __restrict__ score,
+                                                           unsigned long long anchor_mask, int R,
+                                                           uint32_t* __restrict__ stats) {
   __shared__ unsigned long long y[kHistBins];     // the last block's subset sums
   __shared__ uint32_t h[kHistBins];               // this block's histogram
   __shared__ int last;
   const int nb = 1 << N;
   for (int i = (int)threadIdx.x; i < nb; i += kHistThreads) h[i] = 0u;
   __syncthreads();
-  const int sub = (int)threadIdx.x & 3;           // which 8 tokens of the word
-  for (int64_t wg = ((int64_t)blockIdx.x * kHistThreads + threadIdx.x) >> 2; wg < n_words;
-       wg += (int64_t)gridDim.x * (kHistThreads / 4)) {
-    const int bv = (int)(wg / wpr);
-    const int wi = (int)(wg - (int64_t)bv * wpr);
+  const int lane = __lane_id();
+  const int sub = lane & 3;                       // which 8 tokens of the word
+  // the whole wave runs every round (a lane past the end only contributes
+  // nothing), so the statistics' wave reductions see every lane
+  for (int64_t base = ((int64_t)blockIdx.x * kHistThreads + (threadIdx.x & ~63)) >> 2; base < n_words;
+       base += (int64_t)gridDim.x * (kHistThreads / 4)) {
+    const int64_t wg = base + (lane >> 2);
+    const bool active = wg < n_words;
+    const int bv = active ? (int)(wg / wpr) : 0;
+    const int wi = active ? (int)(wg - (int64_t)bv * wpr) : 0;
     const int b = bv / N, v = bv - b * N;
-    uint32_t w[2];   // weights 1 + staleness of the lane's 8 tokens (0: background and past the row)
-    load_8_bytes<VEC>(stale + (int64_t)bv * HW, HW, wi * 32 + 8 * sub, w);
-    w[0] = bytes_plus_one(w[0]);
-    w[1] = bytes_plus_one(w[1]);
-    if (!(w[0] | w[1])) continue;
-    uint32_t pb[kHistViews];   // the other views' pair bits of these 8 tokens
+    uint32_t d[2] = {~0u, ~0u};   // staleness bytes of the lane's 8 tokens (background past the row)
+    if (active) load_8_bytes<VEC>(stale + (int64_t)bv * HW, HW, wi * 32 + 8 * sub, d);
+    uint32_t pb[kHistViews];      // the other views' pair bits of these 8 tokens
 #pragma unroll
     for (int u = 0; u < kHistViews; ++u)
-      pb[u] = (u < N && u != v) ? (pair_word(bits, B, N, wpr, u, b, v, wi) >> (8 * sub)) & 0xffu : 0u;
+      pb[u] = (active && u < N && u != v) ? (pair_word(bits, B, N, wpr, u, b, v, wi) >> (8 * sub)) & 0xffu : 0u;
+    if constexpr (UPDATE) {
+      uint32_t fresh = (anchor_mask >> v) & 1ull ? 0xffu : 0u;
+#pragma unroll
+      for (int u = 0; u < kHistViews; ++u) fresh |= (anchor_mask >> u) & 1ull ? pb[u] : 0u;
+      fresh &= (valid_bits(HW, wi) >> (8 * sub)) & 0xffu;
+      uint32_t c_fg = 0u, c_ge = 0u, c_sum = 0u, c_max = 0u;
+#pragma unroll
+      for (int k = 0; k < 2; ++k) {
+        const uint32_t s0 = d[k];
+        const uint32_t n = stale_step(s0, nibble_bytes(fresh, k) * 0xffu);
+        d[k] = n;
+        const uint32_t fgm = (bytes_nonzero(~s0) >> 7) * 0xffu;
+        const uint32_t nf = n & fgm;                               // background reads 0
+        c_fg += (uint32_t)__popc(bytes_nonzero(~s0));
+        c_sum = __builtin_amdgcn_udot4(nf, 0x01010101u, c_sum, false);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const uint32_t x = (nf >> (8 * j)) & 0xffu;
+          c_ge += x >= (uint32_t)R ? 1u : 0u;
+          c_max = max(c_max, x);
+        }
+      }
+      if (active) store_8_bytes<VEC>(stale + (int64_t)bv * HW, HW, wi * 32 + 8 * sub, d);
+      // per-row statistics: one atomic per counter for a wave within one row
+      const int bv0 = __builtin_amdgcn_readfirstlane(bv);   // lane 0 is always active
+      if (__ballot(active && bv != bv0) == 0ull) {
+        c_fg = wave_add(c_fg);
+        c_ge = wave_add(c_ge);
+        c_sum = wave_add(c_sum);
+        c_max = wave_max(c_max);
+        if (lane == 0) {
+          uint32_t* st = stats + (int64_t)bv0 * 4;
+          if (c_fg) atomicAdd(st + 0, c_fg);
+          if (c_ge) atomicAdd(st + 1, c_ge);
+          if (c_sum) atomicAdd(st + 2, c_sum);
+          if (c_max) atomicMax(st + 3, c_max);
+        }
+      } else if (active) {
+        uint32_t* st = stats + (int64_t)bv * 4;
+        if (c_fg) atomicAdd(st + 0, c_fg);
+        if (c_ge) atomicAdd(st + 1, c_ge);
+        if (c_sum) atomicAdd(st + 2, c_sum);
+        if (c_max) atomicMax(st + 3, c_max);
+      }
+    }
+    const uint32_t w[2] = {bytes_plus_one(d[0]), bytes_plus_one(d[1])};   // weights 1 + staleness, 0: background
+    if (!(w[0] | w[1])) continue;
     // neighbouring tokens mostly share a mask: runs of one mask go to LDS as one add
     uint32_t run_m = 0u, run_w = 0u;
 #pragma unroll
@@ -424,26 +521,31 @@ __global__ __launch_bounds__(kHistThreads) void k_cov_hist(const uint32_t* __res
   if constexpr (SCORE) {
     if ((int)threadIdx.x < M) score[threadIdx.x] = y[all] - y[all & ~(unsigned)sets.m[threadIdx.x]];
   } else {
-    if (threadIdx.x >= 64) return;
-    const int u = (int)threadIdx.x;
+    // one thread runs the rounds; per round the N + 1 lookups are issued
+    // together (a view outside [0, N) or already chosen looks up its own
+    // mask and is no candidate); the larger gain wins, on equal gains the
+    // lower view
+    if (threadIdx.x != 0) return;
     unsigned chosen = (unsigned)forced;
     for (int n = __popc(chosen); n < a; ++n) {
       const unsigned free_views = all & ~chosen;
-      const bool cand = u < N && !((chosen >> u) & 1u);
-      unsigned long long g = cand ? y[free_views] - y[free_views & ~(1u << u)] : 0ull;
-      int best = cand ? u : 64;
-      // wave arg-max: the larger gain, on equal gains the lower view
-      for (int o = 32; o > 0; o >>= 1) {
-        const unsigned long long og = (unsigned long long)__shfl_xor((long long)g, o);
-        const int ob = __shfl_xor(best, o);
-        if (ob < 64 && (best == 64 || og > g || (og == g && ob < best))) {
-          g = og;
-          best = ob;
-        }
+      unsigned long long rest[kHistViews];
+#pragma unroll
+      for (int u = 0; u < kHistViews; ++u) rest[u] = y[free_views & ~(1u << u)];
+      const unsigned long long base = y[free_views];
+      unsigned long long best_g = 0ull;
+      int best = kHistViews;
+#pragma unroll
+      for (int u = 0; u < kHistViews; ++u) {
+        const bool cand = u < N && !((chosen >> u) & 1u);
+        const unsigned long long g = base - rest[u];
+        const bool take = cand && (best == kHistViews || g > best_g);
+        best_g = take ? g : best_g;
+        best = take ? u : best;
       }
       chosen |= 1u << best;
     }
-    if (u == 0) write_set(chosen, N, out);
+    write_set(chosen, N, out);
   }
 }
 
@@ -587,23 +689,29 @@ __global__ __launch_bounds__(1024) void k_score_final(const SelState* st, int M,
 
 // The histogram path: clear H and the ticket, then the pass over the tokens
 // with the last block's rounds (select) or scores (score).
-template <bool SCORE>
-void launch_hist(const uint32_t* bits, const uint8_t* stale, int B, int N, size_t HW, HistState* hs, bool vec, int a,
+// The histogram path: clear H and the ticket (and the statistics), then the
+// pass over the tokens with the last block's rounds (select) or scores
+// (score); UPDATE applies the staleness step first (anchor_mask, R, stats).
+template <bool SCORE, bool UPDATE>
+void launch_hist(const uint32_t* bits, uint8_t* stale, int B, int N, size_t HW, HistState* hs, bool vec, int a,
                  unsigned long long forced, int32_t* out, const SetMasks& sets, int M, unsigned long long* score,
-                 hipStream_t stream) {
+                 unsigned long long anchor_mask, int R, uint32_t* stats, hipStream_t stream) {
   const int wpr = (int)((HW + 31) / 32);
   const int64_t n_words = (int64_t)B * N * wpr;
   int64_t nblk = (n_words * 4 + kHistThreads - 1) / kHistThreads;
   if (nblk > kHistBlocks) nblk = kHistBlocks;
   const int64_t need = (n_words + kHistMaxWords - 1) / kHistMaxWords;
   if (nblk < need) nblk = need;
-  hipLaunchKernelGGL(k_hist_clear, dim3((unsigned)(((1 << N) + 255) / 256)), dim3(256), 0, stream, hs, 1 << N);
+  const int n_stats = UPDATE ? B * N * 4 : 0;   // B * N <= 65535 (check_grid)
+  const int n_clear = (1 << N) > n_stats ? (1 << N) : n_stats;
+  hipLaunchKernelGGL(k_hist_clear, dim3((unsigned)((n_clear + 255) / 256)), dim3(256), 0, stream, hs, 1 << N, stats,
+                     n_stats);
   if (vec)
-    hipLaunchKernelGGL((k_cov_hist<true, SCORE>), dim3((unsigned)nblk), dim3(kHistThreads), 0, stream, bits, stale, B,
-                       N, (int)HW, wpr, n_words, hs, a, forced, out, sets, M, score);
+    hipLaunchKernelGGL((k_cov_hist<true, SCORE, UPDATE>), dim3((unsigned)nblk), dim3(kHistThreads), 0, stream, bits,
+                       stale, B, N, (int)HW, wpr, n_words, hs, a, forced, out, sets, M, score, anchor_mask, R, stats);
   else
-    hipLaunchKernelGGL((k_cov_hist<false, SCORE>), dim3((unsigned)nblk), dim3(kHistThreads), 0, stream, bits, stale, B,
-                       N, (int)HW, wpr, n_words, hs, a, forced, out, sets, M, score);
+    hipLaunchKernelGGL((k_cov_hist<false, SCORE, UPDATE>), dim3((unsigned)nblk), dim3(kHistThreads), 0, stream, bits,
+                       stale, B, N, (int)HW, wpr, n_words, hs, a, forced, out, sets, M, score, anchor_mask, R, stats);
 }
 
 // The histogram path serves N <= kHistViews (its grid stays below 2^31 blocks for any legal size).
@@ -662,28 +770,97 @@ extern "C" int gc_coverage_init(const float* pos, int B, int N, int H, int W, ui
   return after_launch(stream, "gc_coverage_init");
 }
 
-extern "C" int gc_coverage_update(const uint32_t* pair_bits, int B, int N, int H, int W, const int32_t* anchors, int a,
-                                  int R, uint8_t* stale, uint32_t* stats, hipStream_t stream) {
-  clear_error();
-  if (!pair_bits || !anchors || !stale || !stats) return fail(GC_ERR_ARG, "gc_coverage_update: null pointer");
-  int rc = check_grid(B, N, H, W, "gc_coverage_update");
+namespace gc {
+namespace {
+
+// Argument checks of one staleness step; mask: the anchor set's views.
+int check_update(const uint32_t* pair_bits, int B, int N, int H, int W, const int32_t* anchors, int a, int R,
+                 const uint8_t* stale, const uint32_t* stats, const char* who, unsigned long long* mask) {
+  if (!pair_bits || !anchors || !stale || !stats) return fail(GC_ERR_ARG, "%s: null pointer", who);
+  int rc = check_grid(B, N, H, W, who);
   if (rc) return rc;
-  if (a < 1 || a > N) return fail(GC_ERR_ARG, "gc_coverage_update: a=%d outside [1, N=%d]", a, N);
-  if (R < 1) return fail(GC_ERR_ARG, "gc_coverage_update: R=%d must be >= 1", R);
-  unsigned long long mask = 0;
+  if (a < 1 || a > N) return fail(GC_ERR_ARG, "%s: a=%d outside [1, N=%d]", who, a, N);
+  if (R < 1) return fail(GC_ERR_ARG, "%s: R=%d must be >= 1", who, R);
+  *mask = 0;
   for (int s = 0; s < a; ++s) {
-    if (anchors[s] < 0 || anchors[s] >= N) return fail(GC_ERR_ARG, "gc_coverage_update: anchor %d outside [0, %d)", anchors[s], N);
-    if ((mask >> anchors[s]) & 1ull) return fail(GC_ERR_ARG, "gc_coverage_update: anchor %d listed twice", anchors[s]);
-    mask |= 1ull << anchors[s];
+    if (anchors[s] < 0 || anchors[s] >= N) return fail(GC_ERR_ARG, "%s: anchor %d outside [0, %d)", who, anchors[s], N);
+    if ((*mask >> anchors[s]) & 1ull) return fail(GC_ERR_ARG, "%s: anchor %d listed twice", who, anchors[s]);
+    *mask |= 1ull << anchors[s];
   }
   const size_t HW = (size_t)H * W;
   const size_t n_tok = (size_t)B * N * HW, nb = (size_t)gc_coverage_pair_words(B, N, H, W) * 4;
   if (overlaps(stats, (size_t)B * N * 16, stale, n_tok) || overlaps(stats, (size_t)B * N * 16, pair_bits, nb) ||
       overlaps(stale, n_tok, pair_bits, nb))
-    return fail(GC_ERR_ALIAS, "gc_coverage_update: stale, stats and pair_bits must not overlap");
-  if (!aligned16(pair_bits) || !aligned16(stats)) return fail(GC_ERR_ALIGN, "gc_coverage_update: pair_bits and stats must be 16-byte aligned");
+    return fail(GC_ERR_ALIAS, "%s: stale, stats and pair_bits must not overlap", who);
+  if (!aligned16(pair_bits) || !aligned16(stats)) return fail(GC_ERR_ALIGN, "%s: pair_bits and stats must be 16-byte aligned", who);
+  return GC_OK;
+}
+
+// Argument checks of a selection; mask: the forced views.
+int check_select(const uint32_t* pair_bits, const uint8_t* stale, int B, int N, int H, int W, int a,
+                 const int32_t* forced, int n_forced, const int32_t* anchors_out, const void* workspace,
+                 size_t ws_bytes, const char* who, unsigned long long* mask) {
+  if (!pair_bits || !stale || !anchors_out || !workspace) return fail(GC_ERR_ARG, "%s: null pointer", who);
+  int rc = check_grid(B, N, H, W, who);
+  if (rc) return rc;
+  if (a < 1 || a > N) return fail(GC_ERR_ARG, "%s: a=%d outside [1, N=%d]", who, a, N);
+  if (a > GC_MAX_ANCHORS) return fail(GC_ERR_CAPACITY, "%s: a=%d exceeds %d", who, a, GC_MAX_ANCHORS);
+  if (n_forced < 0 || n_forced > a || (n_forced > 0 && !forced))
+    return fail(GC_ERR_ARG, "%s: n_forced=%d outside [0, a=%d]", who, n_forced, a);
+  if (ws_bytes < gc_coverage_workspace_bytes())
+    return fail(GC_ERR_CAPACITY, "%s: workspace of %zu bytes, %zu needed", who, ws_bytes, gc_coverage_workspace_bytes());
+  if (!aligned16(workspace) || !aligned16(pair_bits)) return fail(GC_ERR_ALIGN, "%s: workspace and pair_bits must be 16-byte aligned", who);
+  *mask = 0;
+  for (int j = 0; j < n_forced; ++j) {
+    if (forced[j] < 0 || forced[j] >= N) return fail(GC_ERR_ARG, "%s: forced view %d outside [0, %d)", who, forced[j], N);
+    if ((*mask >> forced[j]) & 1ull) return fail(GC_ERR_ARG, "%s: forced view %d listed twice", who, forced[j]);
+    *mask |= 1ull << forced[j];
+  }
+  const size_t HW = (size_t)H * W;
+  const size_t n_tok = (size_t)B * N * HW, nb = (size_t)gc_coverage_pair_words(B, N, H, W) * 4;
+  const size_t ws = gc_coverage_workspace_bytes();
+  if (overlaps(workspace, ws, pair_bits, nb) || overlaps(workspace, ws, stale, n_tok) ||
+      overlaps(anchors_out, (size_t)a * 4, workspace, ws) || overlaps(anchors_out, (size_t)a * 4, pair_bits, nb) ||
+      overlaps(anchors_out, (size_t)a * 4, stale, n_tok))
+    return fail(GC_ERR_ALIAS, "%s: workspace / anchors_out overlap an input", who);
+  return GC_OK;
+}
+
+// Argument checks of a scoring call; masks: the candidate sets as view masks.
+int check_score(const uint32_t* pair_bits, const uint8_t* stale, int B, int N, int H, int W, const int32_t* sets,
+                int M, int a, const uint64_t* scores, const void* workspace, size_t ws_bytes, const char* who,
+                SetMasks* masks) {
+  if (!pair_bits || !stale || !sets || !scores || !workspace) return fail(GC_ERR_ARG, "%s: null pointer", who);
+  int rc = check_grid(B, N, H, W, who);
+  if (rc) return rc;
+  if (M < 1 || M > kMaxSets) return fail(GC_ERR_CAPACITY, "%s: M=%d outside [1, %d]", who, M, kMaxSets);
+  if (a < 1 || a > N) return fail(GC_ERR_ARG, "%s: a=%d outside [1, N=%d]", who, a, N);
+  std::memset(masks, 0, sizeof(*masks));
+  for (int m = 0; m < M; ++m)
+    for (int j = 0; j < a; ++j) {
+      const int u = sets[m * a + j];
+      if (u < 0 || u >= N) return fail(GC_ERR_ARG, "%s: view %d of set %d outside [0, %d)", who, u, m, N);
+      masks->m[m] |= 1ull << u;
+    }
+  const size_t HW = (size_t)H * W;
+  const size_t n_tok = (size_t)B * N * HW, nb = (size_t)gc_coverage_pair_words(B, N, H, W) * 4;
+  if (ws_bytes < gc_coverage_workspace_bytes())
+    return fail(GC_ERR_CAPACITY, "%s: workspace of %zu bytes, %zu needed", who, ws_bytes, gc_coverage_workspace_bytes());
+  const size_t ws = gc_coverage_workspace_bytes();
+  if (overlaps(scores, (size_t)M * 8, pair_bits, nb) || overlaps(scores, (size_t)M * 8, stale, n_tok) ||
+      overlaps(workspace, ws, pair_bits, nb) || overlaps(workspace, ws, stale, n_tok) ||
+      overlaps(workspace, ws, scores, (size_t)M * 8))
+    return fail(GC_ERR_ALIAS, "%s: scores / workspace overlap an input or each other", who);
+  if (!aligned16(pair_bits) || !aligned16(workspace) || ((uintptr_t)scores & 7u))
+    return fail(GC_ERR_ALIGN, "%s: pair_bits and workspace 16-byte, scores 8-byte aligned", who);
+  return GC_OK;
+}
+
+// The staleness step alone: one block per (asset, view) row, each writing its
+// row's statistics.
+void launch_update(const uint32_t* pair_bits, int B, int N, size_t HW, unsigned long long mask, int R, uint8_t* stale,
+                   uint32_t* stats, hipStream_t stream) {
   const int wpr = (int)((HW + 31) / 32);
-  // one block per (asset, view) row; each writes its row's statistics
   const dim3 grid((unsigned)(B * N));
   if (rows_aligned(stale, HW))
     hipLaunchKernelGGL(k_cov_update<true>, grid, dim3(kRowBlock), 0, stream, pair_bits, B, N, (int)HW, wpr, mask, R,
@@ -691,6 +868,85 @@ extern "C" int gc_coverage_update(const uint32_t* pair_bits, int B, int N, int H
   else
     hipLaunchKernelGGL(k_cov_update<false>, grid, dim3(kRowBlock), 0, stream, pair_bits, B, N, (int)HW, wpr, mask, R,
                        stale, stats);
+}
+
+// The selection on the current staleness (after the optional step of
+// mask_upd, R, stats, which the histogram pass applies itself).
+void launch_select(const uint32_t* pair_bits, uint8_t* stale, int B, int N, size_t HW, int a, unsigned long long forced,
+                   int n_forced, int32_t* anchors_out, void* workspace, bool upd, unsigned long long mask_upd, int R,
+                   uint32_t* stats, hipStream_t stream) {
+  const bool vec = rows_aligned(stale, HW);
+  if (hist_path(N) && n_forced < a) {
+    SetMasks none;
+    std::memset(&none, 0, sizeof(none));
+    HistState* hs = static_cast<HistState*>(workspace);
+    if (upd)
+      launch_hist<false, true>(pair_bits, stale, B, N, HW, hs, vec, a, forced, anchors_out, none, 0, nullptr, mask_upd,
+                               R, stats, stream);
+    else
+      launch_hist<false, false>(pair_bits, stale, B, N, HW, hs, vec, a, forced, anchors_out, none, 0, nullptr, 0ull, 1,
+                                nullptr, stream);
+    return;
+  }
+  if (upd) launch_update(pair_bits, B, N, HW, mask_upd, R, stale, stats, stream);
+  if (n_forced == a) {
+    hipLaunchKernelGGL(k_sel_forced, dim3(1), dim3(64), 0, stream, forced, N, anchors_out);
+    return;
+  }
+  SelState* st = static_cast<SelState*>(workspace);
+  const int wpr = (int)((HW + 31) / 32);
+  const int nblk = red_blocks((int64_t)B * N * ((wpr + 63) / 64));
+  for (int r = n_forced; r < a; ++r) {   // more views: one pass over the tokens per round
+    const int first = r == n_forced;
+    int32_t* out = r == a - 1 ? anchors_out : nullptr;
+    if (vec)
+      hipLaunchKernelGGL(k_sel_gains<true>, dim3(nblk), dim3(64), 0, stream, pair_bits, stale, B, N, (int)HW, wpr, st,
+                         forced, first);
+    else
+      hipLaunchKernelGGL(k_sel_gains<false>, dim3(nblk), dim3(64), 0, stream, pair_bits, stale, B, N, (int)HW, wpr, st,
+                         forced, first);
+    hipLaunchKernelGGL(k_sel_pick, dim3(1), dim3(1024), 0, stream, st, N, nblk, forced, first, out);
+  }
+}
+
+// The set scores on the current staleness (after the optional step, as above).
+void launch_score(const uint32_t* pair_bits, uint8_t* stale, int B, int N, size_t HW, const SetMasks& masks, int M,
+                  int a, uint64_t* scores, void* workspace, bool upd, unsigned long long mask_upd, int R,
+                  uint32_t* stats, hipStream_t stream) {
+  unsigned long long* out = reinterpret_cast<unsigned long long*>(scores);
+  if (hist_path(N)) {
+    HistState* hs = static_cast<HistState*>(workspace);
+    if (upd)
+      launch_hist<true, true>(pair_bits, stale, B, N, HW, hs, rows_aligned(stale, HW), a, 0ull, nullptr, masks, M, out,
+                              mask_upd, R, stats, stream);
+    else
+      launch_hist<true, false>(pair_bits, stale, B, N, HW, hs, rows_aligned(stale, HW), a, 0ull, nullptr, masks, M,
+                               out, 0ull, 1, nullptr, stream);
+    return;
+  }
+  if (upd) launch_update(pair_bits, B, N, HW, mask_upd, R, stale, stats, stream);
+  SelState* st = static_cast<SelState*>(workspace);
+  const int wpr = (int)((HW + 31) / 32);
+  const int nblk = red_blocks((int64_t)B * N * ((wpr + 63) / 64));
+  if (rows_aligned(stale, HW))
+    hipLaunchKernelGGL(k_cov_score<true>, dim3(nblk), dim3(64), 0, stream, pair_bits, stale, B, N, (int)HW, wpr, masks,
+                       M, st);
+  else
+    hipLaunchKernelGGL(k_cov_score<false>, dim3(nblk), dim3(64), 0, stream, pair_bits, stale, B, N, (int)HW, wpr, masks,
+                       M, st);
+  hipLaunchKernelGGL(k_score_final, dim3(1), dim3(1024), 0, stream, st, M, nblk, out);
+}
+
+}  // namespace
+}  // namespace gc
+
+extern "C" int gc_coverage_update(const uint32_t* pair_bits, int B, int N, int H, int W, const int32_t* anchors, int a,
+                                  int R, uint8_t* stale, uint32_t* stats, hipStream_t stream) {
+  clear_error();
+  unsigned long long mask = 0;
+  const int rc = check_update(pair_bits, B, N, H, W, anchors, a, R, stale, stats, "gc_coverage_update", &mask);
+  if (rc) return rc;
+  launch_update(pair_bits, B, N, (size_t)H * W, mask, R, stale, stats, stream);
   return after_launch(stream, "gc_coverage_update");
 }
 
@@ -703,55 +959,13 @@ extern "C" int gc_coverage_select(const uint32_t* pair_bits, const uint8_t* stal
                                   const int32_t* forced, int n_forced, int32_t* anchors_out, void* workspace,
                                   size_t ws_bytes, hipStream_t stream) {
   clear_error();
-  if (!pair_bits || !stale || !anchors_out || !workspace) return fail(GC_ERR_ARG, "gc_coverage_select: null pointer");
-  int rc = check_grid(B, N, H, W, "gc_coverage_select");
-  if (rc) return rc;
-  if (a < 1 || a > N) return fail(GC_ERR_ARG, "gc_coverage_select: a=%d outside [1, N=%d]", a, N);
-  if (a > GC_MAX_ANCHORS) return fail(GC_ERR_CAPACITY, "gc_coverage_select: a=%d exceeds %d", a, GC_MAX_ANCHORS);
-  if (n_forced < 0 || n_forced > a || (n_forced > 0 && !forced))
-    return fail(GC_ERR_ARG, "gc_coverage_select: n_forced=%d outside [0, a=%d]", n_forced, a);
-  if (ws_bytes < gc_coverage_workspace_bytes())
-    return fail(GC_ERR_CAPACITY, "gc_coverage_select: workspace of %zu bytes, %zu needed", ws_bytes, gc_coverage_workspace_bytes());
-  if (!aligned16(workspace) || !aligned16(pair_bits)) return fail(GC_ERR_ALIGN, "gc_coverage_select: workspace and pair_bits must be 16-byte aligned");
   unsigned long long mask = 0;
-  for (int j = 0; j < n_forced; ++j) {
-    if (forced[j] < 0 || forced[j] >= N) return fail(GC_ERR_ARG, "gc_coverage_select: forced view %d outside [0, %d)", forced[j], N);
-    if ((mask >> forced[j]) & 1ull) return fail(GC_ERR_ARG, "gc_coverage_select: forced view %d listed twice", forced[j]);
-    mask |= 1ull << forced[j];
-  }
-  const size_t HW = (size_t)H * W;
-  const size_t n_tok = (size_t)B * N * HW, nb = (size_t)gc_coverage_pair_words(B, N, H, W) * 4;
-  const size_t ws = gc_coverage_workspace_bytes();
-  if (overlaps(workspace, ws, pair_bits, nb) || overlaps(workspace, ws, stale, n_tok) ||
-      overlaps(anchors_out, (size_t)a * 4, workspace, ws) || overlaps(anchors_out, (size_t)a * 4, pair_bits, nb) ||
-      overlaps(anchors_out, (size_t)a * 4, stale, n_tok))
-    return fail(GC_ERR_ALIAS, "gc_coverage_select: workspace / anchors_out overlap an input");
-  SelState* st = static_cast<SelState*>(workspace);
-  const int wpr = (int)((HW + 31) / 32);
-  const int nblk = red_blocks((int64_t)B * N * ((wpr + 63) / 64));
-  const bool vec = rows_aligned(stale, HW);
-  if (n_forced == a) {
-    hipLaunchKernelGGL(k_sel_forced, dim3(1), dim3(64), 0, stream, mask, N, anchors_out);
-    return after_launch(stream, "gc_coverage_select");
-  }
-  if (hist_path(N)) {   // the coverage histogram: two launches for every round
-    SetMasks none;
-    std::memset(&none, 0, sizeof(none));
-    launch_hist<false>(pair_bits, stale, B, N, HW, static_cast<HistState*>(workspace), vec, a, mask, anchors_out, none, 0,
-                       nullptr, stream);
-    return after_launch(stream, "gc_coverage_select");
-  }
-  for (int r = n_forced; r < a; ++r) {   // more views: one pass over the tokens per round
-    const int first = r == n_forced;
-    int32_t* out = r == a - 1 ? anchors_out : nullptr;
-    if (vec)
-      hipLaunchKernelGGL(k_sel_gains<true>, dim3(nblk), dim3(64), 0, stream, pair_bits, stale, B, N, (int)HW, wpr, st,
-                         mask, first);
-    else
-      hipLaunchKernelGGL(k_sel_gains<false>, dim3(nblk), dim3(64), 0, stream, pair_bits, stale, B, N, (int)HW, wpr, st,
-                         mask, first);
-    hipLaunchKernelGGL(k_sel_pick, dim3(1), dim3(1024), 0, stream, st, N, nblk, mask, first, out);
-  }
+  const int rc = check_select(pair_bits, stale, B, N, H, W, a, forced, n_forced, anchors_out, workspace, ws_bytes,
+                              "gc_coverage_select", &mask);
+  if (rc) return rc;
+  // the pass reads the staleness only (no update): the cast is for the shared kernel
+  launch_select(pair_bits, const_cast<uint8_t*>(stale), B, N, (size_t)H * W, a, mask, n_forced, anchors_out, workspace,
+                false, 0ull, 1, nullptr, stream);
   return after_launch(stream, "gc_coverage_select");
 }
 
@@ -759,45 +973,51 @@ extern "C" int gc_coverage_score(const uint32_t* pair_bits, const uint8_t* stale
                                  const int32_t* sets, int M, int a, uint64_t* scores, void* workspace, size_t ws_bytes,
                                  hipStream_t stream) {
   clear_error();
-  if (!pair_bits || !stale || !sets || !scores || !workspace) return fail(GC_ERR_ARG, "gc_coverage_score: null pointer");
-  int rc = check_grid(B, N, H, W, "gc_coverage_score");
-  if (rc) return rc;
-  if (M < 1 || M > kMaxSets) return fail(GC_ERR_CAPACITY, "gc_coverage_score: M=%d outside [1, %d]", M, kMaxSets);
-  if (a < 1 || a > N) return fail(GC_ERR_ARG, "gc_coverage_score: a=%d outside [1, N=%d]", a, N);
   SetMasks masks;
-  std::memset(&masks, 0, sizeof(masks));
-  for (int m = 0; m < M; ++m)
-    for (int j = 0; j < a; ++j) {
-      const int u = sets[m * a + j];
-      if (u < 0 || u >= N) return fail(GC_ERR_ARG, "gc_coverage_score: view %d of set %d outside [0, %d)", u, m, N);
-      masks.m[m] |= 1ull << u;
-    }
-  const size_t HW = (size_t)H * W;
-  const size_t n_tok = (size_t)B * N * HW, nb = (size_t)gc_coverage_pair_words(B, N, H, W) * 4;
-  if (ws_bytes < gc_coverage_workspace_bytes())
-    return fail(GC_ERR_CAPACITY, "gc_coverage_score: workspace of %zu bytes, %zu needed", ws_bytes, gc_coverage_workspace_bytes());
-  const size_t ws = gc_coverage_workspace_bytes();
-  if (overlaps(scores, (size_t)M * 8, pair_bits, nb) || overlaps(scores, (size_t)M * 8, stale, n_tok) ||
-      overlaps(workspace, ws, pair_bits, nb) || overlaps(workspace, ws, stale, n_tok) ||
-      overlaps(workspace, ws, scores, (size_t)M * 8))
-    return fail(GC_ERR_ALIAS, "gc_coverage_score: scores / workspace overlap an input or each other");
-  if (!aligned16(pair_bits) || !aligned16(workspace) || ((uintptr_t)scores & 7u))
-    return fail(GC_ERR_ALIGN, "gc_coverage_score: pair_bits and workspace 16-byte, scores 8-byte aligned");
-  const int wpr = (int)((HW + 31) / 32);
-  if (hist_path(N)) {
-    launch_hist<true>(pair_bits, stale, B, N, HW, static_cast<HistState*>(workspace), rows_aligned(stale, HW), a, 0ull,
-                      nullptr, masks, M, reinterpret_cast<unsigned long long*>(scores), stream);
-    return after_launch(stream, "gc_coverage_score");
-  }
-  SelState* st = static_cast<SelState*>(workspace);
-  const int nblk = red_blocks((int64_t)B * N * ((wpr + 63) / 64));
-  if (rows_aligned(stale, HW))
-    hipLaunchKernelGGL(k_cov_score<true>, dim3(nblk), dim3(64), 0, stream, pair_bits, stale, B, N, (int)HW, wpr, masks,
-                       M, st);
-  else
-    hipLaunchKernelGGL(k_cov_score<false>, dim3(nblk), dim3(64), 0, stream, pair_bits, stale, B, N, (int)HW, wpr, masks,
-                       M, st);
-  hipLaunchKernelGGL(k_score_final, dim3(1), dim3(1024), 0, stream, st, M, nblk,
-                     reinterpret_cast<unsigned long long*>(scores));
+  const int rc = check_score(pair_bits, stale, B, N, H, W, sets, M, a, scores, workspace, ws_bytes,
+                             "gc_coverage_score", &masks);
+  if (rc) return rc;
+  launch_score(pair_bits, const_cast<uint8_t*>(stale), B, N, (size_t)H * W, masks, M, a, scores, workspace, false, 0ull,
+               1, nullptr, stream);
   return after_launch(stream, "gc_coverage_score");
+}
+
+extern "C" int gc_coverage_update_select(const uint32_t* pair_bits, int B, int N, int H, int W, const int32_t* anchors,
+                                         int a, int R, uint8_t* stale, uint32_t* stats, int a_next,
+                                         const int32_t* forced, int n_forced, int32_t* anchors_out, void* workspace,
+                                         size_t ws_bytes, hipStream_t stream) {
+  clear_error();
+  const char* who = "gc_coverage_update_select";
+  unsigned long long mask_upd = 0, mask_forced = 0;
+  int rc = check_update(pair_bits, B, N, H, W, anchors, a, R, stale, stats, who, &mask_upd);
+  if (rc) return rc;
+  rc = check_select(pair_bits, stale, B, N, H, W, a_next, forced, n_forced, anchors_out, workspace, ws_bytes, who,
+                    &mask_forced);
+  if (rc) return rc;
+  const size_t ws = gc_coverage_workspace_bytes();
+  if (overlaps(stats, (size_t)B * N * 16, workspace, ws) || overlaps(stats, (size_t)B * N * 16, anchors_out, (size_t)a_next * 4))
+    return fail(GC_ERR_ALIAS, "%s: stats overlaps the workspace or anchors_out", who);
+  launch_select(pair_bits, stale, B, N, (size_t)H * W, a_next, mask_forced, n_forced, anchors_out, workspace, true,
+                mask_upd, R, stats, stream);
+  return after_launch(stream, who);
+}
+
+extern "C" int gc_coverage_update_score(const uint32_t* pair_bits, int B, int N, int H, int W, const int32_t* anchors,
+                                        int a, int R, uint8_t* stale, uint32_t* stats, const int32_t* sets, int M,
+                                        int a_set, uint64_t* scores, void* workspace, size_t ws_bytes,
+                                        hipStream_t stream) {
+  clear_error();
+  const char* who = "gc_coverage_update_score";
+  unsigned long long mask_upd = 0;
+  int rc = check_update(pair_bits, B, N, H, W, anchors, a, R, stale, stats, who, &mask_upd);
+  if (rc) return rc;
+  SetMasks masks;
+  rc = check_score(pair_bits, stale, B, N, H, W, sets, M, a_set, scores, workspace, ws_bytes, who, &masks);
+  if (rc) return rc;
+  const size_t ws = gc_coverage_workspace_bytes();
+  if (overlaps(stats, (size_t)B * N * 16, workspace, ws) || overlaps(stats, (size_t)B * N * 16, scores, (size_t)M * 8))
+    return fail(GC_ERR_ALIAS, "%s: stats overlaps the workspace or scores", who);
+  launch_score(pair_bits, stale, B, N, (size_t)H * W, masks, M, a_set, scores, workspace, true, mask_upd, R, stats,
+               stream);
+  return after_launch(stream, who);
 }

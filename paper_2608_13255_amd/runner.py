@@ -20,7 +20,8 @@ import torch
 
 from . import (GC_FULL_HEAD_MID_TAIL, GC_FULL_HEAD_TAIL_E, GC_FULL_PERIODIC, Sampler, VisibleIndex,
                gc_build_correspondence, gc_coverage_init, gc_coverage_pairs, gc_coverage_score, gc_coverage_select,
-               gc_coverage_update, gc_coverage_workspace_bytes, gc_index_correspondence, gc_index_foreground,
+               gc_coverage_update, gc_coverage_update_score, gc_coverage_update_select, gc_coverage_workspace_bytes,
+               gc_index_correspondence, gc_index_foreground,
                gc_posmap_bbox, gc_sampler_reconstruct, gc_sampler_step_times, gc_schedule_advance_gaps,
                gc_schedule_anchors, gc_schedule_forced_views, gc_schedule_full_steps, gc_schedule_refresh_due,
                gc_transport_reconstruct, gc_transport_reconstruct_geom, gc_transport_unipc, gc_transport_unipc_geom,
@@ -79,6 +80,10 @@ class GeoCacheRunner:
             self._ws = (torch.empty(gc_coverage_workspace_bytes(), dtype=torch.uint8, device=pos.device)
                         if self.tracking else None)
         self.stale: Optional[torch.Tensor] = None
+        # the next cached step's selection (device) or set scores, computed
+        # with the last step's staleness update in one pass; None: compute it
+        # when needed (after a restart or a resume)
+        self._next: Optional[torch.Tensor] = None
         self.stats_host = None                        # per-view staleness statistics after the last step (refresh rule)
         self.gap: List[int] = [0] * self.N            # cached steps since each view was last an anchor
         self.last_full = False
@@ -125,6 +130,7 @@ class GeoCacheRunner:
         if self.tracking:
             self.stale = gc_coverage_init(self.pos, stream=self.stream)
             self.stats_host = None
+        self._next = None
         self.gap = [0] * self.N
         self.last_full = False
 
@@ -140,20 +146,34 @@ class GeoCacheRunner:
         self.c += 1
         if self.anchor_policy == "rotate":
             return gc_schedule_anchors(self.N, self.a, c)
+        nxt, self._next = self._next, None
         if self.anchor_policy == "rotation_coverage":
-            sc = gc_coverage_score(self.pairs, self.stale, self.rotation_sets, workspace=self._ws,
-                                   stream=self.stream).cpu().tolist()
+            sc = nxt if nxt is not None else gc_coverage_score(self.pairs, self.stale, self.rotation_sets,
+                                                               workspace=self._ws, stream=self.stream)
+            sc = sc.cpu().tolist()
             return list(self.rotation_sets[sc.index(max(sc))])
-        due = gc_schedule_forced_views(self.gap, self.a, self.max_gap)
-        sel = gc_coverage_select(self.pairs, self.stale, self.a, forced=due, workspace=self._ws, stream=self.stream)
-        return [int(v) for v in sel.cpu().tolist()]
+        if nxt is None:
+            due = gc_schedule_forced_views(self.gap, self.a, self.max_gap)
+            nxt = gc_coverage_select(self.pairs, self.stale, self.a, forced=due, workspace=self._ws, stream=self.stream)
+        return [int(v) for v in nxt.cpu().tolist()]
 
     def _after(self, views: List[int], full: bool) -> None:
         """Staleness and anchor gaps after a step with the given views."""
         self.last_full = full
         self.gap = gc_schedule_advance_gaps(self.gap, views, full)
         if self.tracking:
-            stats = gc_coverage_update(self.pairs, self.stale, views, self.refresh_R, stream=self.stream)
+            # the update and the next cached step's choice in one pass over
+            # the tokens (the forced views follow from the gaps just advanced);
+            # unused when the next step is full
+            if self.anchor_policy == "coverage":
+                due = gc_schedule_forced_views(self.gap, self.a, self.max_gap)
+                stats, self._next = gc_coverage_update_select(self.pairs, self.stale, views, self.refresh_R, self.a,
+                                                              forced=due, workspace=self._ws, stream=self.stream)
+            elif self.anchor_policy == "rotation_coverage":
+                stats, self._next = gc_coverage_update_score(self.pairs, self.stale, views, self.refresh_R,
+                                                             self.rotation_sets, workspace=self._ws, stream=self.stream)
+            else:
+                stats = gc_coverage_update(self.pairs, self.stale, views, self.refresh_R, stream=self.stream)
             # the host reads the statistics back only for the refresh rule
             self.stats_host = stats.cpu() if self.refresh_tau is not None else None
 
@@ -244,3 +264,4 @@ class GeoCacheRunner:
             self.stale = cl(st["stale"])
             self.stats_host = cl(st.get("stats"))
         self.gap = list(st.get("gap", [0] * self.N))
+        self._next = None

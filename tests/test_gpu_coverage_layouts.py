@@ -110,3 +110,36 @@ def test_saturation_runs(gc):
         np.testing.assert_array_equal(stats.cpu().numpy().view(np.uint32), stats_o)
     got = st_d.cpu().numpy()
     assert (got[0, 0] == 0).all() and (got[0, 2] == 254).all() and (got[0, 1, :2] == 255).all()
+
+
+@pytest.mark.parametrize("key", list(CASES))
+def test_fused_update_select_score(gc, key):
+    """gc_coverage_update_select / _score (the staleness step and the next
+    step's choice in one pass) equal the oracle's update followed by its
+    selection / scores on the updated staleness: staleness bytes, statistics
+    and results bit for bit, over a few steps, whatever the workspace held."""
+    seed, B, N, H, W, offset = CASES[key]
+    rs, seen, words, stale = random_case(100 + seed, B, N, H, W, density=0.3)
+    bits = torch.from_numpy(words.view(np.int32)).to(DEV)
+    st_d, buf = device_stale(stale, offset)
+    ws = torch.empty(gc.gc_coverage_workspace_bytes(), dtype=torch.uint8, device=DEV)
+    a = min(3, N)
+    sets = oracle.rotation_sets(N, a) + [sorted(rs.choice(N, a, replace=False).tolist())]
+    st_o = stale
+    steps = [([0], 1, []), (sorted(rs.choice(N, a, replace=False).tolist()), 2, [N - 1]), (list(range(N)), 254, []),
+             ([N - 1], 3, list(range(a))), ([1], 2, [0])]
+    for i, (A, R, forced) in enumerate(steps):
+        ws.copy_(torch.randint(0, 256, ws.shape, dtype=torch.uint8, generator=torch.Generator().manual_seed(i)))
+        if i % 2 == 0:
+            stats, sel = gc.gc_coverage_update_select(bits, st_d, A, R, a, forced=forced, workspace=ws)
+            st_o, stats_o = oracle.coverage_update(st_o, seen, A, R)
+            assert sel.cpu().tolist() == oracle.coverage_select(st_o, seen, a, forced=forced), f"step {i}"
+        else:
+            stats, sc = gc.gc_coverage_update_score(bits, st_d, A, R, sets, workspace=ws)
+            st_o, stats_o = oracle.coverage_update(st_o, seen, A, R)
+            np.testing.assert_array_equal(sc.cpu().numpy().view(np.uint64), oracle.coverage_score(st_o, seen, sets),
+                                          err_msg=f"step {i}")
+        np.testing.assert_array_equal(st_d.cpu().numpy(), st_o, err_msg=f"step {i}")
+        np.testing.assert_array_equal(stats.cpu().numpy().view(np.uint32), stats_o, err_msg=f"step {i}")
+    around = torch.cat([buf[:offset], buf[offset + stale.size:]]).cpu().numpy()
+    assert not around.any()
