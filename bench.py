@@ -133,7 +133,8 @@ def ceiling_rows(torch, dev):
 
 def kernel_source_hash():
     h = hashlib.sha256()
-    for f in ("gc_transport.hip", "gc_latent.h", "gc_common.h"):
+    # the step kernel's sources and the index builder, whose list order shapes the step's memory traffic
+    for f in ("gc_transport.hip", "gc_latent.h", "gc_common.h", "gc_index.hip"):
         h.update(open(os.path.join(ROOT, "paper_2608_13255_amd", "csrc", f), "rb").read())
     return h.hexdigest()[:16]
 
@@ -298,7 +299,8 @@ def main():
     e4.record()
     for _ in range(10):
         for A in anchor_sets:
-            rc = gc.lib().gc_index_correspondence(ops[A][0].data_ptr(), n_tok, corr0.shape[-1], bits_i.data_ptr(),
+            rc = gc.lib().gc_index_correspondence(ops[A][0].data_ptr(), corr0.shape[0] * corr0.shape[1],
+                                                  corr0.shape[2], corr0.shape[3], corr0.shape[-1], bits_i.data_ptr(),
                                                   lst_i.data_ptr(), nv_i.data_ptr(), ws.data_ptr(), ws.numel(),
                                                   torch.cuda.current_stream().cuda_stream)
             assert rc == 0, gc.lib().gc_last_error()

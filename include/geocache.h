@@ -65,7 +65,7 @@
 extern "C" {
 #endif
 
-#define GC_ABI_VERSION 3
+#define GC_ABI_VERSION 4
 
 /* limits */
 #define GC_MAX_VIEWS 64     /* views per asset */
@@ -219,21 +219,29 @@ int gc_build_correspondence(const float* pos, const gc_camera* cams, int B, int 
  * row).  The index lets the per-step calls split their work: the visible
  * tokens, listed compactly, get the gathering; every other token is streamed
  * and recognised by one bit instead of its a correspondence words.
- *   corr       device int32 [n_tokens][a] words from gc_build_correspondence,
- *              n_tokens = B * (N - a) * H * W (at most 2^31 - 1)
+ *   corr       device int32 [n_views][H][W][a] words from gc_build_correspondence,
+ *              n_views = B * (N - a); n_tokens = n_views * H * W is at most
+ *              2^31 - 1, and token i is (view i / (H W), row, column)
  *   vis_bits   device uint32 [ceil(n_tokens / 32)] output: bit (i & 31) of word
  *              i >> 5 is set iff token i has a non-zero word
  *   vis_list   device int32 [n_tokens] output (capacity): the first *n_vis
- *              entries are the visible token indices in ascending order
+ *              entries are the visible token indices in tile order: view by
+ *              view, and inside a view by 16 x 16 tiles of the grid (bands of
+ *              16 rows from the top, tiles from the left, the last band and
+ *              column of tiles shorter or narrower when H or W is not a
+ *              multiple of 16), row-major inside a tile.  A block of the
+ *              step's gather part then holds a compact patch of a view, whose
+ *              anchor taps share cache lines.
  *   n_vis      device int32 [1] output
  *   workspace  device scratch of at least gc_index_workspace_bytes(n_tokens)
  *              bytes, owned by the caller; its contents are not meaningful
  *              after the call and calls sharing one workspace must not overlap
- * The result is deterministic.  n_tokens = 0 is legal (n_vis = 0).
+ * The result is deterministic.  n_views = 0 is legal (n_vis = 0); H, W >= 1.
  */
 size_t gc_index_workspace_bytes(int64_t n_tokens);
-int gc_index_correspondence(const int32_t* corr, int64_t n_tokens, int a, uint32_t* vis_bits, int32_t* vis_list,
-                            int32_t* n_vis, void* workspace, size_t workspace_bytes, hipStream_t stream);
+int gc_index_correspondence(const int32_t* corr, int64_t n_views, int H, int W, int a, uint32_t* vis_bits,
+                            int32_t* vis_list, int32_t* n_vis, void* workspace, size_t workspace_bytes,
+                            hipStream_t stream);
 
 /*
  * gc_index_correspondence without a workspace argument, for callers that
@@ -252,7 +260,7 @@ int gc_index_correspondence(const int32_t* corr, int64_t n_tokens, int a, uint32
  * last call's contents; every call writes all of the part it reads, so
  * nothing has to be cleared between calls.
  */
-int gc_index_correspondence_noalloc(const int32_t* corr, int64_t n_tokens, int a, uint32_t* vis_bits,
+int gc_index_correspondence_noalloc(const int32_t* corr, int64_t n_views, int H, int W, int a, uint32_t* vis_bits,
                                     int32_t* vis_list, int32_t* n_vis, hipStream_t stream);
 
 /*
@@ -261,22 +269,23 @@ int gc_index_correspondence_noalloc(const int32_t* corr, int64_t n_tokens, int a
  * can pass the operator's tolerance test (Sec. 3.2: the test compares 3D
  * points), so the on-the-fly step (gc_transport_*_geom) can evaluate the
  * operator for the listed tokens only and stream every other one.
- *   pos        device float32 [n_tokens][3], n_tokens = B * N * H * W (at
- *              most 2^31 - 1); a token is foreground iff its three
- *              components are finite
+ *   pos        device float32 [n_views][H][W][3], n_views = B * N; n_tokens =
+ *              n_views * H * W is at most 2^31 - 1; a token is foreground iff
+ *              its three components are finite
  *   fg_bits    device uint32 [ceil(n_tokens / 32)] output: bit (i & 31) of
  *              word i >> 5 is set iff token i is foreground
  *   fg_recs    device int32 [n_tokens][4] output (capacity): the first *n_fg
- *              records are {i, x, y, z} for the foreground tokens i in
- *              ascending order, x, y, z being the position's float bit patterns
+ *              records are {i, x, y, z} for the foreground tokens i in the
+ *              tile order of gc_index_correspondence, x, y, z being the
+ *              position's float bit patterns
  *   n_fg       device int32 [1] output
  *   workspace  device scratch of at least gc_index_workspace_bytes(n_tokens)
  *              bytes, as for gc_index_correspondence
  * All pointers 16-byte aligned; outputs must not overlap pos or each other.
- * The result is deterministic.  n_tokens = 0 is legal (n_fg = 0).
+ * The result is deterministic.  n_views = 0 is legal (n_fg = 0); H, W >= 1.
  */
-int gc_index_foreground(const float* pos, int64_t n_tokens, uint32_t* fg_bits, int32_t* fg_recs, int32_t* n_fg,
-                        void* workspace, size_t workspace_bytes, hipStream_t stream);
+int gc_index_foreground(const float* pos, int64_t n_views, int H, int W, uint32_t* fg_bits, int32_t* fg_recs,
+                        int32_t* n_fg, void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 /*
  * Delta transport, Eq. 1 (Sec. 3.2, delta transport and loop order), for one

@@ -21,7 +21,7 @@ import torch
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libgeocache.so")
-ABI_VERSION = 3   # GC_ABI_VERSION the binding is written for
+ABI_VERSION = 4   # GC_ABI_VERSION the binding is written for
 
 # constants mirrored from include/geocache.h
 GC_OK = 0
@@ -95,9 +95,9 @@ def lib() -> ctypes.CDLL:
             "gc_posmap_bbox": ([_vp, _i, _i, _i, _i, ctypes.c_float, _vp, _vp], _i),
             "gc_build_correspondence": ([_vp, _vp, _i, _i, _i, _i, _i32p, _i, _i, _vp, _vp, _vp, _vp, _vp], _i),
             "gc_index_workspace_bytes": ([_i64], ctypes.c_size_t),
-            "gc_index_correspondence": ([_vp, _i64, _i, _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp], _i),
-            "gc_index_correspondence_noalloc": ([_vp, _i64, _i, _vp, _vp, _vp, _vp], _i),
-            "gc_index_foreground": ([_vp, _i64, _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp], _i),
+            "gc_index_correspondence": ([_vp, _i64, _i, _i, _i, _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp], _i),
+            "gc_index_correspondence_noalloc": ([_vp, _i64, _i, _i, _i, _vp, _vp, _vp, _vp], _i),
+            "gc_index_foreground": ([_vp, _i64, _i, _i, _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp], _i),
             "gc_transport_step": ([_vp, _vp, _vp, _vp, _vp, _vp, _i64, _i, _i, _i, _i, _i, _i32p, _i, _i, _i, _vp,
                                    _vp], _i),
             "gc_sampler_reconstruct": ([_vp, _vp, _vp, _vp, _i64, _i, ctypes.POINTER(_Sampler), ctypes.c_double,
@@ -309,12 +309,15 @@ class VisibleIndex:
 
 
 def gc_index_correspondence(corr: torch.Tensor, workspace: torch.Tensor = None, stream=None) -> VisibleIndex:
-    """Visible-token index of a correspondence (corr int32 [B, N-a, H, W, a]).
-    Reads the visible count back to the host (one synchronisation)."""
+    """Visible-token index of a correspondence (corr int32 [B, N-a, H, W, a]),
+    its list in tile order.  Reads the visible count back to the host (one
+    synchronisation)."""
     if corr.dtype != torch.int32 or corr.dim() != 5:
         raise ValueError("corr must be int32 [B, N-a, H, W, a]")
     a = corr.shape[-1]
     n_tok = int(corr.numel() // a) if a else 0
+    n_views = corr.shape[0] * corr.shape[1] if n_tok else 0
+    H, W = max(corr.shape[2], 1), max(corr.shape[3], 1)
     dev = corr.device
     need = int(lib().gc_index_workspace_bytes(n_tok))
     if workspace is None:
@@ -324,8 +327,9 @@ def gc_index_correspondence(corr: torch.Tensor, workspace: torch.Tensor = None, 
     bits = torch.empty(max(1, (n_tok + 31) // 32), dtype=torch.int32, device=dev)
     lst = torch.empty(max(1, n_tok), dtype=torch.int32, device=dev)
     nv = torch.empty(1, dtype=torch.int32, device=dev)
-    _check(lib().gc_index_correspondence(_dev(corr, "corr") if n_tok else None, n_tok, a, _dev(bits, "vis_bits"),
-                                         _dev(lst, "vis_list"), _dev(nv, "n_vis"), _dev(workspace, "workspace"),
+    _check(lib().gc_index_correspondence(_dev(corr, "corr") if n_tok else None, n_views, H, W, a,
+                                         _dev(bits, "vis_bits"), _dev(lst, "vis_list"), _dev(nv, "n_vis"),
+                                         _dev(workspace, "workspace"),
                                          workspace.numel() * workspace.element_size(), _stream(stream)),
            "gc_index_correspondence")
     _keep(stream, (bits, lst))
@@ -341,11 +345,13 @@ def gc_index_correspondence_noalloc(corr: torch.Tensor, stream=None) -> VisibleI
         raise ValueError("corr must be int32 [B, N-a, H, W, a]")
     a = corr.shape[-1]
     n_tok = int(corr.numel() // a) if a else 0
+    n_views = corr.shape[0] * corr.shape[1] if n_tok else 0
+    H, W = max(corr.shape[2], 1), max(corr.shape[3], 1)
     dev = corr.device
     bits = torch.empty(max(1, (n_tok + 31) // 32), dtype=torch.int32, device=dev)
     lst = torch.empty(max(1, n_tok), dtype=torch.int32, device=dev)
     nv = torch.empty(1, dtype=torch.int32, device=dev)
-    _check(lib().gc_index_correspondence_noalloc(_dev(corr, "corr") if n_tok else None, n_tok, a,
+    _check(lib().gc_index_correspondence_noalloc(_dev(corr, "corr") if n_tok else None, n_views, H, W, a,
                                                  _dev(bits, "vis_bits"), _dev(lst, "vis_list"), _dev(nv, "n_vis"),
                                                  _stream(stream)), "gc_index_correspondence_noalloc")
     _keep(stream, (bits, lst))
@@ -364,12 +370,14 @@ class ForegroundIndex:
 
 
 def gc_index_foreground(pos: torch.Tensor, workspace: torch.Tensor = None, stream=None) -> ForegroundIndex:
-    """Foreground index of position maps (float32 [..., 3], e.g. [B, N, H, W, 3]),
-    once per asset batch.  Reads the foreground count back to the host (one
-    synchronisation)."""
-    if pos.dtype != torch.float32 or pos.dim() < 1 or pos.shape[-1] != 3:
-        raise ValueError("pos must be float32 [..., 3]")
+    """Foreground index of position maps (float32 [..., H, W, 3], e.g.
+    [B, N, H, W, 3]), once per asset batch; its records in tile order.  Reads
+    the foreground count back to the host (one synchronisation)."""
+    if pos.dtype != torch.float32 or pos.dim() < 3 or pos.shape[-1] != 3:
+        raise ValueError("pos must be float32 [..., H, W, 3]")
+    H, W = pos.shape[-3], pos.shape[-2]
     n_tok = int(pos.numel() // 3)
+    n_views = n_tok // (H * W) if H * W else 0
     dev = pos.device
     need = int(lib().gc_index_workspace_bytes(n_tok))
     if workspace is None:
@@ -379,7 +387,8 @@ def gc_index_foreground(pos: torch.Tensor, workspace: torch.Tensor = None, strea
     bits = torch.empty(max(1, (n_tok + 31) // 32), dtype=torch.int32, device=dev)
     recs = torch.empty((max(1, n_tok), 4), dtype=torch.int32, device=dev)
     nf = torch.empty(1, dtype=torch.int32, device=dev)
-    _check(lib().gc_index_foreground(_dev(pos, "pos") if n_tok else None, n_tok, _dev(bits, "fg_bits"),
+    _check(lib().gc_index_foreground(_dev(pos, "pos") if n_tok else None, n_views, max(H, 1), max(W, 1),
+                                     _dev(bits, "fg_bits"),
                                      _dev(recs, "fg_recs"), _dev(nf, "n_fg"), _dev(workspace, "workspace"),
                                      workspace.numel() * workspace.element_size(), _stream(stream)),
            "gc_index_foreground")

@@ -84,7 +84,7 @@ struct GArgs {
   UniCoef u;
   // foreground launch
   const uint32_t* fg_bits;   // bit per token of [B][N][H][W]: finite position
-  const int4* fg_recs;       // [n_fg] {token, x, y, z}, ascending token
+  const int4* fg_recs;       // [n_fg] {token, x, y, z}, in the index's tile order
   int n_fg;
   int B;
   int gblocks;               // list blocks in front of the streaming blocks (multiple of kXcds)

@@ -13,9 +13,17 @@
 // operator for foreground tokens only; the list holds each one's token index
 // and position, so that one 16-byte load gives a lane both.
 //
-// Three passes, deterministic (the list is in ascending token order):
-//   count    per 1024-token chunk, listed tokens (ballot + popcount);
-//            also writes the bitmask (one 64-bit ballot per wave)
+// The lists are in tile order: view after view, and inside a view 16 x 16
+// tiles of the token grid (bands of 16 rows from the top, tiles from the
+// left, narrower or shorter at the grid's right and bottom edges), row-major
+// inside a tile.  A block of the per-step kernels takes consecutive list
+// entries, so its tokens form a compact patch of the view, whose footprints
+// in each anchor view lie close together: their tap reads share cache lines.
+//
+// Three passes, deterministic:
+//   count    per 1024-entry chunk of the list order, listed tokens (ballot +
+//            popcount); also writes the bitmask in token order (one 64-bit
+//            ballot per wave over consecutive tokens)
 //   scan     exclusive prefix over the chunk counts, total -> list length
 //   scatter  each chunk writes its tokens at its offset, ranked inside the
 //            chunk by (round, wave, mbcnt of the ballot)
@@ -35,6 +43,26 @@ constexpr int kBlock = 256;
 constexpr int kRounds = 4;                 // tokens per block = kRounds * kBlock
 constexpr int kChunk = kRounds * kBlock;
 constexpr int kWaves = kBlock / 64;
+constexpr int kTile = 16;                  // tiles of the list order: kTile x kTile tokens
+
+// Position i of the list order -> token index; a bijection of
+// [0, n_views * H * W) (no padding: edge tiles are narrower or shorter).
+struct TileOrder {
+  int H, W;
+  int64_t HW;
+  __device__ __forceinline__ int64_t token(int64_t i) const {
+    const int64_t view = i / HW;
+    const int r = (int)(i - view * HW);           // position inside the view
+    const int band = r / (kTile * W);             // band of kTile rows (the last may be shorter)
+    const int rb = r - band * kTile * W;
+    const int bh = min(kTile, H - band * kTile);  // rows of this band
+    const int tx = rb / (bh * kTile);             // tile inside the band (the last may be narrower)
+    const int q = rb - tx * bh * kTile;
+    const int tw = min(kTile, W - tx * kTile);    // columns of this tile
+    const int yy = q / tw;
+    return view * HW + (int64_t)(band * kTile + yy) * W + tx * kTile + (q - yy * tw);
+  }
+};
 
 // Listed tokens of the visible-token index: a non-zero correspondence row.
 struct VisiblePred {
@@ -70,20 +98,24 @@ struct ForegroundPred {
 };
 
 template <class Pred>
-__global__ __launch_bounds__(kBlock) void k_index_count(Pred pred, int64_t n_tokens, uint32_t* __restrict__ bits,
-                                                        int64_t n_words, int32_t* __restrict__ counts) {
+__global__ __launch_bounds__(kBlock) void k_index_count(Pred pred, TileOrder order, int64_t n_tokens,
+                                                        uint32_t* __restrict__ bits, int64_t n_words,
+                                                        int32_t* __restrict__ counts) {
   __shared__ int32_t wave_cnt[kWaves];
   const int wv = threadIdx.x / 64;
   int32_t total = 0;
   for (int r = 0; r < kRounds; ++r) {
-    const int64_t tok = (int64_t)blockIdx.x * kChunk + r * kBlock + threadIdx.x;
-    const unsigned long long m = __ballot(tok < n_tokens && pred(tok));
+    const int64_t i = (int64_t)blockIdx.x * kChunk + r * kBlock + threadIdx.x;
+    // the bitmask over consecutive tokens
+    const unsigned long long m = __ballot(i < n_tokens && pred(i));
     if (__lane_id() == 0) {
       const int64_t w0 = ((int64_t)blockIdx.x * kChunk + r * kBlock + wv * 64) >> 5;
       if (w0 < n_words) bits[w0] = (uint32_t)m;
       if (w0 + 1 < n_words) bits[w0 + 1] = (uint32_t)(m >> 32);
-      wave_cnt[wv] = __popcll(m);
     }
+    // the count over this chunk of the list order
+    const unsigned long long c = __ballot(i < n_tokens && pred(order.token(i)));
+    if (__lane_id() == 0) wave_cnt[wv] = __popcll(c);
     __syncthreads();
     if (threadIdx.x == 0)
       for (int w = 0; w < kWaves; ++w) total += wave_cnt[w];
@@ -118,14 +150,16 @@ __global__ __launch_bounds__(kBlock) void k_index_scan(const int32_t* __restrict
 }
 
 template <class Pred>
-__global__ __launch_bounds__(kBlock) void k_index_scatter(Pred pred, int64_t n_tokens, const int32_t* __restrict__ offsets,
+__global__ __launch_bounds__(kBlock) void k_index_scatter(Pred pred, TileOrder order, int64_t n_tokens,
+                                                          const int32_t* __restrict__ offsets,
                                                           int32_t* __restrict__ list) {
   __shared__ int32_t wave_cnt[kWaves];
   const int wv = threadIdx.x / 64;
   int32_t pos = offsets[blockIdx.x];
   for (int r = 0; r < kRounds; ++r) {
-    const int64_t tok = (int64_t)blockIdx.x * kChunk + r * kBlock + threadIdx.x;
-    const bool vis = tok < n_tokens && pred(tok);
+    const int64_t i = (int64_t)blockIdx.x * kChunk + r * kBlock + threadIdx.x;
+    const int64_t tok = i < n_tokens ? order.token(i) : 0;
+    const bool vis = i < n_tokens && pred(tok);
     const unsigned long long m = __ballot(vis);
     if (__lane_id() == 0) wave_cnt[wv] = __popcll(m);
     __syncthreads();
@@ -155,13 +189,25 @@ extern "C" size_t gc_index_workspace_bytes(int64_t n_tokens) {
 namespace gc {
 namespace {
 
+// Views of H x W tokens: the token count (at most 2^31 - 1) and the list order.
+int check_views(int64_t n_views, int H, int W, const char* who, int64_t* n_tokens, TileOrder* order) {
+  if (n_views < 0 || H < 1 || W < 1)
+    return fail(GC_ERR_SHAPE, "%s: bad shape n_views=%lld H=%d W=%d", who, (long long)n_views, H, W);
+  if (H > GC_MAX_GRID || W > GC_MAX_GRID) return fail(GC_ERR_CAPACITY, "%s: grid %dx%d exceeds %d", who, H, W, GC_MAX_GRID);
+  if (n_views > 0x7fffffffLL / ((int64_t)H * W))
+    return fail(GC_ERR_CAPACITY, "%s: n_views * H * W exceeds 2^31-1", who);
+  *n_tokens = n_views * H * W;
+  order->H = H;
+  order->W = W;
+  order->HW = (int64_t)H * W;
+  return GC_OK;
+}
+
 // Validation of the visible-token index's own arguments (everything but
 // the scratch memory).
 int check_visible_index(const int32_t* corr, int64_t n_tokens, int a, const uint32_t* vis_bits,
                         const int32_t* vis_list, const int32_t* n_vis, const char* who) {
   if (!n_vis) return fail(GC_ERR_ARG, "%s: null n_vis", who);
-  if (n_tokens < 0) return fail(GC_ERR_SHAPE, "%s: n_tokens=%lld is negative", who, (long long)n_tokens);
-  if (n_tokens > 0x7fffffffLL) return fail(GC_ERR_CAPACITY, "%s: n_tokens=%lld exceeds 2^31-1", who, (long long)n_tokens);
   if (a < 1 || a > GC_MAX_ANCHORS) return fail(GC_ERR_ARG, "%s: a=%d outside [1, %d]", who, a, GC_MAX_ANCHORS);
   if (n_tokens > 0 && (!corr || !vis_bits || !vis_list)) return fail(GC_ERR_ARG, "%s: null pointer", who);
   if ((corr && !aligned16(corr)) || (vis_bits && !aligned16(vis_bits)) || (vis_list && !aligned16(vis_list)))
@@ -176,19 +222,19 @@ int check_visible_index(const int32_t* corr, int64_t n_tokens, int a, const uint
 
 // The three passes; counts_offsets: 2 * ceil(n_tokens / kChunk) int32 of
 // device scratch, fully written before it is read.
-void launch_visible_index(const int32_t* corr, int64_t n_tokens, int a, uint32_t* vis_bits, int32_t* vis_list,
-                          int32_t* n_vis, int32_t* counts_offsets, hipStream_t stream) {
+void launch_visible_index(const int32_t* corr, int64_t n_tokens, const TileOrder& order, int a, uint32_t* vis_bits,
+                          int32_t* vis_list, int32_t* n_vis, int32_t* counts_offsets, hipStream_t stream) {
   const int64_t n_words = (n_tokens + 31) / 32;
   const int64_t nb = n_tokens > 0 ? (n_tokens + kChunk - 1) / kChunk : 0;
   int32_t* counts = counts_offsets;
   int32_t* offsets = counts + nb;
   if (nb > 0)
     hipLaunchKernelGGL(k_index_count<VisiblePred>, dim3((unsigned)nb), dim3(kBlock), 0, stream,
-                       VisiblePred{corr, a}, n_tokens, vis_bits, n_words, counts);
+                       VisiblePred{corr, a}, order, n_tokens, vis_bits, n_words, counts);
   hipLaunchKernelGGL(k_index_scan, dim3(1), dim3(kBlock), 0, stream, counts, nb, offsets, n_vis);
   if (nb > 0)
     hipLaunchKernelGGL(k_index_scatter<VisiblePred>, dim3((unsigned)nb), dim3(kBlock), 0, stream,
-                       VisiblePred{corr, a}, n_tokens, offsets, vis_list);
+                       VisiblePred{corr, a}, order, n_tokens, offsets, vis_list);
 }
 
 // Device address of this library's scratch array on the current device,
@@ -217,13 +263,17 @@ int scratch_on_current_device(void** out, const char* who) {
 }  // namespace
 }  // namespace gc
 
-extern "C" int gc_index_correspondence(const int32_t* corr, int64_t n_tokens, int a, uint32_t* vis_bits,
+extern "C" int gc_index_correspondence(const int32_t* corr, int64_t n_views, int H, int W, int a, uint32_t* vis_bits,
                                        int32_t* vis_list, int32_t* n_vis, void* workspace, size_t workspace_bytes,
                                        hipStream_t stream) {
   clear_error();
   const char* who = "gc_index_correspondence";
   if (!workspace) return fail(GC_ERR_ARG, "%s: null workspace", who);
-  int rc = check_visible_index(corr, n_tokens, a, vis_bits, vis_list, n_vis, who);
+  int64_t n_tokens = 0;
+  TileOrder order;
+  int rc = check_views(n_views, H, W, who, &n_tokens, &order);
+  if (rc) return rc;
+  rc = check_visible_index(corr, n_tokens, a, vis_bits, vis_list, n_vis, who);
   if (rc) return rc;
   if (!aligned16(workspace)) return fail(GC_ERR_ALIGN, "%s: pointers must be 16-byte aligned", who);
   if (workspace_bytes < gc_index_workspace_bytes(n_tokens))
@@ -233,15 +283,20 @@ extern "C" int gc_index_correspondence(const int32_t* corr, int64_t n_tokens, in
   if (overlaps(workspace, workspace_bytes, corr, nc) || overlaps(workspace, workspace_bytes, vis_list, nl) ||
       overlaps(workspace, workspace_bytes, vis_bits, nbits) || overlaps(workspace, workspace_bytes, n_vis, 4))
     return fail(GC_ERR_ALIAS, "%s: buffers overlap", who);
-  launch_visible_index(corr, n_tokens, a, vis_bits, vis_list, n_vis, static_cast<int32_t*>(workspace), stream);
+  launch_visible_index(corr, n_tokens, order, a, vis_bits, vis_list, n_vis, static_cast<int32_t*>(workspace), stream);
   return after_launch(stream, who);
 }
 
-extern "C" int gc_index_correspondence_noalloc(const int32_t* corr, int64_t n_tokens, int a, uint32_t* vis_bits,
-                                               int32_t* vis_list, int32_t* n_vis, hipStream_t stream) {
+extern "C" int gc_index_correspondence_noalloc(const int32_t* corr, int64_t n_views, int H, int W, int a,
+                                               uint32_t* vis_bits, int32_t* vis_list, int32_t* n_vis,
+                                               hipStream_t stream) {
   clear_error();
   const char* who = "gc_index_correspondence_noalloc";
-  int rc = check_visible_index(corr, n_tokens, a, vis_bits, vis_list, n_vis, who);
+  int64_t n_tokens = 0;
+  TileOrder order;
+  int rc = check_views(n_views, H, W, who, &n_tokens, &order);
+  if (rc) return rc;
+  rc = check_visible_index(corr, n_tokens, a, vis_bits, vis_list, n_vis, who);
   if (rc) return rc;
   if (gc_index_workspace_bytes(n_tokens) > GC_NOALLOC_SCRATCH_BYTES)
     return fail(GC_ERR_CAPACITY, "%s: n_tokens=%lld needs %zu bytes of scratch, above the library's %d", who,
@@ -249,17 +304,19 @@ extern "C" int gc_index_correspondence_noalloc(const int32_t* corr, int64_t n_to
   void* ws = nullptr;
   rc = scratch_on_current_device(&ws, who);
   if (rc) return rc;
-  launch_visible_index(corr, n_tokens, a, vis_bits, vis_list, n_vis, static_cast<int32_t*>(ws), stream);
+  launch_visible_index(corr, n_tokens, order, a, vis_bits, vis_list, n_vis, static_cast<int32_t*>(ws), stream);
   return after_launch(stream, who);
 }
 
-extern "C" int gc_index_foreground(const float* pos, int64_t n_tokens, uint32_t* fg_bits, int32_t* fg_recs,
-                                   int32_t* n_fg, void* workspace, size_t workspace_bytes, hipStream_t stream) {
+extern "C" int gc_index_foreground(const float* pos, int64_t n_views, int H, int W, uint32_t* fg_bits,
+                                   int32_t* fg_recs, int32_t* n_fg, void* workspace, size_t workspace_bytes,
+                                   hipStream_t stream) {
   clear_error();
   if (!n_fg || !workspace) return fail(GC_ERR_ARG, "foreground index: null n_fg or workspace");
-  if (n_tokens < 0) return fail(GC_ERR_SHAPE, "foreground index: n_tokens=%lld is negative", (long long)n_tokens);
-  if (n_tokens > 0x7fffffffLL)
-    return fail(GC_ERR_CAPACITY, "foreground index: n_tokens=%lld exceeds 2^31-1", (long long)n_tokens);
+  int64_t n_tokens = 0;
+  TileOrder order;
+  const int rc = check_views(n_views, H, W, "foreground index", &n_tokens, &order);
+  if (rc) return rc;
   if (n_tokens > 0 && (!pos || !fg_bits || !fg_recs)) return fail(GC_ERR_ARG, "foreground index: null pointer");
   if ((pos && !aligned16(pos)) || (fg_bits && !aligned16(fg_bits)) || (fg_recs && !aligned16(fg_recs)) ||
       !aligned16(workspace))
@@ -279,10 +336,10 @@ extern "C" int gc_index_foreground(const float* pos, int64_t n_tokens, uint32_t*
   int32_t* offsets = counts + nb;
   if (nb > 0)
     hipLaunchKernelGGL(k_index_count<ForegroundPred>, dim3((unsigned)nb), dim3(kBlock), 0, stream,
-                       ForegroundPred{pos}, n_tokens, fg_bits, n_words, counts);
+                       ForegroundPred{pos}, order, n_tokens, fg_bits, n_words, counts);
   hipLaunchKernelGGL(k_index_scan, dim3(1), dim3(kBlock), 0, stream, counts, nb, offsets, n_fg);
   if (nb > 0)
     hipLaunchKernelGGL(k_index_scatter<ForegroundPred>, dim3((unsigned)nb), dim3(kBlock), 0, stream,
-                       ForegroundPred{pos}, n_tokens, offsets, fg_recs);
+                       ForegroundPred{pos}, order, n_tokens, offsets, fg_recs);
   return after_launch(stream, "gc_index_foreground");
 }

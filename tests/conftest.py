@@ -97,3 +97,21 @@ def storage_ulps(got, want, dtype):
         i = np.where(h & 0x8000, -(h & 0x7FFF), h)
         j = np.where(k & 0x8000, -(k & 0x7FFF), k)
     return np.abs(i - j)
+
+
+def tile_order(n_views: int, H: int, W: int) -> np.ndarray:
+    """Token indices of n_views H x W grids in the index lists' order, by its
+    definition: view by view; 16 x 16 tiles in bands of 16 rows from the top,
+    tiles from the left (the last band and tile column shorter or narrower);
+    row-major inside a tile."""
+    y, x = np.meshgrid(np.arange(H), np.arange(W), indexing="ij")
+    key = ((y // 16) * ((W + 15) // 16) + x // 16) * 256 + (y % 16) * 16 + x % 16
+    within = np.argsort(key.reshape(-1), kind="stable")
+    return (np.arange(n_views)[:, None] * (H * W) + within[None, :]).reshape(-1)
+
+
+def listed_in_tile_order(flags: np.ndarray, H: int, W: int) -> np.ndarray:
+    """The tokens whose flag is set (flags over n_views * H * W tokens), in the
+    index lists' order."""
+    order = tile_order(flags.size // (H * W), H, W)
+    return order[flags.reshape(-1)[order]].astype(np.int32)

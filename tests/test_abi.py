@@ -142,21 +142,25 @@ def test_reconstruct_and_build_validation(gc, L):
     assert L.gc_posmap_bbox(A0, 1, 4, 8, 8, 0.01, A1 + 4, None) == -4
     need = L.gc_index_workspace_bytes(1 << 20)
     assert need >= 2 * 4 * 1024 and need % 256 == 0
-    assert L.gc_index_correspondence(A0, 1 << 20, 4, A1, A2, A3, A4, need - 1, None) == -6
-    assert L.gc_index_correspondence(A0, 1 << 20, 9, A1, A2, A3, A4, need, None) == -1
-    assert L.gc_index_correspondence(A0, 1 << 20, 4, A1, A0 + 64, A3, A4, need, None) == -5
-    assert L.gc_index_correspondence(A0, -1, 4, A1, A2, A3, A4, need, None) == -2
+    # visible-token index: 64 views of 128 x 128 tokens = 2^20
+    assert L.gc_index_correspondence(A0, 64, 128, 128, 4, A1, A2, A3, A4, need - 1, None) == -6
+    assert L.gc_index_correspondence(A0, 64, 128, 128, 9, A1, A2, A3, A4, need, None) == -1
+    assert L.gc_index_correspondence(A0, 64, 128, 128, 4, A1, A0 + 64, A3, A4, need, None) == -5
+    assert L.gc_index_correspondence(A0, -1, 128, 128, 4, A1, A2, A3, A4, need, None) == -2
+    assert L.gc_index_correspondence(A0, 64, 0, 128, 4, A1, A2, A3, A4, need, None) == -2
+    assert L.gc_index_correspondence(A0, 64, 128, 5000, 4, A1, A2, A3, A4, need, None) == -6
+    assert L.gc_index_correspondence(A0, 1 << 17, 128, 128, 4, A1, A2, A3, A4, need, None) == -6   # 2^31 tokens
     # foreground index of position maps: pos, bits, records, count, workspace
-    n = 1 << 20
-    assert L.gc_index_foreground(A0, n, A1, A2, A3, A4, need - 1, None) == -6
-    assert L.gc_index_foreground(A0, n, A1, A2, None, A4, need, None) == -1
-    assert L.gc_index_foreground(None, n, A1, A2, A3, A4, need, None) == -1
-    assert L.gc_index_foreground(A0, -1, A1, A2, A3, A4, need, None) == -2
-    assert L.gc_index_foreground(A0, 1 << 31, A1, A2, A3, A4, need, None) == -6
-    assert L.gc_index_foreground(A0, n, A1, A2 + 8, A3, A4, need, None) == -4
-    assert L.gc_index_foreground(A0, n, A1, A0 + 64, A3, A4, need, None) == -5   # records overlap the maps
-    assert L.gc_index_foreground(A0, n, A1, A2, A2 + 16, A4, need, None) == -5   # count inside the records
-    assert L.gc_index_foreground(A0, n, A1, A2, A3, A1 + 16, need, None) == -5   # workspace over the bits
+    assert L.gc_index_foreground(A0, 64, 128, 128, A1, A2, A3, A4, need - 1, None) == -6
+    assert L.gc_index_foreground(A0, 64, 128, 128, A1, A2, None, A4, need, None) == -1
+    assert L.gc_index_foreground(None, 64, 128, 128, A1, A2, A3, A4, need, None) == -1
+    assert L.gc_index_foreground(A0, -1, 128, 128, A1, A2, A3, A4, need, None) == -2
+    assert L.gc_index_foreground(A0, 64, 128, 0, A1, A2, A3, A4, need, None) == -2
+    assert L.gc_index_foreground(A0, 1 << 31, 1, 1, A1, A2, A3, A4, need, None) == -6
+    assert L.gc_index_foreground(A0, 64, 128, 128, A1, A2 + 8, A3, A4, need, None) == -4
+    assert L.gc_index_foreground(A0, 64, 128, 128, A1, A0 + 64, A3, A4, need, None) == -5   # records overlap the maps
+    assert L.gc_index_foreground(A0, 64, 128, 128, A1, A2, A2 + 16, A4, need, None) == -5   # count inside the records
+    assert L.gc_index_foreground(A0, 64, 128, 128, A1, A2, A3, A1 + 16, need, None) == -5   # workspace over the bits
 
 
 def test_host_schedule_matches_oracle(gc):
@@ -427,7 +431,8 @@ def test_noalloc_index_validation(gc, L):
     nv = (ctypes.c_int32 * 1)()
 
     def call(corr=A0, n=4096, a=4, bits=A1, lst=A2, nvp=A3):
-        return L.gc_index_correspondence_noalloc(corr, n, a, bits, lst, nvp, None)
+        # n tokens as n views of one token (the order does not matter here)
+        return L.gc_index_correspondence_noalloc(corr, n, 1, 1, a, bits, lst, nvp, None)
 
     assert gc.GC_NOALLOC_SCRATCH_BYTES == 1 << 20
     big = 134217728

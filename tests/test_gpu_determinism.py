@@ -112,8 +112,8 @@ def test_step_kernels(gc, setup):
         # the foreground launch, with the index rebuilt into pre-filled buffers
         fb = filled(None, r, ((P.numel() // 3 + 31) // 32,), torch.int32)
         fr = filled(None, r, (P.numel() // 3, 4), torch.int32)
-        rc = gc.lib().gc_index_foreground(P.data_ptr(), P.numel() // 3, fb.data_ptr(), fr.data_ptr(),
-                                          nf_d[r].data_ptr(), ws.data_ptr(), ws.numel(),
+        rc = gc.lib().gc_index_foreground(P.data_ptr(), P.shape[0] * P.shape[1], P.shape[2], P.shape[3],
+                                          fb.data_ptr(), fr.data_ptr(), nf_d[r].data_ptr(), ws.data_ptr(), ws.numel(),
                                           torch.cuda.current_stream().cuda_stream)
         assert rc == 0, gc.lib().gc_last_error()
         n_fg = int(nf_d[r].item())

@@ -15,7 +15,7 @@ Every case also runs the foreground launch (with gc_index_foreground's index
 of the position maps), which must give the same bits, and checks that index
 against its definition: a bit per token set iff its three position
 components are finite, and the foreground tokens' {token, x, y, z} records
-in ascending order.  Separately: all-background maps (an empty list), more
+in the lists' tile order.  Separately: all-background maps (an empty list), more
 (asset, anchor) cameras than the launch stages (B * a > 64: the blocked
 launch runs), and token counts that end inside a 32-bit word and a chunk.
 """
@@ -27,7 +27,7 @@ import oracle
 import synth
 from synth.configs import C1, C2, C3, C4, C5
 
-from conftest import latent_maps
+from conftest import latent_maps, listed_in_tile_order
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda:0"
@@ -88,7 +88,7 @@ def expected_foreground(P):
     n = fg.size
     words = np.packbits(np.concatenate([fg, np.zeros((-n) % 32, bool)]).astype(np.uint8), bitorder="little")
     words = words.view(np.uint32) if words.size else np.zeros(0, np.uint32)
-    tok = np.nonzero(fg)[0].astype(np.int32)
+    tok = listed_in_tile_order(fg, P.shape[-3], P.shape[-2]) if n else np.zeros(0, np.int32)
     recs = np.concatenate([tok[:, None], flat[tok].view(np.int32)], 1) if tok.size else np.zeros((0, 4), np.int32)
     return words, recs
 

@@ -20,7 +20,7 @@ import oracle
 import synth
 from synth.configs import C1, C2, C3, C4, C5
 
-from conftest import latent_maps, stored_x0_slack, visible_weights, x0_coef
+from conftest import latent_maps, listed_in_tile_order, stored_x0_slack, visible_weights, x0_coef
 
 pytestmark = pytest.mark.gpu
 
@@ -405,7 +405,7 @@ def _expected_index(corr_o):
     words = np.zeros((n + 31) // 32, np.uint32)
     for i in np.flatnonzero(vis):
         words[i >> 5] |= np.uint32(1) << np.uint32(i & 31)
-    return words, np.flatnonzero(vis).astype(np.int32)
+    return words, listed_in_tile_order(vis, corr_o.shape[-3], corr_o.shape[-2])
 
 
 def _check_index(idx, corr_o):

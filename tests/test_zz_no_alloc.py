@@ -12,7 +12,7 @@ import oracle
 import synth
 from synth.configs import C2, C5
 
-from conftest import latent_maps
+from conftest import latent_maps, listed_in_tile_order
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda:0"
@@ -30,17 +30,18 @@ def _index(gc, corr, noalloc):
     L = gc.lib()
     a = corr.shape[-1]
     n = corr.numel() // a
+    n_views, H, W = corr.shape[0] * corr.shape[1], corr.shape[2], corr.shape[3]
     bits = torch.full(((n + 31) // 32,), -1, dtype=torch.int32, device=DEV)
     lst = torch.full((n,), -7, dtype=torch.int32, device=DEV)
     nv = torch.full((1,), -1, dtype=torch.int32, device=DEV)
     s = torch.cuda.current_stream().cuda_stream
     if noalloc:
-        rc = L.gc_index_correspondence_noalloc(corr.data_ptr(), n, a, bits.data_ptr(), lst.data_ptr(), nv.data_ptr(),
-                                               s)
+        rc = L.gc_index_correspondence_noalloc(corr.data_ptr(), n_views, H, W, a, bits.data_ptr(), lst.data_ptr(),
+                                               nv.data_ptr(), s)
     else:
         ws = torch.empty(int(L.gc_index_workspace_bytes(n)), dtype=torch.uint8, device=DEV)
-        rc = L.gc_index_correspondence(corr.data_ptr(), n, a, bits.data_ptr(), lst.data_ptr(), nv.data_ptr(),
-                                       ws.data_ptr(), ws.numel(), s)
+        rc = L.gc_index_correspondence(corr.data_ptr(), n_views, H, W, a, bits.data_ptr(), lst.data_ptr(),
+                                       nv.data_ptr(), ws.data_ptr(), ws.numel(), s)
     assert rc == 0, L.gc_last_error().decode()
     torch.cuda.synchronize()
     k = int(nv.item())
@@ -57,6 +58,7 @@ def test_noalloc_index_equals_workspace_index_twice():
         assert n1 == n0 > 0
         np.testing.assert_array_equal(b1, b0)
         np.testing.assert_array_equal(l1, l0)
-        # the list is the ascending non-zero rows of the operator
-        rows = np.flatnonzero(corr.view(-1, corr.shape[-1]).cpu().numpy().any(axis=1))
+        # the list is the non-zero rows of the operator, in the lists' tile order
+        rows = listed_in_tile_order(corr.view(-1, corr.shape[-1]).cpu().numpy().any(axis=1), corr.shape[2],
+                                    corr.shape[3])
         np.testing.assert_array_equal(l1, rows)
