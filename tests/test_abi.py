@@ -445,3 +445,17 @@ def test_noalloc_index_validation(gc, L):
     assert call(corr=A0 + 4) == -4
     assert call(lst=A1 + 64) == -5             # list overlaps the bits
     assert call(n=2 ** 31) == -6
+
+
+def test_tile_order_definition():
+    """The tests' definition of the index lists' order on a hand example: a
+    3 x 18 grid is one band of two tiles, 16 columns then 2; row-major inside
+    each; a second view follows the first."""
+    from conftest import tile_order
+    first = [y * 18 + x for y in range(3) for x in range(16)] + [y * 18 + x for y in range(3) for x in (16, 17)]
+    assert tile_order(1, 3, 18).tolist() == first
+    assert tile_order(2, 3, 18).tolist() == first + [54 + t for t in first]
+    # 17 rows: a full band of 16 rows, then a band of one row
+    t = tile_order(1, 17, 4).tolist()
+    assert t == list(range(64)) + [64, 65, 66, 67]
+    assert sorted(tile_order(3, 37, 53).tolist()) == list(range(3 * 37 * 53))
