@@ -439,14 +439,38 @@ __global__ __launch_bounds__(kBlock) void k_transport_geom_fg(GArgs g) {
     pj[j].ok = pj[j].ok && fg && s < g.a;
     any_ok = any_ok || pj[j].ok;
   }
-  if (__ballot(any_ok)) {
-    TapPos tp[kApl];
+  const bool loaded = __ballot(any_ok) != 0ull;
+  TapPos tp[kApl];
+  if (loaded) {
 #pragma unroll
     for (int j = 0; j < kApl; ++j) {
       const int s = j * G + lane_g;
       const int sc = s < g.a ? s : 0;
       tp[j] = anchor_tap_positions(pj[j], g.pos + ((int64_t)b * g.N + view_lds[sc]) * g.HW * 3, g.H, g.W);
     }
+  }
+  // The latent phase reads the token's own x0_prev and sampler input only
+  // after the tap tests and the ranking; one dword of each, loaded now into
+  // an LDS sink that nothing reads, brings their lines into L2 meanwhile
+  // without holding a register (issued after the tap loads, so the tap
+  // tests do not wait for them; the block's barriers wait on LDS only).
+  if (tok_ok) {
+    __shared__ float s_sink[64];
+    const int64_t off = (int64_t)tokg * g.C * (DT == GC_F32 ? 4 : 2);
+    const void* own = nullptr;
+    if (lane_g == 0) own = g.x0_prev;
+    if (lane_g == (G > 1 ? 1 : 0)) {
+      const void* side = MODE == kGeomReconstruct ? g.x_t : MODE == kGeomUniPC ? (g.u.corr ? g.x_prev : g.x_t) : nullptr;
+      if (G > 1) own = side;
+      else if (side)
+        __builtin_amdgcn_global_load_lds(static_cast<const char*>(side) + off,
+                                         (__attribute__((address_space(3))) void*)s_sink, 4, 0, 0);
+    }
+    if (own)
+      __builtin_amdgcn_global_load_lds(static_cast<const char*>(own) + off,
+                                       (__attribute__((address_space(3))) void*)s_sink, 4, 0, 0);
+  }
+  if (loaded) {
     const float tol2 = g.bbox[(int64_t)b * 8 + 6];
 #pragma unroll
     for (int j = 0; j < kApl; ++j) at[j] = anchor_select(P, pj[j], tp[j], g.H, g.W, g.K, tol2);
