@@ -40,7 +40,9 @@
 // list covers all views; a record of an anchor view is skipped.  A block of
 // the list may straddle views and assets, so it stages the cameras of every
 // (asset, anchor slot) in LDS (B * a <= kMaxCamLds; beyond that the blocked
-// launch runs, with the same result).
+// launch runs, with the same result).  Its tokens are all foreground and
+// mostly visible, so it does without the blocked launch's ranking: each lane
+// serves its own token's channel vectors.
 #include "gc_common.h"
 #include "gc_geometry.h"
 #include "gc_latent.h"
@@ -488,87 +490,54 @@ __global__ __launch_bounds__(kBlock) void k_transport_geom_fg(GArgs g) {
 #pragma unroll
   for (int j = 0; j < kApl; ++j) n_vis += __popcll((__ballot(at[j].word != 0) >> gbase) & ((1ull << G) - 1));
 
-  // the block's visible tokens first, then its other listed target tokens;
-  // one (token, channel vector) item per lane in that order
-  __shared__ int32_t s_tok[kTok];
-  __shared__ int32_t s_nvis[kTok];
+  // No ranking here: a list block's tokens are all foreground and mostly
+  // visible (the blocked launch's blocks also hold background), so each lane
+  // serves its own token's channel vectors lane_g, lane_g + G, ...  The
+  // group's lanes put their anchor slots' words and weights in LDS and read
+  // all of them back; the group is part of one wave, so a wave barrier
+  // orders the writes before the reads (no block barrier).
   __shared__ int32_t s_word[kTok][AMAX + 1];       // +1: no bank conflicts between consecutive tokens
   __shared__ float s_wk[kTok][AMAX * 4 + 1];
-  __shared__ int32_t s_count[kBlock / 64][2];      // per wave: visible tokens, listed target tokens
-  const bool vis = tok_ok && n_vis > 0;
-  const bool lead = lane_g == 0;
-  const unsigned long long bvis = __ballot(lead && vis);
-  const unsigned long long blive = __ballot(lead && tok_ok);
-  const int wv = (int)threadIdx.x / 64;
-  if (__lane_id() == 0) {
-    s_count[wv][0] = __popcll(bvis);
-    s_count[wv][1] = __popcll(blive);
-  }
-  __syncthreads();
-  int off_v = 0, off_l = 0, nv = 0, nl = 0;
+  const int rl = (int)threadIdx.x / G;             // this token's place in the block
+  if (tok_ok && n_vis > 0) {
 #pragma unroll
-  for (int q = 0; q < kBlock / 64; ++q) {
-    const int cv_ = s_count[q][0], cl_ = s_count[q][1];
-    off_v += q < wv ? cv_ : 0;
-    off_l += q < wv ? cl_ : 0;
-    nv += cv_;
-    nl += cl_;
-  }
-  if (tok_ok) {
-    const unsigned long long below = (1ull << gbase) - 1;   // the groups before this one in the wave
-    const int rv = off_v + __popcll(bvis & below);
-    const int rl = off_l + __popcll(blive & below);
-    if (lead) s_tok[vis ? rv : nv + (rl - rv)] = tokg;
-    if (vis) {
+    for (int j = 0; j < kApl; ++j) {
+      const int s = j * G + lane_g;
+      if (s < g.a) {
+        s_word[rl][s] = at[j].word;
 #pragma unroll
-      for (int j = 0; j < kApl; ++j) {
-        const int s = j * G + lane_g;
-        if (s < g.a) {
-          s_word[rv][s] = at[j].word;
-#pragma unroll
-          for (int k = 0; k < 4; ++k) s_wk[rv][s * 4 + k] = at[j].wk[k];
-        }
+        for (int k = 0; k < 4; ++k) s_wk[rl][s * 4 + k] = at[j].wk[k];
       }
-      if (lead) s_nvis[rv] = n_vis;
     }
   }
-  __syncthreads();
-
-  const int n_items = nl * g.CV;
-  for (int it = (int)threadIdx.x; it < n_items; it += kBlock) {
-    int slot, c;
-    if (g.cv_shift >= 0) {
-      slot = it >> g.cv_shift;
-      c = it & (g.CV - 1);
-    } else {
-      slot = it / g.CV;
-      c = it - slot * g.CV;
-    }
-    const int tk = s_tok[slot];
-    const int64_t e = (int64_t)tk * g.C + (int64_t)c * VEC;   // latents are [B][N][H][W][C]
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  if (!tok_ok) return;
+  for (int c = lane_g; c < g.CV; c += G) {
+    const int64_t e = (int64_t)tokg * g.C + (int64_t)c * VEC;   // latents are [B][N][H][W][C]
     Side<DT, VEC> sd = load_side<DT, VEC, MODE>(g, e, false);
     const Raw prevr = CD::load_stream(g.x0_prev, e);
     sd.m1 = prevr;   // m_{k-1}: the token's own stored x0
     Raw x0r;
-    if (slot < nv) {
-      const int ib = tk / g.HW / g.N;
-      const float inv = (float)s_nvis[slot];
+    if (n_vis > 0) {
+      const float inv = (float)n_vis;
       float acc[VEC];
 #pragma unroll
       for (int q = 0; q < VEC; ++q) acc[q] = 0.0f;
       for (int s = 0; s < g.a; ++s) {   // ascending slots, as the stored operator sums
-        const uint32_t w = (uint32_t)s_word[slot][s];
+        const uint32_t w = (uint32_t)s_word[rl][s];
         if (!w) continue;
         const int x0 = (int)(w & 0xfffu) - 1;
         const int y0 = (int)((w >> 12) & 0xfffu) - 1;
         const uint32_t mask = (w >> 24) & 0xfu;
-        const int64_t new_view = ((int64_t)ib * g.a + s) * g.HW;
-        const int64_t old_view = ((int64_t)ib * g.N + g.anchor_view[s]) * g.HW;
+        const int64_t new_view = ((int64_t)b * g.a + s) * g.HW;
+        const int64_t old_view = ((int64_t)b * g.N + g.anchor_view[s]) * g.HW;
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
           if (!(mask & (1u << k))) continue;
           const int qq = (y0 + (k >> 1)) * g.W + x0 + (k & 1);
-          const float wt = s_wk[slot][s * 4 + k] / inv;   // the builder's stored weight
+          const float wt = s_wk[rl][s * 4 + k] / inv;   // the builder's stored weight
           float nf[VEC], of[VEC];
           CD::unpack(CD::load(g.x0_new, (new_view + qq) * g.C + (int64_t)c * VEC), nf);
           CD::unpack(CD::load(g.x0_prev, (old_view + qq) * g.C + (int64_t)c * VEC), of);
