@@ -459,3 +459,55 @@ def test_tile_order_definition():
     t = tile_order(1, 17, 4).tolist()
     assert t == list(range(64)) + [64, 65, 66, 67]
     assert sorted(tile_order(3, 37, 53).tolist()) == list(range(3 * 37 * 53))
+
+
+def test_coverage_validation(gc, L):
+    """The coverage calls check their arguments on the host and fail before
+    any launch: update, selection, scoring and the fused update + selection /
+    scoring (whose stats must not overlap the workspace or the result)."""
+    B, N, H, W = 1, 4, 8, 8
+    ws = int(L.gc_coverage_workspace_bytes())
+    assert ws % 256 == 0 and ws >= 8 * (1 << N)
+
+    def ints(*v):
+        return (ctypes.c_int32 * max(len(v), 1))(*v)
+
+    A = ints(0, 2)
+    # update: pair_bits, B, N, H, W, anchors, a, R, stale, stats
+    assert L.gc_coverage_update(None, B, N, H, W, A, 2, 2, A1, A2, None) == -1
+    assert L.gc_coverage_update(A0, B, N, H, W, ints(0, 4), 2, 2, A1, A2, None) == -1     # anchor outside [0, N)
+    assert L.gc_coverage_update(A0, B, N, H, W, ints(1, 1), 2, 2, A1, A2, None) == -1     # anchor twice
+    assert L.gc_coverage_update(A0, B, N, H, W, A, 2, 0, A1, A2, None) == -1              # R < 1
+    assert L.gc_coverage_update(A0, B, 65, H, W, A, 2, 2, A1, A2, None) == -6             # N > GC_MAX_VIEWS
+    assert L.gc_coverage_update(A0, B, N, H, W, A, 2, 2, A1, A2 + 4, None) == -4          # stats misaligned
+    assert L.gc_coverage_update(A0, B, N, H, W, A, 2, 2, A0 + 16, A2, None) == -5         # stale over the pairs
+    # selection: pair_bits, stale, B, N, H, W, a, forced, n_forced, anchors_out, workspace, ws_bytes
+    sel = lambda a=2, f=ints(), nf=0, out=A2, wsp=A3, wsb=ws: L.gc_coverage_select(A0, A1, B, N, H, W, a, f, nf,
+                                                                                     out, wsp, wsb, None)
+    assert sel(a=0) == -1
+    assert sel(f=ints(3, 3), nf=2) == -1                                                  # forced twice
+    assert sel(f=ints(4), nf=1) == -1                                                     # forced outside [0, N)
+    assert sel(nf=3) == -1                                                                # more forced than a
+    assert sel(wsb=ws - 1) == -6
+    assert sel(wsp=A3 + 8) == -4
+    assert sel(out=A3 + 16) == -5                                                         # result in the workspace
+    assert L.gc_coverage_select(A0, A1, B, 12, H, W, 9, ints(), 0, A2, A3, ws, None) == -6   # a > GC_MAX_ANCHORS
+    # scoring: pair_bits, stale, B, N, H, W, sets, M, a, scores, workspace, ws_bytes
+    S = ints(0, 1, 2, 3)
+    assert L.gc_coverage_score(A0, A1, B, N, H, W, S, 0, 2, A2, A3, ws, None) == -6       # M outside [1, 64]
+    assert L.gc_coverage_score(A0, A1, B, N, H, W, ints(0, 5, 2, 3), 2, 2, A2, A3, ws, None) == -1
+    assert L.gc_coverage_score(A0, A1, B, N, H, W, S, 2, 2, A2 + 4, A3, ws, None) == -4   # scores misaligned
+    assert L.gc_coverage_score(A0, A1, B, N, H, W, S, 2, 2, A3 + 64, A3, ws, None) == -5  # scores in the workspace
+    # fused: the update's checks, the selection's / scoring's, and stats apart from both
+    us = lambda st=A4, a_next=2, out=A2, wsp=A3: L.gc_coverage_update_select(A0, B, N, H, W, A, 2, 2, A1, st, a_next,
+                                                                            ints(), 0, out, wsp, ws, None)
+    assert us(a_next=0) == -1
+    assert us(st=A4 + 4) == -4
+    assert us(st=A3 + 256) == -5                                                          # stats in the workspace
+    assert us(st=A2) == -5                                                                # stats over the result
+    assert L.gc_coverage_update_select(A0, B, N, H, W, ints(0, 0), 2, 2, A1, A4, 2, ints(), 0, A2, A3, ws,
+                                       None) == -1
+    sc = lambda st=A4, out=A2: L.gc_coverage_update_score(A0, B, N, H, W, A, 2, 2, A1, st, S, 2, 2, out, A3, ws, None)
+    assert sc(st=A3 + 256) == -5
+    assert sc(st=A2) == -5                                                                # stats over the scores
+    assert L.gc_coverage_update_score(A0, B, N, H, W, A, 2, 0, A1, A4, S, 2, 2, A2, A3, ws, None) == -1   # R < 1
