@@ -13,6 +13,13 @@
  * bit, and x0_out(0) = x0_new(0).  The DDIM step is checked against
  * eps = (x_t - sqrt(abar_t) x0) / sqrt(1 - abar_t),
  * x_next = sqrt(abar_n) x0 + sqrt(1 - abar_n) eps in double.
+ *
+ * The same step then runs through the other launches, each bit-identical to
+ * the first: the split launch over the visible-token index (built with a
+ * workspace and without one), and the on-the-fly step over the foreground
+ * index.  Last, the coverage schedule on the same scene: each view sees all
+ * of the other's tokens, so a full step leaves no token stale and the greedy
+ * choice of one anchor is view 0 (equal gains go to the lower view).
  */
 #include <math.h>
 #include <stdio.h>
@@ -150,6 +157,92 @@ int main(void) {
       }
     }
   CHECK(max_err <= 1e-5, "x_next max error %g", max_err);
+
+  /* the split launch over the visible-token index, with and without a workspace */
+  uint32_t* d_bits;
+  int32_t *d_list, *d_nvis, *d_nvis2;
+  void* d_ws;
+  float* d_out2;
+  const size_t n_tgt = (size_t)H * W;   /* target tokens: one target view */
+  const size_t wsb = gc_index_workspace_bytes((int64_t)n_tgt);
+  HIP_OK(hipMalloc((void**)&d_bits, (n_tgt + 31) / 32 * 4));
+  HIP_OK(hipMalloc((void**)&d_list, n_tgt * 4));
+  HIP_OK(hipMalloc((void**)&d_nvis, 4));
+  HIP_OK(hipMalloc((void**)&d_nvis2, 4));
+  HIP_OK(hipMalloc(&d_ws, wsb));
+  HIP_OK(hipMalloc((void**)&d_out2, n_lat * 4 * 2));
+  float* d_next2 = d_out2 + n_lat;
+  rc = gc_index_correspondence(d_corr, 1, H, W, 1, d_bits, d_list, d_nvis, d_ws, wsb, 0);
+  CHECK(rc == GC_OK, "index rc=%d %s", rc, gc_last_error());
+  int32_t nv = 0, nv2 = 0;
+  HIP_OK(hipMemcpy(&nv, d_nvis, 4, hipMemcpyDeviceToHost));
+  CHECK(nv == H * W, "visible tokens %d, expected %d", nv, H * W);
+  rc = gc_transport_reconstruct(d_prev, d_new, d_corr, d_w, d_bits, d_list, nv, d_xt, 1, NV, H, W, C, anchors, 1, 4,
+                                GC_F32, &smp, t, tn, d_out2, d_next2, d_eps, 0);
+  CHECK(rc == GC_OK, "split launch rc=%d %s", rc, gc_last_error());
+  float *out2 = malloc(n_lat * 4 * 2), *next2 = out2 + n_lat;
+  HIP_OK(hipMemcpy(out2, d_out2, n_lat * 4 * 2, hipMemcpyDeviceToHost));
+  CHECK(memcmp(out2, out, n_lat * 4) == 0 && memcmp(next2, next, n_lat * 4) == 0, "split launch differs");
+  int32_t* list = malloc(n_tgt * 4);
+  int32_t* list2 = malloc(n_tgt * 4);
+  HIP_OK(hipMemcpy(list, d_list, n_tgt * 4, hipMemcpyDeviceToHost));
+  rc = gc_index_correspondence_noalloc(d_corr, 1, H, W, 1, d_bits, d_list, d_nvis2, 0);
+  CHECK(rc == GC_OK, "allocation-free index rc=%d %s", rc, gc_last_error());
+  HIP_OK(hipMemcpy(&nv2, d_nvis2, 4, hipMemcpyDeviceToHost));
+  HIP_OK(hipMemcpy(list2, d_list, n_tgt * 4, hipMemcpyDeviceToHost));
+  CHECK(nv2 == nv && memcmp(list, list2, (size_t)nv * 4) == 0, "allocation-free index differs");
+
+  /* the on-the-fly step over the foreground index of the position maps */
+  uint32_t* d_fgb;
+  int32_t *d_rec, *d_nfg;
+  void* d_ws2;
+  const size_t wsb2 = gc_index_workspace_bytes((int64_t)n_tok);
+  HIP_OK(hipMalloc((void**)&d_fgb, (n_tok + 31) / 32 * 4));
+  HIP_OK(hipMalloc((void**)&d_rec, n_tok * 16));
+  HIP_OK(hipMalloc((void**)&d_nfg, 4));
+  HIP_OK(hipMalloc(&d_ws2, wsb2));
+  rc = gc_index_foreground(d_pos, NV, H, W, d_fgb, d_rec, d_nfg, d_ws2, wsb2, 0);
+  CHECK(rc == GC_OK, "foreground index rc=%d %s", rc, gc_last_error());
+  int32_t nfg = 0;
+  HIP_OK(hipMemcpy(&nfg, d_nfg, 4, hipMemcpyDeviceToHost));
+  CHECK(nfg == (int32_t)n_tok, "foreground tokens %d, expected %zu", nfg, n_tok);
+  rc = gc_transport_reconstruct_geom(d_prev, d_new, d_pos, d_cams, d_bbox, d_fgb, d_rec, nfg, d_xt, 1, NV, H, W, C,
+                                     anchors, 1, 4, GC_F32, &smp, t, tn, d_out2, d_next2, d_eps, 0);
+  CHECK(rc == GC_OK, "on-the-fly step rc=%d %s", rc, gc_last_error());
+  HIP_OK(hipMemcpy(out2, d_out2, n_lat * 4 * 2, hipMemcpyDeviceToHost));
+  CHECK(memcmp(out2, out, n_lat * 4) == 0 && memcmp(next2, next, n_lat * 4) == 0, "on-the-fly step differs");
+
+  /* the coverage schedule: pairs, staleness, a full step fused with the next choice */
+  uint32_t *d_pairs, *d_stats;
+  uint8_t* d_stale;
+  int32_t* d_sel;
+  void* d_cws;
+  const size_t npw = (size_t)gc_coverage_pair_words(1, NV, H, W), cwsb = gc_coverage_workspace_bytes();
+  HIP_OK(hipMalloc((void**)&d_pairs, npw * 4));
+  HIP_OK(hipMalloc((void**)&d_stats, (size_t)NV * 16));
+  HIP_OK(hipMalloc((void**)&d_stale, n_tok));
+  HIP_OK(hipMalloc((void**)&d_sel, 4));
+  HIP_OK(hipMalloc(&d_cws, cwsb));
+  rc = gc_coverage_pairs(d_pos, d_cams, d_bbox, 1, NV, H, W, d_pairs, 0);
+  CHECK(rc == GC_OK, "pairs rc=%d %s", rc, gc_last_error());
+  rc = gc_coverage_init(d_pos, 1, NV, H, W, d_stale, 0);
+  CHECK(rc == GC_OK, "staleness init rc=%d %s", rc, gc_last_error());
+  const int32_t all_views[NV] = {0, 1};
+  rc = gc_coverage_update_select(d_pairs, 1, NV, H, W, all_views, NV, 2, d_stale, d_stats, 1, NULL, 0, d_sel, d_cws,
+                                 cwsb, 0);
+  CHECK(rc == GC_OK, "update + select rc=%d %s", rc, gc_last_error());
+  uint32_t stats[NV * 4];
+  int32_t chosen = -1;
+  HIP_OK(hipMemcpy(stats, d_stats, sizeof stats, hipMemcpyDeviceToHost));
+  HIP_OK(hipMemcpy(&chosen, d_sel, 4, hipMemcpyDeviceToHost));
+  for (int v = 0; v < NV; ++v)
+    CHECK(stats[v * 4] == H * W && stats[v * 4 + 1] == 0 && stats[v * 4 + 2] == 0 && stats[v * 4 + 3] == 0,
+          "statistics of view %d: %u %u %u %u", v, stats[v * 4], stats[v * 4 + 1], stats[v * 4 + 2], stats[v * 4 + 3]);
+  CHECK(chosen == 0, "greedy anchor %d, expected 0", chosen);
+  hipFree(d_bits); hipFree(d_list); hipFree(d_nvis); hipFree(d_nvis2); hipFree(d_ws); hipFree(d_out2);
+  hipFree(d_fgb); hipFree(d_rec); hipFree(d_nfg); hipFree(d_ws2);
+  hipFree(d_pairs); hipFree(d_stats); hipFree(d_stale); hipFree(d_sel); hipFree(d_cws);
+  free(out2); free(list); free(list2);
 
   /* argument errors: negative code, a message, nothing launched */
   rc = gc_transport_step(d_prev, d_new, d_corr, d_w, NULL, NULL, 0, 1, NV, H, W, C, anchors, 1, 5, GC_F32, d_out, 0);

@@ -2,7 +2,11 @@
 with hipMalloc, runs one cached step through the library and checks it
 against closed forms -- a duplicate anchor view transports the increment
 exactly (Eq. 1 with a single tap of weight 1), the DDIM step matches its
-formula -- and that argument errors return negative codes."""
+formula; the split launch over the visible-token index (with a workspace
+and allocation-free) and the on-the-fly step over the foreground index give
+the same bits; the coverage schedule's fused update + selection leaves no
+token stale and picks view 0 -- and that argument errors return negative
+codes."""
 import os
 import subprocess
 
