@@ -18,6 +18,11 @@ void clear_error();
 // Map the launch status (hipGetLastError) and, with GC_SYNC_CHECK=1, the
 // stream's completion status to GC_OK / GC_ERR_HIP.
 int after_launch(hipStream_t stream, const char* what);
+// Work items (target tokens x channel vectors) from which a per-step call
+// given a visible-token index takes the split launch; smaller steps take the
+// dense launch, whose per-token chain has one dependent load fewer (the same
+// result bit for bit).  GC_SPLIT_MIN_ITEMS overrides the default 2^18.
+int64_t split_min_items();
 
 inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 

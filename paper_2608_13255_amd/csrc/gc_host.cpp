@@ -22,6 +22,17 @@ bool sync_check_enabled() {
 }
 }  // namespace
 
+int64_t split_min_items() {
+  static const int64_t n = [] {
+    const char* e = std::getenv("GC_SPLIT_MIN_ITEMS");
+    if (!e || !e[0]) return (int64_t)1 << 18;
+    char* end = nullptr;
+    const long long v = std::strtoll(e, &end, 10);
+    return (end && *end == '\0' && v >= 0) ? (int64_t)v : (int64_t)1 << 18;
+  }();
+  return n;
+}
+
 int fail(int code, const char* fmt, ...) {
   va_list ap;
   va_start(ap, fmt);

@@ -373,6 +373,14 @@ int prepare_transport(const void* x0_prev, const void* x0_new, const int32_t* co
     g->gblocks = (int)gblocks;
     if ((int64_t)g->gblocks + nb > (int64_t)0x7fffffff - kXcds)
       return fail(GC_ERR_CAPACITY, "%s: problem too large for one launch", who);
+    // a small step takes the dense launch: the list's extra dependent load
+    // does not pay there (checked above all the same; same result bit for bit)
+    if (g->n_tokens * g->CV < split_min_items()) {
+      g->vis_bits = nullptr;
+      g->vis_list = nullptr;
+      g->n_vis = 0;
+      g->gblocks = 0;
+    }
   }
   int sorted[GC_MAX_ANCHORS];
   for (int s = 0; s < a; ++s) sorted[s] = anchors[s];

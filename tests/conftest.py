@@ -5,6 +5,11 @@ import sys
 import numpy as np
 import pytest
 
+# Steps given a visible-token index take the split launch at every size here
+# (the library takes the plain launch below 2^18 work items by default), so
+# the small parity cases exercise it; set before the library is loaded.
+os.environ.setdefault("GC_SPLIT_MIN_ITEMS", "0")
+
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
