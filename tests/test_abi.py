@@ -106,6 +106,31 @@ def test_transport_validation(gc, L):
     assert call(bits=A5 + 4, lst=A5 + 4096, nv=3) == -4
 
 
+def test_index_checked_below_the_split_bound():
+    """A step smaller than the split launch's bound (2^18 work items by
+    default) takes the plain launch, but its index is still validated on the
+    host: run in a process that keeps the library's default bound (the test
+    suite lowers it to 0)."""
+    code = f"""
+import ctypes
+L = ctypes.CDLL({LIBSO!r})
+L.gc_last_error.restype = ctypes.c_char_p
+anchors = (ctypes.c_int32 * 2)(0, 3)
+def call(bits, lst, nv):
+    return L.gc_transport_step(ctypes.c_void_p({A0}), ctypes.c_void_p({A1}), ctypes.c_void_p({A2}),
+                               ctypes.c_void_p({A3}), ctypes.c_void_p(bits), ctypes.c_void_p(lst),
+                               ctypes.c_int64(nv), 1, 6, 8, 8, 16, anchors, 2, 4, 1, ctypes.c_void_p({A4}), None)
+assert call({A5}, None, 0) == -1, L.gc_last_error()
+assert call({A5}, {A5} + 4096, -1) == -1, L.gc_last_error()
+assert call({A5}, {A5} + 4096, 1 * 4 * 64 + 1) == -1, L.gc_last_error()
+assert call({A5} + 4, {A5} + 4096, 3) == -4, L.gc_last_error()
+print("index checked")
+"""
+    env = {k: v for k, v in os.environ.items() if k != "GC_SPLIT_MIN_ITEMS"}
+    r = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, env=env, timeout=120)
+    assert r.returncode == 0 and "index checked" in r.stdout, r.stdout + r.stderr
+
+
 def test_fused_validation(gc, L):
     anchors = (ctypes.c_int32 * 2)(0, 3)
     smp = gc.Sampler(kind=gc.GC_FLOW_EULER).c()
