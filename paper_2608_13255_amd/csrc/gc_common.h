@@ -60,4 +60,19 @@ __device__ __forceinline__ uint32_t f_to_bf16_bits(float f) {
   return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
 }
 
+// Two floats to a pair of bfloat16 (lo in the low half) with the hardware's
+// conversion, which rounds to nearest even exactly as f_to_bf16_bits does
+// for every non-NaN float; a NaN becomes the quiet NaN 0x7fc0, as there.
+__device__ __forceinline__ uint32_t f2_to_bf16x2_bits(float lo, float hi) {
+  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+  bf16x2 v;
+  v.x = (__bf16)lo;
+  v.y = (__bf16)hi;
+  uint32_t r;
+  __builtin_memcpy(&r, &v, 4);
+  if (lo != lo) r = (r & 0xffff0000u) | 0x7fc0u;
+  if (hi != hi) r = (r & 0x0000ffffu) | 0x7fc00000u;
+  return r;
+}
+
 }  // namespace gc

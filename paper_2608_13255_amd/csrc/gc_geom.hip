@@ -146,6 +146,52 @@ __device__ __forceinline__ void finish_item(const GArgs& g, int64_t e, const typ
   }
 }
 
+// Eq. 1's sum for one (token, channel vector c) of asset b: the anchors'
+// (new - previous) x0 at the kept taps of each slot's word, in ascending slot
+// and tap order, each weighted by the builder's stored weight w_k / n_vis
+// (words and w_k as the selection left them in LDS).  A slot's taps lie 0,
+// 1, W and W + 1 tokens from its footprint's top-left tap, so only that tap's
+// address is computed per slot; dividing by a power-of-two n_vis is
+// multiplying by its exact reciprocal.
+template <int DT, int VEC>
+__device__ __forceinline__ void gather_delta(const GArgs& g, int b, int c, const int32_t* words, const float* wk,
+                                             int n_vis, float (&acc)[VEC]) {
+  using CD = Codec<DT, VEC>;
+  using Raw = typename CD::Raw;
+  constexpr int kEs = DT == GC_F32 ? 4 : 2;
+  const float inv = (float)n_vis;
+  const bool pow2 = (n_vis & (n_vis - 1)) == 0;
+  const float rcp = __builtin_ldexpf(1.0f, -__builtin_ctz((unsigned)n_vis));
+  const int64_t tb = (int64_t)g.C * kEs;   // bytes per token
+  const int64_t dk[4] = {0, tb, (int64_t)g.W * tb, (int64_t)(g.W + 1) * tb};
+  const char* nb = static_cast<const char*>(g.x0_new) + (int64_t)c * VEC * kEs;
+  const char* ob = static_cast<const char*>(g.x0_prev) + (int64_t)c * VEC * kEs;
+#pragma unroll
+  for (int q = 0; q < VEC; ++q) acc[q] = 0.0f;
+  for (int s = 0; s < g.a; ++s) {
+    const uint32_t w = (uint32_t)words[s];
+    if (!w) continue;
+    const int x0 = (int)(w & 0xfffu) - 1;
+    const int y0 = (int)((w >> 12) & 0xfffu) - 1;
+    const uint32_t mask = (w >> 24) & 0xfu;
+    const int64_t pix = (int64_t)y0 * g.W + x0;   // may lie off the grid; only kept taps are read
+    const char* pn = nb + (((int64_t)b * g.a + s) * g.HW + pix) * tb;
+    const char* po = ob + (((int64_t)b * g.N + g.anchor_view[s]) * g.HW + pix) * tb;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      if (!(mask & (1u << k))) continue;
+      const Raw nr = CD::load(pn + dk[k], 0);
+      const Raw orr = CD::load(po + dk[k], 0);
+      const float wt = pow2 ? wk[s * 4 + k] * rcp : wk[s * 4 + k] / inv;
+      float nf[VEC], of[VEC];
+      CD::unpack(nr, nf);
+      CD::unpack(orr, of);
+#pragma unroll
+      for (int q = 0; q < VEC; ++q) acc[q] = acc[q] + wt * (nf[q] - of[q]);
+    }
+  }
+}
+
 // G lanes per target token; AMAX (4 or 8) bounds the anchor count, so each
 // lane evaluates up to AMAX / G anchor slots.
 template <int DT, int VEC, int MODE, int G, int AMAX>
@@ -317,30 +363,8 @@ __global__ __launch_bounds__(kBlock) void k_transport_geom(GArgs g) {
     sd.m1 = prevr;   // m_{k-1}: the token's own stored x0
     Raw x0r;
     if (slot < nv) {
-      const float inv = (float)s_nvis[slot];
       float acc[VEC];
-#pragma unroll
-      for (int q = 0; q < VEC; ++q) acc[q] = 0.0f;
-      for (int s = 0; s < g.a; ++s) {   // ascending slots, as the stored operator sums
-        const uint32_t w = (uint32_t)s_word[slot][s];
-        if (!w) continue;
-        const int x0 = (int)(w & 0xfffu) - 1;
-        const int y0 = (int)((w >> 12) & 0xfffu) - 1;
-        const uint32_t mask = (w >> 24) & 0xfu;
-        const int64_t new_view = ((int64_t)b * g.a + s) * g.HW;
-        const int64_t old_view = ((int64_t)b * g.N + g.anchor_view[s]) * g.HW;
-#pragma unroll
-        for (int k = 0; k < 4; ++k) {
-          if (!(mask & (1u << k))) continue;
-          const int qq = (y0 + (k >> 1)) * g.W + x0 + (k & 1);
-          const float wt = s_wk[slot][s * 4 + k] / inv;   // the builder's stored weight
-          float nf[VEC], of[VEC];
-          CD::unpack(CD::load(g.x0_new, (new_view + qq) * g.C + (int64_t)c * VEC), nf);
-          CD::unpack(CD::load(g.x0_prev, (old_view + qq) * g.C + (int64_t)c * VEC), of);
-#pragma unroll
-          for (int q2 = 0; q2 < VEC; ++q2) acc[q2] = acc[q2] + wt * (nf[q2] - of[q2]);
-        }
-      }
+      gather_delta<DT, VEC>(g, b, c, s_word[slot], s_wk[slot], s_nvis[slot], acc);
       float prevf[VEC], y[VEC];
       CD::unpack(prevr, prevf);
 #pragma unroll
@@ -521,30 +545,8 @@ __global__ __launch_bounds__(kBlock) void k_transport_geom_fg(GArgs g) {
     sd.m1 = prevr;   // m_{k-1}: the token's own stored x0
     Raw x0r;
     if (n_vis > 0) {
-      const float inv = (float)n_vis;
       float acc[VEC];
-#pragma unroll
-      for (int q = 0; q < VEC; ++q) acc[q] = 0.0f;
-      for (int s = 0; s < g.a; ++s) {   // ascending slots, as the stored operator sums
-        const uint32_t w = (uint32_t)s_word[rl][s];
-        if (!w) continue;
-        const int x0 = (int)(w & 0xfffu) - 1;
-        const int y0 = (int)((w >> 12) & 0xfffu) - 1;
-        const uint32_t mask = (w >> 24) & 0xfu;
-        const int64_t new_view = ((int64_t)b * g.a + s) * g.HW;
-        const int64_t old_view = ((int64_t)b * g.N + g.anchor_view[s]) * g.HW;
-#pragma unroll
-        for (int k = 0; k < 4; ++k) {
-          if (!(mask & (1u << k))) continue;
-          const int qq = (y0 + (k >> 1)) * g.W + x0 + (k & 1);
-          const float wt = s_wk[rl][s * 4 + k] / inv;   // the builder's stored weight
-          float nf[VEC], of[VEC];
-          CD::unpack(CD::load(g.x0_new, (new_view + qq) * g.C + (int64_t)c * VEC), nf);
-          CD::unpack(CD::load(g.x0_prev, (old_view + qq) * g.C + (int64_t)c * VEC), of);
-#pragma unroll
-          for (int q2 = 0; q2 < VEC; ++q2) acc[q2] = acc[q2] + wt * (nf[q2] - of[q2]);
-        }
-      }
+      gather_delta<DT, VEC>(g, b, c, s_word[rl], s_wk[rl], n_vis, acc);
       float prevf[VEC], y[VEC];
       CD::unpack(prevr, prevf);
 #pragma unroll

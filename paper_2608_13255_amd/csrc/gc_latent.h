@@ -65,7 +65,7 @@ template <int DT, int VEC> struct Codec {
       for (int e = 0; e < VEC; ++e) w[e] = __float_as_uint(f[e]);
     } else {
 #pragma unroll
-      for (int e = 0; e < VEC / 2; ++e) w[e] = f_to_bf16_bits(f[2 * e]) | (f_to_bf16_bits(f[2 * e + 1]) << 16);
+      for (int e = 0; e < VEC / 2; ++e) w[e] = f2_to_bf16x2_bits(f[2 * e], f[2 * e + 1]);
     }
     return r;
   }

@@ -361,6 +361,41 @@ def test_nan_latents_propagate(gc):
     assert np.abs(got[fin] - ex[fin]).max() <= 1e-5
 
 
+@pytest.mark.parametrize("name", ["syncmvd", "stress"])
+def test_bf16_nan_outputs_are_canonical(gc, name):
+    """bfloat16 values the step computes from a NaN are stored as the quiet
+    NaN 0x7fc0, whatever the sign and payload of the NaN they came from (the
+    storage rounding rule), while a value the step only copies -- an anchor
+    row, a token no anchor sees -- keeps its input bits; 4- and 8-element
+    channel vectors."""
+    w = C4 if name == "syncmvd" else synth.shrink(C5, B=1)
+    P = latent_maps(w.name) if name == "syncmvd" else latent_maps(C5.name, B=1)
+    A = anchors_of(w, 0)
+    x0_prev, x0_new, x_t = latents(w, P, A, 2)
+    rs = np.random.default_rng(7)
+    nans = np.array([0x7FC0, 0xFFC0, 0x7F81, 0xFFC1, 0x7FFF, 0xFF80, 0x7F80], np.uint16)
+    for arr, frac in ((x0_prev, 0.02), (x0_new, 0.01), (x_t, 0.01)):
+        flat = arr.reshape(-1)
+        at = rs.random(flat.size) < frac
+        flat[at] = nans[rs.integers(0, nans.size, int(at.sum()))]
+    corr_o, wts_o, nvis_o = oracle.build(P, synth.batch_cameras(w), A, w.K, oracle.bbox(P, w.tol_frac))
+    _, x0_state = oracle.transport(x0_prev, x0_new, corr_o, wts_o, A, "bf16")
+    t, tn = step_of(w, 2)
+    pred = "eps" if w.sampler == "ddim" else "vel"
+    xn_o, _ = oracle.reconstruct(x_t, x0_state, "bf16", w.sampler, t, tn, pred=pred)
+    corr, wts = _gpu_build(gc, w, P, A, w.K)
+    x0_out, xn, _ = gc.gc_transport_reconstruct(to_dev(x0_prev, "bf16"), to_dev(x0_new, "bf16"), corr, wts,
+                                                to_dev(x_t, "bf16"), A, sampler_of(gc, w), t, tn)
+    for got, ex in ((to_host(x0_out, "bf16"), x0_state), (to_host(xn, "bf16"), oracle.store(xn_o, "bf16"))):
+        special = np.isnan(synth.values(ex, "bf16")) | np.isinf(synth.values(ex, "bf16"))
+        assert special.any()
+        np.testing.assert_array_equal(got[special], ex[special])
+        np.testing.assert_array_equal(np.isnan(synth.values(got, "bf16")), np.isnan(synth.values(ex, "bf16")))
+    # both kinds occur: computed NaNs (canonical) and copied payloads
+    st = x0_state.reshape(-1)
+    assert (st == 0x7FC0).any() and np.isin(st, [0xFFC0, 0x7F81, 0xFFC1, 0x7FFF]).any()
+
+
 def test_all_views_anchor_is_plain_sampler_step(gc):
     """a = N: the cached step reduces exactly to the plain sampler step."""
     w = synth.shrink(C2, dtype="bf16")
