@@ -21,7 +21,9 @@
 // over all rows follow in the hardware's round-robin order and skip the
 // visible tokens by their bit.  Data each thread touches once (its own
 // x0_prev and x_t, every output) is read and written with nontemporal hints;
-// only the gathered anchor tiles go through L2 normally.
+// the gathered anchor tiles, and an anchor row's own inputs that the gathers
+// also read (its new prediction, its x0_prev for UniPC), go through L2
+// normally.
 #include "gc_common.h"
 #include "gc_latent.h"
 
@@ -81,7 +83,9 @@ __device__ __forceinline__ void token_step(const TArgs& g, int b, int p, int cv,
   if constexpr (MODE == kUniPC) {
     xtr = CD::load_stream(g.u.corr ? g.x_prev : g.x_t, base);
     if (g.u.need_m2) m2r = CD::load_stream(g.m_km2, base);
-    if (g.u.need_m1 && mode == kAnchorRow) m1r = CD::load_stream(g.x0_prev, base);
+    // an anchor row's own x0_prev is also gathered by the target tokens that
+    // see it: a cached load (measured faster than a nontemporal one)
+    if (g.u.need_m1 && mode == kAnchorRow) m1r = CD::load(g.x0_prev, base);
   }
   Raw x0r;
   float x0f[VEC];
