@@ -77,12 +77,15 @@ struct TapPos {
 };
 
 __device__ __forceinline__ TapPos anchor_tap_positions(const AnchorProj& pj, const float* src, int H, int W) {
+  // a view has fewer than 2^24 pixels, so the offsets within it are 32-bit
+  const uint32_t xa = (uint32_t)min(max(pj.x0, 0), W - 1), xb = (uint32_t)min(max(pj.x0 + 1, 0), W - 1);
+  const uint32_t ra = (uint32_t)min(max(pj.y0, 0), H - 1) * (uint32_t)W;
+  const uint32_t rb = (uint32_t)min(max(pj.y0 + 1, 0), H - 1) * (uint32_t)W;
+  const uint32_t px[4] = {ra + xa, ra + xb, rb + xa, rb + xb};
   TapPos t;
 #pragma unroll
   for (int k = 0; k < 4; ++k) {
-    const int x = min(max(pj.x0 + (k & 1), 0), W - 1);
-    const int y = min(max(pj.y0 + (k >> 1), 0), H - 1);
-    const float* Q = src + ((int64_t)y * W + x) * 3;
+    const float* Q = src + px[k] * 3u;
     t.q[k][0] = Q[0];
     t.q[k][1] = Q[1];
     t.q[k][2] = Q[2];
