@@ -11,6 +11,7 @@ values):
 Every workload runs at its full size.
 """
 import math
+import os
 
 import numpy as np
 import pytest
@@ -495,6 +496,61 @@ def test_split_launch_equals_dense_and_oracle(gc, w):
     assert torch.equal(s_[0].view(iv), x0_s.view(iv))
     xn = synth.values(to_host(s_[1], w.dtype), w.dtype).astype(np.float64)
     assert np.abs(xn - o["xn"]).max() <= TOL[w.dtype]
+
+
+_DEFAULT_BOUND_CHILD = """
+import sys, numpy as np, torch
+sys.path.insert(0, sys.argv[1])
+import paper_2608_13255_amd as gc
+d = np.load(sys.argv[2])
+dev = torch.device("cuda:0")
+t = lambda a: torch.from_numpy(a).to(dev)
+bf = lambda a: t(a.view(np.int16)).view(torch.bfloat16)
+pos, cams, bbox = t(d["pos"]), t(d["cams"]), t(d["bbox"])
+A = [int(v) for v in d["A"]]
+corr, wts = gc.gc_build_correspondence(pos, cams, A, int(d["K"]), bbox)
+idx = gc.gc_index_correspondence(corr)
+smp = gc.Sampler(kind=gc.GC_DDIM, pred_out=gc.GC_PRED_EPS)
+x0, xn, mo = gc.gc_transport_reconstruct(bf(d["prev"]), bf(d["new"]), corr, wts, bf(d["xt"]), A, smp,
+                                         float(d["t"]), float(d["tn"]), index=idx)
+np.savez(sys.argv[3], x0=x0.view(torch.int16).cpu().numpy(), xn=xn.view(torch.int16).cpu().numpy(),
+         mo=mo.view(torch.int16).cpu().numpy())
+"""
+
+
+def test_default_split_bound_is_bit_identical(gc, tmp_path):
+    """With the library's default bound a step this small takes the plain
+    launch although it is given the index (run in a fresh process that keeps
+    the default); its outputs equal the split launch's (this process, bound
+    0) bit for bit."""
+    import subprocess
+    import sys
+    w = C4
+    assert w.B * w.N * w.H * w.W * (w.C // 4) < 2 ** 18 and w.sampler == "ddim"
+    P = latent_maps(w.name)
+    A = anchors_of(w, 1)
+    x0_prev, x0_new, x_t = latents(w, P, A, 4)
+    t, tn = step_of(w, 4)
+    Pd = torch.from_numpy(P).to(DEV)
+    cams = gc.camera_tensor(synth.batch_cameras(w), DEV)
+    bbox = gc.gc_posmap_bbox(Pd, w.tol_frac)
+    inp = tmp_path / "in.npz"
+    np.savez(inp, pos=P, cams=cams.cpu().numpy(), bbox=bbox.cpu().numpy(), A=np.array(A), K=w.K, prev=x0_prev,
+             new=x0_new, xt=x_t, t=t, tn=tn)
+    out = tmp_path / "out.npz"
+    env = {k: v for k, v in os.environ.items() if k != "GC_SPLIT_MIN_ITEMS"}
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    r = subprocess.run([sys.executable, "-c", _DEFAULT_BOUND_CHILD, root, str(inp), str(out)], env=env,
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode == 0, r.stdout + r.stderr
+    child = np.load(out)
+    corr, wts = gc.gc_build_correspondence(Pd, cams, A, w.K, bbox)
+    idx = gc.gc_index_correspondence(corr)
+    assert idx.n_vis > 0
+    x0, xn, mo = gc.gc_transport_reconstruct(to_dev(x0_prev, "bf16"), to_dev(x0_new, "bf16"), corr, wts,
+                                             to_dev(x_t, "bf16"), A, sampler_of(gc, w), t, tn, index=idx)
+    for name, got in (("x0", x0), ("xn", xn), ("mo", mo)):
+        np.testing.assert_array_equal(got.view(torch.int16).cpu().numpy(), child[name])
 
 
 def test_split_launch_without_visible_tokens(gc):
