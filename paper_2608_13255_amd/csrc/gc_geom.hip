@@ -268,12 +268,17 @@ __global__ __launch_bounds__(kBlock) void k_transport_geom(GArgs g) {
   AnchorProj pj[kApl];
   AnchorTaps at[kApl];
   bool any_ok = false;
+  if (__ballot(fg)) {   // a wave of background tokens projects nothing
 #pragma unroll
-  for (int j = 0; j < kApl; ++j) {   // branch-free: a lane without the slot keeps the result unused
-    const int s = j * G + lane_g;
-    pj[j] = anchor_project(P, cam_lds[s < g.a ? s : 0], g.H, g.W);
-    pj[j].ok = pj[j].ok && tok_ok && fg && s < g.a;
-    any_ok = any_ok || pj[j].ok;
+    for (int j = 0; j < kApl; ++j) {   // branch-free: a lane without the slot keeps the result unused
+      const int s = j * G + lane_g;
+      pj[j] = anchor_project(P, cam_lds[s < g.a ? s : 0], g.H, g.W);
+      pj[j].ok = pj[j].ok && tok_ok && fg && s < g.a;
+      any_ok = any_ok || pj[j].ok;
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < kApl; ++j) pj[j] = AnchorProj{false, 0, 0, 0.0f, 0.0f};
   }
   if (__ballot(any_ok)) {
     TapPos tp[kApl];
@@ -460,12 +465,17 @@ __global__ __launch_bounds__(kBlock) void k_transport_geom_fg(GArgs g) {
   AnchorProj pj[kApl];
   AnchorTaps at[kApl];
   bool any_ok = false;
+  if (__ballot(fg)) {   // a wave of anchor-view records projects nothing
 #pragma unroll
-  for (int j = 0; j < kApl; ++j) {   // branch-free: a lane without the slot keeps the result unused
-    const int s = j * G + lane_g;
-    pj[j] = anchor_project(P, cam_lds[b * g.a + (s < g.a ? s : 0)], g.H, g.W);
-    pj[j].ok = pj[j].ok && fg && s < g.a;
-    any_ok = any_ok || pj[j].ok;
+    for (int j = 0; j < kApl; ++j) {   // branch-free: a lane without the slot keeps the result unused
+      const int s = j * G + lane_g;
+      pj[j] = anchor_project(P, cam_lds[b * g.a + (s < g.a ? s : 0)], g.H, g.W);
+      pj[j].ok = pj[j].ok && fg && s < g.a;
+      any_ok = any_ok || pj[j].ok;
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < kApl; ++j) pj[j] = AnchorProj{false, 0, 0, 0.0f, 0.0f};
   }
   const bool loaded = __ballot(any_ok) != 0ull;
   TapPos tp[kApl];
