@@ -425,16 +425,24 @@ def main():
     rows["step_us_one_buffer_set"] = r0.elapsed_time(r1) / args.steps * 1e3
 
     # ---- unfused pair and full step, for the record -------------------------
-    def timed(fn, n=20):
-        fn()
-        torch.cuda.synchronize()
-        s, e = ev(), ev()
-        s.record()
-        for _ in range(n):
+    def timed(fn, n=40, batches=7, warm=200):
+        # the same call back to back first (about 10 ms of device work), so
+        # that the clocks have left the host-side setup's idle state; then the
+        # median over batches of n back-to-back calls, each batch between its
+        # own pair of events
+        for _ in range(warm):
             fn()
-        e.record()
         torch.cuda.synchronize()
-        return s.elapsed_time(e) / n
+        per = []
+        for _ in range(batches):
+            s, e = ev(), ev()
+            s.record()
+            for _ in range(n):
+                fn()
+            e.record()
+            torch.cuda.synchronize()
+            per.append(s.elapsed_time(e) / n)
+        return float(np.median(per))
 
     A0 = list(anchor_sets[0])
     corr0, wts0 = ops[anchor_sets[0]]
