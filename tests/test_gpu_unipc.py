@@ -63,6 +63,52 @@ def test_unipc_update_parity(gc, dtype, order, corrector):
         assert np.abs(vals(xn, dtype) - xn_o).max() <= TOL[dtype], k
 
 
+@pytest.mark.parametrize("name", ["syncmvd", "stress"])
+def test_unipc_bf16_nan_outputs_are_canonical(gc, name):
+    """The fused UniPC step, stored operator (plain and split launch) and on
+    the fly: bfloat16 values it computes from a NaN are the quiet NaN 0x7fc0
+    whatever the sign and payload of the NaN they came from, values it only
+    copies keep their bits; 4- and 8-element channel vectors."""
+    w = C4 if name == "syncmvd" else synth.shrink(C5, B=1)
+    P = latent_maps(C4.name) if name == "syncmvd" else latent_maps(C5.name, B=1)
+    A = oracle.anchors(w.N, w.a, 1)
+    S, k = 10, 4
+    rs = np.random.default_rng(11)
+    shape = (w.B, w.N, w.H, w.W, w.C)
+    x_prev, m2, m1 = (synth.storage(0.5 * rs.standard_normal(shape).astype(np.float32), "bf16") for _ in range(3))
+    new = synth.storage(0.5 * rs.standard_normal((w.B, w.a) + shape[2:]).astype(np.float32), "bf16")
+    nans = np.array([0x7FC0, 0xFFC0, 0x7F81, 0xFFC1, 0x7FFF, 0xFF80, 0x7F80], np.uint16)
+    for arr, frac in ((m1, 0.02), (new, 0.01), (x_prev, 0.01), (m2, 0.01)):
+        flat = arr.reshape(-1)
+        at = rs.random(flat.size) < frac
+        flat[at] = nans[rs.integers(0, nans.size, int(at.sum()))]
+    cams_np = synth.batch_cameras(w)
+    corr_o, wts_o, _ = oracle.build(P, cams_np, A, w.K, oracle.bbox(P, w.tol_frac))
+    _, mk_state = oracle.transport(m1, new, corr_o, wts_o, A, "bf16")
+    co = oracle.unipc_coeffs(S, k, 2, True)
+    xc_o, xn_o = oracle.unipc_apply(co, None, x_prev, m2, m1, mk_state, "bf16")
+    ex = [mk_state, oracle.store(xc_o, "bf16"), oracle.store(xn_o, "bf16")]
+    Pd = torch.from_numpy(P).to(DEV)
+    cams = gc.camera_tensor(cams_np, DEV)
+    bbox = gc.gc_posmap_bbox(Pd, w.tol_frac)
+    corr, wts = gc.gc_build_correspondence(Pd, cams, A, w.K, bbox)
+    st = gc.gc_unipc_coeffs(gc.Sampler(kind=gc.GC_DDIM), S, k, 2, True)
+    d = [to_dev(a_, "bf16") for a_ in (m1, new, x_prev, m2)]
+    runs = [gc.gc_transport_unipc(d[0], d[1], corr, wts, A, st, x_prev=d[2], m_km2=d[3], index=index)
+            for index in (None, gc.gc_index_correspondence(corr))]
+    runs.append(gc.gc_transport_unipc_geom(d[0], d[1], Pd, cams, bbox, A, w.K, st, x_prev=d[2], m_km2=d[3],
+                                           fg_index=gc.gc_index_foreground(Pd)))
+    for outs in runs:
+        for got_t, e in zip(outs, ex):
+            got = to_host(got_t, "bf16")
+            ev = synth.values(e, "bf16")
+            special = np.isnan(ev) | np.isinf(ev)
+            assert special.any()
+            np.testing.assert_array_equal(got[special], e[special])
+            np.testing.assert_array_equal(np.isnan(synth.values(got, "bf16")), np.isnan(ev))
+    assert (mk_state == 0x7FC0).any() and np.isin(mk_state, [0xFFC0, 0x7F81, 0xFFC1, 0x7FFF]).any()
+
+
 @pytest.mark.parametrize("w", [C2, C4, C5], ids=lambda w: w.name)
 def test_transport_unipc_parity(gc, w):
     P = latent_maps(w.name)
