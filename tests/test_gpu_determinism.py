@@ -151,6 +151,17 @@ def test_coverage_kernels(gc, setup):
             sc = filled(None, r, (len(rot),), torch.int64)
             gc.gc_coverage_score(pairs, stale, rot, out=sc, workspace=ws)
             o += [st, sel, sc]
+        # the fused update + selection / scoring (one pass with a last-block ticket)
+        for step in range(6, 12):
+            st = filled(None, r, (B, N, 4), torch.int32)
+            sel = filled(None, r, (w.a,), torch.int32)
+            gc.gc_coverage_update_select(pairs, stale, gc.gc_schedule_anchors(N, w.a, step), 2, w.a,
+                                         forced=[step % N], stats=st, out=sel, workspace=ws)
+            st2 = filled(None, r, (B, N, 4), torch.int32)
+            sc = filled(None, r, (len(rot),), torch.int64)
+            gc.gc_coverage_update_score(pairs, stale, gc.gc_schedule_anchors(N, w.a, step + 1), 2, rot, stats=st2,
+                                        out=sc, workspace=ws)
+            o += [st, sel, st2, sc]
         o.append(stale)
         outs.append(o)
     same(outs)
