@@ -30,6 +30,8 @@ new = torch.randn((1, 2, 64, 64, 4), generator=g).cuda()
 xt = torch.randn((1, 6, 64, 64, 4), generator=g).cuda()
 smp = gc.Sampler(kind=gc.GC_DDIM, pred_out=gc.GC_PRED_EPS)
 outs = list(gc.gc_transport_reconstruct(prev, new, corr, wts, xt, A, smp, 700, 660, index=idx))
+outs += list(gc.gc_transport_unipc(prev, new, corr, wts, A, gc.gc_unipc_coeffs(gc.Sampler(kind=gc.GC_DDIM), 10, 4, 2, True),
+                                   x_prev=xt, m_km2=prev, index=idx))
 outs += list(gc.gc_transport_reconstruct_geom(prev, new, P, cams, bb, xt, A, 4, smp, 700, 660))
 fgi = gc.gc_index_foreground(P)
 outs += list(gc.gc_transport_reconstruct_geom(prev, new, P, cams, bb, xt, A, 4, smp, 700, 660, fg_index=fgi))
@@ -42,7 +44,9 @@ stats = gc.gc_coverage_update(pairs, stale, A, 2)
 sel = gc.gc_coverage_select(pairs, stale, 2)
 st = gc.gc_unipc_coeffs(gc.Sampler(kind=gc.GC_DDIM), 10, 3, 2, True)
 xc, xn = gc.gc_unipc_update(st, outs[0], x_prev=xt, m_km2=prev, m_km1=prev)
-outs += [xc, xn, stats, sel]
+stats2, sel2 = gc.gc_coverage_update_select(pairs, stale, sel.tolist(), 2, 2, forced=[1])
+stats3, sc3 = gc.gc_coverage_update_score(pairs, stale, sel2.tolist(), 2, [[0, 3], [1, 4], [2, 5]])
+outs += [xc, xn, stats, sel, stats2, sel2, stats3, sc3, stale]
 torch.save([o.cpu() for o in outs], sys.argv[1])
 print("OK")
 """
