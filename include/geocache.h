@@ -306,8 +306,8 @@ int gc_index_foreground(const float* pos, int64_t n_views, int H, int W, uint32_
  *                  needs n_vis * CV <= 2^31 - 2048, CV being the channel
  *                  vectors per token (C/4 for float32; C/8 for bfloat16 when 8
  *                  divides C, else C/4); larger counts fail with GC_ERR_CAPACITY.
- *                  A step with fewer than 2^18 work items (B*N*H*W tokens
- *                  times CV) validates the index and then takes the plain
+ *                  A step with fewer than 2^18 work items (B*(N-a)*H*W
+ *                  target tokens times CV) validates the index and then takes the plain
  *                  launch, which is faster at that size; the environment
  *                  variable GC_SPLIT_MIN_ITEMS, read once per process, moves
  *                  that bound (0: every indexed step takes the split launch).

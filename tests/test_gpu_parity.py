@@ -526,7 +526,7 @@ def test_default_split_bound_is_bit_identical(gc, tmp_path):
     import subprocess
     import sys
     w = C4
-    assert w.B * w.N * w.H * w.W * (w.C // 4) < 2 ** 18 and w.sampler == "ddim"
+    assert w.B * (w.N - w.a) * w.H * w.W * (w.C // 4) < 2 ** 18 and w.sampler == "ddim"   # target tokens x vectors
     P = latent_maps(w.name)
     A = anchors_of(w, 1)
     x0_prev, x0_new, x_t = latents(w, P, A, 4)
