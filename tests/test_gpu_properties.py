@@ -167,8 +167,8 @@ def test_graph_replays_match_eager():
 
 def test_graph_replays_other_paths():
     """The on-the-fly step (blocked and foreground launches), the fused UniPC
-    step and the coverage update +
-    greedy selection captured in one HIP graph: every replay (with eager
+    step, the coverage update + greedy selection and the fused update +
+    selection / scoring captured in one HIP graph: every replay (with eager
     work, state resets and synchronisations between replays) equals the
     eager result bit for bit."""
     import paper_2608_13255_amd as gc
@@ -198,6 +198,13 @@ def test_graph_replays_other_paths():
     stats = torch.empty((1, w.N, 4), dtype=torch.int32, device=DEV)
     sel = torch.empty(w.a, dtype=torch.int32, device=DEV)
     ws = torch.empty(gc.gc_coverage_workspace_bytes(), dtype=torch.uint8, device=DEV)
+    # the fused update + selection / scoring (their last block reads what every block added)
+    stale2 = stale0.clone()
+    stats2, stats3 = torch.empty_like(stats), torch.empty_like(stats)
+    sel2 = torch.empty(w.a, dtype=torch.int32, device=DEV)
+    rot = [gc.gc_schedule_anchors(w.N, w.a, c) for c in range(3)]
+    sc3 = torch.empty(len(rot), dtype=torch.int64, device=DEV)
+    ws2 = torch.empty(gc.gc_coverage_workspace_bytes(), dtype=torch.uint8, device=DEV)
     s = torch.cuda.Stream()
     torch.cuda.synchronize()
 
@@ -210,27 +217,36 @@ def test_graph_replays_other_paths():
                               x_c=outs["u1"], x_next=outs["u2"], index=idx1, stream=s)
         gc.gc_coverage_update(pairs, stale, A1, 2, stats=stats, stream=s)
         gc.gc_coverage_select(pairs, stale, w.a, forced=[w.N - 1], out=sel, workspace=ws, stream=s)
+        gc.gc_coverage_update_select(pairs, stale2, A0, 2, w.a, forced=[1], stats=stats2, out=sel2, workspace=ws2,
+                                     stream=s)
+        gc.gc_coverage_update_score(pairs, stale2, A1, 2, rot, stats=stats3, out=sc3, workspace=ws2, stream=s)
 
     with torch.cuda.stream(s):
         step()
     torch.cuda.synchronize()
     eager = {k: v.clone() for k, v in outs.items()}
     eager_stale, eager_stats, eager_sel = stale.clone(), stats.clone(), sel.clone()
+    fused = (stale2, stats2, sel2, stats3, sc3)
+    eager_fused = [t.clone() for t in fused]
     g = torch.cuda.CUDAGraph()
     stale.copy_(stale0)
+    stale2.copy_(stale0)
     torch.cuda.synchronize()
     with torch.cuda.graph(g, stream=s):
         step()
     for rep in range(4):
         stale.copy_(stale0)
+        stale2.copy_(stale0)
         for v in outs.values():
             v.fill_(float("nan"))
-        stats.fill_(-1)
-        sel.fill_(-1)
+        for t in (stats, sel, stats2, sel2, stats3, sc3):
+            t.fill_(-1)
         torch.cuda.synchronize()
         g.replay()
         torch.cuda.synchronize()
         for k, v in outs.items():
             assert torch.equal(v.view(torch.int16), eager[k].view(torch.int16)), (rep, k)
         assert torch.equal(stale, eager_stale) and torch.equal(stats, eager_stats) and torch.equal(sel, eager_sel), rep
+        for t, e in zip(fused, eager_fused):
+            assert torch.equal(t, e), rep
         _ = (x0.float() * 2).sum().item()  # eager work between replays
