@@ -487,8 +487,8 @@ __global__ __launch_bounds__(kBlock) void k_transport_geom_fg(GArgs g) {
       tp[j] = anchor_tap_positions(pj[j], g.pos + ((int64_t)b * g.N + view_lds[sc]) * g.HW * 3, g.H, g.W);
     }
   }
-  // The latent phase reads the token's own x0_prev and sampler input only
-  // after the tap tests and the ranking; one dword of each, loaded now into
+  // The latent phase reads the token's own x0_prev and sampler input (and,
+  // for UniPC, m_{k-2}) only after the tap tests; one dword of each, loaded now into
   // an LDS sink that nothing reads, brings their lines into L2 meanwhile
   // without holding a register (issued after the tap loads, so the tap
   // tests do not wait for them; the block's barriers wait on LDS only).
@@ -507,6 +507,11 @@ __global__ __launch_bounds__(kBlock) void k_transport_geom_fg(GArgs g) {
     if (own)
       __builtin_amdgcn_global_load_lds(static_cast<const char*>(own) + off,
                                        (__attribute__((address_space(3))) void*)s_sink, 4, 0, 0);
+    if constexpr (MODE == kGeomUniPC) {   // UniPC reads a third stream of its own
+      if (lane_g == 0 && g.u.need_m2)
+        __builtin_amdgcn_global_load_lds(static_cast<const char*>(g.m_km2) + off,
+                                         (__attribute__((address_space(3))) void*)s_sink, 4, 0, 0);
+    }
   }
   if (loaded) {
     const float tol2 = g.bbox[(int64_t)b * 8 + 6];
