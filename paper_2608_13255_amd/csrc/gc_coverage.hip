@@ -687,8 +687,6 @@ __global__ __launch_bounds__(1024) void k_score_final(const SelState* st, int M,
   if ((int)threadIdx.x < M) score[threadIdx.x] = sum[threadIdx.x];
 }
 
-// The histogram path: clear H and the ticket, then the pass over the tokens
-// with the last block's rounds (select) or scores (score).
 // The histogram path: clear H and the ticket (and the statistics), then the
 // pass over the tokens with the last block's rounds (select) or scores
 // (score); UPDATE applies the staleness step first (anchor_mask, R, stats).
