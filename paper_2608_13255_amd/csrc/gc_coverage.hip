@@ -367,11 +367,6 @@ struct SetMasks {
   unsigned long long m[kMaxSets];
 };
 
-// The pass over the tokens (lane group of 4 per pair word, 8 tokens per
-// lane; blocks stride over the words of every (asset, view) row), then in
-// the last block: SCORE == false, forced views first and a - n_forced greedy
-// rounds (largest gain, ties to the lower view; wave 0, lane u evaluating
-// candidate u), the set to out; SCORE == true, score[m] for the M sets.
 // Staleness bytes of a lane's 8 tokens written back (VEC as for load_8_bytes).
 template <bool VEC>
 __device__ __forceinline__ void store_8_bytes(uint8_t* __restrict__ row, int HW, int t0, const uint32_t (&d)[2]) {
